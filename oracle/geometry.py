@@ -1,0 +1,107 @@
+"""Oracle: stereographic tile coordinates (test infrastructure, CPU only, float64).
+
+This is the plain reference the HIP path is checked against; only tests, the
+smoke check and the bench's CPU-baseline leg may use it.
+
+Follows the paper's section on grid-invariant position encoding (Eq. 1): each
+token's (lat, lon) is projected onto the tangent plane of a stereographic
+projection centred on its tile, and the result divided by
+l_scale = sqrt(4 pi / N_total).
+
+Readings where the paper is silent (stated once here, listed in the design notes):
+* equiangular cube: cell (i, j) of an n x n face has angles
+  alpha = -pi/4 + (j + 1/2) (pi/2)/n (columns, x direction) and beta likewise from
+  the row i (y direction); a token of a p x p patch (I, J) sits at the patch centre,
+  alpha = -pi/4 + (p J + p/2)(pi/2)/n;
+* face orientation, with a = tan(alpha), b = tan(beta):
+  0: (1, a, b)   1: (-a, 1, b)   2: (-1, -a, b)   3: (a, -1, b)
+  4: (-b, a, 1)  (north)          5: (b, a, -1)    (south);
+* the tile centre is the point at the mean of the angles of the tile's first and
+  last token on each axis;
+* N_total counts native horizontal cells: 6 n^2.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def l_scale(n_cells: int = 2048) -> float:
+    """Eq. 1 normaliser sqrt(4 pi / N_total) with N_total = 6 n^2 native cells."""
+    return float(np.sqrt(4.0 * np.pi / (6.0 * n_cells * n_cells)))
+
+
+def cube_point(face, alpha, beta):
+    """Unnormalised point on the cube surface for equiangular angles (alpha, beta)."""
+    face = np.asarray(face)
+    a = np.tan(np.asarray(alpha, dtype=np.float64))
+    b = np.tan(np.asarray(beta, dtype=np.float64))
+    one = np.ones(np.broadcast(face, a, b).shape)
+    a = a * one
+    b = b * one
+    face = face * np.ones(one.shape, dtype=np.int64)
+    X = np.empty(one.shape)
+    Y = np.empty(one.shape)
+    Zc = np.empty(one.shape)
+    table = {
+        0: (one, a, b),
+        1: (-a, one, b),
+        2: (-one, -a, b),
+        3: (a, -one, b),
+        4: (-b, a, one),
+        5: (b, a, -one),
+    }
+    for f, (x, y, z) in table.items():
+        m = face == f
+        X[m], Y[m], Zc[m] = x[m], y[m], z[m]
+    return X, Y, Zc
+
+
+def latlon(face, alpha, beta):
+    """(lat, lon) in radians of the cube point for (face, alpha, beta)."""
+    X, Y, Zc = cube_point(face, alpha, beta)
+    lat = np.arctan2(Zc, np.hypot(X, Y))
+    lon = np.arctan2(Y, X)
+    return lat, lon
+
+
+def token_angle(index, n_cells: int = 2048, patch: int = 4):
+    """Equiangular angle of the centre of patch ``index`` along one face axis."""
+    return -np.pi / 4 + (patch * np.asarray(index, dtype=np.float64) + patch / 2.0) * (np.pi / 2) / n_cells
+
+
+def stereographic(lat, lon, lat0, lon0, lscale):
+    """Eq. 1: tile-centred stereographic (x, y), divided by l_scale."""
+    dl = lon - lon0
+    cos_c = np.sin(lat0) * np.sin(lat) + np.cos(lat0) * np.cos(lat) * np.cos(dl)
+    k = 2.0 / (1.0 + cos_c)
+    x = (k / lscale) * np.cos(lat) * np.sin(dl)
+    y = (k / lscale) * (np.cos(lat0) * np.sin(lat) - np.sin(lat0) * np.cos(lat) * np.cos(dl))
+    return x, y
+
+
+def tile_coords(face, oy, ox, H: int, W: int, n_cells: int = 2048, patch: int = 4,
+                lscale: float | None = None) -> np.ndarray:
+    """Stereographic coordinates coords[B, H, W, 2] (x, y) in float64 for tiles of H x W tokens.
+
+    face/oy/ox: per-tile cube face and token origin (row, column)."""
+    if lscale is None:
+        lscale = l_scale(n_cells)
+    face = np.asarray(face, dtype=np.int64)
+    oy = np.asarray(oy, dtype=np.int64)
+    ox = np.asarray(ox, dtype=np.int64)
+    B = face.shape[0]
+    out = np.empty((B, H, W, 2), dtype=np.float64)
+    I = np.arange(H)
+    J = np.arange(W)
+    for t in range(B):
+        beta = token_angle(oy[t] + I, n_cells, patch)       # rows
+        alpha = token_angle(ox[t] + J, n_cells, patch)      # columns
+        beta0 = 0.5 * (beta[0] + beta[-1])
+        alpha0 = 0.5 * (alpha[0] + alpha[-1])
+        lat0, lon0 = latlon(face[t], alpha0, beta0)
+        A, Bt = np.meshgrid(alpha, beta, indexing="xy")      # [H, W]
+        lat, lon = latlon(np.full(A.shape, face[t]), A, Bt)
+        x, y = stereographic(lat, lon, lat0, lon0, lscale)
+        out[t, :, :, 0] = x
+        out[t, :, :, 1] = y
+    return out

@@ -1,0 +1,127 @@
+"""Pins of the oracle's stereographic tile coordinates (Sec. 3.3, Eq. 1) -- CPU only.
+
+Each check rests on a fact fixed independently of the oracle's code: closed
+forms of the stereographic projection, its conformality, cube-face adjacency and
+the grid scales the paper prints (tests/golden/paper_scales.json)."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import geometry as G
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "paper_scales.json")
+R_EARTH_KM = 6371.0
+
+
+def test_centre_maps_to_origin():
+    # G1: the tile centre itself projects to (0, 0) exactly.
+    lat0, lon0 = 0.3, -1.1
+    x, y = G.stereographic(np.array(lat0), np.array(lon0), lat0, lon0, 1.0)
+    assert x == 0.0 and y == 0.0
+    # odd tile: its middle token is the centre -> (0, 0) up to rounding
+    c = G.tile_coords([2], [100], [37], 5, 5)
+    assert abs(c[0, 2, 2, 0]) < 1e-9 and abs(c[0, 2, 2, 1]) < 1e-9
+
+
+def test_meridian_closed_form():
+    # G2: on the centre's meridian x = 0 and y = 2 tan(dlat/2) / l.
+    lat0, lon0, ls = 0.4, 2.0, 7e-4
+    dl = np.linspace(-0.2, 0.2, 41)
+    x, y = G.stereographic(lat0 + dl, np.full_like(dl, lon0), lat0, lon0, ls)
+    assert np.max(np.abs(x)) < 1e-12
+    np.testing.assert_allclose(y * ls, 2 * np.tan(dl / 2), rtol=1e-12, atol=1e-15)
+
+
+def test_equator_closed_form():
+    # G3: centre on the equator, points on the equator: x = 2 tan(dlon/2)/l, y = 0.
+    dl = np.linspace(-0.3, 0.3, 31)
+    x, y = G.stereographic(np.zeros_like(dl), 0.7 + dl, 0.0, 0.7, 1.0)
+    np.testing.assert_allclose(x, 2 * np.tan(dl / 2), rtol=1e-12, atol=1e-15)
+    assert np.max(np.abs(y)) < 1e-15
+
+
+def test_radial_distance_is_2tan_half_angle():
+    # G4: |(x, y)| l = 2 tan(c/2), with c the great-circle distance (haversine form).
+    r = np.random.default_rng(0)
+    lat0, lon0 = 0.5, -0.3
+    lat = lat0 + r.uniform(-0.3, 0.3, 200)
+    lon = lon0 + r.uniform(-0.3, 0.3, 200)
+    x, y = G.stereographic(lat, lon, lat0, lon0, 1.0)
+    h = np.sin((lat - lat0) / 2) ** 2 + np.cos(lat) * np.cos(lat0) * np.sin((lon - lon0) / 2) ** 2
+    c = 2 * np.arcsin(np.sqrt(h))
+    np.testing.assert_allclose(np.hypot(x, y), 2 * np.tan(c / 2), rtol=1e-10)
+
+
+def test_projection_is_conformal():
+    # G5: the map (lat, lon) -> (x, y) preserves angles: with metric factors,
+    # the Jacobian columns d/dlat and d/(cos(lat) dlon) are orthogonal and equally long.
+    r = np.random.default_rng(1)
+    lat0, lon0 = -0.6, 1.2
+    eps = 1e-6
+    for _ in range(20):
+        lat = lat0 + r.uniform(-0.2, 0.2)
+        lon = lon0 + r.uniform(-0.2, 0.2)
+        def f(a, b):
+            return np.array(G.stereographic(np.array(a), np.array(b), lat0, lon0, 1.0))
+        j_lat = (f(lat + eps, lon) - f(lat - eps, lon)) / (2 * eps)
+        j_lon = (f(lat, lon + eps) - f(lat, lon - eps)) / (2 * eps) / np.cos(lat)
+        n1, n2 = np.linalg.norm(j_lat), np.linalg.norm(j_lon)
+        assert abs(np.dot(j_lat, j_lon)) / (n1 * n2) < 1e-7
+        assert abs(n1 / n2 - 1.0) < 1e-7
+
+
+def test_cube_faces_tile_the_sphere():
+    # Face centres point along the six axes, and neighbouring faces share their edges.
+    axes = []
+    for f in range(6):
+        X, Y, Zc = G.cube_point(np.array([f]), np.array([0.0]), np.array([0.0]))
+        axes.append(np.array([X[0], Y[0], Zc[0]]))
+    A = np.abs(np.stack(axes))
+    assert np.all(np.sort(A.sum(0)) == 2.0) and np.all(A.max(1) == 1.0)
+    t = np.linspace(-np.pi / 4, np.pi / 4, 17)
+    edges = []
+    for f in range(6):
+        for a, b in ((np.full_like(t, np.pi / 4), t), (np.full_like(t, -np.pi / 4), t),
+                     (t, np.full_like(t, np.pi / 4)), (t, np.full_like(t, -np.pi / 4))):
+            X, Y, Zc = G.cube_point(np.full(t.shape, f), a, b)
+            P = np.stack([X, Y, Zc], 1)
+            edges.append((f, np.round(P, 12)))
+    # every edge polyline of a face appears (as a point set) on exactly one other face
+    for i, (f, P) in enumerate(edges):
+        key = set(map(tuple, P))
+        partners = [g for j, (g, Q) in enumerate(edges) if j != i and set(map(tuple, Q)) == key]
+        assert len(partners) == 1 and partners[0] != f
+
+
+def test_paper_grid_scales():
+    # The paper's printed scales: a 6 x 2048^2 cubed sphere of ~4.9-km cells,
+    # 128 x 128-cell tiles ~576 km across, 36 x 36-cell windows ~160 km.
+    g = json.load(open(GOLDEN))
+    ls = G.l_scale(g["face_cells"])
+    assert 6 * g["face_cells"] ** 2 == pytest.approx(g["grid_points"], rel=0.02)
+    cell_km = ls * R_EARTH_KM
+    assert cell_km == pytest.approx(g["grid_km"], rel=0.1)
+    r = np.random.default_rng(2)
+    for _ in range(8):
+        f = int(r.integers(0, 6))
+        T = g["train_tile_cells"] // 4
+        oy, ox = (int(v) for v in r.integers(0, 512 - T + 1, 2))
+        c = G.tile_coords([f], [oy], [ox], T, T)[0]
+        span = np.mean(np.hypot(*(c[:, -1, :] - c[:, 0, :]).T))
+        width_km = span * ls * R_EARTH_KM * T / (T - 1)
+        assert width_km == pytest.approx(g["train_tile_km"], rel=0.25)
+        Wn = g["window_cells"] // 4
+        cw = G.tile_coords([f], [oy], [ox], Wn, Wn)[0]
+        wspan = np.mean(np.hypot(*(cw[:, -1, :] - cw[:, 0, :]).T))
+        wkm = wspan * ls * R_EARTH_KM * Wn / (Wn - 1)
+        assert wkm == pytest.approx(g["window_km"], rel=0.3)
+
+
+def test_tile_frame_axes():
+    # x grows eastward and y northward in the tile frame: on face 0 (+X, lon 0 at
+    # centre) columns run east and rows run north.
+    c = G.tile_coords([0], [200], [200], 16, 16)[0]
+    assert np.all(np.diff(c[:, :, 0], axis=1) > 0)
+    assert np.all(np.diff(c[:, :, 1], axis=0) > 0)
