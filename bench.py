@@ -1,0 +1,208 @@
+"""Throughput of one face rollout step of the STRATA hot path on one MI355X.
+
+Workload (synthetic, seeded): one cube face of 2048^2 cells at 4 x 4 patches =
+512^2 horizontal x 8 vertical tokens, cut into 64 x 64-token tiles overlapping
+by 8 tokens (stride 56, 9 x 9 = 81 tiles); 16 heads of head_dim 64; Q/K/V iid
+N(0,1) in bf16.  One step =
+  stereographic coordinates of every tile token (Eq. 1) -> StereoRoPE phases ->
+  3x7x7 neighbourhood attention forward with the rotation fused into the Q/K
+  loads -> linear-ramp tile stitch of the 81 tile outputs back to the face.
+Inputs are resident in HBM before timing starts.
+
+Prints one JSON line.  ``value`` is the neighbourhood-attention forward's
+algorithmic TFLOP/s over the whole step (4 B h N K d FLOPs per step divided by
+the step time); the dominant kernel's roofline and a timed CPU-oracle sample
+are reported beside it.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "NA3D fwd TFLOP/s + tokens/s at 1 MI355X; % of bf16 MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0        # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0            # MI355X HBM3E
+PMC_FILE = os.path.join(ROOT, "profiles", "na3d_fwd_face_rollout_pmc.json")
+KERNEL_SOURCES = ["paper_2606_31248_amd/csrc/na3d_fwd_mfma.hip", "paper_2606_31248_amd/csrc/na3d_ref.hip"]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(per_launch_alg_bytes: float):
+    """HBM bytes per launch from the committed rocprofv3 counter runs, if they are
+    still for the current kernel source; else None."""
+    try:
+        with open(PMC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None, None
+    if rec.get("kernel_source_hash") != kernel_source_hash():
+        return None, None
+    return rec.get("hbm_bytes_per_launch"), rec
+
+
+def cpu_baseline(wl, tiles_sample: int):
+    """Time the CPU oracle on a bounded sample of the same workload: the
+    coordinates and neighbourhood-attention forward of ``tiles_sample`` tiles
+    (all heads and levels); reported in the metric's unit (algorithmic TFLOP/s)."""
+    import oracle
+    from oracle import geometry as G
+    from paper_2606_31248_amd import inputs as I
+
+    pl = wl.placement()
+    sel = np.arange(tiles_sample)
+    shape = (tiles_sample,) + wl.shape()[1:]
+    q, k, v = (I.gaussian(shape, wl.seed + 100, s, "bf16") for s in (0, 1, 2))
+    q, k, v = (oracle.widen(a, "bf16") for a in (q, k, v))
+    t0 = time.perf_counter()
+    c = G.tile_coords(pl.face[sel], pl.oy[sel], pl.ox[sel], wl.H, wl.W).astype(np.float32)
+    oracle.na3d_fwd(q, k, v, (wl.kz, wl.ky, wl.kx), wl.scale, coords=c)
+    dt = time.perf_counter() - t0
+    flops = 4.0 * tiles_sample * wl.heads * wl.N * wl.K * wl.d
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
+            "kind": "oracle", "seconds": round(dt, 3),
+            "sample": f"coordinates + float64 NA3D forward with StereoRoPE of {tiles_sample} of the "
+                      f"{wl.B} tiles (all {wl.heads} heads x {wl.N} tokens; blend not included)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--cpu-tiles", type=int, default=24, help="tiles in the CPU-oracle sample (0: skip)")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also run one 1 GiB device copy (HBM counter calibration)")
+    a = ap.parse_args()
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build measures one GPU only (no multi-GPU path); run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_31248_amd import binding as Bd
+    from paper_2606_31248_amd import inputs as I
+    from paper_2606_31248_amd import pipeline as Pp
+
+    Bd.load()
+    wl = I.FACE_ROLLOUT
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    nty, ntx, sy, sx = wl.tiling
+    Hf = (nty - 1) * sy + wl.H
+    Wf = (ntx - 1) * sx + wl.W
+    window = (wl.kz, wl.ky, wl.kx)
+
+    def to_dev(bits):
+        return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(dev)
+
+    q, k, v = (to_dev(x) for x in wl.qkv())
+    pl = wl.placement()
+    geom = Pp.TileGeometry(*(torch.from_numpy(x).to(dev) for x in pl.as_int32()))
+    win = torch.from_numpy(I.ramp_window_2d(wl.H, wl.W, I.FACE_OVERLAP)).to(dev)
+    coords = torch.empty((wl.B, wl.H, wl.W, 2), dtype=torch.float32, device=dev)
+    cs = torch.empty((wl.B, wl.H, wl.W, wl.d // 2, 2), dtype=torch.float32, device=dev)
+    out = torch.empty_like(q)
+    face = torch.empty((wl.heads * wl.Z, Hf, Wf, wl.d), dtype=torch.bfloat16, device=dev)
+    desc = Bd.desc_for(q, window, wl.scale)
+
+    if a.calib_copy:
+        src = torch.empty(1 << 29, dtype=torch.int16, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    ev = {n: [] for n in ("coords", "na", "blend")}
+
+    def step(record: bool):
+        st = torch.cuda.current_stream()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)] if record else None
+        if record:
+            e[0].record(st)
+        Bd.strata_stereo_coords(geom.face, geom.oy, geom.ox, wl.H, wl.W, geom.face_cells, geom.patch,
+                                Pp.l_scale(geom.face_cells), coords)
+        Bd.strata_stereorope_phases(coords, wl.d, Pp.ROPE_BASE, cs)
+        if record:
+            e[1].record(st)
+        Bd.strata_na3d_fwd(desc, q, k, v, cs, out, None)
+        if record:
+            e[2].record(st)
+        Bd.strata_tile_blend(out.view(wl.B, wl.heads * wl.Z, wl.H, wl.W, wl.d), nty, ntx, sy, sx, win, face)
+        if record:
+            e[3].record(st)
+            ev["coords"].append((e[0], e[1]))
+            ev["na"].append((e[1], e[2]))
+            ev["blend"].append((e[2], e[3]))
+
+    for _ in range(a.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(a.steps):
+        step(True)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / a.steps
+    avg = {n: float(np.mean([s.elapsed_time(e) for s, e in lst])) for n, lst in ev.items()}
+
+    flops = 4.0 * wl.B * wl.heads * wl.N * wl.K * wl.d
+    tflops_step = flops / (ms_step * 1e-3) / 1e12
+    tflops_na = flops / (avg["na"] * 1e-3) / 1e12
+    alg_bytes = 4.0 * wl.B * wl.heads * wl.N * wl.d * 2        # Q, K, V read + O write, bf16
+    gbs_na = alg_bytes / (avg["na"] * 1e-3) / 1e9
+    blend_bytes = (wl.B * wl.heads * wl.Z * wl.H * wl.W * wl.d + wl.heads * wl.Z * Hf * Wf * wl.d) * 2
+    traffic, pmc = stored_traffic(alg_bytes)
+    tokens = wl.B * wl.N
+
+    res = {
+        "metric": METRIC,
+        "value": round(tflops_step, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded iid N(0,1) Q/K/V; analytic equiangular cubed-sphere tile geometry)",
+        "config": {"workload": wl.name, "tiles": wl.B, "heads": wl.heads, "Z": wl.Z, "H": wl.H,
+                   "W": wl.W, "head_dim": wl.d, "window": list(window), "face_tokens": [Hf, Wf],
+                   "tile_stride": [sy, sx], "overlap": I.FACE_OVERLAP, "blend_window": "linear ramp"},
+        "tokens_per_s": round(tokens / (ms_step * 1e-3), 1),
+        "face_tokens_per_s": round(wl.Z * Hf * Wf / (ms_step * 1e-3), 1),
+        "pct_bf16_peak": round(100.0 * tflops_step / PEAK_BF16_TFLOPS, 2),
+        "kernels_ms": {k2: round(v2, 4) for k2, v2 in avg.items()},
+        "na3d_fwd": {"tflops": round(tflops_na, 2), "pct_bf16_peak": round(100 * tflops_na / PEAK_BF16_TFLOPS, 2),
+                     "hbm_gbs_algorithmic": round(gbs_na, 1)},
+        "blend": {"gbs_algorithmic": round(blend_bytes / (avg["blend"] * 1e-3) / 1e9, 1)},
+        "roofline": {"bound": "hbm", "achieved": round(gbs_na, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(gbs_na / PEAK_HBM_GBS, 4),
+                     "traffic": None if traffic is None else float(traffic),
+                     "kernel": "strata_na3d_fwd", "alg_bytes_per_launch": alg_bytes},
+    }
+    if a.cpu_tiles > 0:
+        res["cpu_baseline"] = cpu_baseline(wl, a.cpu_tiles)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,160 @@
+/*
+ * strata.h -- C ABI of the STRATA hot path on AMD Instinct MI355X (gfx950).
+ *
+ * What it computes (arxiv 2606.31248, "Scaling Storm-Resolving Atmospheric AI
+ * Simulation to the Entire Planet"):
+ *   - the tile-centred stereographic coordinates of every token (Sec. 3.3, Eq. 1);
+ *   - StereoRoPE: axial 2D rotary embedding driven by those coordinates (Sec. 3.3);
+ *   - 3D neighbourhood attention over the (level, y, x) token grid of each tile
+ *     with NATTEN's border-clamped windows (Sec. 3.2), forward and backward;
+ *   - the overlapping-tile stitch S = D^-1 P^T W and its extraction P
+ *     (App. F, "Tile stitching", "Linear operator interpretation").
+ *
+ * Conventions shared by every call:
+ *   - Pointers are DEVICE pointers owned by the caller unless stated otherwise.
+ *     The library never allocates device memory and never frees caller memory.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
+ *     stream).  Arguments are validated synchronously before any launch; on a
+ *     validation error nothing is launched.
+ *   - Activations are [B, heads, Z, H, W, head_dim], contiguous, head_dim
+ *     innermost: B tiles, Z vertical levels, H x W horizontal tokens.
+ *   - Element types: STRATA_F32 (IEEE binary32) or STRATA_BF16 (bfloat16 bit
+ *     patterns in uint16 storage).  Results are rounded to nearest-even.
+ *   - Every call returns a strata_status; a non-OK status leaves a message
+ *     retrievable with strata_last_error() on the calling thread.  Nothing
+ *     throws across the ABI.  Device pointers must be 16-byte aligned.
+ */
+#ifndef STRATA_H_
+#define STRATA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  STRATA_OK = 0,
+  STRATA_ERR_INVALID_ARG = 1, /* null pointer, bad size, misalignment, bad window */
+  STRATA_ERR_UNSUPPORTED = 2, /* valid arguments this build has no kernel for */
+  STRATA_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required */
+  STRATA_ERR_HIP = 4          /* the HIP runtime reported an error at launch */
+} strata_status;
+
+typedef enum { STRATA_F32 = 0, STRATA_BF16 = 1 } strata_dtype;
+
+/* Neighbourhood-attention problem.  Window (kz, ky, kx): odd, 1 <= k <= extent
+ * on its axis, dilation 1.  A query at position i of an axis of extent L sees
+ * the k positions [s, s + k) with s = min(max(i - (k-1)/2, 0), L - k): centred,
+ * shifted inward at the borders, so every query sees exactly kz*ky*kx keys. */
+typedef struct {
+  int32_t B, heads, Z, H, W, head_dim;
+  int32_t kz, ky, kx;
+  float scale;        /* logit scale, > 0 (usually 1/sqrt(head_dim)) */
+  strata_dtype dtype; /* element type of q, k, v, out, dout, dq, dk, dv */
+} strata_na3d_desc;
+
+/* ---- a1: stereographic tile coordinates (Sec. 3.3, Eq. 1) -----------------
+ * For tile b on the equiangular cubed sphere (faces of face_cells^2 cells,
+ * tokens of patch x patch cells), token (y, x) of the tile has face token
+ * (tile_oy[b] + y, tile_ox[b] + x) on face tile_face[b] (0..5).  Its
+ * (lat, lon) is projected stereographically about the tile centre (the point
+ * at the mean angles of the tile's first and last token) and divided by
+ * l_scale (sqrt(4 pi / N_total) in Eq. 1):
+ *   coords[b, y, x, 0] = x_east / l_scale,  coords[b, y, x, 1] = y_north / l_scale.
+ * Face f with a = tan(alpha) (columns), c = tan(beta) (rows) is the cube point
+ *   0:(1,a,c) 1:(-a,1,c) 2:(-1,-a,c) 3:(a,-1,c) 4:(-c,a,1) 5:(c,a,-1).
+ * Computed in float64, stored as float32.  tile_face/oy/ox: device int32[B];
+ * coords: device float32[B, H, W, 2].  Tiles must fit on the face. */
+strata_status strata_stereo_coords(const int32_t* tile_face, const int32_t* tile_oy,
+                                   const int32_t* tile_ox, int32_t B, int32_t H, int32_t W,
+                                   int32_t face_cells, int32_t patch, double l_scale,
+                                   float* coords, void* stream);
+
+/* ---- a2: StereoRoPE phase table (Sec. 3.3) --------------------------------
+ * cs[b, y, x, t] = (cos th, sin th) for pair t < head_dim/2, with
+ *   th = coords[b,y,x,0] * base^(-t/(head_dim/4))               for t <  head_dim/4,
+ *   th = coords[b,y,x,1] * base^(-(t-head_dim/4)/(head_dim/4))  for t >= head_dim/4.
+ * Built in float64, stored as float32 pairs.  coords: float32[B, H, W, 2];
+ * cs: float32[B, H, W, head_dim/2, 2].  head_dim % 4 == 0, base > 0. */
+strata_status strata_stereorope_phases(const float* coords, int32_t B, int32_t H, int32_t W,
+                                       int32_t head_dim, double base, float* cs, void* stream);
+
+/* ---- a2: StereoRoPE application (Sec. 3.3) --------------------------------
+ * Rotates every pair (x[2t], x[2t+1]) of every token by its phase:
+ *   y[2t] = x[2t] cos - x[2t+1] sin,  y[2t+1] = x[2t] sin + x[2t+1] cos;
+ * transpose != 0 rotates by the opposite angle (R^T, used for gradients).
+ * All levels and heads of a column share the phase of (b, y, x).
+ * x, y: [B, heads, Z, H, W, head_dim] of dtype; y may equal x (in place).
+ * Arithmetic in float32. */
+strata_status strata_stereorope_apply(const void* x, void* y, const float* cs, int32_t B,
+                                      int32_t heads, int32_t Z, int32_t H, int32_t W,
+                                      int32_t head_dim, strata_dtype dtype, int32_t transpose,
+                                      void* stream);
+
+/* ---- a3-a6: neighbourhood attention forward (Sec. 3.2) --------------------
+ * For every query i (all heads, tiles, positions):
+ *   s_ij = scale * <R_i q_i, R_j k_j>  over the kz*ky*kx keys j of i's window,
+ *   lse_i = ln sum_j exp(s_ij),   out_i = sum_j exp(s_ij - lse_i) v_j,
+ * where R is the StereoRoPE rotation from the phase table `cs` (float32
+ * [B, H, W, head_dim/2, 2]), or the identity when cs == NULL.
+ * q, k, v, out: [B, heads, Z, H, W, head_dim] of desc->dtype;
+ * lse: float32 [B, heads, Z, H, W] (natural log) or NULL when not needed.
+ * Supported: f32 with head_dim in {32, 64}; bf16 with head_dim in {32, 64}
+ * (bf16 MFMA path for head_dim 64).  Softmax and accumulation in float32. */
+strata_status strata_na3d_fwd(const strata_na3d_desc* desc, const void* q, const void* k,
+                              const void* v, const float* cs, void* out, float* lse,
+                              void* stream);
+
+/* ---- a7: neighbourhood attention backward ----------------------------------
+ * Gradients of the forward above for upstream gradient dout, with the lse the
+ * forward wrote and its output `out`:
+ *   P_ij = exp(s_ij - lse_i),   D_i = <dout_i, out_i>,
+ *   dv_j = sum_{i: j in N(i)} P_ij dout_i,    dS_ij = P_ij (<dout_i, v_j> - D_i),
+ *   dq_i = R_i^T scale sum_j dS_ij R_j k_j,    dk_j = R_j^T scale sum_i dS_ij R_i q_i.
+ * Deterministic (no atomics).  workspace: device memory of at least
+ * strata_na3d_bwd_workspace_size(desc) bytes (holds D), owned by the caller. */
+size_t strata_na3d_bwd_workspace_size(const strata_na3d_desc* desc);
+strata_status strata_na3d_bwd(const strata_na3d_desc* desc, const void* q, const void* k,
+                              const void* v, const float* cs, const void* out, const void* dout,
+                              const float* lse, void* dq, void* dk, void* dv, void* workspace,
+                              size_t workspace_bytes, void* stream);
+
+/* ---- a8: tile stitch S = D^-1 P^T W (App. F, Eq. stitch) -------------------
+ * Regular tiling: tile t = a*ntx + b has origin (a*stride_y, b*stride_x) on the
+ * face.  tiles: [nty*ntx, P, Ht, Wt, C] of dtype; window: float32 [Ht*Wt],
+ * >= 0; out: [P, Hf, Wf, C] of dtype.  For every face cell:
+ *   out = (sum_t w_t * value_t) / (sum_t w_t)  over the tiles t covering it,
+ * summed in ascending a, then b, with fused multiply-adds from zero, divided
+ * with correct rounding; bf16 data accumulate in float32, f32 data in float64.
+ * Cells no tile weights (sum 0) are written as 0.  Requires
+ * (nty-1)*stride_y + Ht <= Hf and (ntx-1)*stride_x + Wt <= Wf.  Bit-exact. */
+strata_status strata_tile_blend(const void* tiles, int32_t nty, int32_t ntx, int32_t P,
+                                int32_t Ht, int32_t Wt, int32_t C, int32_t stride_y,
+                                int32_t stride_x, const float* window, void* out, int32_t Hf,
+                                int32_t Wf, strata_dtype dtype, void* stream);
+
+/* ---- a8': tile extraction P (App. F) ---------------------------------------
+ * tiles[t, p, i, j, c] = face[p, a*stride_y + i, b*stride_x + j, c] (exact copy). */
+strata_status strata_tile_extract(const void* face, int32_t nty, int32_t ntx, int32_t P,
+                                  int32_t Ht, int32_t Wt, int32_t C, int32_t stride_y,
+                                  int32_t stride_x, int32_t Hf, int32_t Wf, void* tiles,
+                                  strata_dtype dtype, void* stream);
+
+/* ---- a3: window indexing of one axis (bit-exact integer export) ------------
+ * starts[i]: first position of query i's window; [qlo[j], qhi[j]]: the
+ * queries whose window holds position j (contiguous).  Device int32[L] each. */
+strata_status strata_na_axis_index(int32_t L, int32_t k, int32_t* starts, int32_t* qlo,
+                                   int32_t* qhi, void* stream);
+
+/* ---- status ---------------------------------------------------------------- */
+const char* strata_status_string(strata_status status);
+/* Detail of the last non-OK status returned on the calling thread ("" if none). */
+const char* strata_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* STRATA_H_ */

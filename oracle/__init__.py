@@ -50,12 +50,13 @@ def lib():
         i32, i64, f64 = ctypes.c_int, ctypes.c_int64, ctypes.c_double
         P = ctypes.c_void_p
         L.oracle_axis_index.argtypes = [i32, i32, P, P, P]
+        L.oracle_rope_phases.argtypes = [P, i32, i32, i32, i32, f64, P]
         L.oracle_rope_apply.argtypes = [P, P, i32, i32, i32, i32, i32, i32, f64, i32, P]
         L.oracle_na3d_fwd.argtypes = [P, P, P, P, f64] + [i32] * 9 + [f64, i64, P, P, P]
         L.oracle_na3d_bwd.argtypes = [P, P, P, P, f64] + [i32] * 9 + [f64, P, i64, P, i64, P, P, P, P]
         L.oracle_tile_blend.argtypes = [P, i32, i32, i32, i32, i32, i32, i32, i32, P, P, i32, i32, i32]
         L.oracle_tile_extract.argtypes = [P, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32, P, i32]
-        for f in ("oracle_axis_index", "oracle_rope_apply", "oracle_na3d_fwd", "oracle_na3d_bwd",
+        for f in ("oracle_axis_index", "oracle_rope_phases", "oracle_rope_apply", "oracle_na3d_fwd", "oracle_na3d_bwd",
                   "oracle_tile_blend", "oracle_tile_extract", "oracle_num_threads"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
@@ -86,6 +87,17 @@ def axis_index(L: int, k: int):
     if rc:
         raise ValueError("invalid axis window (L=%d, k=%d)" % (L, k))
     return starts, qlo, qhi
+
+
+def rope_phases(coords: np.ndarray, d: int, base: float = ROPE_BASE) -> np.ndarray:
+    """(cos, sin) per (b, y, x, pair): float64 [B, H, W, d/2, 2]."""
+    c = np.ascontiguousarray(coords, dtype=np.float32)
+    B, H, W, _ = c.shape
+    out = np.empty((B, H, W, d // 2, 2), np.float64)
+    rc = lib().oracle_rope_phases(_p(c), B, H, W, d, base, _p(out))
+    if rc:
+        raise ValueError("oracle_rope_phases failed (%d)" % rc)
+    return out
 
 
 def rope_apply(x: np.ndarray, coords: np.ndarray, transpose: bool = False,

@@ -104,6 +104,16 @@ static void rotate(const double* in, const double* ph, int d, double sign, doubl
   }
 }
 
+/* Phase table export: ph[b, y, x, t] = (cos th, sin th) in float64. */
+int oracle_rope_phases(const float* coords, int B, int H, int W, int d, double base, double* out) {
+  if (d % 4 != 0) return 1;
+  double* ph = build_phases(coords, B, H, W, d, base);
+  if (!ph) return 2;
+  memcpy(out, ph, sizeof(double) * 2 * (size_t)B * H * W * (d / 2));
+  free(ph);
+  return 0;
+}
+
 int oracle_rope_apply(const double* x, const float* coords, int B, int heads, int Z, int H,
                       int W, int d, double base, int transpose, double* y) {
   if (d % 4 != 0) return 1;

@@ -1,0 +1,175 @@
+"""Thin Python binding of libstrata's C ABI (include/strata.h).
+
+Functions carry the C names and only marshal arguments: torch tensors become
+device pointers, the current HIP stream of torch becomes the stream argument,
+and a non-OK status becomes a ``StrataError``.  Every computation runs in the
+HIP kernels of libstrata.so; there is no fallback of any kind -- if the library
+is not built, loading fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libstrata.so")
+
+STRATA_OK, STRATA_ERR_INVALID_ARG, STRATA_ERR_UNSUPPORTED, STRATA_ERR_WORKSPACE, STRATA_ERR_HIP = range(5)
+STRATA_F32, STRATA_BF16 = 0, 1
+
+# Every entry point declared in include/strata.h.
+EXPORTS = (
+    "strata_stereo_coords", "strata_stereorope_phases", "strata_stereorope_apply",
+    "strata_na3d_fwd", "strata_na3d_bwd_workspace_size", "strata_na3d_bwd",
+    "strata_tile_blend", "strata_tile_extract", "strata_na_axis_index",
+    "strata_status_string", "strata_last_error",
+)
+
+
+class StrataError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{msg} (status {status})")
+        self.status = status
+
+
+class NA3DDesc(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("heads", ctypes.c_int32), ("Z", ctypes.c_int32),
+                ("H", ctypes.c_int32), ("W", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("kz", ctypes.c_int32), ("ky", ctypes.c_int32), ("kx", ctypes.c_int32),
+                ("scale", ctypes.c_float), ("dtype", ctypes.c_int)]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load libstrata.so (built by ``python -m paper_2606_31248_amd.build``)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"libstrata.so not found at {path}: build it with "
+                           "`python -m paper_2606_31248_amd.build` (hipcc, gfx950)")
+    L = ctypes.CDLL(path)
+    P, i32, st = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int
+    D = ctypes.POINTER(NA3DDesc)
+    sig = {
+        "strata_stereo_coords": [P, P, P, i32, i32, i32, i32, i32, ctypes.c_double, P, P],
+        "strata_stereorope_phases": [P, i32, i32, i32, i32, ctypes.c_double, P, P],
+        "strata_stereorope_apply": [P, P, P, i32, i32, i32, i32, i32, i32, st, i32, P],
+        "strata_na3d_fwd": [D, P, P, P, P, P, P, P],
+        "strata_na3d_bwd": [D, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
+        "strata_tile_blend": [P, i32, i32, i32, i32, i32, i32, i32, i32, P, P, i32, i32, st, P],
+        "strata_tile_extract": [P, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32, P, st, P],
+        "strata_na_axis_index": [i32, i32, P, P, P, P],
+    }
+    for name, args in sig.items():
+        f = getattr(L, name)
+        f.argtypes = args
+        f.restype = st
+    L.strata_na3d_bwd_workspace_size.argtypes = [D]
+    L.strata_na3d_bwd_workspace_size.restype = ctypes.c_size_t
+    L.strata_status_string.argtypes = [st]
+    L.strata_status_string.restype = ctypes.c_char_p
+    L.strata_last_error.argtypes = []
+    L.strata_last_error.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to libstrata must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dtype(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return STRATA_BF16
+    if t.dtype == torch.float32:
+        return STRATA_F32
+    raise ValueError(f"unsupported tensor dtype {t.dtype}")
+
+
+def _check(status: int):
+    if status != STRATA_OK:
+        L = load()
+        raise StrataError(status, L.strata_last_error().decode())
+
+
+def make_desc(B, heads, Z, H, W, head_dim, window, scale, dtype: int) -> NA3DDesc:
+    kz, ky, kx = window
+    return NA3DDesc(B, heads, Z, H, W, head_dim, kz, ky, kx, float(scale), int(dtype))
+
+
+def desc_for(q: torch.Tensor, window, scale) -> NA3DDesc:
+    B, heads, Z, H, W, d = q.shape
+    return make_desc(B, heads, Z, H, W, d, window, scale, _dtype(q))
+
+
+# ---- entry points -------------------------------------------------------------
+
+def strata_stereo_coords(tile_face, tile_oy, tile_ox, H, W, face_cells, patch, l_scale, coords,
+                         stream=None):
+    B = tile_face.shape[0]
+    _check(load().strata_stereo_coords(_ptr(tile_face), _ptr(tile_oy), _ptr(tile_ox), B, H, W,
+                                       face_cells, patch, float(l_scale), _ptr(coords),
+                                       _stream(stream)))
+
+
+def strata_stereorope_phases(coords, head_dim, base, cs, stream=None):
+    B, H, W, _ = coords.shape
+    _check(load().strata_stereorope_phases(_ptr(coords), B, H, W, head_dim, float(base), _ptr(cs),
+                                           _stream(stream)))
+
+
+def strata_stereorope_apply(x, y, cs, transpose=False, stream=None):
+    B, heads, Z, H, W, d = x.shape
+    _check(load().strata_stereorope_apply(_ptr(x), _ptr(y), _ptr(cs), B, heads, Z, H, W, d,
+                                          _dtype(x), int(bool(transpose)), _stream(stream)))
+
+
+def strata_na3d_fwd(desc: NA3DDesc, q, k, v, cs, out, lse=None, stream=None):
+    _check(load().strata_na3d_fwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(cs), _ptr(out),
+                                  _ptr(lse), _stream(stream)))
+
+
+def strata_na3d_bwd_workspace_size(desc: NA3DDesc) -> int:
+    return int(load().strata_na3d_bwd_workspace_size(ctypes.byref(desc)))
+
+
+def strata_na3d_bwd(desc: NA3DDesc, q, k, v, cs, out, dout, lse, dq, dk, dv, workspace,
+                    stream=None):
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(load().strata_na3d_bwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(cs), _ptr(out),
+                                  _ptr(dout), _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv),
+                                  _ptr(workspace), nbytes, _stream(stream)))
+
+
+def strata_tile_blend(tiles, nty, ntx, stride_y, stride_x, window, out, stream=None):
+    T, P, Ht, Wt, C = tiles.shape
+    _, Hf, Wf, _ = out.shape
+    _check(load().strata_tile_blend(_ptr(tiles), nty, ntx, P, Ht, Wt, C, stride_y, stride_x,
+                                    _ptr(window), _ptr(out), Hf, Wf, _dtype(tiles), _stream(stream)))
+
+
+def strata_tile_extract(face, nty, ntx, stride_y, stride_x, tiles, stream=None):
+    P, Hf, Wf, C = face.shape
+    _, _, Ht, Wt, _ = tiles.shape
+    _check(load().strata_tile_extract(_ptr(face), nty, ntx, P, Ht, Wt, C, stride_y, stride_x, Hf, Wf,
+                                      _ptr(tiles), _dtype(face), _stream(stream)))
+
+
+def strata_na_axis_index(L, k, starts, qlo, qhi, stream=None):
+    _check(load().strata_na_axis_index(L, k, _ptr(starts), _ptr(qlo), _ptr(qhi), _stream(stream)))

@@ -1,0 +1,232 @@
+// The C ABI of libstrata: argument validation, kernel selection, error reporting.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace strata {
+
+static thread_local char g_err[512] = "";
+
+strata_status set_error(strata_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+strata_status check_launch(const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return set_error(STRATA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return STRATA_OK;
+}
+
+static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+#define REQUIRE(cond, ...)                                          \
+  do {                                                              \
+    if (!(cond)) return set_error(STRATA_ERR_INVALID_ARG, __VA_ARGS__); \
+  } while (0)
+
+#define REQUIRE_PTR(p)                                                              \
+  do {                                                                              \
+    if (!(p)) return set_error(STRATA_ERR_INVALID_ARG, "%s: null pointer", #p);     \
+    if (!aligned16(p)) return set_error(STRATA_ERR_INVALID_ARG, "%s: not 16-byte aligned", #p); \
+  } while (0)
+
+static const int64_t kMaxElems = (int64_t)1 << 40;
+
+static strata_status check_desc(const strata_na3d_desc* d) {
+  REQUIRE(d, "desc: null pointer");
+  REQUIRE(d->B > 0 && d->heads > 0 && d->Z > 0 && d->H > 0 && d->W > 0 && d->head_dim > 0,
+          "desc: every size must be positive (B=%d heads=%d Z=%d H=%d W=%d head_dim=%d)", d->B,
+          d->heads, d->Z, d->H, d->W, d->head_dim);
+  REQUIRE(d->kz > 0 && d->ky > 0 && d->kx > 0 && (d->kz & 1) && (d->ky & 1) && (d->kx & 1),
+          "desc: window sizes must be odd and positive (%d, %d, %d)", d->kz, d->ky, d->kx);
+  REQUIRE(d->kz <= d->Z && d->ky <= d->H && d->kx <= d->W,
+          "desc: window (%d, %d, %d) larger than the grid (%d, %d, %d)", d->kz, d->ky, d->kx, d->Z,
+          d->H, d->W);
+  REQUIRE(d->scale > 0.f && isfinite(d->scale), "desc: scale must be finite and > 0");
+  REQUIRE(d->dtype == STRATA_F32 || d->dtype == STRATA_BF16, "desc: unknown dtype %d", (int)d->dtype);
+  int64_t n = (int64_t)d->B * d->heads * d->Z * d->H * d->W;
+  REQUIRE(n * d->head_dim < kMaxElems, "desc: tensor too large");
+  if (d->head_dim != 32 && d->head_dim != 64)
+    return set_error(STRATA_ERR_UNSUPPORTED, "head_dim %d not supported (32 or 64)", d->head_dim);
+  return STRATA_OK;
+}
+
+}  // namespace strata
+
+using namespace strata;
+
+extern "C" {
+
+const char* strata_status_string(strata_status st) {
+  switch (st) {
+    case STRATA_OK: return "ok";
+    case STRATA_ERR_INVALID_ARG: return "invalid argument";
+    case STRATA_ERR_UNSUPPORTED: return "unsupported";
+    case STRATA_ERR_WORKSPACE: return "workspace too small";
+    case STRATA_ERR_HIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+const char* strata_last_error(void) { return g_err; }
+
+strata_status strata_na_axis_index(int32_t L, int32_t k, int32_t* starts, int32_t* qlo,
+                                   int32_t* qhi, void* stream) {
+  REQUIRE(L > 0 && k > 0 && (k & 1) && k <= L, "axis: need odd 1 <= k <= L (L=%d, k=%d)", L, k);
+  REQUIRE_PTR(starts);
+  REQUIRE_PTR(qlo);
+  REQUIRE_PTR(qhi);
+  launch_axis_index(L, k, starts, qlo, qhi, (hipStream_t)stream);
+  return check_launch("strata_na_axis_index");
+}
+
+strata_status strata_stereo_coords(const int32_t* tile_face, const int32_t* tile_oy,
+                                   const int32_t* tile_ox, int32_t B, int32_t H, int32_t W,
+                                   int32_t face_cells, int32_t patch, double l_scale,
+                                   float* coords, void* stream) {
+  REQUIRE(B > 0 && H > 0 && W > 0, "coords: sizes must be positive");
+  REQUIRE(face_cells > 0 && patch > 0 && face_cells % patch == 0,
+          "coords: face_cells must be a positive multiple of patch");
+  REQUIRE(H * (int64_t)patch <= face_cells && W * (int64_t)patch <= face_cells,
+          "coords: tile larger than the face");
+  REQUIRE(l_scale > 0.0 && isfinite(l_scale), "coords: l_scale must be finite and > 0");
+  REQUIRE_PTR(tile_face);
+  REQUIRE_PTR(tile_oy);
+  REQUIRE_PTR(tile_ox);
+  REQUIRE_PTR(coords);
+  launch_stereo_coords(tile_face, tile_oy, tile_ox, B, H, W, face_cells, patch, l_scale, coords,
+                       (hipStream_t)stream);
+  return check_launch("strata_stereo_coords");
+}
+
+strata_status strata_stereorope_phases(const float* coords, int32_t B, int32_t H, int32_t W,
+                                       int32_t head_dim, double base, float* cs, void* stream) {
+  REQUIRE(B > 0 && H > 0 && W > 0, "phases: sizes must be positive");
+  REQUIRE(head_dim > 0 && head_dim % 4 == 0, "phases: head_dim %d must be a positive multiple of 4",
+          head_dim);
+  REQUIRE(base > 0.0 && isfinite(base), "phases: base must be finite and > 0");
+  REQUIRE_PTR(coords);
+  REQUIRE_PTR(cs);
+  launch_rope_phases(coords, B, H, W, head_dim, base, cs, (hipStream_t)stream);
+  return check_launch("strata_stereorope_phases");
+}
+
+strata_status strata_stereorope_apply(const void* x, void* y, const float* cs, int32_t B,
+                                      int32_t heads, int32_t Z, int32_t H, int32_t W,
+                                      int32_t head_dim, strata_dtype dtype, int32_t transpose,
+                                      void* stream) {
+  REQUIRE(B > 0 && heads > 0 && Z > 0 && H > 0 && W > 0 && head_dim > 0,
+          "rope: sizes must be positive");
+  REQUIRE(head_dim % 4 == 0, "rope: head_dim %d must be a multiple of 4", head_dim);
+  REQUIRE(dtype == STRATA_F32 || dtype == STRATA_BF16, "rope: unknown dtype %d", (int)dtype);
+  REQUIRE((int64_t)B * heads * Z * H * W * head_dim < kMaxElems, "rope: tensor too large");
+  REQUIRE_PTR(x);
+  REQUIRE_PTR(y);
+  REQUIRE_PTR(cs);
+  if (head_dim % 8 != 0)
+    return set_error(STRATA_ERR_UNSUPPORTED, "rope: head_dim %d not a multiple of 8", head_dim);
+  launch_rope_apply(x, y, cs, B, heads, Z, H, W, head_dim, dtype, transpose, (hipStream_t)stream);
+  return check_launch("strata_stereorope_apply");
+}
+
+strata_status strata_na3d_fwd(const strata_na3d_desc* desc, const void* q, const void* k,
+                              const void* v, const float* cs, void* out, float* lse,
+                              void* stream) {
+  strata_status st = check_desc(desc);
+  if (st != STRATA_OK) return st;
+  REQUIRE_PTR(q);
+  REQUIRE_PTR(k);
+  REQUIRE_PTR(v);
+  REQUIRE_PTR(out);
+  if (cs) REQUIRE(aligned16(cs), "cs: not 16-byte aligned");
+  if (lse) REQUIRE(aligned16(lse), "lse: not 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  if (!launch_na3d_fwd_mfma(*desc, q, k, v, cs, out, lse, s))
+    launch_na3d_fwd_ref(*desc, q, k, v, cs, out, lse, s);
+  return check_launch("strata_na3d_fwd");
+}
+
+size_t strata_na3d_bwd_workspace_size(const strata_na3d_desc* desc) {
+  if (!desc || check_desc(desc) != STRATA_OK) return 0;
+  size_t n = (size_t)desc->B * desc->heads * desc->Z * desc->H * desc->W;
+  return ((n * sizeof(float)) + 255) & ~(size_t)255;
+}
+
+strata_status strata_na3d_bwd(const strata_na3d_desc* desc, const void* q, const void* k,
+                              const void* v, const float* cs, const void* out, const void* dout,
+                              const float* lse, void* dq, void* dk, void* dv, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  strata_status st = check_desc(desc);
+  if (st != STRATA_OK) return st;
+  REQUIRE_PTR(q);
+  REQUIRE_PTR(k);
+  REQUIRE_PTR(v);
+  REQUIRE_PTR(out);
+  REQUIRE_PTR(dout);
+  REQUIRE_PTR(lse);
+  REQUIRE_PTR(dq);
+  REQUIRE_PTR(dk);
+  REQUIRE_PTR(dv);
+  if (cs) REQUIRE(aligned16(cs), "cs: not 16-byte aligned");
+  size_t need = strata_na3d_bwd_workspace_size(desc);
+  if (!workspace || workspace_bytes < need)
+    return set_error(STRATA_ERR_WORKSPACE, "workspace: need %zu bytes, got %zu", need,
+                     workspace ? workspace_bytes : (size_t)0);
+  REQUIRE(aligned16(workspace), "workspace: not 16-byte aligned");
+  launch_na3d_bwd_ref(*desc, q, k, v, cs, out, dout, lse, dq, dk, dv, static_cast<float*>(workspace),
+                      (hipStream_t)stream);
+  return check_launch("strata_na3d_bwd");
+}
+
+static strata_status check_tiling(int32_t nty, int32_t ntx, int32_t P, int32_t Ht, int32_t Wt,
+                                  int32_t C, int32_t sy, int32_t sx, int32_t Hf, int32_t Wf,
+                                  strata_dtype dt) {
+  REQUIRE(nty > 0 && ntx > 0 && P > 0 && Ht > 0 && Wt > 0 && C > 0 && sy > 0 && sx > 0 && Hf > 0 &&
+              Wf > 0,
+          "tiling: sizes and strides must be positive");
+  REQUIRE((int64_t)(nty - 1) * sy + Ht <= Hf && (int64_t)(ntx - 1) * sx + Wt <= Wf,
+          "tiling: tiles extend past the face ((%d-1)*%d+%d > %d or (%d-1)*%d+%d > %d)", nty, sy, Ht,
+          Hf, ntx, sx, Wt, Wf);
+  REQUIRE(dt == STRATA_F32 || dt == STRATA_BF16, "tiling: unknown dtype %d", (int)dt);
+  REQUIRE((int64_t)nty * ntx * P * Ht * Wt * C < kMaxElems &&
+              (int64_t)P * Hf * Wf * C < kMaxElems,
+          "tiling: tensor too large");
+  return STRATA_OK;
+}
+
+strata_status strata_tile_blend(const void* tiles, int32_t nty, int32_t ntx, int32_t P,
+                                int32_t Ht, int32_t Wt, int32_t C, int32_t stride_y,
+                                int32_t stride_x, const float* window, void* out, int32_t Hf,
+                                int32_t Wf, strata_dtype dtype, void* stream) {
+  strata_status st = check_tiling(nty, ntx, P, Ht, Wt, C, stride_y, stride_x, Hf, Wf, dtype);
+  if (st != STRATA_OK) return st;
+  REQUIRE_PTR(tiles);
+  REQUIRE_PTR(window);
+  REQUIRE_PTR(out);
+  launch_tile_blend(tiles, nty, ntx, P, Ht, Wt, C, stride_y, stride_x, window, out, Hf, Wf, dtype,
+                    (hipStream_t)stream);
+  return check_launch("strata_tile_blend");
+}
+
+strata_status strata_tile_extract(const void* face, int32_t nty, int32_t ntx, int32_t P,
+                                  int32_t Ht, int32_t Wt, int32_t C, int32_t stride_y,
+                                  int32_t stride_x, int32_t Hf, int32_t Wf, void* tiles,
+                                  strata_dtype dtype, void* stream) {
+  strata_status st = check_tiling(nty, ntx, P, Ht, Wt, C, stride_y, stride_x, Hf, Wf, dtype);
+  if (st != STRATA_OK) return st;
+  REQUIRE_PTR(face);
+  REQUIRE_PTR(tiles);
+  launch_tile_extract(face, nty, ntx, P, Ht, Wt, C, stride_y, stride_x, Hf, Wf, tiles, dtype,
+                      (hipStream_t)stream);
+  return check_launch("strata_tile_extract");
+}
+
+}  // extern "C"

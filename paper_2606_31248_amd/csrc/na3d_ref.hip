@@ -1,0 +1,276 @@
+// Plain neighbourhood-attention kernels: one thread per query (forward, dq) or
+// per key (dk/dv), float32 arithmetic, StereoRoPE applied while loading.
+// They serve the float32 path and every shape the MFMA kernels do not cover.
+#include "common.h"
+#include "kernels.h"
+
+namespace strata {
+
+template <typename T>
+__device__ __forceinline__ float ld(const T* p);
+template <>
+__device__ __forceinline__ float ld<float>(const float* p) { return *p; }
+template <>
+__device__ __forceinline__ float ld<uint16_t>(const uint16_t* p) { return bf16_to_f32(*p); }
+
+template <typename T>
+__device__ __forceinline__ void st(T* p, float v);
+template <>
+__device__ __forceinline__ void st<float>(float* p, float v) { *p = v; }
+template <>
+__device__ __forceinline__ void st<uint16_t>(uint16_t* p, float v) { *p = f32_to_bf16(v); }
+
+// Load a head_dim vector and rotate it by the phases of its (b, y, x) (sign -1: R^T).
+template <typename T, int D>
+__device__ __forceinline__ void load_rot(const T* src, const float2* ph, float sign, float* dst) {
+#pragma unroll
+  for (int t = 0; t < D / 2; ++t) {
+    float a = ld(src + 2 * t), b = ld(src + 2 * t + 1);
+    if (ph) {
+      float2 p = ph[t];
+      float s = sign * p.y;
+      dst[2 * t] = fmaf(a, p.x, -b * s);
+      dst[2 * t + 1] = fmaf(a, s, b * p.x);
+    } else {
+      dst[2 * t] = a;
+      dst[2 * t + 1] = b;
+    }
+  }
+}
+
+struct Dims {
+  int B, heads, Z, H, W, kz, ky, kx;
+  float scale;
+};
+
+__device__ __forceinline__ void split_tok(int64_t i, const Dims& d, int& b, int& h, int& z, int& y,
+                                          int& x) {
+  x = (int)(i % d.W); i /= d.W;
+  y = (int)(i % d.H); i /= d.H;
+  z = (int)(i % d.Z); i /= d.Z;
+  h = (int)(i % d.heads); i /= d.heads;
+  b = (int)i;
+}
+
+template <typename T, int D>
+__global__ void __launch_bounds__(128) na3d_fwd_ref_kernel(const T* __restrict__ q, const T* __restrict__ k,
+                                                           const T* __restrict__ v, const float2* __restrict__ cs,
+                                                           T* __restrict__ out, float* __restrict__ lse, Dims dm) {
+  int64_t nq = (int64_t)dm.B * dm.heads * dm.Z * dm.H * dm.W;
+  int64_t qi = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (qi >= nq) return;
+  int b, h, z, y, x;
+  split_tok(qi, dm, b, h, z, y, x);
+  const int64_t bh = (int64_t)b * dm.heads + h;
+  float qv[D], kv[D], acc[D];
+  load_rot<T, D>(q + qi * D, cs ? cs + (((int64_t)b * dm.H + y) * dm.W + x) * (D / 2) : nullptr, 1.f, qv);
+#pragma unroll
+  for (int e = 0; e < D; ++e) acc[e] = 0.f;
+  float m = -INFINITY, l = 0.f;
+  int zs = win_start(z, dm.Z, dm.kz), ys = win_start(y, dm.H, dm.ky), xs = win_start(x, dm.W, dm.kx);
+  for (int jz = zs; jz < zs + dm.kz; ++jz)
+    for (int jy = ys; jy < ys + dm.ky; ++jy)
+      for (int jx = xs; jx < xs + dm.kx; ++jx) {
+        int64_t kj = ((bh * dm.Z + jz) * dm.H + jy) * dm.W + jx;
+        load_rot<T, D>(k + kj * D, cs ? cs + (((int64_t)b * dm.H + jy) * dm.W + jx) * (D / 2) : nullptr, 1.f, kv);
+        float s = 0.f;
+#pragma unroll
+        for (int e = 0; e < D; ++e) s = fmaf(qv[e], kv[e], s);
+        s *= dm.scale;
+        float mn = fmaxf(m, s);
+        float alpha = expf(m - mn);
+        float p = expf(s - mn);
+        l = fmaf(l, alpha, p);
+        const T* vr = v + kj * D;
+#pragma unroll
+        for (int e = 0; e < D; ++e) acc[e] = fmaf(acc[e], alpha, p * ld(vr + e));
+        m = mn;
+      }
+  float inv = 1.f / l;
+#pragma unroll
+  for (int e = 0; e < D; ++e) st(out + qi * D + e, acc[e] * inv);
+  if (lse) lse[qi] = m + logf(l);
+}
+
+template <typename T, int D>
+static void fwd_ref(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
+                    const float* cs, void* out, float* lse, hipStream_t s) {
+  Dims dm{d.B, d.heads, d.Z, d.H, d.W, d.kz, d.ky, d.kx, d.scale};
+  int64_t nq = (int64_t)d.B * d.heads * d.Z * d.H * d.W;
+  int threads = 128;
+  int blocks = (int)((nq + threads - 1) / threads);
+  hipLaunchKernelGGL((na3d_fwd_ref_kernel<T, D>), dim3(blocks), dim3(threads), 0, s,
+                     static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
+                     reinterpret_cast<const float2*>(cs), static_cast<T*>(out), lse, dm);
+}
+
+void launch_na3d_fwd_ref(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
+                         const float* cs, void* out, float* lse, hipStream_t s) {
+  if (d.dtype == STRATA_BF16) {
+    if (d.head_dim == 32) fwd_ref<uint16_t, 32>(d, q, k, v, cs, out, lse, s);
+    else fwd_ref<uint16_t, 64>(d, q, k, v, cs, out, lse, s);
+  } else {
+    if (d.head_dim == 32) fwd_ref<float, 32>(d, q, k, v, cs, out, lse, s);
+    else fwd_ref<float, 64>(d, q, k, v, cs, out, lse, s);
+  }
+}
+
+// ---- backward ----------------------------------------------------------------
+// D_i = <dout_i, out_i> in float32.
+template <typename T, int D>
+__global__ void na3d_bwd_pre_kernel(const T* __restrict__ out, const T* __restrict__ dout,
+                                    float* __restrict__ dvec, int64_t nq) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= nq) return;
+  float acc = 0.f;
+#pragma unroll
+  for (int e = 0; e < D; ++e) acc = fmaf(ld(dout + i * D + e), ld(out + i * D + e), acc);
+  dvec[i] = acc;
+}
+
+template <typename T, int D>
+__global__ void __launch_bounds__(128) na3d_bwd_dq_ref_kernel(
+    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v, const float2* __restrict__ cs,
+    const T* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ dvec,
+    T* __restrict__ dq, Dims dm) {
+  int64_t nq = (int64_t)dm.B * dm.heads * dm.Z * dm.H * dm.W;
+  int64_t qi = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (qi >= nq) return;
+  int b, h, z, y, x;
+  split_tok(qi, dm, b, h, z, y, x);
+  const int64_t bh = (int64_t)b * dm.heads + h;
+  float qv[D], kv[D], g[D], acc[D];
+  const float2* phq = cs ? cs + (((int64_t)b * dm.H + y) * dm.W + x) * (D / 2) : nullptr;
+  load_rot<T, D>(q + qi * D, phq, 1.f, qv);
+#pragma unroll
+  for (int e = 0; e < D; ++e) {
+    g[e] = ld(dout + qi * D + e);
+    acc[e] = 0.f;
+  }
+  const float L = lse[qi], Di = dvec[qi];
+  int zs = win_start(z, dm.Z, dm.kz), ys = win_start(y, dm.H, dm.ky), xs = win_start(x, dm.W, dm.kx);
+  for (int jz = zs; jz < zs + dm.kz; ++jz)
+    for (int jy = ys; jy < ys + dm.ky; ++jy)
+      for (int jx = xs; jx < xs + dm.kx; ++jx) {
+        int64_t kj = ((bh * dm.Z + jz) * dm.H + jy) * dm.W + jx;
+        load_rot<T, D>(k + kj * D, cs ? cs + (((int64_t)b * dm.H + jy) * dm.W + jx) * (D / 2) : nullptr, 1.f, kv);
+        float s = 0.f, dp = 0.f;
+        const T* vr = v + kj * D;
+#pragma unroll
+        for (int e = 0; e < D; ++e) {
+          s = fmaf(qv[e], kv[e], s);
+          dp = fmaf(g[e], ld(vr + e), dp);
+        }
+        float p = expf(s * dm.scale - L);
+        float ds = p * (dp - Di);
+#pragma unroll
+        for (int e = 0; e < D; ++e) acc[e] = fmaf(ds, kv[e], acc[e]);
+      }
+  // dq = R^T (scale * acc)
+#pragma unroll
+  for (int t = 0; t < D / 2; ++t) {
+    float a = dm.scale * acc[2 * t], bb = dm.scale * acc[2 * t + 1];
+    float c = 1.f, sn = 0.f;
+    if (phq) { c = phq[t].x; sn = -phq[t].y; }
+    st(dq + qi * D + 2 * t, fmaf(a, c, -bb * sn));
+    st(dq + qi * D + 2 * t + 1, fmaf(a, sn, bb * c));
+  }
+}
+
+// dk_j, dv_j: loop over the queries whose window holds key j (a box of
+// contiguous ranges per axis, closed form).
+__device__ __forceinline__ void inv_range(int j, int L, int k, int& lo, int& hi) {
+  int r = k >> 1;
+  hi = (j >= L - k) ? L - 1 : j + r;
+  lo = (j < k) ? 0 : j - r;
+}
+
+template <typename T, int D>
+__global__ void __launch_bounds__(128) na3d_bwd_dkdv_ref_kernel(
+    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v, const float2* __restrict__ cs,
+    const T* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ dvec,
+    T* __restrict__ dk, T* __restrict__ dv, Dims dm) {
+  int64_t nk = (int64_t)dm.B * dm.heads * dm.Z * dm.H * dm.W;
+  int64_t kj = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (kj >= nk) return;
+  int b, h, z, y, x;
+  split_tok(kj, dm, b, h, z, y, x);
+  const int64_t bh = (int64_t)b * dm.heads + h;
+  float kv[D], vv[D], qv[D], ak[D], av[D];
+  const float2* phk = cs ? cs + (((int64_t)b * dm.H + y) * dm.W + x) * (D / 2) : nullptr;
+  load_rot<T, D>(k + kj * D, phk, 1.f, kv);
+#pragma unroll
+  for (int e = 0; e < D; ++e) {
+    vv[e] = ld(v + kj * D + e);
+    ak[e] = 0.f;
+    av[e] = 0.f;
+  }
+  int zlo, zhi, ylo, yhi, xlo, xhi;
+  inv_range(z, dm.Z, dm.kz, zlo, zhi);
+  inv_range(y, dm.H, dm.ky, ylo, yhi);
+  inv_range(x, dm.W, dm.kx, xlo, xhi);
+  for (int iz = zlo; iz <= zhi; ++iz)
+    for (int iy = ylo; iy <= yhi; ++iy)
+      for (int ix = xlo; ix <= xhi; ++ix) {
+        int64_t qi = ((bh * dm.Z + iz) * dm.H + iy) * dm.W + ix;
+        load_rot<T, D>(q + qi * D, cs ? cs + (((int64_t)b * dm.H + iy) * dm.W + ix) * (D / 2) : nullptr, 1.f, qv);
+        float s = 0.f, dp = 0.f;
+        const T* gr = dout + qi * D;
+#pragma unroll
+        for (int e = 0; e < D; ++e) {
+          s = fmaf(qv[e], kv[e], s);
+          dp = fmaf(ld(gr + e), vv[e], dp);
+        }
+        float p = expf(s * dm.scale - lse[qi]);
+        float ds = p * (dp - dvec[qi]);
+#pragma unroll
+        for (int e = 0; e < D; ++e) {
+          av[e] = fmaf(p, ld(gr + e), av[e]);
+          ak[e] = fmaf(ds, qv[e], ak[e]);
+        }
+      }
+#pragma unroll
+  for (int t = 0; t < D / 2; ++t) {
+    float a = dm.scale * ak[2 * t], bb = dm.scale * ak[2 * t + 1];
+    float c = 1.f, sn = 0.f;
+    if (phk) { c = phk[t].x; sn = -phk[t].y; }
+    st(dk + kj * D + 2 * t, fmaf(a, c, -bb * sn));
+    st(dk + kj * D + 2 * t + 1, fmaf(a, sn, bb * c));
+    st(dv + kj * D + 2 * t, av[2 * t]);
+    st(dv + kj * D + 2 * t + 1, av[2 * t + 1]);
+  }
+}
+
+template <typename T, int D>
+static void bwd_ref(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
+                    const float* cs, const void* out, const void* dout, const float* lse, void* dq,
+                    void* dk, void* dv, float* dvec, hipStream_t s) {
+  Dims dm{d.B, d.heads, d.Z, d.H, d.W, d.kz, d.ky, d.kx, d.scale};
+  int64_t n = (int64_t)d.B * d.heads * d.Z * d.H * d.W;
+  int threads = 128;
+  int blocks = (int)((n + threads - 1) / threads);
+  const float2* c2 = reinterpret_cast<const float2*>(cs);
+  hipLaunchKernelGGL((na3d_bwd_pre_kernel<T, D>), dim3((int)((n + 255) / 256)), dim3(256), 0, s,
+                     static_cast<const T*>(out), static_cast<const T*>(dout), dvec, n);
+  hipLaunchKernelGGL((na3d_bwd_dq_ref_kernel<T, D>), dim3(blocks), dim3(threads), 0, s,
+                     static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), c2,
+                     static_cast<const T*>(dout), lse, dvec, static_cast<T*>(dq), dm);
+  hipLaunchKernelGGL((na3d_bwd_dkdv_ref_kernel<T, D>), dim3(blocks), dim3(threads), 0, s,
+                     static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), c2,
+                     static_cast<const T*>(dout), lse, dvec, static_cast<T*>(dk), static_cast<T*>(dv),
+                     dm);
+}
+
+void launch_na3d_bwd_ref(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
+                         const float* cs, const void* out, const void* dout, const float* lse,
+                         void* dq, void* dk, void* dv, float* dvec, hipStream_t s) {
+  if (d.dtype == STRATA_BF16) {
+    if (d.head_dim == 32) bwd_ref<uint16_t, 32>(d, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+    else bwd_ref<uint16_t, 64>(d, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+  } else {
+    if (d.head_dim == 32) bwd_ref<float, 32>(d, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+    else bwd_ref<float, 64>(d, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+  }
+}
+
+}  // namespace strata

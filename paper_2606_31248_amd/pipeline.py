@@ -1,0 +1,69 @@
+"""One pass of the hot path on device tensors, as a sequence of libstrata calls.
+
+coordinates (Eq. 1) -> StereoRoPE phases -> neighbourhood attention forward
+with the rotation fused into the Q/K loads -> tile stitch S = D^-1 P^T W.
+PyTorch only allocates device memory and supplies the stream.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Optional
+
+import torch
+
+from . import binding as B
+
+ROPE_BASE = 100.0
+
+
+def l_scale(face_cells: int) -> float:
+    """Eq. 1 normaliser sqrt(4 pi / N_total), N_total = 6 face_cells^2 native cells."""
+    return (4.0 * 3.141592653589793 / (6.0 * face_cells * face_cells)) ** 0.5
+
+
+@dataclasses.dataclass
+class TileGeometry:
+    face: torch.Tensor   # int32 [B] on device
+    oy: torch.Tensor     # int32 [B] token row of the tile origin
+    ox: torch.Tensor     # int32 [B] token column of the tile origin
+    face_cells: int = 2048
+    patch: int = 4
+
+
+def stereo_phases(geom: TileGeometry, H: int, W: int, head_dim: int,
+                  coords: Optional[torch.Tensor] = None, cs: Optional[torch.Tensor] = None,
+                  base: float = ROPE_BASE):
+    """Coordinates [B, H, W, 2] and phase table [B, H, W, head_dim/2, 2] (float32)."""
+    Bt = geom.face.shape[0]
+    dev = geom.face.device
+    if coords is None:
+        coords = torch.empty((Bt, H, W, 2), dtype=torch.float32, device=dev)
+    if cs is None:
+        cs = torch.empty((Bt, H, W, head_dim // 2, 2), dtype=torch.float32, device=dev)
+    B.strata_stereo_coords(geom.face, geom.oy, geom.ox, H, W, geom.face_cells, geom.patch,
+                           l_scale(geom.face_cells), coords)
+    B.strata_stereorope_phases(coords, head_dim, base, cs)
+    return coords, cs
+
+
+def na3d_forward(q, k, v, window, scale, cs=None, out=None, lse=None):
+    if out is None:
+        out = torch.empty_like(q)
+    desc = B.desc_for(q, window, scale)
+    B.strata_na3d_fwd(desc, q, k, v, cs, out, lse)
+    return out
+
+
+def face_step(q, k, v, geom: TileGeometry, window, scale, tiling, blend_window, face_out,
+              coords=None, cs=None, out=None):
+    """One face rollout step: per-tile NA3D forward with StereoRoPE, then the stitch.
+
+    q, k, v: [T, heads, Z, Ht, Wt, d]; tiling = (nty, ntx, stride_y, stride_x);
+    the tile outputs are viewed as [T, heads*Z, Ht, Wt, d] planes for the blend;
+    face_out: [heads*Z, Hf, Wf, d]."""
+    T, heads, Z, Ht, Wt, d = q.shape
+    coords, cs = stereo_phases(geom, Ht, Wt, d, coords, cs)
+    out = na3d_forward(q, k, v, window, scale, cs=cs, out=out)
+    nty, ntx, sy, sx = tiling
+    B.strata_tile_blend(out.view(T, heads * Z, Ht, Wt, d), nty, ntx, sy, sx, blend_window, face_out)
+    return face_out

@@ -1,0 +1,268 @@
+"""GPU parity of every hot-path entry point against the CPU oracle (through the C ABI).
+
+Rules: integer/index and blend/extract results bit-exact; float32 max abs error
+<= 1e-5; bf16 max abs error <= 2e-2 * RMS of the oracle output; LSE (float32)
+within 1e-5 (f32 inputs) or 2e-2 natural-log units (bf16 inputs)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import geometry as G
+from paper_2606_31248_amd import binding as B
+from paper_2606_31248_amd import inputs as I
+from paper_2606_31248_amd import pipeline
+from _util import LSE_ABS_BF16, check_close, dev_tensor, host_bits, host_f64
+
+pytestmark = pytest.mark.gpu
+
+ROPE_BASE = pipeline.ROPE_BASE
+
+
+def placement_dev(pl):
+    f, oy, ox = pl.as_int32()
+    return pipeline.TileGeometry(*(torch.from_numpy(a).cuda() for a in (f, oy, ox)))
+
+
+def oracle_coords(pl, H, W):
+    return G.tile_coords(pl.face, pl.oy, pl.ox, H, W).astype(np.float32)
+
+
+def gpu_phases(coords32, d):
+    c = torch.from_numpy(coords32).cuda()
+    cs = torch.empty(coords32.shape[:3] + (d // 2, 2), dtype=torch.float32, device="cuda")
+    B.strata_stereorope_phases(c, d, ROPE_BASE, cs)
+    return cs
+
+
+# ----------------------------------------------------------------------------- indexing
+
+@pytest.mark.parametrize("L,k", [(1, 1), (7, 7), (8, 3), (8, 5), (16, 7), (32, 7), (64, 9), (64, 7),
+                                 (512, 9), (5, 1), (13, 13)])
+def test_axis_index_bit_exact(L, k):
+    out = [torch.empty(L, dtype=torch.int32, device="cuda") for _ in range(3)]
+    B.strata_na_axis_index(L, k, *out)
+    ref = oracle.axis_index(L, k)
+    for g, r in zip(out, ref):
+        assert np.array_equal(g.cpu().numpy(), r)
+
+
+# ----------------------------------------------------------------------------- coordinates
+
+@pytest.mark.parametrize("wl", [I.TINY_F32, I.SMALL_BF16, I.FACE_ROLLOUT], ids=lambda w: w.name)
+def test_stereo_coords_match_oracle(wl):
+    pl = wl.placement()
+    geom = placement_dev(pl)
+    coords, _ = pipeline.stereo_phases(geom, wl.H, wl.W, wl.d)
+    got = coords.cpu().numpy().astype(np.float64)
+    ref = G.tile_coords(pl.face, pl.oy, pl.ox, wl.H, wl.W)
+    # float64 arithmetic on both sides, stored as float32: within one float32 ulp
+    ulp = np.spacing(np.abs(ref).astype(np.float32)).astype(np.float64)
+    assert np.all(np.abs(got - ref) <= ulp + 1e-30)
+
+
+def test_phase_table_matches_oracle():
+    wl = I.SMALL_BF16
+    c32 = oracle_coords(wl.placement(), wl.H, wl.W)
+    cs = gpu_phases(c32, wl.d).cpu().numpy().astype(np.float64)
+    ref = oracle.rope_phases(c32, wl.d, ROPE_BASE)
+    assert np.max(np.abs(cs - ref)) <= 1.2e-7
+
+
+# ----------------------------------------------------------------------------- RoPE apply
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("transpose", [False, True])
+def test_rope_apply_matches_oracle(dtype, transpose):
+    shape = (3, 2, 3, 12, 20, 64)
+    pl = I.random_placement(3, 12, 20, 77)
+    c32 = oracle_coords(pl, 12, 20)
+    x = I.gaussian(shape, 5, 0, dtype)
+    xd = dev_tensor(x, dtype)
+    y = torch.empty_like(xd)
+    B.strata_stereorope_apply(xd, y, gpu_phases(c32, 64), transpose=transpose)
+    ref = oracle.rope_apply(oracle.widen(x, dtype), c32, transpose=transpose, base=ROPE_BASE)
+    check_close(host_f64(y), ref, dtype, "rope")
+    if dtype == "bf16":  # one rounding of a float32 result: within 1 bf16 ulp of the exact value
+        assert np.all(np.abs(host_f64(y) - ref) <= np.abs(ref) * 2.0 ** -7 + 1e-6)
+
+
+def test_rope_apply_in_place_and_round_trip():
+    shape = (2, 3, 2, 8, 8, 32)
+    pl = I.random_placement(2, 8, 8, 78)
+    cs = gpu_phases(oracle_coords(pl, 8, 8), 32)
+    x = dev_tensor(I.gaussian(shape, 6, 0, "f32"), "f32")
+    y = x.clone()
+    B.strata_stereorope_apply(y, y, cs)
+    B.strata_stereorope_apply(y, y, cs, transpose=True)
+    assert torch.max(torch.abs(y - x)).item() <= 2e-6
+
+
+# ----------------------------------------------------------------------------- NA3D forward
+
+def run_fwd(wl_shape, window, dtype, seed, coords32=None, scale=None, want_lse=True):
+    Bt, heads, Z, H, W, d = wl_shape
+    q, k, v = (I.gaussian(wl_shape, seed, s, dtype) for s in (0, 1, 2))
+    scale = scale or 1.0 / np.sqrt(d)
+    qd, kd, vd = (dev_tensor(a, dtype) for a in (q, k, v))
+    cs = gpu_phases(coords32, d) if coords32 is not None else None
+    out = torch.empty_like(qd)
+    lse = torch.empty(wl_shape[:-1], dtype=torch.float32, device="cuda") if want_lse else None
+    B.strata_na3d_fwd(B.desc_for(qd, window, scale), qd, kd, vd, cs, out, lse)
+    torch.cuda.synchronize()
+    return (q, k, v), out, lse, scale
+
+
+def test_fwd_tiny_f32_full():
+    wl = I.TINY_F32
+    c32 = oracle_coords(wl.placement(), wl.H, wl.W)
+    (q, k, v), out, lse, scale = run_fwd(wl.shape(), (wl.kz, wl.ky, wl.kx), "f32", wl.seed, c32)
+    ro, rl = oracle.na3d_fwd(*(oracle.widen(a, "f32") for a in (q, k, v)), (wl.kz, wl.ky, wl.kx), scale,
+                             coords=c32)
+    check_close(host_f64(out), ro, "f32", "out")
+    assert np.max(np.abs(host_f64(lse) - rl)) <= 1e-5
+
+
+@pytest.mark.parametrize("shape,window", [
+    ((2, 3, 5, 19, 21, 64), (3, 7, 7)),     # ragged against 8x8 query blocks
+    ((1, 2, 6, 24, 24, 64), (5, 9, 9)),
+    ((2, 2, 3, 16, 12, 32), (3, 5, 7)),
+    ((1, 1, 8, 32, 32, 64), (3, 7, 7)),
+    ((1, 2, 4, 9, 9, 64), (1, 9, 9)),       # window = whole plane
+])
+@pytest.mark.parametrize("rope", [True, False])
+def test_fwd_bf16_full_oracle(shape, window, rope):
+    pl = I.random_placement(shape[0], shape[3], shape[4], 91)
+    c32 = oracle_coords(pl, shape[3], shape[4]) if rope else None
+    (q, k, v), out, lse, scale = run_fwd(shape, window, "bf16", 21, c32)
+    ro, rl = oracle.na3d_fwd(*(oracle.widen(a, "bf16") for a in (q, k, v)), window, scale, coords=c32)
+    check_close(host_f64(out), ro, "bf16", "out")
+    assert np.max(np.abs(host_f64(lse) - rl)) <= LSE_ABS_BF16
+
+
+def sample_queries(shape, n, seed, tiles=None):
+    """Random flat query indices plus every grid corner of the chosen tiles."""
+    Bt, heads, Z, H, W, _ = shape
+    r = np.random.default_rng(seed)
+    tiles = list(range(Bt)) if tiles is None else tiles
+    b = r.choice(tiles, n)
+    idx = np.stack([b, r.integers(0, heads, n), r.integers(0, Z, n), r.integers(0, H, n),
+                    r.integers(0, W, n)], 1)
+    corners = [(t, h, z, y, x) for t in tiles[:2] for h in (0, heads - 1) for z in (0, Z - 1)
+               for y in (0, 1, H - 1) for x in (0, 2, W - 1)]
+    idx = np.concatenate([idx, np.array(corners)], 0)
+    flat = (((idx[:, 0] * heads + idx[:, 1]) * Z + idx[:, 2]) * H + idx[:, 3]) * W + idx[:, 4]
+    return np.unique(flat)
+
+
+@pytest.mark.parametrize("wl", [I.SMALL_BF16, I.TRAIN_TILE, I.FACE_ROLLOUT], ids=lambda w: w.name)
+def test_fwd_full_size_sampled(wl):
+    """Full-size launch (the configuration the bench times); sampled outputs vs oracle.
+
+    The oracle sees only the tiles the samples fall in (tiles are independent)."""
+    shape = wl.shape()
+    window = (wl.kz, wl.ky, wl.kx)
+    pl = wl.placement()
+    c32 = oracle_coords(pl, wl.H, wl.W)
+    (q, k, v), out, lse, scale = run_fwd(shape, window, "bf16", wl.seed, c32)
+    tiles = sorted({0, shape[0] // 2, shape[0] - 1})
+    sel = sample_queries(shape, 3000, wl.seed, tiles)
+    per_tile = shape[1] * wl.N
+    sub = lambda a: oracle.widen(a[tiles], "bf16")
+    # re-index samples into the tile subset
+    tb = sel // per_tile
+    local = np.searchsorted(tiles, tb) * per_tile + sel % per_tile
+    ro, rl = oracle.na3d_fwd(sub(q), sub(k), sub(v), window, scale, coords=c32[tiles], sel=local)
+    got = host_f64(out).reshape(-1, wl.d)[sel]
+    check_close(got, ro, "bf16", "out")
+    assert np.max(np.abs(host_f64(lse).reshape(-1)[sel] - rl)) <= LSE_ABS_BF16
+    # a global property at full size: every output is a convex combination of v rows
+    o = out.float()
+    assert torch.isfinite(o).all()
+    vmax = float(np.max(np.abs(oracle.widen(v, "bf16"))))
+    assert torch.max(torch.abs(o)).item() <= vmax * (1 + 2.0 ** -7)
+
+
+def test_fwd_one_hot_probe_membership_bit_exact():
+    """Q = K = 0, V one-hot on 64 probe tokens: outputs are non-zero exactly where
+    the probe lies in the query's window (membership compared bit for bit)."""
+    Z, H, W, d = 6, 20, 23, 64
+    window = (3, 7, 5)
+    shape = (1, 2, Z, H, W, d)
+    N = Z * H * W
+    r = np.random.default_rng(5)
+    probes = r.choice(N, (2, d), replace=False) if N >= d else None
+    v = np.zeros(shape, np.float32)
+    for h in range(2):
+        for c in range(d):
+            v.reshape(2, N, d)[h, probes[h, c], c] = 1.0
+    zeros = np.zeros(shape, np.float32)
+    qd = dev_tensor(I.f32_to_bf16_bits(zeros), "bf16")
+    vd = dev_tensor(I.f32_to_bf16_bits(v), "bf16")
+    out = torch.empty_like(qd)
+    B.strata_na3d_fwd(B.desc_for(qd, window, 0.125), qd, qd, vd, None, out, None)
+    ro, _ = oracle.na3d_fwd(zeros.astype(np.float64), zeros.astype(np.float64), v.astype(np.float64),
+                            window, 0.125)
+    got = host_f64(out)
+    assert np.array_equal(got != 0, ro != 0)
+    check_close(got, ro, "bf16", "probe")
+
+
+def test_fwd_deterministic_and_lse_optional():
+    shape = (2, 4, 8, 32, 32, 64)
+    pl = I.random_placement(2, 32, 32, 3)
+    c32 = oracle_coords(pl, 32, 32)
+    (q, k, v), out1, lse1, scale = run_fwd(shape, (3, 7, 7), "bf16", 9, c32)
+    _, out2, _, _ = run_fwd(shape, (3, 7, 7), "bf16", 9, c32)
+    _, out3, lse3, _ = run_fwd(shape, (3, 7, 7), "bf16", 9, c32, want_lse=False)
+    assert torch.equal(out1, out2) and torch.equal(out1, out3)
+
+
+# ----------------------------------------------------------------------------- blend / extract
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_blend_and_extract_bit_exact_face_geometry(dtype):
+    nty = ntx = 9
+    Ht = Wt = 64
+    s = 56
+    Hf = Wf = 512
+    P, C = 3, 64 if dtype == "bf16" else 12
+    tiles = I.gaussian((81, P, Ht, Wt, C), 31, I.STREAM_FIELD, dtype)
+    win = I.ramp_window_2d(Ht, Wt, I.FACE_OVERLAP)
+    td = dev_tensor(tiles, dtype)
+    wd = torch.from_numpy(win).cuda()
+    out = torch.empty((P, Hf, Wf, C), dtype=td.dtype, device="cuda")
+    B.strata_tile_blend(td, nty, ntx, s, s, wd, out)
+    ref = oracle.tile_blend(tiles, nty, ntx, s, s, win, Hf, Wf, dtype)
+    assert np.array_equal(host_bits(out), ref)
+    back = torch.empty_like(td)
+    B.strata_tile_extract(out, nty, ntx, s, s, back)
+    assert np.array_equal(host_bits(back), oracle.tile_extract(ref, nty, ntx, Ht, Wt, s, s))
+
+
+@pytest.mark.parametrize("C", [1, 3, 8])
+def test_blend_ragged_channels_and_uncovered_cells(C):
+    # odd channel counts take the scalar path; a top-hat window leaves D == 0 cells
+    nty, ntx, Ht, Wt, sy, sx = 2, 3, 10, 9, 7, 6
+    Hf, Wf = (nty - 1) * sy + Ht + 3, (ntx - 1) * sx + Wt + 2
+    tiles = I.gaussian((6, 2, Ht, Wt, C), 32, I.STREAM_FIELD, "bf16")
+    win = I.tophat_window_2d(Ht, Wt, 1)
+    td = dev_tensor(tiles, "bf16")
+    out = torch.empty((2, Hf, Wf, C), dtype=torch.bfloat16, device="cuda")
+    B.strata_tile_blend(td, nty, ntx, sy, sx, torch.from_numpy(win).cuda(), out)
+    ref = oracle.tile_blend(tiles, nty, ntx, sy, sx, win, Hf, Wf, "bf16")
+    assert np.array_equal(host_bits(out), ref)
+
+
+def test_blend_full_face_rollout_planes():
+    """The face-rollout blend at full size; planes 0, 63, 127 compared bit for bit."""
+    wl = I.FACE_ROLLOUT
+    P = wl.heads * wl.Z
+    tiles = I.gaussian((81, P, 64, 64, 64), 33, I.STREAM_FIELD, "bf16")
+    win = I.ramp_window_2d(64, 64, I.FACE_OVERLAP)
+    td = dev_tensor(tiles, "bf16")
+    out = torch.empty((P, 512, 512, 64), dtype=torch.bfloat16, device="cuda")
+    B.strata_tile_blend(td, 9, 9, 56, 56, torch.from_numpy(win).cuda(), out)
+    planes = [0, 63, P - 1]
+    ref = oracle.tile_blend(np.ascontiguousarray(tiles[:, planes]), 9, 9, 56, 56, win, 512, 512, "bf16")
+    assert np.array_equal(host_bits(out[planes]), ref)
