@@ -1,32 +1,39 @@
-// bf16 MFMA neighbourhood-attention forward for gfx950 (head_dim 64).
+// MFMA neighbourhood-attention forward for gfx950 (bf16 in/out, head_dim 64).
 //
 // Work decomposition
 //   workgroup : one (tile, head), an 8 x 8 block of (y, x) query positions and
-//               ZB consecutive query levels; 4 waves of 64 lanes.
-//   wave      : a 4 x 4 (y, x) sub-block = 16 queries, for each of the ZB levels.
-//   key sweep : the workgroup walks the key levels its queries need, one at a
-//               time.  For each key level it stages the rotated K and the V of
-//               the (8+ky-1) x (8+kx-1) key box into LDS, then every wave updates
-//               the queries of each level whose z-window holds that key level.
+//               ZQ query levels; 8 waves, one workgroup per CU.
+//   wave      : a 4 x 4 (y, x) sub-block = 16 queries, on ZQ/2 of the levels
+//               (waves 0-3 take the even levels of the block, waves 4-7 the odd
+//               ones, so both halves have work at every key level).
+//   key sweep : the workgroup walks the key levels its queries need, each once.
+//               K and V of the (8+ky-1) x (8+kx-1) key box of a level are copied
+//               global -> LDS by the direct-to-LDS load (no registers), one level
+//               ahead of the compute, into a double buffer; K is then rotated in
+//               place (StereoRoPE) and rounded to float16.
 //
-// Per (query level, key level) a wave multiplies the keys of its 4x4 block's
+// Per (query level, key level) a wave multiplies the keys of its 4x4 sub-block's
 // box -- (3+ky) x (3+kx) keys, in 16-key chunks -- with its 16 queries:
 //   S^T (16 keys x 16 queries) = K . Q^T     v_mfma_f32_16x16x32_f16, the
-//                                           accumulator is seeded with the
-//                                           window mask (0 or -inf),
-//   online softmax on S^T in registers (each lane owns one query column),
-//   O^T (64 d x 16 queries) += V^T . P^T    V^T fragments come straight from
-//                                           the row-major V tile through the
-//                                           LDS transpose read; P^T is the S^T
-//                                           accumulator packed to bf16 in place.
-// The rotation of StereoRoPE is applied to Q when it is loaded into registers
-// and to K while it is staged, in float32.  The rotated Q and K are rounded to
-// float16, not bf16, for the Q.K^T contraction (v_mfma_f32_16x16x32_f16, same
-// rate): bf16 rounding of the rotated operands alone costs up to ~0.5% of an
-// output, beyond the parity bound, while float16 keeps it near 0.05%.  Inputs
-// beyond the float16 range (|x| > 65504 after rotation and scaling) saturate.
-// P and V stay bf16.  The logit scale and log2(e) are folded into Q so the
-// softmax uses exp2.
+//                                           accumulator seeded with the window
+//                                           mask (0 or -inf),
+//   online softmax on S^T in registers (a lane owns one query column); the
+//   running maximum only moves when it grows by more than 2^8, so most steps
+//   rescale nothing,
+//   O^T (64 d x 16 queries) += V^T . P^T    bf16 MFMA; V^T fragments come from
+//                                           the row-major V tile through the LDS
+//                                           transpose read, P^T is the S^T
+//                                           accumulator packed to bf16 in place;
+//   row sums of the packed P with v_dot2c_f32_bf16 (the same rounded weights the
+//   P.V product uses).
+// The rotated Q and K are rounded to float16, not bf16, for the Q.K^T contraction
+// (same MFMA rate): bf16 rounding of the rotated operands alone costs up to ~0.5%
+// of an output, beyond the parity bound; float16 keeps it near 0.05%.  Rotated
+// values beyond the float16 range (|x| > 65504) saturate.  P and V stay bf16.
+// The logit scale and log2(e) are folded into Q so the softmax uses exp2.
+//
+// LDS rows are padded (K: 144 bytes, V: 160 bytes per key) so the 16-byte K reads
+// and the 8-byte transpose reads of V hit distinct banks and take immediate offsets.
 #include "common.h"
 #include "kernels.h"
 
@@ -40,14 +47,21 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int kBY = 8, kBX = 8;      // query block of a workgroup (y, x)
-constexpr int kThreads = 256;        // 4 waves
-constexpr int kD = 64;               // head_dim
+constexpr int kBY = 8, kBX = 8;  // query block of a workgroup (y, x)
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kD = 64;           // head_dim
+constexpr int kKRow = 144;       // LDS bytes per key row of K (128 + 16 pad)
+constexpr int kVRow = 160;       // LDS bytes per key row of V (128 + 32 pad)
+constexpr int kLdsMax = 160 * 1024;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kLazy = 8.0f;    // rescale only when the maximum grows by > 2^8
 
-template <int KZ, int KY, int KX, int ZB>
+template <int KZ, int KY, int KX, int ZQ>
 struct Cfg {
   static constexpr int LY = kBY + KY - 1, LX = kBX + KX - 1;  // staged key box per level
   static constexpr int NUY = 3 + KY, NUX = 3 + KX;            // key box of one 4x4 sub-block
@@ -55,8 +69,19 @@ struct Cfg {
   static constexpr int NC = (NU + 15) / 16;                   // 16-key chunks
   static constexpr int NS = (NC + 1) / 2;                     // 32-key PV steps
   static constexpr int KEYS = LY * LX;
-  static constexpr int CHUNKS16 = KEYS * (kD * 2 / 16);       // 16-byte pieces per level per tensor
-  static constexpr int LDS_U4 = 2 * CHUNKS16;                 // K then V
+  static constexpr int KSLOTS = KEYS * (kKRow / 16);          // 16-byte slots of a K tile
+  static constexpr int VSLOTS = KEYS * (kVRow / 16);
+  static constexpr int KBYTES = KEYS * kKRow, VBYTES = KEYS * kVRow;
+  static constexpr int BUF = KBYTES + VBYTES;                 // one level: K then V
+  static constexpr int ITK = (KSLOTS + kThreads - 1) / kThreads;
+  static constexpr int ITV = (VSLOTS + kThreads - 1) / kThreads;
+  // per-thread copy offsets live in LDS when they fit, else in registers
+  static constexpr int GOFF_BYTES = (ITK + ITV) * kThreads * 4;
+  static constexpr bool GOFF_LDS = 2 * BUF + GOFF_BYTES <= kLdsMax;
+  static constexpr int LDS_BYTES = 2 * BUF + (GOFF_LDS ? GOFF_BYTES : 0);
+  static constexpr int QL = ZQ / 2;                           // query levels per wave
+  static_assert(ZQ % 2 == 0, "ZQ must be even");
+  static_assert(2 * BUF <= kLdsMax, "key tiles exceed LDS");
 };
 
 struct Args {
@@ -66,7 +91,7 @@ struct Args {
   const float4* cs;   // [B, H, W, 16] float4 = two (cos, sin) pairs; nullptr: no rotation
   uint16_t* out;
   float* lse;
-  int B, heads, Z, H, W;
+  int heads, Z, H, W;
   int n_zb, n_yb, n_xb;
   float qscale;       // scale * log2(e)
 };
@@ -77,15 +102,15 @@ __device__ __forceinline__ uint32_t pack2(float a, float b) {
   return __builtin_bit_cast(uint32_t, h);
 }
 
-__device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
-
 // Two floats -> packed float16 pair (nearest-even), saturating at +-65504.
 __device__ __forceinline__ uint32_t pack2h(float a, float b) {
   f32x2 f = {__builtin_amdgcn_fmed3f(a, -65504.f, 65504.f), __builtin_amdgcn_fmed3f(b, -65504.f, 65504.f)};
   f16x2 h = __builtin_convertvector(f, f16x2);
   return __builtin_bit_cast(uint32_t, h);
 }
+
+__device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
 // Rotate 4 pairs held as 4 packed bf16x2 words by phases (c0,s0,c1,s1),(c2,s2,c3,s3),
 // multiply by `mul`, and return them as 4 packed float16x2 words.
@@ -97,9 +122,7 @@ __device__ __forceinline__ uint4 rotate8h(uint4 x, float4 p01, float4 p23, float
   for (int t = 0; t < 4; ++t) {
     float a = lo_bf16(w[t]), b = hi_bf16(w[t]);
     float c = cs_[2 * t], s = cs_[2 * t + 1];
-    float y0 = fmaf(a, c, -b * s) * mul;
-    float y1 = fmaf(a, s, b * c) * mul;
-    r[t] = pack2h(y0, y1);
+    r[t] = pack2h(fmaf(a, c, -b * s) * mul, fmaf(a, s, b * c) * mul);
   }
   return make_uint4(r[0], r[1], r[2], r[3]);
 }
@@ -113,17 +136,44 @@ __device__ __forceinline__ uint4 scale8h(uint4 x, float mul) {
   return make_uint4(r[0], r[1], r[2], r[3]);
 }
 
-__device__ __forceinline__ i16x4 tr_read(const char* lds_base, uint32_t byte_off) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (__attribute__((address_space(3))) i16x4*)(lds_base + byte_off));
+__device__ __forceinline__ i16x4 tr_read(uint32_t byte_addr) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(uintptr_t)byte_addr);
 }
 
-template <int KZ, int KY, int KX, int ZB>
-__global__ void __launch_bounds__(kThreads, 2) na3d_fwd_mfma_kernel(Args a) {
-  using C = Cfg<KZ, KY, KX, ZB>;
-  __shared__ uint4 lds[C::LDS_U4];
-  uint4* ldsK = lds;
-  const char* ldsV = reinterpret_cast<const char*>(lds + C::CHUNKS16);
+__device__ __forceinline__ uint4 lds_read16(uint32_t byte_addr) {
+  u32x4 v = *(__attribute__((address_space(3))) u32x4*)(uintptr_t)byte_addr;
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ void lds_write16(uint32_t byte_addr, uint4 v) {
+  *(__attribute__((address_space(3))) u32x4*)(uintptr_t)byte_addr = u32x4{v.x, v.y, v.z, v.w};
+}
+
+__device__ __forceinline__ int lds_read_i32(uint32_t byte_addr) {
+  return *(__attribute__((address_space(3))) int*)(uintptr_t)byte_addr;
+}
+
+__device__ __forceinline__ void lds_write_i32(uint32_t byte_addr, int v) {
+  *(__attribute__((address_space(3))) int*)(uintptr_t)byte_addr = v;
+}
+
+// Direct global -> LDS copy of 16 bytes per lane: lane i of the wave writes
+// wave_dst + 16 i (wave_dst must be the same for the whole wave).
+__device__ __forceinline__ void copy16_to_lds(const uint16_t* src, uint32_t wave_dst) {
+  __builtin_amdgcn_global_load_lds(src, (lds_void*)(uintptr_t)wave_dst, 16, 0, 0);
+}
+
+__device__ __forceinline__ float psum8(uint32_t a, uint32_t b, float acc) {
+  const bf16x2 one = __builtin_bit_cast(bf16x2, 0x3F803F80u);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), one, acc, false);
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, b), one, acc, false);
+}
+
+template <int KZ, int KY, int KX, int ZQ>
+__global__ void __launch_bounds__(kThreads, 1) na3d_fwd_mfma_kernel(Args a) {
+  using C = Cfg<KZ, KY, KX, ZQ>;
+  extern __shared__ __attribute__((aligned(16))) char lds_raw[];
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_raw;
 
   // ---- block coordinates (XCD-aware: neighbouring blocks share an L2) -------
   const int nblk = gridDim.x;
@@ -135,16 +185,17 @@ __global__ void __launch_bounds__(kThreads, 2) na3d_fwd_mfma_kernel(Args a) {
   const int bh = bid / (a.n_xb * a.n_yb * a.n_zb);
   const int b = bh / a.heads;
   const int H = a.H, W = a.W, Z = a.Z;
-  const int by0 = yb * kBY, bx0 = xb * kBX, z0 = zb * ZB;
+  const int by0 = yb * kBY, bx0 = xb * kBX, z0 = zb * ZQ;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, qn = lane & 15;
+  const int sb = wave & 3, grp = wave >> 2;  // xy sub-block, level parity
 
   // staged key box of the workgroup, and the key box of this wave's sub-block
   const int ty0 = win_start(min(by0, H - 1), H, KY);
   const int tx0 = win_start(min(bx0, W - 1), W, KX);
-  const int sy0 = by0 + 4 * (wave >> 1), sx0 = bx0 + 4 * (wave & 1);
+  const int sy0 = by0 + 4 * (sb >> 1), sx0 = bx0 + 4 * (sb & 1);
   const int uy0 = win_start(min(sy0, H - 1), H, KY);
   const int ux0 = win_start(min(sx0, W - 1), W, KX);
   // this lane's query column (clamped into the grid; stores are masked later)
@@ -152,26 +203,22 @@ __global__ void __launch_bounds__(kThreads, 2) na3d_fwd_mfma_kernel(Args a) {
   const int qy = min(qy_raw, H - 1), qx = min(qx_raw, W - 1);
   const int wys = win_start(qy, H, KY), wxs = win_start(qx, W, KX);
 
-  // ---- per-lane LDS addresses and window mask, identical for every key level ----
+  // ---- per-lane LDS offsets and window mask, identical for every key level ----
   uint32_t kaddr[C::NC], vaddr[C::NC];
   f32x4 bias[C::NC];
 #pragma unroll
   for (int c = 0; c < C::NC; ++c) {
-    // K fragment (A operand): row = key 16c + qn, 16 bytes at column g (and g+4)
-    {
+    {  // K fragment (A operand): row = key 16c + qn, 16 bytes at column g (+64 bytes: g+4)
       int u = 16 * c + qn;
       int key = 0;
       if (u < C::NU) key = (uy0 - ty0 + u / C::NUX) * C::LX + (ux0 - tx0 + u % C::NUX);
-      kaddr[c] = key * 128 + ((g ^ (key & 7)) << 4);
+      kaddr[c] = key * kKRow + g * 16;
     }
-    // V^T fragment through the transpose read: source row = key 16c + 4g + qn/4,
-    // 8 bytes at element 4*(qn%4) of each 16-element d tile
-    {
+    {  // V^T fragment by transpose read: source row = key 16c + 4g + qn/4, element 4*(qn%4)
       int u = 16 * c + 4 * g + (qn >> 2);
       int key = 0;
       if (u < C::NU) key = (uy0 - ty0 + u / C::NUX) * C::LX + (ux0 - tx0 + u % C::NUX);
-      int hb = (qn & 3) >> 1;
-      vaddr[c] = key * 128 + ((hb ^ (key & 7)) << 4) + ((qn & 1) << 3);
+      vaddr[c] = C::KBYTES + key * kVRow + (qn & 3) * 8;
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -182,16 +229,79 @@ __global__ void __launch_bounds__(kThreads, 2) na3d_fwd_mfma_kernel(Args a) {
     }
   }
 
-  // ---- queries: load, rotate, scale, keep as the B operand of K.Q^T ----------
+  // ---- direct-to-LDS copy map: slot s = it*512 + tid of a tile ---------------
+  // K: 9 slots per key (8 data + pad), V: 10 slots per key (8 data + 2 pad).
+  // goff: element offset inside a key level, or -1 for pad / past-the-end slots.
+  // Each thread only ever reads back its own offsets: no barrier needed.
   const int64_t HW = (int64_t)H * W;
-  const int64_t bh_base = (int64_t)bh * Z * HW;  // token index of (b, h, 0, 0, 0)
-  f16x8 qf[ZB][2];
-  float m[ZB], l[ZB];
-  f32x4 o[ZB][4];
-  const float4* csq = a.cs ? a.cs + ((int64_t)b * HW + (int64_t)qy * W + qx) * 16 : nullptr;
+  const uint32_t goff_lds = lds0 + 2 * C::BUF + tid * 4;
+  int goffK_r[C::GOFF_LDS ? 1 : C::ITK], goffV_r[C::GOFF_LDS ? 1 : C::ITV];
+  auto goffK = [&](int it) {
+    return C::GOFF_LDS ? lds_read_i32(goff_lds + it * kThreads * 4) : goffK_r[C::GOFF_LDS ? 0 : it];
+  };
+  auto goffV = [&](int it) {
+    return C::GOFF_LDS ? lds_read_i32(goff_lds + (C::ITK + it) * kThreads * 4) : goffV_r[C::GOFF_LDS ? 0 : it];
+  };
 #pragma unroll
-  for (int j = 0; j < ZB; ++j) {
-    int zq = min(z0 + j, Z - 1);
+  for (int it = 0; it < C::ITK; ++it) {
+    int s = it * kThreads + tid, key = s / 9, c = s - key * 9;
+    int gy = min(ty0 + key / C::LX, H - 1), gx = min(tx0 + key % C::LX, W - 1);
+    int off = (s < C::KSLOTS && c < 8) ? (gy * W + gx) * kD + c * 8 : -1;
+    if (C::GOFF_LDS) lds_write_i32(goff_lds + it * kThreads * 4, off);
+    else goffK_r[C::GOFF_LDS ? 0 : it] = off;
+  }
+#pragma unroll
+  for (int it = 0; it < C::ITV; ++it) {
+    int s = it * kThreads + tid, key = s / 10, c = s - key * 10;
+    int gy = min(ty0 + key / C::LX, H - 1), gx = min(tx0 + key % C::LX, W - 1);
+    int off = (s < C::VSLOTS && c < 8) ? (gy * W + gx) * kD + c * 8 : -1;
+    if (C::GOFF_LDS) lds_write_i32(goff_lds + (C::ITK + it) * kThreads * 4, off);
+    else goffV_r[C::GOFF_LDS ? 0 : it] = off;
+  }
+  const float4* csb = a.cs ? a.cs + (int64_t)b * HW * 16 : nullptr;
+  const int64_t bh_base = (int64_t)bh * Z * HW;  // token index of (b, h, 0, 0, 0)
+
+  auto issue_copy = [&](int p, uint32_t buf) {
+    const uint16_t* kp = a.k + (bh_base + (int64_t)p * HW) * kD;
+    const uint16_t* vp = a.v + (bh_base + (int64_t)p * HW) * kD;
+    const uint32_t kdst = lds0 + buf + wave * 64 * 16, vdst = kdst + C::KBYTES;
+#pragma unroll
+    for (int it = 0; it < C::ITK; ++it) {
+      const int o = goffK(it);
+      if (o >= 0) copy16_to_lds(kp + o, kdst + it * kThreads * 16);
+    }
+#pragma unroll
+    for (int it = 0; it < C::ITV; ++it) {
+      const int o = goffV(it);
+      if (o >= 0) copy16_to_lds(vp + o, vdst + it * kThreads * 16);
+    }
+  };
+  // rotate (or convert) this thread's K slots of one buffer in place, bf16 -> float16
+  auto rotate_k = [&](uint32_t buf) {
+#pragma unroll
+    for (int it = 0; it < C::ITK; ++it) {
+      const int o = goffK(it);
+      if (o < 0) continue;
+      const uint32_t ad = lds0 + buf + (it * kThreads + tid) * 16;
+      uint4 x = lds_read16(ad);
+      if (csb) {
+        const float4* pp = csb + (o >> 6) * 16 + ((o & 63) >> 2);
+        x = rotate8h(x, pp[0], pp[1], 1.f);
+      } else {
+        x = scale8h(x, 1.f);
+      }
+      lds_write16(ad, x);
+    }
+  };
+
+  // ---- queries: load, rotate, scale, keep as the B operand of K.Q^T ----------
+  f16x8 qf[C::QL][2];
+  float m[C::QL], l[C::QL];
+  f32x4 o[C::QL][4];
+  const float4* csq = csb ? csb + ((int64_t)qy * W + qx) * 16 : nullptr;
+#pragma unroll
+  for (int j = 0; j < C::QL; ++j) {
+    int zq = min(z0 + grp + 2 * j, Z - 1);
     const uint4* src = reinterpret_cast<const uint4*>(a.q + (bh_base + zq * HW + (int64_t)qy * W + qx) * kD);
     uint4 x0 = src[g], x1 = src[4 + g];
     uint4 r0, r1;
@@ -210,95 +320,96 @@ __global__ void __launch_bounds__(kThreads, 2) na3d_fwd_mfma_kernel(Args a) {
     for (int t = 0; t < 4; ++t) o[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  // ---- key levels needed by the block's query levels --------------------------
-  const int zlast = min(z0 + ZB, Z) - 1;
-  const int kp_lo = win_start(z0, Z, KZ);
-  const int kp_hi = win_start(zlast, Z, KZ) + KZ;
-
-  for (int p = kp_lo; p < kp_hi; ++p) {
-    __syncthreads();  // every wave is done with the previous level's tiles
-    // stage K (rotated, float16) and V (bf16) of key level p: 16 bytes per thread per step
-    const int64_t lvl = bh_base + (int64_t)p * HW;
-    for (int idx = tid; idx < 2 * C::CHUNKS16; idx += kThreads) {
-      const bool isV = idx >= C::CHUNKS16;
-      const int ci = isV ? idx - C::CHUNKS16 : idx;
-      const int key = ci >> 3, col = ci & 7;
-      const int gy = ty0 + key / C::LX, gx = tx0 + key % C::LX;
-      uint4 val = make_uint4(0u, 0u, 0u, 0u);
-      if (gy < H && gx < W) {
-        const int64_t tok = lvl + (int64_t)gy * W + gx;
-        if (isV) {
-          val = reinterpret_cast<const uint4*>(a.v + tok * kD)[col];
-        } else {
-          val = reinterpret_cast<const uint4*>(a.k + tok * kD)[col];
-          if (a.cs) {
-            const float4* ph = a.cs + ((int64_t)b * HW + (int64_t)gy * W + gx) * 16 + 2 * col;
-            val = rotate8h(val, ph[0], ph[1], 1.f);
-          } else {
-            val = scale8h(val, 1.f);
-          }
-        }
-      }
-      lds[(isV ? C::CHUNKS16 : 0) + key * 8 + (col ^ (key & 7))] = val;
+  // one (query level j, key level) update with the key tile at buffer `buf`
+  auto update = [&](int j, uint32_t buf) {
+    f32x4 s[C::NC];
+#pragma unroll
+    for (int c = 0; c < C::NC; ++c) {
+      f16x8 k0 = __builtin_bit_cast(f16x8, lds_read16(lds0 + buf + kaddr[c]));
+      f16x8 k1 = __builtin_bit_cast(f16x8, lds_read16(lds0 + buf + kaddr[c] + 64));
+      f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(k0, qf[j][0], bias[c], 0, 0, 0);
+      s[c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(k1, qf[j][1], acc, 0, 0, 0);
     }
-    __syncthreads();
-
+    float mx = fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3]));
 #pragma unroll
-    for (int j = 0; j < ZB; ++j) {
-      const int zq = z0 + j;
-      if (zq >= Z) continue;
-      const int zs = win_start(zq, Z, KZ);
-      if (p < zs || p >= zs + KZ) continue;
-
-      // S^T = K . Q^T, seeded with the window mask
-      f32x4 s[C::NC];
-#pragma unroll
-      for (int c = 0; c < C::NC; ++c) {
-        const char* kb = reinterpret_cast<const char*>(ldsK);
-        f16x8 k0 = __builtin_bit_cast(f16x8, *reinterpret_cast<const uint4*>(kb + kaddr[c]));
-        f16x8 k1 = __builtin_bit_cast(f16x8, *reinterpret_cast<const uint4*>(kb + (kaddr[c] ^ 64u)));
-        f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(k0, qf[j][0], bias[c], 0, 0, 0);
-        s[c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(k1, qf[j][1], acc, 0, 0, 0);
-      }
-      // online softmax (log2 domain); each lane owns one query, 4 keys per chunk
-      float mx = -INFINITY;
-#pragma unroll
-      for (int c = 0; c < C::NC; ++c)
-        mx = fmaxf(fmaxf(mx, fmaxf(s[c][0], s[c][1])), fmaxf(s[c][2], s[c][3]));
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+    for (int c = 1; c < C::NC; ++c)
+      mx = fmaxf(fmaxf(mx, fmaxf(s[c][0], s[c][1])), fmaxf(s[c][2], s[c][3]));
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    if (__any(mx > m[j] + kLazy)) {  // rare: move the running maximum, rescale
       const float mn = fmaxf(m[j], mx);
       const float alpha = __builtin_amdgcn_exp2f(m[j] - mn);
       m[j] = mn;
-      float ls = 0.f;
-      uint32_t pk[C::NC][2];
-#pragma unroll
-      for (int c = 0; c < C::NC; ++c) {
-        float p0 = __builtin_amdgcn_exp2f(s[c][0] - mn);
-        float p1 = __builtin_amdgcn_exp2f(s[c][1] - mn);
-        float p2 = __builtin_amdgcn_exp2f(s[c][2] - mn);
-        float p3 = __builtin_amdgcn_exp2f(s[c][3] - mn);
-        ls += (p0 + p1) + (p2 + p3);
-        pk[c][0] = pack2(p0, p1);
-        pk[c][1] = pack2(p2, p3);
-      }
-      l[j] = fmaf(l[j], alpha, ls);
+      l[j] *= alpha;
 #pragma unroll
       for (int t = 0; t < 4; ++t) o[j][t] *= alpha;
-      // O^T += V^T . P^T over 32-key steps (chunks 2s, 2s+1)
+    }
+    const float mj = m[j];
+    uint32_t pk[C::NC][2];
+    float ls = l[j];
 #pragma unroll
-      for (int st = 0; st < C::NS; ++st) {
-        const int c0 = 2 * st, c1 = 2 * st + 1;
-        uint4 pb = make_uint4(pk[c0][0], pk[c0][1], c1 < C::NC ? pk[c1][0] : 0u, c1 < C::NC ? pk[c1][1] : 0u);
-        bf16x8 pf = __builtin_bit_cast(bf16x8, pb);
+    for (int c = 0; c < C::NC; ++c) {
+      pk[c][0] = pack2(__builtin_amdgcn_exp2f(s[c][0] - mj), __builtin_amdgcn_exp2f(s[c][1] - mj));
+      pk[c][1] = pack2(__builtin_amdgcn_exp2f(s[c][2] - mj), __builtin_amdgcn_exp2f(s[c][3] - mj));
+      ls = psum8(pk[c][0], pk[c][1], ls);
+    }
+    l[j] = ls;
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          i16x4 lo = tr_read(ldsV, vaddr[c0] ^ (uint32_t)(t << 5));
-          i16x4 hi = c1 < C::NC ? tr_read(ldsV, vaddr[c1] ^ (uint32_t)(t << 5)) : i16x4{0, 0, 0, 0};
-          uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
-          bf16x8 vf = __builtin_bit_cast(bf16x8, make_uint4(l2.x, l2.y, h2.x, h2.y));
-          o[j][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[j][t], 0, 0, 0);
-        }
+    for (int st = 0; st < C::NS; ++st) {
+      const int c0 = 2 * st, c1 = 2 * st + 1;
+      const bool two = c1 < C::NC;
+      bf16x8 pf = __builtin_bit_cast(bf16x8, make_uint4(pk[c0][0], pk[c0][1], two ? pk[c1][0] : 0u, two ? pk[c1][1] : 0u));
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        i16x4 lo = tr_read(lds0 + buf + vaddr[c0] + 32 * t);
+        i16x4 hi = two ? tr_read(lds0 + buf + vaddr[c1] + 32 * t) : i16x4{0, 0, 0, 0};
+        uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
+        bf16x8 vf = __builtin_bit_cast(bf16x8, make_uint4(l2.x, l2.y, h2.x, h2.y));
+        o[j][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[j][t], 0, 0, 0);
+      }
+    }
+  };
+
+  // all query levels of this wave whose window holds key level p
+  auto compute = [&](int p, uint32_t buf) {
+#pragma unroll
+    for (int j = 0; j < C::QL; ++j) {
+      const int zq = z0 + grp + 2 * j;
+      if (zq >= Z) continue;
+      const int zs = win_start(zq, Z, KZ);
+      if (p < zs || p >= zs + KZ) continue;
+      update(j, buf);
+    }
+  };
+
+  // ---- key levels needed by the block's query levels, double-buffered -------
+  const int zlast = min(z0 + ZQ, Z) - 1;
+  const int kp_lo = win_start(z0, Z, KZ);
+  const int kp_hi = win_start(zlast, Z, KZ) + KZ;
+
+  issue_copy(kp_lo, 0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  rotate_k(0);
+  __syncthreads();
+  for (int p = kp_lo; p < kp_hi; p += 2) {
+    // level p in buffer 0, level p+1 (if any) in buffer 1
+    const bool more1 = p + 1 < kp_hi;
+    if (more1) issue_copy(p + 1, C::BUF);
+    compute(p, 0);
+    if (more1) {
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      rotate_k(C::BUF);
+      __syncthreads();
+      const bool more2 = p + 2 < kp_hi;
+      if (more2) issue_copy(p + 2, 0);
+      compute(p + 1, C::BUF);
+      if (more2) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        rotate_k(0);
+        __syncthreads();
       }
     }
   }
@@ -306,28 +417,31 @@ __global__ void __launch_bounds__(kThreads, 2) na3d_fwd_mfma_kernel(Args a) {
   // ---- normalise and store --------------------------------------------------------
   const bool in_grid = qy_raw < H && qx_raw < W;
 #pragma unroll
-  for (int j = 0; j < ZB; ++j) {
-    const int zq = z0 + j;
-    if (zq >= Z) continue;
+  for (int j = 0; j < C::QL; ++j) {
+    const int zq = z0 + grp + 2 * j;
     float lt = l[j];
     lt += __shfl_xor(lt, 16);
     lt += __shfl_xor(lt, 32);
+    if (zq >= Z || !in_grid) continue;
     const float inv = 1.f / lt;
-    if (in_grid) {
-      const int64_t tok = bh_base + zq * HW + (int64_t)qy * W + qx;
-      uint2* dst = reinterpret_cast<uint2*>(a.out + tok * kD);
+    const int64_t tok = bh_base + zq * HW + (int64_t)qy * W + qx;
+    uint2* dst = reinterpret_cast<uint2*>(a.out + tok * kD);
 #pragma unroll
-      for (int t = 0; t < 4; ++t)   // d = 16t + 4g + i
-        dst[4 * t + g] = make_uint2(pack2(o[j][t][0] * inv, o[j][t][1] * inv),
-                                    pack2(o[j][t][2] * inv, o[j][t][3] * inv));
-      if (a.lse && g == 0) a.lse[tok] = (m[j] + __log2f(lt)) * kLn2;
-    }
+    for (int t = 0; t < 4; ++t)  // d = 16t + 4g + i
+      dst[4 * t + g] = make_uint2(pack2(o[j][t][0] * inv, o[j][t][1] * inv),
+                                  pack2(o[j][t][2] * inv, o[j][t][3] * inv));
+    if (a.lse && g == 0) a.lse[tok] = (m[j] + __log2f(lt)) * kLn2;
   }
 }
 
-template <int KZ, int KY, int KX, int ZB>
-void launch(const strata_na3d_desc& d, const void* q, const void* k, const void* v, const float* cs,
+template <int KZ, int KY, int KX, int ZQ>
+bool launch(const strata_na3d_desc& d, const void* q, const void* k, const void* v, const float* cs,
             void* out, float* lse, hipStream_t s) {
+  using C = Cfg<KZ, KY, KX, ZQ>;
+  static const bool lds_ok = hipFuncSetAttribute((const void*)na3d_fwd_mfma_kernel<KZ, KY, KX, ZQ>,
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                 C::LDS_BYTES) == hipSuccess;
+  if (!lds_ok) return false;
   Args a;
   a.q = static_cast<const uint16_t*>(q);
   a.k = static_cast<const uint16_t*>(k);
@@ -335,17 +449,19 @@ void launch(const strata_na3d_desc& d, const void* q, const void* k, const void*
   a.cs = reinterpret_cast<const float4*>(cs);
   a.out = static_cast<uint16_t*>(out);
   a.lse = lse;
-  a.B = d.B;
   a.heads = d.heads;
   a.Z = d.Z;
   a.H = d.H;
   a.W = d.W;
-  a.n_zb = (d.Z + ZB - 1) / ZB;
+  a.n_zb = (d.Z + ZQ - 1) / ZQ;
   a.n_yb = (d.H + kBY - 1) / kBY;
   a.n_xb = (d.W + kBX - 1) / kBX;
   a.qscale = d.scale * kLog2e;
   int64_t blocks = (int64_t)d.B * d.heads * a.n_zb * a.n_yb * a.n_xb;
-  hipLaunchKernelGGL((na3d_fwd_mfma_kernel<KZ, KY, KX, ZB>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
+  if (blocks >= (int64_t)1 << 31) return false;
+  hipLaunchKernelGGL((na3d_fwd_mfma_kernel<KZ, KY, KX, ZQ>), dim3((unsigned)blocks), dim3(kThreads),
+                     C::LDS_BYTES, s, a);
+  return true;
 }
 
 }  // namespace
@@ -353,16 +469,10 @@ void launch(const strata_na3d_desc& d, const void* q, const void* k, const void*
 bool launch_na3d_fwd_mfma(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
                           const float* cs, void* out, float* lse, hipStream_t s) {
   if (d.dtype != STRATA_BF16 || d.head_dim != kD) return false;
-  int64_t blocks = (int64_t)d.B * d.heads * ((d.Z + 3) / 4) * ((d.H + kBY - 1) / kBY) * ((d.W + kBX - 1) / kBX);
-  if (blocks >= (int64_t)1 << 31) return false;
-  if (d.kz == 3 && d.ky == 7 && d.kx == 7) {
-    launch<3, 7, 7, 4>(d, q, k, v, cs, out, lse, s);
-    return true;
-  }
-  if (d.kz == 5 && d.ky == 9 && d.kx == 9) {
-    launch<5, 9, 9, 4>(d, q, k, v, cs, out, lse, s);
-    return true;
-  }
+  // element offsets inside one key level are int32
+  if ((int64_t)d.H * d.W * kD >= (int64_t)1 << 31) return false;
+  if (d.kz == 3 && d.ky == 7 && d.kx == 7) return launch<3, 7, 7, 8>(d, q, k, v, cs, out, lse, s);
+  if (d.kz == 5 && d.ky == 9 && d.kx == 9) return launch<5, 9, 9, 2>(d, q, k, v, cs, out, lse, s);
   return false;
 }
 
