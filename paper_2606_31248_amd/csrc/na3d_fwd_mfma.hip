@@ -9,8 +9,9 @@
 //   key sweep : the workgroup walks the key levels its queries need, each once.
 //               K and V of the (8+ky-1) x (8+kx-1) key box of a level are copied
 //               global -> LDS by the direct-to-LDS load (no registers), one level
-//               ahead of the compute, into a double buffer; K is then rotated in
-//               place (StereoRoPE) and rounded to float16.
+//               ahead of the compute, into a double buffer; each thread then
+//               rotates the K pieces its own copies brought (StereoRoPE) and
+//               rounds them to float16, and one barrier publishes the level.
 //
 // Per (query level, key level) a wave multiplies the keys of its 4x4 sub-block's
 // box -- (3+ky) x (3+kx) keys, in 16-key chunks -- with its 16 queries:
@@ -19,7 +20,7 @@
 //                                           mask (0 or -inf),
 //   online softmax on S^T in registers (a lane owns one query column); the
 //   running maximum only moves when it grows by more than 2^8, so most steps
-//   rescale nothing,
+//   rescale nothing; cross-row maxima use v_permlane16/32_swap,
 //   O^T (64 d x 16 queries) += V^T . P^T    bf16 MFMA; V^T fragments come from
 //                                           the row-major V tile through the LDS
 //                                           transpose read, P^T is the S^T
@@ -32,8 +33,13 @@
 // values beyond the float16 range (|x| > 65504) saturate.  P and V stay bf16.
 // The logit scale and log2(e) are folded into Q so the softmax uses exp2.
 //
-// LDS rows are padded (K: 144 bytes, V: 160 bytes per key) so the 16-byte K reads
-// and the 8-byte transpose reads of V hit distinct banks and take immediate offsets.
+// K rows are 128 bytes with their 16-byte columns XOR-swizzled by
+// ((x >> 1) + 5 y) & 7 of the key's box position: the 16 keys of any chunk of an
+// interior sub-block then sit in 16 distinct bank groups.  V rows are padded to
+// 160 bytes, which spreads the 8-byte transpose reads and lets them take
+// immediate offsets.  The two halves of the double buffer are distinct LDS objects, so the
+// compiler can tell the reads of one from the copies into the other and does not
+// wait for the copies before reading.
 #include "common.h"
 #include "kernels.h"
 
@@ -54,7 +60,7 @@ constexpr int kBY = 8, kBX = 8;  // query block of a workgroup (y, x)
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kD = 64;           // head_dim
-constexpr int kKRow = 144;       // LDS bytes per key row of K (128 + 16 pad)
+constexpr int kKRow = 128;       // LDS bytes per key row of K (16-byte columns swizzled)
 constexpr int kVRow = 160;       // LDS bytes per key row of V (128 + 32 pad)
 constexpr int kLdsMax = 160 * 1024;
 constexpr float kLog2e = 1.4426950408889634f;
@@ -69,16 +75,19 @@ struct Cfg {
   static constexpr int NC = (NU + 15) / 16;                   // 16-key chunks
   static constexpr int NS = (NC + 1) / 2;                     // 32-key PV steps
   static constexpr int KEYS = LY * LX;
-  static constexpr int KSLOTS = KEYS * (kKRow / 16);          // 16-byte slots of a K tile
+  static constexpr int KSLOTS = KEYS * (kKRow / 16);          // 16-byte slots of a K tile (8 per key)
   static constexpr int VSLOTS = KEYS * (kVRow / 16);
   static constexpr int KBYTES = KEYS * kKRow, VBYTES = KEYS * kVRow;
-  static constexpr int BUF = KBYTES + VBYTES;                 // one level: K then V
+  static constexpr int BUF = KBYTES + VBYTES;                 // one level: K and V
   static constexpr int ITK = (KSLOTS + kThreads - 1) / kThreads;
   static constexpr int ITV = (VSLOTS + kThreads - 1) / kThreads;
-  // per-thread copy offsets live in LDS when they fit, else in registers
+  // per-thread copy offsets live in LDS when they fit, else in registers; the
+  // rotary phases of the key box (float16 pairs, one 16-byte slot per K slot)
+  // too, else they are read from memory for every key level
   static constexpr int GOFF_BYTES = (ITK + ITV) * kThreads * 4;
   static constexpr bool GOFF_LDS = 2 * BUF + GOFF_BYTES <= kLdsMax;
-  static constexpr int LDS_BYTES = 2 * BUF + (GOFF_LDS ? GOFF_BYTES : 0);
+  static constexpr int PH_BYTES = KSLOTS * 16;
+  static constexpr bool PH_LDS = GOFF_LDS && 2 * BUF + GOFF_BYTES + PH_BYTES <= kLdsMax;
   static constexpr int QL = ZQ / 2;                           // query levels per wave
   static_assert(ZQ % 2 == 0, "ZQ must be even");
   static_assert(2 * BUF <= kLdsMax, "key tiles exceed LDS");
@@ -136,31 +145,40 @@ __device__ __forceinline__ uint4 scale8h(uint4 x, float mul) {
   return make_uint4(r[0], r[1], r[2], r[3]);
 }
 
-__device__ __forceinline__ i16x4 tr_read(uint32_t byte_addr) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(uintptr_t)byte_addr);
+__device__ __forceinline__ i16x4 tr_read(const char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p);
 }
 
-__device__ __forceinline__ uint4 lds_read16(uint32_t byte_addr) {
-  u32x4 v = *(__attribute__((address_space(3))) u32x4*)(uintptr_t)byte_addr;
+__device__ __forceinline__ uint4 ld16(const char* p) {
+  const u32x4 v = *reinterpret_cast<const u32x4*>(p);
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
-__device__ __forceinline__ void lds_write16(uint32_t byte_addr, uint4 v) {
-  *(__attribute__((address_space(3))) u32x4*)(uintptr_t)byte_addr = u32x4{v.x, v.y, v.z, v.w};
-}
-
-__device__ __forceinline__ int lds_read_i32(uint32_t byte_addr) {
-  return *(__attribute__((address_space(3))) int*)(uintptr_t)byte_addr;
-}
-
-__device__ __forceinline__ void lds_write_i32(uint32_t byte_addr, int v) {
-  *(__attribute__((address_space(3))) int*)(uintptr_t)byte_addr = v;
+__device__ __forceinline__ void st16(char* p, uint4 v) {
+  *reinterpret_cast<u32x4*>(p) = u32x4{v.x, v.y, v.z, v.w};
 }
 
 // Direct global -> LDS copy of 16 bytes per lane: lane i of the wave writes
 // wave_dst + 16 i (wave_dst must be the same for the whole wave).
-__device__ __forceinline__ void copy16_to_lds(const uint16_t* src, uint32_t wave_dst) {
-  __builtin_amdgcn_global_load_lds(src, (lds_void*)(uintptr_t)wave_dst, 16, 0, 0);
+__device__ __forceinline__ void copy16_to_lds(const uint16_t* src, char* wave_dst) {
+  __builtin_amdgcn_global_load_lds(src, (lds_void*)wave_dst, 16, 0, 0);
+}
+
+// Cross-row exchanges without LDS (gfx950 v_permlane16/32_swap): with both
+// operands equal, the two results of a swap are, in some order, the lane's own
+// value and the value of lane l^16 (resp. l^32).
+__device__ __forceinline__ float max_over_rows(float x) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float sum_over_rows(float x) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 __device__ __forceinline__ float psum8(uint32_t a, uint32_t b, float acc) {
@@ -172,8 +190,13 @@ __device__ __forceinline__ float psum8(uint32_t a, uint32_t b, float acc) {
 template <int KZ, int KY, int KX, int ZQ>
 __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_mfma_kernel(Args a) {
   using C = Cfg<KZ, KY, KX, ZQ>;
-  extern __shared__ __attribute__((aligned(16))) char lds_raw[];
-  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_raw;
+  // double buffer of key tiles (distinct objects, see above), copy offsets, phases
+  __shared__ __attribute__((aligned(16))) char tK0[C::KBYTES];
+  __shared__ __attribute__((aligned(16))) char tV0[C::VBYTES];
+  __shared__ __attribute__((aligned(16))) char tK1[C::KBYTES];
+  __shared__ __attribute__((aligned(16))) char tV1[C::VBYTES];
+  __shared__ __attribute__((aligned(16))) int sgoff[C::GOFF_LDS ? C::GOFF_BYTES / 4 : 1];
+  __shared__ __attribute__((aligned(16))) char sph[C::PH_LDS ? C::PH_BYTES : 16];
 
   // ---- block coordinates (XCD-aware: neighbouring blocks share an L2) -------
   const int nblk = gridDim.x;
@@ -203,22 +226,25 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_mfma_kernel(Args a) {
   const int qy = min(qy_raw, H - 1), qx = min(qx_raw, W - 1);
   const int wys = win_start(qy, H, KY), wxs = win_start(qx, W, KX);
 
-  // ---- per-lane LDS offsets and window mask, identical for every key level ----
+  // column swizzle of the K tile (see the header comment)
+  auto kswz = [&](int key) { return ((key % C::LX >> 1) + 5 * (key / C::LX)) & 7; };
+
+  // ---- per-lane tile offsets and window mask, identical for every key level ----
   uint32_t kaddr[C::NC], vaddr[C::NC];
   f32x4 bias[C::NC];
 #pragma unroll
   for (int c = 0; c < C::NC; ++c) {
-    {  // K fragment (A operand): row = key 16c + qn, 16 bytes at column g (+64 bytes: g+4)
+    {  // K fragment (A operand): row = key 16c + qn, 16 bytes at column g (xor 64 bytes: g+4)
       int u = 16 * c + qn;
       int key = 0;
       if (u < C::NU) key = (uy0 - ty0 + u / C::NUX) * C::LX + (ux0 - tx0 + u % C::NUX);
-      kaddr[c] = key * kKRow + g * 16;
+      kaddr[c] = key * kKRow + ((g ^ kswz(key)) << 4);
     }
     {  // V^T fragment by transpose read: source row = key 16c + 4g + qn/4, element 4*(qn%4)
       int u = 16 * c + 4 * g + (qn >> 2);
       int key = 0;
       if (u < C::NU) key = (uy0 - ty0 + u / C::NUX) * C::LX + (ux0 - tx0 + u % C::NUX);
-      vaddr[c] = C::KBYTES + key * kVRow + (qn & 3) * 8;
+      vaddr[c] = key * kVRow + (qn & 3) * 8;
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -230,24 +256,24 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_mfma_kernel(Args a) {
   }
 
   // ---- direct-to-LDS copy map: slot s = it*512 + tid of a tile ---------------
-  // K: 9 slots per key (8 data + pad), V: 10 slots per key (8 data + 2 pad).
+  // K: 8 slots per key, slot column c holds data column c ^ swizzle(key);
+  // V: 10 slots per key (8 data + 2 pad).
   // goff: element offset inside a key level, or -1 for pad / past-the-end slots.
-  // Each thread only ever reads back its own offsets: no barrier needed.
+  // Each thread only reads back its own offsets: no barrier needed.
   const int64_t HW = (int64_t)H * W;
-  const uint32_t goff_lds = lds0 + 2 * C::BUF + tid * 4;
   int goffK_r[C::GOFF_LDS ? 1 : C::ITK], goffV_r[C::GOFF_LDS ? 1 : C::ITV];
   auto goffK = [&](int it) {
-    return C::GOFF_LDS ? lds_read_i32(goff_lds + it * kThreads * 4) : goffK_r[C::GOFF_LDS ? 0 : it];
+    return C::GOFF_LDS ? sgoff[it * kThreads + tid] : goffK_r[C::GOFF_LDS ? 0 : it];
   };
   auto goffV = [&](int it) {
-    return C::GOFF_LDS ? lds_read_i32(goff_lds + (C::ITK + it) * kThreads * 4) : goffV_r[C::GOFF_LDS ? 0 : it];
+    return C::GOFF_LDS ? sgoff[(C::ITK + it) * kThreads + tid] : goffV_r[C::GOFF_LDS ? 0 : it];
   };
 #pragma unroll
   for (int it = 0; it < C::ITK; ++it) {
-    int s = it * kThreads + tid, key = s / 9, c = s - key * 9;
+    int s = it * kThreads + tid, key = s >> 3, c = (s & 7) ^ kswz(key);
     int gy = min(ty0 + key / C::LX, H - 1), gx = min(tx0 + key % C::LX, W - 1);
-    int off = (s < C::KSLOTS && c < 8) ? (gy * W + gx) * kD + c * 8 : -1;
-    if (C::GOFF_LDS) lds_write_i32(goff_lds + it * kThreads * 4, off);
+    int off = s < C::KSLOTS ? (gy * W + gx) * kD + c * 8 : -1;
+    if (C::GOFF_LDS) sgoff[it * kThreads + tid] = off;
     else goffK_r[C::GOFF_LDS ? 0 : it] = off;
   }
 #pragma unroll
@@ -255,42 +281,66 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_mfma_kernel(Args a) {
     int s = it * kThreads + tid, key = s / 10, c = s - key * 10;
     int gy = min(ty0 + key / C::LX, H - 1), gx = min(tx0 + key % C::LX, W - 1);
     int off = (s < C::VSLOTS && c < 8) ? (gy * W + gx) * kD + c * 8 : -1;
-    if (C::GOFF_LDS) lds_write_i32(goff_lds + (C::ITK + it) * kThreads * 4, off);
+    if (C::GOFF_LDS) sgoff[(C::ITK + it) * kThreads + tid] = off;
     else goffV_r[C::GOFF_LDS ? 0 : it] = off;
   }
   const float4* csb = a.cs ? a.cs + (int64_t)b * HW * 16 : nullptr;
   const int64_t bh_base = (int64_t)bh * Z * HW;  // token index of (b, h, 0, 0, 0)
 
-  auto issue_copy = [&](int p, uint32_t buf) {
+  auto issue_copy = [&](int p, char* tk, char* tv) {
     const uint16_t* kp = a.k + (bh_base + (int64_t)p * HW) * kD;
     const uint16_t* vp = a.v + (bh_base + (int64_t)p * HW) * kD;
-    const uint32_t kdst = lds0 + buf + wave * 64 * 16, vdst = kdst + C::KBYTES;
 #pragma unroll
     for (int it = 0; it < C::ITK; ++it) {
       const int o = goffK(it);
-      if (o >= 0) copy16_to_lds(kp + o, kdst + it * kThreads * 16);
+      if (o >= 0) copy16_to_lds(kp + o, tk + (it * kThreads + wave * 64) * 16);
     }
 #pragma unroll
     for (int it = 0; it < C::ITV; ++it) {
       const int o = goffV(it);
-      if (o >= 0) copy16_to_lds(vp + o, vdst + it * kThreads * 16);
+      if (o >= 0) copy16_to_lds(vp + o, tv + (it * kThreads + wave * 64) * 16);
     }
   };
-  // rotate (or convert) this thread's K slots of one buffer in place, bf16 -> float16
-  auto rotate_k = [&](uint32_t buf) {
+
+  // phases of this thread's K slots, as float16 (cos, sin) pairs, staged once
+  if (C::PH_LDS && csb) {
 #pragma unroll
     for (int it = 0; it < C::ITK; ++it) {
       const int o = goffK(it);
       if (o < 0) continue;
-      const uint32_t ad = lds0 + buf + (it * kThreads + tid) * 16;
-      uint4 x = lds_read16(ad);
+      const float4* pp = csb + (o >> 6) * 16 + ((o & 63) >> 2);
+      const float4 p0 = pp[0], p1 = pp[1];
+      st16(sph + (it * kThreads + tid) * 16,
+           make_uint4(pack2h(p0.x, p0.y), pack2h(p0.z, p0.w), pack2h(p1.x, p1.y), pack2h(p1.z, p1.w)));
+    }
+  }
+  // Rotate (or convert) this thread's K slots of one tile in place, bf16 -> float16.
+  // A thread's copies land in its own slots, so its own wait suffices: no barrier.
+  auto rotate_k = [&](char* tk) {
+#pragma unroll
+    for (int it = 0; it < C::ITK; ++it) {
+      const int o = goffK(it);
+      if (o < 0) continue;
+      char* ad = tk + (it * kThreads + tid) * 16;
+      uint4 x = ld16(ad);
       if (csb) {
-        const float4* pp = csb + (o >> 6) * 16 + ((o & 63) >> 2);
-        x = rotate8h(x, pp[0], pp[1], 1.f);
+        float4 p0, p1;
+        if (C::PH_LDS) {
+          const uint4 ph = ld16(sph + (it * kThreads + tid) * 16);
+          const f16x2 c0 = __builtin_bit_cast(f16x2, ph.x), c1 = __builtin_bit_cast(f16x2, ph.y);
+          const f16x2 c2 = __builtin_bit_cast(f16x2, ph.z), c3 = __builtin_bit_cast(f16x2, ph.w);
+          p0 = make_float4((float)c0.x, (float)c0.y, (float)c1.x, (float)c1.y);
+          p1 = make_float4((float)c2.x, (float)c2.y, (float)c3.x, (float)c3.y);
+        } else {
+          const float4* pp = csb + (o >> 6) * 16 + ((o & 63) >> 2);
+          p0 = pp[0];
+          p1 = pp[1];
+        }
+        x = rotate8h(x, p0, p1, 1.f);
       } else {
         x = scale8h(x, 1.f);
       }
-      lds_write16(ad, x);
+      st16(ad, x);
     }
   };
 
@@ -320,13 +370,13 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_mfma_kernel(Args a) {
     for (int t = 0; t < 4; ++t) o[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  // one (query level j, key level) update with the key tile at buffer `buf`
-  auto update = [&](int j, uint32_t buf) {
+  // one (query level j, key level) update with the key tiles tk, tv
+  auto update = [&](int j, const char* tk, const char* tv) {
     f32x4 s[C::NC];
 #pragma unroll
     for (int c = 0; c < C::NC; ++c) {
-      f16x8 k0 = __builtin_bit_cast(f16x8, lds_read16(lds0 + buf + kaddr[c]));
-      f16x8 k1 = __builtin_bit_cast(f16x8, lds_read16(lds0 + buf + kaddr[c] + 64));
+      f16x8 k0 = __builtin_bit_cast(f16x8, ld16(tk + kaddr[c]));
+      f16x8 k1 = __builtin_bit_cast(f16x8, ld16(tk + (kaddr[c] ^ 64u)));
       f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(k0, qf[j][0], bias[c], 0, 0, 0);
       s[c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(k1, qf[j][1], acc, 0, 0, 0);
     }
@@ -334,8 +384,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_mfma_kernel(Args a) {
 #pragma unroll
     for (int c = 1; c < C::NC; ++c)
       mx = fmaxf(fmaxf(mx, fmaxf(s[c][0], s[c][1])), fmaxf(s[c][2], s[c][3]));
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    mx = max_over_rows(mx);
     if (__any(mx > m[j] + kLazy)) {  // rare: move the running maximum, rescale
       const float mn = fmaxf(m[j], mx);
       const float alpha = __builtin_amdgcn_exp2f(m[j] - mn);
@@ -361,8 +410,8 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_mfma_kernel(Args a) {
       bf16x8 pf = __builtin_bit_cast(bf16x8, make_uint4(pk[c0][0], pk[c0][1], two ? pk[c1][0] : 0u, two ? pk[c1][1] : 0u));
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        i16x4 lo = tr_read(lds0 + buf + vaddr[c0] + 32 * t);
-        i16x4 hi = two ? tr_read(lds0 + buf + vaddr[c1] + 32 * t) : i16x4{0, 0, 0, 0};
+        i16x4 lo = tr_read(tv + vaddr[c0] + 32 * t);
+        i16x4 hi = two ? tr_read(tv + vaddr[c1] + 32 * t) : i16x4{0, 0, 0, 0};
         uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
         bf16x8 vf = __builtin_bit_cast(bf16x8, make_uint4(l2.x, l2.y, h2.x, h2.y));
         o[j][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[j][t], 0, 0, 0);
@@ -371,44 +420,44 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_mfma_kernel(Args a) {
   };
 
   // all query levels of this wave whose window holds key level p
-  auto compute = [&](int p, uint32_t buf) {
+  auto compute = [&](int p, const char* tk, const char* tv) {
 #pragma unroll
     for (int j = 0; j < C::QL; ++j) {
       const int zq = z0 + grp + 2 * j;
       if (zq >= Z) continue;
       const int zs = win_start(zq, Z, KZ);
       if (p < zs || p >= zs + KZ) continue;
-      update(j, buf);
+      update(j, tk, tv);
     }
   };
 
   // ---- key levels needed by the block's query levels, double-buffered -------
+  // Level p+1 is copied while level p is computed; then each thread waits for
+  // its own copies, rotates its own K slots, and one barrier publishes the level.
+  // The barrier also retires every read of the tiles the next copy overwrites.
   const int zlast = min(z0 + ZQ, Z) - 1;
   const int kp_lo = win_start(z0, Z, KZ);
   const int kp_hi = win_start(zlast, Z, KZ) + KZ;
 
-  issue_copy(kp_lo, 0);
+  issue_copy(kp_lo, tK0, tV0);
   __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  rotate_k(0);
+  rotate_k(tK0);
   __syncthreads();
   for (int p = kp_lo; p < kp_hi; p += 2) {
-    // level p in buffer 0, level p+1 (if any) in buffer 1
+    // level p in tiles 0, level p+1 (if any) in tiles 1
     const bool more1 = p + 1 < kp_hi;
-    if (more1) issue_copy(p + 1, C::BUF);
-    compute(p, 0);
+    if (more1) issue_copy(p + 1, tK1, tV1);
+    compute(p, tK0, tV0);
     if (more1) {
       __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();
-      rotate_k(C::BUF);
+      rotate_k(tK1);
       __syncthreads();
       const bool more2 = p + 2 < kp_hi;
-      if (more2) issue_copy(p + 2, 0);
-      compute(p + 1, C::BUF);
+      if (more2) issue_copy(p + 2, tK0, tV0);
+      compute(p + 1, tK1, tV1);
       if (more2) {
         __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-        rotate_k(0);
+        rotate_k(tK0);
         __syncthreads();
       }
     }
@@ -419,9 +468,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_mfma_kernel(Args a) {
 #pragma unroll
   for (int j = 0; j < C::QL; ++j) {
     const int zq = z0 + grp + 2 * j;
-    float lt = l[j];
-    lt += __shfl_xor(lt, 16);
-    lt += __shfl_xor(lt, 32);
+    const float lt = sum_over_rows(l[j]);
     if (zq >= Z || !in_grid) continue;
     const float inv = 1.f / lt;
     const int64_t tok = bh_base + zq * HW + (int64_t)qy * W + qx;
@@ -437,11 +484,6 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_mfma_kernel(Args a) {
 template <int KZ, int KY, int KX, int ZQ>
 bool launch(const strata_na3d_desc& d, const void* q, const void* k, const void* v, const float* cs,
             void* out, float* lse, hipStream_t s) {
-  using C = Cfg<KZ, KY, KX, ZQ>;
-  static const bool lds_ok = hipFuncSetAttribute((const void*)na3d_fwd_mfma_kernel<KZ, KY, KX, ZQ>,
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                 C::LDS_BYTES) == hipSuccess;
-  if (!lds_ok) return false;
   Args a;
   a.q = static_cast<const uint16_t*>(q);
   a.k = static_cast<const uint16_t*>(k);
@@ -459,8 +501,7 @@ bool launch(const strata_na3d_desc& d, const void* q, const void* k, const void*
   a.qscale = d.scale * kLog2e;
   int64_t blocks = (int64_t)d.B * d.heads * a.n_zb * a.n_yb * a.n_xb;
   if (blocks >= (int64_t)1 << 31) return false;
-  hipLaunchKernelGGL((na3d_fwd_mfma_kernel<KZ, KY, KX, ZQ>), dim3((unsigned)blocks), dim3(kThreads),
-                     C::LDS_BYTES, s, a);
+  hipLaunchKernelGGL((na3d_fwd_mfma_kernel<KZ, KY, KX, ZQ>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
   return true;
 }
 
