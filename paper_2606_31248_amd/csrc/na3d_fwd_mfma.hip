@@ -136,6 +136,26 @@ __device__ __forceinline__ uint4 rotate8h(uint4 x, float4 p01, float4 p23, float
   return make_uint4(r[0], r[1], r[2], r[3]);
 }
 
+// Rotate 4 pairs held as packed bf16x2 words by float16 phases (c, s) in
+// packed float16 arithmetic (one multiply and one fused multiply-add per pair);
+// returns packed float16x2 words.  Inputs are clamped to +-46000 so that no
+// rotated value leaves the float16 range.
+__device__ __forceinline__ uint4 rotate8h_pk(uint4 x, uint4 ph) {
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  const uint32_t p[4] = {ph.x, ph.y, ph.z, ph.w};
+  uint32_t r[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const float a = __builtin_amdgcn_fmed3f(lo_bf16(w[t]), -46000.f, 46000.f);
+    const float b = __builtin_amdgcn_fmed3f(hi_bf16(w[t]), -46000.f, 46000.f);
+    const f16x2 ab = __builtin_convertvector((f32x2{a, b}), f16x2);
+    const f16x2 cs = __builtin_bit_cast(f16x2, p[t]);
+    const f16x2 aa = {ab.x, ab.x}, bb = {ab.y, ab.y}, ns = {-cs.y, cs.x};
+    r[t] = __builtin_bit_cast(uint32_t, aa * cs + bb * ns);  // (a c - b s, a s + b c)
+  }
+  return make_uint4(r[0], r[1], r[2], r[3]);
+}
+
 // bf16 x 8 -> float16 x 8, times `mul` (no rotation).
 __device__ __forceinline__ uint4 scale8h(uint4 x, float mul) {
   uint32_t w[4] = {x.x, x.y, x.z, x.w};
@@ -324,19 +344,12 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_mfma_kernel(Args a) {
       char* ad = tk + (it * kThreads + tid) * 16;
       uint4 x = ld16(ad);
       if (csb) {
-        float4 p0, p1;
         if (C::PH_LDS) {
-          const uint4 ph = ld16(sph + (it * kThreads + tid) * 16);
-          const f16x2 c0 = __builtin_bit_cast(f16x2, ph.x), c1 = __builtin_bit_cast(f16x2, ph.y);
-          const f16x2 c2 = __builtin_bit_cast(f16x2, ph.z), c3 = __builtin_bit_cast(f16x2, ph.w);
-          p0 = make_float4((float)c0.x, (float)c0.y, (float)c1.x, (float)c1.y);
-          p1 = make_float4((float)c2.x, (float)c2.y, (float)c3.x, (float)c3.y);
+          x = rotate8h_pk(x, ld16(sph + (it * kThreads + tid) * 16));
         } else {
           const float4* pp = csb + (o >> 6) * 16 + ((o & 63) >> 2);
-          p0 = pp[0];
-          p1 = pp[1];
+          x = rotate8h(x, pp[0], pp[1], 1.f);
         }
-        x = rotate8h(x, p0, p1, 1.f);
       } else {
         x = scale8h(x, 1.f);
       }
