@@ -266,3 +266,55 @@ def test_blend_full_face_rollout_planes():
     planes = [0, 63, P - 1]
     ref = oracle.tile_blend(np.ascontiguousarray(tiles[:, planes]), 9, 9, 56, 56, win, 512, 512, "bf16")
     assert np.array_equal(host_bits(out[planes]), ref)
+
+
+# ----------------------------------------------------------------------------- NA3D backward
+
+def run_bwd(shape, window, dtype, seed, coords32=None):
+    """GPU forward (for out and lse) then backward; returns host inputs and GPU grads."""
+    (q, k, v), out, lse, scale = run_fwd(shape, window, dtype, seed, coords32)
+    g = I.gaussian(shape, seed, I.STREAM_DO, dtype)
+    qd, kd, vd, gd = (dev_tensor(a, dtype) for a in (q, k, v, g))
+    cs = gpu_phases(coords32, shape[-1]) if coords32 is not None else None
+    desc = B.desc_for(qd, window, scale)
+    ws = torch.empty(B.strata_na3d_bwd_workspace_size(desc), dtype=torch.uint8, device="cuda")
+    dq, dk, dv = (torch.empty_like(qd) for _ in range(3))
+    B.strata_na3d_bwd(desc, qd, kd, vd, cs, out, gd, lse, dq, dk, dv, ws)
+    torch.cuda.synchronize()
+    return (q, k, v, g), (dq, dk, dv), scale
+
+
+@pytest.mark.parametrize("shape,window,dtype", [
+    ((1, 2, 5, 11, 13, 64), (3, 7, 7), "bf16"),
+    ((2, 1, 6, 12, 10, 64), (5, 9, 9), "bf16"),
+    ((1, 2, 4, 9, 11, 32), (3, 5, 7), "f32"),
+    ((1, 1, 3, 8, 8, 32), (1, 3, 5), "bf16"),
+])
+@pytest.mark.parametrize("rope", [True, False])
+def test_bwd_full_oracle(shape, window, dtype, rope):
+    pl = I.random_placement(shape[0], shape[3], shape[4], 92)
+    c32 = oracle_coords(pl, shape[3], shape[4]) if rope else None
+    (q, k, v, g), grads, scale = run_bwd(shape, window, dtype, 41, c32)
+    refs = oracle.na3d_bwd(*(oracle.widen(a, dtype) for a in (q, k, v, g)), window, scale, coords=c32)
+    # f32 inputs: the forward output feeding D is float32, so the f32 bound applies
+    for name, got, ref in zip(("dq", "dk", "dv"), grads, refs):
+        check_close(host_f64(got), ref, dtype, name)
+
+
+def test_bwd_full_size_sampled():
+    """The 16-tile 5x9x9 backward at full size; sampled rows of dq, dk, dv vs oracle."""
+    wl = I.TRAIN_TILE_BWD
+    shape = wl.shape()
+    window = (wl.kz, wl.ky, wl.kx)
+    pl = wl.placement()
+    c32 = oracle_coords(pl, wl.H, wl.W)
+    (q, k, v, g), (dq, dk, dv), scale = run_bwd(shape, window, "bf16", wl.seed, c32)
+    tiles = [0, shape[0] - 1]
+    per_tile = shape[1] * wl.N
+    sel = sample_queries(shape, 160, wl.seed, tiles)
+    local = np.searchsorted(tiles, sel // per_tile) * per_tile + sel % per_tile
+    sub = lambda a: oracle.widen(a[tiles], "bf16")
+    rq, rk, rv = oracle.na3d_bwd(sub(q), sub(k), sub(v), sub(g), window, scale, coords=c32[tiles],
+                                 selq=local, selk=local)
+    for name, got, ref in (("dq", dq, rq), ("dk", dk, rk), ("dv", dv, rv)):
+        check_close(host_f64(got).reshape(-1, wl.d)[sel], ref, "bf16", name)
