@@ -33,7 +33,8 @@ METRIC = "NA3D fwd TFLOP/s + tokens/s at 1 MI355X; % of bf16 MFMA peak"
 PEAK_BF16_TFLOPS = 2500.0        # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0            # MI355X HBM3E
 PMC_FILE = os.path.join(ROOT, "profiles", "na3d_fwd_face_rollout_pmc.json")
-KERNEL_SOURCES = ["paper_2606_31248_amd/csrc/na3d_fwd_mfma.hip", "paper_2606_31248_amd/csrc/na3d_ref.hip"]
+KERNEL_SOURCES = ["paper_2606_31248_amd/csrc/na3d_mfma_q.hip", "paper_2606_31248_amd/csrc/mfma_util.h",
+                  "paper_2606_31248_amd/csrc/na3d_ref.hip"]
 
 
 def kernel_source_hash() -> str:

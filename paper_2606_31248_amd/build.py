@@ -17,7 +17,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libstrata.so")
 
-SOURCES = ["api.hip", "geometry.hip", "rope.hip", "blend.hip", "na3d_ref.hip", "na3d_fwd_mfma.hip"]
+SOURCES = ["api.hip", "geometry.hip", "rope.hip", "blend.hip", "na3d_ref.hip", "na3d_mfma_q.hip",
+           "na3d_mfma_kv.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
@@ -32,7 +33,7 @@ FLAGS = [
 
 # Per-file extra flags.  The attention kernel never sees NaN inputs by contract
 # (masked logits are -inf, not NaN), so max() needs no NaN canonicalisation.
-EXTRA = {"na3d_fwd_mfma.hip": ["-fno-honor-nans"]}
+EXTRA = {"na3d_mfma_q.hip": ["-fno-honor-nans"], "na3d_mfma_kv.hip": ["-fno-honor-nans"]}
 
 
 def _compile(src: str) -> str:

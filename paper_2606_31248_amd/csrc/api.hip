@@ -181,8 +181,13 @@ strata_status strata_na3d_bwd(const strata_na3d_desc* desc, const void* q, const
     return set_error(STRATA_ERR_WORKSPACE, "workspace: need %zu bytes, got %zu", need,
                      workspace ? workspace_bytes : (size_t)0);
   REQUIRE(aligned16(workspace), "workspace: not 16-byte aligned");
-  launch_na3d_bwd_ref(*desc, q, k, v, cs, out, dout, lse, dq, dk, dv, static_cast<float*>(workspace),
-                      (hipStream_t)stream);
+  hipStream_t s = (hipStream_t)stream;
+  float* dvec = static_cast<float*>(workspace);
+  launch_na3d_bwd_ref(0, *desc, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+  if (!launch_na3d_bwd_dq_mfma(*desc, q, k, v, cs, dout, lse, dvec, dq, s))
+    launch_na3d_bwd_ref(1, *desc, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+  if (!launch_na3d_bwd_dkdv_mfma(*desc, q, k, v, cs, dout, lse, dvec, dk, dv, s))
+    launch_na3d_bwd_ref(2, *desc, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
   return check_launch("strata_na3d_bwd");
 }
 

@@ -29,10 +29,20 @@ void launch_na3d_fwd_ref(const strata_na3d_desc& d, const void* q, const void* k
 bool launch_na3d_fwd_mfma(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
                           const float* cs, void* out, float* lse, hipStream_t s);
 
-// Plain backward (float32 arithmetic): preprocess, dq, dk/dv.
-void launch_na3d_bwd_ref(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
-                         const float* cs, const void* out, const void* dout, const float* lse,
-                         void* dq, void* dk, void* dv, float* dvec, hipStream_t s);
+// Plain backward (float32 arithmetic), one part per call: 0 = D = rowsum(dO * O)
+// into dvec, 1 = dq, 2 = dk and dv (parts 1 and 2 read dvec).
+void launch_na3d_bwd_ref(int part, const strata_na3d_desc& d, const void* q, const void* k,
+                         const void* v, const float* cs, const void* out, const void* dout,
+                         const float* lse, void* dq, void* dk, void* dv, float* dvec, hipStream_t s);
+
+// bf16 MFMA backward parts; each returns false when the problem has no MFMA variant.
+// dq: query-stationary (the forward's decomposition); dk/dv: key-stationary.
+bool launch_na3d_bwd_dq_mfma(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
+                             const float* cs, const void* dout, const float* lse,
+                             const float* dvec, void* dq, hipStream_t s);
+bool launch_na3d_bwd_dkdv_mfma(const strata_na3d_desc& d, const void* q, const void* k,
+                               const void* v, const float* cs, const void* dout, const float* lse,
+                               const float* dvec, void* dk, void* dv, hipStream_t s);
 
 void launch_tile_blend(const void* tiles, int nty, int ntx, int P, int Ht, int Wt, int C, int sy,
                        int sx, const float* window, void* out, int Hf, int Wf, strata_dtype dt,

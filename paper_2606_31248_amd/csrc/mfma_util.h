@@ -1,0 +1,130 @@
+// Device helpers shared by the MFMA neighbourhood-attention kernels (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace strata {
+namespace mfma {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+  f32x2 f = {a, b};
+  bf16x2 h = __builtin_convertvector(f, bf16x2);
+  return __builtin_bit_cast(uint32_t, h);
+}
+
+// Two floats -> packed float16 pair (nearest-even), saturating at +-65504.
+__device__ __forceinline__ uint32_t pack2h(float a, float b) {
+  f32x2 f = {__builtin_amdgcn_fmed3f(a, -65504.f, 65504.f), __builtin_amdgcn_fmed3f(b, -65504.f, 65504.f)};
+  f16x2 h = __builtin_convertvector(f, f16x2);
+  return __builtin_bit_cast(uint32_t, h);
+}
+
+// Two floats -> packed float16 pair, round to nearest even, no saturation (the
+// caller keeps the values inside the float16 range).
+__device__ __forceinline__ uint32_t pack2h_rne(float a, float b) {
+  f16x2 h = __builtin_convertvector((f32x2{a, b}), f16x2);
+  return __builtin_bit_cast(uint32_t, h);
+}
+
+__device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Rotate 4 pairs held as 4 packed bf16x2 words by phases (c0,s0,c1,s1),(c2,s2,c3,s3),
+// multiply by `mul`, and return them as 4 packed float16x2 words.
+__device__ __forceinline__ uint4 rotate8h(uint4 x, float4 p01, float4 p23, float mul) {
+  uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  float cs_[8] = {p01.x, p01.y, p01.z, p01.w, p23.x, p23.y, p23.z, p23.w};
+  uint32_t r[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    float a = lo_bf16(w[t]), b = hi_bf16(w[t]);
+    float c = cs_[2 * t], s = cs_[2 * t + 1];
+    r[t] = pack2h(fmaf(a, c, -b * s) * mul, fmaf(a, s, b * c) * mul);
+  }
+  return make_uint4(r[0], r[1], r[2], r[3]);
+}
+
+// Rotate 4 pairs held as packed bf16x2 words by float16 phases (c, s) in
+// packed float16 arithmetic (one multiply and one fused multiply-add per pair);
+// returns packed float16x2 words.  Inputs are clamped to +-46000 so that no
+// rotated value leaves the float16 range.
+__device__ __forceinline__ uint4 rotate8h_pk(uint4 x, uint4 ph) {
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  const uint32_t p[4] = {ph.x, ph.y, ph.z, ph.w};
+  uint32_t r[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const float a = __builtin_amdgcn_fmed3f(lo_bf16(w[t]), -46000.f, 46000.f);
+    const float b = __builtin_amdgcn_fmed3f(hi_bf16(w[t]), -46000.f, 46000.f);
+    const f16x2 ab = __builtin_convertvector((f32x2{a, b}), f16x2);
+    const f16x2 cs = __builtin_bit_cast(f16x2, p[t]);
+    const f16x2 aa = {ab.x, ab.x}, bb = {ab.y, ab.y}, ns = {-cs.y, cs.x};
+    r[t] = __builtin_bit_cast(uint32_t, aa * cs + bb * ns);  // (a c - b s, a s + b c)
+  }
+  return make_uint4(r[0], r[1], r[2], r[3]);
+}
+
+// bf16 x 8 -> float16 x 8, times `mul` (no rotation).
+__device__ __forceinline__ uint4 scale8h(uint4 x, float mul) {
+  uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  uint32_t r[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) r[t] = pack2h(lo_bf16(w[t]) * mul, hi_bf16(w[t]) * mul);
+  return make_uint4(r[0], r[1], r[2], r[3]);
+}
+
+__device__ __forceinline__ i16x4 tr_read(const char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p);
+}
+
+__device__ __forceinline__ uint4 ld16(const char* p) {
+  const u32x4 v = *reinterpret_cast<const u32x4*>(p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ void st16(char* p, uint4 v) {
+  *reinterpret_cast<u32x4*>(p) = u32x4{v.x, v.y, v.z, v.w};
+}
+
+// Direct global -> LDS copy of 16 bytes per lane: lane i of the wave writes
+// wave_dst + 16 i (wave_dst must be the same for the whole wave).
+__device__ __forceinline__ void copy16_to_lds(const uint16_t* src, char* wave_dst) {
+  __builtin_amdgcn_global_load_lds(src, (lds_void*)wave_dst, 16, 0, 0);
+}
+
+// Cross-row exchanges without LDS (gfx950 v_permlane16/32_swap): with both
+// operands equal, the two results of a swap are, in some order, the lane's own
+// value and the value of lane l^16 (resp. l^32).
+__device__ __forceinline__ float max_over_rows(float x) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float sum_over_rows(float x) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+__device__ __forceinline__ float psum8(uint32_t a, uint32_t b, float acc) {
+  const bf16x2 one = __builtin_bit_cast(bf16x2, 0x3F803F80u);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), one, acc, false);
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, b), one, acc, false);
+}
+
+}  // namespace mfma
+}  // namespace strata

@@ -1,0 +1,444 @@
+// MFMA neighbourhood attention for gfx950, key-stationary kernel: the dK and dV
+// part of the backward (bf16 in/out, head_dim 64).
+//
+// Work decomposition
+//   workgroup : one (tile, head), a 4 x 4 block of (y, x) key positions and 8 key
+//               levels; 8 waves, one per key level, one workgroup per CU.
+//   wave      : the 16 keys of its level, stationary in registers: K~ (rotated,
+//               times scale log2(e), float16) and V (bf16) as B operands, the
+//               dK~^T and dV^T accumulators (64 d x 16 keys).
+//   query sweep: the workgroup walks the query levels whose windows reach its key
+//               levels, each once.  The queries that can see any key of the
+//               block form a box per level -- the union of the per-axis inverse
+//               windows [lo(j), hi(j)] (at most 4 + 3 r wide, checked on the
+//               host).  Q and dO of that box are copied global -> LDS by the
+//               direct-to-LDS load, one level ahead, into a double buffer; each
+//               thread rotates the Q pieces its own copies brought (StereoRoPE,
+//               float16), stores LSE (log2 units) and -D of its queries, and one
+//               barrier publishes the level.
+//
+// Per (key level, query level) a wave walks the box in steps of 32 queries:
+//   X (16 queries x 16 keys) = Q~ . K~^T     float16 MFMA seeded with -LSE (or
+//                                            -inf outside the query's window),
+//                                            so P = exp2(X);
+//   Y (16 queries x 16 keys) = dO . V^T - D  bf16 MFMA seeded with -D;
+//   dV^T (64 d x 16 keys) += dO^T . P        bf16, P packed in place (k order of
+//                                            two 16-query chunks, matched by the
+//                                            transpose reads of the dO rows);
+//   dK~^T (64 d x 16 keys) += Q~^T . dS      float16, dS = P Y carried with a
+//                                            per-key power-of-two scale 2^(15-E),
+//                                            E bounding |Y| seen so far (|dS| <=
+//                                            P |Y|, P <= 1); the accumulator is
+//                                            rescaled exactly when E grows.
+// At the end dK = R^T (scale 2^(E-15) dK~) and dV is stored as is.
+//
+// Staged rows are 128 bytes (Q~ in float16, dO in bf16) with their 16-byte
+// columns XOR-swizzled by sigma(u) = ((u >> 1) & 3) << 1 | ((u >> 3) & 1) of the
+// box index u: the 16 rows of a chunk read at one column hit 16 distinct bank
+// groups, and so do the 8 rows of a half-wave's transpose reads.  Rows past the
+// box (up to the next multiple of 32) are zero and their mask bits clear, so
+// every read address is a lane constant plus an immediate.
+#include "common.h"
+#include "kernels.h"
+#include "mfma_util.h"
+
+#include <algorithm>
+
+namespace strata {
+namespace {
+
+using namespace mfma;
+
+constexpr int kWaves = 8;        // key levels of a workgroup, one per wave
+constexpr int kThreads = 64 * kWaves;
+constexpr int kD = 64;           // head_dim
+constexpr int kRow = 128;        // LDS bytes per staged query row
+constexpr int kLdsMax = 160 * 1024;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kMinExp = -100;    // lower bound of the dS exponent (keeps 2^(15-E) finite)
+
+template <int KZ, int KY, int KX>
+struct KvCfg {
+  static constexpr int MQY = 4 + 3 * (KY / 2), MQX = 4 + 3 * (KX / 2);  // largest query box
+  static constexpr int MQ = (MQY * MQX + 31) / 32 * 32;                  // rows, whole 32-query steps
+  static constexpr int TBYTES = MQ * kRow;
+  static constexpr int SLOTS = MQ * (kRow / 16);
+  static constexpr int IT = (SLOTS + kThreads - 1) / kThreads;           // copy slots per thread
+  static constexpr int IS = (MQ + kThreads - 1) / kThreads;              // LSE / D entries per thread
+  static_assert(4 * TBYTES + 4 * MQ * 4 + MQ * 2 <= kLdsMax, "query tiles exceed LDS");
+};
+
+struct KvArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const float4* cs;      // [B, H, W, 16] float4 = two (cos, sin) pairs; nullptr: no rotation
+  const uint16_t* dout;
+  const float* lse;      // natural log
+  const float* dvec;     // D = rowsum(dO * O)
+  uint16_t* dk;
+  uint16_t* dv;
+  int heads, Z, H, W;
+  int n_zb, n_yb, n_xb;
+  float scale, kscale;   // scale, scale * log2(e)
+};
+
+// queries whose (border-clamped) window holds position j of an axis of extent L
+__host__ __device__ __forceinline__ int inv_lo(int j, int k) { return j < k ? 0 : j - (k >> 1); }
+__host__ __device__ __forceinline__ int inv_hi(int j, int L, int k) { return j >= L - k ? L - 1 : j + (k >> 1); }
+
+__device__ __forceinline__ int rswz(int u) { return (((u >> 1) & 3) << 1) | ((u >> 3) & 1); }
+
+template <int KZ, int KY, int KX>
+__global__ void __launch_bounds__(kThreads, 1) na3d_mfma_kv_kernel(KvArgs a) {
+  using C = KvCfg<KZ, KY, KX>;
+  __shared__ __attribute__((aligned(16))) char tQ0[C::TBYTES];
+  __shared__ __attribute__((aligned(16))) char tG0[C::TBYTES];
+  __shared__ __attribute__((aligned(16))) char tQ1[C::TBYTES];
+  __shared__ __attribute__((aligned(16))) char tG1[C::TBYTES];
+  __shared__ __attribute__((aligned(16))) float sL0[C::MQ];
+  __shared__ __attribute__((aligned(16))) float sD0[C::MQ];
+  __shared__ __attribute__((aligned(16))) float sL1[C::MQ];
+  __shared__ __attribute__((aligned(16))) float sD1[C::MQ];
+  __shared__ __attribute__((aligned(16))) unsigned short smask[C::MQ];
+
+  // ---- block coordinates (XCD-aware: neighbouring blocks share an L2) -------
+  const int nblk = gridDim.x;
+  int bid = blockIdx.x;
+  if ((nblk & 7) == 0) bid = (bid & 7) * (nblk >> 3) + (bid >> 3);
+  const int xb = bid % a.n_xb;
+  const int yb = (bid / a.n_xb) % a.n_yb;
+  const int zb = (bid / (a.n_xb * a.n_yb)) % a.n_zb;
+  const int bh = bid / (a.n_xb * a.n_yb * a.n_zb);
+  const int b = bh / a.heads;
+  const int H = a.H, W = a.W, Z = a.Z;
+  const int y0 = 4 * yb, x0 = 4 * xb, z0 = kWaves * zb;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, qn = lane & 15;
+
+  // ---- the query box of the block (the same on every level) ------------------
+  const int qy0 = inv_lo(y0, KY), qy1 = inv_hi(min(y0 + 3, H - 1), H, KY);
+  const int qx0 = inv_lo(x0, KX), qx1 = inv_hi(min(x0 + 3, W - 1), W, KX);
+  const int nqx = qx1 - qx0 + 1;
+  const int nq = (qy1 - qy0 + 1) * nqx;
+  const int npairs = (nq + 31) >> 5;
+  const int64_t HW = (int64_t)H * W;
+  const int64_t bh_base = (int64_t)bh * Z * HW;  // token index of (b, h, 0, 0, 0)
+  const float4* csb = a.cs ? a.cs + (int64_t)b * HW * 16 : nullptr;
+
+  // window-mask bits per box query (bit 4 dy + dx: key (y0+dy, x0+dx) in the
+  // query's (y, x) window); LSE / D entries past the box are zero
+  for (int u = tid; u < C::MQ; u += kThreads) {
+    unsigned bits = 0;
+    if (u < nq) {
+      const int qy = qy0 + u / nqx, qx = qx0 + u % nqx;
+      const int wy = win_start(qy, H, KY), wx = win_start(qx, W, KX);
+#pragma unroll
+      for (int t = 0; t < 16; ++t) {
+        const int yy = y0 + (t >> 2), xx = x0 + (t & 3);
+        if (yy >= wy && yy < wy + KY && xx >= wx && xx < wx + KX) bits |= 1u << t;
+      }
+    } else {
+      sL0[u] = 0.f;
+      sL1[u] = 0.f;
+      sD0[u] = 0.f;
+      sD1[u] = 0.f;
+    }
+    smask[u] = (unsigned short)bits;
+  }
+  // rows past the box up to the last 32-query step: zero in all four tiles
+  for (int i = nq * 8 + tid; i < npairs * 256; i += kThreads) {
+    const uint4 z = make_uint4(0u, 0u, 0u, 0u);
+    st16(tQ0 + i * 16, z);
+    st16(tG0 + i * 16, z);
+    st16(tQ1 + i * 16, z);
+    st16(tG1 + i * 16, z);
+  }
+
+  // ---- direct-to-LDS copy map (registers): slot s = it*512 + tid ---------------
+  // row u = s / 8 holds box query u; slot column s % 8 holds data column
+  // (s % 8) ^ sigma(u).  Q and dO share the map; goff = -1 past the box.
+  int goff[C::IT];
+  uint4 ph[C::IT];
+#pragma unroll
+  for (int it = 0; it < C::IT; ++it) {
+    const int s = it * kThreads + tid, u = s >> 3, dc = (s & 7) ^ rswz(u);
+    goff[it] = -1;
+    ph[it] = make_uint4(0u, 0u, 0u, 0u);
+    if (s < C::SLOTS && u < nq) {
+      const int qy = qy0 + u / nqx, qx = qx0 + u % nqx;
+      goff[it] = (qy * W + qx) * kD + dc * 8;
+      if (csb) {  // phases of pairs 4dc .. 4dc+3 as float16 (cos, sin)
+        const float4* pp = csb + ((int64_t)qy * W + qx) * 16 + 2 * dc;
+        const float4 p0 = pp[0], p1 = pp[1];
+        ph[it] = make_uint4(pack2h(p0.x, p0.y), pack2h(p0.z, p0.w), pack2h(p1.x, p1.y), pack2h(p1.z, p1.w));
+      }
+    }
+  }
+  // LSE / D entries of this thread: token offset inside a level, or -1
+  int soff[C::IS];
+  float pl[C::IS], pd[C::IS];
+#pragma unroll
+  for (int is = 0; is < C::IS; ++is) {
+    const int u = is * kThreads + tid;
+    soff[is] = u < nq ? (qy0 + u / nqx) * W + qx0 + u % nqx : -1;
+    pl[is] = 0.f;
+    pd[is] = 0.f;
+  }
+
+  auto issue = [&](int p, char* tq, char* tg) {
+    const int64_t lev = bh_base + (int64_t)p * HW;
+    const uint16_t* qp = a.q + lev * kD;
+    const uint16_t* gp = a.dout + lev * kD;
+#pragma unroll
+    for (int it = 0; it < C::IT; ++it) {
+      if (goff[it] < 0) continue;
+      copy16_to_lds(qp + goff[it], tq + (it * kThreads + wave * 64) * 16);
+      copy16_to_lds(gp + goff[it], tg + (it * kThreads + wave * 64) * 16);
+    }
+#pragma unroll
+    for (int is = 0; is < C::IS; ++is) {
+      if (soff[is] < 0) continue;
+      pl[is] = a.lse[lev + soff[is]];
+      pd[is] = a.dvec[lev + soff[is]];
+    }
+  };
+  // wait for this thread's copies and loads, rotate its own Q slots in place
+  // (bf16 -> float16), store its LSE / D entries
+  auto finish = [&](char* tq, float* sl, float* sd) {
+    __builtin_amdgcn_s_waitcnt(0);
+#pragma unroll
+    for (int it = 0; it < C::IT; ++it) {
+      if (goff[it] < 0) continue;
+      char* ad = tq + (it * kThreads + tid) * 16;
+      const uint4 x = ld16(ad);
+      st16(ad, csb ? rotate8h_pk(x, ph[it]) : scale8h(x, 1.f));
+    }
+#pragma unroll
+    for (int is = 0; is < C::IS; ++is) {
+      if (soff[is] < 0) continue;
+      const int u = is * kThreads + tid;
+      sl[u] = pl[is] * kLog2e;
+      sd[u] = -pd[is];
+    }
+  };
+
+  // ---- this wave's keys: K~ and V as B operands (col = key qn, k = d) ----------
+  const int ky_raw = y0 + (qn >> 2), kx_raw = x0 + (qn & 3);
+  const int ky = min(ky_raw, H - 1), kx = min(kx_raw, W - 1);
+  const int kz = z0 + wave;
+  const bool wave_on = kz < Z;
+  const int64_t ktok = bh_base + (int64_t)min(kz, Z - 1) * HW + (int64_t)ky * W + kx;
+  const float4* csk = csb ? csb + ((int64_t)ky * W + kx) * 16 : nullptr;
+  f16x8 kf[2];
+  bf16x8 vf[2];
+  {
+    const uint4* src = reinterpret_cast<const uint4*>(a.k + ktok * kD);
+    const uint4 x0v = src[g], x1v = src[4 + g];
+    uint4 r0, r1;
+    if (csk) {
+      r0 = rotate8h(x0v, csk[2 * g], csk[2 * g + 1], a.kscale);
+      r1 = rotate8h(x1v, csk[8 + 2 * g], csk[8 + 2 * g + 1], a.kscale);
+    } else {
+      r0 = scale8h(x0v, a.kscale);
+      r1 = scale8h(x1v, a.kscale);
+    }
+    kf[0] = __builtin_bit_cast(f16x8, r0);
+    kf[1] = __builtin_bit_cast(f16x8, r1);
+    const uint4* vs = reinterpret_cast<const uint4*>(a.v + ktok * kD);
+    vf[0] = __builtin_bit_cast(bf16x8, vs[g]);
+    vf[1] = __builtin_bit_cast(bf16x8, vs[4 + g]);
+  }
+  f32x4 accK[4], accV[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    accK[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    accV[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  int ex = kMinExp;
+
+  // lane-constant parts of the read addresses
+  // A rows: chunk c, row 16c + qn, column g (xor 64 bytes: g + 4)
+  const uint32_t aoff = qn * kRow + ((g ^ rswz(qn)) << 4);
+  // transpose reads: row 32 st + 4g + qn/4 (+16 for the second chunk), the
+  // 8 bytes holding elements 4 (qn % 4) .. +3 of each 16-wide d block (xor 32 t)
+  const int trow = 4 * g + (qn >> 2);
+  const uint32_t toff = trow * kRow + ((((qn >> 1) & 1) ^ rswz(trow)) << 4) + 8 * (qn & 1);
+
+  auto compute = [&](const char* tq, const char* tg, const float* sl, const float* sd) {
+    for (int st = 0; st < npairs; ++st) {
+      f32x4 x[2], y[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int c = 2 * st + h;
+        const char* rq = tq + c * (16 * kRow);
+        const char* rg = tg + c * (16 * kRow);
+        const f16x8 q0 = __builtin_bit_cast(f16x8, ld16(rq + aoff));
+        const f16x8 q1 = __builtin_bit_cast(f16x8, ld16(rq + (aoff ^ 64u)));
+        const bf16x8 g0 = __builtin_bit_cast(bf16x8, ld16(rg + aoff));
+        const bf16x8 g1 = __builtin_bit_cast(bf16x8, ld16(rg + (aoff ^ 64u)));
+        // seeds for rows 16c + 4g + i (the D layout of X and Y)
+        const int u4 = 16 * c + 4 * g;
+        const float4 l4 = *reinterpret_cast<const float4*>(sl + u4);
+        const float4 d4 = *reinterpret_cast<const float4*>(sd + u4);
+        const uint2 m4 = *reinterpret_cast<const uint2*>(smask + u4);
+        f32x4 xs;
+        xs[0] = ((m4.x >> qn) & 1u) ? -l4.x : -INFINITY;
+        xs[1] = ((m4.x >> (16 + qn)) & 1u) ? -l4.y : -INFINITY;
+        xs[2] = ((m4.y >> qn) & 1u) ? -l4.z : -INFINITY;
+        xs[3] = ((m4.y >> (16 + qn)) & 1u) ? -l4.w : -INFINITY;
+        const f32x4 ys = {d4.x, d4.y, d4.z, d4.w};
+        x[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(q0, kf[0], xs, 0, 0, 0);
+        x[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(q1, kf[1], x[h], 0, 0, 0);
+        y[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(g0, vf[0], ys, 0, 0, 0);
+        y[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(g1, vf[1], y[h], 0, 0, 0);
+      }
+      // exponent bound of |Y| for this lane's key (all four row groups)
+      float my = 0.f;
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        my = fmaxf(fmaxf(my, fmaxf(fabsf(y[h][0]), fabsf(y[h][1]))), fmaxf(fabsf(y[h][2]), fabsf(y[h][3])));
+      my = max_over_rows(my);
+      const int e = max(__builtin_amdgcn_frexp_expf(my), kMinExp);
+      if (__any(e > ex)) {  // the bound grew: rescale the dK~ accumulator exactly
+        const int en = max(ex, e);
+        const float f = __builtin_amdgcn_ldexpf(1.f, ex - en);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) accK[t] *= f;
+        ex = en;
+      }
+      const float sc = __builtin_amdgcn_ldexpf(1.f, 15 - ex);
+      uint32_t pb[2][2], db[2][2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const float p0 = __builtin_amdgcn_exp2f(x[h][0]), p1 = __builtin_amdgcn_exp2f(x[h][1]);
+        const float p2 = __builtin_amdgcn_exp2f(x[h][2]), p3 = __builtin_amdgcn_exp2f(x[h][3]);
+        pb[h][0] = pack2(p0, p1);
+        pb[h][1] = pack2(p2, p3);
+        db[h][0] = pack2h_rne(p0 * sc * y[h][0], p1 * sc * y[h][1]);
+        db[h][1] = pack2h_rne(p2 * sc * y[h][2], p3 * sc * y[h][3]);
+      }
+      const bf16x8 pf = __builtin_bit_cast(bf16x8, make_uint4(pb[0][0], pb[0][1], pb[1][0], pb[1][1]));
+      const f16x8 df = __builtin_bit_cast(f16x8, make_uint4(db[0][0], db[0][1], db[1][0], db[1][1]));
+      const char* tq0 = tq + st * (32 * kRow);
+      const char* tg0 = tg + st * (32 * kRow);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const uint32_t o0 = toff ^ (32u * t);
+        const uint2 g_lo = __builtin_bit_cast(uint2, tr_read(tg0 + o0));
+        const uint2 g_hi = __builtin_bit_cast(uint2, tr_read(tg0 + 16 * kRow + o0));
+        const bf16x8 gt = __builtin_bit_cast(bf16x8, make_uint4(g_lo.x, g_lo.y, g_hi.x, g_hi.y));
+        accV[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gt, pf, accV[t], 0, 0, 0);
+        const uint2 q_lo = __builtin_bit_cast(uint2, tr_read(tq0 + o0));
+        const uint2 q_hi = __builtin_bit_cast(uint2, tr_read(tq0 + 16 * kRow + o0));
+        const f16x8 qt = __builtin_bit_cast(f16x8, make_uint4(q_lo.x, q_lo.y, q_hi.x, q_hi.y));
+        accK[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(qt, df, accK[t], 0, 0, 0);
+      }
+    }
+  };
+  // does query level p see this wave's key level?
+  auto active = [&](int p) {
+    const int zs = win_start(p, Z, KZ);
+    return wave_on && kz >= zs && kz < zs + KZ;
+  };
+
+  // ---- query levels that see the block's key levels, double-buffered ---------
+  // Level p+1 is copied while level p is computed; then each thread waits for
+  // its own copies, finishes its own slots, and one barrier publishes the level.
+  // The barrier also retires every read of the tiles the next copy overwrites.
+  const int zk_last = min(z0 + kWaves, Z) - 1;
+  const int p_lo = inv_lo(z0, KZ), p_hi = inv_hi(zk_last, Z, KZ);
+  issue(p_lo, tQ0, tG0);
+  finish(tQ0, sL0, sD0);
+  __syncthreads();
+  for (int p = p_lo; p <= p_hi; p += 2) {
+    const bool more1 = p + 1 <= p_hi;
+    if (more1) issue(p + 1, tQ1, tG1);
+    if (active(p)) compute(tQ0, tG0, sL0, sD0);
+    if (more1) {
+      finish(tQ1, sL1, sD1);
+      __syncthreads();
+      const bool more2 = p + 2 <= p_hi;
+      if (more2) issue(p + 2, tQ0, tG0);
+      if (active(p + 1)) compute(tQ1, tG1, sL1, sD1);
+      if (more2) {
+        finish(tQ0, sL0, sD0);
+        __syncthreads();
+      }
+    }
+  }
+
+  // ---- store: dV, and dK = R^T (scale 2^(E-15) dK~); lane holds d = 16t + 4g + i ----
+  if (!wave_on || ky_raw >= H || kx_raw >= W) return;
+  const float f = a.scale * __builtin_amdgcn_ldexpf(1.f, ex - 15);
+  uint2* dkd = reinterpret_cast<uint2*>(a.dk + ktok * kD);
+  uint2* dvd = reinterpret_cast<uint2*>(a.dv + ktok * kD);
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    dvd[4 * t + g] = make_uint2(pack2(accV[t][0], accV[t][1]), pack2(accV[t][2], accV[t][3]));
+    float x0v = accK[t][0] * f, x1v = accK[t][1] * f, x2v = accK[t][2] * f, x3v = accK[t][3] * f;
+    if (csk) {
+      const float4 p = csk[4 * t + g];  // pairs 8t+2g and 8t+2g+1
+      const float r0 = fmaf(x0v, p.x, x1v * p.y), r1 = fmaf(x1v, p.x, -x0v * p.y);
+      const float r2 = fmaf(x2v, p.z, x3v * p.w), r3 = fmaf(x3v, p.z, -x2v * p.w);
+      x0v = r0; x1v = r1; x2v = r2; x3v = r3;
+    }
+    dkd[4 * t + g] = make_uint2(pack2(x0v, x1v), pack2(x2v, x3v));
+  }
+}
+
+// widest query box (per axis) over the 4-wide key blocks of an axis of extent L
+int max_box(int L, int k) {
+  int mx = 0;
+  for (int j0 = 0; j0 < L; j0 += 4) {
+    const int n = inv_hi(std::min(j0 + 3, L - 1), L, k) - inv_lo(j0, k) + 1;
+    mx = std::max(mx, n);
+  }
+  return mx;
+}
+
+template <int KZ, int KY, int KX>
+bool launch_kv(const strata_na3d_desc& d, const KvArgs& a0, hipStream_t s) {
+  using C = KvCfg<KZ, KY, KX>;
+  if (max_box(d.H, KY) > C::MQY || max_box(d.W, KX) > C::MQX) return false;
+  KvArgs a = a0;
+  a.n_zb = (d.Z + kWaves - 1) / kWaves;
+  a.n_yb = (d.H + 3) / 4;
+  a.n_xb = (d.W + 3) / 4;
+  const int64_t blocks = (int64_t)d.B * d.heads * a.n_zb * a.n_yb * a.n_xb;
+  if (blocks >= (int64_t)1 << 31) return false;
+  hipLaunchKernelGGL((na3d_mfma_kv_kernel<KZ, KY, KX>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
+  return true;
+}
+
+}  // namespace
+
+bool launch_na3d_bwd_dkdv_mfma(const strata_na3d_desc& d, const void* q, const void* k,
+                               const void* v, const float* cs, const void* dout, const float* lse,
+                               const float* dvec, void* dk, void* dv, hipStream_t s) {
+  if (d.dtype != STRATA_BF16 || d.head_dim != kD) return false;
+  if ((int64_t)d.H * d.W * kD >= (int64_t)1 << 31) return false;
+  KvArgs a = {};
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.cs = reinterpret_cast<const float4*>(cs);
+  a.dout = static_cast<const uint16_t*>(dout);
+  a.lse = lse;
+  a.dvec = dvec;
+  a.dk = static_cast<uint16_t*>(dk);
+  a.dv = static_cast<uint16_t*>(dv);
+  a.heads = d.heads;
+  a.Z = d.Z;
+  a.H = d.H;
+  a.W = d.W;
+  a.scale = d.scale;
+  a.kscale = d.scale * kLog2e;
+  if (d.kz == 3 && d.ky == 7 && d.kx == 7) return launch_kv<3, 7, 7>(d, a, s);
+  if (d.kz == 5 && d.ky == 9 && d.kx == 9) return launch_kv<5, 9, 9>(d, a, s);
+  return false;
+}
+
+}  // namespace strata

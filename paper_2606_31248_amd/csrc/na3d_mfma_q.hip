@@ -1,4 +1,5 @@
-// MFMA neighbourhood-attention forward for gfx950 (bf16 in/out, head_dim 64).
+// MFMA neighbourhood attention for gfx950, query-stationary kernels (bf16 in/out,
+// head_dim 64): the forward, and the dQ part of the backward.
 //
 // Work decomposition
 //   workgroup : one (tile, head), an 8 x 8 block of (y, x) query positions and
@@ -40,21 +41,28 @@
 // immediate offsets.  The two halves of the double buffer are distinct LDS objects, so the
 // compiler can tell the reads of one from the copies into the other and does not
 // wait for the copies before reading.
+//
+// Backward, dQ (same decomposition and key staging; a lane still owns a query):
+//   S^T = K . Q^T as above, seeded with the mask; P^T = exp2(S^T - LSE) from the
+//   forward's log-sum-exp (no online softmax);
+//   Y^T (16 keys x 16 queries) = V . dO^T - D   bf16 MFMA, V rows read as the A
+//                                           operand, dO of the lane's query held
+//                                           in registers, seeded with -D;
+//   dS^T = P^T * Y^T, and dQ~^T (64 d x 16 queries) += K~^T . dS^T as a float16
+//   MFMA whose K~^T fragments come from the rotated K tile by the transpose read.
+//   dS is carried in float16 with a per-query power-of-two scale 2^(15 - E): E
+//   bounds |Y| of every key level seen so far (|dS| <= P |Y|, P <= 1), so the
+//   scaled values stay below 2^15, and the accumulator is rescaled exactly when E
+//   grows.  At the end dQ = R^T (scale 2^(E-15) dQ~).
 #include "common.h"
 #include "kernels.h"
+#include "mfma_util.h"
 
 namespace strata {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
-typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void;
+using namespace mfma;
+
 
 constexpr int kBY = 8, kBX = 8;  // query block of a workgroup (y, x)
 constexpr int kWaves = 8;
@@ -66,6 +74,7 @@ constexpr int kLdsMax = 160 * 1024;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kLazy = 8.0f;    // rescale only when the maximum grows by > 2^8
+constexpr int kMinExp = -100;    // lower bound of the dS exponent (keeps 2^(15-E) finite)
 
 template <int KZ, int KY, int KX, int ZQ>
 struct Cfg {
@@ -98,117 +107,19 @@ struct Args {
   const uint16_t* k;
   const uint16_t* v;
   const float4* cs;   // [B, H, W, 16] float4 = two (cos, sin) pairs; nullptr: no rotation
-  uint16_t* out;
-  float* lse;
+  uint16_t* out;      // forward: O; backward: dQ
+  float* lse;         // forward: optional LSE output
+  const uint16_t* dout;  // backward: dO
+  const float* lse_in;   // backward: LSE of the forward (natural log)
+  const float* dvec;     // backward: D = rowsum(dO * O)
   int heads, Z, H, W;
   int n_zb, n_yb, n_xb;
   float qscale;       // scale * log2(e)
+  float scale;
 };
 
-__device__ __forceinline__ uint32_t pack2(float a, float b) {
-  f32x2 f = {a, b};
-  bf16x2 h = __builtin_convertvector(f, bf16x2);
-  return __builtin_bit_cast(uint32_t, h);
-}
-
-// Two floats -> packed float16 pair (nearest-even), saturating at +-65504.
-__device__ __forceinline__ uint32_t pack2h(float a, float b) {
-  f32x2 f = {__builtin_amdgcn_fmed3f(a, -65504.f, 65504.f), __builtin_amdgcn_fmed3f(b, -65504.f, 65504.f)};
-  f16x2 h = __builtin_convertvector(f, f16x2);
-  return __builtin_bit_cast(uint32_t, h);
-}
-
-__device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
-
-// Rotate 4 pairs held as 4 packed bf16x2 words by phases (c0,s0,c1,s1),(c2,s2,c3,s3),
-// multiply by `mul`, and return them as 4 packed float16x2 words.
-__device__ __forceinline__ uint4 rotate8h(uint4 x, float4 p01, float4 p23, float mul) {
-  uint32_t w[4] = {x.x, x.y, x.z, x.w};
-  float cs_[8] = {p01.x, p01.y, p01.z, p01.w, p23.x, p23.y, p23.z, p23.w};
-  uint32_t r[4];
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    float a = lo_bf16(w[t]), b = hi_bf16(w[t]);
-    float c = cs_[2 * t], s = cs_[2 * t + 1];
-    r[t] = pack2h(fmaf(a, c, -b * s) * mul, fmaf(a, s, b * c) * mul);
-  }
-  return make_uint4(r[0], r[1], r[2], r[3]);
-}
-
-// Rotate 4 pairs held as packed bf16x2 words by float16 phases (c, s) in
-// packed float16 arithmetic (one multiply and one fused multiply-add per pair);
-// returns packed float16x2 words.  Inputs are clamped to +-46000 so that no
-// rotated value leaves the float16 range.
-__device__ __forceinline__ uint4 rotate8h_pk(uint4 x, uint4 ph) {
-  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
-  const uint32_t p[4] = {ph.x, ph.y, ph.z, ph.w};
-  uint32_t r[4];
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const float a = __builtin_amdgcn_fmed3f(lo_bf16(w[t]), -46000.f, 46000.f);
-    const float b = __builtin_amdgcn_fmed3f(hi_bf16(w[t]), -46000.f, 46000.f);
-    const f16x2 ab = __builtin_convertvector((f32x2{a, b}), f16x2);
-    const f16x2 cs = __builtin_bit_cast(f16x2, p[t]);
-    const f16x2 aa = {ab.x, ab.x}, bb = {ab.y, ab.y}, ns = {-cs.y, cs.x};
-    r[t] = __builtin_bit_cast(uint32_t, aa * cs + bb * ns);  // (a c - b s, a s + b c)
-  }
-  return make_uint4(r[0], r[1], r[2], r[3]);
-}
-
-// bf16 x 8 -> float16 x 8, times `mul` (no rotation).
-__device__ __forceinline__ uint4 scale8h(uint4 x, float mul) {
-  uint32_t w[4] = {x.x, x.y, x.z, x.w};
-  uint32_t r[4];
-#pragma unroll
-  for (int t = 0; t < 4; ++t) r[t] = pack2h(lo_bf16(w[t]) * mul, hi_bf16(w[t]) * mul);
-  return make_uint4(r[0], r[1], r[2], r[3]);
-}
-
-__device__ __forceinline__ i16x4 tr_read(const char* p) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p);
-}
-
-__device__ __forceinline__ uint4 ld16(const char* p) {
-  const u32x4 v = *reinterpret_cast<const u32x4*>(p);
-  return make_uint4(v.x, v.y, v.z, v.w);
-}
-
-__device__ __forceinline__ void st16(char* p, uint4 v) {
-  *reinterpret_cast<u32x4*>(p) = u32x4{v.x, v.y, v.z, v.w};
-}
-
-// Direct global -> LDS copy of 16 bytes per lane: lane i of the wave writes
-// wave_dst + 16 i (wave_dst must be the same for the whole wave).
-__device__ __forceinline__ void copy16_to_lds(const uint16_t* src, char* wave_dst) {
-  __builtin_amdgcn_global_load_lds(src, (lds_void*)wave_dst, 16, 0, 0);
-}
-
-// Cross-row exchanges without LDS (gfx950 v_permlane16/32_swap): with both
-// operands equal, the two results of a swap are, in some order, the lane's own
-// value and the value of lane l^16 (resp. l^32).
-__device__ __forceinline__ float max_over_rows(float x) {
-  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-
-__device__ __forceinline__ float sum_over_rows(float x) {
-  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
-  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
-__device__ __forceinline__ float psum8(uint32_t a, uint32_t b, float acc) {
-  const bf16x2 one = __builtin_bit_cast(bf16x2, 0x3F803F80u);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), one, acc, false);
-  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, b), one, acc, false);
-}
-
-template <int KZ, int KY, int KX, int ZQ>
-__global__ void __launch_bounds__(kThreads, 1) na3d_fwd_mfma_kernel(Args a) {
+template <int KZ, int KY, int KX, int ZQ, bool BWD>
+__global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
   using C = Cfg<KZ, KY, KX, ZQ>;
   // double buffer of key tiles (distinct objects, see above), copy offsets, phases
   __shared__ __attribute__((aligned(16))) char tK0[C::KBYTES];
@@ -248,23 +159,29 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_mfma_kernel(Args a) {
 
   // column swizzle of the K tile (see the header comment)
   auto kswz = [&](int key) { return ((key % C::LX >> 1) + 5 * (key / C::LX)) & 7; };
+  // tile row of sub-block key u (u past the box: row 0, masked)
+  auto key_row = [&](int u) {
+    return u < C::NU ? (uy0 - ty0 + u / C::NUX) * C::LX + (ux0 - tx0 + u % C::NUX) : 0;
+  };
 
   // ---- per-lane tile offsets and window mask, identical for every key level ----
-  uint32_t kaddr[C::NC], vaddr[C::NC];
+  // forward: vaddr = V^T transpose-read address; backward: vaddr = V row (A
+  // operand) address, ktaddr = K~^T transpose-read address
+  uint32_t kaddr[C::NC], vaddr[C::NC], ktaddr[BWD ? C::NC : 1];
   f32x4 bias[C::NC];
 #pragma unroll
   for (int c = 0; c < C::NC; ++c) {
     {  // K fragment (A operand): row = key 16c + qn, 16 bytes at column g (xor 64 bytes: g+4)
-      int u = 16 * c + qn;
-      int key = 0;
-      if (u < C::NU) key = (uy0 - ty0 + u / C::NUX) * C::LX + (ux0 - tx0 + u % C::NUX);
+      const int key = key_row(16 * c + qn);
       kaddr[c] = key * kKRow + ((g ^ kswz(key)) << 4);
+      if constexpr (BWD) vaddr[c] = key * kVRow + 16 * g;  // V row, columns g and g+4
     }
-    {  // V^T fragment by transpose read: source row = key 16c + 4g + qn/4, element 4*(qn%4)
-      int u = 16 * c + 4 * g + (qn >> 2);
-      int key = 0;
-      if (u < C::NU) key = (uy0 - ty0 + u / C::NUX) * C::LX + (ux0 - tx0 + u % C::NUX);
-      vaddr[c] = key * kVRow + (qn & 3) * 8;
+    {  // transpose reads: source row = key 16c + 4g + qn/4, elements 4*(qn%4) of a 16-wide block
+      const int key = key_row(16 * c + 4 * g + (qn >> 2));
+      if constexpr (BWD)
+        ktaddr[c] = key * kKRow + ((((qn >> 1) & 1) ^ kswz(key)) << 4) + 8 * (qn & 1);
+      else
+        vaddr[c] = key * kVRow + (qn & 3) * 8;
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -358,14 +275,20 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_mfma_kernel(Args a) {
   };
 
   // ---- queries: load, rotate, scale, keep as the B operand of K.Q^T ----------
+  // forward: running max m, row sum l, O^T accumulator o;
+  // backward: dO^T fragments gf, LSE in log2 units lse2, -D nd, dS exponent ex,
+  //           dQ~^T accumulator o
   f16x8 qf[C::QL][2];
+  bf16x8 gf[BWD ? C::QL : 1][2];
   float m[C::QL], l[C::QL];
+  int ex[C::QL];
   f32x4 o[C::QL][4];
   const float4* csq = csb ? csb + ((int64_t)qy * W + qx) * 16 : nullptr;
 #pragma unroll
   for (int j = 0; j < C::QL; ++j) {
     int zq = min(z0 + grp + 2 * j, Z - 1);
-    const uint4* src = reinterpret_cast<const uint4*>(a.q + (bh_base + zq * HW + (int64_t)qy * W + qx) * kD);
+    const int64_t tok = bh_base + zq * HW + (int64_t)qy * W + qx;
+    const uint4* src = reinterpret_cast<const uint4*>(a.q + tok * kD);
     uint4 x0 = src[g], x1 = src[4 + g];
     uint4 r0, r1;
     if (csq) {
@@ -377,8 +300,17 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_mfma_kernel(Args a) {
     }
     qf[j][0] = __builtin_bit_cast(f16x8, r0);
     qf[j][1] = __builtin_bit_cast(f16x8, r1);
-    m[j] = -INFINITY;
-    l[j] = 0.f;
+    if constexpr (BWD) {
+      const uint4* gsrc = reinterpret_cast<const uint4*>(a.dout + tok * kD);
+      gf[j][0] = __builtin_bit_cast(bf16x8, gsrc[g]);
+      gf[j][1] = __builtin_bit_cast(bf16x8, gsrc[4 + g]);
+      m[j] = a.lse_in[tok] * kLog2e;  // lse2
+      l[j] = -a.dvec[tok];            // -D
+      ex[j] = kMinExp;
+    } else {
+      m[j] = -INFINITY;
+      l[j] = 0.f;
+    }
 #pragma unroll
     for (int t = 0; t < 4; ++t) o[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
@@ -432,6 +364,61 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_mfma_kernel(Args a) {
     }
   };
 
+  // backward: one (query level j, key level) step of dQ~ with the key tiles tk, tv
+  auto update_dq = [&](int j, const char* tk, const char* tv) {
+    f32x4 s[C::NC], y[C::NC];
+    const f32x4 nd = {l[j], l[j], l[j], l[j]};
+#pragma unroll
+    for (int c = 0; c < C::NC; ++c) {
+      f16x8 k0 = __builtin_bit_cast(f16x8, ld16(tk + kaddr[c]));
+      f16x8 k1 = __builtin_bit_cast(f16x8, ld16(tk + (kaddr[c] ^ 64u)));
+      f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(k0, qf[j][0], bias[c], 0, 0, 0);
+      s[c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(k1, qf[j][1], acc, 0, 0, 0);
+      bf16x8 v0 = __builtin_bit_cast(bf16x8, ld16(tv + vaddr[c]));
+      bf16x8 v1 = __builtin_bit_cast(bf16x8, ld16(tv + vaddr[c] + 64));
+      f32x4 t0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v0, gf[j][0], nd, 0, 0, 0);
+      y[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v1, gf[j][1], t0, 0, 0, 0);
+    }
+    // exponent bound of |Y| over this level's keys (all rows of the query)
+    float my = 0.f;
+#pragma unroll
+    for (int c = 0; c < C::NC; ++c)
+      my = fmaxf(fmaxf(my, fmaxf(fabsf(y[c][0]), fabsf(y[c][1]))), fmaxf(fabsf(y[c][2]), fabsf(y[c][3])));
+    my = max_over_rows(my);
+    const int e = max(__builtin_amdgcn_frexp_expf(my), kMinExp);
+    if (__any(e > ex[j])) {  // the bound grew: rescale the accumulator exactly
+      const int en = max(ex[j], e);
+      const float f = __builtin_amdgcn_ldexpf(1.f, ex[j] - en);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) o[j][t] *= f;
+      ex[j] = en;
+    }
+    // P scaled by 2^(15 - E): exp2(S - (lse2 + E - 15))
+    const float cj = m[j] + (float)(ex[j] - 15);
+    uint32_t dk[C::NC][2];
+#pragma unroll
+    for (int c = 0; c < C::NC; ++c) {
+      const float p0 = __builtin_amdgcn_exp2f(s[c][0] - cj), p1 = __builtin_amdgcn_exp2f(s[c][1] - cj);
+      const float p2 = __builtin_amdgcn_exp2f(s[c][2] - cj), p3 = __builtin_amdgcn_exp2f(s[c][3] - cj);
+      dk[c][0] = pack2h_rne(p0 * y[c][0], p1 * y[c][1]);
+      dk[c][1] = pack2h_rne(p2 * y[c][2], p3 * y[c][3]);
+    }
+#pragma unroll
+    for (int st = 0; st < C::NS; ++st) {
+      const int c0 = 2 * st, c1 = 2 * st + 1;
+      const bool two = c1 < C::NC;
+      f16x8 df = __builtin_bit_cast(f16x8, make_uint4(dk[c0][0], dk[c0][1], two ? dk[c1][0] : 0u, two ? dk[c1][1] : 0u));
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        i16x4 lo = tr_read(tk + (ktaddr[c0] ^ (32u * t)));
+        i16x4 hi = two ? tr_read(tk + (ktaddr[c1] ^ (32u * t))) : i16x4{0, 0, 0, 0};
+        uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
+        f16x8 kt = __builtin_bit_cast(f16x8, make_uint4(l2.x, l2.y, h2.x, h2.y));
+        o[j][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kt, df, o[j][t], 0, 0, 0);
+      }
+    }
+  };
+
   // all query levels of this wave whose window holds key level p
   auto compute = [&](int p, const char* tk, const char* tv) {
 #pragma unroll
@@ -440,7 +427,8 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_mfma_kernel(Args a) {
       if (zq >= Z) continue;
       const int zs = win_start(zq, Z, KZ);
       if (p < zs || p >= zs + KZ) continue;
-      update(j, tk, tv);
+      if constexpr (BWD) update_dq(j, tk, tv);
+      else update(j, tk, tv);
     }
   };
 
@@ -481,53 +469,98 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_mfma_kernel(Args a) {
 #pragma unroll
   for (int j = 0; j < C::QL; ++j) {
     const int zq = z0 + grp + 2 * j;
-    const float lt = sum_over_rows(l[j]);
-    if (zq >= Z || !in_grid) continue;
-    const float inv = 1.f / lt;
-    const int64_t tok = bh_base + zq * HW + (int64_t)qy * W + qx;
-    uint2* dst = reinterpret_cast<uint2*>(a.out + tok * kD);
+    if constexpr (BWD) {
+      if (zq >= Z || !in_grid) continue;
+      // dQ = R^T (scale 2^(E-15) dQ~); lane holds d = 16t + 4g + i
+      const float f = a.scale * __builtin_amdgcn_ldexpf(1.f, ex[j] - 15);
+      const int64_t tok = bh_base + zq * HW + (int64_t)qy * W + qx;
+      uint2* dst = reinterpret_cast<uint2*>(a.out + tok * kD);
 #pragma unroll
-    for (int t = 0; t < 4; ++t)  // d = 16t + 4g + i
-      dst[4 * t + g] = make_uint2(pack2(o[j][t][0] * inv, o[j][t][1] * inv),
-                                  pack2(o[j][t][2] * inv, o[j][t][3] * inv));
-    if (a.lse && g == 0) a.lse[tok] = (m[j] + __log2f(lt)) * kLn2;
+      for (int t = 0; t < 4; ++t) {
+        float x0 = o[j][t][0] * f, x1 = o[j][t][1] * f, x2 = o[j][t][2] * f, x3 = o[j][t][3] * f;
+        if (csq) {
+          const float4 ph = csq[4 * t + g];  // pairs 8t+2g and 8t+2g+1
+          const float r0 = fmaf(x0, ph.x, x1 * ph.y), r1 = fmaf(x1, ph.x, -x0 * ph.y);
+          const float r2 = fmaf(x2, ph.z, x3 * ph.w), r3 = fmaf(x3, ph.z, -x2 * ph.w);
+          x0 = r0; x1 = r1; x2 = r2; x3 = r3;
+        }
+        dst[4 * t + g] = make_uint2(pack2(x0, x1), pack2(x2, x3));
+      }
+    } else {
+      const float lt = sum_over_rows(l[j]);
+      if (zq >= Z || !in_grid) continue;
+      const float inv = 1.f / lt;
+      const int64_t tok = bh_base + zq * HW + (int64_t)qy * W + qx;
+      uint2* dst = reinterpret_cast<uint2*>(a.out + tok * kD);
+#pragma unroll
+      for (int t = 0; t < 4; ++t)  // d = 16t + 4g + i
+        dst[4 * t + g] = make_uint2(pack2(o[j][t][0] * inv, o[j][t][1] * inv),
+                                    pack2(o[j][t][2] * inv, o[j][t][3] * inv));
+      if (a.lse && g == 0) a.lse[tok] = (m[j] + __log2f(lt)) * kLn2;
+    }
   }
 }
 
-template <int KZ, int KY, int KX, int ZQ>
-bool launch(const strata_na3d_desc& d, const void* q, const void* k, const void* v, const float* cs,
-            void* out, float* lse, hipStream_t s) {
-  Args a;
+Args make_args(const strata_na3d_desc& d, int zq, const void* q, const void* k, const void* v,
+               const float* cs) {
+  Args a = {};
   a.q = static_cast<const uint16_t*>(q);
   a.k = static_cast<const uint16_t*>(k);
   a.v = static_cast<const uint16_t*>(v);
   a.cs = reinterpret_cast<const float4*>(cs);
-  a.out = static_cast<uint16_t*>(out);
-  a.lse = lse;
   a.heads = d.heads;
   a.Z = d.Z;
   a.H = d.H;
   a.W = d.W;
-  a.n_zb = (d.Z + ZQ - 1) / ZQ;
+  a.n_zb = (d.Z + zq - 1) / zq;
   a.n_yb = (d.H + kBY - 1) / kBY;
   a.n_xb = (d.W + kBX - 1) / kBX;
   a.qscale = d.scale * kLog2e;
+  a.scale = d.scale;
+  return a;
+}
+
+template <int KZ, int KY, int KX, int ZQ, bool BWD>
+bool launch(const strata_na3d_desc& d, const Args& a, hipStream_t s) {
   int64_t blocks = (int64_t)d.B * d.heads * a.n_zb * a.n_yb * a.n_xb;
   if (blocks >= (int64_t)1 << 31) return false;
-  hipLaunchKernelGGL((na3d_fwd_mfma_kernel<KZ, KY, KX, ZQ>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL((na3d_mfma_q_kernel<KZ, KY, KX, ZQ, BWD>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
   return true;
+}
+
+bool supported(const strata_na3d_desc& d) {
+  if (d.dtype != STRATA_BF16 || d.head_dim != kD) return false;
+  // element offsets inside one key level are int32
+  return (int64_t)d.H * d.W * kD < (int64_t)1 << 31;
 }
 
 }  // namespace
 
 bool launch_na3d_fwd_mfma(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
                           const float* cs, void* out, float* lse, hipStream_t s) {
-  if (d.dtype != STRATA_BF16 || d.head_dim != kD) return false;
-  // element offsets inside one key level are int32
-  if ((int64_t)d.H * d.W * kD >= (int64_t)1 << 31) return false;
-  if (d.kz == 3 && d.ky == 7 && d.kx == 7) return launch<3, 7, 7, 8>(d, q, k, v, cs, out, lse, s);
-  if (d.kz == 5 && d.ky == 9 && d.kx == 9) return launch<5, 9, 9, 2>(d, q, k, v, cs, out, lse, s);
-  return false;
+  if (!supported(d)) return false;
+  const bool w377 = d.kz == 3 && d.ky == 7 && d.kx == 7, w599 = d.kz == 5 && d.ky == 9 && d.kx == 9;
+  if (!w377 && !w599) return false;
+  Args a = make_args(d, w377 ? 8 : 2, q, k, v, cs);
+  a.out = static_cast<uint16_t*>(out);
+  a.lse = lse;
+  if (w377) return launch<3, 7, 7, 8, false>(d, a, s);
+  return launch<5, 9, 9, 2, false>(d, a, s);
+}
+
+bool launch_na3d_bwd_dq_mfma(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
+                             const float* cs, const void* dout, const float* lse,
+                             const float* dvec, void* dq, hipStream_t s) {
+  if (!supported(d)) return false;
+  const bool w377 = d.kz == 3 && d.ky == 7 && d.kx == 7, w599 = d.kz == 5 && d.ky == 9 && d.kx == 9;
+  if (!w377 && !w599) return false;
+  Args a = make_args(d, w377 ? 4 : 2, q, k, v, cs);
+  a.out = static_cast<uint16_t*>(dq);
+  a.dout = static_cast<const uint16_t*>(dout);
+  a.lse_in = lse;
+  a.dvec = dvec;
+  if (w377) return launch<3, 7, 7, 4, true>(d, a, s);
+  return launch<5, 9, 9, 2, true>(d, a, s);
 }
 
 }  // namespace strata

@@ -241,8 +241,9 @@ __global__ void __launch_bounds__(128) na3d_bwd_dkdv_ref_kernel(
   }
 }
 
+// part: 0 = D = rowsum(dO * O), 1 = dq, 2 = dk and dv
 template <typename T, int D>
-static void bwd_ref(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
+static void bwd_ref(int part, const strata_na3d_desc& d, const void* q, const void* k, const void* v,
                     const float* cs, const void* out, const void* dout, const float* lse, void* dq,
                     void* dk, void* dv, float* dvec, hipStream_t s) {
   Dims dm{d.B, d.heads, d.Z, d.H, d.W, d.kz, d.ky, d.kx, d.scale};
@@ -250,26 +251,29 @@ static void bwd_ref(const strata_na3d_desc& d, const void* q, const void* k, con
   int threads = 128;
   int blocks = (int)((n + threads - 1) / threads);
   const float2* c2 = reinterpret_cast<const float2*>(cs);
-  hipLaunchKernelGGL((na3d_bwd_pre_kernel<T, D>), dim3((int)((n + 255) / 256)), dim3(256), 0, s,
-                     static_cast<const T*>(out), static_cast<const T*>(dout), dvec, n);
-  hipLaunchKernelGGL((na3d_bwd_dq_ref_kernel<T, D>), dim3(blocks), dim3(threads), 0, s,
-                     static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), c2,
-                     static_cast<const T*>(dout), lse, dvec, static_cast<T*>(dq), dm);
-  hipLaunchKernelGGL((na3d_bwd_dkdv_ref_kernel<T, D>), dim3(blocks), dim3(threads), 0, s,
-                     static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), c2,
-                     static_cast<const T*>(dout), lse, dvec, static_cast<T*>(dk), static_cast<T*>(dv),
-                     dm);
+  if (part == 0)
+    hipLaunchKernelGGL((na3d_bwd_pre_kernel<T, D>), dim3((int)((n + 255) / 256)), dim3(256), 0, s,
+                       static_cast<const T*>(out), static_cast<const T*>(dout), dvec, n);
+  else if (part == 1)
+    hipLaunchKernelGGL((na3d_bwd_dq_ref_kernel<T, D>), dim3(blocks), dim3(threads), 0, s,
+                       static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), c2,
+                       static_cast<const T*>(dout), lse, dvec, static_cast<T*>(dq), dm);
+  else
+    hipLaunchKernelGGL((na3d_bwd_dkdv_ref_kernel<T, D>), dim3(blocks), dim3(threads), 0, s,
+                       static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), c2,
+                       static_cast<const T*>(dout), lse, dvec, static_cast<T*>(dk), static_cast<T*>(dv),
+                       dm);
 }
 
-void launch_na3d_bwd_ref(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
-                         const float* cs, const void* out, const void* dout, const float* lse,
-                         void* dq, void* dk, void* dv, float* dvec, hipStream_t s) {
+void launch_na3d_bwd_ref(int part, const strata_na3d_desc& d, const void* q, const void* k,
+                         const void* v, const float* cs, const void* out, const void* dout,
+                         const float* lse, void* dq, void* dk, void* dv, float* dvec, hipStream_t s) {
   if (d.dtype == STRATA_BF16) {
-    if (d.head_dim == 32) bwd_ref<uint16_t, 32>(d, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
-    else bwd_ref<uint16_t, 64>(d, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+    if (d.head_dim == 32) bwd_ref<uint16_t, 32>(part, d, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+    else bwd_ref<uint16_t, 64>(part, d, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
   } else {
-    if (d.head_dim == 32) bwd_ref<float, 32>(d, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
-    else bwd_ref<float, 64>(d, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+    if (d.head_dim == 32) bwd_ref<float, 32>(part, d, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+    else bwd_ref<float, 64>(part, d, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
   }
 }
 
