@@ -12,7 +12,10 @@ Inputs are resident in HBM before timing starts.
 Prints one JSON line.  ``value`` is the neighbourhood-attention forward's
 algorithmic TFLOP/s over the whole step (4 B h N K d FLOPs per step divided by
 the step time); the dominant kernel's roofline and a timed CPU-oracle sample
-are reported beside it.
+are reported beside it.  Two side measurements follow the step (not part of
+``value``): the training-tile attention (16 tiles x 16 heads x 8x64x64, 5x9x9,
+forward and backward with StereoRoPE) and the standalone StereoRoPE rotation
+of its Q and K.
 """
 from __future__ import annotations
 
@@ -82,12 +85,76 @@ def cpu_baseline(wl, tiles_sample: int):
                       f"{wl.B} tiles (all {wl.heads} heads x {wl.N} tokens; blend not included)"}
 
 
+def train_tile(steps: int):
+    """Forward and backward of the 16-tile 5x9x9 training tile (StereoRoPE on), and
+    the standalone rotation of its Q and K; HIP-event times on the current stream."""
+    import torch
+    from paper_2606_31248_amd import binding as Bd
+    from paper_2606_31248_amd import inputs as I
+    from paper_2606_31248_amd import pipeline as Pp
+
+    wl = I.TRAIN_TILE_BWD
+    dev = torch.device("cuda:0")
+
+    def to_dev(bits):
+        return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(dev)
+
+    q, k, v = (to_dev(x) for x in wl.qkv())
+    g = to_dev(wl.dout())
+    geom = Pp.TileGeometry(*(torch.from_numpy(x).to(dev) for x in wl.placement().as_int32()))
+    _, cs = Pp.stereo_phases(geom, wl.H, wl.W, wl.d)
+    window = (wl.kz, wl.ky, wl.kx)
+    desc = Bd.desc_for(q, window, wl.scale)
+    out = torch.empty_like(q)
+    lse = torch.empty(wl.shape()[:-1], dtype=torch.float32, device=dev)
+    ws = torch.empty(Bd.strata_na3d_bwd_workspace_size(desc), dtype=torch.uint8, device=dev)
+    dq, dk, dv = (torch.empty_like(q) for _ in range(3))
+    qr = torch.empty_like(q)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        st = torch.cuda.current_stream()
+        ts = []
+        for _ in range(steps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(st)
+            fn()
+            e1.record(st)
+            ts.append((e0, e1))
+        torch.cuda.synchronize()
+        return float(np.mean([a.elapsed_time(b) for a, b in ts]))
+
+    fwd_ms = timed(lambda: Bd.strata_na3d_fwd(desc, q, k, v, cs, out, lse))
+    bwd_ms = timed(lambda: Bd.strata_na3d_bwd(desc, q, k, v, cs, out, g, lse, dq, dk, dv, ws))
+
+    def rope_qk():
+        Bd.strata_stereorope_apply(q, qr, cs)
+        Bd.strata_stereorope_apply(k, qr, cs)
+    rope_ms = timed(rope_qk)
+    n = wl.B * wl.heads * wl.N
+    fwd_fl, bwd_fl = 4.0 * n * wl.K * wl.d, 10.0 * n * wl.K * wl.d
+    rope_bytes = 2 * 2 * n * wl.d * 2 + 2 * wl.B * wl.H * wl.W * wl.d * 4   # Q, K read+write; phases
+    return {
+        "workload": f"{wl.name}: {wl.B} tiles x {wl.heads} heads x {wl.Z}x{wl.H}x{wl.W}, window "
+                    f"{wl.kz}x{wl.ky}x{wl.kx}, StereoRoPE on",
+        "fwd_ms": round(fwd_ms, 4), "fwd_tflops": round(fwd_fl / fwd_ms / 1e9, 2),
+        "bwd_ms": round(bwd_ms, 4), "bwd_tflops": round(bwd_fl / bwd_ms / 1e9, 2),
+        "bwd_pct_bf16_peak": round(100 * bwd_fl / bwd_ms / 1e9 / PEAK_BF16_TFLOPS, 2),
+        "bwd_flops_model": "10 B h N K d (QK^T twice, dO.V^T, P^T.dO, dS.K, dS^T.Q)",
+        "rope_apply_qk": {"ms": round(rope_ms, 4), "gbs": round(rope_bytes / rope_ms / 1e6, 1),
+                          "frac_hbm": round(rope_bytes / rope_ms / 1e6 / PEAK_HBM_GBS, 4)},
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--cpu-tiles", type=int, default=24, help="tiles in the CPU-oracle sample (0: skip)")
+    ap.add_argument("--cpu-tiles", type=int, default=32, help="tiles in the CPU-oracle sample (0: skip)")
+    ap.add_argument("--train-steps", type=int, default=5,
+                    help="timed passes of the training-tile forward/backward side measurement (0: skip)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run one 1 GiB device copy (HBM counter calibration)")
     a = ap.parse_args()
@@ -200,6 +267,10 @@ def main():
                      "traffic": None if traffic is None else float(traffic),
                      "kernel": "strata_na3d_fwd", "alg_bytes_per_launch": alg_bytes},
     }
+    if a.train_steps > 0:
+        del q, k, v, out, face, coords, cs
+        torch.cuda.empty_cache()
+        res["train_tile"] = train_tile(a.train_steps)
     if a.cpu_tiles > 0:
         res["cpu_baseline"] = cpu_baseline(wl, a.cpu_tiles)
     print(json.dumps(res), flush=True)

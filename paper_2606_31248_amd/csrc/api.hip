@@ -216,6 +216,10 @@ strata_status strata_tile_blend(const void* tiles, int32_t nty, int32_t ntx, int
   REQUIRE_PTR(tiles);
   REQUIRE_PTR(window);
   REQUIRE_PTR(out);
+  // one block per 256 items of a face row: the grid and in-row indices are 32-bit
+  REQUIRE((int64_t)Wf * C < ((int64_t)1 << 31) &&
+              (int64_t)P * Hf * (((int64_t)Wf * C + 255) / 256) < ((int64_t)1 << 31),
+          "tile_blend: face too large for one launch");
   launch_tile_blend(tiles, nty, ntx, P, Ht, Wt, C, stride_y, stride_x, window, out, Hf, Wf, dtype,
                     (hipStream_t)stream);
   return check_launch("strata_tile_blend");

@@ -42,21 +42,22 @@ __device__ __forceinline__ void cover_range(int y, int Ht, int s, int n, int* lo
   *hi = a1 < n - 1 ? a1 : n - 1;
 }
 
-template <typename T, int VEC>
-__global__ void tile_blend_kernel(const T* __restrict__ tiles, int nty, int ntx, int P, int Ht,
-                                  int Wt, int C, int sy, int sx, const float* __restrict__ window,
-                                  T* __restrict__ out, int Hf, int Wf) {
+// One block covers BLK consecutive (x, channel-vector) items of one face row
+// (p, y); the covering tile rows follow from y once per block.  CV > 0: the
+// number of channel vectors per cell is known at compile time.
+template <typename T, int VEC, int CV>
+__global__ void __launch_bounds__(256) tile_blend_kernel(const T* __restrict__ tiles, int nty, int ntx, int P,
+                                                         int Ht, int Wt, int C, int sy, int sx,
+                                                         const float* __restrict__ window,
+                                                         T* __restrict__ out, int Hf, int Wf, int bpr) {
   using Tr = BlendTraits<T>;
   using Acc = typename Tr::Acc;
-  const int cv = C / VEC;
-  int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  int64_t total = (int64_t)P * Hf * Wf * cv;
-  if (idx >= total) return;
-  int c0 = (int)(idx % cv) * VEC;
-  int64_t cell = idx / cv;
-  int x = (int)(cell % Wf);
-  int y = (int)((cell / Wf) % Hf);
-  int p = (int)(cell / ((int64_t)Wf * Hf));
+  const int cv = CV > 0 ? CV : C / VEC;
+  const int row = blockIdx.x / bpr;                 // p * Hf + y
+  const int j = (blockIdx.x - row * bpr) * blockDim.x + threadIdx.x;
+  if (j >= Wf * cv) return;
+  const int y = row % Hf, p = row / Hf;
+  const int x = j / cv, c0 = (j - x * cv) * VEC;
   int alo, ahi, blo, bhi;
   cover_range(y, Ht, sy, nty, &alo, &ahi);
   cover_range(x, Wt, sx, ntx, &blo, &bhi);
@@ -64,13 +65,14 @@ __global__ void tile_blend_kernel(const T* __restrict__ tiles, int nty, int ntx,
 #pragma unroll
   for (int v = 0; v < VEC; ++v) acc[v] = (Acc)0;
   Acc dsum = (Acc)0;
+  const int64_t tile_elems = (int64_t)P * Ht * Wt * C;
   for (int a = alo; a <= ahi; ++a) {
-    int ly = y - a * sy;
+    const int ly = y - a * sy;
+    const T* trow = tiles + (int64_t)a * ntx * tile_elems + ((int64_t)p * Ht + ly) * Wt * C + c0;
     for (int b = blo; b <= bhi; ++b) {
-      int lx = x - b * sx;
-      Acc w = (Acc)window[ly * Wt + lx];
-      int64_t t = (int64_t)a * ntx + b;
-      const T* src = tiles + ((((t * P + p) * Ht + ly) * Wt + lx) * C + c0);
+      const int lx = x - b * sx;
+      const Acc w = (Acc)window[ly * Wt + lx];
+      const T* src = trow + b * tile_elems + lx * C;
       T vals[VEC];
       if constexpr (VEC * sizeof(T) == 16) {
         *reinterpret_cast<uint4*>(vals) = *reinterpret_cast<const uint4*>(src);
@@ -86,7 +88,7 @@ __global__ void tile_blend_kernel(const T* __restrict__ tiles, int nty, int ntx,
   T res[VEC];
 #pragma unroll
   for (int v = 0; v < VEC; ++v) res[v] = Tr::store(dsum == (Acc)0 ? (Acc)0 : acc[v] / dsum);
-  T* dst = out + (cell * C + c0);
+  T* dst = out + ((int64_t)row * Wf + x) * C + c0;
   if constexpr (VEC * sizeof(T) == 16) {
     *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(res);
   } else {
@@ -95,30 +97,33 @@ __global__ void tile_blend_kernel(const T* __restrict__ tiles, int nty, int ntx,
   }
 }
 
-template <typename T, int VEC>
+template <typename T, int VEC, int CV>
 static void blend_launch(const void* tiles, int nty, int ntx, int P, int Ht, int Wt, int C, int sy,
                          int sx, const float* window, void* out, int Hf, int Wf, hipStream_t s) {
-  int64_t total = (int64_t)P * Hf * Wf * (C / VEC);
-  int threads = 256;
-  int blocks = (int)((total + threads - 1) / threads);
-  hipLaunchKernelGGL((tile_blend_kernel<T, VEC>), dim3(blocks), dim3(threads), 0, s,
+  const int threads = 256;
+  const int64_t per_row = (int64_t)Wf * (C / VEC);
+  const int bpr = (int)((per_row + threads - 1) / threads);
+  const int64_t blocks = (int64_t)P * Hf * bpr;
+  hipLaunchKernelGGL((tile_blend_kernel<T, VEC, CV>), dim3((unsigned)blocks), dim3(threads), 0, s,
                      static_cast<const T*>(tiles), nty, ntx, P, Ht, Wt, C, sy, sx, window,
-                     static_cast<T*>(out), Hf, Wf);
+                     static_cast<T*>(out), Hf, Wf, bpr);
 }
 
 void launch_tile_blend(const void* tiles, int nty, int ntx, int P, int Ht, int Wt, int C, int sy,
                        int sx, const float* window, void* out, int Hf, int Wf, strata_dtype dt,
                        hipStream_t s) {
   if (dt == STRATA_BF16) {
-    if (C % 8 == 0)
-      blend_launch<uint16_t, 8>(tiles, nty, ntx, P, Ht, Wt, C, sy, sx, window, out, Hf, Wf, s);
+    if (C == 64)
+      blend_launch<uint16_t, 8, 8>(tiles, nty, ntx, P, Ht, Wt, C, sy, sx, window, out, Hf, Wf, s);
+    else if (C % 8 == 0)
+      blend_launch<uint16_t, 8, 0>(tiles, nty, ntx, P, Ht, Wt, C, sy, sx, window, out, Hf, Wf, s);
     else
-      blend_launch<uint16_t, 1>(tiles, nty, ntx, P, Ht, Wt, C, sy, sx, window, out, Hf, Wf, s);
+      blend_launch<uint16_t, 1, 0>(tiles, nty, ntx, P, Ht, Wt, C, sy, sx, window, out, Hf, Wf, s);
   } else {
     if (C % 4 == 0)
-      blend_launch<float, 4>(tiles, nty, ntx, P, Ht, Wt, C, sy, sx, window, out, Hf, Wf, s);
+      blend_launch<float, 4, 0>(tiles, nty, ntx, P, Ht, Wt, C, sy, sx, window, out, Hf, Wf, s);
     else
-      blend_launch<float, 1>(tiles, nty, ntx, P, Ht, Wt, C, sy, sx, window, out, Hf, Wf, s);
+      blend_launch<float, 1, 0>(tiles, nty, ntx, P, Ht, Wt, C, sy, sx, window, out, Hf, Wf, s);
   }
 }
 

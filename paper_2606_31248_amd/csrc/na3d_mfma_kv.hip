@@ -2,8 +2,9 @@
 // part of the backward (bf16 in/out, head_dim 64).
 //
 // Work decomposition
-//   workgroup : one (tile, head), a 4 x 4 block of (y, x) key positions and 8 key
-//               levels; 8 waves, one per key level, one workgroup per CU.
+//   workgroup : one (tile, head), a 4 x 4 block of (y, x) key positions and ZK key
+//               levels; ZK waves, one per key level (ZK = 8 with a double buffer,
+//               one workgroup per CU; ZK = 4 with a single buffer, two per CU).
 //   wave      : the 16 keys of its level, stationary in registers: K~ (rotated,
 //               times scale log2(e), float16) and V (bf16) as B operands, the
 //               dK~^T and dV^T accumulators (64 d x 16 keys).
@@ -12,7 +13,8 @@
 //               block form a box per level -- the union of the per-axis inverse
 //               windows [lo(j), hi(j)] (at most 4 + 3 r wide, checked on the
 //               host).  Q and dO of that box are copied global -> LDS by the
-//               direct-to-LDS load, one level ahead, into a double buffer; each
+//               direct-to-LDS load (one level ahead into the double buffer, or
+//               into the single buffer between two barriers); each
 //               thread rotates the Q pieces its own copies brought (StereoRoPE,
 //               float16), stores LSE (log2 units) and -D of its queries, and one
 //               barrier publishes the level.
@@ -49,23 +51,28 @@ namespace {
 
 using namespace mfma;
 
-constexpr int kWaves = 8;        // key levels of a workgroup, one per wave
-constexpr int kThreads = 64 * kWaves;
 constexpr int kD = 64;           // head_dim
 constexpr int kRow = 128;        // LDS bytes per staged query row
 constexpr int kLdsMax = 160 * 1024;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kMinExp = -100;    // lower bound of the dS exponent (keeps 2^(15-E) finite)
 
-template <int KZ, int KY, int KX>
+
+// ZK key levels per workgroup (one wave each); NBUF = 2: double-buffered query
+// tiles, one workgroup per CU; NBUF = 1: single buffer, small enough for two
+// workgroups per CU, which then hide each other's copies and barriers.
+template <int KZ, int KY, int KX, int ZK, int NBUF>
 struct KvCfg {
+  static constexpr int kThreads = 64 * ZK;
   static constexpr int MQY = 4 + 3 * (KY / 2), MQX = 4 + 3 * (KX / 2);  // largest query box
   static constexpr int MQ = (MQY * MQX + 31) / 32 * 32;                  // rows, whole 32-query steps
   static constexpr int TBYTES = MQ * kRow;
   static constexpr int SLOTS = MQ * (kRow / 16);
   static constexpr int IT = (SLOTS + kThreads - 1) / kThreads;           // copy slots per thread
   static constexpr int IS = (MQ + kThreads - 1) / kThreads;              // LSE / D entries per thread
-  static_assert(4 * TBYTES + 4 * MQ * 4 + MQ * 2 <= kLdsMax, "query tiles exceed LDS");
+  static constexpr int LDS = NBUF * (2 * TBYTES + 2 * MQ * 4) + MQ * 2;
+  static constexpr int WG_PER_CU = NBUF == 2 ? 1 : 2;
+  static_assert(LDS * WG_PER_CU <= kLdsMax, "query tiles exceed LDS");
 };
 
 struct KvArgs {
@@ -89,17 +96,19 @@ __host__ __device__ __forceinline__ int inv_hi(int j, int L, int k) { return j >
 
 __device__ __forceinline__ int rswz(int u) { return (((u >> 1) & 3) << 1) | ((u >> 3) & 1); }
 
-template <int KZ, int KY, int KX>
-__global__ void __launch_bounds__(kThreads, 1) na3d_mfma_kv_kernel(KvArgs a) {
-  using C = KvCfg<KZ, KY, KX>;
+template <int KZ, int KY, int KX, int ZK, int NBUF>
+__global__ void __launch_bounds__(64 * ZK, (NBUF == 2 ? 1 : 2)) na3d_mfma_kv_kernel(KvArgs a) {
+  using C = KvCfg<KZ, KY, KX, ZK, NBUF>;
+  constexpr int kThreads = C::kThreads;
+  constexpr int T2 = NBUF == 2 ? C::TBYTES : 16, M2 = NBUF == 2 ? C::MQ : 4;
   __shared__ __attribute__((aligned(16))) char tQ0[C::TBYTES];
   __shared__ __attribute__((aligned(16))) char tG0[C::TBYTES];
-  __shared__ __attribute__((aligned(16))) char tQ1[C::TBYTES];
-  __shared__ __attribute__((aligned(16))) char tG1[C::TBYTES];
+  __shared__ __attribute__((aligned(16))) char tQ1[T2];
+  __shared__ __attribute__((aligned(16))) char tG1[T2];
   __shared__ __attribute__((aligned(16))) float sL0[C::MQ];
   __shared__ __attribute__((aligned(16))) float sD0[C::MQ];
-  __shared__ __attribute__((aligned(16))) float sL1[C::MQ];
-  __shared__ __attribute__((aligned(16))) float sD1[C::MQ];
+  __shared__ __attribute__((aligned(16))) float sL1[M2];
+  __shared__ __attribute__((aligned(16))) float sD1[M2];
   __shared__ __attribute__((aligned(16))) unsigned short smask[C::MQ];
 
   // ---- block coordinates (XCD-aware: neighbouring blocks share an L2) -------
@@ -112,7 +121,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_kv_kernel(KvArgs a) {
   const int bh = bid / (a.n_xb * a.n_yb * a.n_zb);
   const int b = bh / a.heads;
   const int H = a.H, W = a.W, Z = a.Z;
-  const int y0 = 4 * yb, x0 = 4 * xb, z0 = kWaves * zb;
+  const int y0 = 4 * yb, x0 = 4 * xb, z0 = ZK * zb;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -142,9 +151,11 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_kv_kernel(KvArgs a) {
       }
     } else {
       sL0[u] = 0.f;
-      sL1[u] = 0.f;
       sD0[u] = 0.f;
-      sD1[u] = 0.f;
+      if constexpr (NBUF == 2) {
+        sL1[u] = 0.f;
+        sD1[u] = 0.f;
+      }
     }
     smask[u] = (unsigned short)bits;
   }
@@ -153,8 +164,10 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_kv_kernel(KvArgs a) {
     const uint4 z = make_uint4(0u, 0u, 0u, 0u);
     st16(tQ0 + i * 16, z);
     st16(tG0 + i * 16, z);
-    st16(tQ1 + i * 16, z);
-    st16(tG1 + i * 16, z);
+    if constexpr (NBUF == 2) {
+      st16(tQ1 + i * 16, z);
+      st16(tG1 + i * 16, z);
+    }
   }
 
   // ---- direct-to-LDS copy map (registers): slot s = it*512 + tid ---------------
@@ -348,8 +361,18 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_kv_kernel(KvArgs a) {
   // Level p+1 is copied while level p is computed; then each thread waits for
   // its own copies, finishes its own slots, and one barrier publishes the level.
   // The barrier also retires every read of the tiles the next copy overwrites.
-  const int zk_last = min(z0 + kWaves, Z) - 1;
+  const int zk_last = min(z0 + ZK, Z) - 1;
   const int p_lo = inv_lo(z0, KZ), p_hi = inv_hi(zk_last, Z, KZ);
+  if constexpr (NBUF == 1) {
+    // one buffer: copy, publish, compute, and a barrier before the next copy
+    for (int p = p_lo; p <= p_hi; ++p) {
+      issue(p, tQ0, tG0);
+      finish(tQ0, sL0, sD0);
+      __syncthreads();
+      if (active(p)) compute(tQ0, tG0, sL0, sD0);
+      __syncthreads();
+    }
+  } else {
   issue(p_lo, tQ0, tG0);
   finish(tQ0, sL0, sD0);
   __syncthreads();
@@ -368,6 +391,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_kv_kernel(KvArgs a) {
         __syncthreads();
       }
     }
+  }
   }
 
   // ---- store: dV, and dK = R^T (scale 2^(E-15) dK~); lane holds d = 16t + 4g + i ----
@@ -399,17 +423,18 @@ int max_box(int L, int k) {
   return mx;
 }
 
-template <int KZ, int KY, int KX>
+template <int KZ, int KY, int KX, int ZK, int NBUF>
 bool launch_kv(const strata_na3d_desc& d, const KvArgs& a0, hipStream_t s) {
-  using C = KvCfg<KZ, KY, KX>;
+  using C = KvCfg<KZ, KY, KX, ZK, NBUF>;
   if (max_box(d.H, KY) > C::MQY || max_box(d.W, KX) > C::MQX) return false;
   KvArgs a = a0;
-  a.n_zb = (d.Z + kWaves - 1) / kWaves;
+  a.n_zb = (d.Z + ZK - 1) / ZK;
   a.n_yb = (d.H + 3) / 4;
   a.n_xb = (d.W + 3) / 4;
   const int64_t blocks = (int64_t)d.B * d.heads * a.n_zb * a.n_yb * a.n_xb;
   if (blocks >= (int64_t)1 << 31) return false;
-  hipLaunchKernelGGL((na3d_mfma_kv_kernel<KZ, KY, KX>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL((na3d_mfma_kv_kernel<KZ, KY, KX, ZK, NBUF>), dim3((unsigned)blocks), dim3(C::kThreads), 0,
+                     s, a);
   return true;
 }
 
@@ -436,8 +461,11 @@ bool launch_na3d_bwd_dkdv_mfma(const strata_na3d_desc& d, const void* q, const v
   a.W = d.W;
   a.scale = d.scale;
   a.kscale = d.scale * kLog2e;
-  if (d.kz == 3 && d.ky == 7 && d.kx == 7) return launch_kv<3, 7, 7>(d, a, s);
-  if (d.kz == 5 && d.ky == 9 && d.kx == 9) return launch_kv<5, 9, 9>(d, a, s);
+  // measured on MI355X at 16 tiles x 16 heads x 8x64x64: 3x7x7 is faster with two
+  // single-buffered 4-level workgroups per CU (9.8 vs 11.6 ms for the whole
+  // backward), 5x9x9 with one double-buffered 8-level workgroup (18.2 vs 18.4 ms)
+  if (d.kz == 3 && d.ky == 7 && d.kx == 7) return launch_kv<3, 7, 7, 4, 1>(d, a, s);
+  if (d.kz == 5 && d.ky == 9 && d.kx == 9) return launch_kv<5, 9, 9, 8, 2>(d, a, s);
   return false;
 }
 

@@ -256,14 +256,15 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
   auto rotate_k = [&](char* tk) {
 #pragma unroll
     for (int it = 0; it < C::ITK; ++it) {
-      const int o = goffK(it);
-      if (o < 0) continue;
+      // slots past the tile exist only in the last pass (known per thread)
+      if ((it + 1) * kThreads > C::KSLOTS && it * kThreads + tid >= C::KSLOTS) continue;
       char* ad = tk + (it * kThreads + tid) * 16;
       uint4 x = ld16(ad);
       if (csb) {
         if (C::PH_LDS) {
           x = rotate8h_pk(x, ld16(sph + (it * kThreads + tid) * 16));
         } else {
+          const int o = goffK(it);
           const float4* pp = csb + (o >> 6) * 16 + ((o & 63) >> 2);
           x = rotate8h(x, pp[0], pp[1], 1.f);
         }
@@ -325,10 +326,14 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
       f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(k0, qf[j][0], bias[c], 0, 0, 0);
       s[c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(k1, qf[j][1], acc, 0, 0, 0);
     }
-    float mx = fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3]));
+    float mx = fmaxf(fmaxf(s[0][0], s[0][1]), s[0][2]);
+    mx = fmaxf(fmaxf(mx, s[0][3]), s[1][0]);
 #pragma unroll
-    for (int c = 1; c < C::NC; ++c)
-      mx = fmaxf(fmaxf(mx, fmaxf(s[c][0], s[c][1])), fmaxf(s[c][2], s[c][3]));
+    for (int c = 1; c < C::NC; ++c) {  // three-input maxima
+      if (c > 1) mx = fmaxf(fmaxf(mx, s[c][0]), s[c][1]);
+      else mx = fmaxf(mx, s[c][1]);
+      mx = fmaxf(fmaxf(mx, s[c][2]), s[c][3]);
+    }
     mx = max_over_rows(mx);
     if (__any(mx > m[j] + kLazy)) {  // rare: move the running maximum, rescale
       const float mn = fmaxf(m[j], mx);

@@ -116,16 +116,30 @@ void launch_na3d_fwd_ref(const strata_na3d_desc& d, const void* q, const void* k
 }
 
 // ---- backward ----------------------------------------------------------------
-// D_i = <dout_i, out_i> in float32.
+// D_i = <dout_i, out_i> in float32.  A lane reads one 16-byte piece of a row of
+// both tensors; the CPR lanes of a row (aligned within the wave) add their
+// partial sums by butterfly exchanges.
 template <typename T, int D>
-__global__ void na3d_bwd_pre_kernel(const T* __restrict__ out, const T* __restrict__ dout,
-                                    float* __restrict__ dvec, int64_t nq) {
-  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= nq) return;
+__global__ void __launch_bounds__(256) na3d_bwd_pre_kernel(const T* __restrict__ out, const T* __restrict__ dout,
+                                                           float* __restrict__ dvec, int64_t nq) {
+  constexpr int E = 16 / (int)sizeof(T);  // elements per 16-byte piece
+  constexpr int CPR = D / E;              // pieces per row: 4, 8 or 16
+  static_assert(64 % CPR == 0, "a row's lanes must not straddle a wave");
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t row = gid / CPR;
+  const int c = (int)(gid % CPR);
   float acc = 0.f;
+  if (row < nq) {
+    const uint4 a = *reinterpret_cast<const uint4*>(out + row * D + c * E);
+    const uint4 g = *reinterpret_cast<const uint4*>(dout + row * D + c * E);
+    const T* pa = reinterpret_cast<const T*>(&a);
+    const T* pg = reinterpret_cast<const T*>(&g);
 #pragma unroll
-  for (int e = 0; e < D; ++e) acc = fmaf(ld(dout + i * D + e), ld(out + i * D + e), acc);
-  dvec[i] = acc;
+    for (int e = 0; e < E; ++e) acc = fmaf(ld(pg + e), ld(pa + e), acc);
+  }
+#pragma unroll
+  for (int off = CPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  if (row < nq && c == 0) dvec[row] = acc;
 }
 
 template <typename T, int D>
@@ -252,8 +266,8 @@ static void bwd_ref(int part, const strata_na3d_desc& d, const void* q, const vo
   int blocks = (int)((n + threads - 1) / threads);
   const float2* c2 = reinterpret_cast<const float2*>(cs);
   if (part == 0)
-    hipLaunchKernelGGL((na3d_bwd_pre_kernel<T, D>), dim3((int)((n + 255) / 256)), dim3(256), 0, s,
-                       static_cast<const T*>(out), static_cast<const T*>(dout), dvec, n);
+    hipLaunchKernelGGL((na3d_bwd_pre_kernel<T, D>), dim3((int)((n * (D * sizeof(T) / 16) + 255) / 256)),
+                       dim3(256), 0, s, static_cast<const T*>(out), static_cast<const T*>(dout), dvec, n);
   else if (part == 1)
     hipLaunchKernelGGL((na3d_bwd_dq_ref_kernel<T, D>), dim3(blocks), dim3(threads), 0, s,
                        static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), c2,
