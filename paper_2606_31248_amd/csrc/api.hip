@@ -149,7 +149,8 @@ strata_status strata_na3d_fwd(const strata_na3d_desc* desc, const void* q, const
   if (cs) REQUIRE(aligned16(cs), "cs: not 16-byte aligned");
   if (lse) REQUIRE(aligned16(lse), "lse: not 16-byte aligned");
   hipStream_t s = (hipStream_t)stream;
-  if (!launch_na3d_fwd_mfma(*desc, q, k, v, cs, out, lse, s))
+  if (!launch_na3d_fwd_zs(*desc, q, k, v, cs, out, lse, s) &&
+      !launch_na3d_fwd_mfma(*desc, q, k, v, cs, out, lse, s))
     launch_na3d_fwd_ref(*desc, q, k, v, cs, out, lse, s);
   return check_launch("strata_na3d_fwd");
 }

@@ -25,6 +25,11 @@ void launch_rope_apply(const void* x, void* y, const float* cs, int B, int heads
 void launch_na3d_fwd_ref(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
                          const float* cs, void* out, float* lse, hipStream_t s);
 
+// bf16 MFMA forward sweeping the key levels once per head (window 3x7x7, Z = 8);
+// returns false for any other problem.
+bool launch_na3d_fwd_zs(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
+                        const float* cs, void* out, float* lse, hipStream_t s);
+
 // bf16 MFMA forward; returns false when the problem has no MFMA variant.
 bool launch_na3d_fwd_mfma(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
                           const float* cs, void* out, float* lse, hipStream_t s);

@@ -1,0 +1,496 @@
+// Neighbourhood-attention forward for gfx950 with a level sweep: window 3 x 7 x 7,
+// Z = 8 levels, head_dim 64, bf16 in/out, StereoRoPE fused into the Q/K loads.
+//
+// Work decomposition
+//   workgroup : one tile, an 8 x 8 block of (y, x) query positions, all Z levels,
+//               and a run of heads processed one after the other; 4 waves (one
+//               per SIMD), one workgroup per CU.  Consecutive heads share every
+//               piece of geometry (key box, window masks, copy offsets, rotary
+//               phases), so it is set up once and the key-level pipeline runs on
+//               from one head into the next without draining.
+//   wave      : a 4 x 4 (y, x) sub-block = 16 queries, on all Z levels.
+//   key sweep : per head the workgroup walks the Z key levels once.  K and V of
+//               the 14 x 14 key box of a level are copied global -> LDS by the
+//               direct-to-LDS load one level ahead of the compute (double
+//               buffer); each thread rotates the K pieces its own copies brought
+//               (StereoRoPE in packed float16, with the float16 phases of the key
+//               box staged once in LDS) and one barrier publishes the level.
+//               Queries are rotated in float32 with float32 phases and the logit
+//               scale times log2 e, then rounded to float16 once: an exact scale
+//               matters, a scale rounded to float16 shifts every logit by up to
+//               2^-11 relative, which moves sharp softmax rows visibly.
+//
+// K rows are 128 bytes with their 16-byte columns XOR-swizzled by
+// ((x >> 1) + 5 y) & 7 of the key's box position (the 16 keys of a chunk hit 16
+// bank groups); V rows are 160 bytes (8 data columns + 2 pad columns), which
+// spreads the transpose reads and lets them take immediate offsets.  Every
+// thread owns 7 K slots and 8 V slots of 16 bytes per level, with their global
+// offsets in registers; the tiles carry the pad slots of the last pass and V's
+// pad columns copy a valid column, so no copy or rotation needs a branch.
+//
+// At key level p a wave reads the K and V fragments of its sub-block's key box
+// from LDS once and applies them to every query level whose window holds p
+// (two to four of them).  Per (query level, key level):
+//   S^T (16 keys x 16 queries) = K . Q^T   two 16x16x32 float16 MFMAs of the
+//                                         rotated, scaled K and the rotated Q,
+//                                         the accumulator seeded with the window
+//                                         mask (0 or -inf);
+//   P = exp2(S^T - m) packed to bf16 in place, row sums with v_dot2c_f32_bf16;
+//   O^T (64 d x 16 queries) += V^T . P^T  bf16 MFMA, V^T fragments by the LDS
+//                                         transpose read.
+// The reference m starts at 0 for every query and moves only when a logit
+// exceeds it by more than 2^4 (O and the row sum are then rescaled), or when
+// the first key level of a query level has no logit above -2^6 (nothing is
+// accumulated yet).  P is bf16 with float32's exponent range, so exp2(S - m)
+// neither overflows nor loses relevant weights; while m is 0 for the whole
+// wave (the common case for logits of moderate size) no subtraction is done.
+// Every accumulator chain uses one MFMA shape only (the last 16-key chunk of
+// the P.V product is padded with zero weights rather than switching to a
+// 16x16x16 MFMA): gfx950 gives wrong sums when an accumulator is handed from
+// one MFMA shape to another without wait states, which the compiler does not
+// insert.
+//
+// Input range: K is converted to float16 with round-toward-zero before its
+// rotation (bf16 values convert exactly; beyond +-65504 they saturate); the
+// rotated, scaled Q saturates at +-65504.
+#include "common.h"
+#include "kernels.h"
+#include "mfma_util.h"
+
+namespace strata {
+namespace {
+
+using namespace mfma;
+
+constexpr int kThreads = 256;
+constexpr int KZ = 3, KY = 7, KX = 7;
+constexpr int kBY = 8, kBX = 8;
+constexpr int kD = 64;
+constexpr int LY = kBY + KY - 1, LX = kBX + KX - 1;       // staged key box per level (14 x 14)
+constexpr int NUY = 3 + KY, NUX = 3 + KX, NU = NUY * NUX;  // key box of a 4x4 sub-block (10 x 10)
+constexpr int NC = (NU + 15) / 16;                         // 16-key chunks (7)
+constexpr int NS = (NC + 1) / 2;                           // 32-key P.V steps (4)
+constexpr int KEYS = LY * LX;
+constexpr int kKRow = 128, kVRow = 160;                    // LDS bytes per key row
+constexpr int KSLOTS = KEYS * (kKRow / 16), VSLOTS = KEYS * (kVRow / 16);  // 16-byte slots
+constexpr int ITK = (KSLOTS + kThreads - 1) / kThreads;    // K slots per thread (7)
+constexpr int ITV = (VSLOTS + kThreads - 1) / kThreads;    // V slots per thread (8)
+constexpr int KTILE = ITK * kThreads * 16;                 // tile bytes incl. pad slots
+constexpr int VTILE = ITV * kThreads * 16;
+constexpr float kLazy = 16.0f;    // m moves up when a logit exceeds it by 2^4
+constexpr float kLow = -64.0f;    // ... or down, on a level's first key level
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kLog2e = 1.4426950408889634f;
+
+static_assert(3 * KTILE + 2 * VTILE <= 160 * 1024, "LDS budget");
+
+template <int I>
+struct IC {
+  static constexpr int v = I;
+};
+template <int N, int I = 0, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(IC<I>{});
+    static_for<N, I + 1>(f);
+  }
+}
+
+// first key level of query level z (border-clamped window along the levels)
+template <int Z>
+__host__ __device__ constexpr int zstart(int z) {
+  return z - KZ / 2 < 0 ? 0 : (z - KZ / 2 > Z - KZ ? Z - KZ : z - KZ / 2);
+}
+// query levels whose window holds key level p: the consecutive range [zlo, zhi]
+template <int Z>
+__host__ __device__ constexpr int zlo(int p) {
+  int z = 0;
+  while (zstart<Z>(z) + KZ <= p) ++z;
+  return z;
+}
+template <int Z>
+__host__ __device__ constexpr int zhi(int p) {
+  int z = Z - 1;
+  while (zstart<Z>(z) > p) --z;
+  return z;
+}
+
+struct ZArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const float4* cs;   // [B, H, W, 16] float4 = two (cos, sin) pairs; nullptr: no rotation
+  uint16_t* out;
+  float* lse;         // optional
+  int heads, H, W;
+  int n_yb, n_xb, n_hg, hpw;
+  float qscale;       // scale * log2(e)
+};
+
+// Rotate 4 pairs of K held as packed bf16x2 words by packed float16 phases
+// (c, s): round-toward-zero to float16 (exact for bf16 values inside the
+// float16 range, saturating outside it), then in packed float16, the products
+// taking the halves of the phase word through the operand selects,
+//   t = (a c, a s),   r = (b, b) * (s, c) * (-1, 1) + t = (a c - b s, a s + b c).
+__device__ __forceinline__ uint4 rotate_k8(uint4 x, uint4 ph) {
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  const uint32_t p[4] = {ph.x, ph.y, ph.z, ph.w};
+  uint32_t r[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const uint32_t ab = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(lo_bf16(w[t]), hi_bf16(w[t])));
+    uint32_t tt;
+    asm volatile("v_pk_mul_f16 %0, %1, %2 op_sel_hi:[0,1]" : "=v"(tt) : "v"(ab), "v"(p[t]));
+    asm volatile("v_pk_fma_f16 %0, %1, %2, %3 op_sel:[1,1,0] op_sel_hi:[1,0,1] neg_lo:[0,1,0]"
+                 : "=v"(r[t]) : "v"(ab), "v"(p[t]), "v"(tt));
+  }
+  return make_uint4(r[0], r[1], r[2], r[3]);
+}
+
+template <int Z>
+__global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
+  __shared__ __attribute__((aligned(16))) char tK0[KTILE];
+  __shared__ __attribute__((aligned(16))) char tV0[VTILE];
+  __shared__ __attribute__((aligned(16))) char tK1[KTILE];
+  __shared__ __attribute__((aligned(16))) char tV1[VTILE];
+  __shared__ __attribute__((aligned(16))) char sph[KTILE];
+
+  // ---- block coordinates (XCD-aware: neighbouring blocks share an L2) -------
+  const int nblk = gridDim.x;
+  int bid = blockIdx.x;
+  if ((nblk & 7) == 0) bid = (bid & 7) * (nblk >> 3) + (bid >> 3);
+  const int xb = bid % a.n_xb;
+  const int yb = (bid / a.n_xb) % a.n_yb;
+  const int hg = (bid / (a.n_xb * a.n_yb)) % a.n_hg;
+  const int b = bid / (a.n_xb * a.n_yb * a.n_hg);
+  const int h_lo = hg * a.hpw;
+  const int h_hi = min(h_lo + a.hpw, a.heads);
+  const int H = a.H, W = a.W;
+  const int64_t HW = (int64_t)H * W;
+  const int by0 = yb * kBY, bx0 = xb * kBX;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 4, qn = lane & 15;
+
+  const int ty0 = win_start(min(by0, H - 1), H, KY);
+  const int tx0 = win_start(min(bx0, W - 1), W, KX);
+  const int sy0 = by0 + 4 * (wave >> 1), sx0 = bx0 + 4 * (wave & 1);
+  const int uy0 = win_start(min(sy0, H - 1), H, KY);
+  const int ux0 = win_start(min(sx0, W - 1), W, KX);
+  const int qy_raw = sy0 + (qn >> 2), qx_raw = sx0 + (qn & 3);
+  const int qy = min(qy_raw, H - 1), qx = min(qx_raw, W - 1);
+  const bool in_grid = qy_raw < H && qx_raw < W;
+
+  auto kswz = [&](int key) { return ((key % LX >> 1) + 5 * (key / LX)) & 7; };
+  auto key_row = [&](int u) {
+    return u < NU ? (uy0 - ty0 + u / NUX) * LX + (ux0 - tx0 + u % NUX) : 0;
+  };
+
+  // ---- LDS addresses of this lane's fragments and its window mask ----------
+  const int wys = win_start(qy, H, KY), wxs = win_start(qx, W, KX);
+  uint32_t kaddr[NC], vaddr[NC];
+  f32x4 bias[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    {  // K fragment (A operand): row = key 16c + qn, 16 bytes at column g (xor 64 bytes: g+4)
+      const int key = key_row(16 * c + qn);
+      kaddr[c] = key * kKRow + ((g ^ kswz(key)) << 4);
+    }
+    // V^T transpose read: row = key 16c + 4g + qn/4, 8 bytes at d = 4 (qn % 4) (+ 32 t: + 16 t)
+    vaddr[c] = key_row(16 * c + 4 * g + (qn >> 2)) * kVRow + (qn & 3) * 8;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int u = 16 * c + 4 * g + i;
+      const int ky = uy0 + u / NUX, kx = ux0 + u % NUX;
+      const bool ok = u < NU && ky >= wys && ky < wys + KY && kx >= wxs && kx < wxs + KX;
+      bias[c][i] = ok ? 0.f : -INFINITY;
+    }
+  }
+
+  // ---- copy offsets (bytes inside a key level) and the rotary phases of this --
+  // ---- thread's K slots ------------------------------------------------------
+  const float4* csb = a.cs ? a.cs + (int64_t)b * HW * 16 : nullptr;
+  auto pos_of = [&](int key) {  // grid position of a staged key (rows past the grid repeat the last)
+    return min(ty0 + key / LX, H - 1) * W + min(tx0 + key % LX, W - 1);
+  };
+  uint32_t koff[ITK], voff[ITV];
+#pragma unroll
+  for (int it = 0; it < ITK; ++it) {
+    const int s = it * kThreads + tid;
+    const int key = min(s >> 3, KEYS - 1);  // pad slots copy a valid row into the pad
+    const int c = (s & 7) ^ kswz(key);
+    const int pos = pos_of(key);
+    koff[it] = (uint32_t)(pos * kD + c * 8) * 2u;
+    uint4 ph;
+    if (csb) {
+      const float4* pp = csb + (int64_t)pos * 16 + 2 * c;
+      const float4 p0 = pp[0], p1 = pp[1];
+      ph = make_uint4(pack2h(p0.x, p0.y), pack2h(p0.z, p0.w), pack2h(p1.x, p1.y), pack2h(p1.z, p1.w));
+    } else {
+      const uint32_t one = pack2h(1.f, 0.f);
+      ph = make_uint4(one, one, one, one);
+    }
+    st16(sph + s * 16, ph);
+  }
+#pragma unroll
+  for (int it = 0; it < ITV; ++it) {
+    const int s = it * kThreads + tid;
+    const int key = min(s / 10, KEYS - 1);
+    const int c = s % 10 < 8 ? s % 10 : 0;  // pad columns copy column 0
+    voff[it] = (uint32_t)(pos_of(key) * kD + c * 8) * 2u;
+  }
+  // float32 phases of this lane's query position (pairs 4g..4g+3 and 16+4g..)
+  const float4* csq = csb ? csb + ((int64_t)qy * W + qx) * 16 : nullptr;
+
+  auto level_base = [&](int h, int p) { return (((int64_t)b * a.heads + h) * Z + p) * HW; };
+  auto issue_copy = [&](int64_t base, char* tk, char* tv) {
+    const char* kp = reinterpret_cast<const char*>(a.k + base * kD);
+    const char* vp = reinterpret_cast<const char*>(a.v + base * kD);
+#pragma unroll
+    for (int it = 0; it < ITK; ++it)
+      copy16_to_lds(reinterpret_cast<const uint16_t*>(kp + koff[it]), tk + (it * kThreads + wave * 64) * 16);
+#pragma unroll
+    for (int it = 0; it < ITV; ++it)
+      copy16_to_lds(reinterpret_cast<const uint16_t*>(vp + voff[it]), tv + (it * kThreads + wave * 64) * 16);
+  };
+  // Rotate this thread's K slots in place (bf16 -> scaled float16).  A thread's
+  // copies land in its own slots, so its own wait suffices.
+  auto rotate_k = [&](char* tk) {
+#pragma unroll
+    for (int it = 0; it < ITK; ++it) {
+      char* ad = tk + (it * kThreads + tid) * 16;
+      st16(ad, rotate_k8(ld16(ad), ld16(sph + (it * kThreads + tid) * 16)));
+    }
+  };
+  // raw query rows of one level (two 16-byte pieces per lane)
+  auto load_q = [&](int h, int z, uint4& x0, uint4& x1) {
+    const uint4* src = reinterpret_cast<const uint4*>(a.q + (level_base(h, z) + (int64_t)qy * W + qx) * kD);
+    x0 = src[g];
+    x1 = src[4 + g];
+  };
+  auto prep_q = [&](const float4* cq, uint4 x0, uint4 x1, f16x8& q0, f16x8& q1) {
+    uint4 r0, r1;
+    if (cq) {
+      r0 = rotate8h(x0, cq[2 * g], cq[2 * g + 1], a.qscale);
+      r1 = rotate8h(x1, cq[8 + 2 * g], cq[8 + 2 * g + 1], a.qscale);
+    } else {
+      r0 = scale8h(x0, a.qscale);
+      r1 = scale8h(x1, a.qscale);
+    }
+    q0 = __builtin_bit_cast(f16x8, r0);
+    q1 = __builtin_bit_cast(f16x8, r1);
+  };
+
+  // per query level state (only the levels whose window holds the current key
+  // level are live at any time)
+  f16x8 qf[Z][2];
+  float m[Z], l[Z];
+  bool mset[Z];     // wave-uniform: m is non-zero somewhere in the wave
+  f32x4 o[Z][4];
+  uint4 qraw[Z][2];
+
+  // K and V fragments of one key level (shared by every active query level)
+  struct Frags {
+    f16x8 k[NC][2];
+    bf16x8 v[NS][4];
+  };
+  auto load_frags = [&](const char* tk, const char* tv, Frags& f) {
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      f.k[c][0] = __builtin_bit_cast(f16x8, ld16(tk + kaddr[c]));
+      f.k[c][1] = __builtin_bit_cast(f16x8, ld16(tk + (kaddr[c] ^ 64u)));
+    }
+#pragma unroll
+    for (int st = 0; st < NS; ++st) {
+      const int c0 = 2 * st, c1 = 2 * st + 1;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const i16x4 lo = tr_read(tv + vaddr[c0] + 32 * t);
+        const i16x4 hi = c1 < NC ? tr_read(tv + vaddr[c1 < NC ? c1 : c0] + 32 * t) : i16x4{0, 0, 0, 0};
+        const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
+        f.v[st][t] = __builtin_bit_cast(bf16x8, make_uint4(l2.x, l2.y, h2.x, h2.y));
+      }
+    }
+  };
+
+  // one query level z at key level p
+  auto update = [&](auto P, auto Zi, const Frags& f) {
+    constexpr int p = decltype(P)::v, z = decltype(Zi)::v;
+    constexpr bool first = zstart<Z>(z) == p;
+    f32x4 s[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(f.k[c][0], qf[z][0], bias[c], 0, 0, 0);
+      s[c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(f.k[c][1], qf[z][1], acc, 0, 0, 0);
+    }
+    float mx = fmaxf(fmaxf(s[0][0], s[0][1]), s[0][2]);
+    mx = fmaxf(fmaxf(mx, s[0][3]), s[1][0]);
+#pragma unroll
+    for (int c = 1; c < NC; ++c) {
+      if (c > 1) mx = fmaxf(fmaxf(mx, s[c][0]), s[c][1]);
+      else mx = fmaxf(mx, s[c][1]);
+      mx = fmaxf(fmaxf(mx, s[c][2]), s[c][3]);
+    }
+    mx = max_over_rows(mx);
+    const bool move = mx > m[z] + kLazy || (first && mx < kLow);
+    if (__any(move)) {  // rare: move the reference m
+      const float mn = move ? mx : m[z];
+      if constexpr (!first) {  // nothing is accumulated before a level's first key level
+        const float alpha = __builtin_amdgcn_exp2f(m[z] - mn);
+        l[z] *= alpha;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) o[z][t] *= alpha;
+      }
+      m[z] = mn;
+      mset[z] = true;
+    }
+    if (mset[z]) {
+#pragma unroll
+      for (int c = 0; c < NC; ++c) s[c] -= m[z];
+    }
+    uint32_t pk[NC][2];
+    float ls = l[z];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      pk[c][0] = pack2(__builtin_amdgcn_exp2f(s[c][0]), __builtin_amdgcn_exp2f(s[c][1]));
+      pk[c][1] = pack2(__builtin_amdgcn_exp2f(s[c][2]), __builtin_amdgcn_exp2f(s[c][3]));
+      ls = psum8(pk[c][0], pk[c][1], ls);
+    }
+    l[z] = ls;
+#pragma unroll
+    for (int st = 0; st < NS; ++st) {
+      const int c0 = 2 * st, c1 = 2 * st + 1;
+      const uint32_t p2 = c1 < NC ? pk[c1 < NC ? c1 : c0][0] : 0u;
+      const uint32_t p3 = c1 < NC ? pk[c1 < NC ? c1 : c0][1] : 0u;
+      const bf16x8 pf = __builtin_bit_cast(bf16x8, make_uint4(pk[c0][0], pk[c0][1], p2, p3));
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        o[z][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.v[st][t], pf, o[z][t], 0, 0, 0);
+    }
+  };
+
+  // ---- prologue: key level 0 of the first head, queries of its first levels --
+  issue_copy(level_base(h_lo, 0), tK0, tV0);
+  static_for<Z>([&](auto Zi) {
+    constexpr int z = decltype(Zi)::v;
+    if constexpr (zstart<Z>(z) == 0) load_q(h_lo, z, qraw[z][0], qraw[z][1]);
+  });
+  __builtin_amdgcn_s_waitcnt(0);
+  rotate_k(tK0);
+  __syncthreads();
+
+  for (int h = h_lo; h < h_hi; ++h) {
+    const bool more_heads = h + 1 < h_hi;
+    static_for<Z>([&](auto Pi) {
+      constexpr int p = decltype(Pi)::v;
+      char* const tk = (p & 1) ? tK1 : tK0;
+      char* const tv = (p & 1) ? tV1 : tV0;
+      char* const nk = (p & 1) ? tK0 : tK1;
+      char* const nv = (p & 1) ? tV0 : tV1;
+      const bool has_next = p + 1 < Z || more_heads;
+      // Addresses derived from these per-lane constants are recomputed at every
+      // key level (a few adds) instead of being kept live across the whole
+      // sweep, which would crowd out the registers of the attention itself.
+#pragma unroll
+      for (int c = 0; c < NC; ++c) asm volatile("" : "+v"(kaddr[c]), "+v"(vaddr[c]));
+#pragma unroll
+      for (int it = 0; it < ITK; ++it) asm volatile("" : "+v"(koff[it]));
+#pragma unroll
+      for (int it = 0; it < ITV; ++it) asm volatile("" : "+v"(voff[it]));
+      // stage the next key level (this head's p+1, or the next head's level 0)
+      if constexpr (p + 1 < Z) issue_copy(level_base(h, p + 1), nk, nv);
+      else if (more_heads) issue_copy(level_base(h + 1, 0), nk, nv);
+
+      // queries of the levels that start here: rotate the rows loaded earlier (the
+      // phase pointer is made opaque so that the phase loads stay here instead of
+      // being held in registers across the whole sweep)
+      const float4* cq = csq;
+      asm volatile("" : "+v"(cq));
+      static_for<Z>([&](auto Zi) {
+        constexpr int z = decltype(Zi)::v;
+        if constexpr (zstart<Z>(z) == p) {
+          prep_q(cq, qraw[z][0], qraw[z][1], qf[z][0], qf[z][1]);
+          m[z] = 0.f;
+          l[z] = 0.f;
+          mset[z] = false;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) o[z][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+      });
+      // prefetch the query rows of the levels that start at the next key level
+      static_for<Z>([&](auto Zi) {
+        constexpr int z = decltype(Zi)::v;
+        if constexpr (p + 1 < Z && zstart<Z>(z) == p + 1) load_q(h, z, qraw[z][0], qraw[z][1]);
+        if constexpr (p + 1 == Z && zstart<Z>(z) == 0)
+          if (more_heads) load_q(h + 1, z, qraw[z][0], qraw[z][1]);
+      });
+
+      // ---- the active query levels [zlo, zhi], sharing this level's fragments -
+      {
+        Frags f;
+        load_frags(tk, tv, f);
+        static_for<Z>([&](auto Zi) {
+          constexpr int z = decltype(Zi)::v;
+          if constexpr (zlo<Z>(p) <= z && z <= zhi<Z>(p)) update(IC<p>{}, Zi, f);
+        });
+      }
+
+      // ---- query levels whose last key level this was: normalise and store ---
+      static_for<Z>([&](auto Zi) {
+        constexpr int z = decltype(Zi)::v;
+        if constexpr (zstart<Z>(z) + KZ - 1 == p) {
+          const float lt = sum_over_rows(l[z]);
+          if (in_grid) {
+            const float inv = 1.f / lt;
+            const int64_t tok = level_base(h, z) + (int64_t)qy * W + qx;
+            uint2* dst = reinterpret_cast<uint2*>(a.out + tok * kD);
+#pragma unroll
+            for (int t = 0; t < 4; ++t)  // d = 16t + 4g + i
+              dst[4 * t + g] = make_uint2(pack2(o[z][t][0] * inv, o[z][t][1] * inv),
+                                          pack2(o[z][t][2] * inv, o[z][t][3] * inv));
+            if (a.lse && g == 0) a.lse[tok] = (m[z] + __log2f(lt)) * kLn2;
+          }
+        }
+      });
+
+      if (has_next) {
+        __builtin_amdgcn_s_waitcnt(0);
+        rotate_k(nk);
+      }
+      __syncthreads();
+    });
+  }
+}
+
+}  // namespace
+
+// Level-sweep forward for the 3x7x7 window at Z = 8 (bf16, head_dim 64); false
+// when the problem is not that shape.
+bool launch_na3d_fwd_zs(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
+                        const float* cs, void* out, float* lse, hipStream_t s) {
+  if (d.dtype != STRATA_BF16 || d.head_dim != kD) return false;
+  if (d.kz != KZ || d.ky != KY || d.kx != KX || d.Z != 8) return false;
+  if ((int64_t)d.H * d.W * kD * 2 >= (int64_t)1 << 32) return false;  // byte offsets in 32 bits
+  ZArgs a = {};
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.cs = reinterpret_cast<const float4*>(cs);
+  a.out = static_cast<uint16_t*>(out);
+  a.lse = lse;
+  a.heads = d.heads;
+  a.H = d.H;
+  a.W = d.W;
+  a.n_yb = (d.H + kBY - 1) / kBY;
+  a.n_xb = (d.W + kBX - 1) / kBX;
+  a.hpw = d.heads < 8 ? d.heads : 8;
+  a.n_hg = (d.heads + a.hpw - 1) / a.hpw;
+  a.qscale = d.scale * kLog2e;
+  const int64_t blocks = (int64_t)d.B * a.n_hg * a.n_yb * a.n_xb;
+  if (blocks >= (int64_t)1 << 31) return false;
+  hipLaunchKernelGGL((na3d_fwd_zs_kernel<8>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
+  return true;
+}
+
+}  // namespace strata

@@ -128,6 +128,8 @@ def test_fwd_tiny_f32_full():
     ((1, 2, 6, 24, 24, 64), (5, 9, 9)),
     ((2, 2, 3, 16, 12, 32), (3, 5, 7)),
     ((1, 1, 8, 32, 32, 64), (3, 7, 7)),
+    ((2, 3, 8, 19, 21, 64), (3, 7, 7)),     # level-sweep kernel, ragged blocks
+    ((1, 11, 8, 16, 24, 64), (3, 7, 7)),    # level-sweep kernel, ragged head group
     ((1, 2, 4, 9, 9, 64), (1, 9, 9)),       # window = whole plane
 ])
 @pytest.mark.parametrize("rope", [True, False])
@@ -183,11 +185,11 @@ def test_fwd_full_size_sampled(wl):
     assert torch.max(torch.abs(o)).item() <= vmax * (1 + 2.0 ** -7)
 
 
-def test_fwd_one_hot_probe_membership_bit_exact():
+@pytest.mark.parametrize("Z,H,W,window", [(6, 20, 23, (3, 7, 5)), (8, 20, 23, (3, 7, 7))])
+def test_fwd_one_hot_probe_membership_bit_exact(Z, H, W, window):
     """Q = K = 0, V one-hot on 64 probe tokens: outputs are non-zero exactly where
     the probe lies in the query's window (membership compared bit for bit)."""
-    Z, H, W, d = 6, 20, 23, 64
-    window = (3, 7, 5)
+    d = 64
     shape = (1, 2, Z, H, W, d)
     N = Z * H * W
     r = np.random.default_rng(5)
@@ -206,6 +208,19 @@ def test_fwd_one_hot_probe_membership_bit_exact():
     got = host_f64(out)
     assert np.array_equal(got != 0, ro != 0)
     check_close(got, ro, "bf16", "probe")
+
+
+@pytest.mark.parametrize("scale", [0.5, 1.0])
+def test_fwd_large_logits_move_the_maximum(scale):
+    """Logit spread of ~6-12 log2 units per key level: the running maximum moves
+    between key levels (rescaling O and the row sums) for many queries."""
+    shape = (1, 2, 8, 24, 24, 64)
+    pl = I.random_placement(1, 24, 24, 17)
+    c32 = oracle_coords(pl, 24, 24)
+    (q, k, v), out, lse, _ = run_fwd(shape, (3, 7, 7), "bf16", 33, c32, scale=scale)
+    ro, rl = oracle.na3d_fwd(*(oracle.widen(a, "bf16") for a in (q, k, v)), (3, 7, 7), scale, coords=c32)
+    check_close(host_f64(out), ro, "bf16", "out")
+    assert np.max(np.abs(host_f64(lse) - rl)) <= LSE_ABS_BF16
 
 
 def test_fwd_deterministic_and_lse_optional():
