@@ -12,9 +12,11 @@
 //   key sweep : per head the workgroup walks the Z key levels once.  K and V of
 //               the 14 x 14 key box of a level are copied global -> LDS by the
 //               direct-to-LDS load one level ahead of the compute (double
-//               buffer); each thread rotates the K pieces its own copies brought
-//               (StereoRoPE in packed float16, with the float16 phases of the key
-//               box staged once in LDS) and one barrier publishes the level.
+//               buffer; the copies are spread over the first two query levels
+//               of the current key level); once its query levels are issued, each thread waits for its own copies and rotates the K
+//               pieces they brought (StereoRoPE in packed float16, with the float16
+//               phases of the key box staged once in LDS); the barrier at the end
+//               of the key level publishes the next one.
 //               Queries are rotated in float32 with float32 phases and the logit
 //               scale times log2 e, then rounded to float16 once: an exact scale
 //               matters, a scale rounded to float16 shifts every logit by up to
@@ -83,6 +85,7 @@ constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kLog2e = 1.4426950408889634f;
 
 static_assert(3 * KTILE + 2 * VTILE <= 160 * 1024, "LDS budget");
+static_assert(ITK <= NC + 1 && ITV <= NC + 1, "copies are spread over the chunks of two query levels");
 
 template <int I>
 struct IC {
@@ -140,9 +143,9 @@ __device__ __forceinline__ uint4 rotate_k8(uint4 x, uint4 ph) {
   for (int t = 0; t < 4; ++t) {
     const uint32_t ab = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(lo_bf16(w[t]), hi_bf16(w[t])));
     uint32_t tt;
-    asm volatile("v_pk_mul_f16 %0, %1, %2 op_sel_hi:[0,1]" : "=v"(tt) : "v"(ab), "v"(p[t]));
-    asm volatile("v_pk_fma_f16 %0, %1, %2, %3 op_sel:[1,1,0] op_sel_hi:[1,0,1] neg_lo:[0,1,0]"
-                 : "=v"(r[t]) : "v"(ab), "v"(p[t]), "v"(tt));
+    asm("v_pk_mul_f16 %1, %2, %3 op_sel_hi:[0,1]\n\t"
+        "v_pk_fma_f16 %0, %2, %3, %1 op_sel:[1,1,0] op_sel_hi:[1,0,1] neg_lo:[0,1,0]"
+        : "=v"(r[t]), "=&v"(tt) : "v"(ab), "v"(p[t]));
   }
   return make_uint4(r[0], r[1], r[2], r[3]);
 }
@@ -257,11 +260,12 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
   // Rotate this thread's K slots in place (bf16 -> scaled float16).  A thread's
   // copies land in its own slots, so its own wait suffices.
   auto rotate_k = [&](char* tk) {
+    uint4 x[ITK];  // all reads before any write: the slots are distinct, which the compiler cannot tell
 #pragma unroll
-    for (int it = 0; it < ITK; ++it) {
-      char* ad = tk + (it * kThreads + tid) * 16;
-      st16(ad, rotate_k8(ld16(ad), ld16(sph + (it * kThreads + tid) * 16)));
-    }
+    for (int it = 0; it < ITK; ++it) x[it] = ld16(tk + (it * kThreads + tid) * 16);
+#pragma unroll
+    for (int it = 0; it < ITK; ++it)
+      st16(tk + (it * kThreads + tid) * 16, rotate_k8(x[it], ld16(sph + (it * kThreads + tid) * 16)));
   };
   // raw query rows of one level (two 16-byte pieces per lane)
   auto load_q = [&](int h, int z, uint4& x0, uint4& x1) {
@@ -315,15 +319,21 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
   };
 
   // one query level z at key level p
-  auto update = [&](auto P, auto Zi, const Frags& f) {
+  // `hook(c)` runs beside the logits of chunk c (c = 0..NC, the last one after
+  // the chunk loop): the next level's copies are spread over the first two
+  // query levels this way, since a burst of them stalls the issuing wave
+  // until the memory pipeline has taken them all.
+  auto update = [&](auto P, auto Zi, const Frags& f, auto&& hook) {
     constexpr int p = decltype(P)::v, z = decltype(Zi)::v;
     constexpr bool first = zstart<Z>(z) == p;
     f32x4 s[NC];
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
+      hook(c);
       const f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(f.k[c][0], qf[z][0], bias[c], 0, 0, 0);
       s[c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(f.k[c][1], qf[z][1], acc, 0, 0, 0);
     }
+    hook(NC);
     float mx = fmaxf(fmaxf(s[0][0], s[0][1]), s[0][2]);
     mx = fmaxf(fmaxf(mx, s[0][3]), s[1][0]);
 #pragma unroll
@@ -398,9 +408,11 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
       for (int it = 0; it < ITK; ++it) asm volatile("" : "+v"(koff[it]));
 #pragma unroll
       for (int it = 0; it < ITV; ++it) asm volatile("" : "+v"(voff[it]));
-      // stage the next key level (this head's p+1, or the next head's level 0)
-      if constexpr (p + 1 < Z) issue_copy(level_base(h, p + 1), nk, nv);
-      else if (more_heads) issue_copy(level_base(h + 1, 0), nk, nv);
+      // the next key level (this head's p+1, or the next head's level 0) is
+      // staged by copies spread over the first two query levels below
+      const int64_t nbase = p + 1 < Z ? level_base(h, p + 1) : level_base(h + 1, 0);
+      const char* const nkp = reinterpret_cast<const char*>(a.k + nbase * kD);
+      const char* const nvp = reinterpret_cast<const char*>(a.v + nbase * kD);
 
       // queries of the levels that start here: rotate the rows loaded earlier (the
       // phase pointer is made opaque so that the phase loads stay here instead of
@@ -427,12 +439,31 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
       });
 
       // ---- the active query levels [zlo, zhi], sharing this level's fragments -
+      // After the last of them, wait for the next level's copies (issued at the
+      // start of this level) and rotate its K slots; the rotation can run beside
+      // the tail of this level's MFMA work.
       {
         Frags f;
         load_frags(tk, tv, f);
         static_for<Z>([&](auto Zi) {
           constexpr int z = decltype(Zi)::v;
-          if constexpr (zlo<Z>(p) <= z && z <= zhi<Z>(p)) update(IC<p>{}, Zi, f);
+          if constexpr (zlo<Z>(p) <= z && z <= zhi<Z>(p)) {
+            update(IC<p>{}, Zi, f, [&](int c) {
+              if constexpr (z == zlo<Z>(p)) {  // K copies
+                if (has_next && c < ITK)
+                  copy16_to_lds(reinterpret_cast<const uint16_t*>(nkp + koff[c]), nk + (c * kThreads + wave * 64) * 16);
+              } else if constexpr (z == zlo<Z>(p) + 1) {  // V copies
+                if (has_next && c < ITV)
+                  copy16_to_lds(reinterpret_cast<const uint16_t*>(nvp + voff[c]), nv + (c * kThreads + wave * 64) * 16);
+              }
+            });
+            if constexpr (z == zhi<Z>(p)) {
+              if (has_next) {
+                __builtin_amdgcn_s_waitcnt(0);
+                rotate_k(nk);
+              }
+            }
+          }
         });
       }
 
@@ -454,10 +485,6 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
         }
       });
 
-      if (has_next) {
-        __builtin_amdgcn_s_waitcnt(0);
-        rotate_k(nk);
-      }
       __syncthreads();
     });
   }
