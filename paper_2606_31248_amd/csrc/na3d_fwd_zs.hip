@@ -37,9 +37,13 @@
 //                                         rotated, scaled K and the rotated Q,
 //                                         the accumulator seeded with the window
 //                                         mask (0 or -inf);
-//   P = exp2(S^T - m) packed to bf16 in place, row sums with v_dot2c_f32_bf16;
+//   P = exp2(S^T - m) packed to bf16 in place;
 //   O^T (64 d x 16 queries) += V^T . P^T  bf16 MFMA, V^T fragments by the LDS
-//                                         transpose read.
+//                                         transpose read;
+//   L (16 x 16 queries)     += 1 . P^T    the row sums, by one more bf16 MFMA
+//                                         against a tile of ones (every row of
+//                                         L holds the sum, so each lane has its
+//                                         query's sum without a reduction).
 // The reference m starts at 0 for every query and moves only when a logit
 // exceeds it by more than 2^4 (O and the row sum are then rescaled), or when
 // the first key level of a query level has no logit above -2^6 (nothing is
@@ -289,7 +293,9 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
   // per query level state (only the levels whose window holds the current key
   // level are live at any time)
   f16x8 qf[Z][2];
-  float m[Z], l[Z];
+  float m[Z];
+  f32x4 lsum[Z];    // row sums (all four entries equal)
+  const bf16x8 ones = __builtin_bit_cast(bf16x8, make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u));
   bool mset[Z];     // wave-uniform: m is non-zero somewhere in the wave
   f32x4 o[Z][4];
   uint4 qraw[Z][2];
@@ -348,7 +354,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
       const float mn = move ? mx : m[z];
       if constexpr (!first) {  // nothing is accumulated before a level's first key level
         const float alpha = __builtin_amdgcn_exp2f(m[z] - mn);
-        l[z] *= alpha;
+        lsum[z] *= alpha;
 #pragma unroll
         for (int t = 0; t < 4; ++t) o[z][t] *= alpha;
       }
@@ -360,14 +366,11 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
       for (int c = 0; c < NC; ++c) s[c] -= m[z];
     }
     uint32_t pk[NC][2];
-    float ls = l[z];
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       pk[c][0] = pack2(__builtin_amdgcn_exp2f(s[c][0]), __builtin_amdgcn_exp2f(s[c][1]));
       pk[c][1] = pack2(__builtin_amdgcn_exp2f(s[c][2]), __builtin_amdgcn_exp2f(s[c][3]));
-      ls = psum8(pk[c][0], pk[c][1], ls);
     }
-    l[z] = ls;
 #pragma unroll
     for (int st = 0; st < NS; ++st) {
       const int c0 = 2 * st, c1 = 2 * st + 1;
@@ -377,6 +380,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
 #pragma unroll
       for (int t = 0; t < 4; ++t)
         o[z][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.v[st][t], pf, o[z][t], 0, 0, 0);
+      lsum[z] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf, lsum[z], 0, 0, 0);
     }
   };
 
@@ -424,7 +428,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
         if constexpr (zstart<Z>(z) == p) {
           prep_q(cq, qraw[z][0], qraw[z][1], qf[z][0], qf[z][1]);
           m[z] = 0.f;
-          l[z] = 0.f;
+          lsum[z] = f32x4{0.f, 0.f, 0.f, 0.f};
           mset[z] = false;
 #pragma unroll
           for (int t = 0; t < 4; ++t) o[z][t] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -471,7 +475,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
       static_for<Z>([&](auto Zi) {
         constexpr int z = decltype(Zi)::v;
         if constexpr (zstart<Z>(z) + KZ - 1 == p) {
-          const float lt = sum_over_rows(l[z]);
+          const float lt = lsum[z][0];
           if (in_grid) {
             const float inv = 1.f / lt;
             const int64_t tok = level_base(h, z) + (int64_t)qy * W + qx;
