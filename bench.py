@@ -36,8 +36,14 @@ METRIC = "NA3D fwd TFLOP/s + tokens/s at 1 MI355X; % of bf16 MFMA peak"
 PEAK_BF16_TFLOPS = 2500.0        # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0            # MI355X HBM3E
 PMC_FILE = os.path.join(ROOT, "profiles", "na3d_fwd_face_rollout_pmc.json")
-KERNEL_SOURCES = ["paper_2606_31248_amd/csrc/na3d_mfma_q.hip", "paper_2606_31248_amd/csrc/mfma_util.h",
-                  "paper_2606_31248_amd/csrc/na3d_ref.hip"]
+STATS_FILE = os.path.join(ROOT, "profiles", "face_rollout_step_kernel_stats.txt")
+# the sources of the kernel that strata_na3d_fwd runs at the face-rollout shape
+KERNEL_SOURCES = ["paper_2606_31248_amd/csrc/na3d_fwd_zs.hip", "paper_2606_31248_amd/csrc/mfma_util.h",
+                  "paper_2606_31248_amd/csrc/common.h"]
+FWD_KERNEL = "na3d_fwd_zs_kernel"
+BLEND_KERNEL = "tile_blend_kernel"
+COPY_KERNEL = "copyBuffer"
+CALIB_BYTES = 1 << 30
 
 
 def kernel_source_hash() -> str:
@@ -59,6 +65,79 @@ def stored_traffic(per_launch_alg_bytes: float):
     if rec.get("kernel_source_hash") != kernel_source_hash():
         return None, None
     return rec.get("hbm_bytes_per_launch"), rec
+
+
+def _pmc_rows(run_dir: str):
+    """(kernel name, counter, value) of every dispatch in a rocprofv3 --pmc csv run."""
+    import csv
+    import glob
+    rows = []
+    for f in glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True):
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                rows.append((r["Kernel_Name"], r["Counter_Name"], float(r["Counter_Value"])))
+    return rows
+
+
+def summarize_pmc(fetch_dir: str, write_dir: str, commands) -> dict:
+    """HBM traffic per launch of the forward and the blend from a FETCH_SIZE run and
+    a WRITE_SIZE run of ``bench.py --calib-copy``: each counter (KiB per dispatch)
+    is scaled by the factor that makes the 1 GiB device copy read its true size."""
+    def per_kernel(run_dir, counter):
+        acc = {}
+        for k, c, v in _pmc_rows(run_dir):
+            if c.startswith(counter):
+                acc.setdefault(k, []).append(v)
+        return acc
+
+    fe, wr = per_kernel(fetch_dir, "FETCH_SIZE"), per_kernel(write_dir, "WRITE_SIZE")
+
+    def pick(acc, key, how=np.median):
+        vals = [v for k, vs in acc.items() if key in k for v in vs]
+        if not vals:
+            raise SystemExit(f"no dispatch of {key} in the counter run")
+        return float(how(vals))
+
+    # the calibration copy is the largest copy dispatch (the others move a few KiB)
+    cf, cw = pick(fe, COPY_KERNEL, np.max), pick(wr, COPY_KERNEL, np.max)
+    ff, fw = CALIB_BYTES / (cf * 1024), CALIB_BYTES / (cw * 1024)
+    wl_alg = 4.0 * 81 * 16 * 8 * 64 * 64 * 64 * 2
+    blend_alg = (81 * 128 * 64 * 64 * 64 + 128 * 512 * 512 * 64) * 2
+    fwd_f, fwd_w = pick(fe, FWD_KERNEL), pick(wr, FWD_KERNEL)
+    bl_f, bl_w = pick(fe, BLEND_KERNEL), pick(wr, BLEND_KERNEL)
+    return {
+        "kernel": f"strata_na3d_fwd ({FWD_KERNEL}<8>)",
+        "workload": "face_rollout_81x16x8x64x64_d64_w3x7x7",
+        "kernel_source_hash": kernel_source_hash(),
+        "fetch_kb_per_launch": fwd_f,
+        "write_kb_per_launch": fwd_w,
+        "copy_calibration": {"bytes": CALIB_BYTES, "fetch_kb": cf, "write_kb": cw,
+                             "fetch_factor": ff, "write_factor": fw},
+        "hbm_bytes_per_launch": fwd_f * 1024 * ff + fwd_w * 1024 * fw,
+        "alg_bytes_per_launch": wl_alg,
+        "blend": {"fetch_kb": bl_f, "write_kb": bl_w, "hbm_bytes_per_launch": bl_f * 1024 * ff + bl_w * 1024 * fw,
+                  "alg_bytes_per_launch": blend_alg},
+        "commands": list(commands),
+        "note": "Traffic = FETCH_SIZE * fetch_factor + WRITE_SIZE * write_factor, per dispatch; the factors "
+                "make the counters of one 1 GiB device copy read 1 GiB.",
+    }
+
+
+def summarize_stats(stats_csv: str, command: str) -> str:
+    """Text summary of a rocprofv3 --kernel-trace --stats run (kernel_stats.csv)."""
+    import csv
+    with open(stats_csv) as fh:
+        rows = list(csv.DictReader(fh))
+    out = ["# rocprofv3 kernel trace of bench.py (face rollout step, training-tile side measurement), MI355X",
+           f"# command: {command}",
+           f"# forward kernel source hash: {kernel_source_hash()}", "",
+           f"{'kernel':72s} {'calls':>6s} {'avg_us':>10s} {'min_us':>10s} {'max_us':>10s} {'pct':>6s}"]
+    for r in rows:
+        name = r["Name"]
+        name = name if len(name) <= 72 else name[:69] + "..."
+        out.append(f"{name:72s} {int(r['Calls']):6d} {float(r['AverageNs']) / 1e3:10.1f} "
+                   f"{float(r['MinNs']) / 1e3:10.1f} {float(r['MaxNs']) / 1e3:10.1f} {float(r['Percentage']):6.2f}")
+    return "\n".join(out) + "\n"
 
 
 def cpu_baseline(wl, tiles_sample: int):
@@ -157,7 +236,25 @@ def main():
                     help="timed passes of the training-tile forward/backward side measurement (0: skip)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run one 1 GiB device copy (HBM counter calibration)")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="write the HBM-traffic summary of two rocprofv3 --pmc runs to profiles/ and exit")
+    ap.add_argument("--summarize-stats", metavar="KERNEL_STATS_CSV",
+                    help="write the kernel-trace summary of a rocprofv3 --stats run to profiles/ and exit")
+    ap.add_argument("--command", action="append", default=[],
+                    help="the profiler command(s) the summary records")
     a = ap.parse_args()
+    if a.summarize_pmc:
+        rec = summarize_pmc(a.summarize_pmc[0], a.summarize_pmc[1], a.command)
+        with open(PMC_FILE, "w") as f:
+            json.dump(rec, f, indent=1)
+        print(json.dumps(rec))
+        return
+    if a.summarize_stats:
+        txt = summarize_stats(a.summarize_stats, a.command[0] if a.command else "")
+        with open(STATS_FILE, "w") as f:
+            f.write(txt)
+        print(txt)
+        return
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build measures one GPU only (no multi-GPU path); run with --gpus 1",
               file=sys.stderr)
@@ -265,7 +362,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(gbs_na, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(gbs_na / PEAK_HBM_GBS, 4),
                      "traffic": None if traffic is None else float(traffic),
-                     "kernel": "strata_na3d_fwd", "alg_bytes_per_launch": alg_bytes},
+                     "kernel": f"strata_na3d_fwd ({FWD_KERNEL})", "alg_bytes_per_launch": alg_bytes},
     }
     if a.train_steps > 0:
         del q, k, v, out, face, coords, cs
