@@ -97,6 +97,94 @@ __global__ void __launch_bounds__(256) tile_blend_kernel(const T* __restrict__ t
   }
 }
 
+// bf16 stitch for channel counts C % 8 == 0 when no face position is covered
+// by more than two tiles along an axis (Ht <= 2 stride_y, Wt <= 2 stride_x).
+// Each thread handles ITEMS cells x 8 channels of one face row and issues all
+// its loads (up to 2 x 2 covering tiles per cell, predicated) before any
+// arithmetic, which keeps enough bytes in flight per CU to stream at HBM rate.
+// Every tile element is read once and every face element written once, so
+// both go through non-temporal (streaming) accesses.
+// Same operation order as the plain kernel: tiles in ascending (a, b), fmaf,
+// the weight sum from 0, one correctly rounded division (skipped when the sum
+// is exactly 1, where it is the identity), round to nearest even.
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+template <int ITEMS>
+__global__ void __launch_bounds__(256) tile_blend_bf16_kernel(const uint16_t* __restrict__ tiles, int nty, int ntx,
+                                                              int P, int Ht, int Wt, int C, int sy, int sx,
+                                                              const float* __restrict__ window,
+                                                              uint16_t* __restrict__ out, int Hf, int Wf, int bpr) {
+  const int cv = C >> 3;
+  const int row = blockIdx.x / bpr;  // p * Hf + y
+  const int jb = (blockIdx.x - row * bpr) * (256 * ITEMS) + threadIdx.x;
+  const int y = row % Hf, p = row / Hf;
+  int alo, ahi;
+  cover_range(y, Ht, sy, nty, &alo, &ahi);
+  const int64_t tile_elems = (int64_t)P * Ht * Wt * C;
+  const int per_row = Wf * cv;
+  uint4 val[ITEMS][2][2];
+  float wt[ITEMS][2][2];
+  bool ok[ITEMS][2][2];
+#pragma unroll
+  for (int k = 0; k < ITEMS; ++k) {
+    const int j = jb + k * 256;
+    const bool live = j < per_row;
+    const int jj = live ? j : 0;
+    const int x = jj / cv, c0 = (jj - x * cv) * 8;
+    int blo, bhi;
+    cover_range(x, Wt, sx, ntx, &blo, &bhi);
+#pragma unroll
+    for (int ia = 0; ia < 2; ++ia) {
+#pragma unroll
+      for (int ib = 0; ib < 2; ++ib) {
+        const int a = alo + ia, b = blo + ib;
+        ok[k][ia][ib] = live && a <= ahi && b <= bhi;
+        val[k][ia][ib] = make_uint4(0u, 0u, 0u, 0u);
+        wt[k][ia][ib] = 0.f;
+        if (ok[k][ia][ib]) {
+          const int ly = y - a * sy, lx = x - b * sx;
+          const uint16_t* src =
+              tiles + ((int64_t)a * ntx + b) * tile_elems + (((int64_t)p * Ht + ly) * Wt + lx) * C + c0;
+          const u32x4 t = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src));
+          val[k][ia][ib] = make_uint4(t.x, t.y, t.z, t.w);
+          wt[k][ia][ib] = window[ly * Wt + lx];
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < ITEMS; ++k) {
+    const int j = jb + k * 256;
+    if (j >= per_row) continue;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    float dsum = 0.f;
+#pragma unroll
+    for (int ia = 0; ia < 2; ++ia) {
+#pragma unroll
+      for (int ib = 0; ib < 2; ++ib) {
+        if (!ok[k][ia][ib]) continue;
+        const float w = wt[k][ia][ib];
+        const uint32_t wv[4] = {val[k][ia][ib].x, val[k][ia][ib].y, val[k][ia][ib].z, val[k][ia][ib].w};
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          acc[2 * v] = __builtin_fmaf(w, __uint_as_float(wv[v] << 16), acc[2 * v]);
+          acc[2 * v + 1] = __builtin_fmaf(w, __uint_as_float(wv[v] & 0xFFFF0000u), acc[2 * v + 1]);
+        }
+        dsum = dsum + w;
+      }
+    }
+    if (dsum != 1.f) {
+#pragma unroll
+      for (int v = 0; v < 8; ++v) acc[v] = dsum == 0.f ? 0.f : acc[v] / dsum;
+    }
+    uint32_t r[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) r[v] = pack_bf16x2(acc[2 * v], acc[2 * v + 1]);
+    __builtin_nontemporal_store(u32x4{r[0], r[1], r[2], r[3]},
+                                reinterpret_cast<u32x4*>(out + (int64_t)row * Wf * C + (int64_t)j * 8));
+  }
+}
+
 template <typename T, int VEC, int CV>
 static void blend_launch(const void* tiles, int nty, int ntx, int P, int Ht, int Wt, int C, int sy,
                          int sx, const float* window, void* out, int Hf, int Wf, hipStream_t s) {
@@ -113,7 +201,15 @@ void launch_tile_blend(const void* tiles, int nty, int ntx, int P, int Ht, int W
                        int sx, const float* window, void* out, int Hf, int Wf, strata_dtype dt,
                        hipStream_t s) {
   if (dt == STRATA_BF16) {
-    if (C == 64)
+    if (C % 8 == 0 && Ht <= 2 * sy && Wt <= 2 * sx) {
+      constexpr int kItems = 2;
+      const int64_t per_row = (int64_t)Wf * (C / 8);
+      const int bpr = (int)((per_row + 256 * kItems - 1) / (256 * kItems));
+      const int64_t blocks = (int64_t)P * Hf * bpr;
+      hipLaunchKernelGGL((tile_blend_bf16_kernel<kItems>), dim3((unsigned)blocks), dim3(256), 0, s,
+                         static_cast<const uint16_t*>(tiles), nty, ntx, P, Ht, Wt, C, sy, sx, window,
+                         static_cast<uint16_t*>(out), Hf, Wf, bpr);
+    } else if (C == 64)
       blend_launch<uint16_t, 8, 8>(tiles, nty, ntx, P, Ht, Wt, C, sy, sx, window, out, Hf, Wf, s);
     else if (C % 8 == 0)
       blend_launch<uint16_t, 8, 0>(tiles, nty, ntx, P, Ht, Wt, C, sy, sx, window, out, Hf, Wf, s);
