@@ -130,6 +130,8 @@ def test_fwd_tiny_f32_full():
     ((1, 1, 8, 32, 32, 64), (3, 7, 7)),
     ((2, 3, 8, 19, 21, 64), (3, 7, 7)),     # level-sweep kernel, ragged blocks
     ((1, 11, 8, 16, 24, 64), (3, 7, 7)),    # level-sweep kernel, ragged head group
+    ((2, 2, 8, 7, 7, 64), (3, 7, 7)),       # level-sweep kernel, window = whole plane
+    ((1, 3, 8, 7, 9, 64), (3, 7, 7)),       # level-sweep kernel, one-column blocks
     ((1, 2, 4, 9, 9, 64), (1, 9, 9)),       # window = whole plane
 ])
 @pytest.mark.parametrize("rope", [True, False])
@@ -221,6 +223,33 @@ def test_fwd_large_logits_move_the_maximum(scale):
     ro, rl = oracle.na3d_fwd(*(oracle.widen(a, "bf16") for a in (q, k, v)), (3, 7, 7), scale, coords=c32)
     check_close(host_f64(out), ro, "bf16", "out")
     assert np.max(np.abs(host_f64(lse) - rl)) <= LSE_ABS_BF16
+
+
+@pytest.mark.parametrize("sign", [-1.0, 1.0])
+@pytest.mark.parametrize("window", [(3, 7, 7), (5, 9, 9)])
+def test_fwd_uniform_extreme_logits(sign, window):
+    """Every logit equal and about 200 (log2 units) from zero: without moving the
+    softmax reference the weights would underflow to 0 (-) or overflow (+); the
+    result must be the window mean of V, the log-sum-exp logit + ln K."""
+    shape = (1, 2, 8, 16, 16, 64)
+    scale = 0.125
+    logit = sign * 200.0 / 1.4426950408889634          # natural-log units
+    alpha = logit / (64 * scale)                          # q = alpha * ones, k = ones
+    q = I.f32_to_bf16_bits(np.full(shape, alpha, np.float32))
+    k = I.f32_to_bf16_bits(np.ones(shape, np.float32))
+    v = I.gaussian(shape, 77, 2, "bf16")
+    qd, kd, vd = (dev_tensor(a, "bf16") for a in (q, k, v))
+    out = torch.empty_like(qd)
+    lse = torch.empty(shape[:-1], dtype=torch.float32, device="cuda")
+    B.strata_na3d_fwd(B.desc_for(qd, window, scale), qd, kd, vd, None, out, lse)
+    torch.cuda.synchronize()
+    ro, rl = oracle.na3d_fwd(*(oracle.widen(a, "bf16") for a in (q, k, v)), window, scale)
+    got = host_f64(out)
+    assert np.isfinite(got).all()
+    check_close(got, ro, "bf16", "out")
+    # the logits themselves carry the float16 rounding of the scaled query (2^-11
+    # relative), so the log-sum-exp bound grows with their size
+    assert np.max(np.abs(host_f64(lse) - rl)) <= LSE_ABS_BF16 + 2.0 ** -10 * float(np.max(np.abs(rl)))
 
 
 def test_fwd_deterministic_and_lse_optional():
