@@ -214,7 +214,10 @@ def train_tile(steps: int):
     n = wl.B * wl.heads * wl.N
     fwd_fl, bwd_fl = 4.0 * n * wl.K * wl.d, 10.0 * n * wl.K * wl.d
     rope_bytes = 2 * 2 * n * wl.d * 2 + 2 * wl.B * wl.H * wl.W * wl.d * 4   # Q, K read+write; phases
-    return {
+    # algorithmic bytes per token-head: forward reads Q, K, V and writes O (bf16) and
+    # LSE (fp32); backward reads Q, K, V, O, dO (bf16) and LSE, writes dQ, dK, dV
+    fwd_bytes, bwd_bytes = n * (4 * wl.d * 2 + 4), n * (8 * wl.d * 2 + 4)
+    out = {
         "workload": f"{wl.name}: {wl.B} tiles x {wl.heads} heads x {wl.Z}x{wl.H}x{wl.W}, window "
                     f"{wl.kz}x{wl.ky}x{wl.kx}, StereoRoPE on",
         "fwd_ms": round(fwd_ms, 4), "fwd_tflops": round(fwd_fl / fwd_ms / 1e9, 2),
@@ -224,6 +227,18 @@ def train_tile(steps: int):
         "rope_apply_qk": {"ms": round(rope_ms, 4), "gbs": round(rope_bytes / rope_ms / 1e6, 1),
                           "frac_hbm": round(rope_bytes / rope_ms / 1e6 / PEAK_HBM_GBS, 4)},
     }
+    out["_fwd"] = (fwd_fl, fwd_bytes, fwd_ms)
+    out["_bwd"] = (bwd_fl, bwd_bytes, bwd_ms)
+    return out
+
+
+def roofline_row(flops: float, nbytes: float, ms: float) -> dict:
+    """Achieved rate of a kernel against min(MFMA peak, intensity x HBM peak)."""
+    ai = flops / nbytes
+    cap = min(PEAK_BF16_TFLOPS, ai * PEAK_HBM_GBS / 1e3)
+    tf = flops / ms / 1e9
+    return {"bound": "hbm" if cap < PEAK_BF16_TFLOPS else "mfma", "flop_per_byte": round(ai, 1),
+            "cap_tflops": round(cap, 1), "achieved_tflops": round(tf, 2), "frac_of_cap": round(tf / cap, 4)}
 
 
 def main():
@@ -364,10 +379,23 @@ def main():
                      "traffic": None if traffic is None else float(traffic),
                      "kernel": f"strata_na3d_fwd ({FWD_KERNEL})", "alg_bytes_per_launch": alg_bytes},
     }
+    # every row of the hot path against the roofline that bounds it
+    res["rows"] = {
+        "a1_a2_coords_phases": {"ms": round(avg["coords"], 4), "bound": "alu (fp64 geometry)"},
+        "a3_a6_na3d_fwd_face": dict(roofline_row(flops, alg_bytes, avg["na"]), achieved_gbs=round(gbs_na, 1),
+                                    frac_hbm=round(gbs_na / PEAK_HBM_GBS, 4)),
+        "a8_tile_blend_face": {"bound": "hbm", "achieved_gbs": round(blend_bytes / (avg["blend"] * 1e-3) / 1e9, 1),
+                               "frac_hbm": round(blend_bytes / (avg["blend"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
+    }
     if a.train_steps > 0:
         del q, k, v, out, face, coords, cs
         torch.cuda.empty_cache()
-        res["train_tile"] = train_tile(a.train_steps)
+        tt = train_tile(a.train_steps)
+        res["rows"]["a3_a6_na3d_fwd_train_tile"] = roofline_row(*tt.pop("_fwd"))
+        res["rows"]["a7_na3d_bwd_train_tile"] = roofline_row(*tt.pop("_bwd"))
+        res["rows"]["a2_rope_apply_train_tile"] = {"bound": "hbm", "achieved_gbs": tt["rope_apply_qk"]["gbs"],
+                                                   "frac_hbm": tt["rope_apply_qk"]["frac_hbm"]}
+        res["train_tile"] = tt
     if a.cpu_tiles > 0:
         res["cpu_baseline"] = cpu_baseline(wl, a.cpu_tiles)
     print(json.dumps(res), flush=True)
