@@ -8,8 +8,9 @@ its Python binding) never calls it and shares no code with it.
   sphere (numpy, float64).
 * ``strata_oracle.c`` (built into ``liboracle.so`` with gcc, OpenMP, no
   fast-math, no FP contraction): window indexing, StereoRoPE, neighbourhood
-  attention forward/backward, tile blend and extraction, in float64 (the blend
-  follows its fixed operation order).
+  attention forward/backward (optionally with QK RMSNorm and the sigmoid
+  output gate), tile blend and extraction, in float64 (the blend follows its
+  fixed operation order).
 """
 from __future__ import annotations
 
@@ -54,10 +55,13 @@ def lib():
         L.oracle_rope_apply.argtypes = [P, P, i32, i32, i32, i32, i32, i32, f64, i32, P]
         L.oracle_na3d_fwd.argtypes = [P, P, P, P, f64] + [i32] * 9 + [f64, i64, P, P, P]
         L.oracle_na3d_bwd.argtypes = [P, P, P, P, f64] + [i32] * 9 + [f64, P, i64, P, i64, P, P, P, P]
+        L.oracle_na3d_fwd_ex.argtypes = [P, P, P, P, f64] + [i32] * 9 + [f64, i32, f64, P, i32, i64, P, P, P]
+        L.oracle_na3d_bwd_ex.argtypes = ([P, P, P, P, f64] + [i32] * 9 + [f64, i32, f64, P, i32, P, i64, P, i64, P]
+                                         + [P, P, P, P])
         L.oracle_tile_blend.argtypes = [P, i32, i32, i32, i32, i32, i32, i32, i32, P, P, i32, i32, i32]
         L.oracle_tile_extract.argtypes = [P, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32, P, i32]
         for f in ("oracle_axis_index", "oracle_rope_phases", "oracle_rope_apply", "oracle_na3d_fwd", "oracle_na3d_bwd",
-                  "oracle_tile_blend", "oracle_tile_extract", "oracle_num_threads"):
+                  "oracle_na3d_fwd_ex", "oracle_na3d_bwd_ex", "oracle_tile_blend", "oracle_tile_extract", "oracle_num_threads"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -114,11 +118,26 @@ def rope_apply(x: np.ndarray, coords: np.ndarray, transpose: bool = False,
     return y
 
 
-def na3d_fwd(q, k, v, window, scale, coords=None, sel=None, base: float = ROPE_BASE):
+def _gate_arg(gate, shape):
+    """gate logits as float64: [B, heads, Z, H, W] (gate_dim 1) or the full shape (gate_dim d)."""
+    if gate is None:
+        return None, 0
+    g = np.ascontiguousarray(gate, dtype=np.float64)
+    if g.shape == tuple(shape[:-1]):
+        return g, 1
+    if g.shape == tuple(shape):
+        return g, shape[-1]
+    raise ValueError("gate must have shape %s or %s" % (shape[:-1], shape))
+
+
+def na3d_fwd(q, k, v, window, scale, coords=None, sel=None, base: float = ROPE_BASE,
+             qk_norm: bool = False, eps: float = 1e-6, gate=None):
     """Neighbourhood attention forward in float64.
 
     q, k, v: [B, heads, Z, H, W, d] float64.  window: (kz, ky, kx).
     sel: optional flat query indices into [B, heads, Z, H, W].
+    qk_norm: RMS-normalise q and k (no learnable scale) with ``eps``.
+    gate: sigmoid-gate logits, [B, heads, Z, H, W] or [B, heads, Z, H, W, d].
     Returns (out, lse): out [n, d] (or full shape when sel is None), lse [n]."""
     q = np.ascontiguousarray(q, dtype=np.float64)
     k = np.ascontiguousarray(k, dtype=np.float64)
@@ -134,8 +153,14 @@ def na3d_fwd(q, k, v, window, scale, coords=None, sel=None, base: float = ROPE_B
         n = s.shape[0]
     out = np.empty((n, d), np.float64)
     lse = np.empty(n, np.float64)
-    rc = lib().oracle_na3d_fwd(_p(q), _p(k), _p(v), _p(c), base, B, heads, Z, H, W, d, kz, ky, kx,
-                               float(scale), n, _p(s), _p(out), _p(lse))
+    g, gdim = _gate_arg(gate, q.shape)
+    if qk_norm or g is not None:
+        rc = lib().oracle_na3d_fwd_ex(_p(q), _p(k), _p(v), _p(c), base, B, heads, Z, H, W, d, kz, ky, kx,
+                                      float(scale), int(qk_norm), float(eps), _p(g), gdim, n, _p(s),
+                                      _p(out), _p(lse))
+    else:
+        rc = lib().oracle_na3d_fwd(_p(q), _p(k), _p(v), _p(c), base, B, heads, Z, H, W, d, kz, ky, kx,
+                                   float(scale), n, _p(s), _p(out), _p(lse))
     if rc:
         raise ValueError("oracle_na3d_fwd failed (%d)" % rc)
     if sel is None:
@@ -144,10 +169,13 @@ def na3d_fwd(q, k, v, window, scale, coords=None, sel=None, base: float = ROPE_B
 
 
 def na3d_bwd(q, k, v, dout, window, scale, coords=None, selq=None, selk=None,
-             base: float = ROPE_BASE):
-    """Neighbourhood attention backward in float64: (dq, dk, dv).
+             base: float = ROPE_BASE, qk_norm: bool = False, eps: float = 1e-6, gate=None):
+    """Neighbourhood attention backward in float64: (dq, dk, dv), plus dgate when
+    ``gate`` is given (options as in ``na3d_fwd``; dout is the gradient of the
+    gated output).
 
-    dq rows follow selq, dk/dv rows follow selk (flat indices; None = all, full shape)."""
+    dq and dgate rows follow selq, dk/dv rows follow selk (flat indices; None =
+    all, full shape)."""
     q = np.ascontiguousarray(q, dtype=np.float64)
     k = np.ascontiguousarray(k, dtype=np.float64)
     v = np.ascontiguousarray(v, dtype=np.float64)
@@ -163,16 +191,29 @@ def na3d_bwd(q, k, v, dout, window, scale, coords=None, selq=None, selk=None,
     dq = np.empty((nq, d), np.float64)
     dk = np.empty((nk, d), np.float64)
     dv = np.empty((nk, d), np.float64)
-    rc = lib().oracle_na3d_bwd(_p(q), _p(k), _p(v), _p(c), base, B, heads, Z, H, W, d, kz, ky, kx,
-                               float(scale), _p(g), nq, _p(sq), nk, _p(sk), _p(dq), _p(dk), _p(dv))
+    gt, gdim = _gate_arg(gate, q.shape)
+    dg = None
+    if qk_norm or gt is not None:
+        if gt is not None:
+            dg = np.empty((nq,) if gdim == 1 else (nq, d), np.float64)
+        rc = lib().oracle_na3d_bwd_ex(_p(q), _p(k), _p(v), _p(c), base, B, heads, Z, H, W, d, kz, ky, kx,
+                                      float(scale), int(qk_norm), float(eps), _p(gt), gdim, _p(g), nq,
+                                      _p(sq), nk, _p(sk), _p(dq), _p(dk), _p(dv), _p(dg))
+    else:
+        rc = lib().oracle_na3d_bwd(_p(q), _p(k), _p(v), _p(c), base, B, heads, Z, H, W, d, kz, ky, kx,
+                                   float(scale), _p(g), nq, _p(sq), nk, _p(sk), _p(dq), _p(dk), _p(dv))
     if rc:
         raise ValueError("oracle_na3d_bwd failed (%d)" % rc)
     full = (B, heads, Z, H, W, d)
     if sq is None:
         dq = dq.reshape(full)
+        if dg is not None:
+            dg = dg.reshape(gt.shape)
     if sk is None:
         dk = dk.reshape(full)
         dv = dv.reshape(full)
+    if gt is not None:
+        return dq, dk, dv, dg
     return dq, dk, dv
 
 

@@ -16,7 +16,9 @@
  *   - StereoRoPE: axial 2D rotary embedding driven by the stereographic
  *     coordinates of Eq. 1 (Sec. 3.3);
  *   - tile stitching S = D^-1 P^T W with D = P^T W 1 (App. F, "Tile stitching"
- *     and Eq. (stitch)).
+ *     and Eq. (stitch));
+ *   - QK RMSNorm and the sigmoid output gate of every attention block
+ *     (App. B.5).
  * Readings where the paper is silent are stated at each function.
  */
 #include <math.h>
@@ -373,6 +375,174 @@ int oracle_na3d_bwd(const double* q, const double* k, const double* v, const flo
   }
   free(ph);
   return err;
+}
+
+/* ---------------------------------------------------------------------------
+ * QK normalisation and gated attention (App. B.5, "QK normalization and gated
+ * attention").
+ *   - Every query and key vector (one token of one head, its d entries) is
+ *     divided by its root mean square before the dot product, with no
+ *     learnable scale:  x^ = x / sqrt(mean_e x_e^2 + eps).
+ *   - The attention output of every (token, head) is multiplied by a sigmoid
+ *     gate, sigmoid(g) = 1 / (1 + exp(-g)), of gate logits g given either once
+ *     per (token, head) (gate_dim 1) or per channel (gate_dim d).
+ * Readings where the paper is silent: eps is an argument; the norm comes
+ * before the rotary embedding (a rotation keeps every pair's sum of squares,
+ * so the order does not change the result); the gate logits are inputs
+ * (whatever produces them lies outside attention); the lse stays that of the
+ * softmax, before the gate.
+ * ------------------------------------------------------------------------- */
+static double sigmoid(double g) { return 1.0 / (1.0 + exp(-g)); }
+
+/* y[i] = x[i] / sqrt(mean(x[i]^2) + eps) for every row i of n rows of d;
+ * rinv[i] = 1 / sqrt(mean(x[i]^2) + eps).  Returns NULL on allocation failure. */
+static double* rms_normalise(const double* x, int64_t n, int d, double eps, double* rinv) {
+  double* y = (double*)malloc(sizeof(double) * (size_t)n * d);
+  if (!y) return NULL;
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) {
+    double ss = 0.0;
+    for (int e = 0; e < d; ++e) ss += x[i * d + e] * x[i * d + e];
+    double r = 1.0 / sqrt(ss / d + eps);
+    if (rinv) rinv[i] = r;
+    for (int e = 0; e < d; ++e) y[i * d + e] = x[i * d + e] * r;
+  }
+  return y;
+}
+
+static double gate_logit(const double* gate, int gate_dim, int d, int64_t qi, int e) {
+  return gate_dim == 1 ? gate[qi] : gate[qi * d + e];
+}
+
+static int check_options(int d, int qk_norm, double eps, const double* gate, int gate_dim) {
+  if (qk_norm && !(eps >= 0.0)) return 1;
+  if (gate && gate_dim != 1 && gate_dim != d) return 1;
+  return 0;
+}
+
+/* Forward with the options: the neighbourhood attention above on the
+ * normalised q and k (when qk_norm), then the gate on its output (when gate
+ * != NULL).  Selection, outputs and errors as in oracle_na3d_fwd. */
+int oracle_na3d_fwd_ex(const double* q, const double* k, const double* v, const float* coords,
+                       double base, int B, int heads, int Z, int H, int W, int d, int kz, int ky,
+                       int kx, double scale, int qk_norm, double eps, const double* gate,
+                       int gate_dim, int64_t nsel, const int64_t* sel, double* out, double* lse) {
+  if (d <= 0 || check_options(d, qk_norm, eps, gate, gate_dim)) return 1;
+  int64_t nq = (int64_t)B * heads * Z * H * W;
+  if (nq <= 0) return 1;
+  double *qn = NULL, *kn = NULL;
+  if (qk_norm) {
+    qn = rms_normalise(q, nq, d, eps, NULL);
+    kn = rms_normalise(k, nq, d, eps, NULL);
+    if (!qn || !kn) {
+      free(qn);
+      free(kn);
+      return 2;
+    }
+  }
+  int rc = oracle_na3d_fwd(qk_norm ? qn : q, qk_norm ? kn : k, v, coords, base, B, heads, Z, H, W,
+                           d, kz, ky, kx, scale, nsel, sel, out, lse);
+  free(qn);
+  free(kn);
+  if (rc || !gate) return rc;
+  if (!sel) nsel = nq;
+  for (int64_t i = 0; i < nsel; ++i) {
+    int64_t qi = sel ? sel[i] : i;
+    for (int e = 0; e < d; ++e) out[i * d + e] *= sigmoid(gate_logit(gate, gate_dim, d, qi, e));
+  }
+  return 0;
+}
+
+/* Backward with the options, by the chain rule through the steps of the
+ * forward above, for upstream gradient dO of the gated output:
+ *   gate:  out = s * A with s = sigmoid(g), so dA = s * dO and
+ *          dg = s (1 - s) * dO * A  (per channel; gate_dim 1 sums over e);
+ *   attention: the backward above on (q^, k^, v) with upstream gradient dA,
+ *          giving dq^, dk^, dv;
+ *   norm:  x^ = r x with r = (mean(x^2) + eps)^(-1/2), whose Jacobian gives
+ *          dx = r (dx^ - x^ mean_e(dx^_e x^_e)).
+ * dq and dgate rows follow selq, dk and dv rows follow selk (NULL = all);
+ * dgate (shape of gate) is written when both gate and dgate are non-NULL. */
+int oracle_na3d_bwd_ex(const double* q, const double* k, const double* v, const float* coords,
+                       double base, int B, int heads, int Z, int H, int W, int d, int kz, int ky,
+                       int kx, double scale, int qk_norm, double eps, const double* gate,
+                       int gate_dim, const double* dout, int64_t nselq, const int64_t* selq,
+                       int64_t nselk, const int64_t* selk, double* dq, double* dk, double* dv,
+                       double* dgate) {
+  if (d <= 0 || check_options(d, qk_norm, eps, gate, gate_dim)) return 1;
+  int64_t nq = (int64_t)B * heads * Z * H * W;
+  if (nq <= 0) return 1;
+  if (!selq) nselq = nq;
+  if (!selk) nselk = nq;
+  double *qn = NULL, *kn = NULL, *rq = NULL, *rk = NULL, *da = NULL, *A = NULL;
+  int rc = 2;
+  if (qk_norm) {
+    rq = (double*)malloc(sizeof(double) * nq);
+    rk = (double*)malloc(sizeof(double) * nq);
+    if (!rq || !rk) goto done;
+    qn = rms_normalise(q, nq, d, eps, rq);
+    kn = rms_normalise(k, nq, d, eps, rk);
+    if (!qn || !kn) goto done;
+  }
+  const double* qq = qk_norm ? qn : q;
+  const double* kk = qk_norm ? kn : k;
+  if (gate) {
+    da = (double*)malloc(sizeof(double) * (size_t)nq * d);
+    if (!da) goto done;
+    for (int64_t i = 0; i < nq; ++i)
+      for (int e = 0; e < d; ++e) da[i * d + e] = sigmoid(gate_logit(gate, gate_dim, d, i, e)) * dout[i * d + e];
+  }
+  rc = oracle_na3d_bwd(qq, kk, v, coords, base, B, heads, Z, H, W, d, kz, ky, kx, scale,
+                       gate ? da : dout, nselq, selq, nselk, selk, dq, dk, dv);
+  if (rc) goto done;
+  if (qk_norm) {
+    for (int64_t i = 0; i < nselq; ++i) {
+      int64_t qi = selq ? selq[i] : i;
+      double c = 0.0;
+      for (int e = 0; e < d; ++e) c += dq[i * d + e] * qn[qi * d + e];
+      c /= d;
+      for (int e = 0; e < d; ++e) dq[i * d + e] = rq[qi] * (dq[i * d + e] - qn[qi * d + e] * c);
+    }
+    for (int64_t t = 0; t < nselk; ++t) {
+      int64_t kj = selk ? selk[t] : t;
+      double c = 0.0;
+      for (int e = 0; e < d; ++e) c += dk[t * d + e] * kn[kj * d + e];
+      c /= d;
+      for (int e = 0; e < d; ++e) dk[t * d + e] = rk[kj] * (dk[t * d + e] - kn[kj * d + e] * c);
+    }
+  }
+  if (gate && dgate) {
+    /* the ungated attention output A of the selected queries */
+    A = (double*)malloc(sizeof(double) * (size_t)nselq * d);
+    if (!A) {
+      rc = 2;
+      goto done;
+    }
+    rc = oracle_na3d_fwd(qq, kk, v, coords, base, B, heads, Z, H, W, d, kz, ky, kx, scale,
+                         nselq, selq, A, NULL);
+    if (rc) goto done;
+    for (int64_t i = 0; i < nselq; ++i) {
+      int64_t qi = selq ? selq[i] : i;
+      if (gate_dim == 1) {
+        double s = sigmoid(gate[qi]), acc = 0.0;
+        for (int e = 0; e < d; ++e) acc += dout[qi * d + e] * A[i * d + e];
+        dgate[i] = s * (1.0 - s) * acc;
+      } else {
+        for (int e = 0; e < d; ++e) {
+          double s = sigmoid(gate[qi * d + e]);
+          dgate[i * d + e] = s * (1.0 - s) * dout[qi * d + e] * A[i * d + e];
+        }
+      }
+    }
+  }
+done:
+  free(qn);
+  free(kn);
+  free(rq);
+  free(rk);
+  free(da);
+  free(A);
+  return rc;
 }
 
 /* ---------------------------------------------------------------------------
