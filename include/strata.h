@@ -8,7 +8,8 @@
  *   - 3D neighbourhood attention over the (level, y, x) token grid of each tile
  *     with NATTEN's border-clamped windows (Sec. 3.2), forward and backward;
  *   - the overlapping-tile stitch S = D^-1 P^T W and its extraction P
- *     (App. F, "Tile stitching", "Linear operator interpretation").
+ *     (App. F, "Tile stitching", "Linear operator interpretation");
+ *   - QK RMSNorm and the sigmoid output gate of the attention block (App. B.5).
  *
  * Conventions shared by every call:
  *   - Pointers are DEVICE pointers owned by the caller unless stated otherwise.
@@ -120,6 +121,59 @@ strata_status strata_na3d_bwd(const strata_na3d_desc* desc, const void* q, const
                               const void* v, const float* cs, const void* out, const void* dout,
                               const float* lse, void* dq, void* dk, void* dv, void* workspace,
                               size_t workspace_bytes, void* stream);
+
+/* ---- QK normalisation and the output gate (App. B.5) -----------------------
+ * Options of the attention block beyond plain neighbourhood attention; a
+ * zero-initialised struct (or a NULL pointer) selects plain attention.
+ *   qk_norm != 0: every query and key vector (one token of one head, its
+ *     head_dim entries) is divided by its root mean square before the dot
+ *     product, with no learnable scale:  x^ = x / sqrt(mean_e x_e^2 + eps).
+ *     The norm precedes the StereoRoPE rotation (the two commute: a rotation
+ *     keeps every pair's sum of squares).  eps: finite, >= 0 (with eps = 0 an
+ *     all-zero vector gives inf/NaN).
+ *   gate != NULL: the attention output of every (token, head) is multiplied by
+ *     sigmoid(g) = 1 / (1 + exp(-g)) of the gate logits g (device memory of
+ *     desc->dtype): gate_dim == 1 -> g is [B, heads, Z, H, W], one logit per
+ *     token and head; gate_dim == head_dim -> g is [B, heads, Z, H, W,
+ *     head_dim], one per channel.  The logits are inputs: whatever produces
+ *     them (a projection of the block input) lies outside this library. */
+typedef struct {
+  int32_t qk_norm;
+  float eps;
+  const void* gate;
+  int32_t gate_dim;
+} strata_na3d_opts;
+
+/* Forward with options: s_ij = scale <R_i q^_i, R_j k^_j> (q^ = q, k^ = k when
+ * qk_norm == 0), lse_i = ln sum_j exp(s_ij) (the softmax's, before the gate),
+ * out_i = sigmoid(g_i) * sum_j exp(s_ij - lse_i) v_j (no factor without a
+ * gate).  Everything else as strata_na3d_fwd; opts == NULL is strata_na3d_fwd. */
+strata_status strata_na3d_fwd_ex(const strata_na3d_desc* desc, const strata_na3d_opts* opts,
+                                 const void* q, const void* k, const void* v, const float* cs,
+                                 void* out, float* lse, void* stream);
+
+/* Backward with options, for dout = d(loss)/d(out) of the gated output, with the
+ * out and lse the forward wrote.  By the chain rule through the forward:
+ *   gate: a = sigmoid(g), dA = a * dout, dgate = (1 - a) * dout * out per
+ *     channel (gate_dim == head_dim) or (1 - a) * <dout_i, out_i>
+ *     (gate_dim == 1);
+ *   attention: the backward of strata_na3d_bwd on (q^, k^, v) with upstream
+ *     gradient dA (its D_i = <dA_i, A_i> equals <dout_i, out_i>);
+ *   norm: dx = r (dx^ - x^ mean_e(dx^_e x^_e)), r = (mean(x^2) + eps)^(-1/2),
+ *     for x = q and x = k.
+ * dgate: same shape and dtype as the gate, required when opts->gate is set
+ * (NULL otherwise).  workspace: at least strata_na3d_bwd_ex_workspace_size(desc,
+ * opts) bytes of device memory owned by the caller; it holds D and, with a
+ * gate, dA (for bf16 as two bf16 terms whose sum carries it to ~2^-16).  The
+ * norm is applied inside the attention kernels.  The library allocates
+ * nothing. */
+size_t strata_na3d_bwd_ex_workspace_size(const strata_na3d_desc* desc,
+                                         const strata_na3d_opts* opts);
+strata_status strata_na3d_bwd_ex(const strata_na3d_desc* desc, const strata_na3d_opts* opts,
+                                 const void* q, const void* k, const void* v, const float* cs,
+                                 const void* out, const void* dout, const float* lse, void* dq,
+                                 void* dk, void* dv, void* dgate, void* workspace,
+                                 size_t workspace_bytes, void* stream);
 
 /* ---- a8: tile stitch S = D^-1 P^T W (App. F, Eq. stitch) -------------------
  * Regular tiling: tile t = a*ntx + b has origin (a*stride_y, b*stride_x) on the

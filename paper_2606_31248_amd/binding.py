@@ -24,6 +24,7 @@ STRATA_F32, STRATA_BF16 = 0, 1
 EXPORTS = (
     "strata_stereo_coords", "strata_stereorope_phases", "strata_stereorope_apply",
     "strata_na3d_fwd", "strata_na3d_bwd_workspace_size", "strata_na3d_bwd",
+    "strata_na3d_fwd_ex", "strata_na3d_bwd_ex_workspace_size", "strata_na3d_bwd_ex",
     "strata_tile_blend", "strata_tile_extract", "strata_na_axis_index",
     "strata_status_string", "strata_last_error",
 )
@@ -40,6 +41,11 @@ class NA3DDesc(ctypes.Structure):
                 ("H", ctypes.c_int32), ("W", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("kz", ctypes.c_int32), ("ky", ctypes.c_int32), ("kx", ctypes.c_int32),
                 ("scale", ctypes.c_float), ("dtype", ctypes.c_int)]
+
+
+class NA3DOpts(ctypes.Structure):
+    _fields_ = [("qk_norm", ctypes.c_int32), ("eps", ctypes.c_float), ("gate", ctypes.c_void_p),
+                ("gate_dim", ctypes.c_int32)]
 
 
 _lib = None
@@ -70,8 +76,18 @@ def load(path: str = LIB_PATH):
         f = getattr(L, name)
         f.argtypes = args
         f.restype = st
+    O = ctypes.POINTER(NA3DOpts)
+    for name, args in {
+        "strata_na3d_fwd_ex": [D, O, P, P, P, P, P, P, P],
+        "strata_na3d_bwd_ex": [D, O, P, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
+    }.items():
+        f = getattr(L, name)
+        f.argtypes = args
+        f.restype = st
     L.strata_na3d_bwd_workspace_size.argtypes = [D]
     L.strata_na3d_bwd_workspace_size.restype = ctypes.c_size_t
+    L.strata_na3d_bwd_ex_workspace_size.argtypes = [D, O]
+    L.strata_na3d_bwd_ex_workspace_size.restype = ctypes.c_size_t
     L.strata_status_string.argtypes = [st]
     L.strata_status_string.restype = ctypes.c_char_p
     L.strata_last_error.argtypes = []
@@ -155,6 +171,40 @@ def strata_na3d_bwd(desc: NA3DDesc, q, k, v, cs, out, dout, lse, dq, dk, dv, wor
     _check(load().strata_na3d_bwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(cs), _ptr(out),
                                   _ptr(dout), _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv),
                                   _ptr(workspace), nbytes, _stream(stream)))
+
+
+def make_opts(qk_norm: bool = False, eps: float = 1e-6, gate: Optional[torch.Tensor] = None) -> NA3DOpts:
+    """Options of the attention block: QK RMSNorm and the sigmoid output gate.
+
+    gate: logits of the activations' dtype, [B, heads, Z, H, W] (one per token
+    and head) or [B, heads, Z, H, W, head_dim] (one per channel)."""
+    o = NA3DOpts(int(bool(qk_norm)), float(eps), None, 0)
+    if gate is not None:
+        o.gate = _ptr(gate)
+        o.gate_dim = 1 if gate.dim() == 5 else int(gate.shape[-1])
+    o._keep = gate  # the tensor must outlive the call
+    return o
+
+
+def _opts_ref(opts: Optional[NA3DOpts]):
+    return None if opts is None else ctypes.byref(opts)
+
+
+def strata_na3d_fwd_ex(desc: NA3DDesc, opts: Optional[NA3DOpts], q, k, v, cs, out, lse=None, stream=None):
+    _check(load().strata_na3d_fwd_ex(ctypes.byref(desc), _opts_ref(opts), _ptr(q), _ptr(k), _ptr(v), _ptr(cs),
+                                     _ptr(out), _ptr(lse), _stream(stream)))
+
+
+def strata_na3d_bwd_ex_workspace_size(desc: NA3DDesc, opts: Optional[NA3DOpts]) -> int:
+    return int(load().strata_na3d_bwd_ex_workspace_size(ctypes.byref(desc), _opts_ref(opts)))
+
+
+def strata_na3d_bwd_ex(desc: NA3DDesc, opts: Optional[NA3DOpts], q, k, v, cs, out, dout, lse, dq, dk, dv,
+                       dgate, workspace, stream=None):
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(load().strata_na3d_bwd_ex(ctypes.byref(desc), _opts_ref(opts), _ptr(q), _ptr(k), _ptr(v), _ptr(cs),
+                                     _ptr(out), _ptr(dout), _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv),
+                                     _ptr(dgate), _ptr(workspace), nbytes, _stream(stream)))
 
 
 def strata_tile_blend(tiles, nty, ntx, stride_y, stride_x, window, out, stream=None):

@@ -59,6 +59,123 @@ static strata_status check_desc(const strata_na3d_desc* d) {
   return STRATA_OK;
 }
 
+// Options of the attention block; NULL = plain attention.
+static strata_status check_opts(const strata_na3d_desc* d, const strata_na3d_opts* o, NaOpts& out) {
+  out = NaOpts{};
+  if (!o) return STRATA_OK;
+  if (o->qk_norm) {
+    REQUIRE(isfinite(o->eps) && o->eps >= 0.f, "opts: eps must be finite and >= 0");
+    out.qk_norm = 1;
+    out.eps = o->eps;
+  }
+  if (o->gate) {
+    REQUIRE(o->gate_dim == 1 || o->gate_dim == d->head_dim,
+            "opts: gate_dim must be 1 or head_dim (%d), got %d", d->head_dim, o->gate_dim);
+    REQUIRE(aligned16(o->gate), "opts.gate: not 16-byte aligned");
+    out.gate = o->gate;
+    out.gate_dim = o->gate_dim;
+  }
+  return STRATA_OK;
+}
+
+// Backward workspace: D, then (with a gate) dA = sigmoid(g) dO as its rounded
+// value hi and, for bf16, the remainder lo; every region starts on a 256-byte
+// boundary.
+struct BwdLayout {
+  size_t dvec, da_hi, da_lo, total;
+};
+
+static BwdLayout bwd_layout(const strata_na3d_desc& d, const NaOpts& o) {
+  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  const size_t n = (size_t)d.B * d.heads * d.Z * d.H * d.W;
+  const size_t rowb = n * d.head_dim * (d.dtype == STRATA_BF16 ? 2 : 4);
+  BwdLayout L = {};
+  size_t off = al(n * sizeof(float));
+  L.da_hi = off;
+  if (o.gate) off += al(rowb);
+  L.da_lo = off;
+  if (o.gate && d.dtype == STRATA_BF16) off += al(rowb);
+  L.total = off;
+  return L;
+}
+
+static strata_status na3d_fwd_impl(const strata_na3d_desc* desc, const strata_na3d_opts* opts,
+                                   const void* q, const void* k, const void* v, const float* cs,
+                                   void* out, float* lse, void* stream) {
+  strata_status st = check_desc(desc);
+  if (st != STRATA_OK) return st;
+  NaOpts o;
+  st = check_opts(desc, opts, o);
+  if (st != STRATA_OK) return st;
+  REQUIRE_PTR(q);
+  REQUIRE_PTR(k);
+  REQUIRE_PTR(v);
+  REQUIRE_PTR(out);
+  if (cs) REQUIRE(aligned16(cs), "cs: not 16-byte aligned");
+  if (lse) REQUIRE(aligned16(lse), "lse: not 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  if (!launch_na3d_fwd_zs(*desc, o, q, k, v, cs, out, lse, s) &&
+      !launch_na3d_fwd_mfma(*desc, o, q, k, v, cs, out, lse, s))
+    launch_na3d_fwd_ref(*desc, o, q, k, v, cs, out, lse, s);
+  return check_launch(opts ? "strata_na3d_fwd_ex" : "strata_na3d_fwd");
+}
+
+static size_t bwd_workspace_impl(const strata_na3d_desc* desc, const strata_na3d_opts* opts) {
+  NaOpts o;
+  if (!desc || check_desc(desc) != STRATA_OK || check_opts(desc, opts, o) != STRATA_OK) return 0;
+  return bwd_layout(*desc, o).total;
+}
+
+static strata_status na3d_bwd_impl(const strata_na3d_desc* desc, const strata_na3d_opts* opts,
+                                   const void* q, const void* k, const void* v, const float* cs,
+                                   const void* out, const void* dout, const float* lse, void* dq,
+                                   void* dk, void* dv, void* dgate, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+  strata_status st = check_desc(desc);
+  if (st != STRATA_OK) return st;
+  NaOpts o;
+  st = check_opts(desc, opts, o);
+  if (st != STRATA_OK) return st;
+  REQUIRE_PTR(q);
+  REQUIRE_PTR(k);
+  REQUIRE_PTR(v);
+  REQUIRE_PTR(out);
+  REQUIRE_PTR(dout);
+  REQUIRE_PTR(lse);
+  REQUIRE_PTR(dq);
+  REQUIRE_PTR(dk);
+  REQUIRE_PTR(dv);
+  if (o.gate) REQUIRE_PTR(dgate);
+  if (cs) REQUIRE(aligned16(cs), "cs: not 16-byte aligned");
+  const BwdLayout L = bwd_layout(*desc, o);
+  if (!workspace || workspace_bytes < L.total)
+    return set_error(STRATA_ERR_WORKSPACE, "workspace: need %zu bytes, got %zu", L.total,
+                     workspace ? workspace_bytes : (size_t)0);
+  REQUIRE(aligned16(workspace), "workspace: not 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = static_cast<char*>(workspace);
+  float* dvec = reinterpret_cast<float*>(ws + L.dvec);
+  // the attention backward runs with upstream gradient dA (dO without a gate);
+  // QK RMSNorm happens inside its kernels
+  BwdOpts bo;
+  bo.qk_norm = o.qk_norm;
+  bo.eps = o.eps;
+  const void* ga = dout;
+  if (o.gate) {
+    void* lo = desc->dtype == STRATA_BF16 ? ws + L.da_lo : nullptr;
+    launch_na3d_bwd_gate_prep(*desc, o, out, dout, dvec, ws + L.da_hi, lo, dgate, s);
+    ga = ws + L.da_hi;
+    bo.dout_lo = lo;
+  } else {
+    launch_na3d_bwd_ref(0, *desc, bo, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+  }
+  if (!launch_na3d_bwd_dq_mfma(*desc, bo, q, k, v, cs, ga, lse, dvec, dq, s))
+    launch_na3d_bwd_ref(1, *desc, bo, q, k, v, cs, out, ga, lse, dq, dk, dv, dvec, s);
+  if (!launch_na3d_bwd_dkdv_mfma(*desc, bo, q, k, v, cs, ga, lse, dvec, dk, dv, s))
+    launch_na3d_bwd_ref(2, *desc, bo, q, k, v, cs, out, ga, lse, dq, dk, dv, dvec, s);
+  return check_launch(opts ? "strata_na3d_bwd_ex" : "strata_na3d_bwd");
+}
+
 }  // namespace strata
 
 using namespace strata;
@@ -140,56 +257,39 @@ strata_status strata_stereorope_apply(const void* x, void* y, const float* cs, i
 strata_status strata_na3d_fwd(const strata_na3d_desc* desc, const void* q, const void* k,
                               const void* v, const float* cs, void* out, float* lse,
                               void* stream) {
-  strata_status st = check_desc(desc);
-  if (st != STRATA_OK) return st;
-  REQUIRE_PTR(q);
-  REQUIRE_PTR(k);
-  REQUIRE_PTR(v);
-  REQUIRE_PTR(out);
-  if (cs) REQUIRE(aligned16(cs), "cs: not 16-byte aligned");
-  if (lse) REQUIRE(aligned16(lse), "lse: not 16-byte aligned");
-  hipStream_t s = (hipStream_t)stream;
-  if (!launch_na3d_fwd_zs(*desc, q, k, v, cs, out, lse, s) &&
-      !launch_na3d_fwd_mfma(*desc, q, k, v, cs, out, lse, s))
-    launch_na3d_fwd_ref(*desc, q, k, v, cs, out, lse, s);
-  return check_launch("strata_na3d_fwd");
+  return na3d_fwd_impl(desc, nullptr, q, k, v, cs, out, lse, stream);
+}
+
+strata_status strata_na3d_fwd_ex(const strata_na3d_desc* desc, const strata_na3d_opts* opts,
+                                 const void* q, const void* k, const void* v, const float* cs,
+                                 void* out, float* lse, void* stream) {
+  return na3d_fwd_impl(desc, opts, q, k, v, cs, out, lse, stream);
 }
 
 size_t strata_na3d_bwd_workspace_size(const strata_na3d_desc* desc) {
-  if (!desc || check_desc(desc) != STRATA_OK) return 0;
-  size_t n = (size_t)desc->B * desc->heads * desc->Z * desc->H * desc->W;
-  return ((n * sizeof(float)) + 255) & ~(size_t)255;
+  return bwd_workspace_impl(desc, nullptr);
+}
+
+size_t strata_na3d_bwd_ex_workspace_size(const strata_na3d_desc* desc,
+                                         const strata_na3d_opts* opts) {
+  return bwd_workspace_impl(desc, opts);
 }
 
 strata_status strata_na3d_bwd(const strata_na3d_desc* desc, const void* q, const void* k,
                               const void* v, const float* cs, const void* out, const void* dout,
                               const float* lse, void* dq, void* dk, void* dv, void* workspace,
                               size_t workspace_bytes, void* stream) {
-  strata_status st = check_desc(desc);
-  if (st != STRATA_OK) return st;
-  REQUIRE_PTR(q);
-  REQUIRE_PTR(k);
-  REQUIRE_PTR(v);
-  REQUIRE_PTR(out);
-  REQUIRE_PTR(dout);
-  REQUIRE_PTR(lse);
-  REQUIRE_PTR(dq);
-  REQUIRE_PTR(dk);
-  REQUIRE_PTR(dv);
-  if (cs) REQUIRE(aligned16(cs), "cs: not 16-byte aligned");
-  size_t need = strata_na3d_bwd_workspace_size(desc);
-  if (!workspace || workspace_bytes < need)
-    return set_error(STRATA_ERR_WORKSPACE, "workspace: need %zu bytes, got %zu", need,
-                     workspace ? workspace_bytes : (size_t)0);
-  REQUIRE(aligned16(workspace), "workspace: not 16-byte aligned");
-  hipStream_t s = (hipStream_t)stream;
-  float* dvec = static_cast<float*>(workspace);
-  launch_na3d_bwd_ref(0, *desc, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
-  if (!launch_na3d_bwd_dq_mfma(*desc, q, k, v, cs, dout, lse, dvec, dq, s))
-    launch_na3d_bwd_ref(1, *desc, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
-  if (!launch_na3d_bwd_dkdv_mfma(*desc, q, k, v, cs, dout, lse, dvec, dk, dv, s))
-    launch_na3d_bwd_ref(2, *desc, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
-  return check_launch("strata_na3d_bwd");
+  return na3d_bwd_impl(desc, nullptr, q, k, v, cs, out, dout, lse, dq, dk, dv, nullptr, workspace,
+                       workspace_bytes, stream);
+}
+
+strata_status strata_na3d_bwd_ex(const strata_na3d_desc* desc, const strata_na3d_opts* opts,
+                                 const void* q, const void* k, const void* v, const float* cs,
+                                 const void* out, const void* dout, const float* lse, void* dq,
+                                 void* dk, void* dv, void* dgate, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  return na3d_bwd_impl(desc, opts, q, k, v, cs, out, dout, lse, dq, dk, dv, dgate, workspace,
+                       workspace_bytes, stream);
 }
 
 static strata_status check_tiling(int32_t nty, int32_t ntx, int32_t P, int32_t Ht, int32_t Wt,

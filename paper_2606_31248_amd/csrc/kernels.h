@@ -9,6 +9,16 @@
 
 namespace strata {
 
+// Options of the attention block (App. B.5): RMS normalisation of q and k (no
+// learnable scale) and a sigmoid gate on the output, with logits of the
+// problem's dtype, one per (token, head) (gate_dim 1) or per channel.
+struct NaOpts {
+  int qk_norm = 0;
+  float eps = 0.f;
+  const void* gate = nullptr;
+  int gate_dim = 0;
+};
+
 void launch_axis_index(int L, int k, int32_t* starts, int32_t* qlo, int32_t* qhi, hipStream_t s);
 
 void launch_stereo_coords(const int32_t* face, const int32_t* oy, const int32_t* ox, int B, int H,
@@ -22,32 +32,52 @@ void launch_rope_apply(const void* x, void* y, const float* cs, int B, int heads
                        int W, int head_dim, strata_dtype dt, int transpose, hipStream_t s);
 
 // Plain per-query forward (float32 arithmetic), any supported dtype / head_dim.
-void launch_na3d_fwd_ref(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
-                         const float* cs, void* out, float* lse, hipStream_t s);
+void launch_na3d_fwd_ref(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k,
+                         const void* v, const float* cs, void* out, float* lse, hipStream_t s);
 
 // bf16 MFMA forward sweeping the key levels once per head (window 3x7x7, Z = 8);
 // returns false for any other problem.
-bool launch_na3d_fwd_zs(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
-                        const float* cs, void* out, float* lse, hipStream_t s);
+bool launch_na3d_fwd_zs(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k,
+                        const void* v, const float* cs, void* out, float* lse, hipStream_t s);
 
 // bf16 MFMA forward; returns false when the problem has no MFMA variant.
-bool launch_na3d_fwd_mfma(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
-                          const float* cs, void* out, float* lse, hipStream_t s);
+bool launch_na3d_fwd_mfma(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k,
+                          const void* v, const float* cs, void* out, float* lse, hipStream_t s);
+
+// Options of the attention backward kernels: QK RMSNorm (applied to q and k
+// as they are loaded, its Jacobian applied to dq and dk before the store) and
+// the low part of an upstream gradient given as two terms dO = hi + lo of the
+// problem's dtype (the gated dA = sigmoid(g) dO split exactly enough that its
+// rounding does not show); dout_lo = nullptr: dO is `dout` alone.
+struct BwdOpts {
+  int qk_norm = 0;
+  float eps = 0.f;
+  const void* dout_lo = nullptr;
+};
 
 // Plain backward (float32 arithmetic), one part per call: 0 = D = rowsum(dO * O)
 // into dvec, 1 = dq, 2 = dk and dv (parts 1 and 2 read dvec).
-void launch_na3d_bwd_ref(int part, const strata_na3d_desc& d, const void* q, const void* k,
-                         const void* v, const float* cs, const void* out, const void* dout,
-                         const float* lse, void* dq, void* dk, void* dv, float* dvec, hipStream_t s);
+void launch_na3d_bwd_ref(int part, const strata_na3d_desc& d, const BwdOpts& o, const void* q,
+                         const void* k, const void* v, const float* cs, const void* out,
+                         const void* dout, const float* lse, void* dq, void* dk, void* dv,
+                         float* dvec, hipStream_t s);
+
+// Row pass of the gated backward (one 16-byte piece per lane): D = rowsum(dO *
+// out) into dvec, dA = sigmoid(g) dO as da_hi (+ da_lo for bf16: the rounding
+// remainder, so that hi + lo carries dA to ~2^-16), and dgate.
+void launch_na3d_bwd_gate_prep(const strata_na3d_desc& d, const NaOpts& o, const void* out,
+                               const void* dout, float* dvec, void* da_hi, void* da_lo, void* dgate,
+                               hipStream_t s);
 
 // bf16 MFMA backward parts; each returns false when the problem has no MFMA variant.
 // dq: query-stationary (the forward's decomposition); dk/dv: key-stationary.
-bool launch_na3d_bwd_dq_mfma(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
-                             const float* cs, const void* dout, const float* lse,
-                             const float* dvec, void* dq, hipStream_t s);
-bool launch_na3d_bwd_dkdv_mfma(const strata_na3d_desc& d, const void* q, const void* k,
-                               const void* v, const float* cs, const void* dout, const float* lse,
-                               const float* dvec, void* dk, void* dv, hipStream_t s);
+bool launch_na3d_bwd_dq_mfma(const strata_na3d_desc& d, const BwdOpts& o, const void* q,
+                             const void* k, const void* v, const float* cs, const void* dout,
+                             const float* lse, const float* dvec, void* dq, hipStream_t s);
+bool launch_na3d_bwd_dkdv_mfma(const strata_na3d_desc& d, const BwdOpts& o, const void* q,
+                               const void* k, const void* v, const float* cs, const void* dout,
+                               const float* lse, const float* dvec, void* dk, void* dv,
+                               hipStream_t s);
 
 void launch_tile_blend(const void* tiles, int nty, int ntx, int P, int Ht, int Wt, int C, int sy,
                        int sx, const float* window, void* out, int Hf, int Wf, strata_dtype dt,

@@ -57,16 +57,16 @@ __device__ __forceinline__ uint4 rotate8h(uint4 x, float4 p01, float4 p23, float
 
 // Rotate 4 pairs held as packed bf16x2 words by float16 phases (c, s) in
 // packed float16 arithmetic (one multiply and one fused multiply-add per pair);
-// returns packed float16x2 words.  Inputs are clamped to +-46000 so that no
-// rotated value leaves the float16 range.
-__device__ __forceinline__ uint4 rotate8h_pk(uint4 x, uint4 ph) {
+// returns packed float16x2 words.  The inputs, times `mul` in float32, are
+// clamped to +-46000 so that no rotated value leaves the float16 range.
+__device__ __forceinline__ uint4 rotate8h_pk(uint4 x, uint4 ph, float mul = 1.f) {
   const uint32_t w[4] = {x.x, x.y, x.z, x.w};
   const uint32_t p[4] = {ph.x, ph.y, ph.z, ph.w};
   uint32_t r[4];
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
-    const float a = __builtin_amdgcn_fmed3f(lo_bf16(w[t]), -46000.f, 46000.f);
-    const float b = __builtin_amdgcn_fmed3f(hi_bf16(w[t]), -46000.f, 46000.f);
+    const float a = __builtin_amdgcn_fmed3f(lo_bf16(w[t]) * mul, -46000.f, 46000.f);
+    const float b = __builtin_amdgcn_fmed3f(hi_bf16(w[t]) * mul, -46000.f, 46000.f);
     const f16x2 ab = __builtin_convertvector((f32x2{a, b}), f16x2);
     const f16x2 cs = __builtin_bit_cast(f16x2, p[t]);
     const f16x2 aa = {ab.x, ab.x}, bb = {ab.y, ab.y}, ns = {-cs.y, cs.x};
@@ -118,6 +118,38 @@ __device__ __forceinline__ float sum_over_rows(float x) {
   x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
   r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Sum of squares of the 8 bf16 values of a 16-byte piece, added to acc (the
+// products are exact in float32).
+__device__ __forceinline__ float sumsq8(uint4 x, float acc) {
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[t]), __builtin_bit_cast(bf16x2, w[t]), acc,
+                                          false);
+  return acc;
+}
+
+// Sum over each aligned group of 8 consecutive lanes (every lane of the group
+// active): two quad permutations, then the mirror inside each half row.
+__device__ __forceinline__ float sum_over_8_lanes(float x) {
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x141, 0xF, 0xF, false));  // row_half_mirror
+  return x;
+}
+
+// Logistic sigmoid 1 / (1 + e^-g) of the output gate (hardware exp2 and
+// reciprocal; 0 and 1 at the extremes).
+__device__ __forceinline__ float sigmoid_fast(float g) {
+  return __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-1.4426950408889634f * g));
+}
+
+// Output-gate factors of 4 consecutive channels held as 4 bf16 in a uint2.
+__device__ __forceinline__ f32x4 sigmoid4_bf16(uint2 g) {
+  return f32x4{sigmoid_fast(lo_bf16(g.x)), sigmoid_fast(hi_bf16(g.x)), sigmoid_fast(lo_bf16(g.y)),
+               sigmoid_fast(hi_bf16(g.y))};
 }
 
 __device__ __forceinline__ float psum8(uint32_t a, uint32_t b, float acc) {

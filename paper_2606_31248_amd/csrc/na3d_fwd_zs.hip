@@ -59,6 +59,15 @@
 // Input range: K is converted to float16 with round-toward-zero before its
 // rotation (bf16 values convert exactly; beyond +-65504 they saturate); the
 // rotated, scaled Q saturates at +-65504.
+//
+// Options (App. B.5).  QK RMSNorm: the factor (mean square + eps)^(-1/2) of a
+// query comes from the sums of squares of the 4 lanes holding its row, that of
+// a key from the 8 lanes whose copies brought its row; each scales its vector
+// in float32 before the float16 rounding.  The normalised logits are bounded
+// by B = scale log2(e) head_dim, so the reference m is the constant B, folded
+// into the accumulator seed (no maxima, no rescaling).  Output gate: the logits
+// of a query level are loaded at the start of its last key level and sigmoid(g)
+// multiplies the normalised output at the store.
 #include "common.h"
 #include "kernels.h"
 #include "mfma_util.h"
@@ -132,6 +141,11 @@ struct ZArgs {
   int heads, H, W;
   int n_yb, n_xb, n_hg, hpw;
   float qscale;       // scale * log2(e)
+  // options: QK RMSNorm (eps; bound = a bound on every logit in log2 units
+  // once q and k are normalised) and the sigmoid output gate
+  float eps, bound;
+  const uint16_t* gate;
+  int gate_dim;
 };
 
 // Rotate 4 pairs of K held as packed bf16x2 words by packed float16 phases
@@ -139,13 +153,15 @@ struct ZArgs {
 // float16 range, saturating outside it), then in packed float16, the products
 // taking the halves of the phase word through the operand selects,
 //   t = (a c, a s),   r = (b, b) * (s, c) * (-1, 1) + t = (a c - b s, a s + b c).
-__device__ __forceinline__ uint4 rotate_k8(uint4 x, uint4 ph) {
+// With `mul` (the QK RMSNorm factor) the values are scaled in float32 first.
+__device__ __forceinline__ uint4 rotate_k8(uint4 x, uint4 ph, float mul = 1.f) {
   const uint32_t w[4] = {x.x, x.y, x.z, x.w};
   const uint32_t p[4] = {ph.x, ph.y, ph.z, ph.w};
   uint32_t r[4];
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
-    const uint32_t ab = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(lo_bf16(w[t]), hi_bf16(w[t])));
+    const uint32_t ab =
+        __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(lo_bf16(w[t]) * mul, hi_bf16(w[t]) * mul));
     uint32_t tt;
     asm("v_pk_mul_f16 %1, %2, %3 op_sel_hi:[0,1]\n\t"
         "v_pk_fma_f16 %0, %2, %3, %1 op_sel:[1,1,0] op_sel_hi:[1,0,1] neg_lo:[0,1,0]"
@@ -154,7 +170,7 @@ __device__ __forceinline__ uint4 rotate_k8(uint4 x, uint4 ph) {
   return make_uint4(r[0], r[1], r[2], r[3]);
 }
 
-template <int Z>
+template <int Z, bool NORM, bool GATE>
 __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
   __shared__ __attribute__((aligned(16))) char tK0[KTILE];
   __shared__ __attribute__((aligned(16))) char tV0[VTILE];
@@ -211,7 +227,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
       const int u = 16 * c + 4 * g + i;
       const int ky = uy0 + u / NUX, kx = ux0 + u % NUX;
       const bool ok = u < NU && ky >= wys && ky < wys + KY && kx >= wxs && kx < wxs + KX;
-      bias[c][i] = ok ? 0.f : -INFINITY;
+      bias[c][i] = ok ? (NORM ? -a.bound : 0.f) : -INFINITY;
     }
   }
 
@@ -263,13 +279,19 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
   };
   // Rotate this thread's K slots in place (bf16 -> scaled float16).  A thread's
   // copies land in its own slots, so its own wait suffices.
+  // With QK RMSNorm the 8 slots of a key row (8 consecutive lanes) add their
+  // sums of squares for the row's factor.
   auto rotate_k = [&](char* tk) {
     uint4 x[ITK];  // all reads before any write: the slots are distinct, which the compiler cannot tell
 #pragma unroll
     for (int it = 0; it < ITK; ++it) x[it] = ld16(tk + (it * kThreads + tid) * 16);
+    float rn[ITK];
 #pragma unroll
     for (int it = 0; it < ITK; ++it)
-      st16(tk + (it * kThreads + tid) * 16, rotate_k8(x[it], ld16(sph + (it * kThreads + tid) * 16)));
+      rn[it] = NORM ? __builtin_amdgcn_rsqf(sum_over_8_lanes(sumsq8(x[it], 0.f)) * (1.f / kD) + a.eps) : 1.f;
+#pragma unroll
+    for (int it = 0; it < ITK; ++it)
+      st16(tk + (it * kThreads + tid) * 16, rotate_k8(x[it], ld16(sph + (it * kThreads + tid) * 16), rn[it]));
   };
   // raw query rows of one level (two 16-byte pieces per lane)
   auto load_q = [&](int h, int z, uint4& x0, uint4& x1) {
@@ -279,12 +301,15 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
   };
   auto prep_q = [&](const float4* cq, uint4 x0, uint4 x1, f16x8& q0, f16x8& q1) {
     uint4 r0, r1;
+    float mul = a.qscale;
+    if constexpr (NORM)  // the 4 lanes of a query row hold its 64 values
+      mul *= __builtin_amdgcn_rsqf(sum_over_rows(sumsq8(x1, sumsq8(x0, 0.f))) * (1.f / kD) + a.eps);
     if (cq) {
-      r0 = rotate8h(x0, cq[2 * g], cq[2 * g + 1], a.qscale);
-      r1 = rotate8h(x1, cq[8 + 2 * g], cq[8 + 2 * g + 1], a.qscale);
+      r0 = rotate8h(x0, cq[2 * g], cq[2 * g + 1], mul);
+      r1 = rotate8h(x1, cq[8 + 2 * g], cq[8 + 2 * g + 1], mul);
     } else {
-      r0 = scale8h(x0, a.qscale);
-      r1 = scale8h(x1, a.qscale);
+      r0 = scale8h(x0, mul);
+      r1 = scale8h(x1, mul);
     }
     q0 = __builtin_bit_cast(f16x8, r0);
     q1 = __builtin_bit_cast(f16x8, r1);
@@ -299,6 +324,8 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
   bool mset[Z];     // wave-uniform: m is non-zero somewhere in the wave
   f32x4 o[Z][4];
   uint4 qraw[Z][2];
+  uint2 gch[GATE ? Z : 1][4];  // gate logits (bf16) of a level, loaded at the start of its last key level
+  uint32_t ghd[GATE ? Z : 1];
 
   // K and V fragments of one key level (shared by every active query level)
   struct Frags {
@@ -340,30 +367,32 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
       s[c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(f.k[c][1], qf[z][1], acc, 0, 0, 0);
     }
     hook(NC);
-    float mx = fmaxf(fmaxf(s[0][0], s[0][1]), s[0][2]);
-    mx = fmaxf(fmaxf(mx, s[0][3]), s[1][0]);
+    if constexpr (!NORM) {  // with QK RMSNorm the seed already subtracted the bound
+      float mx = fmaxf(fmaxf(s[0][0], s[0][1]), s[0][2]);
+      mx = fmaxf(fmaxf(mx, s[0][3]), s[1][0]);
 #pragma unroll
-    for (int c = 1; c < NC; ++c) {
-      if (c > 1) mx = fmaxf(fmaxf(mx, s[c][0]), s[c][1]);
-      else mx = fmaxf(mx, s[c][1]);
-      mx = fmaxf(fmaxf(mx, s[c][2]), s[c][3]);
-    }
-    mx = max_over_rows(mx);
-    const bool move = mx > m[z] + kLazy || (first && mx < kLow);
-    if (__any(move)) {  // rare: move the reference m
-      const float mn = move ? mx : m[z];
-      if constexpr (!first) {  // nothing is accumulated before a level's first key level
-        const float alpha = __builtin_amdgcn_exp2f(m[z] - mn);
-        lsum[z] *= alpha;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) o[z][t] *= alpha;
+      for (int c = 1; c < NC; ++c) {
+        if (c > 1) mx = fmaxf(fmaxf(mx, s[c][0]), s[c][1]);
+        else mx = fmaxf(mx, s[c][1]);
+        mx = fmaxf(fmaxf(mx, s[c][2]), s[c][3]);
       }
-      m[z] = mn;
-      mset[z] = true;
-    }
-    if (mset[z]) {
+      mx = max_over_rows(mx);
+      const bool move = mx > m[z] + kLazy || (first && mx < kLow);
+      if (__any(move)) {  // rare: move the reference m
+        const float mn = move ? mx : m[z];
+        if constexpr (!first) {  // nothing is accumulated before a level's first key level
+          const float alpha = __builtin_amdgcn_exp2f(m[z] - mn);
+          lsum[z] *= alpha;
 #pragma unroll
-      for (int c = 0; c < NC; ++c) s[c] -= m[z];
+          for (int t = 0; t < 4; ++t) o[z][t] *= alpha;
+        }
+        m[z] = mn;
+        mset[z] = true;
+      }
+      if (mset[z]) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c) s[c] -= m[z];
+      }
     }
     uint32_t pk[NC][2];
 #pragma unroll
@@ -427,7 +456,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
         constexpr int z = decltype(Zi)::v;
         if constexpr (zstart<Z>(z) == p) {
           prep_q(cq, qraw[z][0], qraw[z][1], qf[z][0], qf[z][1]);
-          m[z] = 0.f;
+          m[z] = NORM ? a.bound : 0.f;
           lsum[z] = f32x4{0.f, 0.f, 0.f, 0.f};
           mset[z] = false;
 #pragma unroll
@@ -441,6 +470,23 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
         if constexpr (p + 1 == Z && zstart<Z>(z) == 0)
           if (more_heads) load_q(h + 1, z, qraw[z][0], qraw[z][1]);
       });
+
+      // gate logits of the levels that end at this key level (used at their store)
+      if constexpr (GATE) {
+        static_for<Z>([&](auto Zi) {
+          constexpr int z = decltype(Zi)::v;
+          if constexpr (zstart<Z>(z) + KZ - 1 == p) {
+            const int64_t tok = level_base(h, z) + (int64_t)qy * W + qx;
+            if (a.gate_dim == 1) {
+              ghd[z] = a.gate[tok];
+            } else {
+              const uint2* src = reinterpret_cast<const uint2*>(a.gate + tok * kD);
+#pragma unroll
+              for (int t = 0; t < 4; ++t) gch[z][t] = src[4 * t + g];
+            }
+          }
+        });
+      }
 
       // ---- the active query levels [zlo, zhi], sharing this level's fragments -
       // After the last of them, wait for the next level's copies (issued at the
@@ -477,13 +523,18 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
         if constexpr (zstart<Z>(z) + KZ - 1 == p) {
           const float lt = lsum[z][0];
           if (in_grid) {
-            const float inv = 1.f / lt;
+            float inv = 1.f / lt;
+            if constexpr (GATE)
+              if (a.gate_dim == 1) inv *= sigmoid_fast(__uint_as_float(ghd[z] << 16));
             const int64_t tok = level_base(h, z) + (int64_t)qy * W + qx;
             uint2* dst = reinterpret_cast<uint2*>(a.out + tok * kD);
 #pragma unroll
-            for (int t = 0; t < 4; ++t)  // d = 16t + 4g + i
-              dst[4 * t + g] = make_uint2(pack2(o[z][t][0] * inv, o[z][t][1] * inv),
-                                          pack2(o[z][t][2] * inv, o[z][t][3] * inv));
+            for (int t = 0; t < 4; ++t) {  // d = 16t + 4g + i
+              f32x4 r = o[z][t] * inv;
+              if constexpr (GATE)
+                if (a.gate_dim != 1) r *= sigmoid4_bf16(gch[z][t]);
+              dst[4 * t + g] = make_uint2(pack2(r[0], r[1]), pack2(r[2], r[3]));
+            }
             if (a.lse && g == 0) a.lse[tok] = (m[z] + __log2f(lt)) * kLn2;
           }
         }
@@ -498,12 +549,22 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
 
 // Level-sweep forward for the 3x7x7 window at Z = 8 (bf16, head_dim 64); false
 // when the problem is not that shape.
-bool launch_na3d_fwd_zs(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
-                        const float* cs, void* out, float* lse, hipStream_t s) {
+bool launch_na3d_fwd_zs(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k,
+                        const void* v, const float* cs, void* out, float* lse, hipStream_t s) {
   if (d.dtype != STRATA_BF16 || d.head_dim != kD) return false;
   if (d.kz != KZ || d.ky != KY || d.kx != KX || d.Z != 8) return false;
   if ((int64_t)d.H * d.W * kD * 2 >= (int64_t)1 << 32) return false;  // byte offsets in 32 bits
+  // With QK RMSNorm |q^| and |k^| are below sqrt(head_dim), so every logit lies
+  // within B = scale log2(e) head_dim of 0 (the margin covers the float16
+  // rounding of both operands).  The softmax then subtracts B throughout, which
+  // keeps every weight in [2^-2B, 1]: B <= 60 keeps them normal floats.
+  const float bound = d.scale * kLog2e * kD * (1.f + 1.f / 256.f);
+  if (o.qk_norm && !(bound <= 60.f)) return false;
   ZArgs a = {};
+  a.eps = o.eps;
+  a.bound = bound;
+  a.gate = static_cast<const uint16_t*>(o.gate);
+  a.gate_dim = o.gate_dim;
   a.q = static_cast<const uint16_t*>(q);
   a.k = static_cast<const uint16_t*>(k);
   a.v = static_cast<const uint16_t*>(v);
@@ -520,7 +581,11 @@ bool launch_na3d_fwd_zs(const strata_na3d_desc& d, const void* q, const void* k,
   a.qscale = d.scale * kLog2e;
   const int64_t blocks = (int64_t)d.B * a.n_hg * a.n_yb * a.n_xb;
   if (blocks >= (int64_t)1 << 31) return false;
-  hipLaunchKernelGGL((na3d_fwd_zs_kernel<8>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
+  const dim3 grid((unsigned)blocks), block(kThreads);
+  if (o.qk_norm && o.gate) hipLaunchKernelGGL((na3d_fwd_zs_kernel<8, true, true>), grid, block, 0, s, a);
+  else if (o.qk_norm) hipLaunchKernelGGL((na3d_fwd_zs_kernel<8, true, false>), grid, block, 0, s, a);
+  else if (o.gate) hipLaunchKernelGGL((na3d_fwd_zs_kernel<8, false, true>), grid, block, 0, s, a);
+  else hipLaunchKernelGGL((na3d_fwd_zs_kernel<8, false, false>), grid, block, 0, s, a);
   return true;
 }
 

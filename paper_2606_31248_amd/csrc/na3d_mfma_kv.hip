@@ -34,6 +34,11 @@
 //                                            rescaled exactly when E grows.
 // At the end dK = R^T (scale 2^(E-15) dK~) and dV is stored as is.
 //
+// Options: QK RMSNorm scales the stationary keys and the staged queries in
+// float32 before their float16 rounding and applies the norm's Jacobian to dK
+// before the store; a two-term dO = hi + lo (the gated upstream gradient) is
+// staged as a third tile and adds one MFMA to Y and one to dV per step.
+//
 // Staged rows are 128 bytes (Q~ in float16, dO in bf16) with their 16-byte
 // columns XOR-swizzled by sigma(u) = ((u >> 1) & 3) << 1 | ((u >> 3) & 1) of the
 // box index u: the 16 rows of a chunk read at one column hit 16 distinct bank
@@ -61,7 +66,7 @@ constexpr int kMinExp = -100;    // lower bound of the dS exponent (keeps 2^(15-
 // ZK key levels per workgroup (one wave each); NBUF = 2: double-buffered query
 // tiles, one workgroup per CU; NBUF = 1: single buffer, small enough for two
 // workgroups per CU, which then hide each other's copies and barriers.
-template <int KZ, int KY, int KX, int ZK, int NBUF>
+template <int KZ, int KY, int KX, int ZK, int NBUF, bool LO>
 struct KvCfg {
   static constexpr int kThreads = 64 * ZK;
   static constexpr int MQY = 4 + 3 * (KY / 2), MQX = 4 + 3 * (KX / 2);  // largest query box
@@ -70,8 +75,8 @@ struct KvCfg {
   static constexpr int SLOTS = MQ * (kRow / 16);
   static constexpr int IT = (SLOTS + kThreads - 1) / kThreads;           // copy slots per thread
   static constexpr int IS = (MQ + kThreads - 1) / kThreads;              // LSE / D entries per thread
-  static constexpr int LDS = NBUF * (2 * TBYTES + 2 * MQ * 4) + MQ * 2;
-  static constexpr int WG_PER_CU = NBUF == 2 ? 1 : 2;
+  static constexpr int LDS = NBUF * ((LO ? 3 : 2) * TBYTES + 2 * MQ * 4) + MQ * 2;
+  static constexpr int WG_PER_CU = NBUF == 1 && 2 * LDS <= kLdsMax ? 2 : 1;
   static_assert(LDS * WG_PER_CU <= kLdsMax, "query tiles exceed LDS");
 };
 
@@ -88,6 +93,9 @@ struct KvArgs {
   int heads, Z, H, W;
   int n_zb, n_yb, n_xb;
   float scale, kscale;   // scale, scale * log2(e)
+  int qk_norm;           // QK RMSNorm of the stationary keys and the staged queries
+  float eps;
+  const uint16_t* dout_lo;  // low term of a two-term dO (with LO)
 };
 
 // queries whose (border-clamped) window holds position j of an axis of extent L
@@ -96,15 +104,18 @@ __host__ __device__ __forceinline__ int inv_hi(int j, int L, int k) { return j >
 
 __device__ __forceinline__ int rswz(int u) { return (((u >> 1) & 3) << 1) | ((u >> 3) & 1); }
 
-template <int KZ, int KY, int KX, int ZK, int NBUF>
-__global__ void __launch_bounds__(64 * ZK, (NBUF == 2 ? 1 : 2)) na3d_mfma_kv_kernel(KvArgs a) {
-  using C = KvCfg<KZ, KY, KX, ZK, NBUF>;
+template <int KZ, int KY, int KX, int ZK, int NBUF, bool LO, bool NORM>
+__global__ void __launch_bounds__(64 * ZK, (KvCfg<KZ, KY, KX, ZK, NBUF, LO>::WG_PER_CU)) na3d_mfma_kv_kernel(KvArgs a) {
+  using C = KvCfg<KZ, KY, KX, ZK, NBUF, LO>;
   constexpr int kThreads = C::kThreads;
   constexpr int T2 = NBUF == 2 ? C::TBYTES : 16, M2 = NBUF == 2 ? C::MQ : 4;
+  constexpr int TL0 = LO ? C::TBYTES : 16, TL1 = LO && NBUF == 2 ? C::TBYTES : 16;
   __shared__ __attribute__((aligned(16))) char tQ0[C::TBYTES];
   __shared__ __attribute__((aligned(16))) char tG0[C::TBYTES];
   __shared__ __attribute__((aligned(16))) char tQ1[T2];
   __shared__ __attribute__((aligned(16))) char tG1[T2];
+  __shared__ __attribute__((aligned(16))) char tL0[TL0];  // low term of dO (LO)
+  __shared__ __attribute__((aligned(16))) char tL1[TL1];
   __shared__ __attribute__((aligned(16))) float sL0[C::MQ];
   __shared__ __attribute__((aligned(16))) float sD0[C::MQ];
   __shared__ __attribute__((aligned(16))) float sL1[M2];
@@ -164,9 +175,11 @@ __global__ void __launch_bounds__(64 * ZK, (NBUF == 2 ? 1 : 2)) na3d_mfma_kv_ker
     const uint4 z = make_uint4(0u, 0u, 0u, 0u);
     st16(tQ0 + i * 16, z);
     st16(tG0 + i * 16, z);
+    if constexpr (LO) st16(tL0 + i * 16, z);
     if constexpr (NBUF == 2) {
       st16(tQ1 + i * 16, z);
       st16(tG1 + i * 16, z);
+      if constexpr (LO) st16(tL1 + i * 16, z);
     }
   }
 
@@ -201,15 +214,17 @@ __global__ void __launch_bounds__(64 * ZK, (NBUF == 2 ? 1 : 2)) na3d_mfma_kv_ker
     pd[is] = 0.f;
   }
 
-  auto issue = [&](int p, char* tq, char* tg) {
+  auto issue = [&](int p, char* tq, char* tg, char* tl) {
     const int64_t lev = bh_base + (int64_t)p * HW;
     const uint16_t* qp = a.q + lev * kD;
     const uint16_t* gp = a.dout + lev * kD;
+    const uint16_t* lp = LO ? a.dout_lo + lev * kD : nullptr;
 #pragma unroll
     for (int it = 0; it < C::IT; ++it) {
       if (goff[it] < 0) continue;
       copy16_to_lds(qp + goff[it], tq + (it * kThreads + wave * 64) * 16);
       copy16_to_lds(gp + goff[it], tg + (it * kThreads + wave * 64) * 16);
+      if constexpr (LO) copy16_to_lds(lp + goff[it], tl + (it * kThreads + wave * 64) * 16);
     }
 #pragma unroll
     for (int is = 0; is < C::IS; ++is) {
@@ -219,7 +234,9 @@ __global__ void __launch_bounds__(64 * ZK, (NBUF == 2 ? 1 : 2)) na3d_mfma_kv_ker
     }
   };
   // wait for this thread's copies and loads, rotate its own Q slots in place
-  // (bf16 -> float16), store its LSE / D entries
+  // (bf16 -> float16; with QK RMSNorm the 8 slots of a row, 8 consecutive
+  // lanes all in or all past the box, add their sums of squares for the row's
+  // factor), store its LSE / D entries
   auto finish = [&](char* tq, float* sl, float* sd) {
     __builtin_amdgcn_s_waitcnt(0);
 #pragma unroll
@@ -227,7 +244,8 @@ __global__ void __launch_bounds__(64 * ZK, (NBUF == 2 ? 1 : 2)) na3d_mfma_kv_ker
       if (goff[it] < 0) continue;
       char* ad = tq + (it * kThreads + tid) * 16;
       const uint4 x = ld16(ad);
-      st16(ad, csb ? rotate8h_pk(x, ph[it]) : scale8h(x, 1.f));
+      const float mul = NORM ? __builtin_amdgcn_rsqf(sum_over_8_lanes(sumsq8(x, 0.f)) * (1.f / kD) + a.eps) : 1.f;
+      st16(ad, csb ? rotate8h_pk(x, ph[it], mul) : scale8h(x, mul));
     }
 #pragma unroll
     for (int is = 0; is < C::IS; ++is) {
@@ -247,16 +265,19 @@ __global__ void __launch_bounds__(64 * ZK, (NBUF == 2 ? 1 : 2)) na3d_mfma_kv_ker
   const float4* csk = csb ? csb + ((int64_t)ky * W + kx) * 16 : nullptr;
   f16x8 kf[2];
   bf16x8 vf[2];
+  float rk = 1.f;  // QK RMSNorm factor of this lane's key
   {
     const uint4* src = reinterpret_cast<const uint4*>(a.k + ktok * kD);
     const uint4 x0v = src[g], x1v = src[4 + g];
+    if constexpr (NORM)  // the 4 lanes of a key row hold its 64 values
+      rk = __builtin_amdgcn_rsqf(sum_over_rows(sumsq8(x1v, sumsq8(x0v, 0.f))) * (1.f / kD) + a.eps);
     uint4 r0, r1;
     if (csk) {
-      r0 = rotate8h(x0v, csk[2 * g], csk[2 * g + 1], a.kscale);
-      r1 = rotate8h(x1v, csk[8 + 2 * g], csk[8 + 2 * g + 1], a.kscale);
+      r0 = rotate8h(x0v, csk[2 * g], csk[2 * g + 1], a.kscale * rk);
+      r1 = rotate8h(x1v, csk[8 + 2 * g], csk[8 + 2 * g + 1], a.kscale * rk);
     } else {
-      r0 = scale8h(x0v, a.kscale);
-      r1 = scale8h(x1v, a.kscale);
+      r0 = scale8h(x0v, a.kscale * rk);
+      r1 = scale8h(x1v, a.kscale * rk);
     }
     kf[0] = __builtin_bit_cast(f16x8, r0);
     kf[1] = __builtin_bit_cast(f16x8, r1);
@@ -280,7 +301,7 @@ __global__ void __launch_bounds__(64 * ZK, (NBUF == 2 ? 1 : 2)) na3d_mfma_kv_ker
   const int trow = 4 * g + (qn >> 2);
   const uint32_t toff = trow * kRow + ((((qn >> 1) & 1) ^ rswz(trow)) << 4) + 8 * (qn & 1);
 
-  auto compute = [&](const char* tq, const char* tg, const float* sl, const float* sd) {
+  auto compute = [&](const char* tq, const char* tg, const char* tl, const float* sl, const float* sd) {
     for (int st = 0; st < npairs; ++st) {
       f32x4 x[2], y[2];
 #pragma unroll
@@ -307,6 +328,13 @@ __global__ void __launch_bounds__(64 * ZK, (NBUF == 2 ? 1 : 2)) na3d_mfma_kv_ker
         x[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(q1, kf[1], x[h], 0, 0, 0);
         y[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(g0, vf[0], ys, 0, 0, 0);
         y[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(g1, vf[1], y[h], 0, 0, 0);
+        if constexpr (LO) {
+          const char* rl = tl + c * (16 * kRow);
+          const bf16x8 l0 = __builtin_bit_cast(bf16x8, ld16(rl + aoff));
+          const bf16x8 l1 = __builtin_bit_cast(bf16x8, ld16(rl + (aoff ^ 64u)));
+          y[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(l0, vf[0], y[h], 0, 0, 0);
+          y[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(l1, vf[1], y[h], 0, 0, 0);
+        }
       }
       // exponent bound of |Y| for this lane's key (all four row groups)
       float my = 0.f;
@@ -344,6 +372,13 @@ __global__ void __launch_bounds__(64 * ZK, (NBUF == 2 ? 1 : 2)) na3d_mfma_kv_ker
         const uint2 g_hi = __builtin_bit_cast(uint2, tr_read(tg0 + 16 * kRow + o0));
         const bf16x8 gt = __builtin_bit_cast(bf16x8, make_uint4(g_lo.x, g_lo.y, g_hi.x, g_hi.y));
         accV[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gt, pf, accV[t], 0, 0, 0);
+        if constexpr (LO) {
+          const char* tl0 = tl + st * (32 * kRow);
+          const uint2 l_lo = __builtin_bit_cast(uint2, tr_read(tl0 + o0));
+          const uint2 l_hi = __builtin_bit_cast(uint2, tr_read(tl0 + 16 * kRow + o0));
+          const bf16x8 lt = __builtin_bit_cast(bf16x8, make_uint4(l_lo.x, l_lo.y, l_hi.x, l_hi.y));
+          accV[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lt, pf, accV[t], 0, 0, 0);
+        }
         const uint2 q_lo = __builtin_bit_cast(uint2, tr_read(tq0 + o0));
         const uint2 q_hi = __builtin_bit_cast(uint2, tr_read(tq0 + 16 * kRow + o0));
         const f16x8 qt = __builtin_bit_cast(f16x8, make_uint4(q_lo.x, q_lo.y, q_hi.x, q_hi.y));
@@ -366,26 +401,26 @@ __global__ void __launch_bounds__(64 * ZK, (NBUF == 2 ? 1 : 2)) na3d_mfma_kv_ker
   if constexpr (NBUF == 1) {
     // one buffer: copy, publish, compute, and a barrier before the next copy
     for (int p = p_lo; p <= p_hi; ++p) {
-      issue(p, tQ0, tG0);
+      issue(p, tQ0, tG0, tL0);
       finish(tQ0, sL0, sD0);
       __syncthreads();
-      if (active(p)) compute(tQ0, tG0, sL0, sD0);
+      if (active(p)) compute(tQ0, tG0, tL0, sL0, sD0);
       __syncthreads();
     }
   } else {
-  issue(p_lo, tQ0, tG0);
+  issue(p_lo, tQ0, tG0, tL0);
   finish(tQ0, sL0, sD0);
   __syncthreads();
   for (int p = p_lo; p <= p_hi; p += 2) {
     const bool more1 = p + 1 <= p_hi;
-    if (more1) issue(p + 1, tQ1, tG1);
-    if (active(p)) compute(tQ0, tG0, sL0, sD0);
+    if (more1) issue(p + 1, tQ1, tG1, tL1);
+    if (active(p)) compute(tQ0, tG0, tL0, sL0, sD0);
     if (more1) {
       finish(tQ1, sL1, sD1);
       __syncthreads();
       const bool more2 = p + 2 <= p_hi;
-      if (more2) issue(p + 2, tQ0, tG0);
-      if (active(p + 1)) compute(tQ1, tG1, sL1, sD1);
+      if (more2) issue(p + 2, tQ0, tG0, tL0);
+      if (active(p + 1)) compute(tQ1, tG1, tL1, sL1, sD1);
       if (more2) {
         finish(tQ0, sL0, sD0);
         __syncthreads();
@@ -395,21 +430,44 @@ __global__ void __launch_bounds__(64 * ZK, (NBUF == 2 ? 1 : 2)) na3d_mfma_kv_ker
   }
 
   // ---- store: dV, and dK = R^T (scale 2^(E-15) dK~); lane holds d = 16t + 4g + i ----
-  if (!wave_on || ky_raw >= H || kx_raw >= W) return;
+  // With QK RMSNorm that is the gradient of k^ = r k, carried back through the
+  // norm: dk = r (dk^ - k^ mean(dk^ k^)), k^ from the raw row in float32.
   const float f = a.scale * __builtin_amdgcn_ldexpf(1.f, ex - 15);
+  f32x4 xk[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    xk[t] = accK[t] * f;
+    if (csk) {
+      const float4 p = csk[4 * t + g];  // pairs 8t+2g and 8t+2g+1
+      const float r0 = fmaf(xk[t][0], p.x, xk[t][1] * p.y), r1 = fmaf(xk[t][1], p.x, -xk[t][0] * p.y);
+      const float r2 = fmaf(xk[t][2], p.z, xk[t][3] * p.w), r3 = fmaf(xk[t][3], p.z, -xk[t][2] * p.w);
+      xk[t] = f32x4{r0, r1, r2, r3};
+    }
+  }
+  if constexpr (NORM) {
+    const uint2* kr = reinterpret_cast<const uint2*>(a.k + ktok * kD);
+    f32x4 kh[4];
+    float c = 0.f;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const uint2 w = kr[4 * t + g];
+      kh[t] = f32x4{lo_bf16(w.x), hi_bf16(w.x), lo_bf16(w.y), hi_bf16(w.y)} * rk;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) c = fmaf(xk[t][i], kh[t][i], c);
+    }
+    c = sum_over_rows(c) * (1.f / kD);
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) xk[t][i] = rk * fmaf(-kh[t][i], c, xk[t][i]);
+  }
+  if (!wave_on || ky_raw >= H || kx_raw >= W) return;
   uint2* dkd = reinterpret_cast<uint2*>(a.dk + ktok * kD);
   uint2* dvd = reinterpret_cast<uint2*>(a.dv + ktok * kD);
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
     dvd[4 * t + g] = make_uint2(pack2(accV[t][0], accV[t][1]), pack2(accV[t][2], accV[t][3]));
-    float x0v = accK[t][0] * f, x1v = accK[t][1] * f, x2v = accK[t][2] * f, x3v = accK[t][3] * f;
-    if (csk) {
-      const float4 p = csk[4 * t + g];  // pairs 8t+2g and 8t+2g+1
-      const float r0 = fmaf(x0v, p.x, x1v * p.y), r1 = fmaf(x1v, p.x, -x0v * p.y);
-      const float r2 = fmaf(x2v, p.z, x3v * p.w), r3 = fmaf(x3v, p.z, -x2v * p.w);
-      x0v = r0; x1v = r1; x2v = r2; x3v = r3;
-    }
-    dkd[4 * t + g] = make_uint2(pack2(x0v, x1v), pack2(x2v, x3v));
+    dkd[4 * t + g] = make_uint2(pack2(xk[t][0], xk[t][1]), pack2(xk[t][2], xk[t][3]));
   }
 }
 
@@ -423,9 +481,9 @@ int max_box(int L, int k) {
   return mx;
 }
 
-template <int KZ, int KY, int KX, int ZK, int NBUF>
+template <int KZ, int KY, int KX, int ZK, int NBUF, bool LO>
 bool launch_kv(const strata_na3d_desc& d, const KvArgs& a0, hipStream_t s) {
-  using C = KvCfg<KZ, KY, KX, ZK, NBUF>;
+  using C = KvCfg<KZ, KY, KX, ZK, NBUF, LO>;
   if (max_box(d.H, KY) > C::MQY || max_box(d.W, KX) > C::MQX) return false;
   KvArgs a = a0;
   a.n_zb = (d.Z + ZK - 1) / ZK;
@@ -433,16 +491,21 @@ bool launch_kv(const strata_na3d_desc& d, const KvArgs& a0, hipStream_t s) {
   a.n_xb = (d.W + 3) / 4;
   const int64_t blocks = (int64_t)d.B * d.heads * a.n_zb * a.n_yb * a.n_xb;
   if (blocks >= (int64_t)1 << 31) return false;
-  hipLaunchKernelGGL((na3d_mfma_kv_kernel<KZ, KY, KX, ZK, NBUF>), dim3((unsigned)blocks), dim3(C::kThreads), 0,
-                     s, a);
+  if (a.qk_norm)
+    hipLaunchKernelGGL((na3d_mfma_kv_kernel<KZ, KY, KX, ZK, NBUF, LO, true>), dim3((unsigned)blocks),
+                       dim3(C::kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL((na3d_mfma_kv_kernel<KZ, KY, KX, ZK, NBUF, LO, false>), dim3((unsigned)blocks),
+                       dim3(C::kThreads), 0, s, a);
   return true;
 }
 
 }  // namespace
 
-bool launch_na3d_bwd_dkdv_mfma(const strata_na3d_desc& d, const void* q, const void* k,
-                               const void* v, const float* cs, const void* dout, const float* lse,
-                               const float* dvec, void* dk, void* dv, hipStream_t s) {
+bool launch_na3d_bwd_dkdv_mfma(const strata_na3d_desc& d, const BwdOpts& o, const void* q,
+                               const void* k, const void* v, const float* cs, const void* dout,
+                               const float* lse, const float* dvec, void* dk, void* dv,
+                               hipStream_t s) {
   if (d.dtype != STRATA_BF16 || d.head_dim != kD) return false;
   if ((int64_t)d.H * d.W * kD >= (int64_t)1 << 31) return false;
   KvArgs a = {};
@@ -461,11 +524,19 @@ bool launch_na3d_bwd_dkdv_mfma(const strata_na3d_desc& d, const void* q, const v
   a.W = d.W;
   a.scale = d.scale;
   a.kscale = d.scale * kLog2e;
+  a.qk_norm = o.qk_norm;
+  a.eps = o.eps;
+  a.dout_lo = static_cast<const uint16_t*>(o.dout_lo);
   // measured on MI355X at 16 tiles x 16 heads x 8x64x64: 3x7x7 is faster with two
   // single-buffered 4-level workgroups per CU (9.8 vs 11.6 ms for the whole
   // backward), 5x9x9 with one double-buffered 8-level workgroup (18.2 vs 18.4 ms)
-  if (d.kz == 3 && d.ky == 7 && d.kx == 7) return launch_kv<3, 7, 7, 4, 1>(d, a, s);
-  if (d.kz == 5 && d.ky == 9 && d.kx == 9) return launch_kv<5, 9, 9, 8, 2>(d, a, s);
+  // A two-term dO adds a third staged tile: 5x9x9 then fits one single-buffered
+  // workgroup per CU.
+  const bool lo = o.dout_lo != nullptr;
+  if (d.kz == 3 && d.ky == 7 && d.kx == 7)
+    return lo ? launch_kv<3, 7, 7, 4, 1, true>(d, a, s) : launch_kv<3, 7, 7, 4, 1, false>(d, a, s);
+  if (d.kz == 5 && d.ky == 9 && d.kx == 9)
+    return lo ? launch_kv<5, 9, 9, 8, 1, true>(d, a, s) : launch_kv<5, 9, 9, 8, 2, false>(d, a, s);
   return false;
 }
 

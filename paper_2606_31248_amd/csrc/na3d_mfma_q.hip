@@ -33,6 +33,11 @@
 // of an output, beyond the parity bound; float16 keeps it near 0.05%.  Rotated
 // values beyond the float16 range (|x| > 65504) saturate.  P and V stay bf16.
 // The logit scale and log2(e) are folded into Q so the softmax uses exp2.
+// Options: QK RMSNorm (the factor of every query and key, from its sum of
+// squares over the lanes that hold it, scales it in float32 before the float16
+// rounding; the backward applies the norm's Jacobian to dQ before the store),
+// the sigmoid gate applied with the final 1/l (forward), and dO given as two
+// bf16 terms hi + lo (backward: one more MFMA pair for Y).
 //
 // K rows are 128 bytes with their 16-byte columns XOR-swizzled by
 // ((x >> 1) + 5 y) & 7 of the key's box position: the 16 keys of any chunk of an
@@ -116,10 +121,25 @@ struct Args {
   int n_zb, n_yb, n_xb;
   float qscale;       // scale * log2(e)
   float scale;
+  // options: QK RMSNorm (factor applied in float32 before the float16
+  // rounding), the sigmoid output gate (forward), the low term of a two-term
+  // dO (backward)
+  int qk_norm;
+  float eps;
+  const uint16_t* gate;
+  int gate_dim;
+  const uint16_t* dout_lo;
 };
 
-template <int KZ, int KY, int KX, int ZQ, bool BWD>
+// OPT: bit 0 = QK RMSNorm; bit 1 = the output gate (forward) or the low term of
+// a two-term dO (backward)
+constexpr int kNorm = 1, kOpt2 = 2;
+
+template <int KZ, int KY, int KX, int ZQ, bool BWD, int OPT>
 __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
+  constexpr bool NORM = (OPT & kNorm) != 0;
+  constexpr bool GATE = !BWD && (OPT & kOpt2) != 0;
+  constexpr bool LO = BWD && (OPT & kOpt2) != 0;
   using C = Cfg<KZ, KY, KX, ZQ>;
   // double buffer of key tiles (distinct objects, see above), copy offsets, phases
   __shared__ __attribute__((aligned(16))) char tK0[C::KBYTES];
@@ -253,6 +273,9 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
   }
   // Rotate (or convert) this thread's K slots of one tile in place, bf16 -> float16.
   // A thread's copies land in its own slots, so its own wait suffices: no barrier.
+  // With QK RMSNorm the 8 slots of a key (8 consecutive lanes, all in or all
+  // past the tile) add their sums of squares, and the factor scales the values
+  // in float32 before they are rounded.
   auto rotate_k = [&](char* tk) {
 #pragma unroll
     for (int it = 0; it < C::ITK; ++it) {
@@ -260,16 +283,18 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
       if ((it + 1) * kThreads > C::KSLOTS && it * kThreads + tid >= C::KSLOTS) continue;
       char* ad = tk + (it * kThreads + tid) * 16;
       uint4 x = ld16(ad);
+      float mul = 1.f;
+      if constexpr (NORM) mul = __builtin_amdgcn_rsqf(sum_over_8_lanes(sumsq8(x, 0.f)) * (1.f / kD) + a.eps);
       if (csb) {
         if (C::PH_LDS) {
-          x = rotate8h_pk(x, ld16(sph + (it * kThreads + tid) * 16));
+          x = rotate8h_pk(x, ld16(sph + (it * kThreads + tid) * 16), mul);
         } else {
           const int o = goffK(it);
           const float4* pp = csb + (o >> 6) * 16 + ((o & 63) >> 2);
-          x = rotate8h(x, pp[0], pp[1], 1.f);
+          x = rotate8h(x, pp[0], pp[1], mul);
         }
       } else {
-        x = scale8h(x, 1.f);
+        x = scale8h(x, mul);
       }
       st16(ad, x);
     }
@@ -280,7 +305,8 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
   // backward: dO^T fragments gf, LSE in log2 units lse2, -D nd, dS exponent ex,
   //           dQ~^T accumulator o
   f16x8 qf[C::QL][2];
-  bf16x8 gf[BWD ? C::QL : 1][2];
+  bf16x8 gf[BWD ? C::QL : 1][2], gl[LO ? C::QL : 1][2];  // dO (hi and low terms)
+  float rq[BWD && NORM ? C::QL : 1];                     // QK RMSNorm factor of the query
   float m[C::QL], l[C::QL];
   int ex[C::QL];
   f32x4 o[C::QL][4];
@@ -292,12 +318,18 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
     const uint4* src = reinterpret_cast<const uint4*>(a.q + tok * kD);
     uint4 x0 = src[g], x1 = src[4 + g];
     uint4 r0, r1;
+    float mul = a.qscale;
+    if constexpr (NORM) {  // the 4 lanes of a query row hold its 64 values
+      const float rn = __builtin_amdgcn_rsqf(sum_over_rows(sumsq8(x1, sumsq8(x0, 0.f))) * (1.f / kD) + a.eps);
+      mul *= rn;
+      if constexpr (BWD) rq[j] = rn;
+    }
     if (csq) {
-      r0 = rotate8h(x0, csq[2 * g], csq[2 * g + 1], a.qscale);
-      r1 = rotate8h(x1, csq[8 + 2 * g], csq[8 + 2 * g + 1], a.qscale);
+      r0 = rotate8h(x0, csq[2 * g], csq[2 * g + 1], mul);
+      r1 = rotate8h(x1, csq[8 + 2 * g], csq[8 + 2 * g + 1], mul);
     } else {
-      r0 = scale8h(x0, a.qscale);
-      r1 = scale8h(x1, a.qscale);
+      r0 = scale8h(x0, mul);
+      r1 = scale8h(x1, mul);
     }
     qf[j][0] = __builtin_bit_cast(f16x8, r0);
     qf[j][1] = __builtin_bit_cast(f16x8, r1);
@@ -305,6 +337,11 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
       const uint4* gsrc = reinterpret_cast<const uint4*>(a.dout + tok * kD);
       gf[j][0] = __builtin_bit_cast(bf16x8, gsrc[g]);
       gf[j][1] = __builtin_bit_cast(bf16x8, gsrc[4 + g]);
+      if constexpr (LO) {
+        const uint4* lsrc = reinterpret_cast<const uint4*>(a.dout_lo + tok * kD);
+        gl[j][0] = __builtin_bit_cast(bf16x8, lsrc[g]);
+        gl[j][1] = __builtin_bit_cast(bf16x8, lsrc[4 + g]);
+      }
       m[j] = a.lse_in[tok] * kLog2e;  // lse2
       l[j] = -a.dvec[tok];            // -D
       ex[j] = kMinExp;
@@ -383,6 +420,10 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
       bf16x8 v1 = __builtin_bit_cast(bf16x8, ld16(tv + vaddr[c] + 64));
       f32x4 t0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v0, gf[j][0], nd, 0, 0, 0);
       y[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v1, gf[j][1], t0, 0, 0, 0);
+      if constexpr (LO) {
+        y[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v0, gl[j][0], y[c], 0, 0, 0);
+        y[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v1, gl[j][1], y[c], 0, 0, 0);
+      }
     }
     // exponent bound of |Y| over this level's keys (all rows of the query)
     float my = 0.f;
@@ -475,32 +516,58 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
   for (int j = 0; j < C::QL; ++j) {
     const int zq = z0 + grp + 2 * j;
     if constexpr (BWD) {
-      if (zq >= Z || !in_grid) continue;
-      // dQ = R^T (scale 2^(E-15) dQ~); lane holds d = 16t + 4g + i
+      // dQ = R^T (scale 2^(E-15) dQ~); lane holds d = 16t + 4g + i.  With QK
+      // RMSNorm that is the gradient of q^ = r q, carried back through the
+      // norm: dq = r (dq^ - q^ mean(dq^ q^)), q^ from the raw row in float32.
       const float f = a.scale * __builtin_amdgcn_ldexpf(1.f, ex[j] - 15);
-      const int64_t tok = bh_base + zq * HW + (int64_t)qy * W + qx;
-      uint2* dst = reinterpret_cast<uint2*>(a.out + tok * kD);
+      const int64_t tok = bh_base + min(zq, Z - 1) * HW + (int64_t)qy * W + qx;
+      f32x4 x[4];
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        float x0 = o[j][t][0] * f, x1 = o[j][t][1] * f, x2 = o[j][t][2] * f, x3 = o[j][t][3] * f;
+        x[t] = o[j][t] * f;
         if (csq) {
           const float4 ph = csq[4 * t + g];  // pairs 8t+2g and 8t+2g+1
-          const float r0 = fmaf(x0, ph.x, x1 * ph.y), r1 = fmaf(x1, ph.x, -x0 * ph.y);
-          const float r2 = fmaf(x2, ph.z, x3 * ph.w), r3 = fmaf(x3, ph.z, -x2 * ph.w);
-          x0 = r0; x1 = r1; x2 = r2; x3 = r3;
+          const float r0 = fmaf(x[t][0], ph.x, x[t][1] * ph.y), r1 = fmaf(x[t][1], ph.x, -x[t][0] * ph.y);
+          const float r2 = fmaf(x[t][2], ph.z, x[t][3] * ph.w), r3 = fmaf(x[t][3], ph.z, -x[t][2] * ph.w);
+          x[t] = f32x4{r0, r1, r2, r3};
         }
-        dst[4 * t + g] = make_uint2(pack2(x0, x1), pack2(x2, x3));
       }
+      if constexpr (NORM) {
+        const uint2* qr = reinterpret_cast<const uint2*>(a.q + tok * kD);
+        f32x4 qh[4];
+        float c = 0.f;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const uint2 w = qr[4 * t + g];
+          qh[t] = f32x4{lo_bf16(w.x), hi_bf16(w.x), lo_bf16(w.y), hi_bf16(w.y)} * rq[j];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) c = fmaf(x[t][i], qh[t][i], c);
+        }
+        c = sum_over_rows(c) * (1.f / kD);
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) x[t][i] = rq[j] * fmaf(-qh[t][i], c, x[t][i]);
+      }
+      if (zq >= Z || !in_grid) continue;
+      uint2* dst = reinterpret_cast<uint2*>(a.out + tok * kD);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) dst[4 * t + g] = make_uint2(pack2(x[t][0], x[t][1]), pack2(x[t][2], x[t][3]));
     } else {
       const float lt = sum_over_rows(l[j]);
       if (zq >= Z || !in_grid) continue;
-      const float inv = 1.f / lt;
+      float inv = 1.f / lt;
       const int64_t tok = bh_base + zq * HW + (int64_t)qy * W + qx;
       uint2* dst = reinterpret_cast<uint2*>(a.out + tok * kD);
+      if constexpr (GATE)
+        if (a.gate_dim == 1) inv *= sigmoid_fast(bf16_to_f32(a.gate[tok]));
 #pragma unroll
-      for (int t = 0; t < 4; ++t)  // d = 16t + 4g + i
-        dst[4 * t + g] = make_uint2(pack2(o[j][t][0] * inv, o[j][t][1] * inv),
-                                    pack2(o[j][t][2] * inv, o[j][t][3] * inv));
+      for (int t = 0; t < 4; ++t) {  // d = 16t + 4g + i
+        f32x4 r = o[j][t] * inv;
+        if constexpr (GATE)
+          if (a.gate_dim != 1) r *= sigmoid4_bf16(reinterpret_cast<const uint2*>(a.gate + tok * kD)[4 * t + g]);
+        dst[4 * t + g] = make_uint2(pack2(r[0], r[1]), pack2(r[2], r[3]));
+      }
       if (a.lse && g == 0) a.lse[tok] = (m[j] + __log2f(lt)) * kLn2;
     }
   }
@@ -526,10 +593,16 @@ Args make_args(const strata_na3d_desc& d, int zq, const void* q, const void* k, 
 }
 
 template <int KZ, int KY, int KX, int ZQ, bool BWD>
-bool launch(const strata_na3d_desc& d, const Args& a, hipStream_t s) {
+bool launch(const strata_na3d_desc& d, const Args& a, int opt, hipStream_t s) {
   int64_t blocks = (int64_t)d.B * d.heads * a.n_zb * a.n_yb * a.n_xb;
   if (blocks >= (int64_t)1 << 31) return false;
-  hipLaunchKernelGGL((na3d_mfma_q_kernel<KZ, KY, KX, ZQ, BWD>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
+  const dim3 grid((unsigned)blocks), block(kThreads);
+  switch (opt) {
+    case 0: hipLaunchKernelGGL((na3d_mfma_q_kernel<KZ, KY, KX, ZQ, BWD, 0>), grid, block, 0, s, a); break;
+    case 1: hipLaunchKernelGGL((na3d_mfma_q_kernel<KZ, KY, KX, ZQ, BWD, 1>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((na3d_mfma_q_kernel<KZ, KY, KX, ZQ, BWD, 2>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((na3d_mfma_q_kernel<KZ, KY, KX, ZQ, BWD, 3>), grid, block, 0, s, a); break;
+  }
   return true;
 }
 
@@ -541,21 +614,26 @@ bool supported(const strata_na3d_desc& d) {
 
 }  // namespace
 
-bool launch_na3d_fwd_mfma(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
-                          const float* cs, void* out, float* lse, hipStream_t s) {
+bool launch_na3d_fwd_mfma(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k,
+                          const void* v, const float* cs, void* out, float* lse, hipStream_t s) {
   if (!supported(d)) return false;
   const bool w377 = d.kz == 3 && d.ky == 7 && d.kx == 7, w599 = d.kz == 5 && d.ky == 9 && d.kx == 9;
   if (!w377 && !w599) return false;
   Args a = make_args(d, w377 ? 8 : 2, q, k, v, cs);
   a.out = static_cast<uint16_t*>(out);
   a.lse = lse;
-  if (w377) return launch<3, 7, 7, 8, false>(d, a, s);
-  return launch<5, 9, 9, 2, false>(d, a, s);
+  a.qk_norm = o.qk_norm;
+  a.eps = o.eps;
+  a.gate = static_cast<const uint16_t*>(o.gate);
+  a.gate_dim = o.gate_dim;
+  const int opt = (o.qk_norm ? kNorm : 0) | (o.gate ? kOpt2 : 0);
+  if (w377) return launch<3, 7, 7, 8, false>(d, a, opt, s);
+  return launch<5, 9, 9, 2, false>(d, a, opt, s);
 }
 
-bool launch_na3d_bwd_dq_mfma(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
-                             const float* cs, const void* dout, const float* lse,
-                             const float* dvec, void* dq, hipStream_t s) {
+bool launch_na3d_bwd_dq_mfma(const strata_na3d_desc& d, const BwdOpts& o, const void* q,
+                             const void* k, const void* v, const float* cs, const void* dout,
+                             const float* lse, const float* dvec, void* dq, hipStream_t s) {
   if (!supported(d)) return false;
   const bool w377 = d.kz == 3 && d.ky == 7 && d.kx == 7, w599 = d.kz == 5 && d.ky == 9 && d.kx == 9;
   if (!w377 && !w599) return false;
@@ -564,8 +642,12 @@ bool launch_na3d_bwd_dq_mfma(const strata_na3d_desc& d, const void* q, const voi
   a.dout = static_cast<const uint16_t*>(dout);
   a.lse_in = lse;
   a.dvec = dvec;
-  if (w377) return launch<3, 7, 7, 4, true>(d, a, s);
-  return launch<5, 9, 9, 2, true>(d, a, s);
+  a.qk_norm = o.qk_norm;
+  a.eps = o.eps;
+  a.dout_lo = static_cast<const uint16_t*>(o.dout_lo);
+  const int opt = (o.qk_norm ? kNorm : 0) | (o.dout_lo ? kOpt2 : 0);
+  if (w377) return launch<3, 7, 7, 4, true>(d, a, opt, s);
+  return launch<5, 9, 9, 2, true>(d, a, opt, s);
 }
 
 }  // namespace strata

@@ -1,5 +1,9 @@
 // Plain neighbourhood-attention kernels: one thread per query (forward, dq) or
-// per key (dk/dv), float32 arithmetic, StereoRoPE applied while loading.
+// per key (dk/dv), float32 arithmetic, StereoRoPE applied while loading.  The
+// options: QK RMSNorm after the rotation (the rotation keeps the mean square;
+// in the backward its Jacobian is applied to dq and dk before the transposed
+// rotation), the sigmoid gate on the forward output, and the backward's
+// upstream gradient given as two terms.
 // They serve the float32 path and every shape the MFMA kernels do not cover.
 #include "common.h"
 #include "kernels.h"
@@ -38,6 +42,40 @@ __device__ __forceinline__ void load_rot(const T* src, const float2* ph, float s
   }
 }
 
+// Divide a head_dim vector by its root mean square (QK RMSNorm, no scale);
+// returns the factor r = (mean(x^2) + eps)^(-1/2).
+template <int D>
+__device__ __forceinline__ float rms_normalise(float* x, float eps) {
+  float ss = 0.f;
+#pragma unroll
+  for (int e = 0; e < D; ++e) ss = fmaf(x[e], x[e], ss);
+  const float r = 1.f / sqrtf(ss / D + eps);
+#pragma unroll
+  for (int e = 0; e < D; ++e) x[e] *= r;
+  return r;
+}
+
+// Jacobian of the norm applied to a gradient g of x^ = r x (in place):
+// g <- r (g - x^ mean(g x^)).  Rotation-invariant, so g and x^ may both be
+// given in the rotated frame.
+template <int D>
+__device__ __forceinline__ void rms_norm_vjp(float* g, const float* xh, float r) {
+  float c = 0.f;
+#pragma unroll
+  for (int e = 0; e < D; ++e) c = fmaf(g[e], xh[e], c);
+  c /= D;
+#pragma unroll
+  for (int e = 0; e < D; ++e) g[e] = r * fmaf(-xh[e], c, g[e]);
+}
+
+// upstream gradient element: dout (+ its low part when given as two terms)
+template <typename T>
+__device__ __forceinline__ float ld_g(const T* hi, const T* lo, int64_t i) {
+  return lo ? ld(hi + i) + ld(lo + i) : ld(hi + i);
+}
+
+__device__ __forceinline__ float sigmoid(float g) { return 1.f / (1.f + expf(-g)); }
+
 struct Dims {
   int B, heads, Z, H, W, kz, ky, kx;
   float scale;
@@ -55,7 +93,8 @@ __device__ __forceinline__ void split_tok(int64_t i, const Dims& d, int& b, int&
 template <typename T, int D>
 __global__ void __launch_bounds__(128) na3d_fwd_ref_kernel(const T* __restrict__ q, const T* __restrict__ k,
                                                            const T* __restrict__ v, const float2* __restrict__ cs,
-                                                           T* __restrict__ out, float* __restrict__ lse, Dims dm) {
+                                                           T* __restrict__ out, float* __restrict__ lse, Dims dm,
+                                                           NaOpts opt) {
   int64_t nq = (int64_t)dm.B * dm.heads * dm.Z * dm.H * dm.W;
   int64_t qi = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (qi >= nq) return;
@@ -64,6 +103,7 @@ __global__ void __launch_bounds__(128) na3d_fwd_ref_kernel(const T* __restrict__
   const int64_t bh = (int64_t)b * dm.heads + h;
   float qv[D], kv[D], acc[D];
   load_rot<T, D>(q + qi * D, cs ? cs + (((int64_t)b * dm.H + y) * dm.W + x) * (D / 2) : nullptr, 1.f, qv);
+  if (opt.qk_norm) rms_normalise<D>(qv, opt.eps);  // the rotation keeps the mean square
 #pragma unroll
   for (int e = 0; e < D; ++e) acc[e] = 0.f;
   float m = -INFINITY, l = 0.f;
@@ -73,6 +113,7 @@ __global__ void __launch_bounds__(128) na3d_fwd_ref_kernel(const T* __restrict__
       for (int jx = xs; jx < xs + dm.kx; ++jx) {
         int64_t kj = ((bh * dm.Z + jz) * dm.H + jy) * dm.W + jx;
         load_rot<T, D>(k + kj * D, cs ? cs + (((int64_t)b * dm.H + jy) * dm.W + jx) * (D / 2) : nullptr, 1.f, kv);
+        if (opt.qk_norm) rms_normalise<D>(kv, opt.eps);
         float s = 0.f;
 #pragma unroll
         for (int e = 0; e < D; ++e) s = fmaf(qv[e], kv[e], s);
@@ -87,31 +128,37 @@ __global__ void __launch_bounds__(128) na3d_fwd_ref_kernel(const T* __restrict__
         m = mn;
       }
   float inv = 1.f / l;
+  const T* gate = static_cast<const T*>(opt.gate);
+  if (gate && opt.gate_dim == 1) inv *= sigmoid(ld(gate + qi));
 #pragma unroll
-  for (int e = 0; e < D; ++e) st(out + qi * D + e, acc[e] * inv);
+  for (int e = 0; e < D; ++e) {
+    float val = acc[e] * inv;
+    if (gate && opt.gate_dim != 1) val *= sigmoid(ld(gate + qi * D + e));
+    st(out + qi * D + e, val);
+  }
   if (lse) lse[qi] = m + logf(l);
 }
 
 template <typename T, int D>
-static void fwd_ref(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
-                    const float* cs, void* out, float* lse, hipStream_t s) {
+static void fwd_ref(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k,
+                    const void* v, const float* cs, void* out, float* lse, hipStream_t s) {
   Dims dm{d.B, d.heads, d.Z, d.H, d.W, d.kz, d.ky, d.kx, d.scale};
   int64_t nq = (int64_t)d.B * d.heads * d.Z * d.H * d.W;
   int threads = 128;
   int blocks = (int)((nq + threads - 1) / threads);
   hipLaunchKernelGGL((na3d_fwd_ref_kernel<T, D>), dim3(blocks), dim3(threads), 0, s,
                      static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
-                     reinterpret_cast<const float2*>(cs), static_cast<T*>(out), lse, dm);
+                     reinterpret_cast<const float2*>(cs), static_cast<T*>(out), lse, dm, o);
 }
 
-void launch_na3d_fwd_ref(const strata_na3d_desc& d, const void* q, const void* k, const void* v,
-                         const float* cs, void* out, float* lse, hipStream_t s) {
+void launch_na3d_fwd_ref(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k,
+                         const void* v, const float* cs, void* out, float* lse, hipStream_t s) {
   if (d.dtype == STRATA_BF16) {
-    if (d.head_dim == 32) fwd_ref<uint16_t, 32>(d, q, k, v, cs, out, lse, s);
-    else fwd_ref<uint16_t, 64>(d, q, k, v, cs, out, lse, s);
+    if (d.head_dim == 32) fwd_ref<uint16_t, 32>(d, o, q, k, v, cs, out, lse, s);
+    else fwd_ref<uint16_t, 64>(d, o, q, k, v, cs, out, lse, s);
   } else {
-    if (d.head_dim == 32) fwd_ref<float, 32>(d, q, k, v, cs, out, lse, s);
-    else fwd_ref<float, 64>(d, q, k, v, cs, out, lse, s);
+    if (d.head_dim == 32) fwd_ref<float, 32>(d, o, q, k, v, cs, out, lse, s);
+    else fwd_ref<float, 64>(d, o, q, k, v, cs, out, lse, s);
   }
 }
 
@@ -146,19 +193,21 @@ template <typename T, int D>
 __global__ void __launch_bounds__(128) na3d_bwd_dq_ref_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v, const float2* __restrict__ cs,
     const T* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ dvec,
-    T* __restrict__ dq, Dims dm) {
+    T* __restrict__ dq, Dims dm, BwdOpts opt) {
   int64_t nq = (int64_t)dm.B * dm.heads * dm.Z * dm.H * dm.W;
   int64_t qi = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (qi >= nq) return;
   int b, h, z, y, x;
   split_tok(qi, dm, b, h, z, y, x);
   const int64_t bh = (int64_t)b * dm.heads + h;
+  const T* dlo = static_cast<const T*>(opt.dout_lo);
   float qv[D], kv[D], g[D], acc[D];
   const float2* phq = cs ? cs + (((int64_t)b * dm.H + y) * dm.W + x) * (D / 2) : nullptr;
   load_rot<T, D>(q + qi * D, phq, 1.f, qv);
+  const float rq = opt.qk_norm ? rms_normalise<D>(qv, opt.eps) : 1.f;
 #pragma unroll
   for (int e = 0; e < D; ++e) {
-    g[e] = ld(dout + qi * D + e);
+    g[e] = ld_g(dout, dlo, qi * D + e);
     acc[e] = 0.f;
   }
   const float L = lse[qi], Di = dvec[qi];
@@ -168,6 +217,7 @@ __global__ void __launch_bounds__(128) na3d_bwd_dq_ref_kernel(
       for (int jx = xs; jx < xs + dm.kx; ++jx) {
         int64_t kj = ((bh * dm.Z + jz) * dm.H + jy) * dm.W + jx;
         load_rot<T, D>(k + kj * D, cs ? cs + (((int64_t)b * dm.H + jy) * dm.W + jx) * (D / 2) : nullptr, 1.f, kv);
+        if (opt.qk_norm) rms_normalise<D>(kv, opt.eps);
         float s = 0.f, dp = 0.f;
         const T* vr = v + kj * D;
 #pragma unroll
@@ -180,10 +230,13 @@ __global__ void __launch_bounds__(128) na3d_bwd_dq_ref_kernel(
 #pragma unroll
         for (int e = 0; e < D; ++e) acc[e] = fmaf(ds, kv[e], acc[e]);
       }
-  // dq = R^T (scale * acc)
+  // dq = R^T (scale * acc), through the norm's Jacobian first when normalising
+#pragma unroll
+  for (int e = 0; e < D; ++e) acc[e] *= dm.scale;
+  if (opt.qk_norm) rms_norm_vjp<D>(acc, qv, rq);
 #pragma unroll
   for (int t = 0; t < D / 2; ++t) {
-    float a = dm.scale * acc[2 * t], bb = dm.scale * acc[2 * t + 1];
+    float a = acc[2 * t], bb = acc[2 * t + 1];
     float c = 1.f, sn = 0.f;
     if (phq) { c = phq[t].x; sn = -phq[t].y; }
     st(dq + qi * D + 2 * t, fmaf(a, c, -bb * sn));
@@ -203,16 +256,18 @@ template <typename T, int D>
 __global__ void __launch_bounds__(128) na3d_bwd_dkdv_ref_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v, const float2* __restrict__ cs,
     const T* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ dvec,
-    T* __restrict__ dk, T* __restrict__ dv, Dims dm) {
+    T* __restrict__ dk, T* __restrict__ dv, Dims dm, BwdOpts opt) {
   int64_t nk = (int64_t)dm.B * dm.heads * dm.Z * dm.H * dm.W;
   int64_t kj = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (kj >= nk) return;
   int b, h, z, y, x;
   split_tok(kj, dm, b, h, z, y, x);
   const int64_t bh = (int64_t)b * dm.heads + h;
+  const T* dlo = static_cast<const T*>(opt.dout_lo);
   float kv[D], vv[D], qv[D], ak[D], av[D];
   const float2* phk = cs ? cs + (((int64_t)b * dm.H + y) * dm.W + x) * (D / 2) : nullptr;
   load_rot<T, D>(k + kj * D, phk, 1.f, kv);
+  const float rk = opt.qk_norm ? rms_normalise<D>(kv, opt.eps) : 1.f;
 #pragma unroll
   for (int e = 0; e < D; ++e) {
     vv[e] = ld(v + kj * D + e);
@@ -228,24 +283,28 @@ __global__ void __launch_bounds__(128) na3d_bwd_dkdv_ref_kernel(
       for (int ix = xlo; ix <= xhi; ++ix) {
         int64_t qi = ((bh * dm.Z + iz) * dm.H + iy) * dm.W + ix;
         load_rot<T, D>(q + qi * D, cs ? cs + (((int64_t)b * dm.H + iy) * dm.W + ix) * (D / 2) : nullptr, 1.f, qv);
+        if (opt.qk_norm) rms_normalise<D>(qv, opt.eps);
         float s = 0.f, dp = 0.f;
-        const T* gr = dout + qi * D;
 #pragma unroll
         for (int e = 0; e < D; ++e) {
           s = fmaf(qv[e], kv[e], s);
-          dp = fmaf(ld(gr + e), vv[e], dp);
+          dp = fmaf(ld_g(dout, dlo, qi * D + e), vv[e], dp);
         }
         float p = expf(s * dm.scale - lse[qi]);
         float ds = p * (dp - dvec[qi]);
 #pragma unroll
         for (int e = 0; e < D; ++e) {
-          av[e] = fmaf(p, ld(gr + e), av[e]);
+          av[e] = fmaf(p, ld_g(dout, dlo, qi * D + e), av[e]);
           ak[e] = fmaf(ds, qv[e], ak[e]);
         }
       }
+  // dk = R^T (scale * ak), through the norm's Jacobian first when normalising
+#pragma unroll
+  for (int e = 0; e < D; ++e) ak[e] *= dm.scale;
+  if (opt.qk_norm) rms_norm_vjp<D>(ak, kv, rk);
 #pragma unroll
   for (int t = 0; t < D / 2; ++t) {
-    float a = dm.scale * ak[2 * t], bb = dm.scale * ak[2 * t + 1];
+    float a = ak[2 * t], bb = ak[2 * t + 1];
     float c = 1.f, sn = 0.f;
     if (phk) { c = phk[t].x; sn = -phk[t].y; }
     st(dk + kj * D + 2 * t, fmaf(a, c, -bb * sn));
@@ -257,9 +316,9 @@ __global__ void __launch_bounds__(128) na3d_bwd_dkdv_ref_kernel(
 
 // part: 0 = D = rowsum(dO * O), 1 = dq, 2 = dk and dv
 template <typename T, int D>
-static void bwd_ref(int part, const strata_na3d_desc& d, const void* q, const void* k, const void* v,
-                    const float* cs, const void* out, const void* dout, const float* lse, void* dq,
-                    void* dk, void* dv, float* dvec, hipStream_t s) {
+static void bwd_ref(int part, const strata_na3d_desc& d, const BwdOpts& o, const void* q, const void* k,
+                    const void* v, const float* cs, const void* out, const void* dout, const float* lse,
+                    void* dq, void* dk, void* dv, float* dvec, hipStream_t s) {
   Dims dm{d.B, d.heads, d.Z, d.H, d.W, d.kz, d.ky, d.kx, d.scale};
   int64_t n = (int64_t)d.B * d.heads * d.Z * d.H * d.W;
   int threads = 128;
@@ -271,23 +330,24 @@ static void bwd_ref(int part, const strata_na3d_desc& d, const void* q, const vo
   else if (part == 1)
     hipLaunchKernelGGL((na3d_bwd_dq_ref_kernel<T, D>), dim3(blocks), dim3(threads), 0, s,
                        static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), c2,
-                       static_cast<const T*>(dout), lse, dvec, static_cast<T*>(dq), dm);
+                       static_cast<const T*>(dout), lse, dvec, static_cast<T*>(dq), dm, o);
   else
     hipLaunchKernelGGL((na3d_bwd_dkdv_ref_kernel<T, D>), dim3(blocks), dim3(threads), 0, s,
                        static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), c2,
                        static_cast<const T*>(dout), lse, dvec, static_cast<T*>(dk), static_cast<T*>(dv),
-                       dm);
+                       dm, o);
 }
 
-void launch_na3d_bwd_ref(int part, const strata_na3d_desc& d, const void* q, const void* k,
-                         const void* v, const float* cs, const void* out, const void* dout,
-                         const float* lse, void* dq, void* dk, void* dv, float* dvec, hipStream_t s) {
+void launch_na3d_bwd_ref(int part, const strata_na3d_desc& d, const BwdOpts& o, const void* q,
+                         const void* k, const void* v, const float* cs, const void* out,
+                         const void* dout, const float* lse, void* dq, void* dk, void* dv,
+                         float* dvec, hipStream_t s) {
   if (d.dtype == STRATA_BF16) {
-    if (d.head_dim == 32) bwd_ref<uint16_t, 32>(part, d, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
-    else bwd_ref<uint16_t, 64>(part, d, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+    if (d.head_dim == 32) bwd_ref<uint16_t, 32>(part, d, o, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+    else bwd_ref<uint16_t, 64>(part, d, o, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
   } else {
-    if (d.head_dim == 32) bwd_ref<float, 32>(part, d, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
-    else bwd_ref<float, 64>(part, d, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+    if (d.head_dim == 32) bwd_ref<float, 32>(part, d, o, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+    else bwd_ref<float, 64>(part, d, o, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
   }
 }
 

@@ -16,7 +16,7 @@ from typing import Optional, Tuple
 
 import numpy as np
 
-STREAM_Q, STREAM_K, STREAM_V, STREAM_DO, STREAM_PLACE, STREAM_FIELD = 0, 1, 2, 3, 4, 5
+STREAM_Q, STREAM_K, STREAM_V, STREAM_DO, STREAM_PLACE, STREAM_FIELD, STREAM_GATE = 0, 1, 2, 3, 4, 5, 6
 
 # Cubed-sphere grid of the 4.9-km workload: 6 faces of 2048 x 2048 native cells,
 # tokens are 4 x 4 horizontal patches (one vertical level per token).

@@ -109,3 +109,64 @@ def test_axis_and_rope_rules():
     assert L.strata_stereorope_phases(p, 1, 4, 4, 32, -1.0, p, None) == B.STRATA_ERR_INVALID_ARG
     assert L.strata_stereorope_apply(p, p, p, 1, 1, 1, 4, 4, 36, 1, 0, None) == B.STRATA_ERR_UNSUPPORTED
     assert L.strata_stereo_coords(p, p, p, 1, 600, 4, 2048, 4, 1e-3, p, None) == B.STRATA_ERR_INVALID_ARG
+
+
+def opts(qk_norm=0, eps=1e-6, gate=None, gate_dim=0):
+    return B.NA3DOpts(qk_norm, eps, gate, gate_dim)
+
+
+def call_fwd_ex(d, o):
+    p = fake()
+    return B.load().strata_na3d_fwd_ex(ctypes.byref(d), None if o is None else ctypes.byref(o), p, p, p, None, p,
+                                       None, None)
+
+
+@pytest.mark.parametrize("o", [
+    opts(qk_norm=1, eps=float("nan")),
+    opts(qk_norm=1, eps=-1e-6),
+    opts(qk_norm=1, eps=float("inf")),
+    opts(gate=fake(), gate_dim=0),
+    opts(gate=fake(), gate_dim=32),           # neither 1 nor head_dim (64)
+    opts(gate=fake(0x10002), gate_dim=1),     # misaligned
+])
+def test_fwd_ex_rejects_bad_options(o):
+    assert call_fwd_ex(desc(), o) == B.STRATA_ERR_INVALID_ARG
+    assert b"opts" in B.load().strata_last_error()
+
+
+def test_fwd_ex_checks_the_descriptor_first():
+    assert call_fwd_ex(desc(window=(2, 7, 7)), opts(qk_norm=1)) == B.STRATA_ERR_INVALID_ARG
+
+
+def test_bwd_ex_workspace_layout():
+    L = B.load()
+    d = desc()
+    n = 1 * 2 * 8 * 16 * 16
+    row = n * 64 * 2
+    base = L.strata_na3d_bwd_workspace_size(ctypes.byref(d))
+    assert L.strata_na3d_bwd_ex_workspace_size(ctypes.byref(d), None) == base
+    assert L.strata_na3d_bwd_ex_workspace_size(ctypes.byref(d), ctypes.byref(opts())) == base
+    # a gate adds dA as two bf16 terms; the norm needs no workspace
+    assert L.strata_na3d_bwd_ex_workspace_size(ctypes.byref(d), ctypes.byref(opts(gate=fake(), gate_dim=1))) == \
+        base + 2 * row
+    assert L.strata_na3d_bwd_ex_workspace_size(ctypes.byref(d), ctypes.byref(opts(qk_norm=1))) == base
+    both = opts(qk_norm=1, gate=fake(), gate_dim=64)
+    assert L.strata_na3d_bwd_ex_workspace_size(ctypes.byref(d), ctypes.byref(both)) == base + 2 * row
+    f32 = desc(dtype=B.STRATA_F32)
+    assert L.strata_na3d_bwd_ex_workspace_size(ctypes.byref(f32), ctypes.byref(both)) == \
+        L.strata_na3d_bwd_workspace_size(ctypes.byref(f32)) + 2 * row  # one float32 term
+    assert L.strata_na3d_bwd_ex_workspace_size(ctypes.byref(d), ctypes.byref(opts(gate=fake(), gate_dim=3))) == 0
+
+
+def test_bwd_ex_requires_dgate_with_a_gate_and_enough_workspace():
+    L = B.load()
+    d = desc()
+    o = opts(gate=fake(), gate_dim=1)
+    need = L.strata_na3d_bwd_ex_workspace_size(ctypes.byref(d), ctypes.byref(o))
+    p = fake()
+    st = L.strata_na3d_bwd_ex(ctypes.byref(d), ctypes.byref(o), p, p, p, None, p, p, p, p, p, p, None, p, need,
+                              None)
+    assert st == B.STRATA_ERR_INVALID_ARG and b"dgate" in L.strata_last_error()
+    st = L.strata_na3d_bwd_ex(ctypes.byref(d), ctypes.byref(o), p, p, p, None, p, p, p, p, p, p, p, p, need - 1,
+                              None)
+    assert st == B.STRATA_ERR_WORKSPACE
