@@ -232,6 +232,83 @@ def train_tile(steps: int):
     return out
 
 
+def _timed(fn, steps: int) -> float:
+    """Mean HIP-event time (ms) of fn on the current stream over `steps` passes."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream()
+    ts = []
+    for _ in range(steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        fn()
+        e1.record(st)
+        ts.append((e0, e1))
+    torch.cuda.synchronize()
+    return float(np.mean([a.elapsed_time(b) for a, b in ts]))
+
+
+def options_face_fwd(wl, desc, q, k, v, cs, out, steps: int) -> dict:
+    """The face forward with the attention-block options (QK RMSNorm, sigmoid
+    output gate per channel or per token-head) against the plain forward."""
+    import torch
+    from paper_2606_31248_amd import binding as Bd
+    from paper_2606_31248_amd import inputs as I
+    dev = q.device
+    gd = torch.from_numpy(I.gaussian(wl.shape(), wl.seed, I.STREAM_GATE, "bf16", 2.0).view(np.int16)).view(
+        torch.bfloat16).to(dev)
+    g1 = gd[..., 0].contiguous()
+    n = wl.B * wl.heads * wl.N
+    flops = 4.0 * n * wl.K * wl.d
+    variants = {"plain": (None, 0), "norm": (Bd.make_opts(True, 1e-6, None), 0),
+                "gate_d": (Bd.make_opts(False, 1e-6, gd), n * wl.d * 2),
+                "norm_gate_1": (Bd.make_opts(True, 1e-6, g1), n * 2),
+                "norm_gate_d": (Bd.make_opts(True, 1e-6, gd), n * wl.d * 2)}
+    res = {}
+    for name, (opts, extra) in variants.items():
+        ms = _timed(lambda: Bd.strata_na3d_fwd_ex(desc, opts, q, k, v, cs, out, None), steps)
+        nbytes = 4.0 * n * wl.d * 2 + extra
+        res[name] = dict(roofline_row(flops, nbytes, ms), ms=round(ms, 4),
+                         achieved_gbs=round(nbytes / ms / 1e6, 1), frac_hbm=round(nbytes / ms / 1e6 / PEAK_HBM_GBS, 4))
+    del gd, g1
+    return res
+
+
+def options_train_bwd(steps: int) -> dict:
+    """The 16-tile 5x9x9 training-tile backward with QK RMSNorm and a per-channel
+    gate (gate row pass included) against the plain backward."""
+    import torch
+    from paper_2606_31248_amd import binding as Bd
+    from paper_2606_31248_amd import inputs as I
+    from paper_2606_31248_amd import pipeline as Pp
+    wl = I.TRAIN_TILE_BWD
+    dev = torch.device("cuda:0")
+    to_dev = lambda bits: torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(dev)
+    q, k, v = (to_dev(x) for x in wl.qkv())
+    g = to_dev(wl.dout())
+    gd = to_dev(I.gaussian(wl.shape(), wl.seed, I.STREAM_GATE, "bf16", 2.0))
+    geom = Pp.TileGeometry(*(torch.from_numpy(x).to(dev) for x in wl.placement().as_int32()))
+    _, cs = Pp.stereo_phases(geom, wl.H, wl.W, wl.d)
+    desc = Bd.desc_for(q, (wl.kz, wl.ky, wl.kx), wl.scale)
+    out = torch.empty_like(q)
+    lse = torch.empty(wl.shape()[:-1], dtype=torch.float32, device=dev)
+    dq, dk, dv, dgt = (torch.empty_like(q) for _ in range(4))
+    n = wl.B * wl.heads * wl.N
+    flops = 10.0 * n * wl.K * wl.d
+    res = {}
+    for name, opts in (("plain", None), ("norm", Bd.make_opts(True, 1e-6, None)),
+                       ("norm_gate_d", Bd.make_opts(True, 1e-6, gd))):
+        ws = torch.empty(Bd.strata_na3d_bwd_ex_workspace_size(desc, opts), dtype=torch.uint8, device=dev)
+        Bd.strata_na3d_fwd_ex(desc, opts, q, k, v, cs, out, lse)
+        dgate = dgt if opts is not None and opts.gate else None
+        ms = _timed(lambda: Bd.strata_na3d_bwd_ex(desc, opts, q, k, v, cs, out, g, lse, dq, dk, dv, dgate, ws),
+                    steps)
+        res[name] = {"ms": round(ms, 4), "tflops": round(flops / ms / 1e9, 2)}
+        del ws
+    return res
+
+
 def roofline_row(flops: float, nbytes: float, ms: float) -> dict:
     """Achieved rate of a kernel against min(MFMA peak, intensity x HBM peak)."""
     ai = flops / nbytes
@@ -388,6 +465,10 @@ def main():
                                "frac_hbm": round(blend_bytes / (avg["blend"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
     }
     if a.train_steps > 0:
+        # the attention-block options (App. B.5) on the same face forward
+        opt = options_face_fwd(wl, desc, q, k, v, cs, out, a.train_steps)
+        res["options"] = {"face_fwd": opt}
+        res["rows"]["f1_qk_norm_gate_fwd_face"] = opt["norm_gate_d"]
         del q, k, v, out, face, coords, cs
         torch.cuda.empty_cache()
         tt = train_tile(a.train_steps)
@@ -396,6 +477,9 @@ def main():
         res["rows"]["a2_rope_apply_train_tile"] = {"bound": "hbm", "achieved_gbs": tt["rope_apply_qk"]["gbs"],
                                                    "frac_hbm": tt["rope_apply_qk"]["frac_hbm"]}
         res["train_tile"] = tt
+        torch.cuda.empty_cache()
+        res["options"]["train_tile_bwd"] = options_train_bwd(a.train_steps)
+        res["rows"]["f1_qk_norm_gate_bwd_train_tile"] = res["options"]["train_tile_bwd"]["norm_gate_d"]
     if a.cpu_tiles > 0:
         res["cpu_baseline"] = cpu_baseline(wl, a.cpu_tiles)
     print(json.dumps(res), flush=True)

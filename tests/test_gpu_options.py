@@ -141,9 +141,8 @@ def test_fwd_options_full_oracle(shape, window, dtype, qk_norm, gkind):
 @pytest.mark.parametrize("scale", [0.125, 0.5, 0.7])
 def test_fwd_norm_tames_huge_inputs(shape, window, scale):
     """q, k of magnitude ~64 (logits of +-1000s without the norm): with QK RMSNorm
-    the logits are bounded by scale * head_dim; scale 0.5 gives the sharpest
-    softmax the level-sweep kernel takes with its constant reference, 0.7 goes to
-    the kernel with a running maximum."""
+    the logits are bounded by scale * head_dim; larger scales give sharper
+    softmax rows, whose maximum the kernels' reference then has to follow."""
     c32 = coords_for(shape, 96)
     inputs, _, out, lse, _ = run_fwd_ex(shape, window, "bf16", 52, True, "d", c32, scale=scale, qk_mult=64.0)
     ro, rl = oracle_fwd(inputs, window, scale, "bf16", True, c32)
