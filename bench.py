@@ -22,6 +22,7 @@ from __future__ import annotations
 import argparse
 import hashlib
 import json
+import re
 import os
 import sys
 import time
@@ -41,7 +42,7 @@ STATS_FILE = os.path.join(ROOT, "profiles", "face_rollout_step_kernel_stats.txt"
 KERNEL_SOURCES = ["paper_2606_31248_amd/csrc/na3d_fwd_zs.hip", "paper_2606_31248_amd/csrc/mfma_util.h",
                   "paper_2606_31248_amd/csrc/common.h"]
 FWD_KERNEL = "na3d_fwd_zs_kernel"
-BLEND_KERNEL = "tile_blend_kernel"
+BLEND_KERNEL = "tile_blend_bf16_kernel"
 COPY_KERNEL = "copyBuffer"
 CALIB_BYTES = 1 << 30
 
@@ -106,7 +107,7 @@ def summarize_pmc(fetch_dir: str, write_dir: str, commands) -> dict:
     fwd_f, fwd_w = pick(fe, FWD_KERNEL), pick(wr, FWD_KERNEL)
     bl_f, bl_w = pick(fe, BLEND_KERNEL), pick(wr, BLEND_KERNEL)
     return {
-        "kernel": f"strata_na3d_fwd ({FWD_KERNEL}<8>)",
+        "kernel": f"strata_na3d_fwd ({FWD_KERNEL}<8, false, false>: no options)",
         "workload": "face_rollout_81x16x8x64x64_d64_w3x7x7",
         "kernel_source_hash": kernel_source_hash(),
         "fetch_kb_per_launch": fwd_f,
@@ -133,7 +134,9 @@ def summarize_stats(stats_csv: str, command: str) -> str:
            f"# forward kernel source hash: {kernel_source_hash()}", "",
            f"{'kernel':72s} {'calls':>6s} {'avg_us':>10s} {'min_us':>10s} {'max_us':>10s} {'pct':>6s}"]
     for r in rows:
-        name = r["Name"]
+        # kernel name with its template arguments, without namespaces and parameter list
+        name = re.sub(r"\(.*$", "", r["Name"].replace("(anonymous namespace)::", ""))
+        name = re.sub(r"^void |strata::", "", name)
         name = name if len(name) <= 72 else name[:69] + "..."
         out.append(f"{name:72s} {int(r['Calls']):6d} {float(r['AverageNs']) / 1e3:10.1f} "
                    f"{float(r['MinNs']) / 1e3:10.1f} {float(r['MaxNs']) / 1e3:10.1f} {float(r['Percentage']):6.2f}")
