@@ -47,11 +47,16 @@ static int in_window(int j, int i, int L, int k) {
   return j >= s && j < s + k;
 }
 
+/* A window size is valid when it is odd and fits the axis, or when it is the
+ * whole axis (any parity: the rule above then gives every query all L
+ * positions; column-wise attention over all levels is that case). */
+static int window_ok(int L, int k) { return L > 0 && k > 0 && k <= L && ((k % 2) == 1 || k == L); }
+
 /* starts[i] for every query position, and for every key position j the
  * inclusive range [qlo[j], qhi[j]] of queries whose window holds j
  * (found by scanning all queries; qlo = L, qhi = -1 if none). */
 int oracle_axis_index(int L, int k, int32_t* starts, int32_t* qlo, int32_t* qhi) {
-  if (L <= 0 || k <= 0 || (k % 2) == 0 || k > L) return 1;
+  if (!window_ok(L, k)) return 1;
   for (int i = 0; i < L; ++i) starts[i] = win_start(i, L, k);
   for (int j = 0; j < L; ++j) {
     int lo = L, hi = -1;
@@ -198,9 +203,7 @@ static void na_query(const na_dims* D, const double* q, const double* k, const d
 
 static int check_dims(const na_dims* D) {
   if (D->B <= 0 || D->heads <= 0 || D->Z <= 0 || D->H <= 0 || D->W <= 0 || D->d <= 0) return 1;
-  if (D->kz <= 0 || D->ky <= 0 || D->kx <= 0) return 1;
-  if (D->kz % 2 == 0 || D->ky % 2 == 0 || D->kx % 2 == 0) return 1;
-  if (D->kz > D->Z || D->ky > D->H || D->kx > D->W) return 1;
+  if (!window_ok(D->Z, D->kz) || !window_ok(D->H, D->ky) || !window_ok(D->W, D->kx)) return 1;
   if (!(D->scale > 0.0)) return 1;
   return 0;
 }

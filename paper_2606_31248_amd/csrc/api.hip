@@ -40,22 +40,28 @@ static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 
 
 static const int64_t kMaxElems = (int64_t)1 << 40;
 
+// odd and inside the axis, or the whole axis (any parity)
+static bool window_ok(int L, int k) { return k > 0 && k <= L && ((k & 1) || k == L); }
+
 static strata_status check_desc(const strata_na3d_desc* d) {
   REQUIRE(d, "desc: null pointer");
   REQUIRE(d->B > 0 && d->heads > 0 && d->Z > 0 && d->H > 0 && d->W > 0 && d->head_dim > 0,
           "desc: every size must be positive (B=%d heads=%d Z=%d H=%d W=%d head_dim=%d)", d->B,
           d->heads, d->Z, d->H, d->W, d->head_dim);
-  REQUIRE(d->kz > 0 && d->ky > 0 && d->kx > 0 && (d->kz & 1) && (d->ky & 1) && (d->kx & 1),
-          "desc: window sizes must be odd and positive (%d, %d, %d)", d->kz, d->ky, d->kx);
+  REQUIRE(d->kz > 0 && d->ky > 0 && d->kx > 0, "desc: window sizes must be positive (%d, %d, %d)", d->kz,
+          d->ky, d->kx);
   REQUIRE(d->kz <= d->Z && d->ky <= d->H && d->kx <= d->W,
           "desc: window (%d, %d, %d) larger than the grid (%d, %d, %d)", d->kz, d->ky, d->kx, d->Z,
           d->H, d->W);
+  REQUIRE(window_ok(d->Z, d->kz) && window_ok(d->H, d->ky) && window_ok(d->W, d->kx),
+          "desc: window sizes must be odd or span their whole axis (%d, %d, %d) on (%d, %d, %d)", d->kz,
+          d->ky, d->kx, d->Z, d->H, d->W);
   REQUIRE(d->scale > 0.f && isfinite(d->scale), "desc: scale must be finite and > 0");
   REQUIRE(d->dtype == STRATA_F32 || d->dtype == STRATA_BF16, "desc: unknown dtype %d", (int)d->dtype);
   int64_t n = (int64_t)d->B * d->heads * d->Z * d->H * d->W;
   REQUIRE(n * d->head_dim < kMaxElems, "desc: tensor too large");
-  if (d->head_dim != 32 && d->head_dim != 64)
-    return set_error(STRATA_ERR_UNSUPPORTED, "head_dim %d not supported (32 or 64)", d->head_dim);
+  if (d->head_dim != 32 && d->head_dim != 64 && d->head_dim != 128)
+    return set_error(STRATA_ERR_UNSUPPORTED, "head_dim %d not supported (32, 64 or 128)", d->head_dim);
   return STRATA_OK;
 }
 
@@ -114,7 +120,8 @@ static strata_status na3d_fwd_impl(const strata_na3d_desc* desc, const strata_na
   if (cs) REQUIRE(aligned16(cs), "cs: not 16-byte aligned");
   if (lse) REQUIRE(aligned16(lse), "lse: not 16-byte aligned");
   hipStream_t s = (hipStream_t)stream;
-  if (!launch_na3d_fwd_zs(*desc, o, q, k, v, cs, out, lse, s) &&
+  if (!launch_na3d_fwd_col(*desc, o, q, k, v, out, lse, s) &&
+      !launch_na3d_fwd_zs(*desc, o, q, k, v, cs, out, lse, s) &&
       !launch_na3d_fwd_mfma(*desc, o, q, k, v, cs, out, lse, s))
     launch_na3d_fwd_ref(*desc, o, q, k, v, cs, out, lse, s);
   return check_launch(opts ? "strata_na3d_fwd_ex" : "strata_na3d_fwd");
@@ -197,7 +204,7 @@ const char* strata_last_error(void) { return g_err; }
 
 strata_status strata_na_axis_index(int32_t L, int32_t k, int32_t* starts, int32_t* qlo,
                                    int32_t* qhi, void* stream) {
-  REQUIRE(L > 0 && k > 0 && (k & 1) && k <= L, "axis: need odd 1 <= k <= L (L=%d, k=%d)", L, k);
+  REQUIRE(L > 0 && window_ok(L, k), "axis: need odd 1 <= k <= L or k == L (L=%d, k=%d)", L, k);
   REQUIRE_PTR(starts);
   REQUIRE_PTR(qlo);
   REQUIRE_PTR(qhi);

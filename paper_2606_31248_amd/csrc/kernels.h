@@ -40,6 +40,11 @@ void launch_na3d_fwd_ref(const strata_na3d_desc& d, const NaOpts& o, const void*
 bool launch_na3d_fwd_zs(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k,
                         const void* v, const float* cs, void* out, float* lse, hipStream_t s);
 
+// bf16 column-wise forward, windows (kz, 1, 1) with Z <= 32, head_dim 64;
+// returns false for any other problem.
+bool launch_na3d_fwd_col(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k,
+                         const void* v, void* out, float* lse, hipStream_t s);
+
 // bf16 MFMA forward; returns false when the problem has no MFMA variant.
 bool launch_na3d_fwd_mfma(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k,
                           const void* v, const float* cs, void* out, float* lse, hipStream_t s);

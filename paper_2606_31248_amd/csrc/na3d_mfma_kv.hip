@@ -537,6 +537,8 @@ bool launch_na3d_bwd_dkdv_mfma(const strata_na3d_desc& d, const BwdOpts& o, cons
     return lo ? launch_kv<3, 7, 7, 4, 1, true>(d, a, s) : launch_kv<3, 7, 7, 4, 1, false>(d, a, s);
   if (d.kz == 5 && d.ky == 9 && d.kx == 9)
     return lo ? launch_kv<5, 9, 9, 8, 1, true>(d, a, s) : launch_kv<5, 9, 9, 8, 2, false>(d, a, s);
+  if (d.kz == 9 && d.ky == 9 && d.kx == 9)
+    return lo ? launch_kv<9, 9, 9, 8, 1, true>(d, a, s) : launch_kv<9, 9, 9, 8, 2, false>(d, a, s);
   return false;
 }
 

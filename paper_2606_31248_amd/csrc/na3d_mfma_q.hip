@@ -618,8 +618,9 @@ bool launch_na3d_fwd_mfma(const strata_na3d_desc& d, const NaOpts& o, const void
                           const void* v, const float* cs, void* out, float* lse, hipStream_t s) {
   if (!supported(d)) return false;
   const bool w377 = d.kz == 3 && d.ky == 7 && d.kx == 7, w599 = d.kz == 5 && d.ky == 9 && d.kx == 9;
-  if (!w377 && !w599) return false;
-  Args a = make_args(d, w377 ? 8 : 2, q, k, v, cs);
+  const bool w999 = d.kz == 9 && d.ky == 9 && d.kx == 9;
+  if (!w377 && !w599 && !w999) return false;
+  Args a = make_args(d, w599 ? 2 : (w999 ? 6 : 8), q, k, v, cs);
   a.out = static_cast<uint16_t*>(out);
   a.lse = lse;
   a.qk_norm = o.qk_norm;
@@ -628,6 +629,7 @@ bool launch_na3d_fwd_mfma(const strata_na3d_desc& d, const NaOpts& o, const void
   a.gate_dim = o.gate_dim;
   const int opt = (o.qk_norm ? kNorm : 0) | (o.gate ? kOpt2 : 0);
   if (w377) return launch<3, 7, 7, 8, false>(d, a, opt, s);
+  if (w999) return launch<9, 9, 9, 6, false>(d, a, opt, s);
   return launch<5, 9, 9, 2, false>(d, a, opt, s);
 }
 
@@ -636,8 +638,9 @@ bool launch_na3d_bwd_dq_mfma(const strata_na3d_desc& d, const BwdOpts& o, const 
                              const float* lse, const float* dvec, void* dq, hipStream_t s) {
   if (!supported(d)) return false;
   const bool w377 = d.kz == 3 && d.ky == 7 && d.kx == 7, w599 = d.kz == 5 && d.ky == 9 && d.kx == 9;
-  if (!w377 && !w599) return false;
-  Args a = make_args(d, w377 ? 4 : 2, q, k, v, cs);
+  const bool w999 = d.kz == 9 && d.ky == 9 && d.kx == 9;
+  if (!w377 && !w599 && !w999) return false;
+  Args a = make_args(d, w599 ? 2 : (w999 ? 2 : 4), q, k, v, cs);
   a.out = static_cast<uint16_t*>(dq);
   a.dout = static_cast<const uint16_t*>(dout);
   a.lse_in = lse;
@@ -647,6 +650,7 @@ bool launch_na3d_bwd_dq_mfma(const strata_na3d_desc& d, const BwdOpts& o, const 
   a.dout_lo = static_cast<const uint16_t*>(o.dout_lo);
   const int opt = (o.qk_norm ? kNorm : 0) | (o.dout_lo ? kOpt2 : 0);
   if (w377) return launch<3, 7, 7, 4, true>(d, a, opt, s);
+  if (w999) return launch<9, 9, 9, 2, true>(d, a, opt, s);
   return launch<5, 9, 9, 2, true>(d, a, opt, s);
 }
 

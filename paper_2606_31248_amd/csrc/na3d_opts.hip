@@ -136,10 +136,12 @@ unsigned blocks_for(int64_t n) {
   do {                                                 \
     if ((d).dtype == STRATA_BF16) {                    \
       if ((d).head_dim == 32) F(uint16_t, 32);         \
-      else F(uint16_t, 64);                            \
+      else if ((d).head_dim == 64) F(uint16_t, 64);    \
+      else F(uint16_t, 128);                           \
     } else {                                           \
       if ((d).head_dim == 32) F(float, 32);            \
-      else F(float, 64);                               \
+      else if ((d).head_dim == 64) F(float, 64);       \
+      else F(float, 128);                              \
     }                                                  \
   } while (0)
 

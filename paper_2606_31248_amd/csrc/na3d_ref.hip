@@ -155,10 +155,12 @@ void launch_na3d_fwd_ref(const strata_na3d_desc& d, const NaOpts& o, const void*
                          const void* v, const float* cs, void* out, float* lse, hipStream_t s) {
   if (d.dtype == STRATA_BF16) {
     if (d.head_dim == 32) fwd_ref<uint16_t, 32>(d, o, q, k, v, cs, out, lse, s);
-    else fwd_ref<uint16_t, 64>(d, o, q, k, v, cs, out, lse, s);
+    else if (d.head_dim == 64) fwd_ref<uint16_t, 64>(d, o, q, k, v, cs, out, lse, s);
+    else fwd_ref<uint16_t, 128>(d, o, q, k, v, cs, out, lse, s);
   } else {
     if (d.head_dim == 32) fwd_ref<float, 32>(d, o, q, k, v, cs, out, lse, s);
-    else fwd_ref<float, 64>(d, o, q, k, v, cs, out, lse, s);
+    else if (d.head_dim == 64) fwd_ref<float, 64>(d, o, q, k, v, cs, out, lse, s);
+    else fwd_ref<float, 128>(d, o, q, k, v, cs, out, lse, s);
   }
 }
 
@@ -344,10 +346,12 @@ void launch_na3d_bwd_ref(int part, const strata_na3d_desc& d, const BwdOpts& o, 
                          float* dvec, hipStream_t s) {
   if (d.dtype == STRATA_BF16) {
     if (d.head_dim == 32) bwd_ref<uint16_t, 32>(part, d, o, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
-    else bwd_ref<uint16_t, 64>(part, d, o, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+    else if (d.head_dim == 64) bwd_ref<uint16_t, 64>(part, d, o, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+    else bwd_ref<uint16_t, 128>(part, d, o, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
   } else {
     if (d.head_dim == 32) bwd_ref<float, 32>(part, d, o, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
-    else bwd_ref<float, 64>(part, d, o, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+    else if (d.head_dim == 64) bwd_ref<float, 64>(part, d, o, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+    else bwd_ref<float, 128>(part, d, o, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
   }
 }
 

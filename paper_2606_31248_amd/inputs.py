@@ -166,6 +166,21 @@ FACE_ROLLOUT = Workload("face_rollout_81x16x8x64x64_d64_w3x7x7", 1005, "bf16",
 
 WORKLOADS = {w.name: w for w in (TINY_F32, SMALL_BF16, TRAIN_TILE, TRAIN_TILE_BWD, FACE_ROLLOUT)}
 
+# The paper's own shapes (App. B.1): 24 levels, NA3D window 9x9x9 on tiles of
+# 64x64 or 128x128 cells = 16x16 or 32x32 tokens (16 heads, head_dim 64); the
+# column-wise blocks attend along all 24 levels of a column (window 24x1x1);
+# the de-aliasing decoder's NA3D runs at full resolution, 64x64 pixels x 24
+# levels, with width 128 (one head of 128 channels here).
+PAPER_TILE16 = Workload("paper_96x16x24x16x16_d64_w9x9x9", 1006, "bf16",
+                        96, 16, 24, 16, 16, 64, 9, 9, 9)
+PAPER_TILE32 = Workload("paper_24x16x24x32x32_d64_w9x9x9", 1007, "bf16",
+                        24, 16, 24, 32, 32, 64, 9, 9, 9)
+PAPER_COLUMN = Workload("paper_column_96x16x24x16x16_d64_w24x1x1", 1008, "bf16",
+                        96, 16, 24, 16, 16, 64, 24, 1, 1)
+PAPER_DECODER = Workload("paper_decoder_2x1x24x64x64_d128_w9x9x9", 1009, "bf16",
+                         2, 1, 24, 64, 64, 128, 9, 9, 9)
+PAPER_WORKLOADS = {w.name: w for w in (PAPER_TILE16, PAPER_TILE32, PAPER_COLUMN, PAPER_DECODER)}
+
 FACE_OVERLAP = 8  # tokens shared by neighbouring tiles of the face rollout step
 
 

@@ -21,7 +21,8 @@ def brute_window(i, L, k):
     return set(range(best, best + k))
 
 
-@pytest.mark.parametrize("L,k", [(1, 1), (5, 1), (7, 7), (10, 7), (16, 7), (9, 3), (64, 9), (8, 5), (13, 13)])
+@pytest.mark.parametrize("L,k", [(1, 1), (5, 1), (7, 7), (10, 7), (16, 7), (9, 3), (64, 9), (8, 5), (13, 13),
+                                 (6, 6), (24, 24)])
 def test_axis_index_brute_force(L, k):
     starts, qlo, qhi = oracle.axis_index(L, k)
     for i in range(L):
@@ -32,7 +33,8 @@ def test_axis_index_brute_force(L, k):
 
 
 def test_axis_index_rejects_bad_windows():
-    for L, k in ((5, 2), (5, 7), (0, 1), (5, 0)):
+    # even windows are accepted only when they span the whole axis
+    for L, k in ((5, 2), (5, 7), (0, 1), (5, 0), (8, 6), (24, 22)):
         with pytest.raises(ValueError):
             oracle.axis_index(L, k)
 
@@ -67,7 +69,9 @@ def rand(shape, seed):
 
 @pytest.mark.parametrize("shape,window", [((1, 2, 3, 6, 7, 8), (3, 3, 5)),
                                           ((2, 1, 4, 5, 9, 4), (1, 5, 3)),
-                                          ((1, 1, 5, 8, 8, 16), (5, 7, 7))])
+                                          ((1, 1, 5, 8, 8, 16), (5, 7, 7)),
+                                          ((1, 2, 6, 4, 5, 8), (6, 1, 1)),    # column-wise: all levels, even
+                                          ((1, 1, 10, 9, 9, 8), (9, 9, 9))])
 def test_fwd_matches_dense_masked_attention(shape, window):
     q, k, v = (rand(shape, s) for s in (1, 2, 3))
     scale = 0.37
@@ -76,6 +80,21 @@ def test_fwd_matches_dense_masked_attention(shape, window):
     assert mask.sum(1).min() == mask.sum(1).max() == np.prod(window)
     np.testing.assert_allclose(o, O, rtol=0, atol=1e-12)
     np.testing.assert_allclose(lse, L, rtol=0, atol=1e-12)
+
+
+def test_column_window_is_attention_along_each_column():
+    """Window (Z, 1, 1): every query attends to all Z levels of its own column --
+    plain softmax attention per column (torch SDPA, float64), even Z included."""
+    shape = (2, 2, 6, 3, 4, 8)
+    q, k, v = (rand(shape, s) for s in (70, 71, 72))
+    out, lse = oracle.na3d_fwd(q, k, v, (6, 1, 1), 0.4)
+    t = lambda a: torch.from_numpy(np.moveaxis(a, 2, 4).copy())  # [B, h, H, W, Z, d]
+    ref = torch.nn.functional.scaled_dot_product_attention(t(q), t(k), t(v), scale=0.4).numpy()
+    np.testing.assert_allclose(out, np.moveaxis(ref, 4, 2), rtol=0, atol=1e-12)
+    S = np.einsum("bhyxid,bhyxjd->bhyxij", t(q).numpy(), t(k).numpy()) * 0.4
+    m = S.max(-1)
+    rl = m + np.log(np.exp(S - m[..., None]).sum(-1))
+    np.testing.assert_allclose(lse, np.moveaxis(rl, 4, 2), rtol=0, atol=1e-12)
 
 
 def test_full_window_is_plain_attention():
