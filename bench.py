@@ -312,6 +312,47 @@ def options_train_bwd(steps: int) -> dict:
     return res
 
 
+def paper_shapes(steps: int) -> dict:
+    """The paper's own attention shapes (24 levels): NA3D 9x9x9 on 16x16- and
+    32x32-token tiles, column-wise attention over all 24 levels, the decoder's
+    head_dim-128 NA3D; forward (and backward) against their rooflines.  Inputs
+    are seeded N(0,1) drawn on the device (their values do not change the time)."""
+    import torch
+    from paper_2606_31248_amd import binding as Bd
+    from paper_2606_31248_amd import inputs as I
+    from paper_2606_31248_amd import pipeline as Pp
+    dev = torch.device("cuda:0")
+    res = {}
+    for wl, bwd in ((I.PAPER_TILE16, True), (I.PAPER_TILE32, True), (I.PAPER_COLUMN, True), (I.PAPER_DECODER, False)):
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(wl.seed)
+        q, k, v, g = (torch.randn(wl.shape(), generator=gen, device=dev).to(torch.bfloat16) for _ in range(4))
+        cs = None
+        if wl.ky > 1 or wl.kx > 1:  # the rotation cancels inside a column
+            geom = Pp.TileGeometry(*(torch.from_numpy(x).to(dev) for x in wl.placement().as_int32()))
+            _, cs = Pp.stereo_phases(geom, wl.H, wl.W, wl.d)
+        desc = Bd.desc_for(q, (wl.kz, wl.ky, wl.kx), wl.scale)
+        out = torch.empty_like(q)
+        lse = torch.empty(wl.shape()[:-1], dtype=torch.float32, device=dev)
+        n = wl.B * wl.heads * wl.N
+        fl, nb = 4.0 * n * wl.K * wl.d, n * (4 * wl.d * 2 + 4)
+        ms = _timed(lambda: Bd.strata_na3d_fwd(desc, q, k, v, cs, out, lse), steps)
+        row = dict(roofline_row(fl, nb, ms), ms=round(ms, 4), pct_bf16_peak=round(100 * fl / ms / 1e9 / PEAK_BF16_TFLOPS, 2))
+        entry = {"shape": list(wl.shape()), "window": [wl.kz, wl.ky, wl.kx], "fwd": row}
+        if bwd:
+            ws = torch.empty(Bd.strata_na3d_bwd_workspace_size(desc), dtype=torch.uint8, device=dev)
+            dq, dk, dv = (torch.empty_like(q) for _ in range(3))
+            ms = _timed(lambda: Bd.strata_na3d_bwd(desc, q, k, v, cs, out, g, lse, dq, dk, dv, ws), steps)
+            fl, nb = 10.0 * n * wl.K * wl.d, n * (8 * wl.d * 2 + 4)
+            entry["bwd"] = dict(roofline_row(fl, nb, ms), ms=round(ms, 4),
+                                pct_bf16_peak=round(100 * fl / ms / 1e9 / PEAK_BF16_TFLOPS, 2))
+            del ws, dq, dk, dv
+        res[wl.name] = entry
+        del q, k, v, g, out, lse, cs
+        torch.cuda.empty_cache()
+    return res
+
+
 def roofline_row(flops: float, nbytes: float, ms: float) -> dict:
     """Achieved rate of a kernel against min(MFMA peak, intensity x HBM peak)."""
     ai = flops / nbytes
@@ -483,6 +524,12 @@ def main():
         torch.cuda.empty_cache()
         res["options"]["train_tile_bwd"] = options_train_bwd(a.train_steps)
         res["rows"]["f1_qk_norm_gate_bwd_train_tile"] = res["options"]["train_tile_bwd"]["norm_gate_d"]
+        torch.cuda.empty_cache()
+        ps = paper_shapes(a.train_steps)
+        res["paper_shapes"] = ps
+        res["rows"]["f2_na3d_fwd_w999_paper_tile16"] = ps[I.PAPER_TILE16.name]["fwd"]
+        res["rows"]["f2_na3d_bwd_w999_paper_tile16"] = ps[I.PAPER_TILE16.name]["bwd"]
+        res["rows"]["f2_column_fwd_paper"] = ps[I.PAPER_COLUMN.name]["fwd"]
     if a.cpu_tiles > 0:
         res["cpu_baseline"] = cpu_baseline(wl, a.cpu_tiles)
     print(json.dumps(res), flush=True)
