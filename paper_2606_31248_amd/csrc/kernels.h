@@ -79,6 +79,11 @@ void launch_na3d_bwd_gate_prep(const strata_na3d_desc& d, const NaOpts& o, const
 bool launch_na3d_bwd_dq_mfma(const strata_na3d_desc& d, const BwdOpts& o, const void* q,
                              const void* k, const void* v, const float* cs, const void* dout,
                              const float* lse, const float* dvec, void* dq, hipStream_t s);
+// bf16 column-wise backward (dq, dk, dv together), windows (kz, 1, 1) with Z <= 32,
+// head_dim 64; false for any other problem.
+bool launch_na3d_bwd_col(const strata_na3d_desc& d, const BwdOpts& o, const void* q, const void* k,
+                         const void* v, const void* dout, const float* lse, const float* dvec, void* dq,
+                         void* dk, void* dv, hipStream_t s);
 bool launch_na3d_bwd_dkdv_mfma(const strata_na3d_desc& d, const BwdOpts& o, const void* q,
                                const void* k, const void* v, const float* cs, const void* dout,
                                const float* lse, const float* dvec, void* dk, void* dv,

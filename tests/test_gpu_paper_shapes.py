@@ -224,3 +224,53 @@ def test_d128_fwd_bwd_full_oracle(dtype, qk_norm, gkind):
     refs = oracle.na3d_bwd(w(q), w(k), w(v), w(r["dout"]), window, r["scale"], coords=r["c32"], qk_norm=qk_norm,
                            gate=w(g))
     check_bwd_grads((q, k, v, g, r["dout"]), r["grads"], refs, window, r["scale"], dtype, qk_norm, r["c32"])
+
+
+@pytest.mark.parametrize("g_shift", [-40, 24])
+def test_column_bwd_dout_magnitude(g_shift):
+    """dS enters its float16 product with a per-column power-of-two scale: tiny
+    and huge dO keep the bf16 bound (every gradient is linear in dO)."""
+    shape, window = (1, 2, 24, 4, 5, 64), (24, 1, 1)
+    q, k, v = (I.gaussian(shape, 79, s, "bf16") for s in (0, 1, 2))
+    gf = I.bf16_bits_to_f32(I.gaussian(shape, 79, I.STREAM_DO, "bf16")) * np.float32(2.0 ** g_shift)
+    dout = I.f32_to_bf16_bits(gf.astype(np.float32))
+    qd, kd, vd, gd = (dev_tensor(a, "bf16") for a in (q, k, v, dout))
+    scale = 0.125
+    desc = B.desc_for(qd, window, scale)
+    out = torch.empty_like(qd)
+    lse = torch.empty(shape[:-1], dtype=torch.float32, device="cuda")
+    B.strata_na3d_fwd(desc, qd, kd, vd, None, out, lse)
+    ws = torch.empty(B.strata_na3d_bwd_workspace_size(desc), dtype=torch.uint8, device="cuda")
+    dq, dk, dv = (torch.empty_like(qd) for _ in range(3))
+    B.strata_na3d_bwd(desc, qd, kd, vd, None, out, gd, lse, dq, dk, dv, ws)
+    torch.cuda.synchronize()
+    w = lambda a: oracle.widen(a, "bf16")
+    refs = oracle.na3d_bwd(w(q), w(k), w(v), w(dout), window, scale)
+    for name, got, ref in zip(("dq", "dk", "dv"), (dq, dk, dv), refs):
+        check_close(host_f64(got), ref, "bf16", name)
+
+
+def test_column_bwd_full_size_sampled():
+    """Column-wise backward over all 24 levels of the paper tile, one launch;
+    sampled rows of dq, dk, dv vs the oracle on the sampled tiles."""
+    wl = I.PAPER_COLUMN
+    shape = wl.shape()
+    q, k, v, dout = (I.gaussian(shape, wl.seed, s, "bf16") for s in (0, 1, 2, I.STREAM_DO))
+    qd, kd, vd, gd = (dev_tensor(a, "bf16") for a in (q, k, v, dout))
+    desc = B.desc_for(qd, (24, 1, 1), wl.scale)
+    out = torch.empty_like(qd)
+    lse = torch.empty(shape[:-1], dtype=torch.float32, device="cuda")
+    B.strata_na3d_fwd(desc, qd, kd, vd, None, out, lse)
+    ws = torch.empty(B.strata_na3d_bwd_workspace_size(desc), dtype=torch.uint8, device="cuda")
+    dq, dk, dv = (torch.empty_like(qd) for _ in range(3))
+    B.strata_na3d_bwd(desc, qd, kd, vd, None, out, gd, lse, dq, dk, dv, ws)
+    torch.cuda.synchronize()
+    tiles = [0, wl.B - 1]
+    per_tile = wl.heads * wl.N
+    r = np.random.default_rng(wl.seed)
+    sel = np.unique(np.concatenate([r.integers(0, per_tile, 600) + t * per_tile for t in tiles]))
+    local = np.searchsorted(tiles, sel // per_tile) * per_tile + sel % per_tile
+    sub = lambda a: oracle.widen(a[tiles], "bf16")
+    refs = oracle.na3d_bwd(sub(q), sub(k), sub(v), sub(dout), (24, 1, 1), wl.scale, selq=local, selk=local)
+    for name, got, ref in zip(("dq", "dk", "dv"), (dq, dk, dv), refs):
+        check_close(host_f64(got).reshape(-1, wl.d)[sel], ref, "bf16", name)
