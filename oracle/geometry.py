@@ -105,3 +105,57 @@ def tile_coords(face, oy, ox, H: int, W: int, n_cells: int = 2048, patch: int = 
         out[t, :, :, 0] = x
         out[t, :, :, 1] = y
     return out
+
+
+# ----------------------------------------------------------------------------- wind frame (Eq. 2)
+
+def east_north_radial(lat, lon):
+    """Unit vectors (e_hat, n_hat, r_hat) of the local East-North frame at (lat, lon), [..., 3]."""
+    lat, lon = np.broadcast_arrays(np.asarray(lat, dtype=np.float64), np.asarray(lon, dtype=np.float64))
+    e = np.stack([-np.sin(lon), np.cos(lon), np.zeros_like(lon)], -1)
+    n = np.stack([-np.sin(lat) * np.cos(lon), -np.sin(lat) * np.sin(lon), np.cos(lat)], -1)
+    r = np.stack([np.cos(lat) * np.cos(lon), np.cos(lat) * np.sin(lon), np.sin(lat)], -1)
+    return e, n, r
+
+
+def wind_to_tile_frame(U, V, lat, lon, lat0, lon0):
+    """Eq. 2: v = U e + V n at (lat, lon); v_perp = v - (v . r0) r0 on the tangent
+    plane of the tile centre (lat0, lon0); U_loc = v_perp . e0, V_loc = v_perp . n0.
+    Reading: at a pole the frame is the formula's at the computed longitude."""
+    e, n, _ = east_north_radial(lat, lon)
+    e0, n0, r0 = east_north_radial(lat0, lon0)
+    v = np.asarray(U, dtype=np.float64)[..., None] * e + np.asarray(V, dtype=np.float64)[..., None] * n
+    vr = np.sum(v * r0, -1)
+    vp = v - vr[..., None] * r0
+    return np.sum(vp * e0, -1), np.sum(vp * n0, -1)
+
+
+def cell_angle(index, n_cells: int = 2048):
+    """Equiangular angle of the centre of cell ``index`` along one face axis."""
+    return -np.pi / 4 + (np.asarray(index, dtype=np.float64) + 0.5) * (np.pi / 2) / n_cells
+
+
+def wind_tiles(field, face: int, n_cells: int, nty: int, ntx: int, Ht: int, Wt: int, stride_y: int,
+               stride_x: int) -> np.ndarray:
+    """Tiles of a face's wind field in each tile's centre frame.
+
+    field: [P, n_cells, n_cells, 2] float64 (U, V per cell of face ``face``);
+    tile t = a * ntx + b covers cells (a stride_y + i, b stride_x + j), i < Ht,
+    j < Wt; its centre is the point at the mean angles of its first and last
+    cell on each axis.  Returns [nty * ntx, P, Ht, Wt, 2] float64."""
+    field = np.asarray(field, dtype=np.float64)
+    P = field.shape[0]
+    out = np.empty((nty * ntx, P, Ht, Wt, 2))
+    for a in range(nty):
+        for b in range(ntx):
+            rows = a * stride_y + np.arange(Ht)
+            cols = b * stride_x + np.arange(Wt)
+            beta, alpha = cell_angle(rows, n_cells), cell_angle(cols, n_cells)
+            lat0, lon0 = latlon(face, 0.5 * (alpha[0] + alpha[-1]), 0.5 * (beta[0] + beta[-1]))
+            A, Bt = np.meshgrid(alpha, beta, indexing="xy")
+            lat, lon = latlon(np.full(A.shape, face), A, Bt)
+            sub = field[:, rows[0]:rows[-1] + 1, cols[0]:cols[-1] + 1, :]
+            u, v = wind_to_tile_frame(sub[..., 0], sub[..., 1], lat, lon, lat0, lon0)
+            out[a * ntx + b, ..., 0] = u
+            out[a * ntx + b, ..., 1] = v
+    return out

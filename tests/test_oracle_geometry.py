@@ -125,3 +125,62 @@ def test_tile_frame_axes():
     c = G.tile_coords([0], [200], [200], 16, 16)[0]
     assert np.all(np.diff(c[:, :, 0], axis=1) > 0)
     assert np.all(np.diff(c[:, :, 1], axis=0) > 0)
+
+
+# ----------------------------------------------------------------------------- wind frame (Eq. 2)
+
+def test_wind_frame_is_identity_at_the_centre():
+    r = np.random.default_rng(80)
+    lat0, lon0 = 0.3, -1.1
+    U, V = r.standard_normal(5), r.standard_normal(5)
+    u, v = G.wind_to_tile_frame(U, V, lat0, lon0, lat0, lon0)
+    np.testing.assert_allclose(u, U, atol=1e-15)
+    np.testing.assert_allclose(v, V, atol=1e-15)
+
+
+def test_wind_frame_on_the_equator_closed_form():
+    # centre and points on the equator: n = n0 = z, e . e0 = cos(dlon)
+    r = np.random.default_rng(81)
+    lon = r.uniform(-1.2, 1.2, 7)
+    U, V = r.standard_normal(7), r.standard_normal(7)
+    u, v = G.wind_to_tile_frame(U, V, 0.0, lon, 0.0, 0.4)
+    np.testing.assert_allclose(u, U * np.cos(lon - 0.4), atol=1e-14)
+    np.testing.assert_allclose(v, V, atol=1e-14)
+
+
+def test_wind_frame_on_the_centre_meridian_closed_form():
+    # same longitude: e = e0, n . n0 = cos(dlat)
+    r = np.random.default_rng(82)
+    lat = r.uniform(-1.0, 1.0, 7)
+    U, V = r.standard_normal(7), r.standard_normal(7)
+    u, v = G.wind_to_tile_frame(U, V, lat, 0.7, 0.2, 0.7)
+    np.testing.assert_allclose(u, U, atol=1e-14)
+    np.testing.assert_allclose(v, V * np.cos(lat - 0.2), atol=1e-14)
+
+
+def test_wind_frame_keeps_the_tangential_length():
+    # U_loc^2 + V_loc^2 = |v|^2 - (v . r0)^2 with |v|^2 = U^2 + V^2
+    r = np.random.default_rng(83)
+    lat, lon = r.uniform(-1.3, 1.3, 50), r.uniform(-3, 3, 50)
+    lat0, lon0 = 0.5, 2.0
+    U, V = r.standard_normal(50), r.standard_normal(50)
+    u, v = G.wind_to_tile_frame(U, V, lat, lon, lat0, lon0)
+    e, n, _ = G.east_north_radial(lat, lon)
+    _, _, r0 = G.east_north_radial(lat0, lon0)
+    vr = np.sum((U[:, None] * e + V[:, None] * n) * r0, -1)
+    np.testing.assert_allclose(u * u + v * v, U * U + V * V - vr * vr, atol=1e-12)
+
+
+def test_wind_tiles_cut_the_face_and_use_each_tile_centre():
+    n = 64
+    r = np.random.default_rng(84)
+    field = r.standard_normal((2, n, n, 2))
+    t = G.wind_tiles(field, 4, n, 2, 3, 16, 12, 40, 20)
+    assert t.shape == (6, 2, 16, 12, 2)
+    # tile (1, 2): cells (40.., 40..); centre at the mean angles of its first and last cells
+    rows, cols = 40 + np.arange(16), 40 + np.arange(12)
+    beta, alpha = G.cell_angle(rows, n), G.cell_angle(cols, n)
+    lat0, lon0 = G.latlon(4, (alpha[0] + alpha[-1]) / 2, (beta[0] + beta[-1]) / 2)
+    lat, lon = G.latlon(4, alpha[5], beta[3])
+    u, v = G.wind_to_tile_frame(field[1, 43, 45, 0], field[1, 43, 45, 1], lat, lon, lat0, lon0)
+    np.testing.assert_allclose(t[5, 1, 3, 5], [u, v], atol=1e-15)
