@@ -353,6 +353,25 @@ def paper_shapes(steps: int) -> dict:
     return res
 
 
+def wind_frame(steps: int) -> dict:
+    """Wind vectors of the face-rollout tiling, in cells (9 x 9 tiles of 256 x 256
+    cells, stride 224, 8 levels, bf16), rotated into each tile's centre frame
+    while being cut from the face: HBM-bound (one read, one write per value)."""
+    import torch
+    from paper_2606_31248_amd import binding as Bd
+    dev = torch.device("cuda:0")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(1010)
+    n, P = 2048, 8
+    field = torch.randn((P, n, n, 2), generator=gen, device=dev).to(torch.bfloat16)
+    tiles = torch.empty((81, P, 256, 256, 2), dtype=torch.bfloat16, device=dev)
+    ms = _timed(lambda: Bd.strata_wind_tile_frame(field, 0, 9, 9, 224, 224, tiles), steps)
+    nbytes = 2 * tiles.numel() * 2
+    del field, tiles
+    return {"workload": "face_rollout_cells_81x8x256x256x2_bf16", "ms": round(ms, 4), "bound": "hbm",
+            "achieved_gbs": round(nbytes / ms / 1e6, 1), "frac_hbm": round(nbytes / ms / 1e6 / PEAK_HBM_GBS, 4)}
+
+
 def roofline_row(flops: float, nbytes: float, ms: float) -> dict:
     """Achieved rate of a kernel against min(MFMA peak, intensity x HBM peak)."""
     ai = flops / nbytes
@@ -530,6 +549,8 @@ def main():
         res["rows"]["f2_na3d_fwd_w999_paper_tile16"] = ps[I.PAPER_TILE16.name]["fwd"]
         res["rows"]["f2_na3d_bwd_w999_paper_tile16"] = ps[I.PAPER_TILE16.name]["bwd"]
         res["rows"]["f2_column_fwd_paper"] = ps[I.PAPER_COLUMN.name]["fwd"]
+        torch.cuda.empty_cache()
+        res["rows"]["f4_wind_tile_frame_face"] = wind_frame(a.train_steps)
     if a.cpu_tiles > 0:
         res["cpu_baseline"] = cpu_baseline(wl, a.cpu_tiles)
     print(json.dumps(res), flush=True)

@@ -9,7 +9,9 @@
  *     with NATTEN's border-clamped windows (Sec. 3.2), forward and backward;
  *   - the overlapping-tile stitch S = D^-1 P^T W and its extraction P
  *     (App. F, "Tile stitching", "Linear operator interpretation");
- *   - QK RMSNorm and the sigmoid output gate of the attention block (App. B.5).
+ *   - QK RMSNorm and the sigmoid output gate of the attention block (App. B.5);
+ *   - the wind vectors of each tile in its centre's East-North frame (Sec. 3.3,
+ *     Eq. 2).
  *
  * Conventions shared by every call:
  *   - Pointers are DEVICE pointers owned by the caller unless stated otherwise.
@@ -72,6 +74,25 @@ strata_status strata_stereo_coords(const int32_t* tile_face, const int32_t* tile
                                    const int32_t* tile_ox, int32_t B, int32_t H, int32_t W,
                                    int32_t face_cells, int32_t patch, double l_scale,
                                    float* coords, void* stream);
+
+/* ---- wind vectors into the tile-centre frame (Sec. 3.3, Eq. 2) -------------
+ * Cuts tiles from one cube face's horizontal wind and expresses every wind
+ * vector in the East-North frame at its tile's centre:
+ *   v = U e + V n  with the unit East and North vectors (e, n) at the cell's
+ *   (lat, lon);  v_perp = v - (v . r0) r0;  U_loc = v_perp . e0,
+ *   V_loc = v_perp . n0  with (e0, n0, r0) at the tile centre.
+ * field: [P, face_cells, face_cells, 2] of dtype, (U, V) per cell of face
+ * `face` (0..5, orientation as in strata_stereo_coords) for P planes (levels);
+ * cell (i, j) has angles alpha = -pi/4 + (j + 1/2) (pi/2)/face_cells (columns)
+ * and beta likewise from the row i.  Tile t = a*ntx + b covers the Ht x Wt
+ * cells from (a*stride_y, b*stride_x); its centre is the point at the mean
+ * angles of its first and last cell on each axis (at a pole the frame is the
+ * formula's at the computed longitude).  tiles: [nty*ntx, P, Ht, Wt, 2] of
+ * dtype.  Geometry and the 2x2 rotation in float32 for bf16 data, in float64
+ * for float32 data.  Tiles must fit on the face. */
+strata_status strata_wind_tile_frame(const void* field, int32_t face, int32_t face_cells, int32_t nty,
+                                     int32_t ntx, int32_t P, int32_t Ht, int32_t Wt, int32_t stride_y,
+                                     int32_t stride_x, void* tiles, strata_dtype dtype, void* stream);
 
 /* ---- a2: StereoRoPE phase table (Sec. 3.3) --------------------------------
  * cs[b, y, x, t] = (cos th, sin th) for pair t < head_dim/2, with

@@ -25,7 +25,7 @@ EXPORTS = (
     "strata_stereo_coords", "strata_stereorope_phases", "strata_stereorope_apply",
     "strata_na3d_fwd", "strata_na3d_bwd_workspace_size", "strata_na3d_bwd",
     "strata_na3d_fwd_ex", "strata_na3d_bwd_ex_workspace_size", "strata_na3d_bwd_ex",
-    "strata_tile_blend", "strata_tile_extract", "strata_na_axis_index",
+    "strata_tile_blend", "strata_tile_extract", "strata_na_axis_index", "strata_wind_tile_frame",
     "strata_status_string", "strata_last_error",
 )
 
@@ -71,6 +71,7 @@ def load(path: str = LIB_PATH):
         "strata_tile_blend": [P, i32, i32, i32, i32, i32, i32, i32, i32, P, P, i32, i32, st, P],
         "strata_tile_extract": [P, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32, P, st, P],
         "strata_na_axis_index": [i32, i32, P, P, P, P],
+        "strata_wind_tile_frame": [P, i32, i32, i32, i32, i32, i32, i32, i32, i32, P, st, P],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -223,3 +224,11 @@ def strata_tile_extract(face, nty, ntx, stride_y, stride_x, tiles, stream=None):
 
 def strata_na_axis_index(L, k, starts, qlo, qhi, stream=None):
     _check(load().strata_na_axis_index(L, k, _ptr(starts), _ptr(qlo), _ptr(qhi), _stream(stream)))
+
+
+def strata_wind_tile_frame(field, face, nty, ntx, stride_y, stride_x, tiles, stream=None):
+    """field: [P, n, n, 2] (U, V per cell of one face); tiles: [nty*ntx, P, Ht, Wt, 2]."""
+    P, n, _, _ = field.shape
+    _, _, Ht, Wt, _ = tiles.shape
+    _check(load().strata_wind_tile_frame(_ptr(field), int(face), n, nty, ntx, P, Ht, Wt, stride_y, stride_x,
+                                         _ptr(tiles), _dtype(field), _stream(stream)))

@@ -233,6 +233,25 @@ strata_status strata_stereo_coords(const int32_t* tile_face, const int32_t* tile
   return check_launch("strata_stereo_coords");
 }
 
+strata_status strata_wind_tile_frame(const void* field, int32_t face, int32_t face_cells, int32_t nty,
+                                     int32_t ntx, int32_t P, int32_t Ht, int32_t Wt, int32_t stride_y,
+                                     int32_t stride_x, void* tiles, strata_dtype dtype, void* stream) {
+  REQUIRE(face >= 0 && face < 6, "wind: face %d not in 0..5", face);
+  REQUIRE(face_cells > 0 && nty > 0 && ntx > 0 && P > 0 && Ht > 0 && Wt > 0 && stride_y > 0 && stride_x > 0,
+          "wind: sizes and strides must be positive");
+  REQUIRE((int64_t)(nty - 1) * stride_y + Ht <= face_cells && (int64_t)(ntx - 1) * stride_x + Wt <= face_cells,
+          "wind: tiles extend past the face");
+  REQUIRE(dtype == STRATA_F32 || dtype == STRATA_BF16, "wind: unknown dtype %d", (int)dtype);
+  REQUIRE((int64_t)P * face_cells * face_cells * 2 < kMaxElems &&
+              (int64_t)nty * ntx * P * Ht * Wt * 2 < kMaxElems && (int64_t)nty * ntx * Ht * Wt < ((int64_t)1 << 31) * 256,
+          "wind: tensor too large");
+  REQUIRE_PTR(field);
+  REQUIRE_PTR(tiles);
+  launch_wind_tile_frame(field, face, face_cells, nty, ntx, P, Ht, Wt, stride_y, stride_x, tiles, dtype,
+                         (hipStream_t)stream);
+  return check_launch("strata_wind_tile_frame");
+}
+
 strata_status strata_stereorope_phases(const float* coords, int32_t B, int32_t H, int32_t W,
                                        int32_t head_dim, double base, float* cs, void* stream) {
   REQUIRE(B > 0 && H > 0 && W > 0, "phases: sizes must be positive");

@@ -25,6 +25,9 @@ void launch_stereo_coords(const int32_t* face, const int32_t* oy, const int32_t*
                           int W, int face_cells, int patch, double l_scale, float* coords,
                           hipStream_t s);
 
+void launch_wind_tile_frame(const void* field, int face, int n_cells, int nty, int ntx, int P, int Ht, int Wt,
+                            int sy, int sx, void* tiles, strata_dtype dt, hipStream_t s);
+
 void launch_rope_phases(const float* coords, int B, int H, int W, int head_dim, double base,
                         float* cs, hipStream_t s);
 

@@ -170,3 +170,13 @@ def test_bwd_ex_requires_dgate_with_a_gate_and_enough_workspace():
     st = L.strata_na3d_bwd_ex(ctypes.byref(d), ctypes.byref(o), p, p, p, None, p, p, p, p, p, p, p, p, need - 1,
                               None)
     assert st == B.STRATA_ERR_WORKSPACE
+
+
+def test_wind_rules():
+    L = B.load()
+    p = fake()
+    assert L.strata_wind_tile_frame(p, 6, 64, 1, 1, 1, 8, 8, 8, 8, p, B.STRATA_F32, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_wind_tile_frame(p, 0, 64, 2, 1, 1, 40, 8, 30, 8, p, B.STRATA_F32, None) == \
+        B.STRATA_ERR_INVALID_ARG   # (2-1)*30 + 40 > 64
+    assert L.strata_wind_tile_frame(None, 0, 64, 1, 1, 1, 8, 8, 8, 8, p, B.STRATA_F32, None) == \
+        B.STRATA_ERR_INVALID_ARG

@@ -1,0 +1,72 @@
+"""GPU parity of the wind rotation into the tile-centre frame (Sec. 3.3, Eq. 2)
+against the CPU oracle, through the C ABI.  float32: max abs error <= 1e-5;
+bf16: within half a bf16 ulp of the exact value plus the float32 arithmetic
+bound 2^-20 (|U| + |V|).  Tiles centred exactly on a pole are left out: the
+East-North frame is undefined there and the computed longitude depends on the
+last bit of the centre."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import geometry as G
+from paper_2606_31248_amd import binding as B
+from paper_2606_31248_amd import inputs as I
+from _util import bf16_half_ulp, dev_tensor, host_f64
+
+pytestmark = pytest.mark.gpu
+
+
+def check_wind(got, ref, uv, dtype):
+    diff = np.abs(got - ref)
+    if dtype == "f32":
+        assert float(np.max(diff)) <= 1e-5
+    else:
+        mag = np.abs(uv[..., 0:1]) + np.abs(uv[..., 1:2])
+        excess = diff - bf16_half_ulp(ref) - 2.0 ** -20 * mag
+        assert float(np.max(excess)) <= 0.0, float(np.max(excess))
+
+
+def run(field_shape, face, nty, ntx, Ht, Wt, sy, sx, dtype, seed):
+    P, n = field_shape[0], field_shape[1]
+    f = I.gaussian(field_shape, seed, 0, dtype, 10.0)
+    fd = dev_tensor(f, dtype)
+    tiles = torch.empty((nty * ntx, P, Ht, Wt, 2), dtype=fd.dtype, device="cuda")
+    B.strata_wind_tile_frame(fd, face, nty, ntx, sy, sx, tiles)
+    torch.cuda.synchronize()
+    fw = I.bf16_bits_to_f32(f).astype(np.float64) if dtype == "bf16" else f.astype(np.float64)
+    ref = G.wind_tiles(fw, face, n, nty, ntx, Ht, Wt, sy, sx)
+    return host_f64(tiles), ref, fw
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("face", [0, 2, 4, 5])
+def test_wind_tiles_match_oracle(dtype, face):
+    # 2 x 3 tiles of 16 x 12 cells on a 64-cell face (no tile centred on a pole)
+    got, ref, fw = run((3, 64, 64, 2), face, 2, 3, 16, 12, 40, 20, dtype, 90 + face)
+    # the (U, V) the oracle saw at every output cell, for the bf16 bound
+    uv = np.stack([fw[:, a * 40:a * 40 + 16, b * 20:b * 20 + 12] for a in range(2) for b in range(3)])
+    check_wind(got, ref, uv, dtype)
+
+
+def test_wind_face_rollout_tiling_sampled():
+    """The face-rollout tiling in cells (9 x 9 tiles of 256 x 256 cells, stride
+    224, on a 2048-cell face), 8 levels, bf16; three tiles checked in full."""
+    n, P = 2048, 8
+    f = I.gaussian((P, n, n, 2), 91, 0, "bf16", 10.0)
+    fd = dev_tensor(f, "bf16")
+    tiles = torch.empty((81, P, 256, 256, 2), dtype=fd.dtype, device="cuda")
+    B.strata_wind_tile_frame(fd, 0, 9, 9, 224, 224, tiles)
+    torch.cuda.synchronize()
+    got = host_f64(tiles)
+    fw = I.bf16_bits_to_f32(f).astype(np.float64)
+    for t in (0, 40, 80):
+        a, b = divmod(t, 9)
+        sub = fw[:, a * 224:a * 224 + 256, b * 224:b * 224 + 256]
+        # the oracle's steps for this tile: its cells' (lat, lon), its centre, Eq. 2
+        rows, cols = a * 224 + np.arange(256), b * 224 + np.arange(256)
+        beta, alpha = G.cell_angle(rows, n), G.cell_angle(cols, n)
+        lat0, lon0 = G.latlon(0, 0.5 * (alpha[0] + alpha[-1]), 0.5 * (beta[0] + beta[-1]))
+        A, Bt = np.meshgrid(alpha, beta, indexing="xy")
+        lat, lon = G.latlon(np.zeros(A.shape, np.int64), A, Bt)
+        u, v = G.wind_to_tile_frame(sub[..., 0], sub[..., 1], lat, lon, lat0, lon0)
+        check_wind(got[t], np.stack([u, v], -1), sub, "bf16")
