@@ -210,6 +210,19 @@ strata_status strata_tile_blend(const void* tiles, int32_t nty, int32_t ntx, int
                                 int32_t stride_x, const float* window, void* out, int32_t Hf,
                                 int32_t Wf, strata_dtype dtype, void* stream);
 
+/* ---- a8: Kaiser-Bessel-derived blend window (App. F, "Tile stitching") -----
+ * window[y * Wt + x] = w(y, Ht) * w(x, Wt) (float32 [Ht * Wt], device) with,
+ * per axis of length L, w(i) = 1 in the interior and, over the `overlap` cells
+ * at each end, the rising half of the KBD window of length 2*overlap:
+ *   w(i) = sqrt(sum_{j<=i} k_j / sum_{j<=overlap} k_j),
+ *   k_j = I0(beta sqrt(1 - (2j/overlap - 1)^2)),  j = 0..overlap,
+ * mirrored at the far end (the smaller value where both ends reach).  The
+ * paper gives no alpha or taper length: beta (= pi alpha) is an argument and
+ * the taper spans the overlap, as the linear ramp does.  1 <= overlap <=
+ * min(Ht, Wt); 0 <= beta <= 700.  Computed in float64, rounded once. */
+strata_status strata_kbd_window(int32_t Ht, int32_t Wt, int32_t overlap, double beta, float* window,
+                                void* stream);
+
 /* ---- a8': tile extraction P (App. F) ---------------------------------------
  * tiles[t, p, i, j, c] = face[p, a*stride_y + i, b*stride_x + j, c] (exact copy). */
 strata_status strata_tile_extract(const void* face, int32_t nty, int32_t ntx, int32_t P,

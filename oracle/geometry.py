@@ -159,3 +159,30 @@ def wind_tiles(field, face: int, n_cells: int, nty: int, ntx: int, Ht: int, Wt: 
             out[a * ntx + b, ..., 0] = u
             out[a * ntx + b, ..., 1] = v
     return out
+
+
+# ----------------------------------------------------------------------------- KBD blend window (App. F)
+
+def kbd_taper(overlap: int, beta: float) -> np.ndarray:
+    """Rising half of the Kaiser-Bessel-derived window of length 2 * overlap:
+    k[j] = I0(beta sqrt(1 - (2 j / overlap - 1)^2)), j = 0..overlap (the Kaiser
+    window of length overlap + 1), w[n] = sqrt(sum_{j<=n} k[j] / sum_j k[j]),
+    n = 0..overlap-1."""
+    j = np.arange(overlap + 1, dtype=np.float64)
+    k = np.i0(beta * np.sqrt(np.clip(1.0 - (2.0 * j / overlap - 1.0) ** 2, 0.0, None)))
+    c = np.cumsum(k)
+    return np.sqrt(c[:-1] / c[-1])
+
+
+def kbd_window_2d(Ht: int, Wt: int, overlap: int, beta: float) -> np.ndarray:
+    """Blend window [Ht * Wt]: per axis 1 in the interior and the KBD taper over
+    ``overlap`` cells at each end (mirrored at the far end); the 2D window is the
+    product of the two axes.  Reading: the taper spans the overlap, as the
+    linear ramp does."""
+    def axis(L):
+        w = np.ones(L)
+        t = kbd_taper(overlap, beta)
+        w[:overlap] = np.minimum(w[:overlap], t)
+        w[L - overlap:] = np.minimum(w[L - overlap:], t[::-1])
+        return w
+    return np.outer(axis(Ht), axis(Wt)).reshape(-1)

@@ -25,7 +25,7 @@ EXPORTS = (
     "strata_stereo_coords", "strata_stereorope_phases", "strata_stereorope_apply",
     "strata_na3d_fwd", "strata_na3d_bwd_workspace_size", "strata_na3d_bwd",
     "strata_na3d_fwd_ex", "strata_na3d_bwd_ex_workspace_size", "strata_na3d_bwd_ex",
-    "strata_tile_blend", "strata_tile_extract", "strata_na_axis_index", "strata_wind_tile_frame",
+    "strata_tile_blend", "strata_tile_extract", "strata_na_axis_index", "strata_wind_tile_frame", "strata_kbd_window",
     "strata_status_string", "strata_last_error",
 )
 
@@ -72,6 +72,7 @@ def load(path: str = LIB_PATH):
         "strata_tile_extract": [P, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32, P, st, P],
         "strata_na_axis_index": [i32, i32, P, P, P, P],
         "strata_wind_tile_frame": [P, i32, i32, i32, i32, i32, i32, i32, i32, i32, P, st, P],
+        "strata_kbd_window": [i32, i32, i32, ctypes.c_double, P, P],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -232,3 +233,8 @@ def strata_wind_tile_frame(field, face, nty, ntx, stride_y, stride_x, tiles, str
     _, _, Ht, Wt, _ = tiles.shape
     _check(load().strata_wind_tile_frame(_ptr(field), int(face), n, nty, ntx, P, Ht, Wt, stride_y, stride_x,
                                          _ptr(tiles), _dtype(field), _stream(stream)))
+
+
+def strata_kbd_window(Ht, Wt, overlap, beta, window, stream=None):
+    """window: float32 [Ht * Wt] on the device."""
+    _check(load().strata_kbd_window(Ht, Wt, overlap, float(beta), _ptr(window), _stream(stream)))

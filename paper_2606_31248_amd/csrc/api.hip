@@ -354,6 +354,16 @@ strata_status strata_tile_blend(const void* tiles, int32_t nty, int32_t ntx, int
   return check_launch("strata_tile_blend");
 }
 
+strata_status strata_kbd_window(int32_t Ht, int32_t Wt, int32_t overlap, double beta, float* window,
+                                void* stream) {
+  REQUIRE(Ht > 0 && Wt > 0 && (int64_t)Ht * Wt < ((int64_t)1 << 31), "kbd: sizes must be positive");
+  REQUIRE(overlap > 0 && overlap <= Ht && overlap <= Wt, "kbd: need 1 <= overlap <= min(Ht, Wt) (got %d)", overlap);
+  REQUIRE(beta >= 0.0 && beta <= 700.0, "kbd: beta must lie in [0, 700]");
+  REQUIRE_PTR(window);
+  launch_kbd_window(Ht, Wt, overlap, beta, window, (hipStream_t)stream);
+  return check_launch("strata_kbd_window");
+}
+
 strata_status strata_tile_extract(const void* face, int32_t nty, int32_t ntx, int32_t P,
                                   int32_t Ht, int32_t Wt, int32_t C, int32_t stride_y,
                                   int32_t stride_x, int32_t Hf, int32_t Wf, void* tiles,

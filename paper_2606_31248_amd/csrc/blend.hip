@@ -274,4 +274,53 @@ void launch_tile_extract(const void* face, int nty, int ntx, int P, int Ht, int 
   }
 }
 
+// ---- Kaiser-Bessel-derived blend window (App. F) -----------------------------
+// Per axis: 1 in the interior, over `overlap` cells at each end the rising half
+// of the KBD window of length 2*overlap, w[n] = sqrt(sum_{j<=n} k_j / sum_j k_j)
+// with the Kaiser weights k_j = I0(beta sqrt(1 - (2j/overlap - 1)^2)),
+// j = 0..overlap; the 2D window is the product of the axes.  I0 by its power
+// series sum_m ((x/2)^(2m) / (m!)^2), summed until the terms stop changing the
+// float64 sum; everything in float64, rounded to float32 once.
+__device__ double bessel_i0(double x) {
+  const double q = 0.25 * x * x;
+  double term = 1.0, sum = 1.0;
+  for (int m = 1; m < 500; ++m) {
+    term *= q / ((double)m * (double)m);
+    const double next = sum + term;
+    if (next == sum) break;
+    sum = next;
+  }
+  return sum;
+}
+
+__device__ double kbd_rise(int n, int overlap, double beta) {
+  double part = 0.0, total = 0.0;
+  for (int j = 0; j <= overlap; ++j) {
+    const double r = 2.0 * (double)j / (double)overlap - 1.0;
+    const double k = bessel_i0(beta * sqrt(fmax(0.0, 1.0 - r * r)));
+    total += k;
+    if (j <= n) part += k;
+  }
+  return sqrt(part / total);
+}
+
+__device__ double kbd_axis(int i, int L, int overlap, double beta) {
+  double w = 1.0;
+  if (i < overlap) w = fmin(w, kbd_rise(i, overlap, beta));
+  if (i >= L - overlap) w = fmin(w, kbd_rise(L - 1 - i, overlap, beta));
+  return w;
+}
+
+__global__ void kbd_window_kernel(int Ht, int Wt, int overlap, double beta, float* __restrict__ window) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= Ht * Wt) return;
+  const int y = idx / Wt, x = idx % Wt;
+  window[idx] = (float)(kbd_axis(y, Ht, overlap, beta) * kbd_axis(x, Wt, overlap, beta));
+}
+
+void launch_kbd_window(int Ht, int Wt, int overlap, double beta, float* window, hipStream_t s) {
+  const int n = Ht * Wt;
+  hipLaunchKernelGGL(kbd_window_kernel, dim3((n + 255) / 256), dim3(256), 0, s, Ht, Wt, overlap, beta, window);
+}
+
 }  // namespace strata

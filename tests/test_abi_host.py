@@ -180,3 +180,12 @@ def test_wind_rules():
         B.STRATA_ERR_INVALID_ARG   # (2-1)*30 + 40 > 64
     assert L.strata_wind_tile_frame(None, 0, 64, 1, 1, 1, 8, 8, 8, 8, p, B.STRATA_F32, None) == \
         B.STRATA_ERR_INVALID_ARG
+
+
+def test_kbd_rules():
+    L = B.load()
+    p = fake()
+    assert L.strata_kbd_window(8, 8, 0, 4.0, p, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_kbd_window(8, 8, 9, 4.0, p, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_kbd_window(8, 8, 4, -1.0, p, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_kbd_window(8, 8, 4, 4.0, None, None) == B.STRATA_ERR_INVALID_ARG

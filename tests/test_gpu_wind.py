@@ -70,3 +70,26 @@ def test_wind_face_rollout_tiling_sampled():
         lat, lon = G.latlon(np.zeros(A.shape, np.int64), A, Bt)
         u, v = G.wind_to_tile_frame(sub[..., 0], sub[..., 1], lat, lon, lat0, lon0)
         check_wind(got[t], np.stack([u, v], -1), sub, "bf16")
+
+
+# ----------------------------------------------------------------------------- KBD window
+
+@pytest.mark.parametrize("Ht,Wt,overlap,beta", [(64, 64, 8, 4 * np.pi), (64, 40, 8, 2.0), (16, 16, 8, 10.0),
+                                                (256, 256, 32, 4 * np.pi), (5, 7, 3, 0.0)])
+def test_kbd_window_matches_oracle(Ht, Wt, overlap, beta):
+    w = torch.empty(Ht * Wt, dtype=torch.float32, device="cuda")
+    B.strata_kbd_window(Ht, Wt, overlap, beta, w)
+    torch.cuda.synchronize()
+    ref = G.kbd_window_2d(Ht, Wt, overlap, beta)
+    assert float(np.max(np.abs(w.cpu().numpy().astype(np.float64) - ref))) <= 1e-7
+
+
+def test_kbd_window_blends_a_constant_field_exactly():
+    """Any positive window reproduces a constant field through the stitch (D^-1 P^T W)."""
+    w = torch.empty(64 * 64, dtype=torch.float32, device="cuda")
+    B.strata_kbd_window(64, 64, 8, 4 * np.pi, w)
+    tiles = torch.full((9, 2, 64, 64, 4), 0.75, dtype=torch.float32, device="cuda")
+    face = torch.empty((2, 176, 176, 4), dtype=torch.float32, device="cuda")
+    B.strata_tile_blend(tiles, 3, 3, 56, 56, w, face)
+    torch.cuda.synchronize()
+    assert torch.all(face == 0.75)

@@ -3,6 +3,7 @@ import numpy as np
 import pytest
 
 import oracle
+from oracle import geometry as G
 from paper_2606_31248_amd import inputs
 
 
@@ -110,3 +111,27 @@ def test_blend_rejects_tiles_past_the_face():
     tiles = np.zeros((4, 1, 8, 8, 1), np.float32)
     with pytest.raises(ValueError):
         oracle.tile_blend(tiles, 2, 2, 8, 8, np.ones(64, np.float32), 15, 16, "f32")
+
+
+# ----------------------------------------------------------------------------- KBD window
+
+@pytest.mark.parametrize("overlap,beta", [(8, 4 * np.pi), (8, 2.0), (16, 10.0), (3, 1.0)])
+def test_kbd_taper_is_scipys_kaiser_bessel_derived_half(overlap, beta):
+    from scipy.signal.windows import kaiser_bessel_derived
+    ref = kaiser_bessel_derived(2 * overlap, beta)[:overlap]
+    np.testing.assert_allclose(G.kbd_taper(overlap, beta), ref, rtol=0, atol=1e-14)
+
+
+def test_kbd_taper_is_power_complementary():
+    # Princen-Bradley: w[n]^2 + w[overlap-1-n]^2 = 1 for the rising half and its mirror
+    t = G.kbd_taper(8, 4 * np.pi)
+    np.testing.assert_allclose(t ** 2 + t[::-1] ** 2, 1.0, atol=1e-14)
+
+
+def test_kbd_window_2d_shape_and_interior():
+    w = G.kbd_window_2d(64, 40, 8, 4 * np.pi).reshape(64, 40)
+    assert np.all(w[8:56, 8:32] == 1.0)
+    t = G.kbd_taper(8, 4 * np.pi)
+    np.testing.assert_allclose(w[3, 20], t[3], atol=0)
+    np.testing.assert_allclose(w[63, 39], t[0] * t[0], atol=1e-16)
+    assert np.all(w > 0) and np.all(w <= 1)
