@@ -186,3 +186,81 @@ def kbd_window_2d(Ht: int, Wt: int, overlap: int, beta: float) -> np.ndarray:
         w[L - overlap:] = np.minimum(w[L - overlap:], t[::-1])
         return w
     return np.outer(axis(Ht), axis(Wt)).reshape(-1)
+
+
+# ----------------------------------------------------------------------------- Duo-grid halo padding (App. F)
+
+# Face axes: a point of face f is normal + a * right + b * up with a = tan(alpha)
+# (columns) and b = tan(beta) (rows), the orientation table above.
+FACE_AXES = {
+    0: ((1, 0, 0), (0, 1, 0), (0, 0, 1)),
+    1: ((0, 1, 0), (-1, 0, 0), (0, 0, 1)),
+    2: ((-1, 0, 0), (0, -1, 0), (0, 0, 1)),
+    3: ((0, -1, 0), (1, 0, 0), (0, 0, 1)),
+    4: ((0, 0, 1), (0, 1, 0), (-1, 0, 0)),
+    5: ((0, 0, -1), (0, 1, 0), (1, 0, 0)),
+}
+
+
+def _unit(v):
+    v = np.asarray(v, dtype=np.float64)
+    return v / np.linalg.norm(v, axis=-1, keepdims=True)
+
+
+def cell_point(face, i, j, n_cells):
+    """Unit sphere point of cell (row i, column j) of a face; indices may lie
+    beyond [0, n) (the face's equiangular mesh extended on its own plane)."""
+    X, Y, Zc = cube_point(face, cell_angle(j, n_cells), cell_angle(i, n_cells))
+    return _unit(np.stack([X, Y, Zc], -1))
+
+
+DUO_TIE = 1e-12  # distances (radians) are compared on this grid; equal ones by (row, col)
+
+
+def duo_halo_neighbours(face, i, j, n_cells):
+    """For the (extended) cell (i, j) of ``face``: the face f' containing its
+    sphere point p (the axis of p's largest component), the 4 cells of f'
+    nearest to p (great-circle distance; distances equal on a 1e-12-radian grid
+    ordered by row, then column), and their inverse-distance weights
+    normalised to sum 1 (a cell at distance 0 takes weight 1).
+    Returns (f', rows[4], cols[4], weights[4]), nearest first."""
+    p = cell_point(face, i, j, n_cells)
+    normals = np.array([FACE_AXES[f][0] for f in range(6)], dtype=np.float64)
+    fp = int(np.argmax(normals @ p))
+    I, J = np.meshgrid(np.arange(n_cells), np.arange(n_cells), indexing="ij")
+    c = cell_point(np.full(I.shape, fp), I, J, n_cells).reshape(-1, 3)
+    d = np.arctan2(np.linalg.norm(np.cross(c, p), axis=-1), c @ p)
+    key = np.round(d / DUO_TIE).astype(np.int64)
+    order = np.lexsort((J.reshape(-1), I.reshape(-1), key))[:4]
+    rows, cols, dist = I.reshape(-1)[order], J.reshape(-1)[order], d[order]
+    if dist[0] == 0.0:
+        w = np.array([1.0, 0.0, 0.0, 0.0])
+    else:
+        w = 1.0 / dist
+        w = w / w.sum()
+    return fp, rows, cols, w
+
+
+def duo_pad(field, halo: int) -> np.ndarray:
+    """Duo-grid padding of all six faces: field [6, P, n, n, C] -> [6, P, n + 2h,
+    n + 2h, C].  Interior cells are copied; every halo cell of face f extends
+    f's equiangular mesh on its own plane, is projected to the sphere and takes
+    the inverse-distance-weighted values of the 4 nearest cells of the face that
+    contains it (summed nearest first)."""
+    field = np.asarray(field, dtype=np.float64)
+    _, P, n, _, C = field.shape
+    m = n + 2 * halo
+    out = np.empty((6, P, m, m, C))
+    for f in range(6):
+        out[f, :, halo:halo + n, halo:halo + n] = field[f]
+        for ip in range(m):
+            for jp in range(m):
+                i, j = ip - halo, jp - halo
+                if 0 <= i < n and 0 <= j < n:
+                    continue
+                fp, rows, cols, w = duo_halo_neighbours(f, i, j, n)
+                acc = np.zeros((P, C))
+                for k in range(4):
+                    acc = acc + w[k] * field[fp, :, rows[k], cols[k]]
+                out[f, :, ip, jp] = acc
+    return out

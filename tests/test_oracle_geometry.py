@@ -184,3 +184,77 @@ def test_wind_tiles_cut_the_face_and_use_each_tile_centre():
     lat, lon = G.latlon(4, alpha[5], beta[3])
     u, v = G.wind_to_tile_frame(field[1, 43, 45, 0], field[1, 43, 45, 1], lat, lon, lat0, lon0)
     np.testing.assert_allclose(t[5, 1, 3, 5], [u, v], atol=1e-15)
+
+
+# ----------------------------------------------------------------------------- Duo-grid padding (App. F)
+
+def test_duo_extended_mesh_continues_the_face():
+    # on the face's own plane the extended mesh keeps the angular spacing: a halo
+    # cell's point is the cube point at the extended equiangular angles
+    p = G.cell_point(0, -1, 5, 16)
+    X, Y, Zc = G.cube_point(0, G.cell_angle(5, 16), G.cell_angle(-1, 16))
+    np.testing.assert_allclose(p, np.array([X, Y, Zc]) / np.sqrt(X * X + Y * Y + Zc * Zc), atol=1e-15)
+
+
+@pytest.mark.parametrize("face", range(6))
+def test_duo_halo_points_land_on_the_neighbouring_faces(face):
+    # a point half a cell beyond an edge lies on the face across that edge, next to it
+    n = 16
+    for i, j in ((-1, 7), (n, 7), (7, -1), (7, n)):
+        fp, rows, cols, w = G.duo_halo_neighbours(face, i, j, n)
+        assert fp != face
+        assert np.isclose(w.sum(), 1.0) and np.all(w >= 0)
+        on_edge = (rows.min() == 0) or (rows.max() == n - 1) or (cols.min() == 0) or (cols.max() == n - 1)
+        assert on_edge
+
+
+def test_duo_nearest_cells_lie_in_the_lattice_block_around_the_point():
+    # the four nearest cells of the containing face always lie within the 6 x 6
+    # block of its cell lattice around the point's (clamped) floor index: a
+    # local search finds them
+    for n, h in ((16, 4), (48, 6)):
+        for f in range(6):
+            for i in range(-h, n + h):
+                for j in range(-h, n + h):
+                    if 0 <= i < n and 0 <= j < n:
+                        continue
+                    fp, rows, cols, _ = G.duo_halo_neighbours(f, i, j, n)
+                    nrm, right, up = (np.asarray(v, dtype=np.float64) for v in G.FACE_AXES[fp])
+                    p = G.cell_point(f, i, j, n)
+                    step = (np.pi / 2) / n
+                    u = (np.arctan((p @ right) / (p @ nrm)) + np.pi / 4) / step - 0.5
+                    v = (np.arctan((p @ up) / (p @ nrm)) + np.pi / 4) / step - 0.5
+                    j0 = min(max(int(np.floor(u)), 0), n - 2)
+                    i0 = min(max(int(np.floor(v)), 0), n - 2)
+                    r0, c0 = min(max(i0 - 2, 0), n - 6), min(max(j0 - 2, 0), n - 6)
+                    assert np.all((rows >= r0) & (rows < r0 + 6) & (cols >= c0) & (cols < c0 + 6)), (n, f, i, j)
+
+
+def test_duo_pad_copies_the_interior_and_keeps_constants():
+    n, h = 8, 2
+    r = np.random.default_rng(86)
+    field = r.standard_normal((6, 2, n, n, 3))
+    out = G.duo_pad(field, h)
+    np.testing.assert_array_equal(out[:, :, h:h + n, h:h + n], field)
+    const = G.duo_pad(np.full((6, 1, n, n, 1), 2.5), h)
+    np.testing.assert_allclose(const, 2.5, atol=1e-14)
+
+
+def test_duo_pad_continues_a_smooth_field():
+    # f(p) = p . g sampled at the cell centres of all faces: the halo holds f at the
+    # halo point to within the inverse-distance interpolation error (<= the
+    # largest neighbour distance times |g|), an O(1) error for a wrong face or
+    # orientation
+    n, h = 24, 3
+    g = np.array([0.3, -1.1, 0.7])
+    field = np.empty((6, 1, n, n, 1))
+    I, J = np.meshgrid(np.arange(n), np.arange(n), indexing="ij")
+    for f in range(6):
+        field[f, 0, :, :, 0] = G.cell_point(np.full(I.shape, f), I, J, n) @ g
+    out = G.duo_pad(field, h)
+    step = (np.pi / 2) / n
+    m = n + 2 * h
+    for f in range(6):
+        Ip, Jp = np.meshgrid(np.arange(m) - h, np.arange(m) - h, indexing="ij")
+        exact = G.cell_point(np.full(Ip.shape, f), Ip, Jp, n) @ g
+        assert np.max(np.abs(out[f, 0, :, :, 0] - exact)) <= 2.0 * step * np.linalg.norm(g)
