@@ -214,19 +214,20 @@ def cell_point(face, i, j, n_cells):
     return _unit(np.stack([X, Y, Zc], -1))
 
 
-DUO_TIE = 1e-12  # distances (radians) are compared on this grid; equal ones by (row, col)
+DUO_TIE = 1e-12  # face scores and distances are compared on this grid; equal ones by index
 
 
 def duo_halo_neighbours(face, i, j, n_cells):
     """For the (extended) cell (i, j) of ``face``: the face f' containing its
-    sphere point p (the axis of p's largest component), the 4 cells of f'
-    nearest to p (great-circle distance; distances equal on a 1e-12-radian grid
+    sphere point p (the axis of p's largest component; a point on an edge or
+    corner, where components are equal on the 1e-12 grid, belongs to the
+    lowest-numbered of its faces), the 4 cells of f' nearest to p (great-circle distance; distances equal on a 1e-12-radian grid
     ordered by row, then column), and their inverse-distance weights
     normalised to sum 1 (a cell at distance 0 takes weight 1).
     Returns (f', rows[4], cols[4], weights[4]), nearest first."""
     p = cell_point(face, i, j, n_cells)
     normals = np.array([FACE_AXES[f][0] for f in range(6)], dtype=np.float64)
-    fp = int(np.argmax(normals @ p))
+    fp = int(np.argmax(np.round((normals @ p) / DUO_TIE).astype(np.int64)))
     I, J = np.meshgrid(np.arange(n_cells), np.arange(n_cells), indexing="ij")
     c = cell_point(np.full(I.shape, fp), I, J, n_cells).reshape(-1, 3)
     d = np.arctan2(np.linalg.norm(np.cross(c, p), axis=-1), c @ p)

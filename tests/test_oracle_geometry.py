@@ -208,11 +208,35 @@ def test_duo_halo_points_land_on_the_neighbouring_faces(face):
         assert on_edge
 
 
+@pytest.mark.parametrize("face", range(6))
+def test_duo_points_on_an_edge_belong_to_the_lower_face_at_equal_distances(face):
+    # halo cells on the diagonal beyond a face corner project onto the edge
+    # shared by the two faces across that corner: both faces contain the point,
+    # their 4 nearest cells are mirror images at the same distances, and the
+    # lower-numbered face is taken
+    n = 20
+    normals = np.array([G.FACE_AXES[g][0] for g in range(6)], dtype=np.float64)
+    for k in range(3):
+        for i, j in ((-1 - k, -1 - k), (-1 - k, n + k), (n + k, -1 - k), (n + k, n + k)):
+            p = G.cell_point(face, i, j, n)
+            s = normals @ p
+            both = np.flatnonzero(s > s.max() - 1e-12)
+            assert len(both) == 2 and face not in both
+            fp, _, _, _ = G.duo_halo_neighbours(face, i, j, n)
+            assert fp == both.min()
+            dists = []
+            for g in both:
+                I, J = np.meshgrid(np.arange(n), np.arange(n), indexing="ij")
+                c = G.cell_point(np.full(I.shape, g), I, J, n).reshape(-1, 3)
+                dists.append(np.sort(np.arccos(np.clip(c @ p, -1, 1)))[:4])
+            np.testing.assert_allclose(dists[0], dists[1], atol=1e-7)
+
+
 def test_duo_nearest_cells_lie_in_the_lattice_block_around_the_point():
     # the four nearest cells of the containing face always lie within the 6 x 6
     # block of its cell lattice around the point's (clamped) floor index: a
     # local search finds them
-    for n, h in ((16, 4), (48, 6)):
+    for n, h in ((16, 4), (20, 3), (32, 8), (48, 6)):
         for f in range(6):
             for i in range(-h, n + h):
                 for j in range(-h, n + h):
