@@ -372,6 +372,24 @@ def wind_frame(steps: int) -> dict:
             "achieved_gbs": round(nbytes / ms / 1e6, 1), "frac_hbm": round(nbytes / ms / 1e6 / PEAK_HBM_GBS, 4)}
 
 
+def duo_padding(steps: int) -> dict:
+    """Duo-grid halo padding of all six 2048-cell faces by 16 cells (8 levels x 4
+    channels, bf16): interior copy plus the 4-neighbour halo gather; HBM-bound."""
+    import torch
+    from paper_2606_31248_amd import binding as Bd
+    dev = torch.device("cuda:0")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(1011)
+    n, h, P, C = 2048, 16, 8, 4
+    faces = torch.randn((6, P, n, n, C), generator=gen, device=dev).to(torch.bfloat16)
+    padded = torch.empty((6, P, n + 2 * h, n + 2 * h, C), dtype=torch.bfloat16, device=dev)
+    ms = _timed(lambda: Bd.strata_duo_pad(faces, h, padded), steps)
+    nbytes = (faces.numel() + padded.numel()) * 2
+    del faces, padded
+    return {"workload": "duo_pad_6x8x2048x2048x4_halo16_bf16", "ms": round(ms, 4), "bound": "hbm",
+            "achieved_gbs": round(nbytes / ms / 1e6, 1), "frac_hbm": round(nbytes / ms / 1e6 / PEAK_HBM_GBS, 4)}
+
+
 def roofline_row(flops: float, nbytes: float, ms: float) -> dict:
     """Achieved rate of a kernel against min(MFMA peak, intensity x HBM peak)."""
     ai = flops / nbytes
@@ -551,6 +569,8 @@ def main():
         res["rows"]["f2_column_fwd_paper"] = ps[I.PAPER_COLUMN.name]["fwd"]
         torch.cuda.empty_cache()
         res["rows"]["f4_wind_tile_frame_face"] = wind_frame(a.train_steps)
+        torch.cuda.empty_cache()
+        res["rows"]["f3_duo_pad_faces"] = duo_padding(a.train_steps)
     if a.cpu_tiles > 0:
         res["cpu_baseline"] = cpu_baseline(wl, a.cpu_tiles)
     print(json.dumps(res), flush=True)

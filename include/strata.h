@@ -11,7 +11,9 @@
  *     (App. F, "Tile stitching", "Linear operator interpretation");
  *   - QK RMSNorm and the sigmoid output gate of the attention block (App. B.5);
  *   - the wind vectors of each tile in its centre's East-North frame (Sec. 3.3,
- *     Eq. 2).
+ *     Eq. 2);
+ *   - the Duo-grid halo padding across cube faces and the Kaiser-Bessel-derived
+ *     blend window (App. F).
  *
  * Conventions shared by every call:
  *   - Pointers are DEVICE pointers owned by the caller unless stated otherwise.
@@ -209,6 +211,21 @@ strata_status strata_tile_blend(const void* tiles, int32_t nty, int32_t ntx, int
                                 int32_t Ht, int32_t Wt, int32_t C, int32_t stride_y,
                                 int32_t stride_x, const float* window, void* out, int32_t Hf,
                                 int32_t Wf, strata_dtype dtype, void* stream);
+
+/* ---- Duo-grid halo padding P (App. F, "DUO-style boundary padding") --------
+ * faces: [6, P, n, n, C] of dtype (P planes of n x n cells with C channels per
+ * face, orientation as in strata_stereo_coords); padded: [6, P, n + 2 halo,
+ * n + 2 halo, C].  Interior cells are copied.  Halo cell (i, j) of face f
+ * (i or j outside [0, n)) extends f's equiangular mesh on f's own plane
+ * (angles -pi/4 + (index + 1/2)(pi/2)/n), is projected to the sphere, and
+ * takes the inverse great-circle-distance weighted average of the 4 cells
+ * nearest to that point on the face containing it (the face of its largest
+ * coordinate); distances equal on a 1e-12-radian grid are ordered by (row,
+ * column), a cell at distance 0 takes the whole weight.  Sums nearest first,
+ * in float32 for bf16 data, float64 for float32 data.  n >= 16,
+ * 1 <= halo <= n/4. */
+strata_status strata_duo_pad(const void* faces, int32_t P, int32_t n, int32_t C, int32_t halo, void* padded,
+                             strata_dtype dtype, void* stream);
 
 /* ---- a8: Kaiser-Bessel-derived blend window (App. F, "Tile stitching") -----
  * window[y * Wt + x] = w(y, Ht) * w(x, Wt) (float32 [Ht * Wt], device) with,

@@ -26,6 +26,7 @@ EXPORTS = (
     "strata_na3d_fwd", "strata_na3d_bwd_workspace_size", "strata_na3d_bwd",
     "strata_na3d_fwd_ex", "strata_na3d_bwd_ex_workspace_size", "strata_na3d_bwd_ex",
     "strata_tile_blend", "strata_tile_extract", "strata_na_axis_index", "strata_wind_tile_frame", "strata_kbd_window",
+    "strata_duo_pad",
     "strata_status_string", "strata_last_error",
 )
 
@@ -73,6 +74,7 @@ def load(path: str = LIB_PATH):
         "strata_na_axis_index": [i32, i32, P, P, P, P],
         "strata_wind_tile_frame": [P, i32, i32, i32, i32, i32, i32, i32, i32, i32, P, st, P],
         "strata_kbd_window": [i32, i32, i32, ctypes.c_double, P, P],
+        "strata_duo_pad": [P, i32, i32, i32, i32, P, st, P],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -238,3 +240,9 @@ def strata_wind_tile_frame(field, face, nty, ntx, stride_y, stride_x, tiles, str
 def strata_kbd_window(Ht, Wt, overlap, beta, window, stream=None):
     """window: float32 [Ht * Wt] on the device."""
     _check(load().strata_kbd_window(Ht, Wt, overlap, float(beta), _ptr(window), _stream(stream)))
+
+
+def strata_duo_pad(faces, halo, padded, stream=None):
+    """faces: [6, P, n, n, C]; padded: [6, P, n + 2 halo, n + 2 halo, C]."""
+    _, P, n, _, C = faces.shape
+    _check(load().strata_duo_pad(_ptr(faces), P, n, C, int(halo), _ptr(padded), _dtype(faces), _stream(stream)))

@@ -17,7 +17,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libstrata.so")
 
-SOURCES = ["api.hip", "geometry.hip", "rope.hip", "blend.hip", "na3d_ref.hip", "na3d_opts.hip", "na3d_col.hip", "na3d_mfma_q.hip",
+SOURCES = ["api.hip", "geometry.hip", "rope.hip", "blend.hip", "na3d_ref.hip", "na3d_opts.hip", "na3d_col.hip", "duo.hip", "na3d_mfma_q.hip",
            "na3d_mfma_kv.hip", "na3d_fwd_zs.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -354,6 +354,19 @@ strata_status strata_tile_blend(const void* tiles, int32_t nty, int32_t ntx, int
   return check_launch("strata_tile_blend");
 }
 
+strata_status strata_duo_pad(const void* faces, int32_t P, int32_t n, int32_t C, int32_t halo, void* padded,
+                             strata_dtype dtype, void* stream) {
+  REQUIRE(P > 0 && C > 0, "duo: P and C must be positive");
+  REQUIRE(n >= 16 && halo > 0 && halo <= n / 4, "duo: need n >= 16 and 1 <= halo <= n/4 (n=%d, halo=%d)", n, halo);
+  REQUIRE(dtype == STRATA_F32 || dtype == STRATA_BF16, "duo: unknown dtype %d", (int)dtype);
+  const int64_t m = (int64_t)n + 2 * halo;
+  REQUIRE(6LL * P * m * m * C < kMaxElems, "duo: tensor too large");
+  REQUIRE_PTR(faces);
+  REQUIRE_PTR(padded);
+  launch_duo_pad(faces, P, n, C, halo, padded, dtype, (hipStream_t)stream);
+  return check_launch("strata_duo_pad");
+}
+
 strata_status strata_kbd_window(int32_t Ht, int32_t Wt, int32_t overlap, double beta, float* window,
                                 void* stream) {
   REQUIRE(Ht > 0 && Wt > 0 && (int64_t)Ht * Wt < ((int64_t)1 << 31), "kbd: sizes must be positive");

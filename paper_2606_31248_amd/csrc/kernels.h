@@ -96,6 +96,8 @@ void launch_tile_blend(const void* tiles, int nty, int ntx, int P, int Ht, int W
                        int sx, const float* window, void* out, int Hf, int Wf, strata_dtype dt,
                        hipStream_t s);
 
+void launch_duo_pad(const void* in, int P, int n, int C, int halo, void* out, strata_dtype dt, hipStream_t s);
+
 void launch_kbd_window(int Ht, int Wt, int overlap, double beta, float* window, hipStream_t s);
 
 void launch_tile_extract(const void* face, int nty, int ntx, int P, int Ht, int Wt, int C, int sy,

@@ -189,3 +189,11 @@ def test_kbd_rules():
     assert L.strata_kbd_window(8, 8, 9, 4.0, p, None) == B.STRATA_ERR_INVALID_ARG
     assert L.strata_kbd_window(8, 8, 4, -1.0, p, None) == B.STRATA_ERR_INVALID_ARG
     assert L.strata_kbd_window(8, 8, 4, 4.0, None, None) == B.STRATA_ERR_INVALID_ARG
+
+
+def test_duo_rules():
+    L = B.load()
+    p = fake()
+    assert L.strata_duo_pad(p, 1, 8, 1, 1, p, B.STRATA_F32, None) == B.STRATA_ERR_INVALID_ARG     # n < 16
+    assert L.strata_duo_pad(p, 1, 32, 1, 9, p, B.STRATA_F32, None) == B.STRATA_ERR_INVALID_ARG    # halo > n/4
+    assert L.strata_duo_pad(p, 1, 32, 1, 0, p, B.STRATA_F32, None) == B.STRATA_ERR_INVALID_ARG

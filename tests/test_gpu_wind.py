@@ -93,3 +93,63 @@ def test_kbd_window_blends_a_constant_field_exactly():
     B.strata_tile_blend(tiles, 3, 3, 56, 56, w, face)
     torch.cuda.synchronize()
     assert torch.all(face == 0.75)
+
+
+# ----------------------------------------------------------------------------- Duo-grid padding
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("n,halo,P,C", [(16, 4, 2, 3), (32, 8, 1, 8), (20, 3, 1, 2)])
+def test_duo_pad_matches_oracle(dtype, n, halo, P, C):
+    f = I.gaussian((6, P, n, n, C), 95 + n, 0, dtype)
+    fd = dev_tensor(f, dtype)
+    m = n + 2 * halo
+    out = torch.empty((6, P, m, m, C), dtype=fd.dtype, device="cuda")
+    B.strata_duo_pad(fd, halo, out)
+    torch.cuda.synchronize()
+    got = host_f64(out)
+    fw = I.bf16_bits_to_f32(f).astype(np.float64) if dtype == "bf16" else f.astype(np.float64)
+    ref = G.duo_pad(fw, halo)
+    # interior: an exact copy
+    assert np.array_equal(got[:, :, halo:halo + n, halo:halo + n], fw)
+    diff = np.abs(got - ref)
+    if dtype == "f32":
+        assert float(np.max(diff)) <= 1e-5
+    else:  # one rounding of a float32 sum of 4 weighted values
+        bound = bf16_half_ulp(ref) + 2.0 ** -20 * 4 * float(np.max(np.abs(fw)))
+        assert float(np.max(diff - bound)) <= 0.0
+
+
+@pytest.mark.parametrize("dtype", ["bf16"])
+def test_duo_pad_full_size_sampled(dtype):
+    # six 2048-cell faces, 8 levels x 4 channels, halo 16 (the measured
+    # workload): interior exact, sampled halo cells (corner diagonals among
+    # them) against the oracle's brute-force neighbours over the whole face
+    # (about 5 s of CPU per cell)
+    n, h, P, C = 2048, 16, 8, 4
+    m = n + 2 * h
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(1011)
+    fd = torch.randn((6, P, n, n, C), generator=gen, device="cuda").to(torch.bfloat16)
+    out = torch.empty((6, P, m, m, C), dtype=torch.bfloat16, device="cuda")
+    B.strata_duo_pad(fd, h, out)
+    torch.cuda.synchronize()
+    assert torch.equal(out[:, :, h:h + n, h:h + n], fd)
+    rng = np.random.default_rng(7)
+    cells = [(0, 0, 0), (1, m - 1, m - 1), (2, h - 1, n + h), (5, m // 3, m - 1)]
+    for _ in range(2):
+        f = int(rng.integers(6))
+        side = int(rng.integers(4))
+        t = int(rng.integers(m))
+        band = int(rng.integers(h))
+        ip, jp = [(band, t), (m - 1 - band, t), (t, band), (t, m - 1 - band)][side]
+        cells.append((f, ip, jp))
+    for f, ip, jp in cells:
+        fp, rows, cols, w = G.duo_halo_neighbours(f, ip - h, jp - h, n)
+        vals = fd[fp][:, torch.as_tensor(rows, device="cuda"), torch.as_tensor(cols, device="cuda")]
+        vals = vals.float().cpu().numpy().astype(np.float64)  # [P, 4, C]
+        ref = np.zeros((P, C))
+        for k in range(4):
+            ref = ref + w[k] * vals[:, k]
+        got = out[f, :, ip, jp].float().cpu().numpy().astype(np.float64)
+        bound = bf16_half_ulp(ref) + 2.0 ** -20 * 4 * float(np.max(np.abs(vals)))
+        assert float(np.max(np.abs(got - ref) - bound)) <= 0.0, (f, ip, jp)
