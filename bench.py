@@ -374,7 +374,9 @@ def wind_frame(steps: int) -> dict:
 
 def duo_padding(steps: int) -> dict:
     """Duo-grid halo padding of all six 2048-cell faces by 16 cells (8 levels x 4
-    channels, bf16): interior copy plus the 4-neighbour halo gather; HBM-bound."""
+    channels, bf16): the padding operator built once as a plan, then applied
+    (interior copy plus the 4-neighbour halo gather, HBM-bound); the one-shot
+    entry point (geometry recomputed in the same launch) beside it."""
     import torch
     from paper_2606_31248_amd import binding as Bd
     dev = torch.device("cuda:0")
@@ -383,11 +385,21 @@ def duo_padding(steps: int) -> dict:
     n, h, P, C = 2048, 16, 8, 4
     faces = torch.randn((6, P, n, n, C), generator=gen, device=dev).to(torch.bfloat16)
     padded = torch.empty((6, P, n + 2 * h, n + 2 * h, C), dtype=torch.bfloat16, device=dev)
-    ms = _timed(lambda: Bd.strata_duo_pad(faces, h, padded), steps)
+    plan = torch.empty(Bd.strata_duo_plan_bytes(n, h), dtype=torch.uint8, device=dev)
+    plan_ms = _timed(lambda: Bd.strata_duo_plan(n, h, plan), max(steps, 3))
+    ms = _timed(lambda: Bd.strata_duo_pad_planned(faces, h, plan, padded), steps)
+    one_shot_ms = _timed(lambda: Bd.strata_duo_pad(faces, h, padded), steps)
     nbytes = (faces.numel() + padded.numel()) * 2
-    del faces, padded
+    del faces, padded, plan
     return {"workload": "duo_pad_6x8x2048x2048x4_halo16_bf16", "ms": round(ms, 4), "bound": "hbm",
-            "achieved_gbs": round(nbytes / ms / 1e6, 1), "frac_hbm": round(nbytes / ms / 1e6 / PEAK_HBM_GBS, 4)}
+            "achieved_gbs": round(nbytes / ms / 1e6, 1), "frac_hbm": round(nbytes / ms / 1e6 / PEAK_HBM_GBS, 4),
+            "plan_build_ms": round(plan_ms, 4), "one_shot_ms": round(one_shot_ms, 4),
+            "alg_bytes": nbytes}
+
+
+def _done(what: str, t_start: float) -> None:
+    """One progress line on stderr per finished measurement (stdout carries only the result)."""
+    print(f"bench: {what} done at {time.perf_counter() - t_start:.1f} s", file=sys.stderr, flush=True)
 
 
 def roofline_row(flops: float, nbytes: float, ms: float) -> dict:
@@ -439,6 +451,8 @@ def main():
     from paper_2606_31248_amd import pipeline as Pp
 
     Bd.load()
+    t_start = time.perf_counter()
+    _done("library load", t_start)
     wl = I.FACE_ROLLOUT
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -499,6 +513,7 @@ def main():
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / a.steps
     avg = {n: float(np.mean([s.elapsed_time(e) for s, e in lst])) for n, lst in ev.items()}
+    _done("face-rollout step", t_start)
 
     flops = 4.0 * wl.B * wl.heads * wl.N * wl.K * wl.d
     tflops_step = flops / (ms_step * 1e-3) / 1e12
@@ -550,6 +565,7 @@ def main():
         opt = options_face_fwd(wl, desc, q, k, v, cs, out, a.train_steps)
         res["options"] = {"face_fwd": opt}
         res["rows"]["f1_qk_norm_gate_fwd_face"] = opt["norm_gate_d"]
+        _done("options face forward", t_start)
         del q, k, v, out, face, coords, cs
         torch.cuda.empty_cache()
         tt = train_tile(a.train_steps)
@@ -558,21 +574,27 @@ def main():
         res["rows"]["a2_rope_apply_train_tile"] = {"bound": "hbm", "achieved_gbs": tt["rope_apply_qk"]["gbs"],
                                                    "frac_hbm": tt["rope_apply_qk"]["frac_hbm"]}
         res["train_tile"] = tt
+        _done("training tile", t_start)
         torch.cuda.empty_cache()
         res["options"]["train_tile_bwd"] = options_train_bwd(a.train_steps)
         res["rows"]["f1_qk_norm_gate_bwd_train_tile"] = res["options"]["train_tile_bwd"]["norm_gate_d"]
+        _done("options backward", t_start)
         torch.cuda.empty_cache()
         ps = paper_shapes(a.train_steps)
         res["paper_shapes"] = ps
         res["rows"]["f2_na3d_fwd_w999_paper_tile16"] = ps[I.PAPER_TILE16.name]["fwd"]
         res["rows"]["f2_na3d_bwd_w999_paper_tile16"] = ps[I.PAPER_TILE16.name]["bwd"]
         res["rows"]["f2_column_fwd_paper"] = ps[I.PAPER_COLUMN.name]["fwd"]
+        _done("paper shapes", t_start)
         torch.cuda.empty_cache()
         res["rows"]["f4_wind_tile_frame_face"] = wind_frame(a.train_steps)
+        _done("wind frame", t_start)
         torch.cuda.empty_cache()
         res["rows"]["f3_duo_pad_faces"] = duo_padding(a.train_steps)
+        _done("duo padding", t_start)
     if a.cpu_tiles > 0:
         res["cpu_baseline"] = cpu_baseline(wl, a.cpu_tiles)
+        _done("cpu baseline", t_start)
     print(json.dumps(res), flush=True)
 
 

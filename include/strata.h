@@ -220,12 +220,35 @@ strata_status strata_tile_blend(const void* tiles, int32_t nty, int32_t ntx, int
  * (angles -pi/4 + (index + 1/2)(pi/2)/n), is projected to the sphere, and
  * takes the inverse great-circle-distance weighted average of the 4 cells
  * nearest to that point on the face containing it (the face of its largest
- * coordinate); distances equal on a 1e-12-radian grid are ordered by (row,
- * column), a cell at distance 0 takes the whole weight.  Sums nearest first,
- * in float32 for bf16 data, float64 for float32 data.  n >= 16,
- * 1 <= halo <= n/4. */
+ * coordinate; a point on an edge or corner, where face scores are equal on a
+ * 1e-12 grid, belongs to the lowest-numbered face); distances equal on a
+ * 1e-12-radian grid are ordered by (row, column), a cell at distance 0 takes
+ * the whole weight.  Sums nearest first, in float32 for bf16 data, float64 for
+ * float32 data.  Both buffers are device memory owned by the caller and must
+ * not overlap.  n >= 16, 1 <= halo <= n/4, 6 P n rows plus one block per 256
+ * halo cells below 2^31; otherwise STRATA_ERR_INVALID_ARG and nothing is
+ * launched.  One kernel launch on `stream`. */
 strata_status strata_duo_pad(const void* faces, int32_t P, int32_t n, int32_t C, int32_t halo, void* padded,
                              strata_dtype dtype, void* stream);
+
+/* The same padding operator P built once and applied many times (App. F: P is a
+ * fixed sparse matrix with 4 non-zeros per halo cell, so a model that pads
+ * every layer of a rollout reuses it).
+ *
+ * strata_duo_plan_bytes: size of the plan for (n, halo), 0 if the pair is
+ * invalid.  strata_duo_plan: writes the plan (geometry only, no field data)
+ * into `plan`, caller-owned device memory of at least that many bytes, 16-byte
+ * aligned; its contents are opaque and valid for this (n, halo) only.
+ * strata_duo_pad_planned: as strata_duo_pad, with the neighbours and weights
+ * read from a plan written by strata_duo_plan for the same (n, halo); results
+ * are identical to strata_duo_pad's.  Errors: STRATA_ERR_INVALID_ARG for the
+ * rules of strata_duo_pad, a NULL or misaligned plan, or plan_bytes below
+ * strata_duo_plan_bytes(n, halo); nothing is launched then. */
+size_t strata_duo_plan_bytes(int32_t n, int32_t halo);
+strata_status strata_duo_plan(int32_t n, int32_t halo, void* plan, size_t plan_bytes, void* stream);
+strata_status strata_duo_pad_planned(const void* faces, int32_t P, int32_t n, int32_t C, int32_t halo,
+                                     const void* plan, size_t plan_bytes, void* padded, strata_dtype dtype,
+                                     void* stream);
 
 /* ---- a8: Kaiser-Bessel-derived blend window (App. F, "Tile stitching") -----
  * window[y * Wt + x] = w(y, Ht) * w(x, Wt) (float32 [Ht * Wt], device) with,

@@ -26,7 +26,7 @@ EXPORTS = (
     "strata_na3d_fwd", "strata_na3d_bwd_workspace_size", "strata_na3d_bwd",
     "strata_na3d_fwd_ex", "strata_na3d_bwd_ex_workspace_size", "strata_na3d_bwd_ex",
     "strata_tile_blend", "strata_tile_extract", "strata_na_axis_index", "strata_wind_tile_frame", "strata_kbd_window",
-    "strata_duo_pad",
+    "strata_duo_pad", "strata_duo_plan_bytes", "strata_duo_plan", "strata_duo_pad_planned",
     "strata_status_string", "strata_last_error",
 )
 
@@ -75,6 +75,8 @@ def load(path: str = LIB_PATH):
         "strata_wind_tile_frame": [P, i32, i32, i32, i32, i32, i32, i32, i32, i32, P, st, P],
         "strata_kbd_window": [i32, i32, i32, ctypes.c_double, P, P],
         "strata_duo_pad": [P, i32, i32, i32, i32, P, st, P],
+        "strata_duo_plan": [i32, i32, P, ctypes.c_size_t, P],
+        "strata_duo_pad_planned": [P, i32, i32, i32, i32, P, ctypes.c_size_t, P, st, P],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -92,6 +94,8 @@ def load(path: str = LIB_PATH):
     L.strata_na3d_bwd_workspace_size.restype = ctypes.c_size_t
     L.strata_na3d_bwd_ex_workspace_size.argtypes = [D, O]
     L.strata_na3d_bwd_ex_workspace_size.restype = ctypes.c_size_t
+    L.strata_duo_plan_bytes.argtypes = [i32, i32]
+    L.strata_duo_plan_bytes.restype = ctypes.c_size_t
     L.strata_status_string.argtypes = [st]
     L.strata_status_string.restype = ctypes.c_char_p
     L.strata_last_error.argtypes = []
@@ -246,3 +250,22 @@ def strata_duo_pad(faces, halo, padded, stream=None):
     """faces: [6, P, n, n, C]; padded: [6, P, n + 2 halo, n + 2 halo, C]."""
     _, P, n, _, C = faces.shape
     _check(load().strata_duo_pad(_ptr(faces), P, n, C, int(halo), _ptr(padded), _dtype(faces), _stream(stream)))
+
+
+def strata_duo_plan_bytes(n, halo):
+    """Bytes of the padding plan for (n, halo); 0 if the pair is invalid."""
+    return int(load().strata_duo_plan_bytes(int(n), int(halo)))
+
+
+def strata_duo_plan(n, halo, plan, stream=None):
+    """plan: a device buffer (e.g. uint8) of at least strata_duo_plan_bytes(n, halo) bytes."""
+    _check(load().strata_duo_plan(int(n), int(halo), _ptr(plan), plan.numel() * plan.element_size(),
+                                  _stream(stream)))
+
+
+def strata_duo_pad_planned(faces, halo, plan, padded, stream=None):
+    """As strata_duo_pad, with the neighbours and weights read from a plan."""
+    _, P, n, _, C = faces.shape
+    _check(load().strata_duo_pad_planned(_ptr(faces), P, n, C, int(halo), _ptr(plan),
+                                         plan.numel() * plan.element_size(), _ptr(padded), _dtype(faces),
+                                         _stream(stream)))

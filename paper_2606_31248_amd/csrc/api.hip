@@ -361,10 +361,47 @@ strata_status strata_duo_pad(const void* faces, int32_t P, int32_t n, int32_t C,
   REQUIRE(dtype == STRATA_F32 || dtype == STRATA_BF16, "duo: unknown dtype %d", (int)dtype);
   const int64_t m = (int64_t)n + 2 * halo;
   REQUIRE(6LL * P * m * m * C < kMaxElems, "duo: tensor too large");
+  // one block per interior row plus one per 256 halo cells
+  REQUIRE(6LL * P * n + (6 * (m * m - (int64_t)n * n) + 255) / 256 < INT32_MAX, "duo: too many rows (P*n=%lld)",
+          (long long)P * n);
   REQUIRE_PTR(faces);
   REQUIRE_PTR(padded);
   launch_duo_pad(faces, P, n, C, halo, padded, dtype, (hipStream_t)stream);
   return check_launch("strata_duo_pad");
+}
+
+size_t strata_duo_plan_bytes(int32_t n, int32_t halo) {
+  if (n < 16 || halo < 1 || halo > n / 4) return 0;
+  return (size_t)duo_plan_bytes(n, halo);
+}
+
+strata_status strata_duo_plan(int32_t n, int32_t halo, void* plan, size_t plan_bytes, void* stream) {
+  REQUIRE(n >= 16 && halo > 0 && halo <= n / 4, "duo plan: need n >= 16 and 1 <= halo <= n/4 (n=%d, halo=%d)", n,
+          halo);
+  REQUIRE_PTR(plan);
+  REQUIRE(reinterpret_cast<uintptr_t>(plan) % 16 == 0, "duo plan: plan must be 16-byte aligned");
+  REQUIRE(plan_bytes >= (size_t)duo_plan_bytes(n, halo), "duo plan: plan_bytes %zu < %lld", plan_bytes,
+          (long long)duo_plan_bytes(n, halo));
+  launch_duo_plan(n, halo, plan, (hipStream_t)stream);
+  return check_launch("strata_duo_plan");
+}
+
+strata_status strata_duo_pad_planned(const void* faces, int32_t P, int32_t n, int32_t C, int32_t halo,
+                                     const void* plan, size_t plan_bytes, void* padded, strata_dtype dtype,
+                                     void* stream) {
+  REQUIRE(P > 0 && C > 0, "duo: P and C must be positive");
+  REQUIRE(n >= 16 && halo > 0 && halo <= n / 4, "duo: need n >= 16 and 1 <= halo <= n/4 (n=%d, halo=%d)", n, halo);
+  REQUIRE(dtype == STRATA_F32 || dtype == STRATA_BF16, "duo: unknown dtype %d", (int)dtype);
+  const int64_t m = (int64_t)n + 2 * halo;
+  REQUIRE(6LL * P * m * m * C < kMaxElems, "duo: tensor too large");
+  REQUIRE_PTR(faces);
+  REQUIRE_PTR(padded);
+  REQUIRE_PTR(plan);
+  REQUIRE(reinterpret_cast<uintptr_t>(plan) % 16 == 0, "duo: plan must be 16-byte aligned");
+  REQUIRE(plan_bytes >= (size_t)duo_plan_bytes(n, halo), "duo: plan_bytes %zu < %lld (a plan for other n, halo?)",
+          plan_bytes, (long long)duo_plan_bytes(n, halo));
+  launch_duo_pad_planned(faces, plan, P, n, C, halo, padded, dtype, (hipStream_t)stream);
+  return check_launch("strata_duo_pad_planned");
 }
 
 strata_status strata_kbd_window(int32_t Ht, int32_t Wt, int32_t overlap, double beta, float* window,

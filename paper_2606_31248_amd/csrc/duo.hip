@@ -8,8 +8,9 @@
 //
 // Neighbour search: the 4 nearest cells lie within the 6 x 6 block of the
 // containing face's cell lattice around the point's (clamped) floor index, so
-// only those 36 candidates are measured.  Face scores and distances are
-// compared on a 1e-12 grid, equal ones by index (face number; row, then
+// only those 36 candidates are ranked, first by the cosine of their angle to the
+// point; the exact great-circle distance is taken for the few within 1e-9 of the
+// fourth-largest cosine.  Face scores and distances are compared on a 1e-12 grid, equal ones by index (face number; row, then
 // column): exact ties -- a point on an edge, cells mirrored about it -- resolve
 // the same way everywhere.  Geometry in float64 per halo cell; the weighted
 // sums (nearest first, fused multiply-adds from 0) in float32 for bf16 data, in
@@ -73,40 +74,93 @@ __device__ void halo_neighbours(int f, int i, int j, int n, int* fp_out, int* ro
   double nn[3], rr[3], uu[3];
   face_axes(fp, nn, rr, uu);
   const double pn = nn[0] * p[0] + nn[1] * p[1] + nn[2] * p[2];
-  const double a = (rr[0] * p[0] + rr[1] * p[1] + rr[2] * p[2]) / pn;
-  const double b = (uu[0] * p[0] + uu[1] * p[1] + uu[2] * p[2]) / pn;
+  const double pr = rr[0] * p[0] + rr[1] * p[1] + rr[2] * p[2];
+  const double pu = uu[0] * p[0] + uu[1] * p[1] + uu[2] * p[2];
+  const double a = pr / pn, b = pu / pn;
   const int j0 = min(max((int)floor((atan(a) + 0.25 * M_PI) / step - 0.5), 0), n - 2);
   const int i0 = min(max((int)floor((atan(b) + 0.25 * M_PI) / step - 0.5), 0), n - 2);
   const int r0 = min(max(i0 - 2, 0), n - 6), c0 = min(max(j0 - 2, 0), n - 6);
+  // the block's mesh is separable: one tangent per row and per column
+  double ta[6], tb[6];
+  for (int t = 0; t < 6; ++t) {
+    ta[t] = tan(-0.25 * M_PI + ((double)(c0 + t) + 0.5) * step);
+    tb[t] = tan(-0.25 * M_PI + ((double)(r0 + t) + 0.5) * step);
+  }
+  // cosine of the angle from p to candidate (r, c) of the block: decreasing in
+  // the great-circle distance
+  // (the face axes are orthonormal: |n + x r + y u|^2 = 1 + x^2 + y^2)
+  auto cosine = [&](int r, int c) {
+    const double x = ta[c], y = tb[r];
+    return (pn + x * pr + y * pu) * rsqrt(1.0 + x * x + y * y);
+  };
+  // pass 1: the fourth-largest cosine (fixed-index bubble steps keep the list
+  // in registers)
+  double top[4] = {-2.0, -2.0, -2.0, -2.0};
+  for (int r = 0; r < 6; ++r)
+    for (int c = 0; c < 6; ++c) {
+      const double cs = cosine(r, c);
+      if (cs > top[3]) {
+        top[3] = cs;
+#pragma unroll
+        for (int t = 3; t > 0; --t)
+          if (top[t] > top[t - 1]) {
+            const double x = top[t];
+            top[t] = top[t - 1];
+            top[t - 1] = x;
+          }
+      }
+    }
+  // pass 2: exact distances on the tie grid for the shortlist only.  A
+  // candidate whose cosine is 1e-9 below the fourth-largest lies more than
+  // 1e-9 rad farther than four others (|d cos / d angle| <= 1), far beyond the
+  // grid, so dropping it cannot change the selected four.
+  const double floor_cos = top[3] - 1e-9;
   long long key[4];
   double dist[4];
+#pragma unroll
   for (int k = 0; k < 4; ++k) {
     key[k] = LLONG_MAX;
     rows[k] = n;
     cols[k] = n;
     dist[k] = 0.0;
   }
-  for (int r = r0; r < r0 + 6; ++r)
-    for (int c = c0; c < c0 + 6; ++c) {
-      double q[3];
-      cell_point(fp, r, c, step, q);
+  for (int r = 0; r < 6; ++r)
+    for (int c = 0; c < 6; ++c) {
+      if (cosine(r, c) < floor_cos) continue;
+      double q[3], qs = 0.0;
+      for (int k = 0; k < 3; ++k) {
+        q[k] = nn[k] + ta[c] * rr[k] + tb[r] * uu[k];
+        qs += q[k] * q[k];
+      }
+      const double qi = 1.0 / sqrt(qs);
+      for (int k = 0; k < 3; ++k) q[k] *= qi;
       const double cx = q[1] * p[2] - q[2] * p[1], cy = q[2] * p[0] - q[0] * p[2], cz = q[0] * p[1] - q[1] * p[0];
       const double d = atan2(sqrt(cx * cx + cy * cy + cz * cz), q[0] * p[0] + q[1] * p[1] + q[2] * p[2]);
       const long long kd = llrint(d / kTie);
-      // insert (kd, r, c) into the sorted top 4 (candidates come in (row, column) order)
-      int pos = 4;
-      while (pos > 0 && kd < key[pos - 1]) --pos;
-      if (pos == 4) continue;
-      for (int s = 3; s > pos; --s) {
-        key[s] = key[s - 1];
-        rows[s] = rows[s - 1];
-        cols[s] = cols[s - 1];
-        dist[s] = dist[s - 1];
+      // place (kd, row, column) last and move it up past strictly larger keys:
+      // candidates come in (row, column) order, so equal keys keep that order
+      if (kd < key[3]) {
+        key[3] = kd;
+        rows[3] = r0 + r;
+        cols[3] = c0 + c;
+        dist[3] = d;
+#pragma unroll
+        for (int t = 3; t > 0; --t)
+          if (key[t] < key[t - 1]) {
+            const long long k1 = key[t];
+            key[t] = key[t - 1];
+            key[t - 1] = k1;
+            const int r1 = rows[t];
+            rows[t] = rows[t - 1];
+            rows[t - 1] = r1;
+            const int c1 = cols[t];
+            cols[t] = cols[t - 1];
+            cols[t - 1] = c1;
+            const double d1 = dist[t];
+            dist[t] = dist[t - 1];
+            dist[t - 1] = d1;
+          }
       }
-      key[pos] = kd;
-      rows[pos] = r;
-      cols[pos] = c;
-      dist[pos] = d;
     }
   if (dist[0] == 0.0) {
     w[0] = 1.0;
@@ -122,29 +176,113 @@ __device__ void halo_neighbours(int f, int i, int j, int n, int* fp_out, int* ro
   *fp_out = fp;
 }
 
-template <typename T>
-__global__ void duo_halo_kernel(const T* __restrict__ in, int P, int n, int C, int halo, T* __restrict__ out) {
+// padded cell (ip, jp) of halo cell number hc of a face: the top band (halo
+// rows of m cells), the bottom band, then the left/right strips (2 halo cells
+// per interior row)
+__device__ __forceinline__ void halo_cell_position(int64_t hc, int n, int halo, int* ip, int* jp) {
   const int m = n + 2 * halo;
+  const int64_t band = (int64_t)halo * m;
+  if (hc < band) {
+    *ip = (int)(hc / m);
+    *jp = (int)(hc % m);
+  } else if (hc < 2 * band) {
+    const int64_t r = hc - band;
+    *ip = n + halo + (int)(r / m);
+    *jp = (int)(r % m);
+  } else {
+    const int64_t r = hc - 2 * band;
+    *ip = halo + (int)(r / (2 * halo));
+    const int k = (int)(r % (2 * halo));
+    *jp = k < halo ? k : n + k;
+  }
+}
+
+// G channels of one cell moved as one access
+template <typename T, int G>
+struct alignas(sizeof(T) * G) Group {
+  T v[G];
+};
+
+// accumulation type: float for bf16 data, double for float32 data
+__device__ __forceinline__ float widen(uint16_t x) { return bf16_to_f32(x); }
+__device__ __forceinline__ double widen(float x) { return x; }
+
+// one channel group of one halo cell, all P levels: weighted sum of the 4
+// source cells, nearest first.  src and dst point at the group's first channel
+// of level 0; off holds the source cells' element offsets.
+template <typename T, int G>
+__device__ __forceinline__ void gather_group(const T* src, const int64_t* off, const double* w, int P,
+                                             int64_t plane_in, int64_t plane_out, T* dst) {
+  using Acc = decltype(widen(T{}));
+  Acc wk[4];
+  for (int k = 0; k < 4; ++k) wk[k] = (Acc)w[k];
+  for (int p = 0; p < P; ++p) {
+    Group<T, G> g[4], o;
+    for (int k = 0; k < 4; ++k) g[k] = *reinterpret_cast<const Group<T, G>*>(src + p * plane_in + off[k]);
+    for (int e = 0; e < G; ++e) {
+      Acc acc = 0;
+      for (int k = 0; k < 4; ++k) acc = fma(wk[k], widen(g[k].v[e]), acc);
+      if constexpr (sizeof(T) == 2)
+        o.v[e] = f32_to_bf16(acc);
+      else
+        o.v[e] = (float)acc;
+    }
+    *reinterpret_cast<Group<T, G>*>(dst + p * plane_out) = o;
+  }
+}
+
+// one halo cell, all P levels and C channels, G channels per access
+template <typename T, int G>
+__device__ __forceinline__ void gather_cell(const T* src, const int64_t* off, const double* w, int P, int C,
+                                            int64_t plane_in, int64_t plane_out, T* dst) {
+  for (int c = 0; c < C; c += G) gather_group<T, G>(src + c, off, w, P, plane_in, plane_out, dst + c);
+}
+
+// interior row i of plane pl: out[pl, halo + i, halo : halo + n, :] = in[pl, i, :, :]
+template <typename W>
+__device__ __forceinline__ void copy_row(const char* in, int64_t row, int64_t row_bytes, int n, int halo,
+                                         int64_t cell_bytes, char* out) {
+  const int m = n + 2 * halo;
+  const int64_t pl = row / n;
+  const int i = (int)(row % n);
+  const W* s = reinterpret_cast<const W*>(in + row * row_bytes);
+  W* d = reinterpret_cast<W*>(out + ((pl * m + halo + i) * m + halo) * cell_bytes);
+  const int64_t words = row_bytes / (int64_t)sizeof(W);
+  for (int64_t x = threadIdx.x; x < words; x += blockDim.x) d[x] = s[x];
+}
+
+// One launch for the whole padding.  Blocks [0, halo_blocks) take one halo
+// cell per thread (geometry-bound); the following blocks copy one interior
+// row each (bandwidth-bound), so the two kinds of work overlap on the chip.
+// `group` is the channel access width of the halo gathers (4, 2 or 1
+// elements) and `word` the byte width of the interior copy (16, 8, 4 or 2),
+// both chosen by the host from the layout and the base addresses.
+template <typename T>
+__global__ __launch_bounds__(256) void duo_pad_kernel(const T* __restrict__ in, int P, int n, int C, int halo,
+                                                      int group, int word, int64_t halo_blocks,
+                                                      T* __restrict__ out) {
+  const int m = n + 2 * halo;
+  if ((int64_t)blockIdx.x >= halo_blocks) {
+    const int64_t row = (int64_t)blockIdx.x - halo_blocks;
+    const int64_t cell = (int64_t)C * sizeof(T), row_bytes = (int64_t)n * cell;
+    const char* src = reinterpret_cast<const char*>(in);
+    char* dst = reinterpret_cast<char*>(out);
+    if (word == 16)
+      copy_row<uint4>(src, row, row_bytes, n, halo, cell, dst);
+    else if (word == 8)
+      copy_row<uint2>(src, row, row_bytes, n, halo, cell, dst);
+    else if (word == 4)
+      copy_row<uint32_t>(src, row, row_bytes, n, halo, cell, dst);
+    else
+      copy_row<uint16_t>(src, row, row_bytes, n, halo, cell, dst);
+    return;
+  }
   const int64_t per_face = (int64_t)m * m - (int64_t)n * n;
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= 6 * per_face) return;
   const int f = (int)(idx / per_face);
-  const int64_t hc = idx % per_face;
-  int ip, jp;  // padded cell of the halo: top band, bottom band, then left/right strips
-  const int64_t band = (int64_t)halo * m;
-  if (hc < band) {
-    ip = (int)(hc / m);
-    jp = (int)(hc % m);
-  } else if (hc < 2 * band) {
-    const int64_t r = hc - band;
-    ip = n + halo + (int)(r / m);
-    jp = (int)(r % m);
-  } else {
-    const int64_t r = hc - 2 * band;
-    ip = halo + (int)(r / (2 * halo));
-    const int k = (int)(r % (2 * halo));
-    jp = k < halo ? k : n + k;
-  }
+  int ip, jp;
+  halo_cell_position(idx % per_face, n, halo, &ip, &jp);
   int fp, rows[4], cols[4];
   double w[4];
   halo_neighbours(f, ip - halo, jp - halo, n, &fp, rows, cols, w);
@@ -153,38 +291,107 @@ __global__ void duo_halo_kernel(const T* __restrict__ in, int P, int n, int C, i
   T* dst = out + (int64_t)f * P * plane_out + ((int64_t)ip * m + jp) * C;
   int64_t off[4];
   for (int k = 0; k < 4; ++k) off[k] = ((int64_t)rows[k] * n + cols[k]) * C;
+  if (group == 4)
+    gather_cell<T, 4>(src, off, w, P, C, plane_in, plane_out, dst);
+  else if (group == 2)
+    gather_cell<T, 2>(src, off, w, P, C, plane_in, plane_out, dst);
+  else
+    gather_cell<T, 1>(src, off, w, P, C, plane_in, plane_out, dst);
+}
+
+// ---- the padding operator as a plan --------------------------------------
+// The neighbours and weights depend only on (n, halo): built once, the
+// operator is then applied as a bandwidth-bound gather.  One 64-byte entry per
+// halo cell, faces in order, cells of a face in the order top band, bottom
+// band, left/right strips (the halo enumeration above).
+struct alignas(16) DuoEntry {
+  double w[4];       // inverse-distance weights, nearest first, sum 1
+  int32_t cell[4];   // source cells r * n + c on `face`
+  int32_t face;
+  int32_t unused[3];
+};
+static_assert(sizeof(DuoEntry) == 64, "plan entry layout");
+
+// halo cell number of padded cell (ip, jp), inverse of the enumeration
+__device__ __forceinline__ int64_t halo_cell_number(int ip, int jp, int n, int halo) {
+  const int m = n + 2 * halo;
+  const int64_t band = (int64_t)halo * m;
+  if (ip < halo) return (int64_t)ip * m + jp;
+  if (ip >= n + halo) return band + (int64_t)(ip - n - halo) * m + jp;
+  return 2 * band + (int64_t)(ip - halo) * 2 * halo + (jp < halo ? jp : jp - n);
+}
+
+__global__ __launch_bounds__(256) void duo_plan_kernel(int n, int halo, DuoEntry* __restrict__ plan) {
+  const int m = n + 2 * halo;
+  const int64_t per_face = (int64_t)m * m - (int64_t)n * n;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= 6 * per_face) return;
+  const int f = (int)(idx / per_face);
+  int ip, jp;
+  halo_cell_position(idx % per_face, n, halo, &ip, &jp);
+  int fp, rows[4], cols[4];
+  double w[4];
+  halo_neighbours(f, ip - halo, jp - halo, n, &fp, rows, cols, w);
+  DuoEntry e;
+  for (int k = 0; k < 4; ++k) {
+    e.w[k] = w[k];
+    e.cell[k] = rows[k] * n + cols[k];
+  }
+  e.face = fp;
+  e.unused[0] = e.unused[1] = e.unused[2] = 0;
+  plan[idx] = e;
+}
+
+// the n interior cells of a padded row at every level, in W-byte words
+template <typename W>
+__device__ __forceinline__ void copy_span(const char* src, char* dst, int64_t bytes, int P, int64_t plane_in,
+                                          int64_t plane_out) {
+  const int64_t words = bytes / (int64_t)sizeof(W);
   for (int p = 0; p < P; ++p) {
-    const T* s = src + p * plane_in;
-    T* d = dst + p * plane_out;
-    for (int c = 0; c < C; ++c) {
-      if constexpr (sizeof(T) == 2) {
-        float acc = 0.f;
-        for (int k = 0; k < 4; ++k) acc = fmaf((float)w[k], bf16_to_f32(s[off[k] + c]), acc);
-        d[c] = f32_to_bf16(acc);
-      } else {
-        double acc = 0.0;
-        for (int k = 0; k < 4; ++k) acc = fma(w[k], (double)s[off[k] + c], acc);
-        d[c] = (float)acc;
-      }
-    }
+    const W* s = reinterpret_cast<const W*>(src + p * plane_in);
+    W* d = reinterpret_cast<W*>(dst + p * plane_out);
+    for (int64_t x = threadIdx.x; x < words; x += blockDim.x) d[x] = s[x];
   }
 }
 
-// interior: out[f, p, halo + i, halo + j, :] = in[f, p, i, j, :], one row of n*C
-// elements per (f, p, i), copied in 4-byte words when the layout allows, else
-// element by element
-template <typename W>
-__global__ void duo_interior_kernel(const char* __restrict__ in, int64_t rows, int64_t row_bytes, int n, int halo,
-                                    int64_t cell_bytes, char* __restrict__ out) {
-  const int64_t words = row_bytes / (int64_t)sizeof(W);
+// One block per padded row (f, ip), all P levels.  Halo cells are gathered
+// through the plan with the same weights and summation order as the
+// on-the-fly kernel (identical results), G channels per access; the interior
+// span of the row is copied in `word`-byte words.
+template <typename T, int G>
+__global__ __launch_bounds__(1024) void duo_apply_kernel(const T* __restrict__ in, const DuoEntry* __restrict__ plan,
+                                                        int P, int n, int C, int halo, int word,
+                                                        T* __restrict__ out) {
   const int m = n + 2 * halo;
-  for (int64_t row = blockIdx.x; row < rows; row += gridDim.x) {
-    const int64_t fp_ = row / n;  // (f, p) plane
-    const int i = (int)(row % n);
-    const W* s = reinterpret_cast<const W*>(in + row * row_bytes);
-    W* d = reinterpret_cast<W*>(out + ((fp_ * m + halo + i) * m + halo) * cell_bytes);
-    for (int64_t x = threadIdx.x; x < words; x += blockDim.x) d[x] = s[x];
+  const int f = blockIdx.x / m, ip = blockIdx.x % m;
+  const int groups = C / G;
+  const int64_t plane_in = (int64_t)n * n * C, plane_out = (int64_t)m * m * C;
+  const int64_t per_face = (int64_t)m * m - (int64_t)n * n;
+  const bool band = ip < halo || ip >= n + halo;
+  T* orow = out + (int64_t)f * P * plane_out + (int64_t)ip * m * C;
+  // halo cells of this row: all m in a band row, else the 2 halo strip cells
+  const int nh = band ? m : 2 * halo;
+  for (int t = threadIdx.x; t < nh * groups; t += blockDim.x) {
+    const int h = t / groups, c = (t - h * groups) * G;
+    const int jp = band ? h : (h < halo ? h : n + h);
+    const DuoEntry e = plan[(int64_t)f * per_face + halo_cell_number(ip, jp, n, halo)];
+    int64_t off[4];
+    for (int k = 0; k < 4; ++k) off[k] = (int64_t)e.cell[k] * C;
+    gather_group<T, G>(in + (int64_t)e.face * P * plane_in + c, off, e.w, P, plane_in, plane_out,
+                       orow + (int64_t)jp * C + c);
   }
+  if (band) return;
+  const char* src = reinterpret_cast<const char*>(in + (int64_t)f * P * plane_in + (int64_t)(ip - halo) * n * C);
+  char* dst = reinterpret_cast<char*>(orow + (int64_t)halo * C);
+  const int64_t bytes = (int64_t)n * C * sizeof(T), pin = plane_in * sizeof(T), pout = plane_out * sizeof(T);
+  if (word == 16)
+    copy_span<uint4>(src, dst, bytes, P, pin, pout);
+  else if (word == 8)
+    copy_span<uint2>(src, dst, bytes, P, pin, pout);
+  else if (word == 4)
+    copy_span<uint32_t>(src, dst, bytes, P, pin, pout);
+  else
+    copy_span<uint16_t>(src, dst, bytes, P, pin, pout);
 }
 
 }  // namespace
@@ -192,21 +399,66 @@ __global__ void duo_interior_kernel(const char* __restrict__ in, int64_t rows, i
 void launch_duo_pad(const void* in, int P, int n, int C, int halo, void* out, strata_dtype dt, hipStream_t s) {
   const int64_t es = dt == STRATA_BF16 ? 2 : 4;
   const int64_t cell = C * es, row_bytes = (int64_t)n * cell, rows = 6LL * P * n;
-  const unsigned blocks = (unsigned)(rows < 65536 ? rows : 65536);
-  if (row_bytes % 4 == 0 && (halo * cell) % 4 == 0 && (halo * 2 * cell) % 4 == 0)
-    hipLaunchKernelGGL((duo_interior_kernel<uint32_t>), dim3(blocks), dim3(256), 0, s,
-                       static_cast<const char*>(in), rows, row_bytes, n, halo, cell, static_cast<char*>(out));
-  else
-    hipLaunchKernelGGL((duo_interior_kernel<uint16_t>), dim3(blocks), dim3(256), 0, s,
-                       static_cast<const char*>(in), rows, row_bytes, n, halo, cell, static_cast<char*>(out));
   const int64_t m = n + 2 * halo, nh = 6 * (m * m - (int64_t)n * n);
-  const unsigned hb = (unsigned)((nh + 127) / 128);
+  const int64_t halo_blocks = (nh + 255) / 256;
+  const uintptr_t base = reinterpret_cast<uintptr_t>(in) | reinterpret_cast<uintptr_t>(out);
+  // widest copy word that divides every row start and length on both sides
+  const uint64_t align = (uint64_t)row_bytes | (uint64_t)(halo * cell) | (uint64_t)(2 * halo * cell) | base;
+  const int word = align % 16 == 0 ? 16 : align % 8 == 0 ? 8 : align % 4 == 0 ? 4 : 2;
+  // channel groups of 4, 2 or 1, as the channel count and base addresses allow
+  const int group = (C % 4 == 0 && base % (4 * es) == 0) ? 4 : (C % 2 == 0 && base % (2 * es) == 0) ? 2 : 1;
+  const dim3 grid((unsigned)(halo_blocks + rows));
   if (dt == STRATA_BF16)
-    hipLaunchKernelGGL((duo_halo_kernel<uint16_t>), dim3(hb), dim3(128), 0, s, static_cast<const uint16_t*>(in), P,
-                       n, C, halo, static_cast<uint16_t*>(out));
+    hipLaunchKernelGGL((duo_pad_kernel<uint16_t>), grid, dim3(256), 0, s, static_cast<const uint16_t*>(in), P, n, C,
+                       halo, group, word, halo_blocks, static_cast<uint16_t*>(out));
   else
-    hipLaunchKernelGGL((duo_halo_kernel<float>), dim3(hb), dim3(128), 0, s, static_cast<const float*>(in), P, n, C,
-                       halo, static_cast<float*>(out));
+    hipLaunchKernelGGL((duo_pad_kernel<float>), grid, dim3(256), 0, s, static_cast<const float*>(in), P, n, C, halo,
+                       group, word, halo_blocks, static_cast<float*>(out));
+}
+
+int64_t duo_plan_bytes(int n, int halo) {
+  const int64_t m = n + 2 * halo;
+  return 6 * (m * m - (int64_t)n * n) * (int64_t)sizeof(DuoEntry);
+}
+
+void launch_duo_plan(int n, int halo, void* plan, hipStream_t s) {
+  const int64_t m = n + 2 * halo, nh = 6 * (m * m - (int64_t)n * n);
+  hipLaunchKernelGGL(duo_plan_kernel, dim3((unsigned)((nh + 255) / 256)), dim3(256), 0, s, n, halo,
+                     static_cast<DuoEntry*>(plan));
+}
+
+void launch_duo_pad_planned(const void* in, const void* plan, int P, int n, int C, int halo, void* out,
+                            strata_dtype dt, hipStream_t s) {
+  const int64_t es = dt == STRATA_BF16 ? 2 : 4;
+  const uintptr_t base = reinterpret_cast<uintptr_t>(in) | reinterpret_cast<uintptr_t>(out);
+  const int group = (C % 4 == 0 && base % (4 * es) == 0) ? 4 : (C % 2 == 0 && base % (2 * es) == 0) ? 2 : 1;
+  // widest copy word dividing the interior span, its start in the padded row,
+  // both row strides, both plane strides and the base addresses
+  const int64_t cell = C * es, m = n + 2 * halo;
+  const uint64_t align = (uint64_t)(n * cell) | (uint64_t)(halo * cell) | (uint64_t)(m * cell) |
+                         (uint64_t)((int64_t)n * n * cell) | (uint64_t)(m * m * cell) | base;
+  const int word = align % 16 == 0 ? 16 : align % 8 == 0 ? 8 : align % 4 == 0 ? 4 : 2;
+  const dim3 grid((unsigned)(6 * m));
+  const DuoEntry* pl = static_cast<const DuoEntry*>(plan);
+#define STRATA_DUO_APPLY(T, GG)                                                                                   \
+  hipLaunchKernelGGL((duo_apply_kernel<T, GG>), grid, dim3(1024), 0, s, static_cast<const T*>(in), pl, P, n, C, \
+                     halo, word, static_cast<T*>(out))
+  if (dt == STRATA_BF16) {
+    if (group == 4)
+      STRATA_DUO_APPLY(uint16_t, 4);
+    else if (group == 2)
+      STRATA_DUO_APPLY(uint16_t, 2);
+    else
+      STRATA_DUO_APPLY(uint16_t, 1);
+  } else {
+    if (group == 4)
+      STRATA_DUO_APPLY(float, 4);
+    else if (group == 2)
+      STRATA_DUO_APPLY(float, 2);
+    else
+      STRATA_DUO_APPLY(float, 1);
+  }
+#undef STRATA_DUO_APPLY
 }
 
 }  // namespace strata

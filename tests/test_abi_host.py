@@ -197,3 +197,25 @@ def test_duo_rules():
     assert L.strata_duo_pad(p, 1, 8, 1, 1, p, B.STRATA_F32, None) == B.STRATA_ERR_INVALID_ARG     # n < 16
     assert L.strata_duo_pad(p, 1, 32, 1, 9, p, B.STRATA_F32, None) == B.STRATA_ERR_INVALID_ARG    # halo > n/4
     assert L.strata_duo_pad(p, 1, 32, 1, 0, p, B.STRATA_F32, None) == B.STRATA_ERR_INVALID_ARG
+    # within the element limit, but more interior rows than one launch can take
+    assert L.strata_duo_pad(p, 1 << 27, 16, 1, 4, p, B.STRATA_F32, None) == B.STRATA_ERR_INVALID_ARG
+
+
+def test_duo_plan_rules():
+    L = B.load()
+    p = fake()
+    # one 64-byte entry per halo cell of the six faces
+    assert B.strata_duo_plan_bytes(16, 4) == 6 * (24 * 24 - 16 * 16) * 64
+    assert B.strata_duo_plan_bytes(2048, 16) == 6 * (2080 * 2080 - 2048 * 2048) * 64
+    assert B.strata_duo_plan_bytes(8, 1) == 0 and B.strata_duo_plan_bytes(32, 9) == 0
+    need = B.strata_duo_plan_bytes(32, 4)
+    assert L.strata_duo_plan(32, 4, p, need - 1, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_duo_plan(32, 4, None, need, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_duo_plan(32, 4, fake(0x10008), need, None) == B.STRATA_ERR_INVALID_ARG  # misaligned
+    assert L.strata_duo_plan(32, 9, p, need, None) == B.STRATA_ERR_INVALID_ARG
+    F = B.STRATA_F32
+    assert L.strata_duo_pad_planned(p, 1, 32, 1, 4, p, need - 1, p, F, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_duo_pad_planned(p, 1, 32, 1, 4, None, need, p, F, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_duo_pad_planned(p, 1, 32, 1, 4, fake(0x10004), need, p, F, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_duo_pad_planned(p, 0, 32, 1, 4, p, need, p, F, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_duo_pad_planned(p, 1, 32, 1, 4, p, need, p, 7, None) == B.STRATA_ERR_INVALID_ARG

@@ -98,7 +98,7 @@ def test_kbd_window_blends_a_constant_field_exactly():
 # ----------------------------------------------------------------------------- Duo-grid padding
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("n,halo,P,C", [(16, 4, 2, 3), (32, 8, 1, 8), (20, 3, 1, 2)])
+@pytest.mark.parametrize("n,halo,P,C", [(16, 4, 2, 3), (32, 8, 1, 8), (20, 3, 1, 2), (17, 3, 1, 1)])
 def test_duo_pad_matches_oracle(dtype, n, halo, P, C):
     f = I.gaussian((6, P, n, n, C), 95 + n, 0, dtype)
     fd = dev_tensor(f, dtype)
@@ -153,3 +153,72 @@ def test_duo_pad_full_size_sampled(dtype):
         got = out[f, :, ip, jp].float().cpu().numpy().astype(np.float64)
         bound = bf16_half_ulp(ref) + 2.0 ** -20 * 4 * float(np.max(np.abs(vals)))
         assert float(np.max(np.abs(got - ref) - bound)) <= 0.0, (f, ip, jp)
+
+
+def _halo_cells(n, halo):
+    """Halo cells (ip, jp) of a padded face in plan order: top band, bottom band,
+    then the left/right strips row by row."""
+    m = n + 2 * halo
+    top = [(ip, jp) for ip in range(halo) for jp in range(m)]
+    bottom = [(ip, jp) for ip in range(n + halo, m) for jp in range(m)]
+    strips = [(ip, jp) for ip in range(halo, n + halo) for jp in list(range(halo)) + list(range(n + halo, m))]
+    return top + bottom + strips
+
+
+@pytest.mark.parametrize("n,halo", [(16, 4), (20, 3), (17, 3)])
+def test_duo_plan_entries_match_oracle(n, halo):
+    # plan entries (64 bytes: float64 weights[4], int32 cells[4], int32 face):
+    # face and cells exact, weights to float64 rounding
+    nb = B.strata_duo_plan_bytes(n, halo)
+    plan = torch.empty(nb, dtype=torch.uint8, device="cuda")
+    B.strata_duo_plan(n, halo, plan)
+    torch.cuda.synchronize()
+    raw = plan.cpu().numpy()
+    ent = np.dtype([("w", "<f8", 4), ("cell", "<i4", 4), ("face", "<i4"), ("unused", "<i4", 3)])
+    e = raw.view(ent)
+    cells = _halo_cells(n, halo)
+    assert len(e) == 6 * len(cells)
+    for f in range(6):
+        for h, (ip, jp) in enumerate(cells):
+            fp, rows, cols, w = G.duo_halo_neighbours(f, ip - halo, jp - halo, n)
+            x = e[f * len(cells) + h]
+            assert int(x["face"]) == fp, (f, ip, jp)
+            assert np.array_equal(x["cell"], rows * n + cols), (f, ip, jp)
+            np.testing.assert_allclose(x["w"], w, rtol=0, atol=1e-13)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("n,halo,P,C", [(16, 4, 2, 3), (32, 8, 1, 8), (17, 3, 3, 1), (20, 3, 2, 2)])
+def test_duo_planned_equals_one_shot(dtype, n, halo, P, C):
+    # the plan gives the same weights and summation order: identical bits; one
+    # plan serves fields of any level and channel count
+    nb = B.strata_duo_plan_bytes(n, halo)
+    plan = torch.empty(nb, dtype=torch.uint8, device="cuda")
+    B.strata_duo_plan(n, halo, plan)
+    m = n + 2 * halo
+    for PP, CC in ((P, C), (1, 2 * C)):
+        f = I.gaussian((6, PP, n, n, CC), 131 + n + CC, 0, dtype)
+        fd = dev_tensor(f, dtype)
+        a = torch.empty((6, PP, m, m, CC), dtype=fd.dtype, device="cuda")
+        b = torch.full_like(a, float("nan"))
+        B.strata_duo_pad(fd, halo, a)
+        B.strata_duo_pad_planned(fd, halo, plan, b)
+        torch.cuda.synchronize()
+        assert torch.equal(a.view(torch.int16) if dtype == "bf16" else a.view(torch.int32),
+                           b.view(torch.int16) if dtype == "bf16" else b.view(torch.int32))
+
+
+def test_duo_planned_full_size_equals_one_shot():
+    n, h, P, C = 2048, 16, 8, 4
+    m = n + 2 * h
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(1011)
+    fd = torch.randn((6, P, n, n, C), generator=gen, device="cuda").to(torch.bfloat16)
+    plan = torch.empty(B.strata_duo_plan_bytes(n, h), dtype=torch.uint8, device="cuda")
+    B.strata_duo_plan(n, h, plan)
+    a = torch.empty((6, P, m, m, C), dtype=torch.bfloat16, device="cuda")
+    b = torch.empty_like(a)
+    B.strata_duo_pad(fd, h, a)
+    B.strata_duo_pad_planned(fd, h, plan, b)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))

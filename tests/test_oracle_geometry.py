@@ -236,7 +236,7 @@ def test_duo_nearest_cells_lie_in_the_lattice_block_around_the_point():
     # the four nearest cells of the containing face always lie within the 6 x 6
     # block of its cell lattice around the point's (clamped) floor index: a
     # local search finds them
-    for n, h in ((16, 4), (20, 3), (32, 8), (48, 6)):
+    for n, h in ((16, 4), (17, 3), (20, 3), (32, 8), (48, 6)):
         for f in range(6):
             for i in range(-h, n + h):
                 for j in range(-h, n + h):
