@@ -265,3 +265,25 @@ def duo_pad(field, halo: int) -> np.ndarray:
                     acc = acc + w[k] * field[fp, :, rows[k], cols[k]]
                 out[f, :, ip, jp] = acc
     return out
+
+
+def duo_pad_vjp(grad_padded, halo: int) -> np.ndarray:
+    """Adjoint of the padding (the vector-Jacobian product of ``duo_pad``; App. F:
+    P is a fixed sparse matrix, so gradients reach the faces through its
+    transpose).  grad_padded [6, P, n + 2h, n + 2h, C] -> [6, P, n, n, C]: each
+    face's interior gradient, plus, for every halo cell, its gradient times each
+    of its 4 weights added to the source cell that weight belongs to."""
+    g = np.asarray(grad_padded, dtype=np.float64)
+    _, P, m, _, C = g.shape
+    n = m - 2 * halo
+    out = g[:, :, halo:halo + n, halo:halo + n].copy()
+    for f in range(6):
+        for ip in range(m):
+            for jp in range(m):
+                i, j = ip - halo, jp - halo
+                if 0 <= i < n and 0 <= j < n:
+                    continue
+                fp, rows, cols, w = duo_halo_neighbours(f, i, j, n)
+                for k in range(4):
+                    out[fp, :, rows[k], cols[k]] += w[k] * g[f, :, ip, jp]
+    return out

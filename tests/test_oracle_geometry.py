@@ -282,3 +282,32 @@ def test_duo_pad_continues_a_smooth_field():
         Ip, Jp = np.meshgrid(np.arange(m) - h, np.arange(m) - h, indexing="ij")
         exact = G.cell_point(np.full(Ip.shape, f), Ip, Jp, n) @ g
         assert np.max(np.abs(out[f, 0, :, :, 0] - exact)) <= 2.0 * step * np.linalg.norm(g)
+
+
+def test_duo_pad_vjp_is_the_adjoint_of_the_padding():
+    # <P x, y> = <x, P^T y> for arbitrary x, y: a dropped term, a wrong weight
+    # or a misplaced source cell breaks the identity
+    rng = np.random.default_rng(5)
+    n, h, P, C = 16, 4, 2, 3
+    m = n + 2 * h
+    x = rng.standard_normal((6, P, n, n, C))
+    y = rng.standard_normal((6, P, m, m, C))
+    lhs = float(np.sum(G.duo_pad(x, h) * y))
+    rhs = float(np.sum(x * G.duo_pad_vjp(y, h)))
+    assert abs(lhs - rhs) <= 1e-12 * (abs(lhs) + np.sum(np.abs(x)) * 1.0)
+
+
+def test_duo_pad_vjp_conserves_the_total_and_copies_the_interior():
+    n, h, P, C = 20, 3, 1, 2
+    m = n + 2 * h
+    # every halo cell's weights sum to 1: the total of P^T 1 counts every padded cell once
+    ones = G.duo_pad_vjp(np.ones((6, P, m, m, C)), h)
+    assert np.isclose(ones.sum(), 6 * P * C * m * m, rtol=1e-13)
+    # no halo gradient: the interior is returned unchanged
+    rng = np.random.default_rng(6)
+    g = np.zeros((6, P, m, m, C))
+    g[:, :, h:h + n, h:h + n] = rng.standard_normal((6, P, n, n, C))
+    assert np.array_equal(G.duo_pad_vjp(g, h), g[:, :, h:h + n, h:h + n])
+    # cells far from every edge receive no halo gradient
+    inner = ones[:, :, h + 3:n - h - 3, h + 3:n - h - 3]
+    assert np.array_equal(inner, np.ones_like(inner))
