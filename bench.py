@@ -389,11 +389,14 @@ def duo_padding(steps: int) -> dict:
     plan_ms = _timed(lambda: Bd.strata_duo_plan(n, h, plan), max(steps, 3))
     ms = _timed(lambda: Bd.strata_duo_pad_planned(faces, h, plan, padded), steps)
     one_shot_ms = _timed(lambda: Bd.strata_duo_pad(faces, h, padded), steps)
+    # the adjoint: padded-shape gradient in, face-shape gradient out (same bytes)
+    vjp_ms = _timed(lambda: Bd.strata_duo_pad_vjp(padded, h, plan, faces), steps)
     nbytes = (faces.numel() + padded.numel()) * 2
     del faces, padded, plan
     return {"workload": "duo_pad_6x8x2048x2048x4_halo16_bf16", "ms": round(ms, 4), "bound": "hbm",
             "achieved_gbs": round(nbytes / ms / 1e6, 1), "frac_hbm": round(nbytes / ms / 1e6 / PEAK_HBM_GBS, 4),
             "plan_build_ms": round(plan_ms, 4), "one_shot_ms": round(one_shot_ms, 4),
+            "vjp_ms": round(vjp_ms, 4), "vjp_frac_hbm": round(nbytes / vjp_ms / 1e6 / PEAK_HBM_GBS, 4),
             "alg_bytes": nbytes}
 
 

@@ -233,22 +233,36 @@ strata_status strata_duo_pad(const void* faces, int32_t P, int32_t n, int32_t C,
 
 /* The same padding operator P built once and applied many times (App. F: P is a
  * fixed sparse matrix with 4 non-zeros per halo cell, so a model that pads
- * every layer of a rollout reuses it).
+ * every layer of a rollout reuses it), and its transpose for gradients.
  *
  * strata_duo_plan_bytes: size of the plan for (n, halo), 0 if the pair is
- * invalid.  strata_duo_plan: writes the plan (geometry only, no field data)
- * into `plan`, caller-owned device memory of at least that many bytes, 16-byte
- * aligned; its contents are opaque and valid for this (n, halo) only.
+ * invalid or too large (n + 2 halo < 2^14, 4 entries per halo cell below
+ * 2^31).  strata_duo_plan: writes the plan (geometry only, no field
+ * data: P and its transpose) into `plan`, caller-owned device memory of at
+ * least that many bytes, 16-byte aligned; its contents are opaque and valid
+ * for this (n, halo) only.  The build is deterministic.
  * strata_duo_pad_planned: as strata_duo_pad, with the neighbours and weights
  * read from a plan written by strata_duo_plan for the same (n, halo); results
- * are identical to strata_duo_pad's.  Errors: STRATA_ERR_INVALID_ARG for the
- * rules of strata_duo_pad, a NULL or misaligned plan, or plan_bytes below
- * strata_duo_plan_bytes(n, halo); nothing is launched then. */
+ * are identical to strata_duo_pad's.
+ * strata_duo_pad_vjp: the adjoint, grad_faces = P^T grad_padded
+ * (grad_padded: [6, P, n + 2 halo, n + 2 halo, C], grad_faces: [6, P, n, n,
+ * C], both of dtype, not overlapping): every face cell's interior gradient
+ * plus, for each halo cell whose 4 neighbours include it, that halo cell's
+ * gradient times the weight, summed in ascending padded-cell order (face,
+ * row, column) after the interior term, with fused multiply-adds; float32
+ * sums for bf16 data, float64 for float32 data; one rounding.  Deterministic.
+ * P <= 65535.
+ * Errors: STRATA_ERR_INVALID_ARG for the rules of strata_duo_pad, a NULL or
+ * misaligned plan, or plan_bytes below strata_duo_plan_bytes(n, halo); nothing
+ * is launched then. */
 size_t strata_duo_plan_bytes(int32_t n, int32_t halo);
 strata_status strata_duo_plan(int32_t n, int32_t halo, void* plan, size_t plan_bytes, void* stream);
 strata_status strata_duo_pad_planned(const void* faces, int32_t P, int32_t n, int32_t C, int32_t halo,
                                      const void* plan, size_t plan_bytes, void* padded, strata_dtype dtype,
                                      void* stream);
+strata_status strata_duo_pad_vjp(const void* grad_padded, int32_t P, int32_t n, int32_t C, int32_t halo,
+                                 const void* plan, size_t plan_bytes, void* grad_faces, strata_dtype dtype,
+                                 void* stream);
 
 /* ---- a8: Kaiser-Bessel-derived blend window (App. F, "Tile stitching") -----
  * window[y * Wt + x] = w(y, Ht) * w(x, Wt) (float32 [Ht * Wt], device) with,

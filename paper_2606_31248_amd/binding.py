@@ -27,6 +27,7 @@ EXPORTS = (
     "strata_na3d_fwd_ex", "strata_na3d_bwd_ex_workspace_size", "strata_na3d_bwd_ex",
     "strata_tile_blend", "strata_tile_extract", "strata_na_axis_index", "strata_wind_tile_frame", "strata_kbd_window",
     "strata_duo_pad", "strata_duo_plan_bytes", "strata_duo_plan", "strata_duo_pad_planned",
+    "strata_duo_pad_vjp",
     "strata_status_string", "strata_last_error",
 )
 
@@ -77,6 +78,7 @@ def load(path: str = LIB_PATH):
         "strata_duo_pad": [P, i32, i32, i32, i32, P, st, P],
         "strata_duo_plan": [i32, i32, P, ctypes.c_size_t, P],
         "strata_duo_pad_planned": [P, i32, i32, i32, i32, P, ctypes.c_size_t, P, st, P],
+        "strata_duo_pad_vjp": [P, i32, i32, i32, i32, P, ctypes.c_size_t, P, st, P],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -269,3 +271,13 @@ def strata_duo_pad_planned(faces, halo, plan, padded, stream=None):
     _check(load().strata_duo_pad_planned(_ptr(faces), P, n, C, int(halo), _ptr(plan),
                                          plan.numel() * plan.element_size(), _ptr(padded), _dtype(faces),
                                          _stream(stream)))
+
+
+def strata_duo_pad_vjp(grad_padded, halo, plan, grad_faces, stream=None):
+    """grad_faces = P^T grad_padded: grad_padded [6, P, n + 2 halo, n + 2 halo, C] ->
+    grad_faces [6, P, n, n, C], through a plan built for (n, halo)."""
+    _, P, m, _, C = grad_padded.shape
+    n = m - 2 * int(halo)
+    _check(load().strata_duo_pad_vjp(_ptr(grad_padded), P, n, C, int(halo), _ptr(plan),
+                                     plan.numel() * plan.element_size(), _ptr(grad_faces), _dtype(grad_padded),
+                                     _stream(stream)))

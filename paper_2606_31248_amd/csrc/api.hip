@@ -370,14 +370,22 @@ strata_status strata_duo_pad(const void* faces, int32_t P, int32_t n, int32_t C,
   return check_launch("strata_duo_pad");
 }
 
+// the plan packs a cell of a (padded) face in 28 bits and counts transposed
+// entries with int32
+static bool duo_plan_fits(int32_t n, int32_t halo) {
+  const int64_t m = (int64_t)n + 2 * halo;
+  return m < (1 << 14) && 4 * 6 * (m * m - (int64_t)n * n) < INT32_MAX;
+}
+
 size_t strata_duo_plan_bytes(int32_t n, int32_t halo) {
-  if (n < 16 || halo < 1 || halo > n / 4) return 0;
+  if (n < 16 || halo < 1 || halo > n / 4 || !duo_plan_fits(n, halo)) return 0;
   return (size_t)duo_plan_bytes(n, halo);
 }
 
 strata_status strata_duo_plan(int32_t n, int32_t halo, void* plan, size_t plan_bytes, void* stream) {
   REQUIRE(n >= 16 && halo > 0 && halo <= n / 4, "duo plan: need n >= 16 and 1 <= halo <= n/4 (n=%d, halo=%d)", n,
           halo);
+  REQUIRE(duo_plan_fits(n, halo), "duo plan: n=%d too large for a plan", n);
   REQUIRE_PTR(plan);
   REQUIRE(reinterpret_cast<uintptr_t>(plan) % 16 == 0, "duo plan: plan must be 16-byte aligned");
   REQUIRE(plan_bytes >= (size_t)duo_plan_bytes(n, halo), "duo plan: plan_bytes %zu < %lld", plan_bytes,
@@ -402,6 +410,26 @@ strata_status strata_duo_pad_planned(const void* faces, int32_t P, int32_t n, in
           plan_bytes, (long long)duo_plan_bytes(n, halo));
   launch_duo_pad_planned(faces, plan, P, n, C, halo, padded, dtype, (hipStream_t)stream);
   return check_launch("strata_duo_pad_planned");
+}
+
+strata_status strata_duo_pad_vjp(const void* grad_padded, int32_t P, int32_t n, int32_t C, int32_t halo,
+                                 const void* plan, size_t plan_bytes, void* grad_faces, strata_dtype dtype,
+                                 void* stream) {
+  REQUIRE(P > 0 && C > 0 && P <= 65535, "duo vjp: need 0 < P <= 65535 and C > 0 (P=%d, C=%d)", P, C);
+  REQUIRE(n >= 16 && halo > 0 && halo <= n / 4, "duo vjp: need n >= 16 and 1 <= halo <= n/4 (n=%d, halo=%d)", n,
+          halo);
+  REQUIRE(dtype == STRATA_F32 || dtype == STRATA_BF16, "duo vjp: unknown dtype %d", (int)dtype);
+  REQUIRE(duo_plan_fits(n, halo), "duo vjp: n=%d too large for a plan", n);
+  const int64_t m = (int64_t)n + 2 * halo;
+  REQUIRE(6LL * P * m * m * C < kMaxElems, "duo vjp: tensor too large");
+  REQUIRE_PTR(grad_padded);
+  REQUIRE_PTR(grad_faces);
+  REQUIRE_PTR(plan);
+  REQUIRE(reinterpret_cast<uintptr_t>(plan) % 16 == 0, "duo vjp: plan must be 16-byte aligned");
+  REQUIRE(plan_bytes >= (size_t)duo_plan_bytes(n, halo), "duo vjp: plan_bytes %zu < %lld (a plan for other n, halo?)",
+          plan_bytes, (long long)duo_plan_bytes(n, halo));
+  launch_duo_pad_vjp(grad_padded, plan, P, n, C, halo, grad_faces, dtype, (hipStream_t)stream);
+  return check_launch("strata_duo_pad_vjp");
 }
 
 strata_status strata_kbd_window(int32_t Ht, int32_t Wt, int32_t overlap, double beta, float* window,

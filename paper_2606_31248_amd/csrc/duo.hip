@@ -375,6 +375,10 @@ __global__ __launch_bounds__(1024) void duo_apply_kernel(const T* __restrict__ i
     const int h = t / groups, c = (t - h * groups) * G;
     const int jp = band ? h : (h < halo ? h : n + h);
     const DuoEntry e = plan[(int64_t)f * per_face + halo_cell_number(ip, jp, n, halo)];
+    // entries of a plan for other (n, halo) could point anywhere: skip them
+    if (e.face < 0 || e.face > 5 || (e.cell[0] | e.cell[1] | e.cell[2] | e.cell[3]) < 0 ||
+        max(max(e.cell[0], e.cell[1]), max(e.cell[2], e.cell[3])) >= n * n)
+      continue;
     int64_t off[4];
     for (int k = 0; k < 4; ++k) off[k] = (int64_t)e.cell[k] * C;
     gather_group<T, G>(in + (int64_t)e.face * P * plane_in + c, off, e.w, P, plane_in, plane_out,
@@ -392,6 +396,285 @@ __global__ __launch_bounds__(1024) void duo_apply_kernel(const T* __restrict__ i
     copy_span<uint32_t>(src, dst, bytes, P, pin, pout);
   else
     copy_span<uint16_t>(src, dst, bytes, P, pin, pout);
+}
+
+// ---- the adjoint P^T -------------------------------------------------------
+// Transposed entries, grouped by source cell and, within a source cell, in
+// ascending padded-cell order (face, row, column), so every gradient sums in
+// one fixed order.  Cells are packed as face << 28 | cell within the face (the
+// plan requires n + 2 halo < 2^14).
+struct alignas(16) DuoTEntry {
+  int32_t src;   // source cell: f << 28 | r * n + c
+  int32_t halo;  // halo cell of the padded faces: f << 28 | ip * m + jp
+  double w;
+};
+constexpr int kFaceShift = 28;
+constexpr int32_t kCellMask = (1 << kFaceShift) - 1;
+static_assert(sizeof(DuoTEntry) == 16, "transposed entry layout");
+
+// byte offsets of the plan's sections
+struct PlanLayout {
+  int64_t fwd, tent, cursor, sums, rank, hsums, heads, nheads, total;
+};
+
+__host__ __device__ inline int64_t align16(int64_t x) { return (x + 15) & ~(int64_t)15; }
+
+inline PlanLayout plan_layout(int n, int halo) {
+  const int64_t m = n + 2 * halo, nh = 6 * (m * m - (int64_t)n * n), cells = 6LL * n * n;
+  PlanLayout L;
+  L.fwd = 0;
+  L.tent = align16(L.fwd + nh * (int64_t)sizeof(DuoEntry));
+  L.cursor = align16(L.tent + 4 * nh * (int64_t)sizeof(DuoTEntry));
+  L.sums = align16(L.cursor + cells * 4);
+  L.rank = align16(L.sums + (cells + 1023) / 1024 * 4);  // segment-start flags, then their ranks
+  L.hsums = align16(L.rank + 4 * nh * 4);
+  L.heads = align16(L.hsums + (4 * nh + 1023) / 1024 * 4);  // first entry of each source cell
+  L.nheads = align16(L.heads + 4 * nh * 4);
+  L.total = align16(L.nheads + 4);
+  return L;
+}
+
+__global__ __launch_bounds__(256) void zero_i32_kernel(int32_t* __restrict__ x, int64_t count) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += (int64_t)gridDim.x * blockDim.x)
+    x[i] = 0;
+}
+
+// entries per source cell (integer atomics: the counts are exact)
+__global__ __launch_bounds__(256) void duo_count_kernel(const DuoEntry* __restrict__ plan, int64_t nh, int n,
+                                                        int32_t* __restrict__ cursor) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= 4 * nh) return;
+  const DuoEntry& e = plan[t >> 2];
+  atomicAdd(&cursor[(int64_t)e.face * n * n + e.cell[t & 3]], 1);
+}
+
+// inclusive scan of one value per lane over a 64-lane wave
+__device__ __forceinline__ int32_t wave_inclusive_scan(int32_t v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int32_t u = __shfl_up(v, d, 64);
+    if (lane >= d) v += u;
+  }
+  return v;
+}
+
+// exclusive scan, pass 1: each block of 256 threads scans 1024 values in place
+// and records its total
+__global__ __launch_bounds__(256) void scan_blocks_kernel(int32_t* __restrict__ x, int64_t count,
+                                                          int32_t* __restrict__ sums) {
+  __shared__ int32_t wave_tot[4];
+  const int64_t base = (int64_t)blockIdx.x * 1024 + threadIdx.x * 4;
+  int32_t v[4], t = 0;
+  for (int k = 0; k < 4; ++k) {
+    v[k] = base + k < count ? x[base + k] : 0;
+    t += v[k];
+  }
+  const int32_t inc = wave_inclusive_scan(t);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 63) wave_tot[w] = inc;
+  __syncthreads();
+  int32_t before = inc - t;
+  for (int k = 0; k < w; ++k) before += wave_tot[k];
+  for (int k = 0; k < 4; ++k) {
+    if (base + k < count) x[base + k] = before;
+    before += v[k];
+  }
+  if (threadIdx.x == 255) sums[blockIdx.x] = before;
+}
+
+// pass 2 (one block of 1024 threads): exclusive scan of the block totals
+__global__ __launch_bounds__(1024) void scan_sums_kernel(int32_t* __restrict__ sums, int64_t nb) {
+  __shared__ int32_t wave_tot[16];
+  __shared__ int32_t carry_s;
+  if (threadIdx.x == 0) carry_s = 0;
+  __syncthreads();
+  for (int64_t c0 = 0; c0 < nb; c0 += 1024) {
+    const int64_t i = c0 + threadIdx.x;
+    const int32_t v = i < nb ? sums[i] : 0;
+    const int32_t inc = wave_inclusive_scan(v);
+    const int w = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 63) wave_tot[w] = inc;
+    __syncthreads();
+    int32_t before = carry_s + inc - v;
+    for (int k = 0; k < w; ++k) before += wave_tot[k];
+    if (i < nb) sums[i] = before;
+    __syncthreads();
+    if (threadIdx.x == 1023) carry_s = before + v;
+    __syncthreads();
+  }
+}
+
+// pass 3: add each block's offset
+__global__ __launch_bounds__(256) void scan_add_kernel(int32_t* __restrict__ x, int64_t count,
+                                                       const int32_t* __restrict__ sums) {
+  const int64_t base = (int64_t)blockIdx.x * 1024;
+  const int32_t add = sums[blockIdx.x];
+  for (int k = threadIdx.x; k < 1024; k += 256)
+    if (base + k < count) x[base + k] += add;
+}
+
+// place every (halo cell, k) entry in its source cell's segment
+__global__ __launch_bounds__(256) void duo_fill_kernel(const DuoEntry* __restrict__ plan, int64_t nh, int n, int halo,
+                                                       int32_t* __restrict__ cursor, DuoTEntry* __restrict__ tent) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= 4 * nh) return;
+  const DuoEntry& e = plan[t >> 2];
+  const int32_t pos = atomicAdd(&cursor[(int64_t)e.face * n * n + e.cell[t & 3]], 1);
+  if (pos < 0 || pos >= 4 * nh) return;  // cannot happen with a correct scan; keeps every store in bounds
+  const int m = n + 2 * halo;
+  const int64_t per_face = (int64_t)m * m - (int64_t)n * n;
+  const int hf = (int)((t >> 2) / per_face);
+  int ip, jp;
+  halo_cell_position((t >> 2) - (int64_t)hf * per_face, n, halo, &ip, &jp);
+  DuoTEntry o;
+  o.src = (e.face << kFaceShift) | e.cell[t & 3];
+  o.halo = (hf << kFaceShift) | (ip * m + jp);
+  o.w = e.w[t & 3];
+  tent[pos] = o;
+}
+
+// the segment starting at pos, if pos starts one: [pos, end)
+__device__ __forceinline__ bool segment_at(const DuoTEntry* tent, int64_t total, int64_t pos, int64_t* end) {
+  const int32_t src = tent[pos].src;
+  if (pos > 0 && tent[pos - 1].src == src) return false;
+  int64_t e = pos + 1;
+  while (e < total && tent[e].src == src) ++e;
+  *end = e;
+  return true;
+}
+
+// order each segment by padded cell (segments are short: insertion sort;
+// other threads only read the src fields, which a sort within a segment keeps)
+__global__ __launch_bounds__(256) void duo_sort_kernel(DuoTEntry* __restrict__ tent, int64_t total) {
+  const int64_t pos = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (pos >= total) return;
+  int64_t end;
+  if (!segment_at(tent, total, pos, &end)) return;
+  for (int64_t a = pos + 1; a < end; ++a) {
+    const DuoTEntry x = tent[a];
+    int64_t b = a;
+    while (b > pos && tent[b - 1].halo > x.halo) {
+      tent[b] = tent[b - 1];
+      --b;
+    }
+    tent[b] = x;
+  }
+}
+
+// 1 where an entry starts its source cell's segment
+__global__ __launch_bounds__(256) void duo_head_flag_kernel(const DuoTEntry* __restrict__ tent, int64_t total,
+                                                            int32_t* __restrict__ flag) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= total) return;
+  flag[t] = (t == 0 || tent[t - 1].src != tent[t].src) ? 1 : 0;
+}
+
+// after the exclusive scan of the flags: the list of segment starts in
+// ascending order, and its length
+__global__ __launch_bounds__(256) void duo_head_list_kernel(const DuoTEntry* __restrict__ tent, int64_t total,
+                                                            const int32_t* __restrict__ rank,
+                                                            int32_t* __restrict__ heads,
+                                                            int32_t* __restrict__ nheads) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= total) return;
+  const bool head = t == 0 || tent[t - 1].src != tent[t].src;
+  if (head) heads[rank[t]] = (int32_t)t;
+  if (t == total - 1) *nheads = rank[t] + (head ? 1 : 0);
+}
+
+// P^T for one source cell with halo entries [pos, end), level p: its interior
+// gradient plus the weighted gradients of those halo cells, in segment order,
+// one rounding (float32 sums for bf16 data, float64 for float32 data).  The
+// entries are taken 8 at a time, all loads issued before the sums.
+template <typename T, int G>
+__device__ __forceinline__ void vjp_segment(const T* gpad, const DuoTEntry* tent, int64_t pos, int64_t end, int p,
+                                            int P, int n, int C, int halo, T* gfaces) {
+  const int m = n + 2 * halo;
+  const int64_t plane_in = (int64_t)n * n * C, plane_out = (int64_t)m * m * C;
+  const int32_t src = tent[pos].src;
+  const int f = src >> kFaceShift, cell = src & kCellMask;
+  if (f > 5 || cell >= n * n) return;  // only a plan for other (n, halo) holds such entries
+  const int r = cell / n, c = cell - r * n;
+  const T* gi = gpad + ((int64_t)f * P + p) * plane_out + ((int64_t)(halo + r) * m + (halo + c)) * C;
+  T* go = gfaces + ((int64_t)f * P + p) * plane_in + (int64_t)cell * C;
+  using Acc = decltype(widen(T{}));
+  for (int c0 = 0; c0 < C; c0 += G) {
+    const Group<T, G> own = *reinterpret_cast<const Group<T, G>*>(gi + c0);
+    Acc acc[G];
+    for (int e = 0; e < G; ++e) acc[e] = widen(own.v[e]);
+    for (int64_t q0 = pos; q0 < end; q0 += 8) {
+      DuoTEntry x[8];
+      Group<T, G> g[8];
+      bool ok[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        ok[u] = q0 + u < end;
+        if (ok[u]) x[u] = tent[q0 + u];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (!ok[u]) continue;
+        const int hf = x[u].halo >> kFaceShift, hcell = x[u].halo & kCellMask;
+        ok[u] = hf <= 5 && hcell < m * m;  // only a plan for other (n, halo) holds others
+        if (ok[u])
+          g[u] = *reinterpret_cast<const Group<T, G>*>(gpad + ((int64_t)hf * P + p) * plane_out +
+                                                       (int64_t)hcell * C + c0);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (!ok[u]) continue;
+        const Acc wv = (Acc)x[u].w;
+        for (int e = 0; e < G; ++e) acc[e] = fma(wv, widen(g[u].v[e]), acc[e]);
+      }
+    }
+    Group<T, G> o;
+    for (int e = 0; e < G; ++e) {
+      if constexpr (sizeof(T) == 2)
+        o.v[e] = f32_to_bf16(acc[e]);
+      else
+        o.v[e] = (float)acc[e];
+    }
+    *reinterpret_cast<Group<T, G>*>(go + c0) = o;
+  }
+}
+
+// P^T, interior part: one block per face row (f, i), all levels, the row's
+// interior span of the padded gradient copied in `word`-byte words
+__global__ __launch_bounds__(1024) void duo_crop_kernel(const char* __restrict__ gpad, int P, int n, int C, int es,
+                                                        int halo, int word, char* __restrict__ gfaces) {
+  const int m = n + 2 * halo;
+  const int f = blockIdx.x / n, i = blockIdx.x % n;
+  const int64_t cell = (int64_t)C * es;
+  const char* src = gpad + ((int64_t)f * P * m * m + (int64_t)(halo + i) * m + halo) * cell;
+  char* dst = gfaces + ((int64_t)f * P * n * n + (int64_t)i * n) * cell;
+  const int64_t bytes = n * cell, pin = (int64_t)m * m * cell, pout = (int64_t)n * n * cell;
+  if (word == 16)
+    copy_span<uint4>(src, dst, bytes, P, pin, pout);
+  else if (word == 8)
+    copy_span<uint2>(src, dst, bytes, P, pin, pout);
+  else if (word == 4)
+    copy_span<uint32_t>(src, dst, bytes, P, pin, pout);
+  else
+    copy_span<uint16_t>(src, dst, bytes, P, pin, pout);
+}
+
+// P^T, halo part (after the crop, on the same stream): one thread per (source
+// cell with halo entries, level), each rewriting that cell's gradient at that
+// level with the halo terms added
+template <typename T, int G>
+__global__ __launch_bounds__(256) void duo_vjp_halo_kernel(const T* __restrict__ gpad,
+                                                           const DuoTEntry* __restrict__ tent,
+                                                           const int32_t* __restrict__ heads,
+                                                           const int32_t* __restrict__ nheads, int64_t total, int P,
+                                                           int n, int C, int halo, T* __restrict__ gfaces) {
+  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int p = blockIdx.y;  // neighbouring lanes: neighbouring source cells of one level
+  const int64_t count = min((int64_t)*nheads, total);
+  if (k >= count) return;
+  const int64_t pos = heads[k], end = k + 1 < count ? (int64_t)heads[k + 1] : total;
+  if (pos < 0 || end > total || pos >= end) return;  // only a plan for other (n, halo) holds such entries
+  vjp_segment<T, G>(gpad, tent, pos, end, p, P, n, C, halo, gfaces);
 }
 
 }  // namespace
@@ -416,15 +699,76 @@ void launch_duo_pad(const void* in, int P, int n, int C, int halo, void* out, st
                        group, word, halo_blocks, static_cast<float*>(out));
 }
 
-int64_t duo_plan_bytes(int n, int halo) {
-  const int64_t m = n + 2 * halo;
-  return 6 * (m * m - (int64_t)n * n) * (int64_t)sizeof(DuoEntry);
-}
+int64_t duo_plan_bytes(int n, int halo) { return plan_layout(n, halo).total; }
 
 void launch_duo_plan(int n, int halo, void* plan, hipStream_t s) {
-  const int64_t m = n + 2 * halo, nh = 6 * (m * m - (int64_t)n * n);
-  hipLaunchKernelGGL(duo_plan_kernel, dim3((unsigned)((nh + 255) / 256)), dim3(256), 0, s, n, halo,
-                     static_cast<DuoEntry*>(plan));
+  const PlanLayout L = plan_layout(n, halo);
+  const int64_t m = n + 2 * halo, nh = 6 * (m * m - (int64_t)n * n), cells = 6LL * n * n;
+  char* base = static_cast<char*>(plan);
+  DuoEntry* fwd = reinterpret_cast<DuoEntry*>(base + L.fwd);
+  DuoTEntry* tent = reinterpret_cast<DuoTEntry*>(base + L.tent);
+  int32_t* cursor = reinterpret_cast<int32_t*>(base + L.cursor);
+  int32_t* sums = reinterpret_cast<int32_t*>(base + L.sums);
+  const int64_t nb = (cells + 1023) / 1024;
+  const unsigned eb = (unsigned)((4 * nh + 255) / 256);
+  hipLaunchKernelGGL(duo_plan_kernel, dim3((unsigned)((nh + 255) / 256)), dim3(256), 0, s, n, halo, fwd);
+  // counters, block sums and the alignment tail: every byte of a plan is defined
+  hipLaunchKernelGGL(zero_i32_kernel, dim3((unsigned)(nb < 4096 ? nb : 4096)), dim3(256), 0, s, cursor,
+                     (L.total - L.cursor) / 4);
+  hipLaunchKernelGGL(duo_count_kernel, dim3(eb), dim3(256), 0, s, fwd, nh, n, cursor);
+  hipLaunchKernelGGL(scan_blocks_kernel, dim3((unsigned)nb), dim3(256), 0, s, cursor, cells, sums);
+  hipLaunchKernelGGL(scan_sums_kernel, dim3(1), dim3(1024), 0, s, sums, nb);
+  hipLaunchKernelGGL(scan_add_kernel, dim3((unsigned)nb), dim3(256), 0, s, cursor, cells, sums);
+  hipLaunchKernelGGL(duo_fill_kernel, dim3(eb), dim3(256), 0, s, fwd, nh, n, halo, cursor, tent);
+  hipLaunchKernelGGL(duo_sort_kernel, dim3(eb), dim3(256), 0, s, tent, 4 * nh);
+  // the list of segment starts: flags, their exclusive scan, then the list
+  int32_t* rank = reinterpret_cast<int32_t*>(base + L.rank);
+  int32_t* hsums = reinterpret_cast<int32_t*>(base + L.hsums);
+  const int64_t nb2 = (4 * nh + 1023) / 1024;
+  hipLaunchKernelGGL(duo_head_flag_kernel, dim3(eb), dim3(256), 0, s, tent, 4 * nh, rank);
+  hipLaunchKernelGGL(scan_blocks_kernel, dim3((unsigned)nb2), dim3(256), 0, s, rank, 4 * nh, hsums);
+  hipLaunchKernelGGL(scan_sums_kernel, dim3(1), dim3(1024), 0, s, hsums, nb2);
+  hipLaunchKernelGGL(scan_add_kernel, dim3((unsigned)nb2), dim3(256), 0, s, rank, 4 * nh, hsums);
+  hipLaunchKernelGGL(duo_head_list_kernel, dim3(eb), dim3(256), 0, s, tent, 4 * nh, rank,
+                     reinterpret_cast<int32_t*>(base + L.heads), reinterpret_cast<int32_t*>(base + L.nheads));
+}
+
+void launch_duo_pad_vjp(const void* gpad, const void* plan, int P, int n, int C, int halo, void* gfaces,
+                        strata_dtype dt, hipStream_t s) {
+  const PlanLayout L = plan_layout(n, halo);
+  const int64_t es = dt == STRATA_BF16 ? 2 : 4, cell = C * es, m = n + 2 * halo;
+  const int64_t nh = 6 * (m * m - (int64_t)n * n);
+  const uintptr_t base = reinterpret_cast<uintptr_t>(gpad) | reinterpret_cast<uintptr_t>(gfaces);
+  const uint64_t align = (uint64_t)(n * cell) | (uint64_t)(halo * cell) | (uint64_t)(m * cell) |
+                         (uint64_t)((int64_t)n * n * cell) | (uint64_t)(m * m * cell) | base;
+  const int word = align % 16 == 0 ? 16 : align % 8 == 0 ? 8 : align % 4 == 0 ? 4 : 2;
+  hipLaunchKernelGGL(duo_crop_kernel, dim3((unsigned)(6 * n)), dim3(1024), 0, s, static_cast<const char*>(gpad), P,
+                     n, C, (int)es, halo, word, static_cast<char*>(gfaces));
+  const int group = (C % 4 == 0 && base % (4 * es) == 0) ? 4 : (C % 2 == 0 && base % (2 * es) == 0) ? 2 : 1;
+  const char* pb = static_cast<const char*>(plan);
+  const DuoTEntry* tent = reinterpret_cast<const DuoTEntry*>(pb + L.tent);
+  const int32_t* heads = reinterpret_cast<const int32_t*>(pb + L.heads);
+  const int32_t* nheads = reinterpret_cast<const int32_t*>(pb + L.nheads);
+  const dim3 grid((unsigned)((4 * nh + 255) / 256), (unsigned)P);
+#define STRATA_DUO_VJP(T, GG)                                                                                      \
+  hipLaunchKernelGGL((duo_vjp_halo_kernel<T, GG>), grid, dim3(256), 0, s, static_cast<const T*>(gpad), tent, heads, \
+                     nheads, 4 * nh, P, n, C, halo, static_cast<T*>(gfaces))
+  if (dt == STRATA_BF16) {
+    if (group == 4)
+      STRATA_DUO_VJP(uint16_t, 4);
+    else if (group == 2)
+      STRATA_DUO_VJP(uint16_t, 2);
+    else
+      STRATA_DUO_VJP(uint16_t, 1);
+  } else {
+    if (group == 4)
+      STRATA_DUO_VJP(float, 4);
+    else if (group == 2)
+      STRATA_DUO_VJP(float, 2);
+    else
+      STRATA_DUO_VJP(float, 1);
+  }
+#undef STRATA_DUO_VJP
 }
 
 void launch_duo_pad_planned(const void* in, const void* plan, int P, int n, int C, int halo, void* out,

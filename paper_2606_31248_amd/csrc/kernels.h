@@ -101,6 +101,8 @@ int64_t duo_plan_bytes(int n, int halo);
 void launch_duo_plan(int n, int halo, void* plan, hipStream_t s);
 void launch_duo_pad_planned(const void* in, const void* plan, int P, int n, int C, int halo, void* out,
                             strata_dtype dt, hipStream_t s);
+void launch_duo_pad_vjp(const void* gpad, const void* plan, int P, int n, int C, int halo, void* gfaces,
+                        strata_dtype dt, hipStream_t s);
 
 void launch_kbd_window(int Ht, int Wt, int overlap, double beta, float* window, hipStream_t s);
 

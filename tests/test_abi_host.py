@@ -204,10 +204,15 @@ def test_duo_rules():
 def test_duo_plan_rules():
     L = B.load()
     p = fake()
-    # one 64-byte entry per halo cell of the six faces
-    assert B.strata_duo_plan_bytes(16, 4) == 6 * (24 * 24 - 16 * 16) * 64
-    assert B.strata_duo_plan_bytes(2048, 16) == 6 * (2080 * 2080 - 2048 * 2048) * 64
+    # P (64 bytes per halo cell), its transpose (4 x 16 bytes per halo cell) and
+    # one build counter per face cell, at least
+    for n, h in ((16, 4), (2048, 16)):
+        nh = 6 * ((n + 2 * h) ** 2 - n * n)
+        assert B.strata_duo_plan_bytes(n, h) >= nh * 128 + 6 * n * n * 4
+        assert B.strata_duo_plan_bytes(n, h) % 16 == 0
     assert B.strata_duo_plan_bytes(8, 1) == 0 and B.strata_duo_plan_bytes(32, 9) == 0
+    assert B.strata_duo_plan_bytes(16384, 16) == 0                       # n + 2 halo >= 2^14
+    assert B.strata_duo_plan_bytes(16350, 16) > 0
     need = B.strata_duo_plan_bytes(32, 4)
     assert L.strata_duo_plan(32, 4, p, need - 1, None) == B.STRATA_ERR_INVALID_ARG
     assert L.strata_duo_plan(32, 4, None, need, None) == B.STRATA_ERR_INVALID_ARG
@@ -219,3 +224,9 @@ def test_duo_plan_rules():
     assert L.strata_duo_pad_planned(p, 1, 32, 1, 4, fake(0x10004), need, p, F, None) == B.STRATA_ERR_INVALID_ARG
     assert L.strata_duo_pad_planned(p, 0, 32, 1, 4, p, need, p, F, None) == B.STRATA_ERR_INVALID_ARG
     assert L.strata_duo_pad_planned(p, 1, 32, 1, 4, p, need, p, 7, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_duo_pad_vjp(p, 1, 32, 1, 4, p, need - 1, p, F, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_duo_pad_vjp(p, 1, 32, 1, 4, None, need, p, F, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_duo_pad_vjp(p, 1, 32, 1, 4, fake(0x10004), need, p, F, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_duo_pad_vjp(p, 1, 32, 1, 9, p, need, p, F, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_duo_pad_vjp(None, 1, 32, 1, 4, p, need, p, F, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_duo_pad_vjp(p, 65536, 32, 1, 4, p, need, p, F, None) == B.STRATA_ERR_INVALID_ARG

@@ -167,7 +167,8 @@ def _halo_cells(n, halo):
 
 @pytest.mark.parametrize("n,halo", [(16, 4), (20, 3), (17, 3)])
 def test_duo_plan_entries_match_oracle(n, halo):
-    # plan entries (64 bytes: float64 weights[4], int32 cells[4], int32 face):
+    # the plan's leading section, one 64-byte entry per halo cell (float64
+    # weights[4], int32 cells[4], int32 face):
     # face and cells exact, weights to float64 rounding
     nb = B.strata_duo_plan_bytes(n, halo)
     plan = torch.empty(nb, dtype=torch.uint8, device="cuda")
@@ -175,9 +176,8 @@ def test_duo_plan_entries_match_oracle(n, halo):
     torch.cuda.synchronize()
     raw = plan.cpu().numpy()
     ent = np.dtype([("w", "<f8", 4), ("cell", "<i4", 4), ("face", "<i4"), ("unused", "<i4", 3)])
-    e = raw.view(ent)
     cells = _halo_cells(n, halo)
-    assert len(e) == 6 * len(cells)
+    e = raw[:6 * len(cells) * 64].view(ent)  # P's entries lead the plan
     for f in range(6):
         for h, (ip, jp) in enumerate(cells):
             fp, rows, cols, w = G.duo_halo_neighbours(f, ip - halo, jp - halo, n)
@@ -222,3 +222,66 @@ def test_duo_planned_full_size_equals_one_shot():
     B.strata_duo_pad_planned(fd, h, plan, b)
     torch.cuda.synchronize()
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def _vjp_tolerance(ref, abs_sum, dtype):
+    if dtype == "f32":  # float64 sums rounded once; weights agree with the oracle's to ~1e-13
+        return np.spacing(np.abs(ref).astype(np.float32)).astype(np.float64) + 1e-12 * abs_sum
+    # float32 fused multiply-adds over a handful of terms, one bf16 rounding
+    return bf16_half_ulp(ref) + 2.0 ** -18 * abs_sum
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("n,halo,P,C", [(16, 4, 2, 3), (20, 3, 1, 2), (17, 3, 1, 1), (32, 8, 1, 8)])
+def test_duo_pad_vjp_matches_oracle(dtype, n, halo, P, C):
+    m = n + 2 * halo
+    g = I.gaussian((6, P, m, m, C), 171 + n, 0, dtype)
+    gd = dev_tensor(g, dtype)
+    plan = torch.empty(B.strata_duo_plan_bytes(n, halo), dtype=torch.uint8, device="cuda")
+    B.strata_duo_plan(n, halo, plan)
+    out = torch.full((6, P, n, n, C), float("nan"), dtype=gd.dtype, device="cuda")
+    B.strata_duo_pad_vjp(gd, halo, plan, out)
+    torch.cuda.synchronize()
+    got = host_f64(out)
+    gw = I.bf16_bits_to_f32(g).astype(np.float64) if dtype == "bf16" else g.astype(np.float64)
+    ref = G.duo_pad_vjp(gw, halo)
+    abs_sum = G.duo_pad_vjp(np.abs(gw), halo)
+    assert float(np.max(np.abs(got - ref) - _vjp_tolerance(ref, abs_sum, dtype))) <= 0.0
+    # deterministic: a second plan and a second pass give the same bits
+    plan2 = torch.empty_like(plan)
+    B.strata_duo_plan(n, halo, plan2)
+    out2 = torch.empty_like(out)
+    B.strata_duo_pad_vjp(gd, halo, plan2, out2)
+    torch.cuda.synchronize()
+    assert torch.equal(plan, plan2)
+    bits = torch.int16 if dtype == "bf16" else torch.int32
+    assert torch.equal(out.view(bits), out2.view(bits))
+
+
+def test_duo_pad_vjp_full_size_adjoint_and_interior():
+    # six 2048-cell faces, halo 16, float32: <P x, y> = <x, P^T y>; the total
+    # of P^T 1 counts every padded cell once; cells deeper than the halo get
+    # their interior gradient bit for bit
+    n, h, P, C = 2048, 16, 2, 4
+    m = n + 2 * h
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(2024)
+    x = torch.randn((6, P, n, n, C), generator=gen, device="cuda")
+    y = torch.randn((6, P, m, m, C), generator=gen, device="cuda")
+    plan = torch.empty(B.strata_duo_plan_bytes(n, h), dtype=torch.uint8, device="cuda")
+    B.strata_duo_plan(n, h, plan)
+    px = torch.empty_like(y)
+    B.strata_duo_pad_planned(x, h, plan, px)
+    pty = torch.empty_like(x)
+    B.strata_duo_pad_vjp(y, h, plan, pty)
+    lhs = float((px.double() * y.double()).sum())
+    rhs = float((x.double() * pty.double()).sum())
+    scale = float((px.double() * y.double()).abs().sum())
+    assert abs(lhs - rhs) <= 1e-6 * scale, (lhs, rhs, scale)
+    d = h + 2
+    assert torch.equal(pty[:, :, d:n - d, d:n - d], y[:, :, h + d:h + n - d, h + d:h + n - d])
+    del x, px
+    ones = torch.ones_like(y)
+    B.strata_duo_pad_vjp(ones, h, plan, pty)
+    total = float(pty.double().sum())
+    assert abs(total - 6 * P * C * m * m) <= 1e-6 * 6 * P * C * m * m
