@@ -122,7 +122,8 @@ static strata_status na3d_fwd_impl(const strata_na3d_desc* desc, const strata_na
   hipStream_t s = (hipStream_t)stream;
   if (!launch_na3d_fwd_col(*desc, o, q, k, v, out, lse, s) &&
       !launch_na3d_fwd_zs(*desc, o, q, k, v, cs, out, lse, s) &&
-      !launch_na3d_fwd_mfma(*desc, o, q, k, v, cs, out, lse, s))
+      !launch_na3d_fwd_mfma(*desc, o, q, k, v, cs, out, lse, s) &&
+      !launch_na3d_fwd_d128(*desc, o, q, k, v, cs, out, lse, s))
     launch_na3d_fwd_ref(*desc, o, q, k, v, cs, out, lse, s);
   return check_launch(opts ? "strata_na3d_fwd_ex" : "strata_na3d_fwd");
 }

@@ -274,3 +274,24 @@ def test_column_bwd_full_size_sampled():
     refs = oracle.na3d_bwd(sub(q), sub(k), sub(v), sub(dout), (24, 1, 1), wl.scale, selq=local, selk=local)
     for name, got, ref in zip(("dq", "dk", "dv"), (dq, dk, dv), refs):
         check_close(host_f64(got).reshape(-1, wl.d)[sel], ref, "bf16", name)
+
+
+# ----------------------------------------------------------------------------- head_dim 128, 9x9x9 (MFMA kernel)
+
+@pytest.mark.parametrize("shape,rope", [((1, 1, 12, 16, 16, 128), True), ((1, 2, 10, 21, 19, 128), False),
+                                        ((2, 1, 9, 9, 9, 128), True)])
+def test_d128_w999_fwd_full_oracle(shape, rope):
+    """The head_dim-128 MFMA forward (single-buffered key levels): every output
+    and LSE against the oracle, ragged blocks and an odd level count included."""
+    r = run(shape, (9, 9, 9), "bf16", 81, rope=rope)
+    check_fwd(r, (9, 9, 9), "bf16", False)
+
+
+def test_d128_w999_fwd_decoder_full_size_sampled():
+    """The decoder shape (2 tiles x 1 head x 24 x 64 x 64, head_dim 128) in one
+    launch; sampled queries (tile corners included) against the oracle."""
+    wl = I.PAPER_DECODER
+    shape = wl.shape()
+    sel = sample_keys(shape, 1500, 82)
+    r = run(shape, (wl.kz, wl.ky, wl.kx), "bf16", wl.seed)
+    check_fwd(r, (wl.kz, wl.ky, wl.kx), "bf16", False, sel=sel)
