@@ -323,7 +323,7 @@ def paper_shapes(steps: int) -> dict:
     from paper_2606_31248_amd import pipeline as Pp
     dev = torch.device("cuda:0")
     res = {}
-    for wl, bwd in ((I.PAPER_TILE16, True), (I.PAPER_TILE32, True), (I.PAPER_COLUMN, True), (I.PAPER_DECODER, False)):
+    for wl, bwd in ((I.PAPER_TILE16, True), (I.PAPER_TILE32, True), (I.PAPER_COLUMN, True), (I.PAPER_DECODER, True)):
         gen = torch.Generator(device=dev)
         gen.manual_seed(wl.seed)
         q, k, v, g = (torch.randn(wl.shape(), generator=gen, device=dev).to(torch.bfloat16) for _ in range(4))

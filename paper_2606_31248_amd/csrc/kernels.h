@@ -94,6 +94,13 @@ bool launch_na3d_bwd_dkdv_mfma(const strata_na3d_desc& d, const BwdOpts& o, cons
                                const void* k, const void* v, const float* cs, const void* dout,
                                const float* lse, const float* dvec, void* dk, void* dv,
                                hipStream_t s);
+// head_dim-128 backward passes (bf16, window 9x9x9, no options); false if not applicable
+bool launch_na3d_bwd_dq_d128(const strata_na3d_desc& d, const BwdOpts& o, const void* q, const void* k,
+                             const void* v, const float* cs, const void* dout, const float* lse,
+                             const float* dvec, void* dq, hipStream_t s);
+bool launch_na3d_bwd_dkdv_d128(const strata_na3d_desc& d, const BwdOpts& o, const void* q, const void* k,
+                               const void* v, const float* cs, const void* dout, const float* lse,
+                               const float* dvec, void* dk, void* dv, hipStream_t s);
 
 void launch_tile_blend(const void* tiles, int nty, int ntx, int P, int Ht, int Wt, int C, int sy,
                        int sx, const float* window, void* out, int Hf, int Wf, strata_dtype dt,

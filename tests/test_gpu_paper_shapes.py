@@ -295,3 +295,36 @@ def test_d128_w999_fwd_decoder_full_size_sampled():
     sel = sample_keys(shape, 1500, 82)
     r = run(shape, (wl.kz, wl.ky, wl.kx), "bf16", wl.seed)
     check_fwd(r, (wl.kz, wl.ky, wl.kx), "bf16", False, sel=sel)
+
+
+@pytest.mark.parametrize("shape,rope", [((1, 1, 12, 16, 16, 128), True), ((1, 1, 11, 13, 17, 128), False)])
+def test_d128_w999_bwd_sampled_keys(shape, rope):
+    """The head_dim-128 MFMA backward: dq of every query, dk and dv of sampled
+    keys (corners included) against the oracle."""
+    window = (9, 9, 9)
+    r = run(shape, window, "bf16", 83, rope=rope, bwd=True)
+    q, k, v, _ = r["inputs"]
+    sel = sample_keys(shape, 64, 84)
+    w = lambda a: oracle.widen(a, "bf16")
+    refs = oracle.na3d_bwd(w(q), w(k), w(v), w(r["dout"]), window, r["scale"], coords=r["c32"], selk=sel)
+    dq, dk, dv, _ = r["grads"]
+    d = shape[-1]
+    check_close(host_f64(dq), refs[0], "bf16", "dq")
+    check_close(host_f64(dk).reshape(-1, d)[sel], refs[1], "bf16", "dk")
+    check_close(host_f64(dv).reshape(-1, d)[sel], refs[2], "bf16", "dv")
+
+
+def test_d128_w999_bwd_decoder_full_size_sampled():
+    """The decoder shape's backward in one launch each; sampled queries and keys
+    against the oracle on both tiles."""
+    wl = I.PAPER_DECODER
+    shape = wl.shape()
+    window = (wl.kz, wl.ky, wl.kx)
+    r = run(shape, window, "bf16", wl.seed, bwd=True)
+    q, k, v, _ = r["inputs"]
+    sel = sample_keys(shape, 160, 85)
+    w = lambda a: oracle.widen(a, "bf16")
+    refs = oracle.na3d_bwd(w(q), w(k), w(v), w(r["dout"]), window, r["scale"], coords=r["c32"], selq=sel, selk=sel)
+    dq, dk, dv, _ = r["grads"]
+    for name, got, ref in zip(("dq", "dk", "dv"), (dq, dk, dv), refs):
+        check_close(host_f64(got).reshape(-1, wl.d)[sel], ref, "bf16", name)
