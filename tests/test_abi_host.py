@@ -230,3 +230,11 @@ def test_duo_plan_rules():
     assert L.strata_duo_pad_vjp(p, 1, 32, 1, 9, p, need, p, F, None) == B.STRATA_ERR_INVALID_ARG
     assert L.strata_duo_pad_vjp(None, 1, 32, 1, 4, p, need, p, F, None) == B.STRATA_ERR_INVALID_ARG
     assert L.strata_duo_pad_vjp(p, 65536, 32, 1, 4, p, need, p, F, None) == B.STRATA_ERR_INVALID_ARG
+    # every device buffer must be 16-byte aligned (the narrow copy paths serve odd layouts only)
+    odd = fake(0x10002)
+    assert L.strata_duo_pad(odd, 1, 32, 1, 4, p, F, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_duo_pad(p, 1, 32, 1, 4, odd, F, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_duo_pad_planned(odd, 1, 32, 1, 4, p, need, p, F, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_duo_pad_planned(p, 1, 32, 1, 4, p, need, odd, F, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_duo_pad_vjp(odd, 1, 32, 1, 4, p, need, p, F, None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_duo_pad_vjp(p, 1, 32, 1, 4, p, need, odd, F, None) == B.STRATA_ERR_INVALID_ARG
