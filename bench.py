@@ -38,6 +38,7 @@ PEAK_BF16_TFLOPS = 2500.0        # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0            # MI355X HBM3E
 PMC_FILE = os.path.join(ROOT, "profiles", "na3d_fwd_face_rollout_pmc.json")
 STATS_FILE = os.path.join(ROOT, "profiles", "face_rollout_step_kernel_stats.txt")
+SQ_FILE = os.path.join(ROOT, "profiles", "na3d_fwd_face_rollout_sq_counters.json")
 # the sources of the kernel that strata_na3d_fwd runs at the face-rollout shape
 KERNEL_SOURCES = ["paper_2606_31248_amd/csrc/na3d_fwd_zs.hip", "paper_2606_31248_amd/csrc/mfma_util.h",
                   "paper_2606_31248_amd/csrc/common.h"]
@@ -122,6 +123,38 @@ def summarize_pmc(fetch_dir: str, write_dir: str, commands) -> dict:
         "note": "Traffic = FETCH_SIZE * fetch_factor + WRITE_SIZE * write_factor, per dispatch; the factors "
                 "make the counters of one 1 GiB device copy read 1 GiB.",
     }
+
+
+def summarize_sq(run_dir: str, commands) -> dict:
+    """Instruction mix of the face forward from one rocprofv3 --pmc run of SQ
+    counters (per dispatch, median over dispatches): every MFMA of the kernel is a
+    16x16x32 one (2*16*16*32 FLOP), so the MFMA count gives the issued FLOP and,
+    against the algorithmic 4*B*h*N*K*d, the useful fraction (window masking
+    over the union key box, the last chunk's padding, the row-sum MFMA)."""
+    acc = {}
+    for k, c, v in _pmc_rows(run_dir):
+        if FWD_KERNEL in k:
+            acc.setdefault(c, []).append(v)
+    if not acc:
+        raise SystemExit(f"no dispatch of {FWD_KERNEL} in the counter run")
+    med = {c: float(np.median(v)) for c, v in acc.items()}
+    flops_alg = 4.0 * 81 * 16 * 8 * 64 * 64 * 147 * 64
+    rec = {"kernel": f"strata_na3d_fwd ({FWD_KERNEL}<8, false, false>: no options)",
+           "workload": "face_rollout_81x16x8x64x64_d64_w3x7x7",
+           "kernel_source_hash": kernel_source_hash(),
+           "counters_per_dispatch": med, "commands": list(commands)}
+    mf = next((v for c, v in med.items() if c.startswith("SQ_INSTS_MFMA")), None)
+    va = next((v for c, v in med.items() if c.startswith("SQ_INSTS_VALU") and "TRANS" not in c), None)
+    tr = next((v for c, v in med.items() if c.startswith("SQ_INSTS_VALU_TRANS_F32")), None)
+    if mf:
+        rec["issued_mfma_flop"] = mf * 2 * 16 * 16 * 32
+        rec["algorithmic_flop"] = flops_alg
+        rec["useful_fraction"] = flops_alg / rec["issued_mfma_flop"]
+        if va:
+            rec["valu_per_mfma"] = (va - mf) / mf  # SQ_INSTS_VALU includes the MFMAs
+        if tr:
+            rec["exp_per_mfma"] = tr / mf
+    return rec
 
 
 def summarize_stats(stats_csv: str, command: str) -> str:
@@ -426,6 +459,8 @@ def main():
                     help="also run one 1 GiB device copy (HBM counter calibration)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write the HBM-traffic summary of two rocprofv3 --pmc runs to profiles/ and exit")
+    ap.add_argument("--summarize-sq", metavar="SQ_DIR",
+                    help="write the instruction-mix summary of a rocprofv3 --pmc run of SQ counters to profiles/ and exit")
     ap.add_argument("--summarize-stats", metavar="KERNEL_STATS_CSV",
                     help="write the kernel-trace summary of a rocprofv3 --stats run to profiles/ and exit")
     ap.add_argument("--command", action="append", default=[],
@@ -434,6 +469,12 @@ def main():
     if a.summarize_pmc:
         rec = summarize_pmc(a.summarize_pmc[0], a.summarize_pmc[1], a.command)
         with open(PMC_FILE, "w") as f:
+            json.dump(rec, f, indent=1)
+        print(json.dumps(rec))
+        return
+    if a.summarize_sq:
+        rec = summarize_sq(a.summarize_sq, a.command)
+        with open(SQ_FILE, "w") as f:
             json.dump(rec, f, indent=1)
         print(json.dumps(rec))
         return
