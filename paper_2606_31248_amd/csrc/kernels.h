@@ -49,7 +49,7 @@ bool launch_na3d_fwd_col(const strata_na3d_desc& d, const NaOpts& o, const void*
                          const void* v, void* out, float* lse, hipStream_t s);
 
 // bf16 MFMA forward; returns false when the problem has no MFMA variant.
-// head_dim-128 forward (bf16, window 9x9x9, no options); false if not applicable
+// head_dim-128 forward (bf16, window 9x9x9, options included); false if not applicable
 bool launch_na3d_fwd_d128(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k,
                           const void* v, const float* cs, void* out, float* lse, hipStream_t s);
 bool launch_na3d_fwd_mfma(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k,

@@ -140,6 +140,14 @@ __device__ __forceinline__ float sum_over_8_lanes(float x) {
   return x;
 }
 
+// Sum over each aligned group of 16 consecutive lanes (a row; every lane of it
+// active): the 8-lane sums, then the mirror across the row pairs the halves.
+__device__ __forceinline__ float sum_over_16_lanes(float x) {
+  x = sum_over_8_lanes(x);
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x140, 0xF, 0xF, false));  // row_mirror
+  return x;
+}
+
 // Logistic sigmoid 1 / (1 + e^-g) of the output gate (hardware exp2 and
 // reciprocal; 0 and 1 at the extremes).
 __device__ __forceinline__ float sigmoid_fast(float g) {

@@ -23,8 +23,11 @@
 // phases read from the float32 table, which stays in the L2 -- published by a
 // barrier, computed, and retired by a second barrier before the next copy.
 // The rotated Q and K are float16 (logit scale and log2(e) folded into Q); P
-// and V are bf16.  Options (QK RMSNorm, the gate) are left to the plain
-// kernel at this head size.
+// and V are bf16.  Options (App. B.5): QK RMSNorm scales each query and key by
+// (mean square + eps)^(-1/2) in float32 before the float16 rounding -- a
+// query's factor from the 4 lanes holding its row, a key's from the 16
+// consecutive lanes whose copies brought it; the sigmoid gate (one logit per
+// token-head or per channel) multiplies the normalised output at the store.
 #include "common.h"
 #include "kernels.h"
 #include "mfma_util.h"
@@ -72,9 +75,12 @@ struct Args {
   int heads, Z, H, W;
   int n_zb, n_yb, n_xb;
   float qscale;      // scale * log2(e)
+  float eps;         // QK RMSNorm
+  const uint16_t* gate;
+  int gate_dim;
 };
 
-template <int KZ, int KY, int KX, int ZQ>
+template <int KZ, int KY, int KX, int ZQ, bool NORM, bool GATE>
 __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_d128_kernel(Args a) {
   using C = Cfg<KZ, KY, KX, ZQ>;
   __shared__ __attribute__((aligned(16))) char tK[C::KBYTES];
@@ -169,11 +175,13 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_d128_kernel(Args a) {
       if (o < 0) continue;
       char* ad = tK + (it * kThreads + tid) * 16;
       uint4 x = ld16(ad);
+      // (a key row is 16 consecutive slots, all in the tile: every lane of the row takes part)
+      const float mul = NORM ? __builtin_amdgcn_rsqf(sum_over_16_lanes(sumsq8(x, 0.f)) * (1.f / kD) + a.eps) : 1.f;
       if (csb) {
         const float4* pp = csb + (o >> 7) * kCS4 + ((o & 127) >> 2);  // pairs 4c..4c+3 of the key's position
-        x = rotate8h(x, pp[0], pp[1], 1.f);
+        x = rotate8h(x, pp[0], pp[1], mul);
       } else {
-        x = scale8h(x, 1.f);
+        x = scale8h(x, mul);
       }
       st16(ad, x);
     }
@@ -189,10 +197,19 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_d128_kernel(Args a) {
     const int zq = min(z0 + grp + 2 * j, Z - 1);
     const int64_t tok = bh_base + zq * HW + (int64_t)qy * W + qx;
     const uint4* src = reinterpret_cast<const uint4*>(a.q + tok * kD);
+    uint4 x[4];
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {  // d = 32 kk + 8 g .. + 7
-      const uint4 x = src[4 * kk + g];
-      const uint4 r = csq ? rotate8h(x, csq[8 * kk + 2 * g], csq[8 * kk + 2 * g + 1], a.qscale) : scale8h(x, a.qscale);
+    for (int kk = 0; kk < 4; ++kk) x[kk] = src[4 * kk + g];  // d = 32 kk + 8 g .. + 7
+    float mul = a.qscale;
+    if constexpr (NORM) {  // the 4 lanes of a query row hold its 128 values
+      float ss = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) ss = sumsq8(x[kk], ss);
+      mul *= __builtin_amdgcn_rsqf(sum_over_rows(ss) * (1.f / kD) + a.eps);
+    }
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const uint4 r = csq ? rotate8h(x[kk], csq[8 * kk + 2 * g], csq[8 * kk + 2 * g + 1], mul) : scale8h(x[kk], mul);
       qf[j][kk] = __builtin_bit_cast(f16x8, r);
     }
     m[j] = -INFINITY;
@@ -280,12 +297,16 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_d128_kernel(Args a) {
     const int zq = z0 + grp + 2 * j;
     const float lt = sum_over_rows(l[j]);
     if (zq >= Z || !in_grid) continue;
-    const float inv = 1.f / lt;
+    float inv = 1.f / lt;
     const int64_t tok = bh_base + zq * HW + (int64_t)qy * W + qx;
     uint2* dst = reinterpret_cast<uint2*>(a.out + tok * kD);
+    if constexpr (GATE)
+      if (a.gate_dim == 1) inv *= sigmoid_fast(bf16_to_f32(a.gate[tok]));
 #pragma unroll
     for (int t = 0; t < 8; ++t) {  // d = 16t + 4g + i
-      const f32x4 r = o[j][t] * inv;
+      f32x4 r = o[j][t] * inv;
+      if constexpr (GATE)
+        if (a.gate_dim != 1) r *= sigmoid4_bf16(reinterpret_cast<const uint2*>(a.gate + tok * kD)[4 * t + g]);
       dst[4 * t + g] = make_uint2(pack2(r[0], r[1]), pack2(r[2], r[3]));
     }
     if (a.lse && g == 0) a.lse[tok] = (m[j] + __log2f(lt)) * kLn2;
@@ -296,7 +317,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_d128_kernel(Args a) {
 
 bool launch_na3d_fwd_d128(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k,
                           const void* v, const float* cs, void* out, float* lse, hipStream_t s) {
-  if (d.dtype != STRATA_BF16 || d.head_dim != kD || o.qk_norm || o.gate) return false;
+  if (d.dtype != STRATA_BF16 || d.head_dim != kD) return false;
   if (!(d.kz == 9 && d.ky == 9 && d.kx == 9)) return false;
   if ((int64_t)d.H * d.W * kD >= (int64_t)1 << 31) return false;  // int32 offsets inside a key level
   constexpr int ZQ = 2;
@@ -315,9 +336,20 @@ bool launch_na3d_fwd_d128(const strata_na3d_desc& d, const NaOpts& o, const void
   a.n_yb = (d.H + kBY - 1) / kBY;
   a.n_xb = (d.W + kBX - 1) / kBX;
   a.qscale = d.scale * kLog2e;
+  a.eps = o.eps;
+  a.gate = static_cast<const uint16_t*>(o.gate);
+  a.gate_dim = o.gate_dim;
   const int64_t blocks = (int64_t)d.B * d.heads * a.n_zb * a.n_yb * a.n_xb;
   if (blocks >= (int64_t)1 << 31) return false;
-  hipLaunchKernelGGL((na3d_fwd_d128_kernel<9, 9, 9, ZQ>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
+  const dim3 grid((unsigned)blocks), block(kThreads);
+  if (o.qk_norm && o.gate)
+    hipLaunchKernelGGL((na3d_fwd_d128_kernel<9, 9, 9, ZQ, true, true>), grid, block, 0, s, a);
+  else if (o.qk_norm)
+    hipLaunchKernelGGL((na3d_fwd_d128_kernel<9, 9, 9, ZQ, true, false>), grid, block, 0, s, a);
+  else if (o.gate)
+    hipLaunchKernelGGL((na3d_fwd_d128_kernel<9, 9, 9, ZQ, false, true>), grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL((na3d_fwd_d128_kernel<9, 9, 9, ZQ, false, false>), grid, block, 0, s, a);
   return true;
 }
 

@@ -328,3 +328,20 @@ def test_d128_w999_bwd_decoder_full_size_sampled():
     dq, dk, dv, _ = r["grads"]
     for name, got, ref in zip(("dq", "dk", "dv"), (dq, dk, dv), refs):
         check_close(host_f64(got).reshape(-1, wl.d)[sel], ref, "bf16", name)
+
+
+@pytest.mark.parametrize("qk_norm,gkind", [(True, 0), (False, 1), (False, "d"), (True, "d")])
+def test_d128_w999_fwd_options_full_oracle(qk_norm, gkind):
+    """QK RMSNorm and the output gate (App. B.5: every attention block has them,
+    the decoder's included) in the head_dim-128 MFMA forward: full grid."""
+    shape = (1, 1, 12, 16, 16, 128)
+    r = run(shape, (9, 9, 9), "bf16", 86, qk_norm=qk_norm, gkind=gkind)
+    check_fwd(r, (9, 9, 9), "bf16", qk_norm)
+
+
+def test_d128_w999_fwd_options_decoder_full_size_sampled():
+    wl = I.PAPER_DECODER
+    shape = wl.shape()
+    sel = sample_keys(shape, 1200, 87)
+    r = run(shape, (wl.kz, wl.ky, wl.kx), "bf16", wl.seed, qk_norm=True, gkind="d")
+    check_fwd(r, (wl.kz, wl.ky, wl.kx), "bf16", True, sel=sel)
