@@ -1,5 +1,9 @@
 // MFMA neighbourhood-attention backward for head_dim 128 (the decoder's NA3D,
-// App. B.3), bf16 in/out, window 9 x 9 x 9, StereoRoPE fused; no options.
+// App. B.3), bf16 in/out, window 9 x 9 x 9, StereoRoPE fused.  Options (App.
+// B.5): QK RMSNorm in both passes (factors at the Q/K loads, the norm's
+// Jacobian applied to dQ and dK at the store); a two-term upstream gradient
+// (the gated dA = hi + lo) in the dQ pass -- the dK/dV pass would need a third
+// 64 KB staged tile, so that case stays on the plain kernel.
 //
 // The same two passes and arithmetic as at head_dim 64, with 128-wide rows:
 //
@@ -66,6 +70,8 @@ struct Args {
   int heads, Z, H, W;
   int n_zb, n_yb, n_xb;
   float scale, qscale;   // scale, scale * log2(e)
+  float eps;             // QK RMSNorm (with NORM)
+  const uint16_t* dout_lo;  // low term of a two-term upstream gradient (with LO)
 };
 
 // ============================================================================ dQ
@@ -89,7 +95,7 @@ struct QCfg {
   static_assert(KBYTES + VBYTES <= kLdsMax, "key tiles exceed LDS");
 };
 
-template <int KZ, int KY, int KX, int ZQ>
+template <int KZ, int KY, int KX, int ZQ, bool NORM, bool LO>
 __global__ void __launch_bounds__(kQThreads, 1) na3d_bwd_dq_d128_kernel(Args a) {
   using C = QCfg<KZ, KY, KX, ZQ>;
   __shared__ __attribute__((aligned(16))) char tK[C::KBYTES];
@@ -185,11 +191,13 @@ __global__ void __launch_bounds__(kQThreads, 1) na3d_bwd_dq_d128_kernel(Args a) 
       if (o < 0) continue;
       char* ad = tK + (it * kQThreads + tid) * 16;
       uint4 x = ld16(ad);
+      // (a key row is 16 consecutive slots, all in the tile)
+      const float mul = NORM ? __builtin_amdgcn_rsqf(sum_over_16_lanes(sumsq8(x, 0.f)) * (1.f / kD) + a.eps) : 1.f;
       if (csb) {
         const float4* pp = csb + (o >> 7) * kCS4 + ((o & 127) >> 2);
-        x = rotate8h(x, pp[0], pp[1], 1.f);
+        x = rotate8h(x, pp[0], pp[1], mul);
       } else {
-        x = scale8h(x, 1.f);
+        x = scale8h(x, mul);
       }
       st16(ad, x);
     }
@@ -197,7 +205,8 @@ __global__ void __launch_bounds__(kQThreads, 1) na3d_bwd_dq_d128_kernel(Args a) 
 
   // queries: Q~ (float16, times scale log2 e) and dO (bf16) as B operands
   f16x8 qf[C::QL][4];
-  bf16x8 gf[C::QL][4];
+  bf16x8 gf[C::QL][4], gl[LO ? C::QL : 1][4];  // dO (hi and low terms)
+  float rq[NORM ? C::QL : 1];                  // QK RMSNorm factor of the query
   float lse2[C::QL], nd[C::QL];
   int ex[C::QL];
   f32x4 o[C::QL][8];
@@ -208,12 +217,23 @@ __global__ void __launch_bounds__(kQThreads, 1) na3d_bwd_dq_d128_kernel(Args a) 
     const int64_t tok = bh_base + zq * HW + (int64_t)qy * W + qx;
     const uint4* src = reinterpret_cast<const uint4*>(a.q + tok * kD);
     const uint4* gsrc = reinterpret_cast<const uint4*>(a.dout + tok * kD);
+    uint4 x[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) x[kk] = src[4 * kk + g];
+    float mul = a.qscale;
+    if constexpr (NORM) {  // the 4 lanes of a query row hold its 128 values
+      float ss = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) ss = sumsq8(x[kk], ss);
+      rq[j] = __builtin_amdgcn_rsqf(sum_over_rows(ss) * (1.f / kD) + a.eps);
+      mul *= rq[j];
+    }
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-      const uint4 x = src[4 * kk + g];
-      const uint4 r = csq ? rotate8h(x, csq[8 * kk + 2 * g], csq[8 * kk + 2 * g + 1], a.qscale) : scale8h(x, a.qscale);
+      const uint4 r = csq ? rotate8h(x[kk], csq[8 * kk + 2 * g], csq[8 * kk + 2 * g + 1], mul) : scale8h(x[kk], mul);
       qf[j][kk] = __builtin_bit_cast(f16x8, r);
       gf[j][kk] = __builtin_bit_cast(bf16x8, gsrc[4 * kk + g]);
+      if constexpr (LO) gl[j][kk] = __builtin_bit_cast(bf16x8, reinterpret_cast<const uint4*>(a.dout_lo + tok * kD)[4 * kk + g]);
     }
     lse2[j] = a.lse[tok] * kLog2e;
     nd[j] = -a.dvec[tok];
@@ -239,6 +259,7 @@ __global__ void __launch_bounds__(kQThreads, 1) na3d_bwd_dq_d128_kernel(Args a) 
         acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf, qf[j][kk], acc, 0, 0, 0);
         const bf16x8 vv = __builtin_bit_cast(bf16x8, ld16(tV + vrow[c] + 64 * kk));
         yy = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vv, gf[j][kk], yy, 0, 0, 0);
+        if constexpr (LO) yy = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vv, gl[j][kk], yy, 0, 0, 0);
       }
       my = fmaxf(fmaxf(my, fmaxf(fabsf(yy[0]), fabsf(yy[1]))), fmaxf(fabsf(yy[2]), fabsf(yy[3])));
 #pragma unroll
@@ -305,17 +326,38 @@ __global__ void __launch_bounds__(kQThreads, 1) na3d_bwd_dq_d128_kernel(Args a) 
     const float f = a.scale * __builtin_amdgcn_ldexpf(1.f, ex[j] - 15);
     const int64_t tok = bh_base + zq * HW + (int64_t)qy * W + qx;
     uint2* dst = reinterpret_cast<uint2*>(a.dq + tok * kD);
+    f32x4 x[8];
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
-      f32x4 x = o[j][t] * f;
+      x[t] = o[j][t] * f;
       if (csq) {
         const float4 ph = csq[4 * t + g];  // pairs 8t+2g and 8t+2g+1
-        const float r0 = fmaf(x[0], ph.x, x[1] * ph.y), r1 = fmaf(x[1], ph.x, -x[0] * ph.y);
-        const float r2 = fmaf(x[2], ph.z, x[3] * ph.w), r3 = fmaf(x[3], ph.z, -x[2] * ph.w);
-        x = f32x4{r0, r1, r2, r3};
+        const float r0 = fmaf(x[t][0], ph.x, x[t][1] * ph.y), r1 = fmaf(x[t][1], ph.x, -x[t][0] * ph.y);
+        const float r2 = fmaf(x[t][2], ph.z, x[t][3] * ph.w), r3 = fmaf(x[t][3], ph.z, -x[t][2] * ph.w);
+        x[t] = f32x4{r0, r1, r2, r3};
       }
-      dst[4 * t + g] = make_uint2(pack2(x[0], x[1]), pack2(x[2], x[3]));
     }
+    if constexpr (NORM) {
+      // the gradient of q^ = r q carried back through the norm:
+      // dq = r (dq^ - q^ mean(dq^ q^)), q^ from the raw row in float32
+      const uint2* qr = reinterpret_cast<const uint2*>(a.q + tok * kD);
+      f32x4 qh[8];
+      float c = 0.f;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const uint2 w = qr[4 * t + g];
+        qh[t] = f32x4{lo_bf16(w.x), hi_bf16(w.x), lo_bf16(w.y), hi_bf16(w.y)} * rq[j];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) c = fmaf(x[t][i], qh[t][i], c);
+      }
+      c = sum_over_rows(c) * (1.f / kD);
+#pragma unroll
+      for (int t = 0; t < 8; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) x[t][i] = rq[j] * fmaf(-qh[t][i], c, x[t][i]);
+    }
+#pragma unroll
+    for (int t = 0; t < 8; ++t) dst[4 * t + g] = make_uint2(pack2(x[t][0], x[t][1]), pack2(x[t][2], x[t][3]));
   }
 }
 
@@ -339,7 +381,7 @@ struct KvCfg {
   static_assert(2 * TBYTES + 2 * MQ * 4 + MQ * 2 <= kLdsMax, "query tiles exceed LDS");
 };
 
-template <int KZ, int KY, int KX, int ZK>
+template <int KZ, int KY, int KX, int ZK, bool NORM>
 __global__ void __launch_bounds__(64 * ZK, 1) na3d_bwd_dkdv_d128_kernel(Args a) {
   using C = KvCfg<KZ, KY, KX, ZK>;
   constexpr int kThreads = C::kThreads;
@@ -445,11 +487,13 @@ __global__ void __launch_bounds__(64 * ZK, 1) na3d_bwd_dkdv_d128_kernel(Args a) 
       if (o < 0) continue;
       char* ad = tQ + (it * kThreads + tid) * 16;
       const uint4 x = ld16(ad);
+      // (a query row is 16 consecutive slots, all in or all past the box)
+      const float mul = NORM ? __builtin_amdgcn_rsqf(sum_over_16_lanes(sumsq8(x, 0.f)) * (1.f / kD) + a.eps) : 1.f;
       if (csb) {
         const float4* pp = csb + (o >> 7) * kCS4 + ((o & 127) >> 2);
-        st16(ad, rotate8h(x, pp[0], pp[1], 1.f));
+        st16(ad, rotate8h(x, pp[0], pp[1], mul));
       } else {
-        st16(ad, scale8h(x, 1.f));
+        st16(ad, scale8h(x, mul));
       }
     }
 #pragma unroll
@@ -470,13 +514,23 @@ __global__ void __launch_bounds__(64 * ZK, 1) na3d_bwd_dkdv_d128_kernel(Args a) 
   const float4* csk = csb ? csb + ((int64_t)ky * W + kx) * kCS4 : nullptr;
   f16x8 kf[4];
   bf16x8 vf[4];
+  float rk = 1.f;  // QK RMSNorm factor of this lane's key
   {
     const uint4* src = reinterpret_cast<const uint4*>(a.k + ktok * kD);
     const uint4* vs = reinterpret_cast<const uint4*>(a.v + ktok * kD);
+    uint4 x[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) x[kk] = src[4 * kk + g];
+    if constexpr (NORM) {  // the 4 lanes of a key row hold its 128 values
+      float ss = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) ss = sumsq8(x[kk], ss);
+      rk = __builtin_amdgcn_rsqf(sum_over_rows(ss) * (1.f / kD) + a.eps);
+    }
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-      const uint4 x = src[4 * kk + g];
-      const uint4 r = csk ? rotate8h(x, csk[8 * kk + 2 * g], csk[8 * kk + 2 * g + 1], a.qscale) : scale8h(x, a.qscale);
+      const float mul = a.qscale * rk;
+      const uint4 r = csk ? rotate8h(x[kk], csk[8 * kk + 2 * g], csk[8 * kk + 2 * g + 1], mul) : scale8h(x[kk], mul);
       kf[kk] = __builtin_bit_cast(f16x8, r);
       vf[kk] = __builtin_bit_cast(bf16x8, vs[4 * kk + g]);
     }
@@ -582,22 +636,45 @@ __global__ void __launch_bounds__(64 * ZK, 1) na3d_bwd_dkdv_d128_kernel(Args a) 
     __syncthreads();  // every read of the level is done before the next copy
   }
 
-  // dV, and dK = R^T (scale 2^(E-15) dK~); the lane holds d = 16t + 4g + i
-  if (!wave_on || ky_raw >= H || kx_raw >= W) return;
+  // dV, and dK = R^T (scale 2^(E-15) dK~); the lane holds d = 16t + 4g + i.
+  // With QK RMSNorm that is the gradient of k^ = r k, carried back through the
+  // norm: dk = r (dk^ - k^ mean(dk^ k^)), k^ from the raw row in float32.
   const float f = a.scale * __builtin_amdgcn_ldexpf(1.f, ex - 15);
+  f32x4 xk[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    xk[t] = accK[t] * f;
+    if (csk) {
+      const float4 p = csk[4 * t + g];  // pairs 8t+2g and 8t+2g+1
+      const float r0 = fmaf(xk[t][0], p.x, xk[t][1] * p.y), r1 = fmaf(xk[t][1], p.x, -xk[t][0] * p.y);
+      const float r2 = fmaf(xk[t][2], p.z, xk[t][3] * p.w), r3 = fmaf(xk[t][3], p.z, -xk[t][2] * p.w);
+      xk[t] = f32x4{r0, r1, r2, r3};
+    }
+  }
+  if constexpr (NORM) {
+    const uint2* kr = reinterpret_cast<const uint2*>(a.k + ktok * kD);
+    f32x4 kh[8];
+    float c = 0.f;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const uint2 w = kr[4 * t + g];
+      kh[t] = f32x4{lo_bf16(w.x), hi_bf16(w.x), lo_bf16(w.y), hi_bf16(w.y)} * rk;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) c = fmaf(xk[t][i], kh[t][i], c);
+    }
+    c = sum_over_rows(c) * (1.f / kD);
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) xk[t][i] = rk * fmaf(-kh[t][i], c, xk[t][i]);
+  }
+  if (!wave_on || ky_raw >= H || kx_raw >= W) return;
   uint2* dkd = reinterpret_cast<uint2*>(a.dk + ktok * kD);
   uint2* dvd = reinterpret_cast<uint2*>(a.dv + ktok * kD);
 #pragma unroll
   for (int t = 0; t < 8; ++t) {
-    f32x4 xk = accK[t] * f;
-    if (csk) {
-      const float4 p = csk[4 * t + g];  // pairs 8t+2g and 8t+2g+1
-      const float r0 = fmaf(xk[0], p.x, xk[1] * p.y), r1 = fmaf(xk[1], p.x, -xk[0] * p.y);
-      const float r2 = fmaf(xk[2], p.z, xk[3] * p.w), r3 = fmaf(xk[3], p.z, -xk[2] * p.w);
-      xk = f32x4{r0, r1, r2, r3};
-    }
     dvd[4 * t + g] = make_uint2(pack2(accV[t][0], accV[t][1]), pack2(accV[t][2], accV[t][3]));
-    dkd[4 * t + g] = make_uint2(pack2(xk[0], xk[1]), pack2(xk[2], xk[3]));
+    dkd[4 * t + g] = make_uint2(pack2(xk[t][0], xk[t][1]), pack2(xk[t][2], xk[t][3]));
   }
 }
 
@@ -611,8 +688,8 @@ int max_box(int L, int k) {
   return mx;
 }
 
-bool supported(const strata_na3d_desc& d, const BwdOpts& o) {
-  if (d.dtype != STRATA_BF16 || d.head_dim != kD || o.qk_norm || o.dout_lo) return false;
+bool supported(const strata_na3d_desc& d) {
+  if (d.dtype != STRATA_BF16 || d.head_dim != kD) return false;
   if (!(d.kz == 9 && d.ky == 9 && d.kx == 9)) return false;
   return (int64_t)d.H * d.W * kD < (int64_t)1 << 31;  // int32 offsets inside a level
 }
@@ -641,35 +718,53 @@ Args make_args(const strata_na3d_desc& d, const void* q, const void* k, const vo
 bool launch_na3d_bwd_dq_d128(const strata_na3d_desc& d, const BwdOpts& o, const void* q, const void* k,
                              const void* v, const float* cs, const void* dout, const float* lse,
                              const float* dvec, void* dq, hipStream_t s) {
-  if (!supported(d, o)) return false;
-  constexpr int ZQ = 2;
+  if (!supported(d)) return false;
   Args a = make_args(d, q, k, v, cs, dout, lse, dvec);
   a.dq = static_cast<uint16_t*>(dq);
-  a.n_zb = (d.Z + ZQ - 1) / ZQ;
+  a.eps = o.eps;
+  a.dout_lo = static_cast<const uint16_t*>(o.dout_lo);
+  // two query levels per wave, one with the two-term dO (its low term's
+  // fragments would not fit beside two levels' state)
+  const int zq = o.dout_lo ? 1 : 2;
+  a.n_zb = (d.Z + zq - 1) / zq;
   a.n_yb = (d.H + kQBY - 1) / kQBY;
   a.n_xb = (d.W + kQBX - 1) / kQBX;
   const int64_t blocks = (int64_t)d.B * d.heads * a.n_zb * a.n_yb * a.n_xb;
   if (blocks >= (int64_t)1 << 31) return false;
-  hipLaunchKernelGGL((na3d_bwd_dq_d128_kernel<9, 9, 9, ZQ>), dim3((unsigned)blocks), dim3(kQThreads), 0, s, a);
+  const dim3 grid((unsigned)blocks), block(kQThreads);
+  if (o.qk_norm && o.dout_lo)
+    hipLaunchKernelGGL((na3d_bwd_dq_d128_kernel<9, 9, 9, 1, true, true>), grid, block, 0, s, a);
+  else if (o.qk_norm)
+    hipLaunchKernelGGL((na3d_bwd_dq_d128_kernel<9, 9, 9, 2, true, false>), grid, block, 0, s, a);
+  else if (o.dout_lo)
+    hipLaunchKernelGGL((na3d_bwd_dq_d128_kernel<9, 9, 9, 1, false, true>), grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL((na3d_bwd_dq_d128_kernel<9, 9, 9, 2, false, false>), grid, block, 0, s, a);
   return true;
 }
 
 bool launch_na3d_bwd_dkdv_d128(const strata_na3d_desc& d, const BwdOpts& o, const void* q, const void* k,
                                const void* v, const float* cs, const void* dout, const float* lse,
                                const float* dvec, void* dk, void* dv, hipStream_t s) {
-  if (!supported(d, o)) return false;
+  // a two-term upstream gradient would need a third 64 KB staged tile: plain kernel
+  if (!supported(d) || o.dout_lo) return false;
   constexpr int ZK = 8;
   using C = KvCfg<9, 9, 9, ZK>;
   if (max_box(d.H, 9) > C::MQY || max_box(d.W, 9) > C::MQX) return false;
   Args a = make_args(d, q, k, v, cs, dout, lse, dvec);
   a.dk = static_cast<uint16_t*>(dk);
   a.dv = static_cast<uint16_t*>(dv);
+  a.eps = o.eps;
   a.n_zb = (d.Z + ZK - 1) / ZK;
   a.n_yb = (d.H + 3) / 4;
   a.n_xb = (d.W + 3) / 4;
   const int64_t blocks = (int64_t)d.B * d.heads * a.n_zb * a.n_yb * a.n_xb;
   if (blocks >= (int64_t)1 << 31) return false;
-  hipLaunchKernelGGL((na3d_bwd_dkdv_d128_kernel<9, 9, 9, ZK>), dim3((unsigned)blocks), dim3(C::kThreads), 0, s, a);
+  if (o.qk_norm)
+    hipLaunchKernelGGL((na3d_bwd_dkdv_d128_kernel<9, 9, 9, ZK, true>), dim3((unsigned)blocks), dim3(C::kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL((na3d_bwd_dkdv_d128_kernel<9, 9, 9, ZK, false>), dim3((unsigned)blocks), dim3(C::kThreads), 0, s,
+                       a);
   return true;
 }
 

@@ -345,3 +345,25 @@ def test_d128_w999_fwd_options_decoder_full_size_sampled():
     sel = sample_keys(shape, 1200, 87)
     r = run(shape, (wl.kz, wl.ky, wl.kx), "bf16", wl.seed, qk_norm=True, gkind="d")
     check_fwd(r, (wl.kz, wl.ky, wl.kx), "bf16", True, sel=sel)
+
+
+@pytest.mark.parametrize("qk_norm,gkind", [(True, 0), (True, "d"), (False, 1), (False, "d")])
+def test_d128_w999_bwd_options_sampled_keys(qk_norm, gkind):
+    """The head_dim-128 backward with QK RMSNorm and the gate (dQ on the MFMA
+    kernel with the two-term dA; dK, dV on it with the norm): dq of every
+    query, dk, dv, dgate of sampled keys and queries against the oracle."""
+    shape, window = (1, 1, 12, 16, 16, 128), (9, 9, 9)
+    r = run(shape, window, "bf16", 88, qk_norm=qk_norm, gkind=gkind, bwd=True)
+    q, k, v, g = r["inputs"]
+    sel = sample_keys(shape, 40, 89)
+    w = lambda a: None if a is None else oracle.widen(a, "bf16")
+    refs = oracle.na3d_bwd(w(q), w(k), w(v), w(r["dout"]), window, r["scale"], coords=r["c32"], selq=sel,
+                           selk=sel, qk_norm=qk_norm, gate=w(g))
+    got = [None if x is None else host_f64(x) for x in r["grads"]]
+    got = [None if x is None else (x.reshape(-1)[sel] if x.ndim == 5 else x.reshape(-1, x.shape[-1])[sel])
+           for x in got]
+    check_bwd_grads((q, k, v, g, r["dout"]), [None if x is None else torch.from_numpy(x) for x in got], refs,
+                    window, r["scale"], "bf16", qk_norm, r["c32"], sel=sel, presliced=True)
+    rq = oracle.na3d_bwd(w(q), w(k), w(v), w(r["dout"]), window, r["scale"], coords=r["c32"],
+                         selk=np.array([0]), qk_norm=qk_norm, gate=w(g))[0]
+    check_close(host_f64(r["grads"][0]), rq, "bf16", "dq (all)")
