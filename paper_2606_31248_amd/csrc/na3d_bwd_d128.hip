@@ -2,8 +2,9 @@
 // App. B.3), bf16 in/out, window 9 x 9 x 9, StereoRoPE fused.  Options (App.
 // B.5): QK RMSNorm in both passes (factors at the Q/K loads, the norm's
 // Jacobian applied to dQ and dK at the store); a two-term upstream gradient
-// (the gated dA = hi + lo) in the dQ pass -- the dK/dV pass would need a third
-// 64 KB staged tile, so that case stays on the plain kernel.
+// (the gated dA = hi + lo) in both passes: one more MFMA per k-step for Y and
+// per tile for dV, the dK/dV pass then staging the query box in two windows
+// of 128 rows (three 32 KB tiles).
 //
 // The same two passes and arithmetic as at head_dim 64, with 128-wide rows:
 //
@@ -369,24 +370,31 @@ __host__ __device__ __forceinline__ int inv_lo(int j, int k) { return j < k ? 0 
 __host__ __device__ __forceinline__ int inv_hi(int j, int L, int k) { return j >= L - k ? L - 1 : j + (k >> 1); }
 __device__ __forceinline__ int rswz(int u) { return (((u >> 1) & 3) << 1) | ((u >> 3) & 1); }
 
-template <int KZ, int KY, int KX, int ZK>
+// The query box is staged in row windows of RW rows: the whole box (Q~ and dO,
+// 2 x 64 KB) without the low term; with it, three tiles of 128 rows (96 KB)
+// and two windows per level.
+template <int KZ, int KY, int KX, int ZK, bool LO>
 struct KvCfg {
   static constexpr int kThreads = 64 * ZK;
   static constexpr int MQY = 4 + 3 * (KY / 2), MQX = 4 + 3 * (KX / 2);  // largest query box
   static constexpr int MQ = (MQY * MQX + 31) / 32 * 32;                  // rows, whole 32-query steps
-  static constexpr int TBYTES = MQ * kRow;
-  static constexpr int SLOTS = MQ * (kRow / 16);
+  static constexpr int RW = LO ? 128 : MQ;                               // rows per staged window
+  static constexpr int NW = (MQ + RW - 1) / RW;                          // windows of the largest box
+  static constexpr int TBYTES = RW * kRow;
+  static constexpr int SLOTS = RW * (kRow / 16);
   static constexpr int IT = (SLOTS + kThreads - 1) / kThreads;
   static constexpr int IS = (MQ + kThreads - 1) / kThreads;
-  static_assert(2 * TBYTES + 2 * MQ * 4 + MQ * 2 <= kLdsMax, "query tiles exceed LDS");
+  static_assert(RW % 32 == 0 && SLOTS % kThreads == 0, "windows of whole steps, whole copy passes");
+  static_assert((LO ? 3 : 2) * TBYTES + 2 * MQ * 4 + MQ * 2 <= kLdsMax, "query tiles exceed LDS");
 };
 
-template <int KZ, int KY, int KX, int ZK, bool NORM>
+template <int KZ, int KY, int KX, int ZK, bool NORM, bool LO>
 __global__ void __launch_bounds__(64 * ZK, 1) na3d_bwd_dkdv_d128_kernel(Args a) {
-  using C = KvCfg<KZ, KY, KX, ZK>;
+  using C = KvCfg<KZ, KY, KX, ZK, LO>;
   constexpr int kThreads = C::kThreads;
   __shared__ __attribute__((aligned(16))) char tQ[C::TBYTES];
   __shared__ __attribute__((aligned(16))) char tG[C::TBYTES];
+  __shared__ __attribute__((aligned(16))) char tL[LO ? C::TBYTES : 16];  // low term of dO (LO)
   __shared__ __attribute__((aligned(16))) float sL[C::MQ];
   __shared__ __attribute__((aligned(16))) float sD[C::MQ];
   __shared__ __attribute__((aligned(16))) unsigned short smask[C::MQ];
@@ -434,22 +442,19 @@ __global__ void __launch_bounds__(64 * ZK, 1) na3d_bwd_dkdv_d128_kernel(Args a) 
     }
     smask[u] = (unsigned short)bits;
   }
-  // rows past the box up to the last 32-query step: zero in both tiles
-  for (int i = nq * 16 + tid; i < npairs * 512; i += kThreads) {
-    const uint4 z = make_uint4(0u, 0u, 0u, 0u);
-    st16(tQ + i * 16, z);
-    st16(tG + i * 16, z);
-  }
-
-  // copy map: row u = s / 16 holds box query u, slot column s % 16 holds data
-  // column (s % 16) ^ sigma(u); Q and dO share it; -1 past the box
-  int goff[C::IT];
+  // copy map of window w: tile row r = s / 16 holds box query u = w RW + r,
+  // slot column s % 16 holds data column (s % 16) ^ sigma(r) (sigma of the row
+  // inside its 32-row step, which is also sigma(u)); Q and dO share it.
+  // goff: element offset inside a level; -1: a row past the box but inside the
+  // last 32-query step (written as zeros); -2: past that (untouched)
+  int goff[C::NW][C::IT];
 #pragma unroll
-  for (int it = 0; it < C::IT; ++it) {
-    const int s = it * kThreads + tid, u = s >> 4, dc = (s & 15) ^ rswz(u);
-    goff[it] = -1;
-    if (s < C::SLOTS && u < nq) goff[it] = ((qy0 + u / nqx) * W + qx0 + u % nqx) * kD + dc * 8;
-  }
+  for (int w = 0; w < C::NW; ++w)
+#pragma unroll
+    for (int it = 0; it < C::IT; ++it) {
+      const int s = it * kThreads + tid, r = s >> 4, u = w * C::RW + r, dc = (s & 15) ^ rswz(r);
+      goff[w][it] = u < nq ? ((qy0 + u / nqx) * W + qx0 + u % nqx) * kD + dc * 8 : (u < npairs * 32 ? -1 : -2);
+    }
   int soff[C::IS];
   float pl[C::IS], pd[C::IS];
 #pragma unroll
@@ -460,30 +465,42 @@ __global__ void __launch_bounds__(64 * ZK, 1) na3d_bwd_dkdv_d128_kernel(Args a) 
     pd[is] = 0.f;
   }
 
-  auto issue = [&](int p) {
+  // stage window w of level p (and, with the first window, its LSE / D)
+  auto issue = [&](int p, int w) {
     const int64_t lev = bh_base + (int64_t)p * HW;
     const uint16_t* qp = a.q + lev * kD;
     const uint16_t* gp = a.dout + lev * kD;
+    const uint16_t* lp = LO ? a.dout_lo + lev * kD : nullptr;
 #pragma unroll
     for (int it = 0; it < C::IT; ++it) {
-      if (goff[it] < 0) continue;
-      copy16_to_lds(qp + goff[it], tQ + (it * kThreads + wave * 64) * 16);
-      copy16_to_lds(gp + goff[it], tG + (it * kThreads + wave * 64) * 16);
+      const int o = goff[w][it];
+      if (o >= 0) {
+        copy16_to_lds(qp + o, tQ + (it * kThreads + wave * 64) * 16);
+        copy16_to_lds(gp + o, tG + (it * kThreads + wave * 64) * 16);
+        if constexpr (LO) copy16_to_lds(lp + o, tL + (it * kThreads + wave * 64) * 16);
+      } else if (o == -1) {  // rows past the box inside the last step: zeros
+        const uint4 z = make_uint4(0u, 0u, 0u, 0u);
+        st16(tQ + (it * kThreads + tid) * 16, z);
+        st16(tG + (it * kThreads + tid) * 16, z);
+        if constexpr (LO) st16(tL + (it * kThreads + tid) * 16, z);
+      }
     }
+    if (w == 0) {
 #pragma unroll
-    for (int is = 0; is < C::IS; ++is) {
-      if (soff[is] < 0) continue;
-      pl[is] = a.lse[lev + soff[is]];
-      pd[is] = a.dvec[lev + soff[is]];
+      for (int is = 0; is < C::IS; ++is) {
+        if (soff[is] < 0) continue;
+        pl[is] = a.lse[lev + soff[is]];
+        pd[is] = a.dvec[lev + soff[is]];
+      }
     }
   };
   // wait for this thread's copies, rotate its own Q slots in place, store its
-  // LSE / D entries
-  auto finish = [&]() {
+  // LSE / D entries (first window)
+  auto finish = [&](int w) {
     __builtin_amdgcn_s_waitcnt(0);
 #pragma unroll
     for (int it = 0; it < C::IT; ++it) {
-      const int o = goff[it];
+      const int o = goff[w][it];
       if (o < 0) continue;
       char* ad = tQ + (it * kThreads + tid) * 16;
       const uint4 x = ld16(ad);
@@ -496,12 +513,14 @@ __global__ void __launch_bounds__(64 * ZK, 1) na3d_bwd_dkdv_d128_kernel(Args a) 
         st16(ad, scale8h(x, mul));
       }
     }
+    if (w == 0) {
 #pragma unroll
-    for (int is = 0; is < C::IS; ++is) {
-      if (soff[is] < 0) continue;
-      const int u = is * kThreads + tid;
-      sL[u] = pl[is] * kLog2e;
-      sD[u] = -pd[is];
+      for (int is = 0; is < C::IS; ++is) {
+        if (soff[is] < 0) continue;
+        const int u = is * kThreads + tid;
+        sL[u] = pl[is] * kLog2e;
+        sD[u] = -pd[is];
+      }
     }
   };
 
@@ -550,14 +569,16 @@ __global__ void __launch_bounds__(64 * ZK, 1) na3d_bwd_dkdv_d128_kernel(Args a) 
   const int trow = 4 * g + (qn >> 2);
   const uint32_t toff = trow * kRow + ((((qn >> 1) & 1) ^ rswz(trow)) << 4) + 8 * (qn & 1);
 
-  auto compute = [&]() {
-    for (int st = 0; st < npairs; ++st) {
+  auto compute = [&](int w) {
+    const int st0 = w * (C::RW / 32), st1 = min(npairs, st0 + C::RW / 32);
+    for (int st = st0; st < st1; ++st) {
       f32x4 x[2], y[2];
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
-        const int c = 2 * st + h;
-        const char* rq = tQ + c * (16 * kRow);
-        const char* rg = tG + c * (16 * kRow);
+        const int c = 2 * st + h;                 // chunk of the box (mask, LSE, D)
+        const int cl = 2 * (st - st0) + h;        // chunk of the staged window
+        const char* rq = tQ + cl * (16 * kRow);
+        const char* rg = tG + cl * (16 * kRow);
         const int u4 = 16 * c + 4 * g;
         const float4 l4 = *reinterpret_cast<const float4*>(sL + u4);
         const float4 d4 = *reinterpret_cast<const float4*>(sD + u4);
@@ -574,6 +595,10 @@ __global__ void __launch_bounds__(64 * ZK, 1) na3d_bwd_dkdv_d128_kernel(Args a) 
           const bf16x8 ga = __builtin_bit_cast(bf16x8, ld16(rg + (aoff ^ (64u * kk))));
           xs = __builtin_amdgcn_mfma_f32_16x16x32_f16(qa, kf[kk], xs, 0, 0, 0);
           ys = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ga, vf[kk], ys, 0, 0, 0);
+          if constexpr (LO) {
+            const bf16x8 la = __builtin_bit_cast(bf16x8, ld16(tL + cl * (16 * kRow) + (aoff ^ (64u * kk))));
+            ys = __builtin_amdgcn_mfma_f32_16x16x32_bf16(la, vf[kk], ys, 0, 0, 0);
+          }
         }
         x[h] = xs;
         y[h] = ys;
@@ -604,8 +629,8 @@ __global__ void __launch_bounds__(64 * ZK, 1) na3d_bwd_dkdv_d128_kernel(Args a) 
       }
       const bf16x8 pf = __builtin_bit_cast(bf16x8, make_uint4(pb[0][0], pb[0][1], pb[1][0], pb[1][1]));
       const f16x8 df = __builtin_bit_cast(f16x8, make_uint4(db[0][0], db[0][1], db[1][0], db[1][1]));
-      const char* tq0 = tQ + st * (32 * kRow);
-      const char* tg0 = tG + st * (32 * kRow);
+      const char* tq0 = tQ + (st - st0) * (32 * kRow);
+      const char* tg0 = tG + (st - st0) * (32 * kRow);
 #pragma unroll
       for (int t = 0; t < 8; ++t) {
         const uint32_t o0 = toff ^ (32u * t);
@@ -613,6 +638,13 @@ __global__ void __launch_bounds__(64 * ZK, 1) na3d_bwd_dkdv_d128_kernel(Args a) 
         const uint2 g_hi = __builtin_bit_cast(uint2, tr_read(tg0 + 16 * kRow + o0));
         const bf16x8 gt = __builtin_bit_cast(bf16x8, make_uint4(g_lo.x, g_lo.y, g_hi.x, g_hi.y));
         accV[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gt, pf, accV[t], 0, 0, 0);
+        if constexpr (LO) {
+          const char* tl0 = tL + (st - st0) * (32 * kRow);
+          const uint2 l_lo = __builtin_bit_cast(uint2, tr_read(tl0 + o0));
+          const uint2 l_hi = __builtin_bit_cast(uint2, tr_read(tl0 + 16 * kRow + o0));
+          const bf16x8 lt = __builtin_bit_cast(bf16x8, make_uint4(l_lo.x, l_lo.y, l_hi.x, l_hi.y));
+          accV[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lt, pf, accV[t], 0, 0, 0);
+        }
         const uint2 q_lo = __builtin_bit_cast(uint2, tr_read(tq0 + o0));
         const uint2 q_hi = __builtin_bit_cast(uint2, tr_read(tq0 + 16 * kRow + o0));
         const f16x8 qt = __builtin_bit_cast(f16x8, make_uint4(q_lo.x, q_lo.y, q_hi.x, q_hi.y));
@@ -628,13 +660,15 @@ __global__ void __launch_bounds__(64 * ZK, 1) na3d_bwd_dkdv_d128_kernel(Args a) 
   // query levels that see the block's key levels, one at a time
   const int zk_last = min(z0 + ZK, Z) - 1;
   const int p_lo = inv_lo(z0, KZ), p_hi = inv_hi(zk_last, Z, KZ);
-  for (int p = p_lo; p <= p_hi; ++p) {
-    issue(p);
-    finish();
-    __syncthreads();  // the level is published
-    if (active(p)) compute();
-    __syncthreads();  // every read of the level is done before the next copy
-  }
+  const int nwin = (npairs * 32 + C::RW - 1) / C::RW;
+  for (int p = p_lo; p <= p_hi; ++p)
+    for (int w = 0; w < nwin; ++w) {
+      issue(p, w);
+      finish(w);
+      __syncthreads();  // the window is published
+      if (active(p)) compute(w);
+      __syncthreads();  // every read of the window is done before the next copy
+    }
 
   // dV, and dK = R^T (scale 2^(E-15) dK~); the lane holds d = 16t + 4g + i.
   // With QK RMSNorm that is the gradient of k^ = r k, carried back through the
@@ -746,10 +780,9 @@ bool launch_na3d_bwd_dq_d128(const strata_na3d_desc& d, const BwdOpts& o, const 
 bool launch_na3d_bwd_dkdv_d128(const strata_na3d_desc& d, const BwdOpts& o, const void* q, const void* k,
                                const void* v, const float* cs, const void* dout, const float* lse,
                                const float* dvec, void* dk, void* dv, hipStream_t s) {
-  // a two-term upstream gradient would need a third 64 KB staged tile: plain kernel
-  if (!supported(d) || o.dout_lo) return false;
+  if (!supported(d)) return false;
   constexpr int ZK = 8;
-  using C = KvCfg<9, 9, 9, ZK>;
+  using C = KvCfg<9, 9, 9, ZK, false>;
   if (max_box(d.H, 9) > C::MQY || max_box(d.W, 9) > C::MQX) return false;
   Args a = make_args(d, q, k, v, cs, dout, lse, dvec);
   a.dk = static_cast<uint16_t*>(dk);
@@ -760,11 +793,16 @@ bool launch_na3d_bwd_dkdv_d128(const strata_na3d_desc& d, const BwdOpts& o, cons
   a.n_xb = (d.W + 3) / 4;
   const int64_t blocks = (int64_t)d.B * d.heads * a.n_zb * a.n_yb * a.n_xb;
   if (blocks >= (int64_t)1 << 31) return false;
-  if (o.qk_norm)
-    hipLaunchKernelGGL((na3d_bwd_dkdv_d128_kernel<9, 9, 9, ZK, true>), dim3((unsigned)blocks), dim3(C::kThreads), 0, s, a);
+  a.dout_lo = static_cast<const uint16_t*>(o.dout_lo);
+  const dim3 grid((unsigned)blocks), block(C::kThreads);
+  if (o.qk_norm && o.dout_lo)
+    hipLaunchKernelGGL((na3d_bwd_dkdv_d128_kernel<9, 9, 9, ZK, true, true>), grid, block, 0, s, a);
+  else if (o.qk_norm)
+    hipLaunchKernelGGL((na3d_bwd_dkdv_d128_kernel<9, 9, 9, ZK, true, false>), grid, block, 0, s, a);
+  else if (o.dout_lo)
+    hipLaunchKernelGGL((na3d_bwd_dkdv_d128_kernel<9, 9, 9, ZK, false, true>), grid, block, 0, s, a);
   else
-    hipLaunchKernelGGL((na3d_bwd_dkdv_d128_kernel<9, 9, 9, ZK, false>), dim3((unsigned)blocks), dim3(C::kThreads), 0, s,
-                       a);
+    hipLaunchKernelGGL((na3d_bwd_dkdv_d128_kernel<9, 9, 9, ZK, false, false>), grid, block, 0, s, a);
   return true;
 }
 
