@@ -380,6 +380,19 @@ def paper_shapes(steps: int) -> dict:
             entry["bwd"] = dict(roofline_row(fl, nb, ms), ms=round(ms, 4),
                                 pct_bf16_peak=round(100 * fl / ms / 1e9 / PEAK_BF16_TFLOPS, 2))
             del ws, dq, dk, dv
+        if wl is I.PAPER_DECODER:
+            # the production attention block (App. B.5): QK RMSNorm and a per-channel gate
+            gt = torch.randn(wl.shape(), generator=gen, device=dev).to(torch.bfloat16)
+            opts = Bd.make_opts(True, 1e-6, gt)
+            ms = _timed(lambda: Bd.strata_na3d_fwd_ex(desc, opts, q, k, v, cs, out, lse), steps)
+            entry["fwd_norm_gate_d"] = dict(roofline_row(4.0 * n * wl.K * wl.d, n * (5 * wl.d * 2 + 4), ms),
+                                            ms=round(ms, 4))
+            ws = torch.empty(Bd.strata_na3d_bwd_ex_workspace_size(desc, opts), dtype=torch.uint8, device=dev)
+            dq, dk, dv, dg = (torch.empty_like(q) for _ in range(4))
+            ms = _timed(lambda: Bd.strata_na3d_bwd_ex(desc, opts, q, k, v, cs, out, g, lse, dq, dk, dv, dg, ws), steps)
+            entry["bwd_norm_gate_d"] = dict(roofline_row(10.0 * n * wl.K * wl.d, n * (10 * wl.d * 2 + 4), ms),
+                                            ms=round(ms, 4))
+            del gt, ws, dq, dk, dv, dg
         res[wl.name] = entry
         del q, k, v, g, out, lse, cs
         torch.cuda.empty_cache()
@@ -629,6 +642,10 @@ def main():
         res["rows"]["f2_na3d_fwd_w999_paper_tile16"] = ps[I.PAPER_TILE16.name]["fwd"]
         res["rows"]["f2_na3d_bwd_w999_paper_tile16"] = ps[I.PAPER_TILE16.name]["bwd"]
         res["rows"]["f2_column_fwd_paper"] = ps[I.PAPER_COLUMN.name]["fwd"]
+        res["rows"]["f2_na3d_fwd_d128_decoder"] = ps[I.PAPER_DECODER.name]["fwd"]
+        res["rows"]["f2_na3d_bwd_d128_decoder"] = ps[I.PAPER_DECODER.name]["bwd"]
+        res["rows"]["f1_f2_decoder_norm_gate_fwd"] = ps[I.PAPER_DECODER.name]["fwd_norm_gate_d"]
+        res["rows"]["f1_f2_decoder_norm_gate_bwd"] = ps[I.PAPER_DECODER.name]["bwd_norm_gate_d"]
         _done("paper shapes", t_start)
         torch.cuda.empty_cache()
         res["rows"]["f4_wind_tile_frame_face"] = wind_frame(a.train_steps)
