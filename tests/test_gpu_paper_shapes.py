@@ -297,7 +297,8 @@ def test_d128_w999_fwd_decoder_full_size_sampled():
     check_fwd(r, (wl.kz, wl.ky, wl.kx), "bf16", False, sel=sel)
 
 
-@pytest.mark.parametrize("shape,rope", [((1, 1, 12, 16, 16, 128), True), ((1, 1, 11, 13, 17, 128), False)])
+@pytest.mark.parametrize("shape,rope", [((1, 1, 12, 16, 16, 128), True), ((1, 1, 11, 13, 17, 128), False),
+                                        ((2, 2, 10, 12, 12, 128), True)])
 def test_d128_w999_bwd_sampled_keys(shape, rope):
     """The head_dim-128 MFMA backward: dq of every query, dk and dv of sampled
     keys (corners included) against the oracle."""
