@@ -11,17 +11,21 @@
 //               K and V of the (8+ky-1) x (8+kx-1) key box of a level are copied
 //               global -> LDS by the direct-to-LDS load (no registers), one level
 //               ahead of the compute, into a double buffer; each thread then
-//               rotates the K pieces its own copies brought (StereoRoPE) and
-//               rounds them to float16, and one barrier publishes the level.
+//               rotates the K pieces its own copies brought (StereoRoPE, in
+//               packed float16 with float16 phases, staged in LDS when they
+//               fit, else converted from the float32 table) and one barrier
+//               publishes the level.
 //
 // Per (query level, key level) a wave multiplies the keys of its 4x4 sub-block's
 // box -- (3+ky) x (3+kx) keys, in 16-key chunks -- with its 16 queries:
 //   S^T (16 keys x 16 queries) = K . Q^T     v_mfma_f32_16x16x32_f16, the
 //                                           accumulator seeded with the window
 //                                           mask (0 or -inf),
-//   online softmax on S^T in registers (a lane owns one query column); the
-//   running maximum only moves when it grows by more than 2^8, so most steps
-//   rescale nothing; cross-row maxima use v_permlane16/32_swap,
+//   online softmax on S^T in registers (a lane owns one query column) against
+//   a lazy reference m: it starts at 0 and moves only when a logit exceeds it
+//   by more than 2^8 (or, on a query level's first key level, when no logit
+//   reaches -2^6), so most steps rescale nothing and, while m is 0 across the
+//   wave, subtract nothing; cross-row maxima use v_permlane16/32_swap,
 //   O^T (64 d x 16 queries) += V^T . P^T    bf16 MFMA; V^T fragments come from
 //                                           the row-major V tile through the LDS
 //                                           transpose read, P^T is the S^T
@@ -78,7 +82,8 @@ constexpr int kVRow = 160;       // LDS bytes per key row of V (128 + 32 pad)
 constexpr int kLdsMax = 160 * 1024;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
-constexpr float kLazy = 8.0f;    // rescale only when the maximum grows by > 2^8
+constexpr float kLazy = 8.0f;    // move the softmax reference only when a logit exceeds it by > 2^8
+constexpr float kLow = -64.0f;   // ... or down, on a level's first key level
 constexpr int kMinExp = -100;    // lower bound of the dS exponent (keeps 2^(15-E) finite)
 
 template <int KZ, int KY, int KX, int ZQ>
@@ -288,10 +293,12 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
       if (csb) {
         if (C::PH_LDS) {
           x = rotate8h_pk(x, ld16(sph + (it * kThreads + tid) * 16), mul);
-        } else {
+        } else {  // the same float16 phases, converted here (|cos|, |sin| <= 1: no saturation)
           const int o = goffK(it);
           const float4* pp = csb + (o >> 6) * 16 + ((o & 63) >> 2);
-          x = rotate8h(x, pp[0], pp[1], mul);
+          const float4 p0 = pp[0], p1 = pp[1];
+          x = rotate8h_pk(x, make_uint4(pack2h_rne(p0.x, p0.y), pack2h_rne(p0.z, p0.w), pack2h_rne(p1.x, p1.y),
+                                        pack2h_rne(p1.z, p1.w)), mul);
         }
       } else {
         x = scale8h(x, mul);
@@ -308,6 +315,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
   bf16x8 gf[BWD ? C::QL : 1][2], gl[LO ? C::QL : 1][2];  // dO (hi and low terms)
   float rq[BWD && NORM ? C::QL : 1];                     // QK RMSNorm factor of the query
   float m[C::QL], l[C::QL];
+  bool mset[C::QL];  // forward, wave-uniform: the reference m has moved from 0 somewhere in the wave
   int ex[C::QL];
   f32x4 o[C::QL][4];
   const float4* csq = csb ? csb + ((int64_t)qy * W + qx) * 16 : nullptr;
@@ -346,15 +354,17 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
       l[j] = -a.dvec[tok];            // -D
       ex[j] = kMinExp;
     } else {
-      m[j] = -INFINITY;
+      m[j] = 0.f;
       l[j] = 0.f;
+      mset[j] = false;
     }
 #pragma unroll
     for (int t = 0; t < 4; ++t) o[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  // one (query level j, key level) update with the key tiles tk, tv
-  auto update = [&](int j, const char* tk, const char* tv) {
+  // one (query level j, key level) update with the key tiles tk, tv; `first`:
+  // the query level's first key level (nothing accumulated yet)
+  auto update = [&](int j, bool first, const char* tk, const char* tv) {
     f32x4 s[C::NC];
 #pragma unroll
     for (int c = 0; c < C::NC; ++c) {
@@ -372,21 +382,33 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
       mx = fmaxf(fmaxf(mx, s[c][2]), s[c][3]);
     }
     mx = max_over_rows(mx);
-    if (__any(mx > m[j] + kLazy)) {  // rare: move the running maximum, rescale
-      const float mn = fmaxf(m[j], mx);
-      const float alpha = __builtin_amdgcn_exp2f(m[j] - mn);
-      m[j] = mn;
-      l[j] *= alpha;
+    // the reference m starts at 0 and moves when a logit exceeds it by more
+    // than 2^kLazy, or when a query level's first key level has no logit above
+    // kLow (nothing is accumulated yet); while it is 0 across the wave no
+    // subtraction is needed
+    const bool move = mx > m[j] + kLazy || (first && mx < kLow);
+    if (__any(move)) {  // rare: move the reference, rescale
+      const float mn = move ? mx : m[j];
+      if (!first) {  // nothing is accumulated before the first key level (and a downward
+                     // move there would make the factor overflow)
+        const float alpha = __builtin_amdgcn_exp2f(m[j] - mn);
+        l[j] *= alpha;
 #pragma unroll
-      for (int t = 0; t < 4; ++t) o[j][t] *= alpha;
+        for (int t = 0; t < 4; ++t) o[j][t] *= alpha;
+      }
+      m[j] = mn;
+      mset[j] = true;
     }
-    const float mj = m[j];
+    if (mset[j]) {
+#pragma unroll
+      for (int c = 0; c < C::NC; ++c) s[c] -= m[j];
+    }
     uint32_t pk[C::NC][2];
     float ls = l[j];
 #pragma unroll
     for (int c = 0; c < C::NC; ++c) {
-      pk[c][0] = pack2(__builtin_amdgcn_exp2f(s[c][0] - mj), __builtin_amdgcn_exp2f(s[c][1] - mj));
-      pk[c][1] = pack2(__builtin_amdgcn_exp2f(s[c][2] - mj), __builtin_amdgcn_exp2f(s[c][3] - mj));
+      pk[c][0] = pack2(__builtin_amdgcn_exp2f(s[c][0]), __builtin_amdgcn_exp2f(s[c][1]));
+      pk[c][1] = pack2(__builtin_amdgcn_exp2f(s[c][2]), __builtin_amdgcn_exp2f(s[c][3]));
       ls = psum8(pk[c][0], pk[c][1], ls);
     }
     l[j] = ls;
@@ -474,7 +496,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
       const int zs = win_start(zq, Z, KZ);
       if (p < zs || p >= zs + KZ) continue;
       if constexpr (BWD) update_dq(j, tk, tv);
-      else update(j, tk, tv);
+      else update(j, p == zs, tk, tv);
     }
   };
 
