@@ -194,9 +194,11 @@ __global__ void __launch_bounds__(kQThreads, 1) na3d_bwd_dq_d128_kernel(Args a) 
       uint4 x = ld16(ad);
       // (a key row is 16 consecutive slots, all in the tile)
       const float mul = NORM ? __builtin_amdgcn_rsqf(sum_over_16_lanes(sumsq8(x, 0.f)) * (1.f / kD) + a.eps) : 1.f;
-      if (csb) {
+      if (csb) {  // packed float16 rotation, phases converted from the float32 table
         const float4* pp = csb + (o >> 7) * kCS4 + ((o & 127) >> 2);
-        x = rotate8h(x, pp[0], pp[1], mul);
+        const float4 p0 = pp[0], p1 = pp[1];
+        x = rotate8h_pk(x, make_uint4(pack2h_rne(p0.x, p0.y), pack2h_rne(p0.z, p0.w), pack2h_rne(p1.x, p1.y),
+                                      pack2h_rne(p1.z, p1.w)), mul);
       } else {
         x = scale8h(x, mul);
       }
@@ -506,9 +508,11 @@ __global__ void __launch_bounds__(64 * ZK, 1) na3d_bwd_dkdv_d128_kernel(Args a) 
       const uint4 x = ld16(ad);
       // (a query row is 16 consecutive slots, all in or all past the box)
       const float mul = NORM ? __builtin_amdgcn_rsqf(sum_over_16_lanes(sumsq8(x, 0.f)) * (1.f / kD) + a.eps) : 1.f;
-      if (csb) {
+      if (csb) {  // packed float16 rotation, phases converted from the float32 table
         const float4* pp = csb + (o >> 7) * kCS4 + ((o & 127) >> 2);
-        st16(ad, rotate8h(x, pp[0], pp[1], mul));
+        const float4 p0 = pp[0], p1 = pp[1];
+        st16(ad, rotate8h_pk(x, make_uint4(pack2h_rne(p0.x, p0.y), pack2h_rne(p0.z, p0.w), pack2h_rne(p1.x, p1.y),
+                                           pack2h_rne(p1.z, p1.w)), mul));
       } else {
         st16(ad, scale8h(x, mul));
       }

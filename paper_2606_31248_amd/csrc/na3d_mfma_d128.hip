@@ -10,8 +10,9 @@
 //   S^T (16 keys x 16 queries) = K . Q^T   four 16x16x32 float16 MFMAs per
 //                                          16-key chunk (128 = 4 x 32), the
 //                                          accumulator seeded with the mask;
-//   online softmax with a lazy maximum (rescale only past 2^8 growth), row
-//   sums of the packed bf16 weights by v_dot2c;
+//   online softmax against a lazy reference (from 0; it moves only past 2^8
+//   growth, or below -2^6 on the first key level), row sums of the packed
+//   bf16 weights by v_dot2c;
 //   O^T (128 d x 16 queries) += V^T . P^T  eight 16-row bf16 MFMA tiles, V^T
 //                                          fragments from the LDS transpose
 //                                          read.
@@ -19,8 +20,9 @@
 // float16 K (256-byte rows, 16-byte columns XOR-swizzled as for head_dim 64)
 // and 72 KB of bf16 V (288-byte rows: 256 + a 32-byte pad that spreads the
 // transpose reads), so the tiles are single-buffered: each key level is copied
-// (direct to LDS), rotated in place by the thread whose copies brought it --
-// phases read from the float32 table, which stays in the L2 -- published by a
+// (direct to LDS), rotated in place in packed float16 by the thread whose
+// copies brought it -- phases converted from the float32 table, which stays
+// in the L2 -- published by a
 // barrier, computed, and retired by a second barrier before the next copy.
 // The rotated Q and K are float16 (logit scale and log2(e) folded into Q); P
 // and V are bf16.  Options (App. B.5): QK RMSNorm scales each query and key by
@@ -46,7 +48,8 @@ constexpr int kVRow = 288;  // LDS bytes per key row of V (256 + 32 pad)
 constexpr int kCS4 = kD / 4;  // float4 entries of the phase table per position (two pairs each)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
-constexpr float kLazy = 8.0f;
+constexpr float kLazy = 8.0f;   // move the softmax reference only when a logit exceeds it by > 2^8
+constexpr float kLow = -64.0f;  // ... or down, on a level's first key level
 
 template <int KZ, int KY, int KX, int ZQ>
 struct Cfg {
@@ -177,9 +180,11 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_d128_kernel(Args a) {
       uint4 x = ld16(ad);
       // (a key row is 16 consecutive slots, all in the tile: every lane of the row takes part)
       const float mul = NORM ? __builtin_amdgcn_rsqf(sum_over_16_lanes(sumsq8(x, 0.f)) * (1.f / kD) + a.eps) : 1.f;
-      if (csb) {
-        const float4* pp = csb + (o >> 7) * kCS4 + ((o & 127) >> 2);  // pairs 4c..4c+3 of the key's position
-        x = rotate8h(x, pp[0], pp[1], mul);
+      if (csb) {  // packed float16 rotation, phases of pairs 4c..4c+3 of the key's position
+        const float4* pp = csb + (o >> 7) * kCS4 + ((o & 127) >> 2);
+        const float4 p0 = pp[0], p1 = pp[1];
+        x = rotate8h_pk(x, make_uint4(pack2h_rne(p0.x, p0.y), pack2h_rne(p0.z, p0.w), pack2h_rne(p1.x, p1.y),
+                                      pack2h_rne(p1.z, p1.w)), mul);
       } else {
         x = scale8h(x, mul);
       }
@@ -190,6 +195,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_d128_kernel(Args a) {
   // ---- queries: load, rotate, scale (float16 B operands of K.Q^T) ----------
   f16x8 qf[C::QL][4];
   float m[C::QL], l[C::QL];
+  bool mset[C::QL];  // wave-uniform: the reference m has moved from 0 somewhere in the wave
   f32x4 o[C::QL][8];
   const float4* csq = csb ? csb + ((int64_t)qy * W + qx) * kCS4 : nullptr;
 #pragma unroll
@@ -212,14 +218,16 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_d128_kernel(Args a) {
       const uint4 r = csq ? rotate8h(x[kk], csq[8 * kk + 2 * g], csq[8 * kk + 2 * g + 1], mul) : scale8h(x[kk], mul);
       qf[j][kk] = __builtin_bit_cast(f16x8, r);
     }
-    m[j] = -INFINITY;
+    m[j] = 0.f;
     l[j] = 0.f;
+    mset[j] = false;
 #pragma unroll
     for (int t = 0; t < 8; ++t) o[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  // one (query level j, key level) update from the staged tiles
-  auto update = [&](int j) {
+  // one (query level j, key level) update from the staged tiles; `first`: the
+  // query level's first key level (nothing accumulated yet)
+  auto update = [&](int j, bool first) {
     f32x4 s[C::NC];
 #pragma unroll
     for (int c = 0; c < C::NC; ++c) {
@@ -235,21 +243,30 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_d128_kernel(Args a) {
 #pragma unroll
     for (int c = 1; c < C::NC; ++c) mx = fmaxf(fmaxf(mx, fmaxf(s[c][0], s[c][1])), fmaxf(s[c][2], s[c][3]));
     mx = max_over_rows(mx);
-    if (__any(mx > m[j] + kLazy)) {  // rare: move the running maximum, rescale
-      const float mn = fmaxf(m[j], mx);
-      const float alpha = __builtin_amdgcn_exp2f(m[j] - mn);
-      m[j] = mn;
-      l[j] *= alpha;
+    // lazy reference: starts at 0, moves past 2^kLazy growth or, on the first
+    // key level, below kLow; while 0 across the wave nothing is subtracted
+    const bool move = mx > m[j] + kLazy || (first && mx < kLow);
+    if (__any(move)) {  // rare: move the reference, rescale
+      const float mn = move ? mx : m[j];
+      if (!first) {  // nothing accumulated before the first key level
+        const float alpha = __builtin_amdgcn_exp2f(m[j] - mn);
+        l[j] *= alpha;
 #pragma unroll
-      for (int t = 0; t < 8; ++t) o[j][t] *= alpha;
+        for (int t = 0; t < 8; ++t) o[j][t] *= alpha;
+      }
+      m[j] = mn;
+      mset[j] = true;
     }
-    const float mj = m[j];
+    if (mset[j]) {
+#pragma unroll
+      for (int c = 0; c < C::NC; ++c) s[c] -= m[j];
+    }
     uint32_t pk[C::NC][2];
     float ls = l[j];
 #pragma unroll
     for (int c = 0; c < C::NC; ++c) {
-      pk[c][0] = pack2(__builtin_amdgcn_exp2f(s[c][0] - mj), __builtin_amdgcn_exp2f(s[c][1] - mj));
-      pk[c][1] = pack2(__builtin_amdgcn_exp2f(s[c][2] - mj), __builtin_amdgcn_exp2f(s[c][3] - mj));
+      pk[c][0] = pack2(__builtin_amdgcn_exp2f(s[c][0]), __builtin_amdgcn_exp2f(s[c][1]));
+      pk[c][1] = pack2(__builtin_amdgcn_exp2f(s[c][2]), __builtin_amdgcn_exp2f(s[c][3]));
       ls = psum8(pk[c][0], pk[c][1], ls);
     }
     l[j] = ls;
@@ -285,7 +302,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_d128_kernel(Args a) {
       if (zq >= Z) continue;
       const int zs = win_start(zq, Z, KZ);
       if (p < zs || p >= zs + KZ) continue;
-      update(j);
+      update(j, p == zs);
     }
     __syncthreads();  // every read of the level is done before the next copy
   }

@@ -368,3 +368,27 @@ def test_d128_w999_bwd_options_sampled_keys(qk_norm, gkind):
     rq = oracle.na3d_bwd(w(q), w(k), w(v), w(r["dout"]), window, r["scale"], coords=r["c32"],
                          selk=np.array([0]), qk_norm=qk_norm, gate=w(g))[0]
     check_close(host_f64(r["grads"][0]), rq, "bf16", "dq (all)")
+
+
+@pytest.mark.parametrize("sign", [-1.0, 1.0])
+def test_d128_w999_fwd_uniform_extreme_logits(sign):
+    """Every logit equal and 200 (log2 units) from zero at head_dim 128: the lazy
+    softmax reference must move (down on the first key level, or up) without
+    overflow; the output is the window mean of V, the LSE logit + ln K."""
+    shape = (1, 1, 10, 12, 12, 128)
+    scale = 1.0 / np.sqrt(128.0)
+    logit = sign * 200.0 / 1.4426950408889634
+    alpha = logit / (128 * scale)
+    q = I.f32_to_bf16_bits(np.full(shape, alpha, np.float32))
+    k = I.f32_to_bf16_bits(np.ones(shape, np.float32))
+    v = I.gaussian(shape, 90, 2, "bf16")
+    qd, kd, vd = (dev_tensor(a, "bf16") for a in (q, k, v))
+    out = torch.empty_like(qd)
+    lse = torch.empty(shape[:-1], dtype=torch.float32, device="cuda")
+    B.strata_na3d_fwd(B.desc_for(qd, (9, 9, 9), scale), qd, kd, vd, None, out, lse)
+    torch.cuda.synchronize()
+    ro, rl = oracle.na3d_fwd(*(oracle.widen(a, "bf16") for a in (q, k, v)), (9, 9, 9), scale)
+    got = host_f64(out)
+    assert np.isfinite(got).all()
+    check_close(got, ro, "bf16", "out")
+    assert np.max(np.abs(host_f64(lse) - rl)) <= LSE_ABS_BF16 + 2.0 ** -10 * float(np.max(np.abs(rl)))
