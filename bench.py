@@ -41,9 +41,11 @@ STATS_FILE = os.path.join(ROOT, "profiles", "face_rollout_step_kernel_stats.txt"
 SQ_FILE = os.path.join(ROOT, "profiles", "na3d_fwd_face_rollout_sq_counters.json")
 # the sources of the kernel that strata_na3d_fwd runs at the face-rollout shape
 KERNEL_SOURCES = ["paper_2606_31248_amd/csrc/na3d_fwd_zs.hip", "paper_2606_31248_amd/csrc/mfma_util.h",
-                  "paper_2606_31248_amd/csrc/common.h"]
-FWD_KERNEL = "na3d_fwd_zs_kernel"
-BLEND_KERNEL = "tile_blend_bf16_kernel"
+                  "paper_2606_31248_amd/csrc/common.h", "paper_2606_31248_amd/csrc/blend.hip"]
+# the face step: the forward with the stitch of single-cover cells fused into its
+# store, then the stitch of the overlap cells
+FWD_KERNEL = "na3d_fwd_zs_kernel<8, false, false, true>"
+BLEND_KERNEL = "tile_blend_overlap_bf16_kernel"
 COPY_KERNEL = "copyBuffer"
 CALIB_BYTES = 1 << 30
 
@@ -104,11 +106,11 @@ def summarize_pmc(fetch_dir: str, write_dir: str, commands) -> dict:
     cf, cw = pick(fe, COPY_KERNEL, np.max), pick(wr, COPY_KERNEL, np.max)
     ff, fw = CALIB_BYTES / (cf * 1024), CALIB_BYTES / (cw * 1024)
     wl_alg = 4.0 * 81 * 16 * 8 * 64 * 64 * 64 * 2
-    blend_alg = (81 * 128 * 64 * 64 * 64 + 128 * 512 * 512 * 64) * 2
+    blend_alg = overlap_stitch_bytes(9, 9, 64, 64, 56, 56, 128, 64)
     fwd_f, fwd_w = pick(fe, FWD_KERNEL), pick(wr, FWD_KERNEL)
     bl_f, bl_w = pick(fe, BLEND_KERNEL), pick(wr, BLEND_KERNEL)
     return {
-        "kernel": f"strata_na3d_fwd ({FWD_KERNEL}<8, false, false>: no options)",
+        "kernel": f"strata_na3d_fwd_stitch ({FWD_KERNEL}: no options)",
         "workload": "face_rollout_81x16x8x64x64_d64_w3x7x7",
         "kernel_source_hash": kernel_source_hash(),
         "fetch_kb_per_launch": fwd_f,
@@ -117,7 +119,7 @@ def summarize_pmc(fetch_dir: str, write_dir: str, commands) -> dict:
                              "fetch_factor": ff, "write_factor": fw},
         "hbm_bytes_per_launch": fwd_f * 1024 * ff + fwd_w * 1024 * fw,
         "alg_bytes_per_launch": wl_alg,
-        "blend": {"fetch_kb": bl_f, "write_kb": bl_w, "hbm_bytes_per_launch": bl_f * 1024 * ff + bl_w * 1024 * fw,
+        "blend": {"kernel": f"strata_tile_blend_overlap ({BLEND_KERNEL})", "fetch_kb": bl_f, "write_kb": bl_w, "hbm_bytes_per_launch": bl_f * 1024 * ff + bl_w * 1024 * fw,
                   "alg_bytes_per_launch": blend_alg},
         "commands": list(commands),
         "note": "Traffic = FETCH_SIZE * fetch_factor + WRITE_SIZE * write_factor, per dispatch; the factors "
@@ -139,7 +141,7 @@ def summarize_sq(run_dir: str, commands) -> dict:
         raise SystemExit(f"no dispatch of {FWD_KERNEL} in the counter run")
     med = {c: float(np.median(v)) for c, v in acc.items()}
     flops_alg = 4.0 * 81 * 16 * 8 * 64 * 64 * 147 * 64
-    rec = {"kernel": f"strata_na3d_fwd ({FWD_KERNEL}<8, false, false>: no options)",
+    rec = {"kernel": f"strata_na3d_fwd_stitch ({FWD_KERNEL}: no options)",
            "workload": "face_rollout_81x16x8x64x64_d64_w3x7x7",
            "kernel_source_hash": kernel_source_hash(),
            "counters_per_dispatch": med, "commands": list(commands)}
@@ -155,6 +157,17 @@ def summarize_sq(run_dir: str, commands) -> dict:
         if tr:
             rec["exp_per_mfma"] = tr / mf
     return rec
+
+
+def overlap_stitch_bytes(nty, ntx, Ht, Wt, sy, sx, P, C, elem=2) -> float:
+    """Algorithmic bytes of the overlap-only stitch: every tile value of a cell
+    covered by two or more tiles read once, every such face cell written once."""
+    Hf, Wf = (nty - 1) * sy + Ht, (ntx - 1) * sx + Wt
+    ny = np.array([sum(a * sy <= y < a * sy + Ht for a in range(nty)) for y in range(Hf)])
+    nx = np.array([sum(b * sx <= x < b * sx + Wt for b in range(ntx)) for x in range(Wf)])
+    cover = ny[:, None] * nx[None, :]
+    multi = (ny[:, None] > 1) | (nx[None, :] > 1)
+    return float((cover[multi].sum() + multi.sum()) * P * C * elem)
 
 
 def summarize_stats(stats_csv: str, command: str) -> str:
@@ -539,6 +552,7 @@ def main():
         del src, dst
 
     ev = {n: [] for n in ("coords", "na", "blend")}
+    planes = out.view(wl.B, wl.heads * wl.Z, wl.H, wl.W, wl.d)
 
     def step(record: bool):
         st = torch.cuda.current_stream()
@@ -550,10 +564,10 @@ def main():
         Bd.strata_stereorope_phases(coords, wl.d, Pp.ROPE_BASE, cs)
         if record:
             e[1].record(st)
-        Bd.strata_na3d_fwd(desc, q, k, v, cs, out, None)
+        Bd.strata_na3d_fwd_stitch(desc, None, q, k, v, cs, out, None, nty, ntx, sy, sx, win, face)
         if record:
             e[2].record(st)
-        Bd.strata_tile_blend(out.view(wl.B, wl.heads * wl.Z, wl.H, wl.W, wl.d), nty, ntx, sy, sx, win, face)
+        Bd.strata_tile_blend_overlap(planes, nty, ntx, sy, sx, win, face)
         if record:
             e[3].record(st)
             ev["coords"].append((e[0], e[1]))
@@ -577,7 +591,7 @@ def main():
     tflops_na = flops / (avg["na"] * 1e-3) / 1e12
     alg_bytes = 4.0 * wl.B * wl.heads * wl.N * wl.d * 2        # Q, K, V read + O write, bf16
     gbs_na = alg_bytes / (avg["na"] * 1e-3) / 1e9
-    blend_bytes = (wl.B * wl.heads * wl.Z * wl.H * wl.W * wl.d + wl.heads * wl.Z * Hf * Wf * wl.d) * 2
+    blend_bytes = overlap_stitch_bytes(nty, ntx, wl.H, wl.W, sy, sx, wl.heads * wl.Z, wl.d)
     traffic, pmc = stored_traffic(alg_bytes)
     tokens = wl.B * wl.N
 
@@ -596,7 +610,8 @@ def main():
         "data": "synthetic (seeded iid N(0,1) Q/K/V; analytic equiangular cubed-sphere tile geometry)",
         "config": {"workload": wl.name, "tiles": wl.B, "heads": wl.heads, "Z": wl.Z, "H": wl.H,
                    "W": wl.W, "head_dim": wl.d, "window": list(window), "face_tokens": [Hf, Wf],
-                   "tile_stride": [sy, sx], "overlap": I.FACE_OVERLAP, "blend_window": "linear ramp"},
+                   "tile_stride": [sy, sx], "overlap": I.FACE_OVERLAP, "blend_window": "linear ramp",
+                   "stitch": "fused: the forward stores the cells one tile covers, then the overlap-only stitch"},
         "tokens_per_s": round(tokens / (ms_step * 1e-3), 1),
         "face_tokens_per_s": round(wl.Z * Hf * Wf / (ms_step * 1e-3), 1),
         "pct_bf16_peak": round(100.0 * tflops_step / PEAK_BF16_TFLOPS, 2),
@@ -607,7 +622,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(gbs_na, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(gbs_na / PEAK_HBM_GBS, 4),
                      "traffic": None if traffic is None else float(traffic),
-                     "kernel": f"strata_na3d_fwd ({FWD_KERNEL})", "alg_bytes_per_launch": alg_bytes},
+                     "kernel": f"strata_na3d_fwd_stitch ({FWD_KERNEL})", "alg_bytes_per_launch": alg_bytes},
     }
     # every row of the hot path against the roofline that bounds it
     res["rows"] = {
@@ -618,6 +633,15 @@ def main():
                                "frac_hbm": round(blend_bytes / (avg["blend"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
     }
     if a.train_steps > 0:
+        # the same step without the fusion: every tile output written, then the whole stitch
+        full_bytes = (wl.B * wl.heads * wl.Z * wl.H * wl.W * wl.d + wl.heads * wl.Z * Hf * Wf * wl.d) * 2
+        na_plain = _timed(lambda: Bd.strata_na3d_fwd(desc, q, k, v, cs, out, None), a.train_steps)
+        bl_full = _timed(lambda: Bd.strata_tile_blend(planes, nty, ntx, sy, sx, win, face), a.train_steps)
+        res["face_step_unfused"] = {
+            "na3d_fwd_ms": round(na_plain, 4), "tile_blend_ms": round(bl_full, 4),
+            "tile_blend_gbs": round(full_bytes / (bl_full * 1e-3) / 1e9, 1),
+            "step_ms": round(avg["coords"] + na_plain + bl_full, 4)}
+        _done("unfused face step", t_start)
         # the attention-block options (App. B.5) on the same face forward
         opt = options_face_fwd(wl, desc, q, k, v, cs, out, a.train_steps)
         res["options"] = {"face_fwd": opt}

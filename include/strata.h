@@ -212,6 +212,39 @@ strata_status strata_tile_blend(const void* tiles, int32_t nty, int32_t ntx, int
                                 int32_t stride_x, const float* window, void* out, int32_t Hf,
                                 int32_t Wf, strata_dtype dtype, void* stream);
 
+/* ---- a4-a6 + a8: face step with the stitch fused into the forward ----------
+ * (Sec. 3.2 attention on each tile of one face, App. F, Eq. stitch.)  The
+ * batch of `desc` is the nty x ntx tiling of one face, tile t = a*ntx + b at
+ * origin (a*stride_y, b*stride_x), P = heads*Z planes, Ht = H, Wt = W,
+ * C = head_dim, window float32 [H*W] >= 0, face [heads*Z, Hf, Wf, head_dim]
+ * of the problem's dtype.  Two calls on one stream give
+ *   strata_tile_blend(strata_na3d_fwd_ex(...))      bit for bit:
+ * strata_na3d_fwd_stitch, then strata_tile_blend_overlap with the same tiles,
+ * tiling, window and face.  The first writes the attention output (options
+ * and lse as in strata_na3d_fwd_ex) and stores every cell that one tile alone
+ * covers straight into `face`: there the stitch returns the tile's value
+ * (w v / w), or 0 where w = 0, and -0 becomes +0 as the stitch's fused
+ * multiply-add from +0 makes it.  The other cells go to `tiles`
+ * ([B, heads, Z, H, W, head_dim], caller-owned scratch; the contents of
+ * single-cover cells are unspecified).  The second stitches the cells that two
+ * or more tiles cover and leaves the rest of the face as it is.  The fusion
+ * applies to bf16 tilings whose tiles cover the face with
+ * stride <= extent <= 2 stride on both axes, at the shape of the level-sweep
+ * forward (3x7x7, Z = 8, head_dim 64); elsewhere the first call writes every
+ * tile output and stitches the whole face, and the second re-stitches cells
+ * with the same values.  tiles, face and the inputs must not overlap.
+ * Validation as strata_na3d_fwd_ex and strata_tile_blend, plus B = nty*ntx.
+ * One or two kernel launches per call; nothing is allocated. */
+strata_status strata_na3d_fwd_stitch(const strata_na3d_desc* desc, const strata_na3d_opts* opts,
+                                     const void* q, const void* k, const void* v, const float* cs,
+                                     void* tiles, float* lse, int32_t nty, int32_t ntx,
+                                     int32_t stride_y, int32_t stride_x, const float* window,
+                                     void* face, int32_t Hf, int32_t Wf, void* stream);
+strata_status strata_tile_blend_overlap(const void* tiles, int32_t nty, int32_t ntx, int32_t P,
+                                        int32_t Ht, int32_t Wt, int32_t C, int32_t stride_y,
+                                        int32_t stride_x, const float* window, void* out,
+                                        int32_t Hf, int32_t Wf, strata_dtype dtype, void* stream);
+
 /* ---- Duo-grid halo padding P (App. F, "DUO-style boundary padding") --------
  * faces: [6, P, n, n, C] of dtype (P planes of n x n cells with C channels per
  * face, orientation as in strata_stereo_coords); padded: [6, P, n + 2 halo,

@@ -27,7 +27,7 @@ EXPORTS = (
     "strata_na3d_fwd_ex", "strata_na3d_bwd_ex_workspace_size", "strata_na3d_bwd_ex",
     "strata_tile_blend", "strata_tile_extract", "strata_na_axis_index", "strata_wind_tile_frame", "strata_kbd_window",
     "strata_duo_pad", "strata_duo_plan_bytes", "strata_duo_plan", "strata_duo_pad_planned",
-    "strata_duo_pad_vjp",
+    "strata_duo_pad_vjp", "strata_na3d_fwd_stitch", "strata_tile_blend_overlap",
     "strata_status_string", "strata_last_error",
 )
 
@@ -71,6 +71,7 @@ def load(path: str = LIB_PATH):
         "strata_na3d_fwd": [D, P, P, P, P, P, P, P],
         "strata_na3d_bwd": [D, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
         "strata_tile_blend": [P, i32, i32, i32, i32, i32, i32, i32, i32, P, P, i32, i32, st, P],
+        "strata_tile_blend_overlap": [P, i32, i32, i32, i32, i32, i32, i32, i32, P, P, i32, i32, st, P],
         "strata_tile_extract": [P, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32, P, st, P],
         "strata_na_axis_index": [i32, i32, P, P, P, P],
         "strata_wind_tile_frame": [P, i32, i32, i32, i32, i32, i32, i32, i32, i32, P, st, P],
@@ -87,6 +88,7 @@ def load(path: str = LIB_PATH):
     O = ctypes.POINTER(NA3DOpts)
     for name, args in {
         "strata_na3d_fwd_ex": [D, O, P, P, P, P, P, P, P],
+        "strata_na3d_fwd_stitch": [D, O, P, P, P, P, P, P, i32, i32, i32, i32, P, P, i32, i32, P],
         "strata_na3d_bwd_ex": [D, O, P, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
     }.items():
         f = getattr(L, name)
@@ -222,6 +224,23 @@ def strata_tile_blend(tiles, nty, ntx, stride_y, stride_x, window, out, stream=N
     _, Hf, Wf, _ = out.shape
     _check(load().strata_tile_blend(_ptr(tiles), nty, ntx, P, Ht, Wt, C, stride_y, stride_x,
                                     _ptr(window), _ptr(out), Hf, Wf, _dtype(tiles), _stream(stream)))
+
+
+def strata_tile_blend_overlap(tiles, nty, ntx, stride_y, stride_x, window, out, stream=None):
+    """Stitch of the face cells that two or more tiles cover (the second call of the fused face step)."""
+    T, P, Ht, Wt, C = tiles.shape
+    _, Hf, Wf, _ = out.shape
+    _check(load().strata_tile_blend_overlap(_ptr(tiles), nty, ntx, P, Ht, Wt, C, stride_y, stride_x,
+                                            _ptr(window), _ptr(out), Hf, Wf, _dtype(tiles), _stream(stream)))
+
+
+def strata_na3d_fwd_stitch(desc: NA3DDesc, opts: Optional[NA3DOpts], q, k, v, cs, tiles, lse, nty, ntx,
+                           stride_y, stride_x, window, face, stream=None):
+    """Forward of the nty x ntx tiles of one face, cells covered by one tile stored into face [heads*Z, Hf, Wf, d]."""
+    _, Hf, Wf, _ = face.shape
+    _check(load().strata_na3d_fwd_stitch(ctypes.byref(desc), _opts_ref(opts), _ptr(q), _ptr(k), _ptr(v), _ptr(cs),
+                                         _ptr(tiles), _ptr(lse), nty, ntx, stride_y, stride_x, _ptr(window),
+                                         _ptr(face), Hf, Wf, _stream(stream)))
 
 
 def strata_tile_extract(face, nty, ntx, stride_y, stride_x, tiles, stream=None):

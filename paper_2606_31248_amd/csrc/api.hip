@@ -105,6 +105,14 @@ static BwdLayout bwd_layout(const strata_na3d_desc& d, const NaOpts& o) {
   return L;
 }
 
+// the forward kernel for the problem's shape
+static void launch_fwd(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k, const void* v,
+                       const float* cs, void* out, float* lse, hipStream_t s) {
+  if (!launch_na3d_fwd_col(d, o, q, k, v, out, lse, s) && !launch_na3d_fwd_zs(d, o, q, k, v, cs, out, lse, s) &&
+      !launch_na3d_fwd_mfma(d, o, q, k, v, cs, out, lse, s) && !launch_na3d_fwd_d128(d, o, q, k, v, cs, out, lse, s))
+    launch_na3d_fwd_ref(d, o, q, k, v, cs, out, lse, s);
+}
+
 static strata_status na3d_fwd_impl(const strata_na3d_desc* desc, const strata_na3d_opts* opts,
                                    const void* q, const void* k, const void* v, const float* cs,
                                    void* out, float* lse, void* stream) {
@@ -119,12 +127,7 @@ static strata_status na3d_fwd_impl(const strata_na3d_desc* desc, const strata_na
   REQUIRE_PTR(out);
   if (cs) REQUIRE(aligned16(cs), "cs: not 16-byte aligned");
   if (lse) REQUIRE(aligned16(lse), "lse: not 16-byte aligned");
-  hipStream_t s = (hipStream_t)stream;
-  if (!launch_na3d_fwd_col(*desc, o, q, k, v, out, lse, s) &&
-      !launch_na3d_fwd_zs(*desc, o, q, k, v, cs, out, lse, s) &&
-      !launch_na3d_fwd_mfma(*desc, o, q, k, v, cs, out, lse, s) &&
-      !launch_na3d_fwd_d128(*desc, o, q, k, v, cs, out, lse, s))
-    launch_na3d_fwd_ref(*desc, o, q, k, v, cs, out, lse, s);
+  launch_fwd(*desc, o, q, k, v, cs, out, lse, (hipStream_t)stream);
   return check_launch(opts ? "strata_na3d_fwd_ex" : "strata_na3d_fwd");
 }
 
@@ -355,6 +358,71 @@ strata_status strata_tile_blend(const void* tiles, int32_t nty, int32_t ntx, int
   launch_tile_blend(tiles, nty, ntx, P, Ht, Wt, C, stride_y, stride_x, window, out, Hf, Wf, dtype,
                     (hipStream_t)stream);
   return check_launch("strata_tile_blend");
+}
+
+// A bf16 tiling whose overlap cells the overlap-only stitch handles: the tiles
+// cover the face, and no cell lies in more than two tiles along an axis.
+static bool overlap_form(int32_t nty, int32_t ntx, int32_t Ht, int32_t Wt, int32_t C, int32_t sy, int32_t sx,
+                         int32_t Hf, int32_t Wf, strata_dtype dt) {
+  return dt == STRATA_BF16 && C % 8 == 0 && sy <= Ht && Ht <= 2 * sy && sx <= Wt && Wt <= 2 * sx &&
+         (int64_t)(nty - 1) * sy + Ht == Hf && (int64_t)(ntx - 1) * sx + Wt == Wf;
+}
+
+strata_status strata_tile_blend_overlap(const void* tiles, int32_t nty, int32_t ntx, int32_t P, int32_t Ht,
+                                        int32_t Wt, int32_t C, int32_t stride_y, int32_t stride_x,
+                                        const float* window, void* out, int32_t Hf, int32_t Wf,
+                                        strata_dtype dtype, void* stream) {
+  strata_status st = check_tiling(nty, ntx, P, Ht, Wt, C, stride_y, stride_x, Hf, Wf, dtype);
+  if (st != STRATA_OK) return st;
+  REQUIRE_PTR(tiles);
+  REQUIRE_PTR(window);
+  REQUIRE_PTR(out);
+  REQUIRE((int64_t)Wf * C < ((int64_t)1 << 31) &&
+              (int64_t)P * Hf * (((int64_t)Wf * C + 255) / 256) < ((int64_t)1 << 31),
+          "tile_blend_overlap: face too large for one launch");
+  if (overlap_form(nty, ntx, Ht, Wt, C, stride_y, stride_x, Hf, Wf, dtype))
+    launch_tile_blend_overlap(tiles, nty, ntx, P, Ht, Wt, C, stride_y, stride_x, window, out, Hf, Wf,
+                              (hipStream_t)stream);
+  else
+    launch_tile_blend(tiles, nty, ntx, P, Ht, Wt, C, stride_y, stride_x, window, out, Hf, Wf, dtype,
+                      (hipStream_t)stream);
+  return check_launch("strata_tile_blend_overlap");
+}
+
+strata_status strata_na3d_fwd_stitch(const strata_na3d_desc* desc, const strata_na3d_opts* opts, const void* q,
+                                     const void* k, const void* v, const float* cs, void* tiles, float* lse,
+                                     int32_t nty, int32_t ntx, int32_t stride_y, int32_t stride_x,
+                                     const float* window, void* face, int32_t Hf, int32_t Wf, void* stream) {
+  strata_status st = check_desc(desc);
+  if (st != STRATA_OK) return st;
+  NaOpts o;
+  st = check_opts(desc, opts, o);
+  if (st != STRATA_OK) return st;
+  REQUIRE_PTR(q);
+  REQUIRE_PTR(k);
+  REQUIRE_PTR(v);
+  REQUIRE_PTR(tiles);
+  REQUIRE_PTR(window);
+  REQUIRE_PTR(face);
+  if (cs) REQUIRE(aligned16(cs), "cs: not 16-byte aligned");
+  if (lse) REQUIRE(aligned16(lse), "lse: not 16-byte aligned");
+  REQUIRE((int64_t)nty * ntx == desc->B, "fwd_stitch: the batch (%d tiles) is not the %d x %d tiling", desc->B,
+          nty, ntx);
+  const int32_t P = desc->heads * desc->Z, Ht = desc->H, Wt = desc->W, C = desc->head_dim;
+  st = check_tiling(nty, ntx, P, Ht, Wt, C, stride_y, stride_x, Hf, Wf, desc->dtype);
+  if (st != STRATA_OK) return st;
+  REQUIRE((int64_t)Wf * C < ((int64_t)1 << 31) &&
+              (int64_t)P * Hf * (((int64_t)Wf * C + 255) / 256) < ((int64_t)1 << 31),
+          "fwd_stitch: face too large for one launch");
+  hipStream_t s = (hipStream_t)stream;
+  const StitchArgs sa = {face, window, nty, ntx, stride_y, stride_x, Hf, Wf};
+  const bool fused = overlap_form(nty, ntx, Ht, Wt, C, stride_y, stride_x, Hf, Wf, desc->dtype) &&
+                     launch_na3d_fwd_zs(*desc, o, q, k, v, cs, tiles, lse, s, &sa);
+  if (!fused) {  // every tile output, then the whole stitch
+    launch_fwd(*desc, o, q, k, v, cs, tiles, lse, s);
+    launch_tile_blend(tiles, nty, ntx, P, Ht, Wt, C, stride_y, stride_x, window, face, Hf, Wf, desc->dtype, s);
+  }
+  return check_launch("strata_na3d_fwd_stitch");
 }
 
 strata_status strata_duo_pad(const void* faces, int32_t P, int32_t n, int32_t C, int32_t halo, void* padded,

@@ -109,28 +109,25 @@ __global__ void __launch_bounds__(256) tile_blend_kernel(const T* __restrict__ t
 // is exactly 1, where it is the identity), round to nearest even.
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
-template <int ITEMS>
-__global__ void __launch_bounds__(256) tile_blend_bf16_kernel(const uint16_t* __restrict__ tiles, int nty, int ntx,
-                                                              int P, int Ht, int Wt, int C, int sy, int sx,
-                                                              const float* __restrict__ window,
-                                                              uint16_t* __restrict__ out, int Hf, int Wf, int bpr) {
-  const int cv = C >> 3;
-  const int row = blockIdx.x / bpr;  // p * Hf + y
-  const int jb = (blockIdx.x - row * bpr) * (256 * ITEMS) + threadIdx.x;
-  const int y = row % Hf, p = row / Hf;
-  int alo, ahi;
-  cover_range(y, Ht, sy, nty, &alo, &ahi);
+// ITEMS cells x 8 channels of face row (p, y), whose covering tile rows are
+// [alo, ahi]; item(k, x, c0) names the k-th cell of this thread (false: none).
+template <int ITEMS, typename Item>
+__device__ __forceinline__ void stitch_cells_bf16(const uint16_t* __restrict__ tiles, int ntx, int P, int Ht,
+                                                  int Wt, int C, int sy, int sx, const float* __restrict__ window,
+                                                  uint16_t* __restrict__ out_row, int y, int p, int alo, int ahi,
+                                                  Item item) {
   const int64_t tile_elems = (int64_t)P * Ht * Wt * C;
-  const int per_row = Wf * cv;
   uint4 val[ITEMS][2][2];
   float wt[ITEMS][2][2];
   bool ok[ITEMS][2][2];
+  bool live[ITEMS];
+  int xs[ITEMS], cs[ITEMS];
 #pragma unroll
   for (int k = 0; k < ITEMS; ++k) {
-    const int j = jb + k * 256;
-    const bool live = j < per_row;
-    const int jj = live ? j : 0;
-    const int x = jj / cv, c0 = (jj - x * cv) * 8;
+    int x = 0, c0 = 0;
+    live[k] = item(k, x, c0);
+    xs[k] = x;
+    cs[k] = c0;
     int blo, bhi;
     cover_range(x, Wt, sx, ntx, &blo, &bhi);
 #pragma unroll
@@ -138,7 +135,7 @@ __global__ void __launch_bounds__(256) tile_blend_bf16_kernel(const uint16_t* __
 #pragma unroll
       for (int ib = 0; ib < 2; ++ib) {
         const int a = alo + ia, b = blo + ib;
-        ok[k][ia][ib] = live && a <= ahi && b <= bhi;
+        ok[k][ia][ib] = live[k] && a <= ahi && b <= bhi;
         val[k][ia][ib] = make_uint4(0u, 0u, 0u, 0u);
         wt[k][ia][ib] = 0.f;
         if (ok[k][ia][ib]) {
@@ -154,8 +151,7 @@ __global__ void __launch_bounds__(256) tile_blend_bf16_kernel(const uint16_t* __
   }
 #pragma unroll
   for (int k = 0; k < ITEMS; ++k) {
-    const int j = jb + k * 256;
-    if (j >= per_row) continue;
+    if (!live[k]) continue;
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     float dsum = 0.f;
 #pragma unroll
@@ -181,8 +177,70 @@ __global__ void __launch_bounds__(256) tile_blend_bf16_kernel(const uint16_t* __
 #pragma unroll
     for (int v = 0; v < 4; ++v) r[v] = pack_bf16x2(acc[2 * v], acc[2 * v + 1]);
     __builtin_nontemporal_store(u32x4{r[0], r[1], r[2], r[3]},
-                                reinterpret_cast<u32x4*>(out + (int64_t)row * Wf * C + (int64_t)j * 8));
+                                reinterpret_cast<u32x4*>(out_row + (int64_t)xs[k] * C + cs[k]));
   }
+}
+
+template <int ITEMS>
+__global__ void __launch_bounds__(256) tile_blend_bf16_kernel(const uint16_t* __restrict__ tiles, int nty, int ntx,
+                                                              int P, int Ht, int Wt, int C, int sy, int sx,
+                                                              const float* __restrict__ window,
+                                                              uint16_t* __restrict__ out, int Hf, int Wf, int bpr) {
+  const int cv = C >> 3;
+  const int row = blockIdx.x / bpr;  // p * Hf + y
+  const int jb = (blockIdx.x - row * bpr) * (256 * ITEMS) + threadIdx.x;
+  const int y = row % Hf, p = row / Hf;
+  int alo, ahi;
+  cover_range(y, Ht, sy, nty, &alo, &ahi);
+  const int per_row = Wf * cv;
+  stitch_cells_bf16<ITEMS>(tiles, ntx, P, Ht, Wt, C, sy, sx, window, out + (int64_t)row * Wf * C, y, p, alo, ahi,
+                           [&](int k, int& x, int& c0) {
+                             const int j = jb + k * 256;
+                             if (j >= per_row) return false;
+                             x = j / cv;
+                             c0 = (j - x * cv) * 8;
+                             return true;
+                           });
+}
+
+// The same stitch restricted to the cells that two or more tiles cover, for a
+// tiling whose tiles cover the face with sy <= Ht <= 2 sy, sx <= Wt <= 2 sx:
+// one block per face row (p, y); a row inside a y overlap [a sy, (a-1) sy + Ht)
+// is stitched whole, any other row only at the x overlaps [b sx, (b-1) sx + Wt).
+// The cells one tile covers alone are left as they are.
+template <int ITEMS>
+__global__ void __launch_bounds__(256) tile_blend_overlap_bf16_kernel(const uint16_t* __restrict__ tiles, int nty,
+                                                                      int ntx, int P, int Ht, int Wt, int C, int sy,
+                                                                      int sx, const float* __restrict__ window,
+                                                                      uint16_t* __restrict__ out, int Hf, int Wf) {
+  const int cv = C >> 3;
+  const int row = blockIdx.x;  // p * Hf + y
+  const int y = row % Hf, p = row / Hf;
+  int alo, ahi;
+  cover_range(y, Ht, sy, nty, &alo, &ahi);
+  const bool whole = alo < ahi;
+  const int ovx = Wt - sx;
+  const int nitems = (whole ? Wf : (ntx - 1) * ovx) * cv;
+  uint16_t* const out_row = out + (int64_t)row * Wf * C;
+  for (int j0 = 0; j0 < nitems; j0 += 256 * ITEMS) {
+    stitch_cells_bf16<ITEMS>(tiles, ntx, P, Ht, Wt, C, sy, sx, window, out_row, y, p, alo, ahi,
+                             [&](int k, int& x, int& c0) {
+                               const int j = j0 + k * 256 + (int)threadIdx.x;
+                               if (j >= nitems) return false;
+                               const int cell = j / cv;
+                               c0 = (j - cell * cv) * 8;
+                               x = whole ? cell : (cell / ovx + 1) * sx + cell % ovx;
+                               return true;
+                             });
+  }
+}
+
+void launch_tile_blend_overlap(const void* tiles, int nty, int ntx, int P, int Ht, int Wt, int C, int sy,
+                               int sx, const float* window, void* out, int Hf, int Wf, hipStream_t s) {
+  const int64_t blocks = (int64_t)P * Hf;
+  hipLaunchKernelGGL((tile_blend_overlap_bf16_kernel<2>), dim3((unsigned)blocks), dim3(256), 0, s,
+                     static_cast<const uint16_t*>(tiles), nty, ntx, P, Ht, Wt, C, sy, sx, window,
+                     static_cast<uint16_t*>(out), Hf, Wf);
 }
 
 template <typename T, int VEC, int CV>

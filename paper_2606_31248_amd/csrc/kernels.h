@@ -40,8 +40,18 @@ void launch_na3d_fwd_ref(const strata_na3d_desc& d, const NaOpts& o, const void*
 
 // bf16 MFMA forward sweeping the key levels once per head (window 3x7x7, Z = 8);
 // returns false for any other problem.
+// A regular tiling of one face that a forward stitches into: tile (a, b) of
+// the batch (index a ntx + b) has its origin at (a sy, b sx) of the face
+// [heads Z, Hf, Wf, head_dim]; `window` [H, W] holds the stitch weights.
+struct StitchArgs {
+  void* face;
+  const float* window;
+  int nty, ntx, sy, sx, Hf, Wf;
+};
+
 bool launch_na3d_fwd_zs(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k,
-                        const void* v, const float* cs, void* out, float* lse, hipStream_t s);
+                        const void* v, const float* cs, void* out, float* lse, hipStream_t s,
+                        const StitchArgs* st = nullptr);
 
 // bf16 column-wise forward, windows (kz, 1, 1) with Z <= 32, head_dim 64;
 // returns false for any other problem.
@@ -102,6 +112,11 @@ bool launch_na3d_bwd_dkdv_d128(const strata_na3d_desc& d, const BwdOpts& o, cons
                                const void* v, const float* cs, const void* dout, const float* lse,
                                const float* dvec, void* dk, void* dv, hipStream_t s);
 
+// Stitch of the cells covered by two or more tiles along y or x of a bf16
+// tiling with sy <= Ht <= 2 sy, sx <= Wt <= 2 sx, C % 8 == 0, whose tiles
+// cover the face ((nty-1) sy + Ht == Hf, (ntx-1) sx + Wt == Wf).
+void launch_tile_blend_overlap(const void* tiles, int nty, int ntx, int P, int Ht, int Wt, int C, int sy,
+                               int sx, const float* window, void* out, int Hf, int Wf, hipStream_t s);
 void launch_tile_blend(const void* tiles, int nty, int ntx, int P, int Ht, int Wt, int C, int sy,
                        int sx, const float* window, void* out, int Hf, int Wf, strata_dtype dt,
                        hipStream_t s);

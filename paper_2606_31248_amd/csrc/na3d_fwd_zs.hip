@@ -147,7 +147,23 @@ struct ZArgs {
   float eps;
   const uint16_t* gate;
   int gate_dim;
+  // stitch into the face: the tiles of the batch form an nty x ntx regular
+  // tiling with strides (sy, sx) of a face [heads Z, Hf, Wf, 64]; cells that
+  // one tile alone covers go to the face, the others to `out`
+  uint16_t* face;
+  const float* window;  // [H, W] stitch weights
+  int nty, ntx, sy, sx, Hf, Wf;
 };
+
+// A bf16 pair with each -0 half turned into +0: the stitch of a cell covered by
+// one tile returns w v / w, which is v for every value except -0 (its fused
+// multiply-add starts from +0).  Magnitude m = bits & 0x7fff; m + 0x7fff sets
+// bit 15 exactly when m > 0, and the sign survives only there.
+__device__ __forceinline__ uint32_t plus_zero2(uint32_t w) {
+  const uint32_t m = w & 0x7fff7fffu;
+  const uint32_t keep = ((m + 0x7fff7fffu) & 0x80008000u) | 0x7fff7fffu;
+  return w & keep;
+}
 
 // Rotate 4 pairs of K held as packed bf16x2 words by packed float16 phases
 // (c, s): round-toward-zero to float16 (exact for bf16 values inside the
@@ -171,7 +187,7 @@ __device__ __forceinline__ uint4 rotate_k8(uint4 x, uint4 ph, float mul = 1.f) {
   return make_uint4(r[0], r[1], r[2], r[3]);
 }
 
-template <int Z, bool NORM, bool GATE>
+template <int Z, bool NORM, bool GATE, bool STITCH>
 __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
   __shared__ __attribute__((aligned(16))) char tK0[KTILE];
   __shared__ __attribute__((aligned(16))) char tV0[VTILE];
@@ -205,6 +221,18 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
   const int qy_raw = sy0 + (qn >> 2), qx_raw = sx0 + (qn & 3);
   const int qy = min(qy_raw, H - 1), qx = min(qx_raw, W - 1);
   const bool in_grid = qy_raw < H && qx_raw < W;
+  // stitch: a cell no other tile of the tiling covers (sy <= H <= 2 sy, and
+  // likewise along x) takes this tile's value, or 0 where its weight is 0
+  bool direct = false, wzero = false;
+  int64_t fcell = 0;
+  if constexpr (STITCH) {
+    const int ta = b / a.ntx, tb = b - ta * a.ntx;
+    const bool one_y = !(ta > 0 && qy < H - a.sy) && !(ta < a.nty - 1 && qy >= a.sy);
+    const bool one_x = !(tb > 0 && qx < W - a.sx) && !(tb < a.ntx - 1 && qx >= a.sx);
+    direct = one_y && one_x;
+    fcell = (int64_t)(ta * a.sy + qy) * a.Wf + (tb * a.sx + qx);
+    wzero = a.window[qy * W + qx] == 0.f;
+  }
 
   auto kswz = [&](int key) { return ((key % LX >> 1) + 5 * (key / LX)) & 7; };
   auto key_row = [&](int u) {
@@ -530,12 +558,21 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
               if (a.gate_dim == 1) inv *= sigmoid_fast(__uint_as_float(ghd[z] << 16));
             const int64_t tok = level_base(h, z) + (int64_t)qy * W + qx;
             uint2* dst = reinterpret_cast<uint2*>(a.out + tok * kD);
+            if constexpr (STITCH)
+              if (direct)
+                dst = reinterpret_cast<uint2*>(a.face + ((int64_t)(h * Z + z) * a.Hf * a.Wf + fcell) * kD);
 #pragma unroll
             for (int t = 0; t < 4; ++t) {  // d = 16t + 4g + i
               f32x4 r = o[z][t] * inv;
               if constexpr (GATE)
                 if (a.gate_dim != 1) r *= sigmoid4_bf16(gch[z][t]);
-              dst[4 * t + g] = make_uint2(pack2(r[0], r[1]), pack2(r[2], r[3]));
+              uint32_t w0 = pack2(r[0], r[1]), w1 = pack2(r[2], r[3]);
+              if constexpr (STITCH)
+                if (direct) {
+                  w0 = wzero ? 0u : plus_zero2(w0);
+                  w1 = wzero ? 0u : plus_zero2(w1);
+                }
+              dst[4 * t + g] = make_uint2(w0, w1);
             }
             if (a.lse && g == 0) a.lse[tok] = (m[z] + __log2f(lt)) * kLn2;
           }
@@ -550,9 +587,12 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
 }  // namespace
 
 // Level-sweep forward for the 3x7x7 window at Z = 8 (bf16, head_dim 64); false
-// when the problem is not that shape.
+// when the problem is not that shape.  With `st` (a regular tiling of one face,
+// sy <= H <= 2 sy, sx <= W <= 2 sx, checked by the caller) the cells one tile
+// alone covers are stored into st->face instead of `out`.
 bool launch_na3d_fwd_zs(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k,
-                        const void* v, const float* cs, void* out, float* lse, hipStream_t s) {
+                        const void* v, const float* cs, void* out, float* lse, hipStream_t s,
+                        const StitchArgs* st) {
   if (d.dtype != STRATA_BF16 || d.head_dim != kD) return false;
   if (d.kz != KZ || d.ky != KY || d.kx != KX || d.Z != 8) return false;
   if ((int64_t)d.H * d.W * kD * 2 >= (int64_t)1 << 32) return false;  // byte offsets in 32 bits
@@ -574,13 +614,30 @@ bool launch_na3d_fwd_zs(const strata_na3d_desc& d, const NaOpts& o, const void* 
   a.hpw = d.heads < 8 ? d.heads : 8;
   a.n_hg = (d.heads + a.hpw - 1) / a.hpw;
   a.qscale = d.scale * kLog2e;
+  if (st) {
+    a.face = static_cast<uint16_t*>(st->face);
+    a.window = st->window;
+    a.nty = st->nty;
+    a.ntx = st->ntx;
+    a.sy = st->sy;
+    a.sx = st->sx;
+    a.Hf = st->Hf;
+    a.Wf = st->Wf;
+  }
   const int64_t blocks = (int64_t)d.B * a.n_hg * a.n_yb * a.n_xb;
   if (blocks >= (int64_t)1 << 31) return false;
   const dim3 grid((unsigned)blocks), block(kThreads);
-  if (o.qk_norm && o.gate) hipLaunchKernelGGL((na3d_fwd_zs_kernel<8, true, true>), grid, block, 0, s, a);
-  else if (o.qk_norm) hipLaunchKernelGGL((na3d_fwd_zs_kernel<8, true, false>), grid, block, 0, s, a);
-  else if (o.gate) hipLaunchKernelGGL((na3d_fwd_zs_kernel<8, false, true>), grid, block, 0, s, a);
-  else hipLaunchKernelGGL((na3d_fwd_zs_kernel<8, false, false>), grid, block, 0, s, a);
+  const int variant = (o.qk_norm ? 1 : 0) | (o.gate ? 2 : 0) | (st ? 4 : 0);
+  switch (variant) {
+    case 0: hipLaunchKernelGGL((na3d_fwd_zs_kernel<8, false, false, false>), grid, block, 0, s, a); break;
+    case 1: hipLaunchKernelGGL((na3d_fwd_zs_kernel<8, true, false, false>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((na3d_fwd_zs_kernel<8, false, true, false>), grid, block, 0, s, a); break;
+    case 3: hipLaunchKernelGGL((na3d_fwd_zs_kernel<8, true, true, false>), grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((na3d_fwd_zs_kernel<8, false, false, true>), grid, block, 0, s, a); break;
+    case 5: hipLaunchKernelGGL((na3d_fwd_zs_kernel<8, true, false, true>), grid, block, 0, s, a); break;
+    case 6: hipLaunchKernelGGL((na3d_fwd_zs_kernel<8, false, true, true>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((na3d_fwd_zs_kernel<8, true, true, true>), grid, block, 0, s, a); break;
+  }
   return true;
 }
 

@@ -55,15 +55,25 @@ def na3d_forward(q, k, v, window, scale, cs=None, out=None, lse=None):
 
 
 def face_step(q, k, v, geom: TileGeometry, window, scale, tiling, blend_window, face_out,
-              coords=None, cs=None, out=None):
+              coords=None, cs=None, out=None, fused: bool = True, opts=None):
     """One face rollout step: per-tile NA3D forward with StereoRoPE, then the stitch.
 
     q, k, v: [T, heads, Z, Ht, Wt, d]; tiling = (nty, ntx, stride_y, stride_x);
     the tile outputs are viewed as [T, heads*Z, Ht, Wt, d] planes for the blend;
-    face_out: [heads*Z, Hf, Wf, d]."""
+    face_out: [heads*Z, Hf, Wf, d].  fused: the forward stores the cells one tile
+    alone covers straight into the face and the stitch visits only the overlaps
+    (the same face bit for bit); `out` then holds only the overlap cells."""
     T, heads, Z, Ht, Wt, d = q.shape
     coords, cs = stereo_phases(geom, Ht, Wt, d, coords, cs)
-    out = na3d_forward(q, k, v, window, scale, cs=cs, out=out)
+    if out is None:
+        out = torch.empty_like(q)
     nty, ntx, sy, sx = tiling
-    B.strata_tile_blend(out.view(T, heads * Z, Ht, Wt, d), nty, ntx, sy, sx, blend_window, face_out)
+    planes = out.view(T, heads * Z, Ht, Wt, d)
+    desc = B.desc_for(q, window, scale)
+    if fused:
+        B.strata_na3d_fwd_stitch(desc, opts, q, k, v, cs, out, None, nty, ntx, sy, sx, blend_window, face_out)
+        B.strata_tile_blend_overlap(planes, nty, ntx, sy, sx, blend_window, face_out)
+    else:
+        B.strata_na3d_fwd_ex(desc, opts, q, k, v, cs, out, None)
+        B.strata_tile_blend(planes, nty, ntx, sy, sx, blend_window, face_out)
     return face_out

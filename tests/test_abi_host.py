@@ -238,3 +238,24 @@ def test_duo_plan_rules():
     assert L.strata_duo_pad_planned(p, 1, 32, 1, 4, p, need, odd, F, None) == B.STRATA_ERR_INVALID_ARG
     assert L.strata_duo_pad_vjp(odd, 1, 32, 1, 4, p, need, p, F, None) == B.STRATA_ERR_INVALID_ARG
     assert L.strata_duo_pad_vjp(p, 1, 32, 1, 4, p, need, odd, F, None) == B.STRATA_ERR_INVALID_ARG
+
+
+def test_fwd_stitch_rules():
+    L = B.load()
+    p = fake()
+    d = desc(B=4)
+
+    def call(nty=2, ntx=2, sy=8, sx=8, Hf=24, Wf=24, face=p, dd=d):
+        return L.strata_na3d_fwd_stitch(ctypes.byref(dd), None, p, p, p, None, p, None, nty, ntx, sy, sx, p,
+                                        face, Hf, Wf, None)
+
+    assert call(nty=3, ntx=1) == B.STRATA_ERR_INVALID_ARG          # the batch is not the tiling
+    assert call(Hf=20) == B.STRATA_ERR_INVALID_ARG                 # tiles reach past the face
+    assert call(sy=0) == B.STRATA_ERR_INVALID_ARG
+    assert call(face=None) == B.STRATA_ERR_INVALID_ARG
+    assert call(face=fake(0x10008)) == B.STRATA_ERR_INVALID_ARG     # misaligned
+    assert call(dd=desc(B=4, window=(2, 7, 7))) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_tile_blend_overlap(p, 9, 9, 4, 64, 64, 64, 56, 56, p, p, 511, 512, B.STRATA_BF16,
+                                       None) == B.STRATA_ERR_INVALID_ARG
+    assert L.strata_tile_blend_overlap(p, 9, 9, 4, 64, 64, 64, 56, 56, None, p, 512, 512, B.STRATA_BF16,
+                                       None) == B.STRATA_ERR_INVALID_ARG
