@@ -33,10 +33,17 @@ def rng(seed: int, stream: int) -> np.random.Generator:
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round float32 values to bfloat16 (round-to-nearest-even); returns uint16 bit patterns.
 
-    Storage conversion of the synthetic draws (finite inputs only)."""
-    b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    b = b + 0x7FFF + ((b >> 16) & 1)
-    return (b >> 16).astype(np.uint16)
+    Storage conversion of the synthetic draws (finite inputs only: the largest
+    finite pattern plus 0x8000 stays below 2^32, so 32-bit integers suffice).
+    Converted in chunks, so a multi-GB draw needs no wide temporaries."""
+    xa = np.ascontiguousarray(x, dtype=np.float32)
+    b = xa.reshape(-1).view(np.uint32)
+    out = np.empty(b.size, np.uint16)
+    step = 1 << 24
+    for i in range(0, b.size, step):
+        c = b[i:i + step]
+        out[i:i + step] = ((c + ((c >> 16) & np.uint32(1)) + np.uint32(0x7FFF)) >> 16).astype(np.uint16)
+    return out.reshape(xa.shape)
 
 
 def bf16_bits_to_f32(h: np.ndarray) -> np.ndarray:

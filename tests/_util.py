@@ -21,6 +21,15 @@ def host_f64(t: torch.Tensor) -> np.ndarray:
     return t.detach().float().cpu().numpy().astype(np.float64)
 
 
+def host_rows(t: torch.Tensor, sel, width: int = 0) -> np.ndarray:
+    """Rows ``sel`` of a device tensor viewed as [-1, width] (its flat elements
+    when width is 0), gathered on the device, as float64 on the host: a sampled
+    check of a full-size output moves only the samples."""
+    flat = t.reshape(-1, width) if width else t.reshape(-1)
+    idx = torch.from_numpy(np.asarray(sel, dtype=np.int64)).to(t.device)
+    return host_f64(flat.index_select(0, idx))
+
+
 def host_bits(t: torch.Tensor) -> np.ndarray:
     """Raw storage of a bf16 / f32 device tensor as a numpy array (bit-exact comparisons)."""
     c = t.detach().contiguous().cpu()

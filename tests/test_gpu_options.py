@@ -12,7 +12,7 @@ import oracle
 from paper_2606_31248_amd import binding as B
 from paper_2606_31248_amd import inputs as I
 from paper_2606_31248_amd import pipeline
-from _util import LSE_ABS_BF16, bf16_half_ulp, check_close, dev_tensor, host_bits, host_f64
+from _util import LSE_ABS_BF16, bf16_half_ulp, check_close, dev_tensor, host_bits, host_f64, host_rows
 from oracle import geometry as G
 
 pytestmark = pytest.mark.gpu
@@ -222,8 +222,8 @@ def test_fwd_options_full_size_sampled():
     local = np.searchsorted(tiles, sel // per_tile) * per_tile + sel % per_tile
     sub = tuple(None if a is None else a[tiles] for a in inputs)
     ro, rl = oracle_fwd(sub, window, scale, "bf16", True, c32[tiles], sel=local)
-    check_out(host_f64(out).reshape(-1, wl.d)[sel], sub, window, scale, "bf16", True, c32[tiles], ro, sel=local)
-    assert np.max(np.abs(host_f64(lse).reshape(-1)[sel] - rl)) <= LSE_ABS_BF16
+    check_out(host_rows(out, sel, wl.d), sub, window, scale, "bf16", True, c32[tiles], ro, sel=local)
+    assert np.max(np.abs(host_rows(lse, sel) - rl)) <= LSE_ABS_BF16
     assert torch.isfinite(out.float()).all()
 
 
@@ -344,7 +344,7 @@ def test_bwd_options_full_size_sampled():
     refs = oracle.na3d_bwd(sub(q), sub(k), sub(v), sub(dout), window, scale, coords=c32[tiles],
                            selq=local, selk=local, qk_norm=True, gate=sub(g))
     # gradients of the sampled rows, the oracle seeing only the sampled tiles
-    got = [host_f64(x).reshape(-1, wl.d)[sel] for x in (dq, dk, dv, dg)]
+    got = [host_rows(x, sel, wl.d) for x in (dq, dk, dv, dg)]
     st = lambda a: a[tiles]
     check_bwd_grads((st(q), st(k), st(v), st(g), st(dout)), [torch.from_numpy(x) for x in got], refs, window,
                     scale, "bf16", True, c32[tiles], sel=local, presliced=True)

@@ -10,7 +10,7 @@ import oracle
 from paper_2606_31248_amd import binding as B
 from paper_2606_31248_amd import inputs as I
 from paper_2606_31248_amd import pipeline
-from _util import LSE_ABS_BF16, check_close, dev_tensor, host_f64
+from _util import LSE_ABS_BF16, check_close, dev_tensor, host_f64, host_rows
 from oracle import geometry as G
 from test_gpu_options import check_bwd_grads, check_out
 
@@ -148,8 +148,8 @@ def test_w999_fwd_full_size_sampled():
     local = np.searchsorted(tiles, sel // per_tile) * per_tile + sel % per_tile
     sub = lambda a: oracle.widen(a[tiles], "bf16")
     ro, rl = oracle.na3d_fwd(sub(q), sub(k), sub(v), (9, 9, 9), wl.scale, coords=c32[tiles], sel=local)
-    check_close(host_f64(out).reshape(-1, wl.d)[sel], ro, "bf16", "out")
-    assert np.max(np.abs(host_f64(lse).reshape(-1)[sel] - rl)) <= LSE_ABS_BF16
+    check_close(host_rows(out, sel, wl.d), ro, "bf16", "out")
+    assert np.max(np.abs(host_rows(lse, sel) - rl)) <= LSE_ABS_BF16
 
 
 # ----------------------------------------------------------------------------- column-wise attention
@@ -207,8 +207,8 @@ def test_column_fwd_full_size_sampled():
     local = np.searchsorted(tiles, sel // per_tile) * per_tile + sel % per_tile
     sub = lambda a: oracle.widen(a[tiles], "bf16")
     ro, rl = oracle.na3d_fwd(sub(q), sub(k), sub(v), (24, 1, 1), wl.scale, sel=local)
-    check_close(host_f64(out).reshape(-1, wl.d)[sel], ro, "bf16", "out")
-    assert np.max(np.abs(host_f64(lse).reshape(-1)[sel] - rl)) <= LSE_ABS_BF16
+    check_close(host_rows(out, sel, wl.d), ro, "bf16", "out")
+    assert np.max(np.abs(host_rows(lse, sel) - rl)) <= LSE_ABS_BF16
 
 
 # ----------------------------------------------------------------------------- head_dim 128
@@ -273,7 +273,7 @@ def test_column_bwd_full_size_sampled():
     sub = lambda a: oracle.widen(a[tiles], "bf16")
     refs = oracle.na3d_bwd(sub(q), sub(k), sub(v), sub(dout), (24, 1, 1), wl.scale, selq=local, selk=local)
     for name, got, ref in zip(("dq", "dk", "dv"), (dq, dk, dv), refs):
-        check_close(host_f64(got).reshape(-1, wl.d)[sel], ref, "bf16", name)
+        check_close(host_rows(got, sel, wl.d), ref, "bf16", name)
 
 
 # ----------------------------------------------------------------------------- head_dim 128, 9x9x9 (MFMA kernel)
@@ -311,8 +311,8 @@ def test_d128_w999_bwd_sampled_keys(shape, rope):
     dq, dk, dv, _ = r["grads"]
     d = shape[-1]
     check_close(host_f64(dq), refs[0], "bf16", "dq")
-    check_close(host_f64(dk).reshape(-1, d)[sel], refs[1], "bf16", "dk")
-    check_close(host_f64(dv).reshape(-1, d)[sel], refs[2], "bf16", "dv")
+    check_close(host_rows(dk, sel, d), refs[1], "bf16", "dk")
+    check_close(host_rows(dv, sel, d), refs[2], "bf16", "dv")
 
 
 def test_d128_w999_bwd_decoder_full_size_sampled():
@@ -328,7 +328,7 @@ def test_d128_w999_bwd_decoder_full_size_sampled():
     refs = oracle.na3d_bwd(w(q), w(k), w(v), w(r["dout"]), window, r["scale"], coords=r["c32"], selq=sel, selk=sel)
     dq, dk, dv, _ = r["grads"]
     for name, got, ref in zip(("dq", "dk", "dv"), (dq, dk, dv), refs):
-        check_close(host_f64(got).reshape(-1, wl.d)[sel], ref, "bf16", name)
+        check_close(host_rows(got, sel, wl.d), ref, "bf16", name)
 
 
 @pytest.mark.parametrize("qk_norm,gkind", [(True, 0), (False, 1), (False, "d"), (True, "d")])

@@ -12,7 +12,7 @@ from oracle import geometry as G
 from paper_2606_31248_amd import binding as B
 from paper_2606_31248_amd import inputs as I
 from paper_2606_31248_amd import pipeline
-from _util import LSE_ABS_BF16, bf16_half_ulp, check_close, dev_tensor, host_bits, host_f64
+from _util import LSE_ABS_BF16, bf16_half_ulp, check_close, dev_tensor, host_bits, host_f64, host_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -177,9 +177,9 @@ def test_fwd_full_size_sampled(wl):
     tb = sel // per_tile
     local = np.searchsorted(tiles, tb) * per_tile + sel % per_tile
     ro, rl = oracle.na3d_fwd(sub(q), sub(k), sub(v), window, scale, coords=c32[tiles], sel=local)
-    got = host_f64(out).reshape(-1, wl.d)[sel]
+    got = host_rows(out, sel, wl.d)
     check_close(got, ro, "bf16", "out")
-    assert np.max(np.abs(host_f64(lse).reshape(-1)[sel] - rl)) <= LSE_ABS_BF16
+    assert np.max(np.abs(host_rows(lse, sel) - rl)) <= LSE_ABS_BF16
     # a global property at full size: every output is a convex combination of v rows
     o = out.float()
     assert torch.isfinite(o).all()
@@ -369,7 +369,7 @@ def test_bwd_full_size_sampled():
     rq, rk, rv = oracle.na3d_bwd(sub(q), sub(k), sub(v), sub(g), window, scale, coords=c32[tiles],
                                  selq=local, selk=local)
     for name, got, ref in (("dq", dq, rq), ("dk", dk, rk), ("dv", dv, rv)):
-        check_close(host_f64(got).reshape(-1, wl.d)[sel], ref, "bf16", name)
+        check_close(host_rows(got, sel, wl.d), ref, "bf16", name)
 
 
 @pytest.mark.parametrize("window", [(3, 7, 7), (5, 9, 9)])
