@@ -70,6 +70,12 @@
 // are loaded at the start of its last key level (later loads leave their
 // latency exposed, measured) and sigmoid(g) multiplies the normalised output
 // at the store.
+//
+// Stitch (App. F, Eq. stitch).  When the batch is the regular tiling of one
+// face, a query cell that no other tile covers is stored straight into the face
+// (its stitch is the tile's own value, 0 where its weight is 0, with -0 turned
+// into +0 as the stitch's multiply-add from +0 does); the other cells go to the
+// tile output for the overlap stitch.
 #include "common.h"
 #include "kernels.h"
 #include "mfma_util.h"
