@@ -135,3 +135,42 @@ def test_kbd_window_2d_shape_and_interior():
     np.testing.assert_allclose(w[3, 20], t[3], atol=0)
     np.testing.assert_allclose(w[63, 39], t[0] * t[0], atol=1e-16)
     assert np.all(w > 0) and np.all(w <= 1)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_single_cover_cells_return_the_tile_value(dtype):
+    """A face cell that one tile alone covers stitches to w v / w: the tile's own
+    value bit for bit for any positive float32 weight (one rounding of the
+    product, one of the quotient, then the store rounding), 0 where w = 0, and
+    +0 for -0 (the multiply-add starts from +0).  The fused face step stores
+    these cells from the forward on this basis."""
+    nty, ntx, Ht, Wt, sy, sx = 3, 3, 12, 14, 9, 10
+    Hf, Wf, P_, C = (nty - 1) * sy + Ht, (ntx - 1) * sx + Wt, 2, 4
+    T = nty * ntx
+    r = np.random.default_rng(90)
+    tiles = inputs.gaussian((T, P_, Ht, Wt, C), 90, inputs.STREAM_FIELD, dtype)
+    neg_zero = np.uint16(0x8000) if dtype == "bf16" else np.float32(-0.0)
+    tiles[r.random(tiles.shape) < 0.05] = neg_zero
+    # arbitrary positive float32 weights (not dyadic), some exactly 0
+    win = r.uniform(0.01, 3.0, Ht * Wt).astype(np.float32)
+    win[r.random(Ht * Wt) < 0.1] = 0.0
+    out = oracle.tile_blend(tiles, nty, ntx, sy, sx, win, Hf, Wf, dtype)
+    ny = np.array([sum(a * sy <= y < a * sy + Ht for a in range(nty)) for y in range(Hf)])
+    nx = np.array([sum(b * sx <= x < b * sx + Wt for b in range(ntx)) for x in range(Wf)])
+    bits = (lambda a: a) if dtype == "bf16" else (lambda a: a.view(np.uint32))
+    zero = 0
+    singles = 0
+    for a in range(nty):
+        for b in range(ntx):
+            for i in range(Ht):
+                for j in range(Wt):
+                    y, x = a * sy + i, b * sx + j
+                    if ny[y] != 1 or nx[x] != 1:
+                        continue
+                    singles += 1
+                    v = bits(tiles[a * ntx + b, :, i, j, :])
+                    expect = np.where(v == bits(np.array([neg_zero]))[0], zero, v)
+                    if win[i * Wt + j] == 0.0:
+                        expect = np.zeros_like(v)
+                    assert np.array_equal(bits(out[:, y, x, :]), expect), (a, b, i, j)
+    assert singles > 0.4 * Hf * Wf
