@@ -110,6 +110,17 @@ def test_fused_face_step_zero_weights():
     assert np.all(bits[:, :2] == 0) and np.all(bits[:, :, :2] == 0)
 
 
+def test_fused_face_step_arbitrary_weights():
+    """Random positive float32 weights (not dyadic: the stitch rounds w v and w v / w), 10% of them 0."""
+    nty, ntx, H, W, s = 3, 3, 32, 32, 24
+    shape, qkv, coords, Hf, Wf = tiling_case(nty, ntx, H, W, s, s, seed=77)
+    r = np.random.default_rng(77)
+    win = r.uniform(0.01, 3.0, H * W).astype(np.float32)
+    win[r.random(H * W) < 0.1] = 0.0
+    fa, fb, _, _ = run_both(shape, qkv, coords, (nty, ntx, s, s), (3, 7, 7), win)
+    assert np.array_equal(host_bits(fa), host_bits(fb))
+
+
 @pytest.mark.parametrize("qk_norm,gate", [(True, None), (False, "token"), (True, "channel")])
 def test_fused_face_step_options(qk_norm, gate):
     """QK RMSNorm and the gate; gate logits of -200 on some tokens drive outputs to +-0."""
