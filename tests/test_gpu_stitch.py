@@ -60,15 +60,16 @@ def run_both(shape, qkv, coords, tiling, window, win, dtype="bf16", opts=None, s
     return face_a, face_b, tiles_b, (lse_a, lse_b)
 
 
-@pytest.mark.parametrize("nty,ntx,H,W,sy,sx", [
-    (3, 3, 32, 32, 24, 24),   # overlap 8 on whole 4x4 query sub-blocks
-    (2, 3, 36, 36, 28, 28),   # ragged 8x8 query blocks
-    (2, 2, 32, 40, 27, 29),   # overlaps of 5 and 11 cut through sub-blocks
-    (2, 2, 16, 16, 16, 16),   # no overlap: every cell goes straight to the face
-    (1, 3, 24, 32, 24, 17),   # one tile row
+@pytest.mark.parametrize("nty,ntx,H,W,sy,sx,heads", [
+    (3, 3, 32, 32, 24, 24, 2),   # overlap 8 on whole 4x4 query sub-blocks
+    (2, 3, 36, 36, 28, 28, 2),   # ragged 8x8 query blocks
+    (2, 2, 32, 40, 27, 29, 2),   # overlaps of 5 and 11 cut through sub-blocks
+    (2, 2, 16, 16, 16, 16, 2),   # no overlap: every cell goes straight to the face
+    (1, 3, 24, 32, 24, 17, 2),   # one tile row
+    (2, 2, 24, 24, 16, 16, 11),  # two head groups of 8 and 3 heads: face planes h Z + z
 ])
-def test_fused_face_step_bit_exact(nty, ntx, H, W, sy, sx):
-    shape, qkv, coords, Hf, Wf = tiling_case(nty, ntx, H, W, sy, sx)
+def test_fused_face_step_bit_exact(nty, ntx, H, W, sy, sx, heads):
+    shape, qkv, coords, Hf, Wf = tiling_case(nty, ntx, H, W, sy, sx, heads=heads)
     win = I.ramp_window_2d(H, W, max(H - sy, W - sx, 1))
     fa, fb, _, (la, lb) = run_both(shape, qkv, coords, (nty, ntx, sy, sx), (3, 7, 7), win)
     assert np.array_equal(host_bits(fa), host_bits(fb))
