@@ -193,6 +193,20 @@ def test_overlap_stitch_alone_against_oracle():
     assert np.all(got[:, ~multi] == sentinel)
 
 
+@pytest.mark.parametrize("dtype,C", [("f32", 4), ("bf16", 3), ("f32", 3)])
+def test_overlap_stitch_fallback_stitches_every_cell(dtype, C):
+    """Outside its bf16 / C % 8 == 0 form the overlap-only call stitches the whole face (oracle, bit for bit)."""
+    nty, ntx, Ht, Wt, sy, sx, P = 3, 2, 12, 10, 9, 7, 2
+    Hf, Wf = (nty - 1) * sy + Ht, (ntx - 1) * sx + Wt
+    tiles = I.gaussian((nty * ntx, P, Ht, Wt, C), 78, I.STREAM_FIELD, dtype)
+    win = I.ramp_window_2d(Ht, Wt, 3)
+    td = dev_tensor(tiles, dtype)
+    out = torch.full((P, Hf, Wf, C), 7.0, dtype=td.dtype, device="cuda")
+    B.strata_tile_blend_overlap(td, nty, ntx, sy, sx, torch.from_numpy(win).cuda(), out)
+    ref = oracle.tile_blend(tiles, nty, ntx, sy, sx, win, Hf, Wf, dtype)
+    assert np.array_equal(host_bits(out), ref)
+
+
 def test_fused_face_step_full_face_rollout():
     """The face-rollout step at full size (81 tiles x 16 heads x 8x64x64, 3x7x7): fused = plain, bit for bit."""
     wl = I.FACE_ROLLOUT
