@@ -6,17 +6,31 @@
 namespace strata {
 
 // One thread per (b, y, x, pair t).  Phases in float64, stored as float32 (cos, sin).
-__global__ void rope_phases_kernel(const float* __restrict__ coords, int64_t n_pos, int n_pairs,
-                                   double base, float2* __restrict__ cs) {
+// The frequencies base^(-t'/q) depend on the pair alone: a block computes them
+// once into LDS (the same pow call, so the same values) when they fit.
+constexpr int kPhaseThreads = 256;
+
+__global__ void __launch_bounds__(kPhaseThreads) rope_phases_kernel(const float* __restrict__ coords,
+                                                                    int64_t n_pos, int n_pairs, double base,
+                                                                    float2* __restrict__ cs) {
+  __shared__ double omega[kPhaseThreads];
+  const int q = n_pairs >> 1;  // head_dim / 4 pairs per axis
+  auto freq = [&](int t) {
+    const int tt = t - (t >= q) * q;
+    return pow(base, -(double)tt / (double)q);
+  };
+  const bool table = n_pairs <= kPhaseThreads;
+  if (table) {
+    if ((int)threadIdx.x < n_pairs) omega[threadIdx.x] = freq(threadIdx.x);
+    __syncthreads();
+  }
   int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= n_pos * n_pairs) return;
   int t = (int)(idx % n_pairs);
   int64_t pos = idx / n_pairs;
-  int q = n_pairs >> 1;  // head_dim / 4 pairs per axis
   int axis = t >= q;
-  int tt = t - axis * q;
   double c = (double)coords[2 * pos + axis];
-  double th = c * pow(base, -(double)tt / (double)q);
+  double th = c * (table ? omega[t] : freq(t));
   double sn, cn;
   sincos(th, &sn, &cn);
   cs[idx] = make_float2((float)cn, (float)sn);
@@ -27,7 +41,7 @@ void launch_rope_phases(const float* coords, int B, int H, int W, int head_dim, 
   int64_t n_pos = (int64_t)B * H * W;
   int n_pairs = head_dim / 2;
   int64_t n = n_pos * n_pairs;
-  int threads = 256;
+  int threads = kPhaseThreads;
   int blocks = (int)((n + threads - 1) / threads);
   hipLaunchKernelGGL(rope_phases_kernel, dim3(blocks), dim3(threads), 0, s, coords, n_pos, n_pairs,
                      base, reinterpret_cast<float2*>(cs));
