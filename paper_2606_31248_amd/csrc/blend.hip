@@ -306,6 +306,25 @@ __global__ void tile_extract_kernel(const T* __restrict__ face, int ntx, int P, 
   }
 }
 
+// Vectorised extraction: one block per tile row (t, p, i), its threads over
+// the row's Wt C / VEC 16-byte pieces, which sit contiguously in the face row
+// (a sy + i) from column b sx on.  The row indices are block-uniform.
+template <typename T, int VEC>
+__global__ void __launch_bounds__(256) tile_extract_rows_kernel(const T* __restrict__ face, int ntx, int P, int Ht,
+                                                                int Wt, int C, int sy, int sx, int Hf, int Wf,
+                                                                T* __restrict__ tiles) {
+  const int row = blockIdx.x;  // (t * P + p) * Ht + i
+  const int i = row % Ht;
+  const int tp = row / Ht;
+  const int p = tp % P, t = tp / P;
+  const int a = t / ntx, b = t - a * ntx;
+  const int n = Wt * C / VEC;
+  const uint4* src =
+      reinterpret_cast<const uint4*>(face + (((int64_t)p * Hf + (a * sy + i)) * Wf + (int64_t)b * sx) * C);
+  uint4* dst = reinterpret_cast<uint4*>(tiles + (int64_t)row * Wt * C);
+  for (int j = threadIdx.x; j < n; j += blockDim.x) dst[j] = src[j];
+}
+
 template <typename T, int VEC>
 static void extract_launch(const void* face, int nty, int ntx, int P, int Ht, int Wt, int C, int sy,
                            int sx, int Hf, int Wf, void* tiles, hipStream_t s) {
@@ -319,6 +338,19 @@ static void extract_launch(const void* face, int nty, int ntx, int P, int Ht, in
 
 void launch_tile_extract(const void* face, int nty, int ntx, int P, int Ht, int Wt, int C, int sy,
                          int sx, int Hf, int Wf, void* tiles, strata_dtype dt, hipStream_t s) {
+  const int64_t rows = (int64_t)nty * ntx * P * Ht;
+  const int vec = dt == STRATA_BF16 ? 8 : 4;
+  if (C % vec == 0 && rows < ((int64_t)1 << 31) && (int64_t)Wt * C < ((int64_t)1 << 31)) {
+    if (dt == STRATA_BF16)
+      hipLaunchKernelGGL((tile_extract_rows_kernel<uint16_t, 8>), dim3((unsigned)rows), dim3(256), 0, s,
+                         static_cast<const uint16_t*>(face), ntx, P, Ht, Wt, C, sy, sx, Hf, Wf,
+                         static_cast<uint16_t*>(tiles));
+    else
+      hipLaunchKernelGGL((tile_extract_rows_kernel<float, 4>), dim3((unsigned)rows), dim3(256), 0, s,
+                         static_cast<const float*>(face), ntx, P, Ht, Wt, C, sy, sx, Hf, Wf,
+                         static_cast<float*>(tiles));
+    return;
+  }
   if (dt == STRATA_BF16) {
     if (C % 8 == 0)
       extract_launch<uint16_t, 8>(face, nty, ntx, P, Ht, Wt, C, sy, sx, Hf, Wf, tiles, s);

@@ -298,6 +298,19 @@ def test_blend_ragged_channels_and_uncovered_cells(C):
     assert np.array_equal(host_bits(out), ref)
 
 
+@pytest.mark.parametrize("dtype,C", [("bf16", 8), ("bf16", 3), ("f32", 4), ("f32", 3)])
+def test_extract_ragged_tiling_bit_exact(dtype, C):
+    """Extraction on a tiling that leaves face margins uncovered: rows of 16-byte pieces (C a multiple of
+    8 bf16 or 4 f32 values) and the element-wise kernel (other C), against the oracle's copy."""
+    nty, ntx, Ht, Wt, sy, sx = 2, 3, 10, 9, 7, 6
+    Hf, Wf = (nty - 1) * sy + Ht + 3, (ntx - 1) * sx + Wt + 2
+    face = I.gaussian((2, Hf, Wf, C), 34, I.STREAM_FIELD, dtype)
+    fd = dev_tensor(face, dtype)
+    tiles = torch.empty((nty * ntx, 2, Ht, Wt, C), dtype=fd.dtype, device="cuda")
+    B.strata_tile_extract(fd, nty, ntx, sy, sx, tiles)
+    assert np.array_equal(host_bits(tiles), oracle.tile_extract(face, nty, ntx, Ht, Wt, sy, sx))
+
+
 def test_blend_full_face_rollout_planes():
     """The face-rollout blend at full size; planes 0, 63, 127 compared bit for bit."""
     wl = I.FACE_ROLLOUT
