@@ -41,7 +41,9 @@ STATS_FILE = os.path.join(ROOT, "profiles", "face_rollout_step_kernel_stats.txt"
 SQ_FILE = os.path.join(ROOT, "profiles", "na3d_fwd_face_rollout_sq_counters.json")
 # the sources of the kernel that strata_na3d_fwd runs at the face-rollout shape
 KERNEL_SOURCES = ["paper_2606_31248_amd/csrc/na3d_fwd_zs.hip", "paper_2606_31248_amd/csrc/mfma_util.h",
-                  "paper_2606_31248_amd/csrc/common.h", "paper_2606_31248_amd/csrc/blend.hip"]
+                  "paper_2606_31248_amd/csrc/common.h"]
+# the sources of the stitch kernels (the overlap stitch of the face step)
+BLEND_SOURCES = ["paper_2606_31248_amd/csrc/blend.hip", "paper_2606_31248_amd/csrc/common.h"]
 # the face step: the forward with the stitch of single-cover cells fused into its
 # store, then the stitch of the overlap cells
 FWD_KERNEL = "na3d_fwd_zs_kernel<8, false, false, true>"
@@ -50,9 +52,9 @@ COPY_KERNEL = "copyBuffer"
 CALIB_BYTES = 1 << 30
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(sources=None) -> str:
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
+    for p in sources or KERNEL_SOURCES:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -119,7 +121,8 @@ def summarize_pmc(fetch_dir: str, write_dir: str, commands) -> dict:
                              "fetch_factor": ff, "write_factor": fw},
         "hbm_bytes_per_launch": fwd_f * 1024 * ff + fwd_w * 1024 * fw,
         "alg_bytes_per_launch": wl_alg,
-        "blend": {"kernel": f"strata_tile_blend_overlap ({BLEND_KERNEL})", "fetch_kb": bl_f, "write_kb": bl_w, "hbm_bytes_per_launch": bl_f * 1024 * ff + bl_w * 1024 * fw,
+        "blend": {"kernel": f"strata_tile_blend_overlap ({BLEND_KERNEL})",
+                  "source_hash": kernel_source_hash(BLEND_SOURCES), "fetch_kb": bl_f, "write_kb": bl_w, "hbm_bytes_per_launch": bl_f * 1024 * ff + bl_w * 1024 * fw,
                   "alg_bytes_per_launch": blend_alg},
         "commands": list(commands),
         "note": "Traffic = FETCH_SIZE * fetch_factor + WRITE_SIZE * write_factor, per dispatch; the factors "
