@@ -6,9 +6,11 @@ stitch of a cell covered by one tile is w v / w = v, or 0 where w = 0, with -0
 turned into +0 by the fused multiply-add from +0); and the face must match the
 oracle's forward and stitch under the bf16 rule.  Cases: the fused kernel at
 small tilings (overlaps that split query sub-blocks, ragged query blocks, no
-overlap, a window with zero weights, every option with saturated gates) and at
-the full face-rollout size; the shapes and tilings that fall back to forward +
-whole stitch; and the overlap-only stitch on its own against the oracle."""
+overlap, a ragged head group, a window with zero weights, random non-dyadic
+weights, every option with saturated gates) and at the full face-rollout size;
+the shapes and tilings that fall back to forward + whole stitch; and the
+overlap-only stitch on its own against the oracle, in its bf16 form and in the
+forms where it stitches the whole face."""
 import numpy as np
 import pytest
 import torch
