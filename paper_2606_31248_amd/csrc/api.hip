@@ -408,6 +408,7 @@ strata_status strata_na3d_fwd_stitch(const strata_na3d_desc* desc, const strata_
   if (lse) REQUIRE(aligned16(lse), "lse: not 16-byte aligned");
   REQUIRE((int64_t)nty * ntx == desc->B, "fwd_stitch: the batch (%d tiles) is not the %d x %d tiling", desc->B,
           nty, ntx);
+  REQUIRE((int64_t)desc->heads * desc->Z < ((int64_t)1 << 31), "fwd_stitch: heads * Z planes exceed 32 bits");
   const int32_t P = desc->heads * desc->Z, Ht = desc->H, Wt = desc->W, C = desc->head_dim;
   st = check_tiling(nty, ntx, P, Ht, Wt, C, stride_y, stride_x, Hf, Wf, desc->dtype);
   if (st != STRATA_OK) return st;

@@ -255,6 +255,10 @@ def test_fwd_stitch_rules():
     assert call(face=None) == B.STRATA_ERR_INVALID_ARG
     assert call(face=fake(0x10008)) == B.STRATA_ERR_INVALID_ARG     # misaligned
     assert call(dd=desc(B=4, window=(2, 7, 7))) == B.STRATA_ERR_INVALID_ARG
+    # heads * Z beyond 32 bits (a descriptor the attention calls accept)
+    big = desc(B=4, heads=1 << 16, Z=(1 << 16) + 1, H=1, W=1, head_dim=32, window=(1, 1, 1))
+    assert call(nty=2, ntx=2, sy=1, sx=1, Hf=2, Wf=2, dd=big) == B.STRATA_ERR_INVALID_ARG
+    assert b"32 bits" in B.load().strata_last_error()
     assert L.strata_tile_blend_overlap(p, 9, 9, 4, 64, 64, 64, 56, 56, p, p, 511, 512, B.STRATA_BF16,
                                        None) == B.STRATA_ERR_INVALID_ARG
     assert L.strata_tile_blend_overlap(p, 9, 9, 4, 64, 64, 64, 56, 56, None, p, 512, 512, B.STRATA_BF16,
