@@ -216,6 +216,31 @@ def cpu_baseline(wl, tiles_sample: int):
                       f"{wl.B} tiles (all {wl.heads} heads x {wl.N} tokens; blend not included)"}
 
 
+def cpu_one_thread() -> dict:
+    """The oracle on one thread: the whole tiny float32 forward (C1) and one of the
+    eight tiles of the bf16 forward with StereoRoPE (C2, scaled to all eight)."""
+    import oracle
+    from oracle import geometry as G
+    from paper_2606_31248_amd import inputs as I
+    res = {}
+    n0 = oracle.num_threads()
+    oracle.set_num_threads(1)
+    try:
+        for key, wl, tiles in (("C1", I.TINY_F32, 1), ("C2", I.SMALL_BF16, 1)):
+            pl = wl.placement()
+            qkv = tuple(oracle.widen(x[:tiles], wl.dtype) for x in wl.qkv())
+            t0 = time.perf_counter()
+            c = G.tile_coords(pl.face[:tiles], pl.oy[:tiles], pl.ox[:tiles], wl.H, wl.W).astype(np.float32)
+            oracle.na3d_fwd(*qkv, (wl.kz, wl.ky, wl.kx), wl.scale, coords=c)
+            dt = (time.perf_counter() - t0) * wl.B / tiles
+            flops = 4.0 * wl.B * wl.heads * wl.N * wl.K * wl.d
+            res[key] = {"seconds": round(dt, 4), "tflops": flops / dt / 1e12, "cores": 1,
+                        "sample": f"{tiles} of {wl.B} tiles, scaled to all" if tiles < wl.B else "whole workload"}
+    finally:
+        oracle.set_num_threads(n0)
+    return res
+
+
 def train_tile(steps: int):
     """Forward and backward of the 16-tile 5x9x9 training tile (StereoRoPE on), and
     the standalone rotation of its Q and K; HIP-event times on the current stream."""
@@ -462,6 +487,376 @@ def duo_padding(steps: int) -> dict:
             "alg_bytes": nbytes}
 
 
+def _seeded_device(wl, dev, gen_seed=None):
+    """q, k, v (and dO) of a workload on the device: N(0,1) bf16 drawn on the device
+    from a seeded generator (the time does not depend on the values)."""
+    import torch
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(wl.seed if gen_seed is None else gen_seed)
+    dt = torch.float32 if wl.dtype == "f32" else torch.bfloat16
+    return tuple(torch.randn(wl.shape(), generator=gen, device=dev).to(dt) for _ in range(4))
+
+
+def profile_workload(name: str, steps: int, warmup: int) -> dict:
+    """Run one kernel call of one workload `warmup + steps` times and nothing else
+    (no oracle, no side measurements): the target of rocprofv3 counter runs.
+
+    Names: face_step (the timed step of the default run), c1 .. c3 (forwards of
+    the tiny, 8-tile and training-tile workloads), c4 (the training-tile
+    backward), paper16_fwd / paper16_bwd (9x9x9 at 24 levels on 16x16-token
+    tiles), paper32_fwd / paper32_bwd, z24_fwd (3x7x7 at 24 levels),
+    rope (the standalone rotation of the training tile's Q), blend (the whole
+    stitch of the face tiling), duo (the planned Duo padding)."""
+    import torch
+    from paper_2606_31248_amd import binding as Bd
+    from paper_2606_31248_amd import inputs as I
+    from paper_2606_31248_amd import pipeline as Pp
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    Bd.load()
+    fwd_wl = {"c1": I.TINY_F32, "c2": I.SMALL_BF16, "c3": I.TRAIN_TILE, "paper16_fwd": I.PAPER_TILE16,
+              "paper32_fwd": I.PAPER_TILE32, "z24_fwd": I.Z24_TILE}
+    bwd_wl = {"c4": I.TRAIN_TILE_BWD, "paper16_bwd": I.PAPER_TILE16, "paper32_bwd": I.PAPER_TILE32}
+    if name in fwd_wl or name in bwd_wl or name == "rope":
+        wl = fwd_wl.get(name) or bwd_wl.get(name) or I.TRAIN_TILE
+        q, k, v, g = _seeded_device(wl, dev)
+        geom = Pp.TileGeometry(*(torch.from_numpy(x).to(dev) for x in wl.placement().as_int32()))
+        _, cs = Pp.stereo_phases(geom, wl.H, wl.W, wl.d)
+        desc = Bd.desc_for(q, (wl.kz, wl.ky, wl.kx), wl.scale)
+        out = torch.empty_like(q)
+        lse = torch.empty(wl.shape()[:-1], dtype=torch.float32, device=dev)
+        if name == "rope":
+            fn = lambda: Bd.strata_stereorope_apply(q, out, cs)
+        elif name in fwd_wl:
+            fn = lambda: Bd.strata_na3d_fwd(desc, q, k, v, cs, out, lse)
+        else:
+            Bd.strata_na3d_fwd(desc, q, k, v, cs, out, lse)
+            ws = torch.empty(Bd.strata_na3d_bwd_workspace_size(desc), dtype=torch.uint8, device=dev)
+            dq, dk, dv = (torch.empty_like(q) for _ in range(3))
+            fn = lambda: Bd.strata_na3d_bwd(desc, q, k, v, cs, out, g, lse, dq, dk, dv, ws)
+    elif name in ("face_step", "blend"):
+        wl = I.FACE_ROLLOUT
+        nty, ntx, sy, sx = wl.tiling
+        Hf, Wf = (nty - 1) * sy + wl.H, (ntx - 1) * sx + wl.W
+        q, k, v, _ = _seeded_device(wl, dev)
+        geom = Pp.TileGeometry(*(torch.from_numpy(x).to(dev) for x in wl.placement().as_int32()))
+        win = torch.from_numpy(I.ramp_window_2d(wl.H, wl.W, I.FACE_OVERLAP)).to(dev)
+        face = torch.empty((wl.heads * wl.Z, Hf, Wf, wl.d), dtype=torch.bfloat16, device=dev)
+        out = torch.empty_like(q)
+        coords = torch.empty((wl.B, wl.H, wl.W, 2), dtype=torch.float32, device=dev)
+        cs = torch.empty((wl.B, wl.H, wl.W, wl.d // 2, 2), dtype=torch.float32, device=dev)
+        if name == "blend":
+            planes = q.view(wl.B, wl.heads * wl.Z, wl.H, wl.W, wl.d)
+            fn = lambda: Bd.strata_tile_blend(planes, nty, ntx, sy, sx, win, face)
+        else:
+            fn = lambda: Pp.face_step(q, k, v, geom, (wl.kz, wl.ky, wl.kx), wl.scale, wl.tiling, win, face,
+                                      coords=coords, cs=cs, out=out, fused=True)
+    elif name == "duo":
+        n, h, P, C = 2048, 16, 8, 4
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(1011)
+        faces = torch.randn((6, P, n, n, C), generator=gen, device=dev).to(torch.bfloat16)
+        padded = torch.empty((6, P, n + 2 * h, n + 2 * h, C), dtype=torch.bfloat16, device=dev)
+        plan = torch.empty(Bd.strata_duo_plan_bytes(n, h), dtype=torch.uint8, device=dev)
+        Bd.strata_duo_plan(n, h, plan)
+        fn = lambda: Bd.strata_duo_pad_planned(faces, h, plan, padded)
+    else:
+        raise SystemExit(f"unknown profile workload {name!r}")
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    ms = _timed(fn, steps)
+    return {"profile_workload": name, "steps": steps, "warmup": warmup, "ms_mean": round(ms, 4)}
+
+
+# ---- the workloads C1-C4 on the GPU, and the parity of every timed output -------
+# The GPU half (config_runs) times each workload and keeps a seeded sample of its
+# outputs on the host; the CPU leg (cpu_leg) evaluates the oracle on those same
+# samples and on the sampled face cells of the timed step, and times the oracle.
+
+BF16_RULE = 2e-2      # max |gpu - oracle| <= 2e-2 RMS(oracle) for bf16 results
+F32_RULE = 1e-5       # max |gpu - oracle| for float32 results
+
+
+def _half_ulp_bf16(a: np.ndarray) -> np.ndarray:
+    """Half a bf16 ulp of every exact value: the error of storing it in bf16 at all."""
+    a = np.abs(a)
+    e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
+    return np.where(a > 0, np.exp2(e - 8), 0.0)
+
+
+def parity_bf16(got: np.ndarray, ref: np.ndarray, carried=None) -> dict:
+    """The bf16 rule as written (max |err| / RMS(ref) <= 2e-2) and as applied by the
+    tests: beyond half a bf16 ulp of the exact value (the rounding of storing it at
+    all) plus `carried` (rounding the value inherits, e.g. the tiles' own storage
+    rounding carried through the stitch)."""
+    got, ref = np.asarray(got, np.float64), np.asarray(ref, np.float64)
+    diff = np.abs(got - ref)
+    rms = float(np.sqrt(np.mean(ref * ref)))
+    excess = diff - _half_ulp_bf16(ref) - (0.0 if carried is None else carried)
+    lit, r11 = float(diff.max()) / rms, float(excess.max()) / rms
+    return {"n_values": int(ref.size), "max_abs_err": float(diff.max()), "rms_ref": rms,
+            "err_over_rms_literal": round(lit, 6), "r11_excess_over_rms": round(r11, 6), "bound": BF16_RULE,
+            "pass_literal": bool(lit <= BF16_RULE), "pass_r11": bool(r11 <= BF16_RULE)}
+
+
+def face_sample_cells(wl, per_plane: int = 16, seed: int = 1105):
+    """Face cells of the face-rollout step to check: on every plane, the face
+    corners, single-cover cells of the corner tile and of an interior tile, and
+    cells of the y-overlap strip, the x-overlap strip and the four-tile corner
+    where the interior tile row/column meets the next one.  Returns (plane, y, x)
+    arrays; every covering tile lies in a small set (corner tiles and the 2 x 2
+    junction), which keeps the oracle's work bounded."""
+    nty, ntx, sy, sx = wl.tiling
+    Hf, Wf = (nty - 1) * sy + wl.H, (ntx - 1) * sx + wl.W
+    ov_y, ov_x = wl.H - sy, wl.W - sx
+    a0, b0 = nty // 2 - 1, ntx // 2 - 1
+    ys1, xs1 = (a0 * sy + ov_y, (a0 + 1) * sy), (b0 * sx + ov_x, (b0 + 1) * sx)   # interior single cover
+    ysov, xsov = ((a0 + 1) * sy, a0 * sy + wl.H), ((b0 + 1) * sx, b0 * sx + wl.W)  # overlap strips
+    regions = [((0, sy), (0, sx), 2), (ys1, xs1, 3), (ysov, xs1, 3), (ys1, xsov, 3), (ysov, xsov, 3)]
+    corners = [(0, 0), (0, Wf - 1), (Hf - 1, 0), (Hf - 1, Wf - 1)]
+    rng = np.random.default_rng(seed)
+    cells = []
+    for p in range(wl.heads * wl.Z):
+        for j in range(per_plane - sum(r[2] for r in regions)):
+            cells.append((p,) + corners[(p * 2 + j) % 4])
+        for (y0, y1), (x0, x1), n in regions:
+            for _ in range(n):
+                cells.append((p, int(rng.integers(y0, y1)), int(rng.integers(x0, x1))))
+    c = np.array(cells, np.int64)
+    return c[:, 0], c[:, 1], c[:, 2]
+
+
+def _covering(y, L, s, n):
+    """Tiles along one axis covering face position y, with the local position."""
+    return [(a, y - a * s) for a in range(n) if 0 <= y - a * s < L]
+
+
+def oracle_rows(oracle, G, qkv_bits, pl, wl, groups, coords_cache=None):
+    """Oracle forward rows for {(tile, head): [flat query index in [Z, H, W]]}: each
+    (tile, head) slice widened on its own, so the full tensors never go to float64."""
+    out = {}
+    cc = {} if coords_cache is None else coords_cache
+    for (t, h), sel in groups.items():
+        if t not in cc:
+            cc[t] = G.tile_coords(pl.face[t:t + 1], pl.oy[t:t + 1], pl.ox[t:t + 1], wl.H, wl.W).astype(np.float32)
+        q, k, v = (oracle.widen(a[t:t + 1, h:h + 1], wl.dtype) for a in qkv_bits)
+        o, lse = oracle.na3d_fwd(q, k, v, (wl.kz, wl.ky, wl.kx), wl.scale, coords=cc[t] if wl.rope else None,
+                                 sel=np.asarray(sel, np.int64))
+        out[(t, h)] = (o, lse)
+    return out
+
+
+def face_parity(wl, qkv_bits, face_rows, cells, win) -> dict:
+    """Parity of the timed step's own face against the oracle: the oracle forward of
+    every covering tile's query of each sampled cell, stitched in float64 with the
+    same weights (ref = sum w o / sum w).  The face stores the stitch of bf16 tile
+    values, so the applied rule also carries the tiles' own storage rounding
+    through the weights."""
+    ref, carried, meta = face_reference(wl, qkv_bits, cells, win)
+    rec = parity_bf16(face_rows, ref, carried)
+    rec.update(meta)
+    return rec
+
+
+def face_reference(wl, qkv_bits, cells, win):
+    """(ref, carried, meta) of face_parity: the oracle's stitched value of every
+    sampled cell [n, d], the tiles' bf16 storage rounding carried through the
+    stitch weights [n, d], and a description of the sample."""
+    import oracle
+    from oracle import geometry as G
+    nty, ntx, sy, sx = wl.tiling
+    pl = wl.placement()
+    P_, Y, X = cells
+    groups, plan = {}, []
+    for p, y, x in zip(P_, Y, X):
+        h, z = divmod(int(p), wl.Z)
+        cov = [(a * ntx + b, ly, lx) for a, ly in _covering(int(y), wl.H, sy, nty)
+               for b, lx in _covering(int(x), wl.W, sx, ntx)]
+        ent = []
+        for t, ly, lx in cov:
+            sel = groups.setdefault((t, h), [])
+            ent.append((t, h, len(sel), float(win[ly * wl.W + lx])))
+            sel.append((z * wl.H + ly) * wl.W + lx)
+        plan.append(ent)
+    rows = oracle_rows(oracle, G, qkv_bits, pl, wl, groups)
+    ref = np.zeros((len(plan), wl.d))
+    carried = np.zeros((len(plan), wl.d))
+    for i, ent in enumerate(plan):
+        wsum = sum(w for *_, w in ent)
+        for t, h, j, w in ent:
+            o = rows[(t, h)][0][j]
+            ref[i] += w * o
+            carried[i] += w * _half_ulp_bf16(o)
+        ref[i] /= wsum
+        carried[i] /= wsum
+    meta = {"n_cells": len(plan), "n_tiles": len({t for t, _ in groups}), "planes": int(len(np.unique(P_))),
+            "cells": "every plane: face corners, single-cover cells of a corner and an interior tile, the "
+                     "y- and x-overlap strips and the 4-tile corner of an interior junction"}
+    return ref, carried, meta
+
+
+def _flush_mall(buf):
+    """Overwrite a 1 GiB buffer: evicts the 256 MB last-level cache (MALL) between timed launches."""
+    buf.fill_(1)
+
+
+def config_runs(steps: int) -> dict:
+    """C1-C4 of the workload list on the GPU, with seeded host inputs: times per
+    launch (HIP events on the launch stream) and, for the CPU leg, the outputs
+    to check (C1, C2 whole; C3, C4 sampled rows)."""
+    import torch
+    from paper_2606_31248_amd import binding as Bd
+    from paper_2606_31248_amd import inputs as I
+    from paper_2606_31248_amd import pipeline as Pp
+    dev = torch.device("cuda:0")
+    rng = np.random.default_rng(2024)
+    runs = {}
+
+    def to_dev(bits, dtype):
+        if dtype == "bf16":
+            return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(bits).to(dev)
+
+    def fwd_setup(wl, mult=1.0):
+        qkv = tuple(I.gaussian(wl.shape(), wl.seed, s, wl.dtype, mult) for s in (I.STREAM_Q, I.STREAM_K, I.STREAM_V))
+        q, k, v = (to_dev(x, wl.dtype) for x in qkv)
+        geom = Pp.TileGeometry(*(torch.from_numpy(x).to(dev) for x in wl.placement().as_int32()))
+        _, cs = Pp.stereo_phases(geom, wl.H, wl.W, wl.d)
+        out = torch.empty_like(q)
+        lse = torch.empty(wl.shape()[:-1], dtype=torch.float32, device=dev)
+        return qkv, (q, k, v), cs, out, lse
+
+    def sample(wl, n_groups, per_group):
+        """(tile, head) groups and flat query indices inside [Z, H, W]."""
+        N = wl.Z * wl.H * wl.W
+        th = rng.choice(wl.B * wl.heads, size=min(n_groups, wl.B * wl.heads), replace=False)
+        return {(int(x) // wl.heads, int(x) % wl.heads): np.sort(rng.choice(N, per_group, replace=False))
+                for x in th}
+
+    def rows_of(t, groups, wl):
+        idx = np.concatenate([(t_ * wl.heads + h) * wl.Z * wl.H * wl.W + sel for (t_, h), sel in groups.items()])
+        flat = t.reshape(-1, wl.d)
+        return flat.index_select(0, torch.from_numpy(idx).to(dev)).float().cpu().numpy().astype(np.float64)
+
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    for key, wl, mult, scale in (("C1", I.TINY_F32, 1.0, None), ("C2", I.SMALL_BF16, 1.0, None),
+                                 ("C2_literal", I.SMALL_BF16, 1.0 / 8.0, None), ("C3", I.TRAIN_TILE, 1.0, None)):
+        qkv, (q, k, v), cs, out, lse = fwd_setup(wl, mult)
+        desc = Bd.desc_for(q, (wl.kz, wl.ky, wl.kx), wl.scale if scale is None else scale)
+        fn = lambda: Bd.strata_na3d_fwd(desc, q, k, v, cs, out, lse)
+        warm = _timed(fn, steps)
+        st = torch.cuda.current_stream()
+        ts = []
+        for _ in range(max(steps, 5)):  # each launch after a cache flush
+            _flush_mall(flush)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(st)
+            fn()
+            e1.record(st)
+            ts.append((e0, e1))
+        torch.cuda.synchronize()
+        cold = float(np.mean([a.elapsed_time(b) for a, b in ts]))
+        n = wl.B * wl.heads * wl.N
+        flops = 4.0 * n * wl.K * wl.d
+        nbytes = n * (4 * wl.d * (4 if wl.dtype == "f32" else 2) + 4)
+        r = {"workload": wl.name + (" (inputs x 1/8 as well: the literal reading of 'scaled by 1/sqrt(64)')"
+                                    if key == "C2_literal" else ""),
+             "ms": round(cold, 4), "ms_cache_warm": round(warm, 4), "timing": "mean of HIP-event times, each "
+             "launch after a 1 GiB write that evicts the 256 MB MALL; ms_cache_warm: back-to-back launches",
+             "tflops": round(flops / cold / 1e9, 2), "tokens_per_s": round(wl.B * wl.N / (cold * 1e-3), 1),
+             "pct_bf16_peak": round(100 * flops / cold / 1e9 / PEAK_BF16_TFLOPS, 3),
+             "roofline": roofline_row(flops, nbytes, cold), "dtype": wl.dtype}
+        if key in ("C1", "C2", "C2_literal"):   # checked whole
+            r["_got"] = (out.float().cpu().numpy().astype(np.float64), lse.cpu().numpy().astype(np.float64))
+        else:
+            groups = sample(wl, 32, 32)
+            r["_groups"] = groups
+            r["_got"] = (rows_of(out, groups, wl), None)
+        r["_qkv"], r["_wl"] = qkv, wl
+        r["_scale"] = wl.scale if scale is None else scale
+        runs[key] = r
+        del q, k, v, out, lse, cs
+        torch.cuda.empty_cache()
+    del flush
+    # C4: the training-tile backward (forward first for out and lse)
+    wl = I.TRAIN_TILE_BWD
+    qkv, (q, k, v), cs, out, lse = fwd_setup(wl)
+    dob = wl.dout()
+    g = to_dev(dob, wl.dtype)
+    desc = Bd.desc_for(q, (wl.kz, wl.ky, wl.kx), wl.scale)
+    Bd.strata_na3d_fwd(desc, q, k, v, cs, out, lse)
+    ws = torch.empty(Bd.strata_na3d_bwd_workspace_size(desc), dtype=torch.uint8, device=dev)
+    dq, dk, dv = (torch.empty_like(q) for _ in range(3))
+    ms = _timed(lambda: Bd.strata_na3d_bwd(desc, q, k, v, cs, out, g, lse, dq, dk, dv, ws), steps)
+    n = wl.B * wl.heads * wl.N
+    flops, nbytes = 10.0 * n * wl.K * wl.d, n * (8 * wl.d * 2 + 4)
+    gq, gk = sample(wl, 16, 16), sample(wl, 16, 16)
+    runs["C4"] = {"workload": wl.name, "ms": round(ms, 4), "tflops": round(flops / ms / 1e9, 2),
+                  "pct_bf16_peak": round(100 * flops / ms / 1e9 / PEAK_BF16_TFLOPS, 3),
+                  "roofline": roofline_row(flops, nbytes, ms), "dtype": wl.dtype,
+                  "flops_model": "10 B h N K d (QK^T twice, dO.V^T, P^T.dO, dS.K, dS^T.Q)",
+                  "_groups": (gq, gk), "_got": (rows_of(dq, gq, wl), rows_of(dk, gk, wl), rows_of(dv, gk, wl)),
+                  "_qkv": qkv, "_dout": dob, "_wl": wl, "_scale": wl.scale}
+    del q, k, v, out, lse, cs, g, ws, dq, dk, dv
+    torch.cuda.empty_cache()
+    return runs
+
+
+def config_parity(runs: dict) -> dict:
+    """The oracle on every config's checked outputs (CPU leg)."""
+    import oracle
+    from oracle import geometry as G
+    res = {}
+    for key, r in runs.items():
+        wl, qkv = r["_wl"], r["_qkv"]
+        pl = wl.placement()
+        window = (wl.kz, wl.ky, wl.kx)
+        if key in ("C1", "C2", "C2_literal"):
+            c32 = G.tile_coords(pl.face, pl.oy, pl.ox, wl.H, wl.W).astype(np.float32)
+            ro, rl = oracle.na3d_fwd(*(oracle.widen(a, wl.dtype) for a in qkv), window, r["_scale"], coords=c32)
+            got, gl = r["_got"]
+            if wl.dtype == "f32":
+                err = float(np.max(np.abs(got - ro)))
+                par = {"n_values": int(ro.size), "max_abs_err": err, "bound": F32_RULE, "pass": bool(err <= F32_RULE)}
+            else:
+                par = parity_bf16(got, ro)
+            par["lse_max_abs_err"] = float(np.max(np.abs(gl - rl)))
+            par["checked"] = "every output of the launch"
+        elif key == "C3":
+            rows = oracle_rows(oracle, G, qkv, pl, wl, r["_groups"])
+            ref = np.concatenate([rows[g][0] for g in r["_groups"]])
+            par = parity_bf16(r["_got"][0], ref)
+            par["checked"] = f"{ref.shape[0]} query rows of {len(r['_groups'])} (tile, head) pairs"
+        else:  # C4
+            gq, gk = r["_groups"]
+            refs = {"dq": [], "dk": [], "dv": []}
+            cc = {}
+            for (t, h), sel in gq.items():
+                s = slice(t, t + 1), slice(h, h + 1)
+                if t not in cc:
+                    cc[t] = G.tile_coords(pl.face[t:t + 1], pl.oy[t:t + 1], pl.ox[t:t + 1], wl.H,
+                                          wl.W).astype(np.float32)
+                dq, _, _ = oracle.na3d_bwd(*(oracle.widen(a[s], wl.dtype) for a in qkv + (r["_dout"],)), window,
+                                           wl.scale, coords=cc[t], selq=sel, selk=sel[:1])
+                refs["dq"].append(dq)
+            for (t, h), sel in gk.items():
+                s = slice(t, t + 1), slice(h, h + 1)
+                if t not in cc:
+                    cc[t] = G.tile_coords(pl.face[t:t + 1], pl.oy[t:t + 1], pl.ox[t:t + 1], wl.H,
+                                          wl.W).astype(np.float32)
+                _, dk, dv = oracle.na3d_bwd(*(oracle.widen(a[s], wl.dtype) for a in qkv + (r["_dout"],)), window,
+                                            wl.scale, coords=cc[t], selq=sel[:1], selk=sel)
+                refs["dk"].append(dk)
+                refs["dv"].append(dv)
+            par = {name: parity_bf16(got, np.concatenate(refs[name]))
+                   for name, got in zip(("dq", "dk", "dv"), r["_got"])}
+            par["checked"] = (f"{sum(len(x) for x in gq.values())} dq rows of {len(gq)} and "
+                              f"{sum(len(x) for x in gk.values())} dk, dv rows of {len(gk)} (tile, head) pairs")
+        res[key] = par
+    return res
+
+
 def _done(what: str, t_start: float) -> None:
     """One progress line on stderr per finished measurement (stdout carries only the result)."""
     print(f"bench: {what} done at {time.perf_counter() - t_start:.1f} s", file=sys.stderr, flush=True)
@@ -484,6 +879,8 @@ def main():
     ap.add_argument("--cpu-tiles", type=int, default=32, help="tiles in the CPU-oracle sample (0: skip)")
     ap.add_argument("--train-steps", type=int, default=5,
                     help="timed passes of the training-tile forward/backward side measurement (0: skip)")
+    ap.add_argument("--config-steps", type=int, default=5,
+                    help="timed launches of each of the workloads C1-C4 (0: skip them)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run one 1 GiB device copy (HBM counter calibration)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -494,7 +891,12 @@ def main():
                     help="write the kernel-trace summary of a rocprofv3 --stats run to profiles/ and exit")
     ap.add_argument("--command", action="append", default=[],
                     help="the profiler command(s) the summary records")
+    ap.add_argument("--profile", metavar="WORKLOAD",
+                    help="run only one kernel call of one workload (see profile_workload) and exit")
     a = ap.parse_args()
+    if a.profile:
+        print(json.dumps(profile_workload(a.profile, a.steps, a.warmup)), flush=True)
+        return
     if a.summarize_pmc:
         rec = summarize_pmc(a.summarize_pmc[0], a.summarize_pmc[1], a.command)
         with open(PMC_FILE, "w") as f:
@@ -537,7 +939,8 @@ def main():
     def to_dev(bits):
         return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(dev)
 
-    q, k, v = (to_dev(x) for x in wl.qkv())
+    qkv_host = wl.qkv()
+    q, k, v = (to_dev(x) for x in qkv_host)
     pl = wl.placement()
     geom = Pp.TileGeometry(*(torch.from_numpy(x).to(dev) for x in pl.as_int32()))
     win = torch.from_numpy(I.ramp_window_2d(wl.H, wl.W, I.FACE_OVERLAP)).to(dev)
@@ -563,7 +966,7 @@ def main():
         if record:
             e[0].record(st)
         Bd.strata_stereo_coords(geom.face, geom.oy, geom.ox, wl.H, wl.W, geom.face_cells, geom.patch,
-                                Pp.l_scale(geom.face_cells), coords)
+                                0.0, coords)
         Bd.strata_stereorope_phases(coords, wl.d, Pp.ROPE_BASE, cs)
         if record:
             e[1].record(st)
@@ -588,6 +991,10 @@ def main():
     ms_step = (t1 - t0) * 1e3 / a.steps
     avg = {n: float(np.mean([s.elapsed_time(e) for s, e in lst])) for n, lst in ev.items()}
     _done("face-rollout step", t_start)
+    # the timed step's own output at the sampled cells (checked against the oracle in the CPU leg)
+    cells = face_sample_cells(wl)
+    cidx = torch.from_numpy((cells[0] * Hf + cells[1]) * Wf + cells[2]).to(dev)
+    face_rows = face.view(-1, wl.d).index_select(0, cidx).float().cpu().numpy().astype(np.float64)
 
     flops = 4.0 * wl.B * wl.heads * wl.N * wl.K * wl.d
     tflops_step = flops / (ms_step * 1e-3) / 1e12
@@ -680,9 +1087,38 @@ def main():
         torch.cuda.empty_cache()
         res["rows"]["f3_duo_pad_faces"] = duo_padding(a.train_steps)
         _done("duo padding", t_start)
+    if a.train_steps <= 0:
+        del q, k, v, out, face, coords, cs
+        torch.cuda.empty_cache()
+    runs = None
+    if a.config_steps > 0:
+        runs = config_runs(a.config_steps)
+        _done("configs C1-C4", t_start)
     if a.cpu_tiles > 0:
+        # CPU leg: the oracle timed on a sample, and evaluated on the outputs sampled above
+        import oracle
+        res["parity"] = face_parity(wl, qkv_host, face_rows, cells, I.ramp_window_2d(wl.H, wl.W, I.FACE_OVERLAP))
+        _done("face parity", t_start)
         res["cpu_baseline"] = cpu_baseline(wl, a.cpu_tiles)
+        res["cpu_baseline"]["host_cpus"] = os.cpu_count()
+        res["cpu_baseline"]["one_thread"] = cpu_one_thread()
         _done("cpu baseline", t_start)
+        if runs is not None:
+            par = config_parity(runs)
+            _done("config parity", t_start)
+    if runs is not None:
+        res["configs"] = {}
+        for key, r in runs.items():
+            ent = {k2: v2 for k2, v2 in r.items() if not k2.startswith("_")}
+            if a.cpu_tiles > 0:
+                ent["parity"] = par[key]
+            res["configs"][key] = ent
+        c5 = {"workload": wl.name, "ms": round(ms_step, 4), "tflops": round(tflops_step, 2),
+              "tokens_per_s": round(tokens / (ms_step * 1e-3), 1), "roofline": res["roofline"],
+              "note": "the timed face step of this line (value)"}
+        if "parity" in res:
+            c5["parity"] = res["parity"]
+        res["configs"]["C5"] = c5
     print(json.dumps(res), flush=True)
 
 

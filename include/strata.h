@@ -66,7 +66,9 @@ typedef struct {
  * (tile_oy[b] + y, tile_ox[b] + x) on face tile_face[b] (0..5).  Its
  * (lat, lon) is projected stereographically about the tile centre (the point
  * at the mean angles of the tile's first and last token) and divided by
- * l_scale (sqrt(4 pi / N_total) in Eq. 1):
+ * l_scale, Eq. 1's length sqrt(4 pi / N_total); l_scale == 0 selects
+ * sqrt(4 pi / (6 face_cells^2)) (N_total = the native cells of the six faces),
+ * any other value must be finite and > 0:
  *   coords[b, y, x, 0] = x_east / l_scale,  coords[b, y, x, 1] = y_north / l_scale.
  * Face f with a = tan(alpha) (columns), c = tan(beta) (rows) is the cube point
  *   0:(1,a,c) 1:(-a,1,c) 2:(-1,-a,c) 3:(a,-1,c) 4:(-c,a,1) 5:(c,a,-1).
@@ -125,8 +127,18 @@ strata_status strata_stereorope_apply(const void* x, void* y, const float* cs, i
  * [B, H, W, head_dim/2, 2]), or the identity when cs == NULL.
  * q, k, v, out: [B, heads, Z, H, W, head_dim] of desc->dtype;
  * lse: float32 [B, heads, Z, H, W] (natural log) or NULL when not needed.
- * Supported: f32 with head_dim in {32, 64}; bf16 with head_dim in {32, 64}
- * (bf16 MFMA path for head_dim 64).  Softmax and accumulation in float32. */
+ * Supported: head_dim 32, 64 or 128 in either dtype.  Kernels: bf16 at
+ * head_dim 64 runs on MFMA for the windows (3,7,7), (5,9,9), (9,9,9) and every
+ * column window (kz,1,1) with Z <= 32; bf16 at head_dim 128 on MFMA for (9,9,9);
+ * every other case (f32, head_dim 32, other windows) on a plain per-query
+ * kernel in float32.  Softmax and accumulation in float32.
+ * Contraction precision: on the MFMA paths the logits q.k are float16 products
+ * (wider mantissa than bf16) of float16 copies of the rotated, normalised and
+ * scaled q and k, accumulated in float32; P.V is a bf16 product.  Input range:
+ * with M = max(1, 2 scale log2(e)), inputs with M |q| <= 32000 and
+ * M |k| <= 32000 (q^, k^ after the QK norm) keep every float16 operand inside
+ * its range; beyond that each path saturates its float16 copies (results stay
+ * finite) and the paths may give different results. */
 strata_status strata_na3d_fwd(const strata_na3d_desc* desc, const void* q, const void* k,
                               const void* v, const float* cs, void* out, float* lse,
                               void* stream);
@@ -138,7 +150,9 @@ strata_status strata_na3d_fwd(const strata_na3d_desc* desc, const void* q, const
  *   dv_j = sum_{i: j in N(i)} P_ij dout_i,    dS_ij = P_ij (<dout_i, v_j> - D_i),
  *   dq_i = R_i^T scale sum_j dS_ij R_j k_j,    dk_j = R_j^T scale sum_i dS_ij R_i q_i.
  * Deterministic (no atomics).  workspace: device memory of at least
- * strata_na3d_bwd_workspace_size(desc) bytes (holds D), owned by the caller. */
+ * strata_na3d_bwd_workspace_size(desc) bytes (holds D), owned by the caller.
+ * Kernels and input range as strata_na3d_fwd; on the MFMA paths the dS products
+ * (dq, dk) are float16 with exact power-of-two scaling, P.dO and dO.V^T bf16. */
 size_t strata_na3d_bwd_workspace_size(const strata_na3d_desc* desc);
 strata_status strata_na3d_bwd(const strata_na3d_desc* desc, const void* q, const void* k,
                               const void* v, const float* cs, const void* out, const void* dout,
@@ -222,9 +236,9 @@ strata_status strata_tile_blend(const void* tiles, int32_t nty, int32_t ntx, int
  * strata_na3d_fwd_stitch, then strata_tile_blend_overlap with the same tiles,
  * tiling, window and face.  The first writes the attention output (options
  * and lse as in strata_na3d_fwd_ex) and stores every cell that one tile alone
- * covers straight into `face`: there the stitch returns the tile's value
- * (w v / w), or 0 where w = 0, and -0 becomes +0 as the stitch's fused
- * multiply-add from +0 makes it.  The other cells go to `tiles`
+ * covers straight into `face`, computed as the stitch computes it: the tile's
+ * value fma(w, v, +0) / w rounded to the dtype, which for 2^-8 <= w <= 1 (the
+ * linear ramp's range) is v itself with -0 turned into +0, and 0 where w = 0.  The other cells go to `tiles`
  * ([B, heads, Z, H, W, head_dim], caller-owned scratch; the contents of
  * single-cover cells are unspecified).  The second stitches the cells that two
  * or more tiles cover and leaves the rest of the face as it is.  The fusion
@@ -317,9 +331,14 @@ strata_status strata_tile_extract(const void* face, int32_t nty, int32_t ntx, in
                                   int32_t stride_x, int32_t Hf, int32_t Wf, void* tiles,
                                   strata_dtype dtype, void* stream);
 
-/* ---- a3: window indexing of one axis (bit-exact integer export) ------------
- * starts[i]: first position of query i's window; [qlo[j], qhi[j]]: the
- * queries whose window holds position j (contiguous).  Device int32[L] each. */
+/* ---- a3: window indexing of one axis (Sec. 3.2, NATTEN's border-clamped ----
+ * neighbourhood; bit-exact integer export).  For an axis of extent L and
+ * window k (odd with 1 <= k <= L, or k == L): starts[i] = min(max(i - (k-1)/2,
+ * 0), L - k) is the first position of query i's window [starts[i],
+ * starts[i] + k); [qlo[j], qhi[j]] is the contiguous range of queries whose
+ * window holds position j.  starts, qlo, qhi: device int32[L] each, written by
+ * one launch on `stream`; STRATA_ERR_INVALID_ARG for other (L, k) or a NULL /
+ * misaligned pointer, with nothing launched. */
 strata_status strata_na_axis_index(int32_t L, int32_t k, int32_t* starts, int32_t* qlo,
                                    int32_t* qhi, void* stream);
 

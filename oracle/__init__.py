@@ -26,6 +26,9 @@ from . import geometry  # noqa: F401
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "strata_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
+# STRATA_ORACLE_LIB: load another build of the same source instead (the sanitizer
+# run of the host tests builds one); build() always writes _LIB
+_LOAD = os.environ.get("STRATA_ORACLE_LIB") or _LIB
 _lib = None
 
 ROPE_BASE = 100.0
@@ -45,9 +48,9 @@ def build(force: bool = False) -> str:
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB):
+        if _LOAD == _LIB and not os.path.exists(_LIB):
             build()
-        L = ctypes.CDLL(_LIB)
+        L = ctypes.CDLL(_LOAD)
         i32, i64, f64 = ctypes.c_int, ctypes.c_int64, ctypes.c_double
         P = ctypes.c_void_p
         L.oracle_axis_index.argtypes = [i32, i32, P, P, P]
@@ -60,6 +63,8 @@ def lib():
                                          + [P, P, P, P])
         L.oracle_tile_blend.argtypes = [P, i32, i32, i32, i32, i32, i32, i32, i32, P, P, i32, i32, i32]
         L.oracle_tile_extract.argtypes = [P, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32, P, i32]
+        L.oracle_set_num_threads.argtypes = [i32]
+        L.oracle_set_num_threads.restype = None
         for f in ("oracle_axis_index", "oracle_rope_phases", "oracle_rope_apply", "oracle_na3d_fwd", "oracle_na3d_bwd",
                   "oracle_na3d_fwd_ex", "oracle_na3d_bwd_ex", "oracle_tile_blend", "oracle_tile_extract", "oracle_num_threads"):
             getattr(L, f).restype = ctypes.c_int
@@ -69,6 +74,11 @@ def lib():
 
 def num_threads() -> int:
     return int(lib().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's OpenMP loops from now on."""
+    lib().oracle_set_num_threads(int(n))
 
 
 def _p(a: Optional[np.ndarray]):

@@ -660,3 +660,13 @@ int oracle_num_threads(void) {
   return 1;
 #endif
 }
+
+/* Thread count of the OpenMP loops that follow (timing runs on one core). */
+void oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+  extern void omp_set_num_threads(int);
+  omp_set_num_threads(n > 0 ? n : 1);
+#else
+  (void)n;
+#endif
+}

@@ -15,7 +15,8 @@ from typing import Optional
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libstrata.so")
+# STRATA_LIB: another build of the same sources (the sanitizer run of the host tests)
+LIB_PATH = os.environ.get("STRATA_LIB") or os.path.join(_HERE, "libstrata.so")
 
 STRATA_OK, STRATA_ERR_INVALID_ARG, STRATA_ERR_UNSUPPORTED, STRATA_ERR_WORKSPACE, STRATA_ERR_HIP = range(5)
 STRATA_F32, STRATA_BF16 = 0, 1
@@ -116,6 +117,66 @@ def _ptr(t: Optional[torch.Tensor]):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _need(name: str, t, shape=None, dtype=None, device=None, numel=None, optional: bool = False):
+    """Check one tensor argument before its pointer crosses the ABI (which sees no
+    sizes): a contiguous GPU tensor, on `device`, of `dtype`, of exactly `shape`
+    (or at least `numel` elements).  Raises ValueError on any mismatch."""
+    if t is None:
+        if optional:
+            return
+        raise ValueError(f"{name}: a tensor is required")
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name}: expected a torch.Tensor, got {type(t).__name__}")
+    if not t.is_cuda:
+        raise ValueError(f"{name}: must be a GPU tensor (got device {t.device})")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name}: on {t.device}, the other arguments are on {device}")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name}: dtype {t.dtype}, expected {dtype}")
+    if shape is not None and tuple(t.shape) != tuple(int(x) for x in shape):
+        raise ValueError(f"{name}: shape {tuple(t.shape)}, expected {tuple(int(x) for x in shape)}")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{name}: {t.numel()} elements, at least {numel} needed")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
+
+
+def _torch_dtype(code: int):
+    if code == STRATA_BF16:
+        return torch.bfloat16
+    if code == STRATA_F32:
+        return torch.float32
+    raise ValueError(f"unknown strata dtype {code}")
+
+
+def _desc_shape(desc: "NA3DDesc"):
+    return (desc.B, desc.heads, desc.Z, desc.H, desc.W, desc.head_dim)
+
+
+def _check_na_tensors(desc: "NA3DDesc", tensors: dict, cs=None, lse=None, lse_required=False, opts=None,
+                      dgate=None):
+    """q, k, v, out, dout, dq, dk, dv of the problem's shape and dtype on one GPU;
+    cs [B, H, W, head_dim/2, 2] and lse [B, heads, Z, H, W] float32; a gate of
+    the problem's dtype, [B, heads, Z, H, W] or the full shape, and dgate alike."""
+    shape = _desc_shape(desc)
+    dt = _torch_dtype(desc.dtype)
+    first = next(iter(tensors.values()))
+    _need("q", first, shape, dt)
+    dev = first.device
+    for name, t in tensors.items():
+        _need(name, t, shape, dt, dev)
+    _need("cs", cs, (desc.B, desc.H, desc.W, desc.head_dim // 2, 2), torch.float32, dev, optional=True)
+    _need("lse", lse, shape[:-1], torch.float32, dev, optional=not lse_required)
+    gate = getattr(opts, "_keep", None) if opts is not None else None
+    if gate is not None:
+        if tuple(gate.shape) not in (shape[:-1], shape):
+            raise ValueError(f"gate: shape {tuple(gate.shape)}, expected {shape[:-1]} or {shape}")
+        _need("gate", gate, tuple(gate.shape), dt, dev)
+        if dgate is not None or lse_required:
+            _need("dgate", dgate, tuple(gate.shape), dt, dev)
+    return dev
+
+
 def _stream(stream=None):
     if stream is None:
         stream = torch.cuda.current_stream()
@@ -151,6 +212,11 @@ def desc_for(q: torch.Tensor, window, scale) -> NA3DDesc:
 def strata_stereo_coords(tile_face, tile_oy, tile_ox, H, W, face_cells, patch, l_scale, coords,
                          stream=None):
     B = tile_face.shape[0]
+    _need("tile_face", tile_face, (B,), torch.int32)
+    dev = tile_face.device
+    _need("tile_oy", tile_oy, (B,), torch.int32, dev)
+    _need("tile_ox", tile_ox, (B,), torch.int32, dev)
+    _need("coords", coords, (B, H, W, 2), torch.float32, dev)
     _check(load().strata_stereo_coords(_ptr(tile_face), _ptr(tile_oy), _ptr(tile_ox), B, H, W,
                                        face_cells, patch, float(l_scale), _ptr(coords),
                                        _stream(stream)))
@@ -158,17 +224,23 @@ def strata_stereo_coords(tile_face, tile_oy, tile_ox, H, W, face_cells, patch, l
 
 def strata_stereorope_phases(coords, head_dim, base, cs, stream=None):
     B, H, W, _ = coords.shape
+    _need("coords", coords, (B, H, W, 2), torch.float32)
+    _need("cs", cs, (B, H, W, head_dim // 2, 2), torch.float32, coords.device)
     _check(load().strata_stereorope_phases(_ptr(coords), B, H, W, head_dim, float(base), _ptr(cs),
                                            _stream(stream)))
 
 
 def strata_stereorope_apply(x, y, cs, transpose=False, stream=None):
     B, heads, Z, H, W, d = x.shape
+    _need("x", x, x.shape)
+    _need("y", y, x.shape, x.dtype, x.device)
+    _need("cs", cs, (B, H, W, d // 2, 2), torch.float32, x.device)
     _check(load().strata_stereorope_apply(_ptr(x), _ptr(y), _ptr(cs), B, heads, Z, H, W, d,
                                           _dtype(x), int(bool(transpose)), _stream(stream)))
 
 
 def strata_na3d_fwd(desc: NA3DDesc, q, k, v, cs, out, lse=None, stream=None):
+    _check_na_tensors(desc, dict(q=q, k=k, v=v, out=out), cs, lse)
     _check(load().strata_na3d_fwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(cs), _ptr(out),
                                   _ptr(lse), _stream(stream)))
 
@@ -179,6 +251,9 @@ def strata_na3d_bwd_workspace_size(desc: NA3DDesc) -> int:
 
 def strata_na3d_bwd(desc: NA3DDesc, q, k, v, cs, out, dout, lse, dq, dk, dv, workspace,
                     stream=None):
+    dev = _check_na_tensors(desc, dict(q=q, k=k, v=v, out=out, dout=dout, dq=dq, dk=dk, dv=dv), cs, lse,
+                            lse_required=True)
+    _need("workspace", workspace, device=dev, optional=True)
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(load().strata_na3d_bwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(cs), _ptr(out),
                                   _ptr(dout), _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv),
@@ -203,6 +278,7 @@ def _opts_ref(opts: Optional[NA3DOpts]):
 
 
 def strata_na3d_fwd_ex(desc: NA3DDesc, opts: Optional[NA3DOpts], q, k, v, cs, out, lse=None, stream=None):
+    _check_na_tensors(desc, dict(q=q, k=k, v=v, out=out), cs, lse, opts=opts)
     _check(load().strata_na3d_fwd_ex(ctypes.byref(desc), _opts_ref(opts), _ptr(q), _ptr(k), _ptr(v), _ptr(cs),
                                      _ptr(out), _ptr(lse), _stream(stream)))
 
@@ -213,15 +289,27 @@ def strata_na3d_bwd_ex_workspace_size(desc: NA3DDesc, opts: Optional[NA3DOpts]) 
 
 def strata_na3d_bwd_ex(desc: NA3DDesc, opts: Optional[NA3DOpts], q, k, v, cs, out, dout, lse, dq, dk, dv,
                        dgate, workspace, stream=None):
+    dev = _check_na_tensors(desc, dict(q=q, k=k, v=v, out=out, dout=dout, dq=dq, dk=dk, dv=dv), cs, lse,
+                            lse_required=True, opts=opts, dgate=dgate)
+    _need("workspace", workspace, device=dev, optional=True)
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(load().strata_na3d_bwd_ex(ctypes.byref(desc), _opts_ref(opts), _ptr(q), _ptr(k), _ptr(v), _ptr(cs),
                                      _ptr(out), _ptr(dout), _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv),
                                      _ptr(dgate), _ptr(workspace), nbytes, _stream(stream)))
 
 
+def _check_tiling(tiles, nty, ntx, window, out):
+    """tiles [nty*ntx, P, Ht, Wt, C], window float32 of Ht*Wt, out [P, Hf, Wf, C] of the tiles' dtype."""
+    T, P, Ht, Wt, C = tiles.shape
+    _need("tiles", tiles, (nty * ntx, P, Ht, Wt, C))
+    _need("window", window, (Ht * Wt,), torch.float32, tiles.device)
+    _need("out", out, (P, out.shape[1], out.shape[2], C), tiles.dtype, tiles.device)
+
+
 def strata_tile_blend(tiles, nty, ntx, stride_y, stride_x, window, out, stream=None):
     T, P, Ht, Wt, C = tiles.shape
     _, Hf, Wf, _ = out.shape
+    _check_tiling(tiles, nty, ntx, window, out)
     _check(load().strata_tile_blend(_ptr(tiles), nty, ntx, P, Ht, Wt, C, stride_y, stride_x,
                                     _ptr(window), _ptr(out), Hf, Wf, _dtype(tiles), _stream(stream)))
 
@@ -230,6 +318,7 @@ def strata_tile_blend_overlap(tiles, nty, ntx, stride_y, stride_x, window, out, 
     """Stitch of the face cells that two or more tiles cover (the second call of the fused face step)."""
     T, P, Ht, Wt, C = tiles.shape
     _, Hf, Wf, _ = out.shape
+    _check_tiling(tiles, nty, ntx, window, out)
     _check(load().strata_tile_blend_overlap(_ptr(tiles), nty, ntx, P, Ht, Wt, C, stride_y, stride_x,
                                             _ptr(window), _ptr(out), Hf, Wf, _dtype(tiles), _stream(stream)))
 
@@ -238,6 +327,9 @@ def strata_na3d_fwd_stitch(desc: NA3DDesc, opts: Optional[NA3DOpts], q, k, v, cs
                            stride_y, stride_x, window, face, stream=None):
     """Forward of the nty x ntx tiles of one face, cells covered by one tile stored into face [heads*Z, Hf, Wf, d]."""
     _, Hf, Wf, _ = face.shape
+    dev = _check_na_tensors(desc, dict(q=q, k=k, v=v, tiles=tiles), cs, lse, opts=opts)
+    _need("window", window, (desc.H * desc.W,), torch.float32, dev)
+    _need("face", face, (desc.heads * desc.Z, Hf, Wf, desc.head_dim), q.dtype, dev)
     _check(load().strata_na3d_fwd_stitch(ctypes.byref(desc), _opts_ref(opts), _ptr(q), _ptr(k), _ptr(v), _ptr(cs),
                                          _ptr(tiles), _ptr(lse), nty, ntx, stride_y, stride_x, _ptr(window),
                                          _ptr(face), Hf, Wf, _stream(stream)))
@@ -246,11 +338,16 @@ def strata_na3d_fwd_stitch(desc: NA3DDesc, opts: Optional[NA3DOpts], q, k, v, cs
 def strata_tile_extract(face, nty, ntx, stride_y, stride_x, tiles, stream=None):
     P, Hf, Wf, C = face.shape
     _, _, Ht, Wt, _ = tiles.shape
+    _need("face", face, face.shape)
+    _need("tiles", tiles, (nty * ntx, P, Ht, Wt, C), face.dtype, face.device)
     _check(load().strata_tile_extract(_ptr(face), nty, ntx, P, Ht, Wt, C, stride_y, stride_x, Hf, Wf,
                                       _ptr(tiles), _dtype(face), _stream(stream)))
 
 
 def strata_na_axis_index(L, k, starts, qlo, qhi, stream=None):
+    _need("starts", starts, (L,), torch.int32)
+    _need("qlo", qlo, (L,), torch.int32, starts.device)
+    _need("qhi", qhi, (L,), torch.int32, starts.device)
     _check(load().strata_na_axis_index(L, k, _ptr(starts), _ptr(qlo), _ptr(qhi), _stream(stream)))
 
 
@@ -258,18 +355,23 @@ def strata_wind_tile_frame(field, face, nty, ntx, stride_y, stride_x, tiles, str
     """field: [P, n, n, 2] (U, V per cell of one face); tiles: [nty*ntx, P, Ht, Wt, 2]."""
     P, n, _, _ = field.shape
     _, _, Ht, Wt, _ = tiles.shape
+    _need("field", field, (P, n, n, 2))
+    _need("tiles", tiles, (nty * ntx, P, Ht, Wt, 2), field.dtype, field.device)
     _check(load().strata_wind_tile_frame(_ptr(field), int(face), n, nty, ntx, P, Ht, Wt, stride_y, stride_x,
                                          _ptr(tiles), _dtype(field), _stream(stream)))
 
 
 def strata_kbd_window(Ht, Wt, overlap, beta, window, stream=None):
     """window: float32 [Ht * Wt] on the device."""
+    _need("window", window, (Ht * Wt,), torch.float32)
     _check(load().strata_kbd_window(Ht, Wt, overlap, float(beta), _ptr(window), _stream(stream)))
 
 
 def strata_duo_pad(faces, halo, padded, stream=None):
     """faces: [6, P, n, n, C]; padded: [6, P, n + 2 halo, n + 2 halo, C]."""
     _, P, n, _, C = faces.shape
+    _need("faces", faces, (6, P, n, n, C))
+    _need("padded", padded, (6, P, n + 2 * halo, n + 2 * halo, C), faces.dtype, faces.device)
     _check(load().strata_duo_pad(_ptr(faces), P, n, C, int(halo), _ptr(padded), _dtype(faces), _stream(stream)))
 
 
@@ -280,6 +382,7 @@ def strata_duo_plan_bytes(n, halo):
 
 def strata_duo_plan(n, halo, plan, stream=None):
     """plan: a device buffer (e.g. uint8) of at least strata_duo_plan_bytes(n, halo) bytes."""
+    _need("plan", plan)
     _check(load().strata_duo_plan(int(n), int(halo), _ptr(plan), plan.numel() * plan.element_size(),
                                   _stream(stream)))
 
@@ -287,6 +390,9 @@ def strata_duo_plan(n, halo, plan, stream=None):
 def strata_duo_pad_planned(faces, halo, plan, padded, stream=None):
     """As strata_duo_pad, with the neighbours and weights read from a plan."""
     _, P, n, _, C = faces.shape
+    _need("faces", faces, (6, P, n, n, C))
+    _need("plan", plan, device=faces.device)
+    _need("padded", padded, (6, P, n + 2 * halo, n + 2 * halo, C), faces.dtype, faces.device)
     _check(load().strata_duo_pad_planned(_ptr(faces), P, n, C, int(halo), _ptr(plan),
                                          plan.numel() * plan.element_size(), _ptr(padded), _dtype(faces),
                                          _stream(stream)))
@@ -297,6 +403,9 @@ def strata_duo_pad_vjp(grad_padded, halo, plan, grad_faces, stream=None):
     grad_faces [6, P, n, n, C], through a plan built for (n, halo)."""
     _, P, m, _, C = grad_padded.shape
     n = m - 2 * int(halo)
+    _need("grad_padded", grad_padded, (6, P, m, m, C))
+    _need("plan", plan, device=grad_padded.device)
+    _need("grad_faces", grad_faces, (6, P, n, n, C), grad_padded.dtype, grad_padded.device)
     _check(load().strata_duo_pad_vjp(_ptr(grad_padded), P, n, C, int(halo), _ptr(plan),
                                      plan.numel() * plan.element_size(), _ptr(grad_faces), _dtype(grad_padded),
                                      _stream(stream)))

@@ -137,6 +137,13 @@ static size_t bwd_workspace_impl(const strata_na3d_desc* desc, const strata_na3d
   return bwd_layout(*desc, o).total;
 }
 
+// The backward's kernels after the arguments have been checked: D (and, with a
+// gate, dA) live in `ws`, laid out as bwd_layout says.
+static strata_status na3d_bwd_launch(const strata_na3d_desc* desc, const strata_na3d_opts* opts, const NaOpts& o,
+                                     const void* q, const void* k, const void* v, const float* cs, const void* out,
+                                     const void* dout, const float* lse, void* dq, void* dk, void* dv, void* dgate,
+                                     char* ws, hipStream_t s);
+
 static strata_status na3d_bwd_impl(const strata_na3d_desc* desc, const strata_na3d_opts* opts,
                                    const void* q, const void* k, const void* v, const float* cs,
                                    const void* out, const void* dout, const float* lse, void* dq,
@@ -163,8 +170,15 @@ static strata_status na3d_bwd_impl(const strata_na3d_desc* desc, const strata_na
     return set_error(STRATA_ERR_WORKSPACE, "workspace: need %zu bytes, got %zu", L.total,
                      workspace ? workspace_bytes : (size_t)0);
   REQUIRE(aligned16(workspace), "workspace: not 16-byte aligned");
-  hipStream_t s = (hipStream_t)stream;
-  char* ws = static_cast<char*>(workspace);
+  return na3d_bwd_launch(desc, opts, o, q, k, v, cs, out, dout, lse, dq, dk, dv, dgate, static_cast<char*>(workspace),
+                         (hipStream_t)stream);
+}
+
+static strata_status na3d_bwd_launch(const strata_na3d_desc* desc, const strata_na3d_opts* opts, const NaOpts& o,
+                                     const void* q, const void* k, const void* v, const float* cs, const void* out,
+                                     const void* dout, const float* lse, void* dq, void* dk, void* dv, void* dgate,
+                                     char* ws, hipStream_t s) {
+  const BwdLayout L = bwd_layout(*desc, o);
   float* dvec = reinterpret_cast<float*>(ws + L.dvec);
   // the attention backward runs with upstream gradient dA (dO without a gate);
   // QK RMSNorm happens inside its kernels
@@ -229,7 +243,9 @@ strata_status strata_stereo_coords(const int32_t* tile_face, const int32_t* tile
           "coords: face_cells must be a positive multiple of patch");
   REQUIRE(H * (int64_t)patch <= face_cells && W * (int64_t)patch <= face_cells,
           "coords: tile larger than the face");
-  REQUIRE(l_scale > 0.0 && isfinite(l_scale), "coords: l_scale must be finite and > 0");
+  REQUIRE(l_scale == 0.0 || (l_scale > 0.0 && isfinite(l_scale)), "coords: l_scale must be 0 or finite and > 0");
+  // Eq. 1's length sqrt(4 pi / N_total), N_total = the native cells of the six faces
+  if (l_scale == 0.0) l_scale = sqrt(4.0 * M_PI / (6.0 * (double)face_cells * (double)face_cells));
   REQUIRE_PTR(tile_face);
   REQUIRE_PTR(tile_oy);
   REQUIRE_PTR(tile_ox);

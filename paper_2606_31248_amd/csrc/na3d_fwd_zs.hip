@@ -57,8 +57,10 @@
 // insert.
 //
 // Input range: K is converted to float16 with round-toward-zero before its
-// rotation (bf16 values convert exactly; beyond +-65504 they saturate); the
-// rotated, scaled Q saturates at +-65504.
+// rotation (bf16 values up to +-65504 convert exactly, larger ones saturate) and
+// rotated by phases of half length (c/2, s/2), so a rotated pair stays below
+// 65504 sqrt(2) / 2 and never overflows; the queries carry the factor 2 instead:
+// 2 scale log2(e) q is rounded to float16, saturating at +-65504.
 //
 // Options (App. B.5).  QK RMSNorm: the factor (mean square + eps)^(-1/2) of a
 // query comes from the sums of squares of the 4 lanes holding its row, that of
@@ -148,7 +150,7 @@ struct ZArgs {
   float* lse;         // optional
   int heads, H, W;
   int n_yb, n_xb, n_hg, hpw;
-  float qscale;       // scale * log2(e)
+  float qscale;       // 2 scale log2(e) (K enters at half length)
   // options: QK RMSNorm (eps) and the sigmoid output gate
   float eps;
   const uint16_t* gate;
@@ -169,6 +171,14 @@ __device__ __forceinline__ uint32_t plus_zero2(uint32_t w) {
   const uint32_t m = w & 0x7fff7fffu;
   const uint32_t keep = ((m + 0x7fff7fffu) & 0x80008000u) | 0x7fff7fffu;
   return w & keep;
+}
+
+// The stitch of a bf16 pair that one tile alone covers with weight w > 0, as
+// the stitch computes it: fma(w, v, +0) / w, correctly rounded, to bf16.
+__device__ __forceinline__ uint32_t stitch_one2(uint32_t v, float w) {
+  const float lo = __builtin_fmaf(w, lo_bf16(v), 0.f) / w;
+  const float hi = __builtin_fmaf(w, hi_bf16(v), 0.f) / w;
+  return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
 }
 
 // Rotate 4 pairs of K held as packed bf16x2 words by packed float16 phases
@@ -229,7 +239,8 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
   const bool in_grid = qy_raw < H && qx_raw < W;
   // stitch: a cell no other tile of the tiling covers (sy <= H <= 2 sy, and
   // likewise along x) takes this tile's value, or 0 where its weight is 0
-  bool direct = false, wzero = false;
+  bool direct = false, wzero = false, wexact = true;
+  float wcell = 0.f;
   int64_t fcell = 0;
   if constexpr (STITCH) {
     const int ta = b / a.ntx, tb = b - ta * a.ntx;
@@ -237,7 +248,13 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
     const bool one_x = !(tb > 0 && qx < W - a.sx) && !(tb < a.ntx - 1 && qx >= a.sx);
     direct = one_y && one_x;
     fcell = (int64_t)(ta * a.sy + qy) * a.Wf + (tb * a.sx + qx);
-    wzero = a.window[qy * W + qx] == 0.f;
+    wcell = a.window[qy * W + qx];
+    wzero = wcell == 0.f;
+    // for 2^-8 <= w <= 1, fl(fl(w v) / w) rounds back to v for every bf16 v (no
+    // overflow, and an underflowing product keeps more than 8 significant bits),
+    // so the tile value is stored as it is; other weights take the stitch's own
+    // arithmetic
+    wexact = wzero || (wcell >= 0x1p-8f && wcell <= 1.f);
   }
 
   auto kswz = [&](int key) { return ((key % LX >> 1) + 5 * (key / LX)) & 7; };
@@ -281,13 +298,13 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
     const int pos = pos_of(key);
     koff[it] = (uint32_t)(pos * kD + c * 8) * 2u;
     uint4 ph;
-    if (csb) {
+    if (csb) {  // half-length phases (exact halving): see the input range above
       const float4* pp = csb + (int64_t)pos * 16 + 2 * c;
-      const float4 p0 = pp[0], p1 = pp[1];
+      const float4 p0 = pp[0] * 0.5f, p1 = pp[1] * 0.5f;
       ph = make_uint4(pack2h(p0.x, p0.y), pack2h(p0.z, p0.w), pack2h(p1.x, p1.y), pack2h(p1.z, p1.w));
     } else {
-      const uint32_t one = pack2h(1.f, 0.f);
-      ph = make_uint4(one, one, one, one);
+      const uint32_t half = pack2h(0.5f, 0.f);
+      ph = make_uint4(half, half, half, half);
     }
     st16(sph + s * 16, ph);
   }
@@ -575,8 +592,13 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
               uint32_t w0 = pack2(r[0], r[1]), w1 = pack2(r[2], r[3]);
               if constexpr (STITCH)
                 if (direct) {
-                  w0 = wzero ? 0u : plus_zero2(w0);
-                  w1 = wzero ? 0u : plus_zero2(w1);
+                  if (wexact) {
+                    w0 = wzero ? 0u : plus_zero2(w0);
+                    w1 = wzero ? 0u : plus_zero2(w1);
+                  } else {
+                    w0 = stitch_one2(w0, wcell);
+                    w1 = stitch_one2(w1, wcell);
+                  }
                 }
               dst[4 * t + g] = make_uint2(w0, w1);
             }
@@ -619,7 +641,7 @@ bool launch_na3d_fwd_zs(const strata_na3d_desc& d, const NaOpts& o, const void* 
   a.n_xb = (d.W + kBX - 1) / kBX;
   a.hpw = d.heads < 8 ? d.heads : 8;
   a.n_hg = (d.heads + a.hpw - 1) / a.hpw;
-  a.qscale = d.scale * kLog2e;
+  a.qscale = 2.f * d.scale * kLog2e;  // K is rotated at half length
   if (st) {
     a.face = static_cast<uint16_t*>(st->face);
     a.window = st->window;

@@ -186,7 +186,11 @@ PAPER_COLUMN = Workload("paper_column_96x16x24x16x16_d64_w24x1x1", 1008, "bf16",
                         96, 16, 24, 16, 16, 64, 24, 1, 1)
 PAPER_DECODER = Workload("paper_decoder_2x1x24x64x64_d128_w9x9x9", 1009, "bf16",
                          2, 1, 24, 64, 64, 128, 9, 9, 9)
-PAPER_WORKLOADS = {w.name: w for w in (PAPER_TILE16, PAPER_TILE32, PAPER_COLUMN, PAPER_DECODER)}
+# The 3x7x7 window of the face workload at the paper's 24 levels (the window
+# sweep of App. B.2 at full depth), on the 32x32-token tiles above.
+Z24_TILE = Workload("paper_24x16x24x32x32_d64_w3x7x7", 1010, "bf16",
+                    24, 16, 24, 32, 32, 64, 3, 7, 7)
+PAPER_WORKLOADS = {w.name: w for w in (PAPER_TILE16, PAPER_TILE32, PAPER_COLUMN, PAPER_DECODER, Z24_TILE)}
 
 FACE_OVERLAP = 8  # tokens shared by neighbouring tiles of the face rollout step
 

@@ -16,11 +16,6 @@ from . import binding as B
 ROPE_BASE = 100.0
 
 
-def l_scale(face_cells: int) -> float:
-    """Eq. 1 normaliser sqrt(4 pi / N_total), N_total = 6 face_cells^2 native cells."""
-    return (4.0 * 3.141592653589793 / (6.0 * face_cells * face_cells)) ** 0.5
-
-
 @dataclasses.dataclass
 class TileGeometry:
     face: torch.Tensor   # int32 [B] on device
@@ -41,7 +36,7 @@ def stereo_phases(geom: TileGeometry, H: int, W: int, head_dim: int,
     if cs is None:
         cs = torch.empty((Bt, H, W, head_dim // 2, 2), dtype=torch.float32, device=dev)
     B.strata_stereo_coords(geom.face, geom.oy, geom.ox, H, W, geom.face_cells, geom.patch,
-                           l_scale(geom.face_cells), coords)
+                           0.0, coords)  # 0: the library's Eq. 1 length for these faces
     B.strata_stereorope_phases(coords, head_dim, base, cs)
     return coords, cs
 

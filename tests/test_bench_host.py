@@ -42,3 +42,41 @@ def test_face_tiling_overlap_stitch_bytes():
     assert b == brute_overlap_bytes(9, 9, 64, 64, 56, 56, 128, 64)
     multi_cells = 512 * 512 - 448 * 448   # cells outside the 48 x 48 single-cover interiors
     assert b == (131072 + multi_cells) * 128 * 64 * 2
+
+
+def test_face_parity_reference_is_the_oracle_stitch():
+    """The bench's sampled face reference (oracle forward of each covering tile's
+    query, stitched in float64) equals the oracle's whole-tile forward stitched
+    by brute force over every tile, at every sampled cell; the sample holds every
+    cell category on every plane."""
+    import oracle
+    from oracle import geometry as G
+    from paper_2606_31248_amd import inputs as I
+
+    wl = I.Workload("face_small_9x2x8x32x32", 1205, "bf16", 9, 2, 8, 32, 32, 64, 3, 7, 7, tiling=(3, 3, 24, 24))
+    qkv = wl.qkv()
+    win = I.ramp_window_2d(wl.H, wl.W, 8)
+    cells = bench.face_sample_cells(wl)
+    ref, carried, meta = bench.face_reference(wl, qkv, cells, win)
+    assert meta["planes"] == wl.heads * wl.Z and meta["n_cells"] == 16 * wl.heads * wl.Z
+    pl = wl.placement()
+    c32 = G.tile_coords(pl.face, pl.oy, pl.ox, wl.H, wl.W).astype(np.float32)
+    ro, _ = oracle.na3d_fwd(*(oracle.widen(a, "bf16") for a in qkv), (3, 7, 7), wl.scale, coords=c32)
+    nty, ntx, sy, sx = wl.tiling
+    num = np.zeros((wl.heads * wl.Z, 80, 80, wl.d))
+    den = np.zeros((80, 80, 1))
+    w2 = win.reshape(wl.H, wl.W, 1).astype(np.float64)
+    planes = ro.reshape(9, wl.heads * wl.Z, wl.H, wl.W, wl.d)
+    for a in range(nty):
+        for b in range(ntx):
+            num[:, a * sy:a * sy + wl.H, b * sx:b * sx + wl.W] += w2 * planes[a * ntx + b]
+            den[a * sy:a * sy + wl.H, b * sx:b * sx + wl.W] += w2
+    brute = (num / den)[cells[0], cells[1], cells[2]]
+    assert np.max(np.abs(ref - brute)) <= 1e-12 * np.max(np.abs(brute))
+    assert np.all(carried > 0)
+    # the categories: single-cover, y strip, x strip, 4-tile corner and face corners are all present
+    ny = np.array([sum(0 <= y - t * sy < wl.H for t in range(nty)) for y in range(80)])
+    nx = np.array([sum(0 <= x - t * sx < wl.W for t in range(ntx)) for x in range(80)])
+    kinds = set(zip(ny[cells[1]], nx[cells[2]]))
+    assert {(1, 1), (2, 1), (1, 2), (2, 2)} <= kinds
+    assert np.any((cells[1] == 0) & (cells[2] == 0)) and np.any((cells[1] == 79) & (cells[2] == 79))

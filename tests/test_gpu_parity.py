@@ -427,3 +427,82 @@ def test_bwd_dout_mixed_magnitudes_dq_per_class(window):
     excess = np.abs(got_v - rv) - bf16_half_ulp(rv) - np.ldexp(a_dv, -8)
     rms = float(np.sqrt(np.mean(rv * rv)))
     assert float(np.max(excess)) <= 2e-2 * rms, f"dv: {float(np.max(excess)):.3e} > {2e-2 * rms:.3e}"
+
+
+# ----------------------------------------------------------------------------- input range
+
+def test_fwd_level_sweep_large_keys_stay_finite():
+    """Keys of magnitude 61440 (inside float16's range, beyond 65504 / sqrt(2)) through the
+    level-sweep kernel (3x7x7, Z = 8): a rotated pair would exceed 65504 at phases near 45
+    degrees, so the kernel rotates at half length.  One such key per 8x8 patch of
+    positions on one level, so every query window holds at most one.  Every output
+    and LSE must be finite.  The float16 copy of such a key carries an absolute
+    error of ~2^-11 * 61440 per element, so its logit is only known to within tens
+    of units: the oracle is matched (bf16 rule, LSE within 2^-9 relative) where the
+    exact logit of the large key is decisive, |s| > 200 (one-hot on it, or no weight),
+    and on every query whose window holds no large key."""
+    shape, window, scale = (1, 2, 8, 24, 24, 64), (3, 7, 7), 0.125
+    q = I.gaussian(shape, 95, 0, "bf16")
+    v = I.gaussian(shape, 95, 2, "bf16")
+    kf = I.bf16_bits_to_f32(I.gaussian(shape, 95, 1, "bf16"))
+    signs = np.where(np.random.default_rng(95).random(shape) < 0.5, -1.0, 1.0).astype(np.float32)
+    big = np.zeros(shape[:-1] + (1,), bool)
+    big[:, :, 3, 2::8, 3::8] = True
+    kf = np.where(big, np.float32(61440.0) * signs, kf).astype(np.float32)
+    k = I.f32_to_bf16_bits(kf)
+    pl = I.random_placement(1, 24, 24, 95)
+    c32 = oracle_coords(pl, 24, 24)
+    qd, kd, vd = (dev_tensor(a, "bf16") for a in (q, k, v))
+    out = torch.empty_like(qd)
+    lse = torch.empty(shape[:-1], dtype=torch.float32, device="cuda")
+    B.strata_na3d_fwd(B.desc_for(qd, window, scale), qd, kd, vd, gpu_phases(c32, 64), out, lse)
+    torch.cuda.synchronize()
+    got, gl = host_f64(out), host_f64(lse)
+    assert np.all(np.isfinite(got)) and np.all(np.isfinite(gl))
+    q64, k64 = (oracle.widen(a, "bf16") for a in (q, k))
+    ro, rl = oracle.na3d_fwd(q64, k64, oracle.widen(v, "bf16"), window, scale, coords=c32)
+    # exact logit of the large key in each query's window (0 where there is none)
+    qr, kr = (oracle.rope_apply(a, c32, base=ROPE_BASE) for a in (q64, k64))
+    s_big = np.zeros(shape[:-1])
+    s_abs = np.zeros(shape[:-1])  # scale sum |q_i k_i| of the large key: bounds its logit's rounding
+    has = np.zeros(shape[:-1], bool)
+    for h in range(shape[1]):
+        for z in range(8):
+            if not (win_lo(z, 8, 3) <= 3 < win_lo(z, 8, 3) + 3):
+                continue
+            for y in range(24):
+                for x in range(24):
+                    ys, xs = win_lo(y, 24, 7), win_lo(x, 24, 7)
+                    for ky in range(ys, ys + 7):
+                        for kx in range(xs, xs + 7):
+                            if big[0, h, 3, ky, kx, 0]:
+                                has[0, h, z, y, x] = True
+                                s_big[0, h, z, y, x] = scale * float(qr[0, h, z, y, x] @ kr[0, h, 3, ky, kx])
+                                s_abs[0, h, z, y, x] = scale * float(np.abs(qr[0, h, z, y, x]) @
+                                                                     np.abs(kr[0, h, 3, ky, kx]))
+    decisive = ~has | (np.abs(s_big) > 200)
+    assert np.count_nonzero(has & (s_big > 200)) > 20 and np.count_nonzero(has & (s_big < -200)) > 20
+    check_close(got[decisive], ro[decisive], "bf16", "out (large keys, decisive logits)")
+    # LSE: the bf16-input rule, plus the float16 rounding of the two operands of the
+    # large key's logit (2^-11 relative each) where that logit dominates
+    lse_bound = LSE_ABS_BF16 + np.where(has & (s_big > 200), 2.0 ** -9 * s_abs, 0.0)
+    assert np.all((np.abs(gl - rl) <= lse_bound)[decisive])
+
+
+def win_lo(i, L, k):
+    """First position of the border-clamped window of position i (the NATTEN rule)."""
+    return min(max(i - k // 2, 0), L - k)
+
+
+def test_stereo_coords_library_length():
+    """l_scale == 0 makes the library use Eq. 1's sqrt(4 pi / N_total) for the six faces:
+    the same coordinates, bit for bit, as passing that length explicitly."""
+    wl = I.SMALL_BF16
+    pl = wl.placement()
+    f, oy, ox = (torch.from_numpy(a).cuda() for a in pl.as_int32())
+    a = torch.empty((wl.B, wl.H, wl.W, 2), dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    B.strata_stereo_coords(f, oy, ox, wl.H, wl.W, 2048, 4, 0.0, a)
+    B.strata_stereo_coords(f, oy, ox, wl.H, wl.W, 2048, 4, G.l_scale(2048), b)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)

@@ -124,6 +124,25 @@ def test_fused_face_step_arbitrary_weights():
     assert np.array_equal(host_bits(fa), host_bits(fb))
 
 
+@pytest.mark.parametrize("vmul,weights", [
+    (2.0 ** 100, (2.0 ** 30, 2.0 ** 31, 0.75, 1.0)),  # w v overflows float32: the stitch gives inf
+    (2.0 ** -120, (2.0 ** -20, 2.0 ** -9, 0.5)),  # w v underflows to float32 subnormals
+    (1.0, (1e-3, 3e-40, 1.0, 7.0)),               # a subnormal weight, and weights outside [2^-8, 1]
+])
+def test_fused_face_step_weights_outside_unit_range(vmul, weights):
+    """Single-cover cells with weights outside [2^-8, 1] take the stitch's own
+    arithmetic fma(w, v, +0) / w in the fused forward: the face equals forward +
+    whole stitch bit for bit, including overflow to inf and subnormal products."""
+    nty, ntx, H, W, s = 2, 2, 32, 32, 24
+    shape, (q, k, v), coords, Hf, Wf = tiling_case(nty, ntx, H, W, s, s, seed=79)
+    v = I.f32_to_bf16_bits((I.bf16_bits_to_f32(v) * np.float32(vmul)).astype(np.float32))
+    win = np.array(weights, np.float32)[np.arange(H * W) % len(weights)]
+    fa, fb, _, _ = run_both(shape, (q, k, v), coords, (nty, ntx, s, s), (3, 7, 7), win)
+    assert np.array_equal(host_bits(fa), host_bits(fb))
+    if vmul > 1:
+        assert np.any(np.isinf(I.bf16_bits_to_f32(host_bits(fa))))
+
+
 @pytest.mark.parametrize("qk_norm,gate", [(True, None), (False, "token"), (True, "channel")])
 def test_fused_face_step_options(qk_norm, gate):
     """QK RMSNorm and the gate; gate logits of -200 on some tokens drive outputs to +-0."""
