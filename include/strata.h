@@ -159,6 +159,21 @@ strata_status strata_na3d_bwd(const strata_na3d_desc* desc, const void* q, const
                               const float* lse, void* dq, void* dk, void* dv, void* workspace,
                               size_t workspace_bytes, void* stream);
 
+/* ---- backward for callers that cannot allocate --------------------------------
+ * For code under HIP graph capture, tight training loops and harnesses that
+ * forbid hipMalloc: strata_na3d_bwd without a workspace.  Same arguments,
+ * results and kernels as strata_na3d_bwd (plain attention, no options); D lives
+ * in a static 32 MiB device array of the library, one per device, held until
+ * the process ends.  Limit: B*heads*Z*H*W <= 2^23 token-heads, otherwise
+ * STRATA_ERR_INVALID_ARG and nothing is launched.  Nothing is allocated; the
+ * array's device address is looked up once per device on the first call.
+ * Every call on a device shares that device's array: calls that overlap on one
+ * device (two streams, two threads) race and must be ordered by the caller. */
+strata_status strata_na3d_bwd_noalloc(const strata_na3d_desc* desc, const void* q, const void* k,
+                                      const void* v, const float* cs, const void* out,
+                                      const void* dout, const float* lse, void* dq, void* dk,
+                                      void* dv, void* stream);
+
 /* ---- QK normalisation and the output gate (App. B.5) -----------------------
  * Options of the attention block beyond plain neighbourhood attention; a
  * zero-initialised struct (or a NULL pointer) selects plain attention.

@@ -28,7 +28,7 @@ EXPORTS = (
     "strata_na3d_fwd_ex", "strata_na3d_bwd_ex_workspace_size", "strata_na3d_bwd_ex",
     "strata_tile_blend", "strata_tile_extract", "strata_na_axis_index", "strata_wind_tile_frame", "strata_kbd_window",
     "strata_duo_pad", "strata_duo_plan_bytes", "strata_duo_plan", "strata_duo_pad_planned",
-    "strata_duo_pad_vjp", "strata_na3d_fwd_stitch", "strata_tile_blend_overlap",
+    "strata_duo_pad_vjp", "strata_na3d_fwd_stitch", "strata_tile_blend_overlap", "strata_na3d_bwd_noalloc",
     "strata_status_string", "strata_last_error",
 )
 
@@ -71,6 +71,7 @@ def load(path: str = LIB_PATH):
         "strata_stereorope_apply": [P, P, P, i32, i32, i32, i32, i32, i32, st, i32, P],
         "strata_na3d_fwd": [D, P, P, P, P, P, P, P],
         "strata_na3d_bwd": [D, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
+        "strata_na3d_bwd_noalloc": [D, P, P, P, P, P, P, P, P, P, P, P],
         "strata_tile_blend": [P, i32, i32, i32, i32, i32, i32, i32, i32, P, P, i32, i32, st, P],
         "strata_tile_blend_overlap": [P, i32, i32, i32, i32, i32, i32, i32, i32, P, P, i32, i32, st, P],
         "strata_tile_extract": [P, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32, P, st, P],
@@ -258,6 +259,14 @@ def strata_na3d_bwd(desc: NA3DDesc, q, k, v, cs, out, dout, lse, dq, dk, dv, wor
     _check(load().strata_na3d_bwd(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(cs), _ptr(out),
                                   _ptr(dout), _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv),
                                   _ptr(workspace), nbytes, _stream(stream)))
+
+
+def strata_na3d_bwd_noalloc(desc: NA3DDesc, q, k, v, cs, out, dout, lse, dq, dk, dv, stream=None):
+    """strata_na3d_bwd without a workspace (D in the library's static device array)."""
+    _check_na_tensors(desc, dict(q=q, k=k, v=v, out=out, dout=dout, dq=dq, dk=dk, dv=dv), cs, lse,
+                      lse_required=True)
+    _check(load().strata_na3d_bwd_noalloc(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(cs), _ptr(out),
+                                          _ptr(dout), _ptr(lse), _ptr(dq), _ptr(dk), _ptr(dv), _stream(stream)))
 
 
 def make_opts(qk_norm: bool = False, eps: float = 1e-6, gate: Optional[torch.Tensor] = None) -> NA3DOpts:

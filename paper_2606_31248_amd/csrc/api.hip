@@ -4,6 +4,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -205,6 +207,63 @@ static strata_status na3d_bwd_launch(const strata_na3d_desc* desc, const strata_
   return check_launch(opts ? "strata_na3d_bwd_ex" : "strata_na3d_bwd");
 }
 
+// ---- backward without a caller workspace ---------------------------------------
+// D = rowsum(dO * O) of a plain backward lives in this file-scope device array
+// instead of a workspace: every device the library runs on holds its own copy
+// for the life of the process.  In host code `scratch` only names the symbol;
+// its device address is looked up once per device (hipGetSymbolAddress, with
+// the device current) and that address is what the kernels receive.
+constexpr int64_t kScratchFloats = (int64_t)1 << 23;  // 32 MiB: D of up to 2^23 token-heads
+static __device__ __align__(256) float scratch[kScratchFloats];
+
+constexpr int kMaxDevices = 64;
+static std::once_flag g_scratch_once[kMaxDevices];
+static float* g_scratch_ptr[kMaxDevices];
+static hipError_t g_scratch_err[kMaxDevices];
+
+// this device's copy of `scratch`, or nullptr (with the HIP error in *err)
+static float* device_scratch(int dev, hipError_t* err) {
+  std::call_once(g_scratch_once[dev], [dev] {
+    void* p = nullptr;
+    g_scratch_err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    g_scratch_ptr[dev] = g_scratch_err[dev] == hipSuccess ? static_cast<float*>(p) : nullptr;
+  });
+  *err = g_scratch_err[dev];
+  return g_scratch_ptr[dev];
+}
+
+static strata_status na3d_bwd_noalloc_impl(const strata_na3d_desc* desc, const void* q, const void* k,
+                                           const void* v, const float* cs, const void* out, const void* dout,
+                                           const float* lse, void* dq, void* dk, void* dv, void* stream) {
+  strata_status st = check_desc(desc);
+  if (st != STRATA_OK) return st;
+  REQUIRE_PTR(q);
+  REQUIRE_PTR(k);
+  REQUIRE_PTR(v);
+  REQUIRE_PTR(out);
+  REQUIRE_PTR(dout);
+  REQUIRE_PTR(lse);
+  REQUIRE_PTR(dq);
+  REQUIRE_PTR(dk);
+  REQUIRE_PTR(dv);
+  if (cs) REQUIRE(aligned16(cs), "cs: not 16-byte aligned");
+  const int64_t n = (int64_t)desc->B * desc->heads * desc->Z * desc->H * desc->W;
+  REQUIRE(n <= kScratchFloats,
+          "bwd_noalloc: %lld token-heads exceed the static scratch of %lld (use strata_na3d_bwd with a workspace)",
+          (long long)n, (long long)kScratchFloats);
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return set_error(STRATA_ERR_HIP, "bwd_noalloc: hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices)
+    return set_error(STRATA_ERR_UNSUPPORTED, "bwd_noalloc: device %d beyond the %d this build tracks", dev,
+                     kMaxDevices);
+  float* ws = device_scratch(dev, &e);
+  if (!ws) return set_error(STRATA_ERR_HIP, "bwd_noalloc: hipGetSymbolAddress: %s", hipGetErrorString(e));
+  const NaOpts o;
+  return na3d_bwd_launch(desc, nullptr, o, q, k, v, cs, out, dout, lse, dq, dk, dv, nullptr,
+                         reinterpret_cast<char*>(ws), (hipStream_t)stream);
+}
+
 }  // namespace strata
 
 using namespace strata;
@@ -340,6 +399,12 @@ strata_status strata_na3d_bwd_ex(const strata_na3d_desc* desc, const strata_na3d
                                  size_t workspace_bytes, void* stream) {
   return na3d_bwd_impl(desc, opts, q, k, v, cs, out, dout, lse, dq, dk, dv, dgate, workspace,
                        workspace_bytes, stream);
+}
+
+strata_status strata_na3d_bwd_noalloc(const strata_na3d_desc* desc, const void* q, const void* k, const void* v,
+                                      const float* cs, const void* out, const void* dout, const float* lse, void* dq,
+                                      void* dk, void* dv, void* stream) {
+  return na3d_bwd_noalloc_impl(desc, q, k, v, cs, out, dout, lse, dq, dk, dv, stream);
 }
 
 static strata_status check_tiling(int32_t nty, int32_t ntx, int32_t P, int32_t Ht, int32_t Wt,
