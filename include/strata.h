@@ -129,12 +129,16 @@ strata_status strata_stereorope_apply(const void* x, void* y, const float* cs, i
  * lse: float32 [B, heads, Z, H, W] (natural log) or NULL when not needed.
  * Supported: head_dim 32, 64 or 128 in either dtype.  Kernels: bf16 at
  * head_dim 64 runs on MFMA for the windows (3,7,7), (5,9,9), (9,9,9) and every
- * column window (kz,1,1) with Z <= 32; bf16 at head_dim 128 on MFMA for (9,9,9);
+ * column window (kz,1,1) with Z <= 32 (level sweeps for (3,7,7) and (5,9,9), a
+ * query-stationary kernel for (9,9,9)); bf16 at head_dim 128 on MFMA for (9,9,9);
  * every other case (f32, head_dim 32, other windows) on a plain per-query
  * kernel in float32.  Softmax and accumulation in float32.
  * Contraction precision: on the MFMA paths the logits q.k are float16 products
  * (wider mantissa than bf16) of float16 copies of the rotated, normalised and
- * scaled q and k, accumulated in float32; P.V is a bf16 product.  Input range:
+ * scaled q and k, accumulated in float32; P.V is a float16 product (weights and
+ * V in float16) on the level-sweep kernels (3x7x7, 5x9x9), a bf16 one on the
+ * others; V of magnitude above 65504 then saturates and below 2^-14 keeps
+ * float16's subnormal spacing.  Input range:
  * with M = max(1, 2 scale log2(e)), inputs with M |q| <= 32000 and
  * M |k| <= 32000 (q^, k^ after the QK norm) keep every float16 operand inside
  * its range; beyond that each path saturates its float16 copies (results stay

@@ -111,7 +111,8 @@ static BwdLayout bwd_layout(const strata_na3d_desc& d, const NaOpts& o) {
 static void launch_fwd(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k, const void* v,
                        const float* cs, void* out, float* lse, hipStream_t s) {
   if (!launch_na3d_fwd_col(d, o, q, k, v, out, lse, s) && !launch_na3d_fwd_zs(d, o, q, k, v, cs, out, lse, s) &&
-      !launch_na3d_fwd_mfma(d, o, q, k, v, cs, out, lse, s) && !launch_na3d_fwd_d128(d, o, q, k, v, cs, out, lse, s))
+      !launch_na3d_fwd_lsg(d, o, q, k, v, cs, out, lse, s) && !launch_na3d_fwd_mfma(d, o, q, k, v, cs, out, lse, s) &&
+      !launch_na3d_fwd_d128(d, o, q, k, v, cs, out, lse, s))
     launch_na3d_fwd_ref(d, o, q, k, v, cs, out, lse, s);
 }
 

@@ -53,6 +53,11 @@ bool launch_na3d_fwd_zs(const strata_na3d_desc& d, const NaOpts& o, const void* 
                         const void* v, const float* cs, void* out, float* lse, hipStream_t s,
                         const StitchArgs* st = nullptr);
 
+// bf16 level sweep over groups of query levels (head_dim 64, windows 3x7x7 and
+// 5x9x9, any Z); returns false for any other problem.
+bool launch_na3d_fwd_lsg(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k,
+                         const void* v, const float* cs, void* out, float* lse, hipStream_t s);
+
 // bf16 column-wise forward, windows (kz, 1, 1) with Z <= 32, head_dim 64;
 // returns false for any other problem.
 bool launch_na3d_fwd_col(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k,

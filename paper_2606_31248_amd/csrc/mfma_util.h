@@ -75,6 +75,17 @@ __device__ __forceinline__ uint4 rotate8h_pk(uint4 x, uint4 ph, float mul = 1.f)
   return make_uint4(r[0], r[1], r[2], r[3]);
 }
 
+// bf16 x 8 -> float16 x 8 by round-toward-zero: exact for bf16 values whose
+// magnitude lies in float16's normal range, saturating at +-65504 above it;
+// smaller values keep float16's subnormal spacing 2^-24.
+__device__ __forceinline__ uint4 bf16x8_to_f16x8(uint4 x) {
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  uint32_t r[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) r[t] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(lo_bf16(w[t]), hi_bf16(w[t])));
+  return make_uint4(r[0], r[1], r[2], r[3]);
+}
+
 // bf16 x 8 -> float16 x 8, times `mul` (no rotation).
 __device__ __forceinline__ uint4 scale8h(uint4 x, float mul) {
   uint32_t w[4] = {x.x, x.y, x.z, x.w};

@@ -13,10 +13,12 @@
 //               the 14 x 14 key box of a level are copied global -> LDS by the
 //               direct-to-LDS load one level ahead of the compute (double
 //               buffer; the copies are spread over the first two query levels
-//               of the current key level); once its query levels are issued, each thread waits for its own copies and rotates the K
-//               pieces they brought (StereoRoPE in packed float16, with the float16
-//               phases of the key box staged once in LDS); the barrier at the end
-//               of the key level publishes the next one.
+//               of the current key level); once its query levels are issued,
+//               each thread waits for its own copies, rotates the K pieces they
+//               brought (StereoRoPE in packed float16, with the float16 phases
+//               of the key box staged once in LDS) and converts the V pieces to
+//               float16; the barrier at the end of the key level publishes the
+//               next one.
 //               Queries are rotated in float32 with float32 phases and the logit
 //               scale times log2 e, then rounded to float16 once: an exact scale
 //               matters, a scale rounded to float16 shifts every logit by up to
@@ -37,26 +39,34 @@
 //                                         rotated, scaled K and the rotated Q,
 //                                         the accumulator seeded with the window
 //                                         mask (0 or -inf);
-//   P = exp2(S^T - m) packed to bf16 in place;
-//   O^T (64 d x 16 queries) += V^T . P^T  bf16 MFMA, V^T fragments by the LDS
-//                                         transpose read;
-//   L (16 x 16 queries)     += 1 . P^T    the row sums, by one more bf16 MFMA
+//   P = exp2(S^T - m) packed to float16 in place;
+//   O^T (64 d x 16 queries) += V^T . P^T  float16 MFMA, V^T fragments by the
+//                                         LDS transpose read of V converted to
+//                                         float16 when it is staged;
+//   L (16 x 16 queries)     += 1 . P^T    the row sums, by one more float16 MFMA
 //                                         against a tile of ones (every row of
 //                                         L holds the sum, so each lane has its
 //                                         query's sum without a reduction).
-// The reference m starts at 0 for every query and moves only when a logit
-// exceeds it by more than 2^4 (O and the row sum are then rescaled), or when
-// the first key level of a query level has no logit above -2^6 (nothing is
-// accumulated yet).  P is bf16 with float32's exponent range, so exp2(S - m)
-// neither overflows nor loses relevant weights; while m is 0 for the whole
-// wave (the common case for logits of moderate size) no subtraction is done.
+// P.V runs in float16 rather than bf16: rounding the weights P to bf16 (8
+// significant bits) moved outputs by up to 2.2% of their RMS beyond their own
+// storage rounding on the 8-tile workload (checked on every output, and
+// reproduced by a CPU emulation of these roundings), float16 weights (11 bits)
+// by 0.7%.  The reference m starts at 0 for every query and moves up when a
+// logit exceeds it by more than 15 (O and the row sum are then rescaled), so
+// P <= 2^15 stays inside float16; on a query level's first key level it moves
+// down when no logit reaches -8 (nothing is accumulated yet), so the largest
+// weight is at least 2^-8 and the small ones keep their relative size; while m
+// is 0 for the whole wave (the common case for logits of moderate size) no
+// subtraction is done.
 // Every accumulator chain uses one MFMA shape only (the last 16-key chunk of
 // the P.V product is padded with zero weights rather than switching to a
 // 16x16x16 MFMA): gfx950 gives wrong sums when an accumulator is handed from
 // one MFMA shape to another without wait states, which the compiler does not
 // insert.
 //
-// Input range: K is converted to float16 with round-toward-zero before its
+// Input range: V is converted to float16 by round-toward-zero (exact for bf16
+// values of magnitude 2^-14 .. 65504, saturating above, float16's subnormal
+// spacing below).  K is converted to float16 with round-toward-zero before its
 // rotation (bf16 values up to +-65504 convert exactly, larger ones saturate) and
 // rotated by phases of half length (c/2, s/2), so a rotated pair stays below
 // 65504 sqrt(2) / 2 and never overflows; the queries carry the factor 2 instead:
@@ -102,8 +112,8 @@ constexpr int ITK = (KSLOTS + kThreads - 1) / kThreads;    // K slots per thread
 constexpr int ITV = (VSLOTS + kThreads - 1) / kThreads;    // V slots per thread (8)
 constexpr int KTILE = ITK * kThreads * 16;                 // tile bytes incl. pad slots
 constexpr int VTILE = ITV * kThreads * 16;
-constexpr float kLazy = 16.0f;    // m moves up when a logit exceeds it by 2^4
-constexpr float kLow = -64.0f;    // ... or down, on a level's first key level
+constexpr float kLazy = 15.0f;    // m moves up when a logit exceeds it by 15 (P <= 2^15)
+constexpr float kLow = -8.0f;     // ... or down, on a level's first key level (max P >= 2^-8)
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kLog2e = 1.4426950408889634f;
 
@@ -315,8 +325,17 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
     const int c = s % 10 < 8 ? s % 10 : 0;  // pad columns copy column 0
     voff[it] = (uint32_t)(pos_of(key) * kD + c * 8) * 2u;
   }
-  // float32 phases of this lane's query position (pairs 4g..4g+3 and 16+4g..)
+  // float32 phases of this lane's query position (pairs 4g..4g+3 and 16+4g..),
+  // the same for every level and head: loaded once and kept (16 registers; a
+  // reload at each key level left its latency exposed, 0.45 ms more per step)
   const float4* csq = csb ? csb + ((int64_t)qy * W + qx) * 16 : nullptr;
+  float4 cqv[4] = {};
+  if (csq) {
+    cqv[0] = csq[2 * g];
+    cqv[1] = csq[2 * g + 1];
+    cqv[2] = csq[8 + 2 * g];
+    cqv[3] = csq[8 + 2 * g + 1];
+  }
 
   auto level_base = [&](int h, int p) { return (((int64_t)b * a.heads + h) * Z + p) * HW; };
   auto issue_copy = [&](int64_t base, char* tk, char* tv) {
@@ -329,11 +348,14 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
     for (int it = 0; it < ITV; ++it)
       copy16_to_lds(reinterpret_cast<const uint16_t*>(vp + voff[it]), tv + (it * kThreads + wave * 64) * 16);
   };
-  // Rotate this thread's K slots in place (bf16 -> scaled float16).  A thread's
-  // copies land in its own slots, so its own wait suffices.
-  // With QK RMSNorm the 8 slots of a key row (8 consecutive lanes) add their
-  // sums of squares for the row's factor.
-  auto rotate_k = [&](char* tk) {
+  // Rotate this thread's K slots in place (bf16 -> scaled float16) and convert
+  // its V slots to float16.  A thread's copies land in its own slots, so its own
+  // wait suffices.  With QK RMSNorm the 8 slots of a key row (8 consecutive
+  // lanes) add their sums of squares for the row's factor.
+  auto rotate_k = [&](char* tk, char* tv) {
+    uint4 y[ITV];
+#pragma unroll
+    for (int it = 0; it < ITV; ++it) y[it] = ld16(tv + (it * kThreads + tid) * 16);
     uint4 x[ITK];  // all reads before any write: the slots are distinct, which the compiler cannot tell
 #pragma unroll
     for (int it = 0; it < ITK; ++it) x[it] = ld16(tk + (it * kThreads + tid) * 16);
@@ -344,6 +366,8 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
 #pragma unroll
     for (int it = 0; it < ITK; ++it)
       st16(tk + (it * kThreads + tid) * 16, rotate_k8(x[it], ld16(sph + (it * kThreads + tid) * 16), rn[it]));
+#pragma unroll
+    for (int it = 0; it < ITV; ++it) st16(tv + (it * kThreads + tid) * 16, bf16x8_to_f16x8(y[it]));
   };
   // raw query rows of one level (two 16-byte pieces per lane)
   auto load_q = [&](int h, int z, uint4& x0, uint4& x1) {
@@ -357,8 +381,8 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
     if constexpr (NORM)  // the 4 lanes of a query row hold its 64 values
       mul *= __builtin_amdgcn_rsqf(sum_over_rows(sumsq8(x1, sumsq8(x0, 0.f))) * (1.f / kD) + a.eps);
     if (cq) {
-      r0 = rotate8h(x0, cq[2 * g], cq[2 * g + 1], mul);
-      r1 = rotate8h(x1, cq[8 + 2 * g], cq[8 + 2 * g + 1], mul);
+      r0 = rotate8h(x0, cqv[0], cqv[1], mul);
+      r1 = rotate8h(x1, cqv[2], cqv[3], mul);
     } else {
       r0 = scale8h(x0, mul);
       r1 = scale8h(x1, mul);
@@ -372,7 +396,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
   f16x8 qf[Z][2];
   float m[Z];
   f32x4 lsum[Z];    // row sums (all four entries equal)
-  const bf16x8 ones = __builtin_bit_cast(bf16x8, make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u));
+  const f16x8 ones = __builtin_bit_cast(f16x8, make_uint4(0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u));
   bool mset[Z];     // wave-uniform: m is non-zero somewhere in the wave
   f32x4 o[Z][4];
   uint4 qraw[Z][2];
@@ -382,7 +406,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
   // K and V fragments of one key level (shared by every active query level)
   struct Frags {
     f16x8 k[NC][2];
-    bf16x8 v[NS][4];
+    f16x8 v[NS][4];
   };
   auto load_frags = [&](const char* tk, const char* tv, Frags& f) {
 #pragma unroll
@@ -398,7 +422,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
         const i16x4 lo = tr_read(tv + vaddr[c0] + 32 * t);
         const i16x4 hi = c1 < NC ? tr_read(tv + vaddr[c1 < NC ? c1 : c0] + 32 * t) : i16x4{0, 0, 0, 0};
         const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
-        f.v[st][t] = __builtin_bit_cast(bf16x8, make_uint4(l2.x, l2.y, h2.x, h2.y));
+        f.v[st][t] = __builtin_bit_cast(f16x8, make_uint4(l2.x, l2.y, h2.x, h2.y));
       }
     }
   };
@@ -449,19 +473,19 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
     uint32_t pk[NC][2];
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
-      pk[c][0] = pack2(__builtin_amdgcn_exp2f(s[c][0]), __builtin_amdgcn_exp2f(s[c][1]));
-      pk[c][1] = pack2(__builtin_amdgcn_exp2f(s[c][2]), __builtin_amdgcn_exp2f(s[c][3]));
+      pk[c][0] = pack2h_rne(__builtin_amdgcn_exp2f(s[c][0]), __builtin_amdgcn_exp2f(s[c][1]));
+      pk[c][1] = pack2h_rne(__builtin_amdgcn_exp2f(s[c][2]), __builtin_amdgcn_exp2f(s[c][3]));
     }
 #pragma unroll
     for (int st = 0; st < NS; ++st) {
       const int c0 = 2 * st, c1 = 2 * st + 1;
       const uint32_t p2 = c1 < NC ? pk[c1 < NC ? c1 : c0][0] : 0u;
       const uint32_t p3 = c1 < NC ? pk[c1 < NC ? c1 : c0][1] : 0u;
-      const bf16x8 pf = __builtin_bit_cast(bf16x8, make_uint4(pk[c0][0], pk[c0][1], p2, p3));
+      const f16x8 pf = __builtin_bit_cast(f16x8, make_uint4(pk[c0][0], pk[c0][1], p2, p3));
 #pragma unroll
       for (int t = 0; t < 4; ++t)
-        o[z][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.v[st][t], pf, o[z][t], 0, 0, 0);
-      lsum[z] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf, lsum[z], 0, 0, 0);
+        o[z][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(f.v[st][t], pf, o[z][t], 0, 0, 0);
+      lsum[z] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ones, pf, lsum[z], 0, 0, 0);
     }
   };
 
@@ -472,7 +496,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
     if constexpr (zstart<Z>(z) == 0) load_q(h_lo, z, qraw[z][0], qraw[z][1]);
   });
   __builtin_amdgcn_s_waitcnt(0);
-  rotate_k(tK0);
+  rotate_k(tK0, tV0);
   __syncthreads();
 
   for (int h = h_lo; h < h_hi; ++h) {
@@ -499,15 +523,11 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
       const char* const nkp = reinterpret_cast<const char*>(a.k + nbase * kD);
       const char* const nvp = reinterpret_cast<const char*>(a.v + nbase * kD);
 
-      // queries of the levels that start here: rotate the rows loaded earlier (the
-      // phase pointer is made opaque so that the phase loads stay here instead of
-      // being held in registers across the whole sweep)
-      const float4* cq = csq;
-      asm volatile("" : "+v"(cq));
+      // queries of the levels that start here: rotate the rows loaded earlier
       static_for<Z>([&](auto Zi) {
         constexpr int z = decltype(Zi)::v;
         if constexpr (zstart<Z>(z) == p) {
-          prep_q(cq, qraw[z][0], qraw[z][1], qf[z][0], qf[z][1]);
+          prep_q(csq, qraw[z][0], qraw[z][1], qf[z][0], qf[z][1]);
           m[z] = 0.f;
           lsum[z] = f32x4{0.f, 0.f, 0.f, 0.f};
           mset[z] = false;
@@ -563,7 +583,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
             if constexpr (z == zhi<Z>(p)) {
               if (has_next) {
                 __builtin_amdgcn_s_waitcnt(0);
-                rotate_k(nk);
+                rotate_k(nk, nv);
               }
             }
           }

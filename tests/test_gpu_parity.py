@@ -133,6 +133,14 @@ def test_fwd_tiny_f32_full():
     ((2, 2, 8, 7, 7, 64), (3, 7, 7)),       # level-sweep kernel, window = whole plane
     ((1, 3, 8, 7, 9, 64), (3, 7, 7)),       # level-sweep kernel, one-column blocks
     ((1, 2, 4, 9, 9, 64), (1, 9, 9)),       # window = whole plane
+    # the grouped level sweep (4 query levels per group): groups cut short by Z,
+    # border-clamped level windows, ragged position blocks, two head groups
+    ((1, 3, 5, 19, 21, 64), (3, 7, 7)),
+    ((1, 2, 10, 16, 16, 64), (3, 7, 7)),
+    ((1, 2, 7, 20, 17, 64), (5, 9, 9)),
+    ((1, 9, 6, 9, 11, 64), (5, 9, 9)),
+    ((1, 2, 9, 16, 16, 64), (9, 9, 9)),
+    ((1, 2, 13, 12, 20, 64), (9, 9, 9)),
 ])
 @pytest.mark.parametrize("rope", [True, False])
 def test_fwd_bf16_full_oracle(shape, window, rope):
@@ -159,7 +167,7 @@ def sample_queries(shape, n, seed, tiles=None):
     return np.unique(flat)
 
 
-@pytest.mark.parametrize("wl", [I.SMALL_BF16, I.TRAIN_TILE, I.FACE_ROLLOUT], ids=lambda w: w.name)
+@pytest.mark.parametrize("wl", [I.SMALL_BF16, I.TRAIN_TILE, I.FACE_ROLLOUT, I.Z24_TILE], ids=lambda w: w.name)
 def test_fwd_full_size_sampled(wl):
     """Full-size launch (the configuration the bench times); sampled outputs vs oracle.
 
@@ -354,6 +362,10 @@ def run_bwd(shape, window, dtype, seed, coords32=None, g_exp=None):
     ((1, 1, 3, 8, 8, 32), (1, 3, 5), "bf16"),
     ((1, 2, 6, 21, 19, 64), (3, 7, 7), "bf16"),
     ((1, 1, 9, 25, 22, 64), (5, 9, 9), "bf16"),
+    # the key levels on a ring of waves (5x9x9): as many levels as the window,
+    # and a long column in which every wave takes three key levels in turn
+    ((1, 2, 5, 12, 12, 64), (5, 9, 9), "bf16"),
+    ((1, 1, 13, 13, 9, 64), (5, 9, 9), "bf16"),
 ])
 @pytest.mark.parametrize("rope", [True, False])
 def test_bwd_full_oracle(shape, window, dtype, rope):

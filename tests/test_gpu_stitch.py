@@ -125,7 +125,7 @@ def test_fused_face_step_arbitrary_weights():
 
 
 @pytest.mark.parametrize("vmul,weights", [
-    (2.0 ** 100, (2.0 ** 30, 2.0 ** 31, 0.75, 1.0)),  # w v overflows float32: the stitch gives inf
+    (2.0 ** 12, (2.0 ** 115, 2.0 ** 116, 0.75, 1.0)),  # w v overflows float32: the stitch gives inf
     (2.0 ** -120, (2.0 ** -20, 2.0 ** -9, 0.5)),  # w v underflows to float32 subnormals
     (1.0, (1e-3, 3e-40, 1.0, 7.0)),               # a subnormal weight, and weights outside [2^-8, 1]
 ])
