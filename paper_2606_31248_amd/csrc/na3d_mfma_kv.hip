@@ -102,6 +102,42 @@ struct KvArgs {
 __host__ __device__ __forceinline__ int inv_lo(int j, int k) { return j < k ? 0 : j - (k >> 1); }
 __host__ __device__ __forceinline__ int inv_hi(int j, int L, int k) { return j >= L - k ? L - 1 : j + (k >> 1); }
 
+template <int I>
+struct IC {
+  static constexpr int v = I;
+};
+template <int N, int I = 0, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(IC<I>{});
+    static_for<N, I + 1>(f);
+  }
+}
+
+// LDS addresses as 32-bit pointers.  A tile base plus a lane offset is passed
+// through an empty asm, so that the compiler keeps it in one register and folds
+// every constant (step, chunk, column) into the read's immediate offset rather
+// than materialising one register per constant (the tiles lie beyond the 64 KB
+// reach of an immediate).
+typedef __attribute__((address_space(3))) char lds_char;
+__device__ __forceinline__ const lds_char* lds_base(const char* p, uint32_t off) {
+  const lds_char* b = (const lds_char*)(p) + off;
+  asm volatile("" : "+v"(b));
+  return b;
+}
+__device__ __forceinline__ uint4 ldl16(const lds_char* p) {
+  const u32x4 v = *reinterpret_cast<const __attribute__((address_space(3))) u32x4*>(p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ float4 ldlf4(const lds_char* p) {
+  const f32x4 v = *reinterpret_cast<const __attribute__((address_space(3))) f32x4*>(p);
+  return make_float4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ uint2 trl(const lds_char* p) {
+  return __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                       (__attribute__((address_space(3))) i16x4*)(const_cast<lds_char*>(p))));
+}
+
 __device__ __forceinline__ int rswz(int u) { return (((u >> 1) & 3) << 1) | ((u >> 3) & 1); }
 
 template <int KZ, int KY, int KX, int ZK, int NBUF, bool LO, bool NORM>
@@ -183,6 +219,17 @@ __global__ void __launch_bounds__(64 * ZK, (KvCfg<KZ, KY, KX, ZK, NBUF, LO>::WG_
     }
   }
 
+  __syncthreads();  // the mask table is read across lanes below
+  // this lane's window bits: bit 4c + i of mb is row 16c + 4g + i of the box (the
+  // rows of the X accumulator this lane holds in chunk c) seen by key qn
+  static_assert(C::MQ <= 256, "window bits of a lane fit two words");
+  uint32_t mb[2] = {0u, 0u};
+#pragma unroll
+  for (int c = 0; c < C::MQ / 16; ++c)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      mb[(4 * c + i) >> 5] |= ((smask[16 * c + 4 * (lane >> 4) + i] >> (lane & 15)) & 1u) << ((4 * c + i) & 31);
+
   // ---- direct-to-LDS copy map (registers): slot s = it*512 + tid ---------------
   // row u = s / 8 holds box query u; slot column s % 8 holds data column
   // (s % 8) ^ sigma(u).  Q and dO share the map; goff = -1 past the box.
@@ -251,7 +298,7 @@ __global__ void __launch_bounds__(64 * ZK, (KvCfg<KZ, KY, KX, ZK, NBUF, LO>::WG_
     for (int is = 0; is < C::IS; ++is) {
       if (soff[is] < 0) continue;
       const int u = is * kThreads + tid;
-      sl[u] = pl[is] * kLog2e;
+      sl[u] = -(pl[is] * kLog2e);  // the seed of X: -LSE in log2 units
       sd[u] = -pd[is];
     }
   };
@@ -302,36 +349,62 @@ __global__ void __launch_bounds__(64 * ZK, (KvCfg<KZ, KY, KX, ZK, NBUF, LO>::WG_
   const uint32_t toff = trow * kRow + ((((qn >> 1) & 1) ^ rswz(trow)) << 4) + 8 * (qn & 1);
 
   auto compute = [&](const char* tq, const char* tg, const char* tl, const float* sl, const float* sd) {
-    for (int st = 0; st < npairs; ++st) {
+    // lane bases of this level's tiles: every read below is one of them plus an
+    // immediate offset (steps fully unrolled up to the largest box)
+    const lds_char* const aq0 = lds_base(tq, aoff);
+    const lds_char* const aq1 = lds_base(tq, aoff ^ 64u);
+    const lds_char* const ag0 = lds_base(tg, aoff);
+    const lds_char* const ag1 = lds_base(tg, aoff ^ 64u);
+    const lds_char* const al0 = LO ? lds_base(tl, aoff) : nullptr;
+    const lds_char* const al1 = LO ? lds_base(tl, aoff ^ 64u) : nullptr;
+    const lds_char* bq[4];
+    const lds_char* bg[4];
+    const lds_char* bl[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      bq[t] = lds_base(tq, toff ^ (32u * t));
+      bg[t] = lds_base(tg, toff ^ (32u * t));
+      bl[t] = LO ? lds_base(tl, toff ^ (32u * t)) : nullptr;
+    }
+    // the window bits pass through an empty asm at every level, so the
+    // compiler derives the seeds' select masks step by step instead of hoisting
+    // all 64 of them into registers
+    uint32_t mw[2] = {mb[0], mb[1]};
+    asm volatile("" : "+v"(mw[0]), "+v"(mw[1]));
+    const lds_char* const sl4 = lds_base(reinterpret_cast<const char*>(sl), 16 * g);
+    const lds_char* const sd4 = lds_base(reinterpret_cast<const char*>(sd), 16 * g);
+    static_for<C::MQ / 32>([&](auto Si) {
+      constexpr int st = decltype(Si)::v;
+      if (st >= npairs) return;  // wave-uniform
       f32x4 x[2], y[2];
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int c = 2 * st + h;
-        const char* rq = tq + c * (16 * kRow);
-        const char* rg = tg + c * (16 * kRow);
-        const f16x8 q0 = __builtin_bit_cast(f16x8, ld16(rq + aoff));
-        const f16x8 q1 = __builtin_bit_cast(f16x8, ld16(rq + (aoff ^ 64u)));
-        const bf16x8 g0 = __builtin_bit_cast(bf16x8, ld16(rg + aoff));
-        const bf16x8 g1 = __builtin_bit_cast(bf16x8, ld16(rg + (aoff ^ 64u)));
-        // seeds for rows 16c + 4g + i (the D layout of X and Y)
-        const int u4 = 16 * c + 4 * g;
-        const float4 l4 = *reinterpret_cast<const float4*>(sl + u4);
-        const float4 d4 = *reinterpret_cast<const float4*>(sd + u4);
-        const uint2 m4 = *reinterpret_cast<const uint2*>(smask + u4);
+        const f16x8 q0 = __builtin_bit_cast(f16x8, ldl16(aq0 + c * (16 * kRow)));
+        const f16x8 q1 = __builtin_bit_cast(f16x8, ldl16(aq1 + c * (16 * kRow)));
+        const bf16x8 g0 = __builtin_bit_cast(bf16x8, ldl16(ag0 + c * (16 * kRow)));
+        const bf16x8 g1 = __builtin_bit_cast(bf16x8, ldl16(ag1 + c * (16 * kRow)));
+        // seeds for rows 16c + 4g + i (the D layout of X and Y): -LSE where the
+        // row's query sees this lane's key, else -inf (bit select by the
+        // sign-extended window bit)
+        const float4 l4 = ldlf4(sl4 + 64 * c);
+        const float4 d4 = ldlf4(sd4 + 64 * c);
+        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
         f32x4 xs;
-        xs[0] = ((m4.x >> qn) & 1u) ? -l4.x : -INFINITY;
-        xs[1] = ((m4.x >> (16 + qn)) & 1u) ? -l4.y : -INFINITY;
-        xs[2] = ((m4.y >> qn) & 1u) ? -l4.z : -INFINITY;
-        xs[3] = ((m4.y >> (16 + qn)) & 1u) ? -l4.w : -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int bit = 4 * c + i;
+          const uint32_t sel = (uint32_t)__builtin_amdgcn_sbfe((int)mw[bit >> 5], bit & 31, 1);
+          xs[i] = __uint_as_float((sel & __float_as_uint(lv[i])) | (~sel & 0xff800000u));
+        }
         const f32x4 ys = {d4.x, d4.y, d4.z, d4.w};
         x[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(q0, kf[0], xs, 0, 0, 0);
         x[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(q1, kf[1], x[h], 0, 0, 0);
         y[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(g0, vf[0], ys, 0, 0, 0);
         y[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(g1, vf[1], y[h], 0, 0, 0);
         if constexpr (LO) {
-          const char* rl = tl + c * (16 * kRow);
-          const bf16x8 l0 = __builtin_bit_cast(bf16x8, ld16(rl + aoff));
-          const bf16x8 l1 = __builtin_bit_cast(bf16x8, ld16(rl + (aoff ^ 64u)));
+          const bf16x8 l0 = __builtin_bit_cast(bf16x8, ldl16(al0 + c * (16 * kRow)));
+          const bf16x8 l1 = __builtin_bit_cast(bf16x8, ldl16(al1 + c * (16 * kRow)));
           y[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(l0, vf[0], y[h], 0, 0, 0);
           y[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(l1, vf[1], y[h], 0, 0, 0);
         }
@@ -363,28 +436,26 @@ __global__ void __launch_bounds__(64 * ZK, (KvCfg<KZ, KY, KX, ZK, NBUF, LO>::WG_
       }
       const bf16x8 pf = __builtin_bit_cast(bf16x8, make_uint4(pb[0][0], pb[0][1], pb[1][0], pb[1][1]));
       const f16x8 df = __builtin_bit_cast(f16x8, make_uint4(db[0][0], db[0][1], db[1][0], db[1][1]));
-      const char* tq0 = tq + st * (32 * kRow);
-      const char* tg0 = tg + st * (32 * kRow);
+      constexpr int o = st * (32 * kRow);
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        const uint32_t o0 = toff ^ (32u * t);
-        const uint2 g_lo = __builtin_bit_cast(uint2, tr_read(tg0 + o0));
-        const uint2 g_hi = __builtin_bit_cast(uint2, tr_read(tg0 + 16 * kRow + o0));
+        const uint2 g_lo = trl(bg[t] + o);
+        const uint2 g_hi = trl(bg[t] + o + 16 * kRow);
         const bf16x8 gt = __builtin_bit_cast(bf16x8, make_uint4(g_lo.x, g_lo.y, g_hi.x, g_hi.y));
         accV[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gt, pf, accV[t], 0, 0, 0);
         if constexpr (LO) {
-          const char* tl0 = tl + st * (32 * kRow);
-          const uint2 l_lo = __builtin_bit_cast(uint2, tr_read(tl0 + o0));
-          const uint2 l_hi = __builtin_bit_cast(uint2, tr_read(tl0 + 16 * kRow + o0));
+          const uint2 l_lo = trl(bl[t] + o);
+          const uint2 l_hi = trl(bl[t] + o + 16 * kRow);
           const bf16x8 lt = __builtin_bit_cast(bf16x8, make_uint4(l_lo.x, l_lo.y, l_hi.x, l_hi.y));
           accV[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lt, pf, accV[t], 0, 0, 0);
         }
-        const uint2 q_lo = __builtin_bit_cast(uint2, tr_read(tq0 + o0));
-        const uint2 q_hi = __builtin_bit_cast(uint2, tr_read(tq0 + 16 * kRow + o0));
+        const uint2 q_lo = trl(bq[t] + o);
+        const uint2 q_hi = trl(bq[t] + o + 16 * kRow);
         const f16x8 qt = __builtin_bit_cast(f16x8, make_uint4(q_lo.x, q_lo.y, q_hi.x, q_hi.y));
         accK[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(qt, df, accK[t], 0, 0, 0);
       }
-    }
+      __builtin_amdgcn_sched_barrier(0);  // keep the next step's loads out of this one's registers
+    });
   };
   // does query level p see this wave's key level?
   auto active = [&](int p) {
