@@ -60,7 +60,8 @@ constexpr int kD = 64;           // head_dim
 constexpr int kRow = 128;        // LDS bytes per staged query row
 constexpr int kLdsMax = 160 * 1024;
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kMinExp = -100;    // lower bound of the dS exponent (keeps 2^(15-E) finite)
+constexpr int kMinExp = -100;
+    // lower bound of the dS exponent (keeps 2^(15-E) finite)
 
 
 // ZK key levels per workgroup (one wave each); NBUF = 2: double-buffered query
@@ -373,23 +374,51 @@ __global__ void __launch_bounds__(64 * ZK, (KvCfg<KZ, KY, KX, ZK, NBUF, LO>::WG_
     asm volatile("" : "+v"(mw[0]), "+v"(mw[1]));
     const lds_char* const sl4 = lds_base(reinterpret_cast<const char*>(sl), 16 * g);
     const lds_char* const sd4 = lds_base(reinterpret_cast<const char*>(sd), 16 * g);
+    // A operands and seeds of one step (two 16-query chunks).  (Reading the next
+    // step's while this one computes needs more registers than two waves per
+    // SIMD leave; measured, the transpose reads issued early pay more.)
+    struct StepIn {
+      f16x8 q0[2], q1[2];
+      bf16x8 g0[2], g1[2];
+      float4 l4[2], d4[2];
+    };
+    auto load_in = [&](auto Si, StepIn& f) {
+      constexpr int st = decltype(Si)::v;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int c = 2 * st + h;
+        f.q0[h] = __builtin_bit_cast(f16x8, ldl16(aq0 + c * (16 * kRow)));
+        f.q1[h] = __builtin_bit_cast(f16x8, ldl16(aq1 + c * (16 * kRow)));
+        f.g0[h] = __builtin_bit_cast(bf16x8, ldl16(ag0 + c * (16 * kRow)));
+        f.g1[h] = __builtin_bit_cast(bf16x8, ldl16(ag1 + c * (16 * kRow)));
+        f.l4[h] = ldlf4(sl4 + 64 * c);
+        f.d4[h] = ldlf4(sd4 + 64 * c);
+      }
+    };
     static_for<C::MQ / 32>([&](auto Si) {
       constexpr int st = decltype(Si)::v;
       if (st >= npairs) return;  // wave-uniform
+      StepIn cur;
+      load_in(Si, cur);
+      constexpr int o = st * (32 * kRow);
+      // transpose reads of this step, issued before its MFMAs and softmax so
+      // that their latency hides there
+      uint2 gtr[4][2], qtr[4][2];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        gtr[t][0] = trl(bg[t] + o);
+        gtr[t][1] = trl(bg[t] + o + 16 * kRow);
+        qtr[t][0] = trl(bq[t] + o);
+        qtr[t][1] = trl(bq[t] + o + 16 * kRow);
+      }
       f32x4 x[2], y[2];
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int c = 2 * st + h;
-        const f16x8 q0 = __builtin_bit_cast(f16x8, ldl16(aq0 + c * (16 * kRow)));
-        const f16x8 q1 = __builtin_bit_cast(f16x8, ldl16(aq1 + c * (16 * kRow)));
-        const bf16x8 g0 = __builtin_bit_cast(bf16x8, ldl16(ag0 + c * (16 * kRow)));
-        const bf16x8 g1 = __builtin_bit_cast(bf16x8, ldl16(ag1 + c * (16 * kRow)));
         // seeds for rows 16c + 4g + i (the D layout of X and Y): -LSE where the
         // row's query sees this lane's key, else -inf (bit select by the
         // sign-extended window bit)
-        const float4 l4 = ldlf4(sl4 + 64 * c);
-        const float4 d4 = ldlf4(sd4 + 64 * c);
-        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+        const float lv[4] = {cur.l4[h].x, cur.l4[h].y, cur.l4[h].z, cur.l4[h].w};
         f32x4 xs;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -397,11 +426,11 @@ __global__ void __launch_bounds__(64 * ZK, (KvCfg<KZ, KY, KX, ZK, NBUF, LO>::WG_
           const uint32_t sel = (uint32_t)__builtin_amdgcn_sbfe((int)mw[bit >> 5], bit & 31, 1);
           xs[i] = __uint_as_float((sel & __float_as_uint(lv[i])) | (~sel & 0xff800000u));
         }
-        const f32x4 ys = {d4.x, d4.y, d4.z, d4.w};
-        x[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(q0, kf[0], xs, 0, 0, 0);
-        x[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(q1, kf[1], x[h], 0, 0, 0);
-        y[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(g0, vf[0], ys, 0, 0, 0);
-        y[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(g1, vf[1], y[h], 0, 0, 0);
+        const f32x4 ys = {cur.d4[h].x, cur.d4[h].y, cur.d4[h].z, cur.d4[h].w};
+        x[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(cur.q0[h], kf[0], xs, 0, 0, 0);
+        x[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(cur.q1[h], kf[1], x[h], 0, 0, 0);
+        y[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur.g0[h], vf[0], ys, 0, 0, 0);
+        y[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur.g1[h], vf[1], y[h], 0, 0, 0);
         if constexpr (LO) {
           const bf16x8 l0 = __builtin_bit_cast(bf16x8, ldl16(al0 + c * (16 * kRow)));
           const bf16x8 l1 = __builtin_bit_cast(bf16x8, ldl16(al1 + c * (16 * kRow)));
@@ -436,12 +465,9 @@ __global__ void __launch_bounds__(64 * ZK, (KvCfg<KZ, KY, KX, ZK, NBUF, LO>::WG_
       }
       const bf16x8 pf = __builtin_bit_cast(bf16x8, make_uint4(pb[0][0], pb[0][1], pb[1][0], pb[1][1]));
       const f16x8 df = __builtin_bit_cast(f16x8, make_uint4(db[0][0], db[0][1], db[1][0], db[1][1]));
-      constexpr int o = st * (32 * kRow);
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        const uint2 g_lo = trl(bg[t] + o);
-        const uint2 g_hi = trl(bg[t] + o + 16 * kRow);
-        const bf16x8 gt = __builtin_bit_cast(bf16x8, make_uint4(g_lo.x, g_lo.y, g_hi.x, g_hi.y));
+        const bf16x8 gt = __builtin_bit_cast(bf16x8, make_uint4(gtr[t][0].x, gtr[t][0].y, gtr[t][1].x, gtr[t][1].y));
         accV[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gt, pf, accV[t], 0, 0, 0);
         if constexpr (LO) {
           const uint2 l_lo = trl(bl[t] + o);
@@ -449,9 +475,7 @@ __global__ void __launch_bounds__(64 * ZK, (KvCfg<KZ, KY, KX, ZK, NBUF, LO>::WG_
           const bf16x8 lt = __builtin_bit_cast(bf16x8, make_uint4(l_lo.x, l_lo.y, l_hi.x, l_hi.y));
           accV[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lt, pf, accV[t], 0, 0, 0);
         }
-        const uint2 q_lo = trl(bq[t] + o);
-        const uint2 q_hi = trl(bq[t] + o + 16 * kRow);
-        const f16x8 qt = __builtin_bit_cast(f16x8, make_uint4(q_lo.x, q_lo.y, q_hi.x, q_hi.y));
+        const f16x8 qt = __builtin_bit_cast(f16x8, make_uint4(qtr[t][0].x, qtr[t][0].y, qtr[t][1].x, qtr[t][1].y));
         accK[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(qt, df, accK[t], 0, 0, 0);
       }
       __builtin_amdgcn_sched_barrier(0);  // keep the next step's loads out of this one's registers

@@ -45,9 +45,10 @@
 //
 // K rows are 128 bytes with their 16-byte columns XOR-swizzled by
 // ((x >> 1) + 5 y) & 7 of the key's box position: the 16 keys of any chunk of an
-// interior sub-block then sit in 16 distinct bank groups.  V rows are padded to
-// 160 bytes, which spreads the 8-byte transpose reads and lets them take
-// immediate offsets.  The two halves of the double buffer are distinct LDS objects, so the
+// interior sub-block then sit in 16 distinct bank groups.  In the forward V rows
+// are padded to 160 bytes, which spreads the 8-byte transpose reads and lets
+// them take immediate offsets; the backward reads V rows as an A operand and
+// stages them like K (128 bytes, same swizzle).  The two halves of the double buffer are distinct LDS objects, so the
 // compiler can tell the reads of one from the copies into the other and does not
 // wait for the copies before reading.
 //
@@ -86,8 +87,12 @@ constexpr float kLazy = 8.0f;    // move the softmax reference only when a logit
 constexpr float kLow = -64.0f;   // ... or down, on a level's first key level
 constexpr int kMinExp = -100;    // lower bound of the dS exponent (keeps 2^(15-E) finite)
 
-template <int KZ, int KY, int KX, int ZQ>
+template <int KZ, int KY, int KX, int ZQ, bool BWD>
 struct Cfg {
+  // V rows: the forward reads V^T by transpose reads (160-byte rows spread
+  // them); the backward reads V rows as an A operand like K (128-byte rows with
+  // K's column swizzle, conflict-free)
+  static constexpr int VROW = BWD ? kKRow : kVRow;
   static constexpr int LY = kBY + KY - 1, LX = kBX + KX - 1;  // staged key box per level
   static constexpr int NUY = 3 + KY, NUX = 3 + KX;            // key box of one 4x4 sub-block
   static constexpr int NU = NUY * NUX;
@@ -95,8 +100,8 @@ struct Cfg {
   static constexpr int NS = (NC + 1) / 2;                     // 32-key PV steps
   static constexpr int KEYS = LY * LX;
   static constexpr int KSLOTS = KEYS * (kKRow / 16);          // 16-byte slots of a K tile (8 per key)
-  static constexpr int VSLOTS = KEYS * (kVRow / 16);
-  static constexpr int KBYTES = KEYS * kKRow, VBYTES = KEYS * kVRow;
+  static constexpr int VSLOTS = KEYS * (VROW / 16);
+  static constexpr int KBYTES = KEYS * kKRow, VBYTES = KEYS * VROW;
   static constexpr int BUF = KBYTES + VBYTES;                 // one level: K and V
   static constexpr int ITK = (KSLOTS + kThreads - 1) / kThreads;
   static constexpr int ITV = (VSLOTS + kThreads - 1) / kThreads;
@@ -145,7 +150,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
   constexpr bool NORM = (OPT & kNorm) != 0;
   constexpr bool GATE = !BWD && (OPT & kOpt2) != 0;
   constexpr bool LO = BWD && (OPT & kOpt2) != 0;
-  using C = Cfg<KZ, KY, KX, ZQ>;
+  using C = Cfg<KZ, KY, KX, ZQ, BWD>;
   // double buffer of key tiles (distinct objects, see above), copy offsets, phases
   __shared__ __attribute__((aligned(16))) char tK0[C::KBYTES];
   __shared__ __attribute__((aligned(16))) char tV0[C::VBYTES];
@@ -199,7 +204,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
     {  // K fragment (A operand): row = key 16c + qn, 16 bytes at column g (xor 64 bytes: g+4)
       const int key = key_row(16 * c + qn);
       kaddr[c] = key * kKRow + ((g ^ kswz(key)) << 4);
-      if constexpr (BWD) vaddr[c] = key * kVRow + 16 * g;  // V row, columns g and g+4
+      if constexpr (BWD) vaddr[c] = kaddr[c];  // V row, the same swizzled layout as K
     }
     {  // transpose reads: source row = key 16c + 4g + qn/4, elements 4*(qn%4) of a 16-wide block
       const int key = key_row(16 * c + 4 * g + (qn >> 2));
@@ -240,7 +245,8 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
   }
 #pragma unroll
   for (int it = 0; it < C::ITV; ++it) {
-    int s = it * kThreads + tid, key = s / 10, c = s - key * 10;
+    // forward: 10 slots per key (8 data + 2 pad); backward: 8, swizzled like K
+    int s = it * kThreads + tid, key = BWD ? s >> 3 : s / 10, c = BWD ? (s & 7) ^ kswz(key) : s - key * 10;
     int gy = min(ty0 + key / C::LX, H - 1), gx = min(tx0 + key % C::LX, W - 1);
     int off = (s < C::VSLOTS && c < 8) ? (gy * W + gx) * kD + c * 8 : -1;
     if (C::GOFF_LDS) sgoff[(C::ITK + it) * kThreads + tid] = off;
@@ -439,7 +445,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
       f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(k0, qf[j][0], bias[c], 0, 0, 0);
       s[c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(k1, qf[j][1], acc, 0, 0, 0);
       bf16x8 v0 = __builtin_bit_cast(bf16x8, ld16(tv + vaddr[c]));
-      bf16x8 v1 = __builtin_bit_cast(bf16x8, ld16(tv + vaddr[c] + 64));
+      bf16x8 v1 = __builtin_bit_cast(bf16x8, ld16(tv + (vaddr[c] ^ 64u)));
       f32x4 t0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v0, gf[j][0], nd, 0, 0, 0);
       y[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v1, gf[j][1], t0, 0, 0, 0);
       if constexpr (LO) {
