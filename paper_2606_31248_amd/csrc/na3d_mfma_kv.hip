@@ -115,29 +115,18 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
-// LDS addresses as 32-bit pointers.  A tile base plus a lane offset is passed
-// through an empty asm, so that the compiler keeps it in one register and folds
-// every constant (step, chunk, column) into the read's immediate offset rather
-// than materialising one register per constant (the tiles lie beyond the 64 KB
-// reach of an immediate).
-typedef __attribute__((address_space(3))) char lds_char;
-__device__ __forceinline__ const lds_char* lds_base(const char* p, uint32_t off) {
-  const lds_char* b = (const lds_char*)(p) + off;
-  asm volatile("" : "+v"(b));
-  return b;
+// A tile plus a lane offset, the offset passed through an empty asm: the
+// compiler keeps the sum in one register per tile and lane pattern and folds
+// every constant (step, chunk, column) into the read's immediate offset.  The
+// pointer still derives from the tile, so the compiler can tell these reads from
+// the copies into the other buffer and does not wait for those copies.
+__device__ __forceinline__ const char* lds_base(const char* p, uint32_t off) {
+  asm volatile("" : "+v"(off));
+  return p + off;
 }
-__device__ __forceinline__ uint4 ldl16(const lds_char* p) {
-  const u32x4 v = *reinterpret_cast<const __attribute__((address_space(3))) u32x4*>(p);
-  return make_uint4(v.x, v.y, v.z, v.w);
-}
-__device__ __forceinline__ float4 ldlf4(const lds_char* p) {
-  const f32x4 v = *reinterpret_cast<const __attribute__((address_space(3))) f32x4*>(p);
-  return make_float4(v[0], v[1], v[2], v[3]);
-}
-__device__ __forceinline__ uint2 trl(const lds_char* p) {
-  return __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                                       (__attribute__((address_space(3))) i16x4*)(const_cast<lds_char*>(p))));
-}
+__device__ __forceinline__ uint4 ldl16(const char* p) { return ld16(p); }
+__device__ __forceinline__ float4 ldlf4(const char* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ uint2 trl(const char* p) { return __builtin_bit_cast(uint2, tr_read(p)); }
 
 __device__ __forceinline__ int rswz(int u) { return (((u >> 1) & 3) << 1) | ((u >> 3) & 1); }
 
@@ -352,15 +341,15 @@ __global__ void __launch_bounds__(64 * ZK, (KvCfg<KZ, KY, KX, ZK, NBUF, LO>::WG_
   auto compute = [&](const char* tq, const char* tg, const char* tl, const float* sl, const float* sd) {
     // lane bases of this level's tiles: every read below is one of them plus an
     // immediate offset (steps fully unrolled up to the largest box)
-    const lds_char* const aq0 = lds_base(tq, aoff);
-    const lds_char* const aq1 = lds_base(tq, aoff ^ 64u);
-    const lds_char* const ag0 = lds_base(tg, aoff);
-    const lds_char* const ag1 = lds_base(tg, aoff ^ 64u);
-    const lds_char* const al0 = LO ? lds_base(tl, aoff) : nullptr;
-    const lds_char* const al1 = LO ? lds_base(tl, aoff ^ 64u) : nullptr;
-    const lds_char* bq[4];
-    const lds_char* bg[4];
-    const lds_char* bl[4];
+    const char* const aq0 = lds_base(tq, aoff);
+    const char* const aq1 = lds_base(tq, aoff ^ 64u);
+    const char* const ag0 = lds_base(tg, aoff);
+    const char* const ag1 = lds_base(tg, aoff ^ 64u);
+    const char* const al0 = LO ? lds_base(tl, aoff) : nullptr;
+    const char* const al1 = LO ? lds_base(tl, aoff ^ 64u) : nullptr;
+    const char* bq[4];
+    const char* bg[4];
+    const char* bl[4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       bq[t] = lds_base(tq, toff ^ (32u * t));
@@ -372,8 +361,8 @@ __global__ void __launch_bounds__(64 * ZK, (KvCfg<KZ, KY, KX, ZK, NBUF, LO>::WG_
     // all 64 of them into registers
     uint32_t mw[2] = {mb[0], mb[1]};
     asm volatile("" : "+v"(mw[0]), "+v"(mw[1]));
-    const lds_char* const sl4 = lds_base(reinterpret_cast<const char*>(sl), 16 * g);
-    const lds_char* const sd4 = lds_base(reinterpret_cast<const char*>(sd), 16 * g);
+    const char* const sl4 = lds_base(reinterpret_cast<const char*>(sl), 16 * g);
+    const char* const sd4 = lds_base(reinterpret_cast<const char*>(sd), 16 * g);
     // A operands and seeds of one step (two 16-query chunks).  (Reading the next
     // step's while this one computes needs more registers than two waves per
     // SIMD leave; measured, the transpose reads issued early pay more.)
