@@ -162,6 +162,56 @@ def summarize_sq(run_dir: str, commands) -> dict:
     return rec
 
 
+def _short_kernel(name: str) -> str:
+    """Kernel name with its template arguments, without namespaces and parameter list."""
+    name = re.sub(r"\(.*$", "", name.replace("(anonymous namespace)::", ""))
+    return re.sub(r"^void |strata::", "", name)
+
+
+def summarize_counters(label: str, run_dirs, commands) -> str:
+    """Text summary of rocprofv3 --pmc runs: per library kernel, the median over its
+    dispatches of every counter collected.  FETCH_SIZE / WRITE_SIZE (KiB per
+    dispatch) are also given in bytes, scaled by the factor that makes the 1 GiB
+    device copy of the same run (--calib-copy) read its size; with SQ_INSTS_VALU
+    (which counts the MFMAs too) and SQ_INSTS_MFMA the VALU instructions per MFMA,
+    and the MFMA FLOP issued (every MFMA of these kernels is a 16x16x32 one)."""
+    acc = {}
+    copy = {}
+    for d in run_dirs:
+        for k, c, v in _pmc_rows(d):
+            if COPY_KERNEL in k:
+                copy.setdefault(c, []).append(v)
+            elif "strata" in k:
+                acc.setdefault(_short_kernel(k), {}).setdefault(c, []).append(v)
+    fac = {}
+    for c, want in (("FETCH_SIZE", CALIB_BYTES), ("WRITE_SIZE", CALIB_BYTES)):
+        vals = [x for cc, xs in copy.items() if cc.startswith(c) for x in xs]
+        if vals:
+            fac[c] = want / (max(vals) * 1024)
+    out = [f"# rocprofv3 --pmc counters, {label}, MI355X (median per dispatch over the run's dispatches)"]
+    out += [f"# command: {c}" for c in commands]
+    if fac:
+        out.append("# copy calibration: " + ", ".join(f"{c} x {f:.4f}" for c, f in fac.items()))
+    out.append("")
+    for kern, cs in sorted(acc.items()):
+        med = {c: float(np.median(v)) for c, v in cs.items()}
+        out.append(f"{kern}   ({max(len(v) for v in cs.values())} dispatches)")
+        for c in sorted(med):
+            out.append(f"    {c:32s} {med[c]:16.6g}")
+        mf = next((v for c, v in med.items() if c.startswith("SQ_INSTS_MFMA")), None)
+        va = next((v for c, v in med.items() if c.startswith("SQ_INSTS_VALU") and c.split("[")[0] == "SQ_INSTS_VALU"), None)
+        if mf:
+            out.append(f"    {'= MFMA FLOP issued':32s} {mf * 2 * 16 * 16 * 32:16.6g}")
+            if va:
+                out.append(f"    {'= VALU per MFMA':32s} {(va - mf) / mf:16.3f}")
+        for c, f in fac.items():
+            x = next((v for cc, v in med.items() if cc.startswith(c)), None)
+            if x is not None:
+                out.append(f"    {'= ' + c + ' bytes':32s} {x * 1024 * f:16.6g}")
+        out.append("")
+    return "\n".join(out)
+
+
 def overlap_stitch_bytes(nty, ntx, Ht, Wt, sy, sx, P, C, elem=2) -> float:
     """Algorithmic bytes of the overlap-only stitch: every tile value of a cell
     covered by two or more tiles read once, every such face cell written once."""
@@ -497,7 +547,7 @@ def _seeded_device(wl, dev, gen_seed=None):
     return tuple(torch.randn(wl.shape(), generator=gen, device=dev).to(dt) for _ in range(4))
 
 
-def profile_workload(name: str, steps: int, warmup: int) -> dict:
+def profile_workload(name: str, steps: int, warmup: int, calib_copy: bool = False) -> dict:
     """Run one kernel call of one workload `warmup + steps` times and nothing else
     (no oracle, no side measurements): the target of rocprofv3 counter runs.
 
@@ -514,6 +564,11 @@ def profile_workload(name: str, steps: int, warmup: int) -> dict:
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     Bd.load()
+    if calib_copy:  # one 1 GiB device copy: the HBM counter calibration of the same run
+        src = torch.empty(CALIB_BYTES // 2, dtype=torch.int16, device=dev).fill_(1)
+        torch.empty_like(src).copy_(src)
+        torch.cuda.synchronize()
+        del src
     fwd_wl = {"c1": I.TINY_F32, "c2": I.SMALL_BF16, "c3": I.TRAIN_TILE, "paper16_fwd": I.PAPER_TILE16,
               "paper32_fwd": I.PAPER_TILE32, "z24_fwd": I.Z24_TILE}
     bwd_wl = {"c4": I.TRAIN_TILE_BWD, "paper16_bwd": I.PAPER_TILE16, "paper32_bwd": I.PAPER_TILE32}
@@ -889,13 +944,23 @@ def main():
                     help="write the instruction-mix summary of a rocprofv3 --pmc run of SQ counters to profiles/ and exit")
     ap.add_argument("--summarize-stats", metavar="KERNEL_STATS_CSV",
                     help="write the kernel-trace summary of a rocprofv3 --stats run to profiles/ and exit")
+    ap.add_argument("--summarize-counters", nargs="+", metavar=("NAME", "DIR"),
+                    help="write profiles/NAME.txt, the per-kernel summary of rocprofv3 --pmc runs in DIR..., and exit")
+    ap.add_argument("--label", default="", help="what the summarized counter runs measured")
     ap.add_argument("--command", action="append", default=[],
                     help="the profiler command(s) the summary records")
     ap.add_argument("--profile", metavar="WORKLOAD",
                     help="run only one kernel call of one workload (see profile_workload) and exit")
     a = ap.parse_args()
     if a.profile:
-        print(json.dumps(profile_workload(a.profile, a.steps, a.warmup)), flush=True)
+        print(json.dumps(profile_workload(a.profile, a.steps, a.warmup, a.calib_copy)), flush=True)
+        return
+    if a.summarize_counters:
+        name, dirs = a.summarize_counters[0], a.summarize_counters[1:]
+        txt = summarize_counters(a.label or name, dirs, a.command)
+        with open(os.path.join(ROOT, "profiles", name + ".txt"), "w") as f:
+            f.write(txt)
+        print(txt)
         return
     if a.summarize_pmc:
         rec = summarize_pmc(a.summarize_pmc[0], a.summarize_pmc[1], a.command)
