@@ -500,6 +500,11 @@ template <int KZ, int KY, int KX, int G, int NBUF, bool NORM, bool GATE>
 bool launch_lsg(const strata_na3d_desc& d, const LsgArgs& a0, hipStream_t s) {
   LsgArgs a = a0;
   a.n_zg = (d.Z + G - 1) / G;
+  // a run of up to 8 heads per workgroup shares its geometry; a small problem
+  // takes fewer, so that the grid still has two workgroups per CU
+  while (a.hpw > 1 && (int64_t)d.B * ((d.heads + a.hpw - 1) / a.hpw) * a.n_zg * a.n_yb * a.n_xb < 512)
+    a.hpw = (a.hpw + 1) / 2;
+  a.n_hg = (d.heads + a.hpw - 1) / a.hpw;
   const int64_t blocks = (int64_t)d.B * a.n_hg * a.n_zg * a.n_yb * a.n_xb;
   if (blocks >= (int64_t)1 << 31) return false;
   hipLaunchKernelGGL((na3d_fwd_lsg_kernel<KZ, KY, KX, G, NBUF, NORM, GATE>), dim3((unsigned)blocks), dim3(kThreads),

@@ -659,7 +659,11 @@ bool launch_na3d_fwd_zs(const strata_na3d_desc& d, const NaOpts& o, const void* 
   a.W = d.W;
   a.n_yb = (d.H + kBY - 1) / kBY;
   a.n_xb = (d.W + kBX - 1) / kBX;
+  // a run of up to 8 heads per workgroup shares its geometry; a small problem
+  // takes fewer, so that the grid still has two workgroups per CU
   a.hpw = d.heads < 8 ? d.heads : 8;
+  while (a.hpw > 1 && (int64_t)d.B * ((d.heads + a.hpw - 1) / a.hpw) * a.n_yb * a.n_xb < 512)
+    a.hpw = (a.hpw + 1) / 2;
   a.n_hg = (d.heads + a.hpw - 1) / a.hpw;
   a.qscale = 2.f * d.scale * kLog2e;  // K is rotated at half length
   if (st) {
