@@ -487,6 +487,14 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_zs_kernel(ZArgs a) {
         o[z][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(f.v[st][t], pf, o[z][t], 0, 0, 0);
       lsum[z] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ones, pf, lsum[z], 0, 0, 0);
     }
+    // scheduling: four VALU instructions (the exponentials and packs of the
+    // later chunks) after each P.V MFMA, instead of the exponentials in one run
+    // ahead of them (measured on the face step: 10.24 -> 10.05 ms)
+#pragma unroll
+    for (int i = 0; i < 5 * NS; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // four VALU
+    }
   };
 
   // ---- prologue: key level 0 of the first head, queries of its first levels --
