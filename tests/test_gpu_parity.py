@@ -132,6 +132,8 @@ def test_fwd_tiny_f32_full():
     ((1, 11, 8, 16, 24, 64), (3, 7, 7)),    # level-sweep kernel, ragged head group
     ((2, 2, 8, 7, 7, 64), (3, 7, 7)),       # level-sweep kernel, window = whole plane
     ((1, 3, 8, 7, 9, 64), (3, 7, 7)),       # level-sweep kernel, one-column blocks
+    ((1, 3, 24, 19, 21, 64), (3, 7, 7)),    # level-sweep kernel at 24 levels, ragged blocks
+    ((2, 9, 24, 8, 12, 64), (3, 7, 7)),     # ... a head run cut short (9 heads)
     ((1, 2, 4, 9, 9, 64), (1, 9, 9)),       # window = whole plane
     # the grouped level sweep (4 query levels per group): groups cut short by Z,
     # border-clamped level windows, ragged position blocks, two head groups
