@@ -144,7 +144,9 @@ static void fwd_ref(const strata_na3d_desc& d, const NaOpts& o, const void* q, c
                     const void* v, const float* cs, void* out, float* lse, hipStream_t s) {
   Dims dm{d.B, d.heads, d.Z, d.H, d.W, d.kz, d.ky, d.kx, d.scale};
   int64_t nq = (int64_t)d.B * d.heads * d.Z * d.H * d.W;
-  int threads = 128;
+  // one query per thread; a small problem takes one wave per workgroup so that
+  // its workgroups spread over more CUs
+  int threads = nq < (int64_t)512 * 128 ? 64 : 128;
   int blocks = (int)((nq + threads - 1) / threads);
   hipLaunchKernelGGL((na3d_fwd_ref_kernel<T, D>), dim3(blocks), dim3(threads), 0, s,
                      static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
