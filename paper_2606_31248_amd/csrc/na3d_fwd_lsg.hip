@@ -173,7 +173,10 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_fwd_lsg_kernel(LsgArgs a) {
   const int qy = min(qy_raw, H - 1), qx = min(qx_raw, W - 1);
   const bool in_grid = qy_raw < H && qx_raw < W;
 
-  auto kswz = [&](int key) { return ((key % LX >> 1) + 5 * (key / LX)) & 7; };
+  // (the row step NUX / 2 keeps the 16 keys of a chunk, which span two or three
+  // rows of the sub-block's key box, in 16 distinct bank groups: 5 for 10-wide
+  // boxes, 6 for 12-wide ones)
+  auto kswz = [&](int key) { return ((key % LX >> 1) + (NUX / 2) * (key / LX)) & 7; };
   auto key_row = [&](int u) { return u < NU ? (uy0 - ty0 + u / NUX) * LX + (ux0 - tx0 + u % NUX) : 0; };
 
   // ---- LDS addresses of this lane's fragments and its window mask ----------

@@ -188,7 +188,10 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
   const int wys = win_start(qy, H, KY), wxs = win_start(qx, W, KX);
 
   // column swizzle of the K tile (see the header comment)
-  auto kswz = [&](int key) { return ((key % C::LX >> 1) + 5 * (key / C::LX)) & 7; };
+  // (the row step NUX / 2 keeps the 16 keys of a chunk, which span two or three
+  // rows of the sub-block's key box, in 16 distinct bank groups: 5 for 10-wide
+  // boxes, 6 for 12-wide ones)
+  auto kswz = [&](int key) { return ((key % C::LX >> 1) + (C::NUX / 2) * (key / C::LX)) & 7; };
   // tile row of sub-block key u (u past the box: row 0, masked)
   auto key_row = [&](int u) {
     return u < C::NU ? (uy0 - ty0 + u / C::NUX) * C::LX + (ux0 - tx0 + u % C::NUX) : 0;
