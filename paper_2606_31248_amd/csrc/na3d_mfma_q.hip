@@ -44,8 +44,9 @@
 // bf16 terms hi + lo (backward: one more MFMA pair for Y).
 //
 // K rows are 128 bytes with their 16-byte columns XOR-swizzled by
-// ((x >> 1) + 5 y) & 7 of the key's box position: the 16 keys of any chunk of an
-// interior sub-block then sit in 16 distinct bank groups.  In the forward V rows
+// ((x >> 1) + (NUX / 2) y) & 7 of the key's box position (NUX = 3 + kx, the
+// width of a sub-block's key box): the 16 keys of any chunk of an interior
+// sub-block then sit in 16 distinct bank groups.  In the forward V rows
 // are padded to 160 bytes, which spreads the 8-byte transpose reads and lets
 // them take immediate offsets; the backward reads V rows as an A operand and
 // stages them like K (128 bytes, same swizzle).  The two halves of the double buffer are distinct LDS objects, so the
