@@ -248,3 +248,33 @@ def test_fused_face_step_full_face_rollout():
     pipeline.face_step(q, k, v, geom, window, wl.scale, wl.tiling, win, fb, cs=cs, fused=False)
     torch.cuda.synchronize()
     assert torch.equal(fa.view(torch.int16), fb.view(torch.int16))
+
+
+def test_face_step_seeded_full_size_against_oracle():
+    """The face-rollout step on the seeded inputs bench.py times (81 tiles x 16 heads
+    x 8x64x64, 3x7x7, StereoRoPE, linear-ramp overlaps): 2048 face cells over all 128
+    planes (face corners, single-cover cells, both overlap strips, four-tile corners)
+    against the oracle's forward of the covering tiles' queries and its stitch
+    (Sec. 3.2; App. F, Eq. stitch) -- the same check as the bench line's parity."""
+    import os
+    import sys
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    import bench
+    wl = I.FACE_ROLLOUT
+    nty, ntx, sy, sx = wl.tiling
+    Hf, Wf = (nty - 1) * sy + wl.H, (ntx - 1) * sx + wl.W
+    qkv_host = wl.qkv()
+    q, k, v = (torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).cuda() for x in qkv_host)
+    geom = pipeline.TileGeometry(*(torch.from_numpy(a).cuda() for a in wl.placement().as_int32()))
+    win_np = I.ramp_window_2d(wl.H, wl.W, I.FACE_OVERLAP)
+    face = torch.empty((wl.heads * wl.Z, Hf, Wf, wl.d), dtype=torch.bfloat16, device="cuda")
+    pipeline.face_step(q, k, v, geom, (wl.kz, wl.ky, wl.kx), wl.scale, wl.tiling,
+                       torch.from_numpy(win_np).cuda(), face, fused=True)
+    torch.cuda.synchronize()
+    del q, k, v
+    cells = bench.face_sample_cells(wl)
+    idx = torch.from_numpy((cells[0] * Hf + cells[1]) * Wf + cells[2]).cuda()
+    rows = face.view(-1, wl.d).index_select(0, idx).float().cpu().numpy().astype(np.float64)
+    par = bench.face_parity(wl, qkv_host, rows, cells, win_np)
+    assert par["n_cells"] == 2048 and par["planes"] == wl.heads * wl.Z, par
+    assert par["pass_r11"], par
