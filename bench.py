@@ -438,8 +438,9 @@ def options_train_bwd(steps: int) -> dict:
 
 def paper_shapes(steps: int) -> dict:
     """The paper's own attention shapes (24 levels): NA3D 9x9x9 on 16x16- and
-    32x32-token tiles, column-wise attention over all 24 levels, the decoder's
-    head_dim-128 NA3D; forward (and backward) against their rooflines.  Inputs
+    32x32-token tiles, 3x7x7 over 24 levels (forward), column-wise attention over
+    all 24 levels, the decoder's head_dim-128 NA3D; forward (and backward) against
+    their rooflines.  Inputs
     are seeded N(0,1) drawn on the device (their values do not change the time)."""
     import torch
     from paper_2606_31248_amd import binding as Bd
@@ -447,7 +448,8 @@ def paper_shapes(steps: int) -> dict:
     from paper_2606_31248_amd import pipeline as Pp
     dev = torch.device("cuda:0")
     res = {}
-    for wl, bwd in ((I.PAPER_TILE16, True), (I.PAPER_TILE32, True), (I.PAPER_COLUMN, True), (I.PAPER_DECODER, True)):
+    for wl, bwd in ((I.PAPER_TILE16, True), (I.PAPER_TILE32, True), (I.Z24_TILE, False), (I.PAPER_COLUMN, True),
+                    (I.PAPER_DECODER, True)):
         gen = torch.Generator(device=dev)
         gen.manual_seed(wl.seed)
         q, k, v, g = (torch.randn(wl.shape(), generator=gen, device=dev).to(torch.bfloat16) for _ in range(4))
@@ -1140,6 +1142,7 @@ def main():
         res["paper_shapes"] = ps
         res["rows"]["f2_na3d_fwd_w999_paper_tile16"] = ps[I.PAPER_TILE16.name]["fwd"]
         res["rows"]["f2_na3d_bwd_w999_paper_tile16"] = ps[I.PAPER_TILE16.name]["bwd"]
+        res["rows"]["f2_na3d_fwd_w377_z24"] = ps[I.Z24_TILE.name]["fwd"]
         res["rows"]["f2_column_fwd_paper"] = ps[I.PAPER_COLUMN.name]["fwd"]
         res["rows"]["f2_na3d_fwd_d128_decoder"] = ps[I.PAPER_DECODER.name]["fwd"]
         res["rows"]["f2_na3d_bwd_d128_decoder"] = ps[I.PAPER_DECODER.name]["bwd"]
