@@ -558,7 +558,8 @@ def profile_workload(name: str, steps: int, warmup: int, calib_copy: bool = Fals
     backward), paper16_fwd / paper16_bwd (9x9x9 at 24 levels on 16x16-token
     tiles), paper32_fwd / paper32_bwd, z24_fwd (3x7x7 at 24 levels),
     rope (the standalone rotation of the training tile's Q), blend (the whole
-    stitch of the face tiling), duo (the planned Duo padding)."""
+    stitch of the face tiling), wind (the wind rotation cut from one face into
+    the face tiling), duo (the planned Duo padding)."""
     import torch
     from paper_2606_31248_amd import binding as Bd
     from paper_2606_31248_amd import inputs as I
@@ -608,6 +609,12 @@ def profile_workload(name: str, steps: int, warmup: int, calib_copy: bool = Fals
         else:
             fn = lambda: Pp.face_step(q, k, v, geom, (wl.kz, wl.ky, wl.kx), wl.scale, wl.tiling, win, face,
                                       coords=coords, cs=cs, out=out, fused=True)
+    elif name == "wind":
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(1010)
+        field = torch.randn((8, 2048, 2048, 2), generator=gen, device=dev).to(torch.bfloat16)
+        tiles = torch.empty((81, 8, 256, 256, 2), dtype=torch.bfloat16, device=dev)
+        fn = lambda: Bd.strata_wind_tile_frame(field, 0, 9, 9, 224, 224, tiles)
     elif name == "duo":
         n, h, P, C = 2048, 16, 8, 4
         gen = torch.Generator(device=dev)
