@@ -256,10 +256,7 @@ def test_face_step_seeded_full_size_against_oracle():
     planes (face corners, single-cover cells, both overlap strips, four-tile corners)
     against the oracle's forward of the covering tiles' queries and its stitch
     (Sec. 3.2; App. F, Eq. stitch) -- the same check as the bench line's parity."""
-    import os
-    import sys
-    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
-    import bench
+    import bench  # the repository root is on sys.path (conftest)
     wl = I.FACE_ROLLOUT
     nty, ntx, sy, sx = wl.tiling
     Hf, Wf = (nty - 1) * sy + wl.H, (ntx - 1) * sx + wl.W
