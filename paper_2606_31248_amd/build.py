@@ -18,7 +18,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libstrata.so")
 
 SOURCES = ["api.hip", "geometry.hip", "rope.hip", "blend.hip", "na3d_ref.hip", "na3d_opts.hip", "na3d_col.hip", "duo.hip", "na3d_mfma_q.hip",
-           "na3d_mfma_kv.hip", "na3d_fwd_zs.hip", "na3d_fwd_lsg.hip", "na3d_mfma_d128.hip",
+           "na3d_mfma_kv.hip", "na3d_mfma_kvp.hip", "na3d_fwd_zs.hip", "na3d_fwd_lsg.hip", "na3d_mfma_d128.hip",
            "na3d_bwd_d128.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -34,7 +34,7 @@ FLAGS = [
 
 # Per-file extra flags.  The attention kernel never sees NaN inputs by contract
 # (masked logits are -inf, not NaN), so max() needs no NaN canonicalisation.
-EXTRA = {"na3d_mfma_q.hip": ["-fno-honor-nans"], "na3d_mfma_d128.hip": ["-fno-honor-nans"], "na3d_bwd_d128.hip": ["-fno-honor-nans"], "na3d_col.hip": ["-fno-honor-nans"], "na3d_mfma_kv.hip": ["-fno-honor-nans"],
+EXTRA = {"na3d_mfma_q.hip": ["-fno-honor-nans"], "na3d_mfma_d128.hip": ["-fno-honor-nans"], "na3d_bwd_d128.hip": ["-fno-honor-nans"], "na3d_col.hip": ["-fno-honor-nans"], "na3d_mfma_kv.hip": ["-fno-honor-nans"], "na3d_mfma_kvp.hip": ["-fno-honor-nans"],
          # the level-sweep forward: MFMA accumulators in VGPRs, so that the logits the
          # softmax reads are not routed through AGPRs
          "na3d_fwd_zs.hip": ["-fno-honor-nans", "-mllvm", "-amdgpu-mfma-vgpr-form=1"],

@@ -202,7 +202,8 @@ static strata_status na3d_bwd_launch(const strata_na3d_desc* desc, const strata_
   if (!launch_na3d_bwd_dq_mfma(*desc, bo, q, k, v, cs, ga, lse, dvec, dq, s) &&
       !launch_na3d_bwd_dq_d128(*desc, bo, q, k, v, cs, ga, lse, dvec, dq, s))
     launch_na3d_bwd_ref(1, *desc, bo, q, k, v, cs, out, ga, lse, dq, dk, dv, dvec, s);
-  if (!launch_na3d_bwd_dkdv_mfma(*desc, bo, q, k, v, cs, ga, lse, dvec, dk, dv, s) &&
+  if (!launch_na3d_bwd_dkdv_kvp(*desc, bo, q, k, v, cs, ga, lse, dvec, dk, dv, s) &&
+      !launch_na3d_bwd_dkdv_mfma(*desc, bo, q, k, v, cs, ga, lse, dvec, dk, dv, s) &&
       !launch_na3d_bwd_dkdv_d128(*desc, bo, q, k, v, cs, ga, lse, dvec, dk, dv, s))
     launch_na3d_bwd_ref(2, *desc, bo, q, k, v, cs, out, ga, lse, dq, dk, dv, dvec, s);
   return check_launch(opts ? "strata_na3d_bwd_ex" : "strata_na3d_bwd");

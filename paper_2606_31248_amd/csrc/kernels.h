@@ -105,6 +105,11 @@ bool launch_na3d_bwd_dq_mfma(const strata_na3d_desc& d, const BwdOpts& o, const 
 bool launch_na3d_bwd_col(const strata_na3d_desc& d, const BwdOpts& o, const void* q, const void* k,
                          const void* v, const void* dout, const float* lse, const float* dvec, void* dq,
                          void* dk, void* dv, hipStream_t s);
+// dK/dV with two key levels x four 4x4 blocks per workgroup (bf16, head_dim 64,
+// windows 5x9x9 and 9x9x9, no two-term dO); false if not applicable
+bool launch_na3d_bwd_dkdv_kvp(const strata_na3d_desc& d, const BwdOpts& o, const void* q, const void* k,
+                              const void* v, const float* cs, const void* dout, const float* lse,
+                              const float* dvec, void* dk, void* dv, hipStream_t s);
 bool launch_na3d_bwd_dkdv_mfma(const strata_na3d_desc& d, const BwdOpts& o, const void* q,
                                const void* k, const void* v, const float* cs, const void* dout,
                                const float* lse, const float* dvec, void* dk, void* dv,
