@@ -130,6 +130,7 @@ struct Args {
   const float* dvec;     // backward: D = rowsum(dO * O)
   int heads, Z, H, W;
   int n_zb, n_yb, n_xb;
+  int n_zc, zb_per;   // runs of query-level groups per column, groups per run
   float qscale;       // scale * log2(e)
   float scale;
   // options: QK RMSNorm (factor applied in float32 before the float16
@@ -166,11 +167,15 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
   if ((nblk & 7) == 0) bid = (bid & 7) * (nblk >> 3) + (bid >> 3);
   const int xb = bid % a.n_xb;
   const int yb = (bid / a.n_xb) % a.n_yb;
-  const int zb = (bid / (a.n_xb * a.n_yb)) % a.n_zb;
-  const int bh = bid / (a.n_xb * a.n_yb * a.n_zb);
+  const int zc = (bid / (a.n_xb * a.n_yb)) % a.n_zc;
+  const int bh = bid / (a.n_xb * a.n_yb * a.n_zc);
   const int b = bh / a.heads;
   const int H = a.H, W = a.W, Z = a.Z;
-  const int by0 = yb * kBY, bx0 = xb * kBX, z0 = zb * ZQ;
+  const int by0 = yb * kBY, bx0 = xb * kBX;
+  // the workgroup takes the groups [zb_lo, zb_hi) of ZQ query levels one after
+  // another; z0 is the first level of the current group
+  const int zb_lo = zc * a.zb_per, zb_hi = min(zb_lo + a.zb_per, a.n_zb);
+  int z0 = zb_lo * ZQ;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -329,48 +334,52 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
   int ex[C::QL];
   f32x4 o[C::QL][4];
   const float4* csq = csb ? csb + ((int64_t)qy * W + qx) * 16 : nullptr;
+  // queries of the group starting at level z0 (and, backward, their dO, LSE, D)
+  auto begin_group = [&]() __attribute__((always_inline)) {
 #pragma unroll
-  for (int j = 0; j < C::QL; ++j) {
-    int zq = min(z0 + grp + 2 * j, Z - 1);
-    const int64_t tok = bh_base + zq * HW + (int64_t)qy * W + qx;
-    const uint4* src = reinterpret_cast<const uint4*>(a.q + tok * kD);
-    uint4 x0 = src[g], x1 = src[4 + g];
-    uint4 r0, r1;
-    float mul = a.qscale;
-    if constexpr (NORM) {  // the 4 lanes of a query row hold its 64 values
-      const float rn = __builtin_amdgcn_rsqf(sum_over_rows(sumsq8(x1, sumsq8(x0, 0.f))) * (1.f / kD) + a.eps);
-      mul *= rn;
-      if constexpr (BWD) rq[j] = rn;
-    }
-    if (csq) {
-      r0 = rotate8h(x0, csq[2 * g], csq[2 * g + 1], mul);
-      r1 = rotate8h(x1, csq[8 + 2 * g], csq[8 + 2 * g + 1], mul);
-    } else {
-      r0 = scale8h(x0, mul);
-      r1 = scale8h(x1, mul);
-    }
-    qf[j][0] = __builtin_bit_cast(f16x8, r0);
-    qf[j][1] = __builtin_bit_cast(f16x8, r1);
-    if constexpr (BWD) {
-      const uint4* gsrc = reinterpret_cast<const uint4*>(a.dout + tok * kD);
-      gf[j][0] = __builtin_bit_cast(bf16x8, gsrc[g]);
-      gf[j][1] = __builtin_bit_cast(bf16x8, gsrc[4 + g]);
-      if constexpr (LO) {
-        const uint4* lsrc = reinterpret_cast<const uint4*>(a.dout_lo + tok * kD);
-        gl[j][0] = __builtin_bit_cast(bf16x8, lsrc[g]);
-        gl[j][1] = __builtin_bit_cast(bf16x8, lsrc[4 + g]);
+    for (int j = 0; j < C::QL; ++j) {
+      int zq = min(z0 + grp + 2 * j, Z - 1);
+      const int64_t tok = bh_base + zq * HW + (int64_t)qy * W + qx;
+      const uint4* src = reinterpret_cast<const uint4*>(a.q + tok * kD);
+      uint4 x0 = src[g], x1 = src[4 + g];
+      uint4 r0, r1;
+      float mul = a.qscale;
+      if constexpr (NORM) {  // the 4 lanes of a query row hold its 64 values
+        const float rn = __builtin_amdgcn_rsqf(sum_over_rows(sumsq8(x1, sumsq8(x0, 0.f))) * (1.f / kD) + a.eps);
+        mul *= rn;
+        if constexpr (BWD) rq[j] = rn;
       }
-      m[j] = a.lse_in[tok] * kLog2e;  // lse2
-      l[j] = -a.dvec[tok];            // -D
-      ex[j] = kMinExp;
-    } else {
-      m[j] = 0.f;
-      l[j] = 0.f;
-      mset[j] = false;
-    }
+      if (csq) {
+        r0 = rotate8h(x0, csq[2 * g], csq[2 * g + 1], mul);
+        r1 = rotate8h(x1, csq[8 + 2 * g], csq[8 + 2 * g + 1], mul);
+      } else {
+        r0 = scale8h(x0, mul);
+        r1 = scale8h(x1, mul);
+      }
+      qf[j][0] = __builtin_bit_cast(f16x8, r0);
+      qf[j][1] = __builtin_bit_cast(f16x8, r1);
+      if constexpr (BWD) {
+        const uint4* gsrc = reinterpret_cast<const uint4*>(a.dout + tok * kD);
+        gf[j][0] = __builtin_bit_cast(bf16x8, gsrc[g]);
+        gf[j][1] = __builtin_bit_cast(bf16x8, gsrc[4 + g]);
+        if constexpr (LO) {
+          const uint4* lsrc = reinterpret_cast<const uint4*>(a.dout_lo + tok * kD);
+          gl[j][0] = __builtin_bit_cast(bf16x8, lsrc[g]);
+          gl[j][1] = __builtin_bit_cast(bf16x8, lsrc[4 + g]);
+        }
+        m[j] = a.lse_in[tok] * kLog2e;  // lse2
+        l[j] = -a.dvec[tok];            // -D
+        ex[j] = kMinExp;
+      } else {
+        m[j] = 0.f;
+        l[j] = 0.f;
+        mset[j] = false;
+      }
 #pragma unroll
-    for (int t = 0; t < 4; ++t) o[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
+      for (int t = 0; t < 4; ++t) o[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  begin_group();
 
   // one (query level j, key level) update with the key tiles tk, tv; `first`:
   // the query level's first key level (nothing accumulated yet)
@@ -510,98 +519,123 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
     }
   };
 
-  // ---- key levels needed by the block's query levels, double-buffered -------
-  // Level p+1 is copied while level p is computed; then each thread waits for
-  // its own copies, rotates its own K slots, and one barrier publishes the level.
-  // The barrier also retires every read of the tiles the next copy overwrites.
-  const int zlast = min(z0 + ZQ, Z) - 1;
-  const int kp_lo = win_start(z0, Z, KZ);
-  const int kp_hi = win_start(zlast, Z, KZ) + KZ;
+  // ---- normalise and store --------------------------------------------------------
+  auto end_group = [&]() __attribute__((always_inline)) {
+    const bool in_grid = qy_raw < H && qx_raw < W;
+#pragma unroll
+    for (int j = 0; j < C::QL; ++j) {
+      const int zq = z0 + grp + 2 * j;
+      if constexpr (BWD) {
+        // dQ = R^T (scale 2^(E-15) dQ~); lane holds d = 16t + 4g + i.  With QK
+        // RMSNorm that is the gradient of q^ = r q, carried back through the
+        // norm: dq = r (dq^ - q^ mean(dq^ q^)), q^ from the raw row in float32.
+        const float f = a.scale * __builtin_amdgcn_ldexpf(1.f, ex[j] - 15);
+        const int64_t tok = bh_base + min(zq, Z - 1) * HW + (int64_t)qy * W + qx;
+        f32x4 x[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          x[t] = o[j][t] * f;
+          if (csq) {
+            const float4 ph = csq[4 * t + g];  // pairs 8t+2g and 8t+2g+1
+            const float r0 = fmaf(x[t][0], ph.x, x[t][1] * ph.y), r1 = fmaf(x[t][1], ph.x, -x[t][0] * ph.y);
+            const float r2 = fmaf(x[t][2], ph.z, x[t][3] * ph.w), r3 = fmaf(x[t][3], ph.z, -x[t][2] * ph.w);
+            x[t] = f32x4{r0, r1, r2, r3};
+          }
+        }
+        if constexpr (NORM) {
+          const uint2* qr = reinterpret_cast<const uint2*>(a.q + tok * kD);
+          f32x4 qh[4];
+          float c = 0.f;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const uint2 w = qr[4 * t + g];
+            qh[t] = f32x4{lo_bf16(w.x), hi_bf16(w.x), lo_bf16(w.y), hi_bf16(w.y)} * rq[j];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) c = fmaf(x[t][i], qh[t][i], c);
+          }
+          c = sum_over_rows(c) * (1.f / kD);
+#pragma unroll
+          for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) x[t][i] = rq[j] * fmaf(-qh[t][i], c, x[t][i]);
+        }
+        if (zq >= Z || !in_grid) continue;
+        uint2* dst = reinterpret_cast<uint2*>(a.out + tok * kD);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) dst[4 * t + g] = make_uint2(pack2(x[t][0], x[t][1]), pack2(x[t][2], x[t][3]));
+      } else {
+        const float lt = sum_over_rows(l[j]);
+        if (zq >= Z || !in_grid) continue;
+        float inv = 1.f / lt;
+        const int64_t tok = bh_base + zq * HW + (int64_t)qy * W + qx;
+        uint2* dst = reinterpret_cast<uint2*>(a.out + tok * kD);
+        if constexpr (GATE)
+          if (a.gate_dim == 1) inv *= sigmoid_fast(bf16_to_f32(a.gate[tok]));
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {  // d = 16t + 4g + i
+          f32x4 r = o[j][t] * inv;
+          if constexpr (GATE)
+            if (a.gate_dim != 1) r *= sigmoid4_bf16(reinterpret_cast<const uint2*>(a.gate + tok * kD)[4 * t + g]);
+          dst[4 * t + g] = make_uint2(pack2(r[0], r[1]), pack2(r[2], r[3]));
+        }
+        if (a.lse && g == 0) a.lse[tok] = (m[j] + __log2f(lt)) * kLn2;
+      }
+    }
+  };
 
-  issue_copy(kp_lo, tK0, tV0);
+  // ---- the groups' key levels, double-buffered ----------------------------------
+  // Group zb needs the key levels [kp_lo(zb), kp_hi(zb)); the workgroup walks
+  // them group after group, copying the next (group, key level) while the
+  // current one is computed, so the copies keep running across the end of a
+  // group.  Each thread waits for its own copies, rotates its own K slots, and
+  // one barrier publishes the level; the barrier also retires every read of the
+  // tiles the next copy overwrites.
+  auto kp_lo = [&](int zb) { return win_start(zb * ZQ, Z, KZ); };
+  auto kp_hi = [&](int zb) { return win_start(min(zb * ZQ + ZQ, Z) - 1, Z, KZ) + KZ; };
+  auto next_of = [&](int zb, int p, int& nz, int& np) {
+    nz = zb;
+    np = p + 1;
+    if (np >= kp_hi(zb)) {
+      nz = zb + 1;
+      np = nz < zb_hi ? kp_lo(nz) : 0;
+    }
+  };
+  auto change_group = [&](int nz, bool more) __attribute__((always_inline)) {
+    end_group();
+    if (more) {
+      z0 = nz * ZQ;
+      begin_group();
+    }
+  };
+  int cz = zb_lo, cp = kp_lo(zb_lo);
+  issue_copy(cp, tK0, tV0);
   __builtin_amdgcn_s_waitcnt(0);
   rotate_k(tK0);
   __syncthreads();
-  for (int p = kp_lo; p < kp_hi; p += 2) {
-    // level p in tiles 0, level p+1 (if any) in tiles 1
-    const bool more1 = p + 1 < kp_hi;
-    if (more1) issue_copy(p + 1, tK1, tV1);
-    compute(p, tK0, tV0);
-    if (more1) {
-      __builtin_amdgcn_s_waitcnt(0);
-      rotate_k(tK1);
-      __syncthreads();
-      const bool more2 = p + 2 < kp_hi;
-      if (more2) issue_copy(p + 2, tK0, tV0);
-      compute(p + 1, tK1, tV1);
-      if (more2) {
-        __builtin_amdgcn_s_waitcnt(0);
-        rotate_k(tK0);
-        __syncthreads();
-      }
-    }
-  }
-
-  // ---- normalise and store --------------------------------------------------------
-  const bool in_grid = qy_raw < H && qx_raw < W;
-#pragma unroll
-  for (int j = 0; j < C::QL; ++j) {
-    const int zq = z0 + grp + 2 * j;
-    if constexpr (BWD) {
-      // dQ = R^T (scale 2^(E-15) dQ~); lane holds d = 16t + 4g + i.  With QK
-      // RMSNorm that is the gradient of q^ = r q, carried back through the
-      // norm: dq = r (dq^ - q^ mean(dq^ q^)), q^ from the raw row in float32.
-      const float f = a.scale * __builtin_amdgcn_ldexpf(1.f, ex[j] - 15);
-      const int64_t tok = bh_base + min(zq, Z - 1) * HW + (int64_t)qy * W + qx;
-      f32x4 x[4];
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        x[t] = o[j][t] * f;
-        if (csq) {
-          const float4 ph = csq[4 * t + g];  // pairs 8t+2g and 8t+2g+1
-          const float r0 = fmaf(x[t][0], ph.x, x[t][1] * ph.y), r1 = fmaf(x[t][1], ph.x, -x[t][0] * ph.y);
-          const float r2 = fmaf(x[t][2], ph.z, x[t][3] * ph.w), r3 = fmaf(x[t][3], ph.z, -x[t][2] * ph.w);
-          x[t] = f32x4{r0, r1, r2, r3};
-        }
-      }
-      if constexpr (NORM) {
-        const uint2* qr = reinterpret_cast<const uint2*>(a.q + tok * kD);
-        f32x4 qh[4];
-        float c = 0.f;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const uint2 w = qr[4 * t + g];
-          qh[t] = f32x4{lo_bf16(w.x), hi_bf16(w.x), lo_bf16(w.y), hi_bf16(w.y)} * rq[j];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) c = fmaf(x[t][i], qh[t][i], c);
-        }
-        c = sum_over_rows(c) * (1.f / kD);
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) x[t][i] = rq[j] * fmaf(-qh[t][i], c, x[t][i]);
-      }
-      if (zq >= Z || !in_grid) continue;
-      uint2* dst = reinterpret_cast<uint2*>(a.out + tok * kD);
-#pragma unroll
-      for (int t = 0; t < 4; ++t) dst[4 * t + g] = make_uint2(pack2(x[t][0], x[t][1]), pack2(x[t][2], x[t][3]));
-    } else {
-      const float lt = sum_over_rows(l[j]);
-      if (zq >= Z || !in_grid) continue;
-      float inv = 1.f / lt;
-      const int64_t tok = bh_base + zq * HW + (int64_t)qy * W + qx;
-      uint2* dst = reinterpret_cast<uint2*>(a.out + tok * kD);
-      if constexpr (GATE)
-        if (a.gate_dim == 1) inv *= sigmoid_fast(bf16_to_f32(a.gate[tok]));
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {  // d = 16t + 4g + i
-        f32x4 r = o[j][t] * inv;
-        if constexpr (GATE)
-          if (a.gate_dim != 1) r *= sigmoid4_bf16(reinterpret_cast<const uint2*>(a.gate + tok * kD)[4 * t + g]);
-        dst[4 * t + g] = make_uint2(pack2(r[0], r[1]), pack2(r[2], r[3]));
-      }
-      if (a.lse && g == 0) a.lse[tok] = (m[j] + __log2f(lt)) * kLn2;
-    }
+  for (;;) {
+    int nz, np;
+    next_of(cz, cp, nz, np);
+    bool more = nz < zb_hi;
+    if (more) issue_copy(np, tK1, tV1);
+    compute(cp, tK0, tV0);
+    if (nz != cz) change_group(nz, more);
+    if (!more) break;
+    __builtin_amdgcn_s_waitcnt(0);
+    rotate_k(tK1);
+    __syncthreads();
+    cz = nz;
+    cp = np;
+    next_of(cz, cp, nz, np);
+    more = nz < zb_hi;
+    if (more) issue_copy(np, tK0, tV0);
+    compute(cp, tK1, tV1);
+    if (nz != cz) change_group(nz, more);
+    if (!more) break;
+    __builtin_amdgcn_s_waitcnt(0);
+    rotate_k(tK0);
+    __syncthreads();
+    cz = nz;
+    cp = np;
   }
 }
 
@@ -619,6 +653,14 @@ Args make_args(const strata_na3d_desc& d, int zq, const void* q, const void* k, 
   a.n_zb = (d.Z + zq - 1) / zq;
   a.n_yb = (d.H + kBY - 1) / kBY;
   a.n_xb = (d.W + kBX - 1) / kBX;
+  // a workgroup walks a whole column of query-level groups (the setup is paid
+  // once, and the key copies run on across groups) unless that leaves fewer
+  // than 1024 workgroups: then the column is cut into runs
+  const int64_t cols = (int64_t)d.B * d.heads * a.n_yb * a.n_xb;
+  a.n_zc = 1;
+  while (a.n_zc < a.n_zb && cols * a.n_zc < 1024) ++a.n_zc;
+  a.zb_per = (a.n_zb + a.n_zc - 1) / a.n_zc;
+  a.n_zc = (a.n_zb + a.zb_per - 1) / a.zb_per;
   a.qscale = d.scale * kLog2e;
   a.scale = d.scale;
   return a;
@@ -626,7 +668,7 @@ Args make_args(const strata_na3d_desc& d, int zq, const void* q, const void* k, 
 
 template <int KZ, int KY, int KX, int ZQ, bool BWD>
 bool launch(const strata_na3d_desc& d, const Args& a, int opt, hipStream_t s) {
-  int64_t blocks = (int64_t)d.B * d.heads * a.n_zb * a.n_yb * a.n_xb;
+  int64_t blocks = (int64_t)d.B * d.heads * a.n_zc * a.n_yb * a.n_xb;
   if (blocks >= (int64_t)1 << 31) return false;
   const dim3 grid((unsigned)blocks), block(kThreads);
   switch (opt) {
