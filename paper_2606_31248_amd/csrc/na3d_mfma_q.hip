@@ -76,8 +76,6 @@ using namespace mfma;
 
 
 constexpr int kBY = 8, kBX = 8;  // query block of a workgroup (y, x)
-constexpr int kWaves = 8;
-constexpr int kThreads = 64 * kWaves;
 constexpr int kD = 64;           // head_dim
 constexpr int kKRow = 128;       // LDS bytes per key row of K (16-byte columns swizzled)
 constexpr int kVRow = 160;       // LDS bytes per key row of V (128 + 32 pad)
@@ -88,8 +86,11 @@ constexpr float kLazy = 8.0f;    // move the softmax reference only when a logit
 constexpr float kLow = -64.0f;   // ... or down, on a level's first key level
 constexpr int kMinExp = -100;    // lower bound of the dS exponent (keeps 2^(15-E) finite)
 
-template <int KZ, int KY, int KX, int ZQ, bool BWD>
+// NG groups of four waves, one wave per 4x4 sub-block in each group; group g
+// takes the levels g, g + NG, ... of the block's ZQ levels
+template <int KZ, int KY, int KX, int ZQ, bool BWD, int NG>
 struct Cfg {
+  static constexpr int kThreads = 256 * NG;
   // V rows: the forward reads V^T by transpose reads (160-byte rows spread
   // them); the backward reads V rows as an A operand like K (128-byte rows with
   // K's column swizzle, conflict-free)
@@ -113,8 +114,8 @@ struct Cfg {
   static constexpr bool GOFF_LDS = 2 * BUF + GOFF_BYTES <= kLdsMax;
   static constexpr int PH_BYTES = KSLOTS * 16;
   static constexpr bool PH_LDS = GOFF_LDS && 2 * BUF + GOFF_BYTES + PH_BYTES <= kLdsMax;
-  static constexpr int QL = ZQ / 2;                           // query levels per wave
-  static_assert(ZQ % 2 == 0, "ZQ must be even");
+  static constexpr int QL = ZQ / NG;                          // query levels per wave
+  static_assert(ZQ % NG == 0, "ZQ must be a multiple of NG");
   static_assert(2 * BUF <= kLdsMax, "key tiles exceed LDS");
 };
 
@@ -147,12 +148,13 @@ struct Args {
 // a two-term dO (backward)
 constexpr int kNorm = 1, kOpt2 = 2;
 
-template <int KZ, int KY, int KX, int ZQ, bool BWD, int OPT>
-__global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
+template <int KZ, int KY, int KX, int ZQ, bool BWD, int OPT, int NG>
+__global__ void __launch_bounds__(256 * NG, 1) na3d_mfma_q_kernel(Args a) {
   constexpr bool NORM = (OPT & kNorm) != 0;
   constexpr bool GATE = !BWD && (OPT & kOpt2) != 0;
   constexpr bool LO = BWD && (OPT & kOpt2) != 0;
-  using C = Cfg<KZ, KY, KX, ZQ, BWD>;
+  using C = Cfg<KZ, KY, KX, ZQ, BWD, NG>;
+  constexpr int kThreads = C::kThreads;
   // double buffer of key tiles (distinct objects, see above), copy offsets, phases
   __shared__ __attribute__((aligned(16))) char tK0[C::KBYTES];
   __shared__ __attribute__((aligned(16))) char tV0[C::VBYTES];
@@ -180,7 +182,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, qn = lane & 15;
-  const int sb = wave & 3, grp = wave >> 2;  // xy sub-block, level parity
+  const int sb = wave & 3, grp = wave >> 2;  // xy sub-block, level group
 
   // staged key box of the workgroup, and the key box of this wave's sub-block
   const int ty0 = win_start(min(by0, H - 1), H, KY);
@@ -207,7 +209,12 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
   // forward: vaddr = V^T transpose-read address; backward: vaddr = V row (A
   // operand) address, ktaddr = K~^T transpose-read address
   uint32_t kaddr[C::NC], vaddr[C::NC], ktaddr[BWD ? C::NC : 1];
-  f32x4 bias[C::NC];
+  // window mask: forward, the accumulator seeds (0 / -inf); backward, bits (bit
+  // 4c + i: row 4g + i of chunk c seen by the lane's query), from which each
+  // step selects its seeds
+  f32x4 bias[BWD ? 1 : C::NC];
+  static_assert(!BWD || C::NC <= 16, "window bits of a lane fit two words");
+  uint32_t mbits[2] = {0u, 0u};
 #pragma unroll
   for (int c = 0; c < C::NC; ++c) {
     {  // K fragment (A operand): row = key 16c + qn, 16 bytes at column g (xor 64 bytes: g+4)
@@ -227,7 +234,10 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
       int u = 16 * c + 4 * g + i;
       int ky = uy0 + u / C::NUX, kx = ux0 + u % C::NUX;
       bool ok = u < C::NU && ky >= wys && ky < wys + KY && kx >= wxs && kx < wxs + KX;
-      bias[c][i] = ok ? 0.f : -INFINITY;
+      if constexpr (BWD)
+        mbits[c >> 3] |= (ok ? 1u : 0u) << (4 * (c & 7) + i);
+      else
+        bias[c][i] = ok ? 0.f : -INFINITY;
     }
   }
 
@@ -338,7 +348,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
   auto begin_group = [&]() __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < C::QL; ++j) {
-      int zq = min(z0 + grp + 2 * j, Z - 1);
+      int zq = min(z0 + grp + NG * j, Z - 1);
       const int64_t tok = bh_base + zq * HW + (int64_t)qy * W + qx;
       const uint4* src = reinterpret_cast<const uint4*>(a.q + tok * kD);
       uint4 x0 = src[g], x1 = src[4 + g];
@@ -447,60 +457,88 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
     }
   };
 
-  // backward: one (query level j, key level) step of dQ~ with the key tiles tk, tv
+  // backward: one (query level j, key level) update of dQ~ with the key tiles
+  // tk, tv, 32 keys (two chunks) at a time: logits and Y, the exponent bound of
+  // |Y| grown to cover them (the accumulator rescaled exactly when it grows), dS
+  // in float16 with the current scale, and the dQ MFMAs of the two chunks.  The
+  // logits are seeded with -(lse2 + E - 15) where the lane's query sees the key
+  // (so that P 2^(15-E) = exp2(S)) and -inf elsewhere, selected by the window
+  // bits; a step whose bound grows moves its own logits by the change.
   auto update_dq = [&](int j, const char* tk, const char* tv) {
-    f32x4 s[C::NC], y[C::NC];
     const f32x4 nd = {l[j], l[j], l[j], l[j]};
-#pragma unroll
-    for (int c = 0; c < C::NC; ++c) {
-      f16x8 k0 = __builtin_bit_cast(f16x8, ld16(tk + kaddr[c]));
-      f16x8 k1 = __builtin_bit_cast(f16x8, ld16(tk + (kaddr[c] ^ 64u)));
-      f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(k0, qf[j][0], bias[c], 0, 0, 0);
-      s[c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(k1, qf[j][1], acc, 0, 0, 0);
-      bf16x8 v0 = __builtin_bit_cast(bf16x8, ld16(tv + vaddr[c]));
-      bf16x8 v1 = __builtin_bit_cast(bf16x8, ld16(tv + (vaddr[c] ^ 64u)));
-      f32x4 t0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v0, gf[j][0], nd, 0, 0, 0);
-      y[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v1, gf[j][1], t0, 0, 0, 0);
-      if constexpr (LO) {
-        y[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v0, gl[j][0], y[c], 0, 0, 0);
-        y[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v1, gl[j][1], y[c], 0, 0, 0);
-      }
-    }
-    // exponent bound of |Y| over this level's keys (all rows of the query)
-    float my = 0.f;
-#pragma unroll
-    for (int c = 0; c < C::NC; ++c)
-      my = fmaxf(fmaxf(my, fmaxf(fabsf(y[c][0]), fabsf(y[c][1]))), fmaxf(fabsf(y[c][2]), fabsf(y[c][3])));
-    my = max_over_rows(my);
-    const int e = max(__builtin_amdgcn_frexp_expf(my), kMinExp);
-    if (__any(e > ex[j])) {  // the bound grew: rescale the accumulator exactly
-      const int en = max(ex[j], e);
-      const float f = __builtin_amdgcn_ldexpf(1.f, ex[j] - en);
-#pragma unroll
-      for (int t = 0; t < 4; ++t) o[j][t] *= f;
-      ex[j] = en;
-    }
-    // P scaled by 2^(15 - E): exp2(S - (lse2 + E - 15))
-    const float cj = m[j] + (float)(ex[j] - 15);
-    uint32_t dk[C::NC][2];
-#pragma unroll
-    for (int c = 0; c < C::NC; ++c) {
-      const float p0 = __builtin_amdgcn_exp2f(s[c][0] - cj), p1 = __builtin_amdgcn_exp2f(s[c][1] - cj);
-      const float p2 = __builtin_amdgcn_exp2f(s[c][2] - cj), p3 = __builtin_amdgcn_exp2f(s[c][3] - cj);
-      dk[c][0] = pack2h_rne(p0 * y[c][0], p1 * y[c][1]);
-      dk[c][1] = pack2h_rne(p2 * y[c][2], p3 * y[c][3]);
-    }
+    uint32_t mw[2] = {mbits[0], mbits[1]};
+    asm volatile("" : "+v"(mw[0]), "+v"(mw[1]));  // derive the selects step by step
 #pragma unroll
     for (int st = 0; st < C::NS; ++st) {
       const int c0 = 2 * st, c1 = 2 * st + 1;
       const bool two = c1 < C::NC;
-      f16x8 df = __builtin_bit_cast(f16x8, make_uint4(dk[c0][0], dk[c0][1], two ? dk[c1][0] : 0u, two ? dk[c1][1] : 0u));
+      // transpose reads of the step's K~^T, issued first: their latency hides
+      // under the MFMAs and the softmax below
+      uint2 ktl[4], kth[4];
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        i16x4 lo = tr_read(tk + (ktaddr[c0] ^ (32u * t)));
-        i16x4 hi = two ? tr_read(tk + (ktaddr[c1] ^ (32u * t))) : i16x4{0, 0, 0, 0};
-        uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
-        f16x8 kt = __builtin_bit_cast(f16x8, make_uint4(l2.x, l2.y, h2.x, h2.y));
+        ktl[t] = __builtin_bit_cast(uint2, tr_read(tk + (ktaddr[c0] ^ (32u * t))));
+        kth[t] = two ? __builtin_bit_cast(uint2, tr_read(tk + (ktaddr[two ? c1 : c0] ^ (32u * t))))
+                     : make_uint2(0u, 0u);
+      }
+      const uint32_t ncj = __float_as_uint(-(m[j] + (float)(ex[j] - 15)));
+      f32x4 s2[2], y2[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int c = h == 0 ? c0 : (two ? c1 : c0);
+        if (h == 1 && !two) {
+          s2[1] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+          y2[1] = f32x4{0.f, 0.f, 0.f, 0.f};
+          continue;
+        }
+        f32x4 seed;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int bit = 4 * c + i;
+          const uint32_t sel = (uint32_t)__builtin_amdgcn_sbfe((int)mw[bit >> 5], bit & 31, 1);
+          seed[i] = __uint_as_float((sel & ncj) | (~sel & 0xff800000u));
+        }
+        f16x8 k0 = __builtin_bit_cast(f16x8, ld16(tk + kaddr[c]));
+        f16x8 k1 = __builtin_bit_cast(f16x8, ld16(tk + (kaddr[c] ^ 64u)));
+        f32x4 acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(k0, qf[j][0], seed, 0, 0, 0);
+        s2[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(k1, qf[j][1], acc, 0, 0, 0);
+        bf16x8 v0 = __builtin_bit_cast(bf16x8, ld16(tv + vaddr[c]));
+        bf16x8 v1 = __builtin_bit_cast(bf16x8, ld16(tv + (vaddr[c] ^ 64u)));
+        f32x4 t0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v0, gf[j][0], nd, 0, 0, 0);
+        y2[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v1, gf[j][1], t0, 0, 0, 0);
+        if constexpr (LO) {
+          y2[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v0, gl[j][0], y2[h], 0, 0, 0);
+          y2[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v1, gl[j][1], y2[h], 0, 0, 0);
+        }
+      }
+      float my = 0.f;
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        my = fmaxf(fmaxf(my, fmaxf(fabsf(y2[h][0]), fabsf(y2[h][1]))), fmaxf(fabsf(y2[h][2]), fabsf(y2[h][3])));
+      my = max_over_rows(my);
+      const int e = max(__builtin_amdgcn_frexp_expf(my), kMinExp);
+      if (__any(e > ex[j])) {  // the bound grew: rescale the accumulator exactly
+        const int en = max(ex[j], e);
+        const float f = __builtin_amdgcn_ldexpf(1.f, ex[j] - en);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) o[j][t] *= f;
+        const float d = (float)(ex[j] - en);  // this step's logits carry the old offset
+#pragma unroll
+        for (int h = 0; h < 2; ++h) s2[h] += d;
+        ex[j] = en;
+      }
+      uint32_t dk[2][2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const float p0 = __builtin_amdgcn_exp2f(s2[h][0]), p1 = __builtin_amdgcn_exp2f(s2[h][1]);
+        const float p2 = __builtin_amdgcn_exp2f(s2[h][2]), p3 = __builtin_amdgcn_exp2f(s2[h][3]);
+        dk[h][0] = pack2h_rne(p0 * y2[h][0], p1 * y2[h][1]);
+        dk[h][1] = pack2h_rne(p2 * y2[h][2], p3 * y2[h][3]);
+      }
+      const f16x8 df = __builtin_bit_cast(f16x8, make_uint4(dk[0][0], dk[0][1], dk[1][0], dk[1][1]));
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const f16x8 kt = __builtin_bit_cast(f16x8, make_uint4(ktl[t].x, ktl[t].y, kth[t].x, kth[t].y));
         o[j][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kt, df, o[j][t], 0, 0, 0);
       }
     }
@@ -510,7 +548,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
   auto compute = [&](int p, const char* tk, const char* tv) {
 #pragma unroll
     for (int j = 0; j < C::QL; ++j) {
-      const int zq = z0 + grp + 2 * j;
+      const int zq = z0 + grp + NG * j;
       if (zq >= Z) continue;
       const int zs = win_start(zq, Z, KZ);
       if (p < zs || p >= zs + KZ) continue;
@@ -524,7 +562,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_q_kernel(Args a) {
     const bool in_grid = qy_raw < H && qx_raw < W;
 #pragma unroll
     for (int j = 0; j < C::QL; ++j) {
-      const int zq = z0 + grp + 2 * j;
+      const int zq = z0 + grp + NG * j;
       if constexpr (BWD) {
         // dQ = R^T (scale 2^(E-15) dQ~); lane holds d = 16t + 4g + i.  With QK
         // RMSNorm that is the gradient of q^ = r q, carried back through the
@@ -666,16 +704,16 @@ Args make_args(const strata_na3d_desc& d, int zq, const void* q, const void* k, 
   return a;
 }
 
-template <int KZ, int KY, int KX, int ZQ, bool BWD>
+template <int KZ, int KY, int KX, int ZQ, bool BWD, int NG = 2>
 bool launch(const strata_na3d_desc& d, const Args& a, int opt, hipStream_t s) {
   int64_t blocks = (int64_t)d.B * d.heads * a.n_zc * a.n_yb * a.n_xb;
   if (blocks >= (int64_t)1 << 31) return false;
-  const dim3 grid((unsigned)blocks), block(kThreads);
+  const dim3 grid((unsigned)blocks), block(Cfg<KZ, KY, KX, ZQ, BWD, NG>::kThreads);
   switch (opt) {
-    case 0: hipLaunchKernelGGL((na3d_mfma_q_kernel<KZ, KY, KX, ZQ, BWD, 0>), grid, block, 0, s, a); break;
-    case 1: hipLaunchKernelGGL((na3d_mfma_q_kernel<KZ, KY, KX, ZQ, BWD, 1>), grid, block, 0, s, a); break;
-    case 2: hipLaunchKernelGGL((na3d_mfma_q_kernel<KZ, KY, KX, ZQ, BWD, 2>), grid, block, 0, s, a); break;
-    default: hipLaunchKernelGGL((na3d_mfma_q_kernel<KZ, KY, KX, ZQ, BWD, 3>), grid, block, 0, s, a); break;
+    case 0: hipLaunchKernelGGL((na3d_mfma_q_kernel<KZ, KY, KX, ZQ, BWD, 0, NG>), grid, block, 0, s, a); break;
+    case 1: hipLaunchKernelGGL((na3d_mfma_q_kernel<KZ, KY, KX, ZQ, BWD, 1, NG>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((na3d_mfma_q_kernel<KZ, KY, KX, ZQ, BWD, 2, NG>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((na3d_mfma_q_kernel<KZ, KY, KX, ZQ, BWD, 3, NG>), grid, block, 0, s, a); break;
   }
   return true;
 }
@@ -714,7 +752,9 @@ bool launch_na3d_bwd_dq_mfma(const strata_na3d_desc& d, const BwdOpts& o, const 
   const bool w377 = d.kz == 3 && d.ky == 7 && d.kx == 7, w599 = d.kz == 5 && d.ky == 9 && d.kx == 9;
   const bool w999 = d.kz == 9 && d.ky == 9 && d.kx == 9;
   if (!w377 && !w599 && !w999) return false;
-  Args a = make_args(d, w599 ? 2 : (w999 ? 2 : 4), q, k, v, cs);
+  // 9-wide windows: three groups of four waves, one query level each (12 waves,
+  // three per SIMD); 3x7x7: two groups, two levels per wave
+  Args a = make_args(d, w377 ? 4 : 3, q, k, v, cs);
   a.out = static_cast<uint16_t*>(dq);
   a.dout = static_cast<const uint16_t*>(dout);
   a.lse_in = lse;
@@ -724,8 +764,8 @@ bool launch_na3d_bwd_dq_mfma(const strata_na3d_desc& d, const BwdOpts& o, const 
   a.dout_lo = static_cast<const uint16_t*>(o.dout_lo);
   const int opt = (o.qk_norm ? kNorm : 0) | (o.dout_lo ? kOpt2 : 0);
   if (w377) return launch<3, 7, 7, 4, true>(d, a, opt, s);
-  if (w999) return launch<9, 9, 9, 2, true>(d, a, opt, s);
-  return launch<5, 9, 9, 2, true>(d, a, opt, s);
+  if (w999) return launch<9, 9, 9, 3, true, 3>(d, a, opt, s);
+  return launch<5, 9, 9, 3, true, 3>(d, a, opt, s);
 }
 
 }  // namespace strata
