@@ -13,6 +13,8 @@
 //               level w / 4 of the pair and block w % 4 (by = (w / 2) % 2,
 //               bx = w % 2).  Waves w and w + 4 share a SIMD and hold the same
 //               block on the two levels, so every SIMD gets the same work.
+//               (The run length is a template parameter; three levels, three
+//               waves per SIMD, leave too few registers.)
 //   blocks    : along each axis the 4-wide blocks are grouped in pairs (0, n-1),
 //               (1, 2), (3, 4), ...  A block's queries (the union of the inverse
 //               windows of its keys) span a run of "squares", 4-aligned runs of
@@ -56,9 +58,7 @@ constexpr int kGrid = 16;                // staged squares (4 x 4)
 constexpr int kNSq = kGrid + 2;          // plus two zero squares read by padding chunks
 constexpr int kRows = kNSq * 16;
 constexpr int kTB = kRows * kRow;        // bytes per staged tile
-constexpr int kThreads = 512;
 constexpr int kSlots = kGrid * 16 * 8;   // 16-byte copy slots of the grid
-constexpr int kIT = kSlots / kThreads;   // per thread
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kMinExp = -100;            // lower bound of the dS exponent
 static_assert(2 * (2 * kTB + 2 * kRows * 4) <= 160 * 1024, "staged tiles exceed LDS");
@@ -178,8 +178,13 @@ struct Walk {
   static constexpr int rel(int c) { return 4 * row(c) + col(c); }  // square offset from the box's first
 };
 
-template <int KZ, int KY, int KX, bool NORM>
-__global__ void __launch_bounds__(kThreads, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
+// NL key levels per workgroup (4 NL waves): wave w takes level w / 4 of the
+// run and block w % 4
+template <int KZ, int KY, int KX, bool NORM, int NL>
+__global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
+  constexpr int kThreads = 256 * NL;
+  constexpr int kIT = (kSlots + kThreads - 1) / kThreads;  // copy slots per thread
+  static_assert(kIT * kThreads <= kNSq * 128, "copy slots stay inside the staged tile");
   __shared__ __attribute__((aligned(16))) char tQ0[kTB];
   __shared__ __attribute__((aligned(16))) char tG0[kTB];
   __shared__ __attribute__((aligned(16))) char tQ1[kTB];
@@ -198,7 +203,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
   const int bh = bid / (a.ngx * a.ngy);
   const int b = bh / a.heads;
   const int H = a.H, W = a.W, Z = a.Z;
-  const int npairs = (Z + 1) >> 1;
+  const int npairs = (Z + NL - 1) / NL;  // runs of NL key levels
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -217,13 +222,13 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
   uint4 ph[kIT];
 #pragma unroll
   for (int it = 0; it < kIT; ++it) {
-    const int s = it * kThreads + tid, u = s >> 3, sq = s >> 7, rho = u & 15;
+    const int s = it * kThreads + tid, u = s >> 3, sq = s >> 7, rho = u & 15;  // sq > 15: past the grid
     const int dc = (s & 7) ^ rswz(u);
     const int ey = sq >> 2, ex = sq & 3;
     goff[it] = -1;
     ph[it] = make_uint4(0u, 0u, 0u, 0u);
     const int qy = 4 * sq_abs(ay, ey) + (rho >> 2), qx = 4 * sq_abs(ax, ex) + (rho & 3);
-    if (ey < ay.n && ex < ax.n && qy < H && qx < W) {
+    if (s < kSlots && ey < ay.n && ex < ax.n && qy < H && qx < W) {
       goff[it] = (qy * W + qx) * kD + dc * 8;
       if (csb) {  // phases of pairs 4dc .. 4dc+3 as float16 (cos, sin)
         const float4* pp = csb + ((int64_t)qy * W + qx) * 16 + 2 * dc;
@@ -351,7 +356,7 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
     uint2 kr[4];         // raw row of the stored key
     uint4 xk[2], xv[2];  // the next pair's K and V rows
   };
-  auto key_tok = [&](int j) { return kpos + (int64_t)min(2 * j + lev_w, Z - 1) * HW; };
+  auto key_tok = [&](int j) { return kpos + (int64_t)min(NL * j + lev_w, Z - 1) * HW; };
   auto load_io = [&](PairIo& io, int j, int jn, bool more) __attribute__((always_inline)) {
     if (csk) {
 #pragma unroll
@@ -529,14 +534,14 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
   };
   // does query level p see this wave's key level in pair j?
   auto active = [&](int j, int p) {
-    const int kz = 2 * j + lev_w, zs = win_start(p, Z, KZ);
+    const int kz = NL * j + lev_w, zs = win_start(p, Z, KZ);
     return blk_on && kz < Z && kz >= zs && kz < zs + KZ;
   };
   // store the pair's dV, and dK = R^T (scale 2^(E-15) dK~); lane holds d = 16t + 4g + i.
   // With QK RMSNorm that is the gradient of k^ = r k, carried back through the
   // norm: dk = r (dk^ - k^ mean(dk^ k^)), k^ from the raw row in float32.
   auto store_pair = [&](int j, const PairIo& io) __attribute__((always_inline)) {
-    const int kz = 2 * j + lev_w;
+    const int kz = NL * j + lev_w;
     const int64_t ktok = key_tok(j);
     const float f = a.scale * __builtin_amdgcn_ldexpf(1.f, ex - 15);
     f32x4 xk[4];
@@ -583,8 +588,8 @@ __global__ void __launch_bounds__(kThreads, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
   // end of a pair.  Each thread waits for its own copies, finishes its own
   // slots, and one barrier publishes the level; the barrier also retires every
   // read of the tiles the next copy overwrites.
-  auto p_lo = [&](int j) { return inv_lo(2 * j, KZ); };
-  auto p_hi = [&](int j) { return inv_hi(min(2 * j + 1, Z - 1), Z, KZ); };
+  auto p_lo = [&](int j) { return inv_lo(NL * j, KZ); };
+  auto p_hi = [&](int j) { return inv_hi(min(NL * j + NL - 1, Z - 1), Z, KZ); };
   // the (pair, level) after (j, p)
   auto next_of = [&](int j, int p, int& nj, int& np) {
     nj = j;
@@ -645,7 +650,7 @@ bool groups_fit(int L, int k, bool x_axis) {
   return true;
 }
 
-template <int KZ, int KY, int KX>
+template <int KZ, int KY, int KX, int NL>
 bool launch_kvp(const strata_na3d_desc& d, const KvpArgs& a0, bool norm, hipStream_t s) {
   if (!groups_fit(d.H, KY, false) || !groups_fit(d.W, KX, true)) return false;
   KvpArgs a = a0;
@@ -654,9 +659,9 @@ bool launch_kvp(const strata_na3d_desc& d, const KvpArgs& a0, bool norm, hipStre
   const int64_t blocks = (int64_t)d.B * d.heads * a.ngy * a.ngx;
   if (blocks >= (int64_t)1 << 31) return false;
   if (norm)
-    hipLaunchKernelGGL((na3d_mfma_kvp_kernel<KZ, KY, KX, true>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((na3d_mfma_kvp_kernel<KZ, KY, KX, true, NL>), dim3((unsigned)blocks), dim3(256 * NL), 0, s, a);
   else
-    hipLaunchKernelGGL((na3d_mfma_kvp_kernel<KZ, KY, KX, false>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((na3d_mfma_kvp_kernel<KZ, KY, KX, false, NL>), dim3((unsigned)blocks), dim3(256 * NL), 0, s, a);
   return true;
 }
 
@@ -684,8 +689,11 @@ bool launch_na3d_bwd_dkdv_kvp(const strata_na3d_desc& d, const BwdOpts& o, const
   a.scale = d.scale;
   a.kscale = d.scale * kLog2e;
   a.eps = o.eps;
-  if (d.kz == 5 && d.ky == 9 && d.kx == 9) return launch_kvp<5, 9, 9>(d, a, o.qk_norm, s);
-  if (d.kz == 9 && d.ky == 9 && d.kx == 9) return launch_kvp<9, 9, 9>(d, a, o.qk_norm, s);
+  // two key levels per workgroup (two waves per SIMD, 214 registers); three
+  // levels (three waves per SIMD) leave 168 registers and spill 52 of them:
+  // 8.94 against 7.67 ms for the training-tile dK/dV
+  if (d.kz == 5 && d.ky == 9 && d.kx == 9) return launch_kvp<5, 9, 9, 2>(d, a, o.qk_norm, s);
+  if (d.kz == 9 && d.ky == 9 && d.kx == 9) return launch_kvp<9, 9, 9, 2>(d, a, o.qk_norm, s);
   return false;
 }
 
