@@ -139,11 +139,92 @@ __global__ void __launch_bounds__(128) na3d_fwd_ref_kernel(const T* __restrict__
   if (lse) lse[qi] = m + logf(l);
 }
 
+// Small problems: one wave per query, so that a problem of a few thousand
+// queries still spreads over the chip.  Lane l takes the keys l, l + 64, ... of
+// the query's window (in (z, y, x) order) with its own running maximum, sum and
+// accumulator; the 64 partial states are then merged by butterfly exchanges
+// (each rescaled to the common maximum before it is added).  The options as in
+// the kernel above.
+template <typename T, int D>
+__global__ void __launch_bounds__(256) na3d_fwd_wave_kernel(const T* __restrict__ q, const T* __restrict__ k,
+                                                            const T* __restrict__ v, const float2* __restrict__ cs,
+                                                            T* __restrict__ out, float* __restrict__ lse, Dims dm,
+                                                            NaOpts opt) {
+  const int64_t nq = (int64_t)dm.B * dm.heads * dm.Z * dm.H * dm.W;
+  const int64_t qi = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (qi >= nq) return;  // whole waves
+  int b, h, z, y, x;
+  split_tok(qi, dm, b, h, z, y, x);
+  const int64_t bh = (int64_t)b * dm.heads + h;
+  float qv[D], kv[D], acc[D];
+  load_rot<T, D>(q + qi * D, cs ? cs + (((int64_t)b * dm.H + y) * dm.W + x) * (D / 2) : nullptr, 1.f, qv);
+  if (opt.qk_norm) rms_normalise<D>(qv, opt.eps);  // the rotation keeps the mean square
+#pragma unroll
+  for (int e = 0; e < D; ++e) acc[e] = 0.f;
+  float m = -INFINITY, l = 0.f;
+  const int zs = win_start(z, dm.Z, dm.kz), ys = win_start(y, dm.H, dm.ky), xs = win_start(x, dm.W, dm.kx);
+  const int nyx = dm.ky * dm.kx, nk = dm.kz * nyx;
+  for (int t = lane; t < nk; t += 64) {
+    const int jz = zs + t / nyx, jy = ys + (t % nyx) / dm.kx, jx = xs + t % dm.kx;
+    const int64_t kj = ((bh * dm.Z + jz) * dm.H + jy) * dm.W + jx;
+    load_rot<T, D>(k + kj * D, cs ? cs + (((int64_t)b * dm.H + jy) * dm.W + jx) * (D / 2) : nullptr, 1.f, kv);
+    if (opt.qk_norm) rms_normalise<D>(kv, opt.eps);
+    float s = 0.f;
+#pragma unroll
+    for (int e = 0; e < D; ++e) s = fmaf(qv[e], kv[e], s);
+    s *= dm.scale;
+    const float mn = fmaxf(m, s);
+    const float alpha = expf(m - mn);
+    const float p = expf(s - mn);
+    l = fmaf(l, alpha, p);
+    const T* vr = v + kj * D;
+#pragma unroll
+    for (int e = 0; e < D; ++e) acc[e] = fmaf(acc[e], alpha, p * ld(vr + e));
+    m = mn;
+  }
+  // merge the lanes: common maximum, then sums of the rescaled partial states
+  float mx = m;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+  const float f = m == -INFINITY ? 0.f : expf(m - mx);  // a lane without keys adds nothing
+  l *= f;
+#pragma unroll
+  for (int e = 0; e < D; ++e) acc[e] *= f;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    l += __shfl_xor(l, off);
+#pragma unroll
+    for (int e = 0; e < D; ++e) acc[e] += __shfl_xor(acc[e], off);
+  }
+  // lane e < D stores element e (times the gate's sigmoid)
+  float val = 0.f;
+#pragma unroll
+  for (int e = 0; e < D; ++e) val = lane == e ? acc[e] : val;
+  if (lane < D) {
+    float r = val / l;
+    const T* gate = static_cast<const T*>(opt.gate);
+    if (gate) r *= sigmoid(ld(gate + (opt.gate_dim == 1 ? qi : qi * D + lane)));
+    st(out + qi * D + lane, r);
+  }
+  if (lse && lane == 0) lse[qi] = mx + logf(l);
+}
+
 template <typename T, int D>
 static void fwd_ref(const strata_na3d_desc& d, const NaOpts& o, const void* q, const void* k,
                     const void* v, const float* cs, void* out, float* lse, hipStream_t s) {
   Dims dm{d.B, d.heads, d.Z, d.H, d.W, d.kz, d.ky, d.kx, d.scale};
   int64_t nq = (int64_t)d.B * d.heads * d.Z * d.H * d.W;
+  // a problem too small to fill the chip with one query per thread (fewer than
+  // 2^18 queries) takes one wave per query
+  if constexpr (D <= 64) {
+    if (nq < ((int64_t)1 << 18)) {
+      hipLaunchKernelGGL((na3d_fwd_wave_kernel<T, D>), dim3((unsigned)((nq + 3) / 4)), dim3(256), 0, s,
+                         static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
+                         reinterpret_cast<const float2*>(cs), static_cast<T*>(out), lse, dm, o);
+      return;
+    }
+  }
   // one query per thread; a small problem takes one wave per workgroup so that
   // its workgroups spread over more CUs
   int threads = nq < (int64_t)512 * 128 ? 64 : 128;
