@@ -124,6 +124,21 @@ def test_fwd_tiny_f32_full():
 
 
 @pytest.mark.parametrize("shape,window", [
+    ((1, 2, 9, 10, 11, 64), (9, 9, 9)),   # 729 keys: every lane of a query's wave takes 11-12
+    ((2, 1, 3, 5, 6, 32), (1, 3, 5)),     # 15 keys: most lanes of the wave take none
+])
+def test_fwd_f32_one_wave_per_query(shape, window):
+    """Small float32 problems run one wave per query (the lanes split the window's
+    keys and merge their softmax states): full grids against the oracle."""
+    pl = I.random_placement(shape[0], shape[3], shape[4], 95)
+    c32 = oracle_coords(pl, shape[3], shape[4])
+    (q, k, v), out, lse, scale = run_fwd(shape, window, "f32", 47, c32)
+    ro, rl = oracle.na3d_fwd(*(oracle.widen(a, "f32") for a in (q, k, v)), window, scale, coords=c32)
+    check_close(host_f64(out), ro, "f32", "out")
+    assert np.max(np.abs(host_f64(lse) - rl)) <= 1e-5
+
+
+@pytest.mark.parametrize("shape,window", [
     ((2, 3, 5, 19, 21, 64), (3, 7, 7)),     # ragged against 8x8 query blocks
     ((1, 2, 6, 24, 24, 64), (5, 9, 9)),
     ((2, 2, 3, 16, 12, 32), (3, 5, 7)),
@@ -368,6 +383,12 @@ def run_bwd(shape, window, dtype, seed, coords32=None, g_exp=None):
     # and a long column in which every wave takes three key levels in turn
     ((1, 2, 5, 12, 12, 64), (5, 9, 9), "bf16"),
     ((1, 1, 13, 13, 9, 64), (5, 9, 9), "bf16"),
+    # the balanced dK/dV kernel (two key levels x four 4x4 blocks) and the
+    # 12-wave dQ (three query levels): ragged planes whose block counts are odd
+    # (a group with one block, square runs of 2, 3 and 4), an odd Z (a run with
+    # one key level, a last group of one query level)
+    ((1, 1, 7, 18, 23, 64), (5, 9, 9), "bf16"),
+    ((1, 1, 11, 13, 17, 64), (9, 9, 9), "bf16"),
 ])
 @pytest.mark.parametrize("rope", [True, False])
 def test_bwd_full_oracle(shape, window, dtype, rope):
