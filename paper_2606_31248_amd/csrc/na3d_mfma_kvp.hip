@@ -40,6 +40,11 @@
 //               padded when the count is odd) and for widths 2 and 4 (two
 //               squares of one row per step); every LDS read is a lane base
 //               plus an immediate.
+//   sweep     : one workgroup takes every run of key levels of its block group
+//               in turn; the copies of the next (run, query level) go out while
+//               the current one is computed, across the end of a run too, and
+//               at a change of run the finished dK/dV are stored and the next
+//               run's keys loaded in one batch.
 #include "common.h"
 #include "kernels.h"
 #include "mfma_util.h"

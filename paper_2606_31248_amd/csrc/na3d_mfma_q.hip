@@ -2,12 +2,17 @@
 // head_dim 64): the forward, and the dQ part of the backward.
 //
 // Work decomposition
-//   workgroup : one (tile, head), an 8 x 8 block of (y, x) query positions and
-//               ZQ query levels; 8 waves, one workgroup per CU.
-//   wave      : a 4 x 4 (y, x) sub-block = 16 queries, on ZQ/2 of the levels
-//               (waves 0-3 take the even levels of the block, waves 4-7 the odd
-//               ones, so both halves have work at every key level).
-//   key sweep : the workgroup walks the key levels its queries need, each once.
+//   workgroup : one (tile, head), an 8 x 8 block of (y, x) query positions, NG
+//               groups of four waves, one workgroup per CU; it takes the groups
+//               of ZQ query levels of its block's column one after another.
+//   wave      : a 4 x 4 (y, x) sub-block = 16 queries, on ZQ/NG of a group's
+//               levels (wave group g takes the levels g, g + NG, ..., so every
+//               group has work at every key level).  NG = 2 (8 waves) for the
+//               forward and the 3x7x7 dQ; NG = 3 (12 waves, three per SIMD, one
+//               query level each) for the dQ of the 9-wide windows.
+//   key sweep : for each group of query levels the workgroup walks the key
+//               levels they need, each once (the copies of the next group's
+//               first level run during the current group's last).
 //               K and V of the (8+ky-1) x (8+kx-1) key box of a level are copied
 //               global -> LDS by the direct-to-LDS load (no registers), one level
 //               ahead of the compute, into a double buffer; each thread then
@@ -53,18 +58,22 @@
 // compiler can tell the reads of one from the copies into the other and does not
 // wait for the copies before reading.
 //
-// Backward, dQ (same decomposition and key staging; a lane still owns a query):
-//   S^T = K . Q^T as above, seeded with the mask; P^T = exp2(S^T - LSE) from the
-//   forward's log-sum-exp (no online softmax);
+// Backward, dQ (same decomposition and key staging; a lane still owns a query),
+// 32 keys (two chunks) per step:
+//   S^T = K . Q^T as above, seeded with -(lse2 + E - 15) where the query sees
+//   the key (window bits, two words per lane) and -inf elsewhere, so that
+//   exp2(S^T) is the weight P^T (from the forward's log-sum-exp, no online
+//   softmax) times the current dS scale 2^(15 - E);
 //   Y^T (16 keys x 16 queries) = V . dO^T - D   bf16 MFMA, V rows read as the A
 //                                           operand, dO of the lane's query held
 //                                           in registers, seeded with -D;
 //   dS^T = P^T * Y^T, and dQ~^T (64 d x 16 queries) += K~^T . dS^T as a float16
 //   MFMA whose K~^T fragments come from the rotated K tile by the transpose read.
 //   dS is carried in float16 with a per-query power-of-two scale 2^(15 - E): E
-//   bounds |Y| of every key level seen so far (|dS| <= P |Y|, P <= 1), so the
-//   scaled values stay below 2^15, and the accumulator is rescaled exactly when E
-//   grows.  At the end dQ = R^T (scale 2^(E-15) dQ~).
+//   bounds |Y| of every step seen so far (|dS| <= P |Y|, P <= 1), so the
+//   scaled values stay below 2^15; when a step raises E the accumulator is
+//   rescaled exactly and the step's logits move by the change.  At the end
+//   dQ = R^T (scale 2^(E-15) dQ~).
 #include "common.h"
 #include "kernels.h"
 #include "mfma_util.h"
