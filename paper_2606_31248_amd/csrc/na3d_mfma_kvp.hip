@@ -15,11 +15,15 @@
 //               block on the two levels, so every SIMD gets the same work.
 //               (The run length is a template parameter; three levels, three
 //               waves per SIMD, leave too few registers.)
-//   blocks    : along each axis the 4-wide blocks are grouped in pairs (0, n-1),
-//               (1, 2), (3, 4), ...  A block's queries (the union of the inverse
+//   blocks    : along each axis the 4-wide blocks are grouped in pairs: the two
+//               edge blocks (0, n-1), then (1, 2), (3, 4), ... from the low
+//               border and ..., (n-5, n-4), (n-3, n-2) from the high one, with
+//               one interior block alone when their count is odd
+//               (kvp_groups.h).  A block's queries (the union of the inverse
 //               windows of its keys) span a run of "squares", 4-aligned runs of
 //               4 positions; for 9-wide windows the runs of a pair cover at most
-//               four squares per axis (the host checks every group).
+//               four squares per axis unless a single block already spans five
+//               (axes of 17 to 20 positions; the host checks every group).
 //   staging   : per query level the workgroup copies the 4 x 4 squares of its
 //               group (16 rows each, 256 rows: Q rotated to float16 in place and
 //               dO, -LSE and -D per row) with the direct-to-LDS load, double
@@ -47,6 +51,7 @@
 //               run's keys loaded in one batch.
 #include "common.h"
 #include "kernels.h"
+#include "kvp_groups.h"
 #include "mfma_util.h"
 
 #include <algorithm>
@@ -55,6 +60,7 @@ namespace strata {
 namespace {
 
 using namespace mfma;
+using namespace kvp;
 
 constexpr int kD = 64;                   // head_dim
 constexpr int kRow = 128;                // LDS bytes per staged query row
@@ -84,62 +90,6 @@ struct KvpArgs {
   float eps;             // QK RMSNorm epsilon
 };
 
-// queries whose (border-clamped) window holds position j of an axis of extent L
-__host__ __device__ __forceinline__ int inv_lo(int j, int k) { return j < k ? 0 : j - (k >> 1); }
-__host__ __device__ __forceinline__ int inv_hi(int j, int L, int k) { return j >= L - k ? L - 1 : j + (k >> 1); }
-
-// One axis of a workgroup: its blocks and the squares their query boxes span.
-// Entry e of the square list is square base + e for e < n0, else base1 + e - n0.
-struct AxisGroup {
-  int nblk;            // blocks in the group (1 or 2)
-  int blk0, blk1;      // block indices (blk1 valid when nblk == 2)
-  int base, n0, base1, n;
-  int run0, len0, run1, len1;  // each block's run of entries
-};
-
-__host__ __device__ __forceinline__ AxisGroup axis_group(int i, int L, int k) {
-  const int nb = (L + 3) >> 2;
-  AxisGroup r;
-  if (i == 0) {
-    r.blk0 = 0;
-    r.blk1 = nb - 1;
-    r.nblk = nb > 1 ? 2 : 1;
-  } else {
-    r.blk0 = 2 * i - 1;
-    r.blk1 = 2 * i;
-    r.nblk = 2 * i <= nb - 2 ? 2 : 1;
-  }
-  const int a0 = inv_lo(4 * r.blk0, k) >> 2;
-  const int a1 = inv_hi(min(4 * r.blk0 + 3, L - 1), L, k) >> 2;
-  r.base = a0;
-  r.run0 = 0;
-  r.len0 = a1 - a0 + 1;
-  r.run1 = 0;
-  r.len1 = 0;
-  r.n0 = r.n = r.len0;
-  r.base1 = a0;
-  if (r.nblk == 2) {
-    const int c0 = inv_lo(4 * r.blk1, k) >> 2;
-    const int c1 = inv_hi(min(4 * r.blk1 + 3, L - 1), L, k) >> 2;
-    r.len1 = c1 - c0 + 1;
-    if (c0 <= a1 + 1) {  // the runs overlap or touch: one run of squares
-      r.n0 = r.n = max(a1, c1) - a0 + 1;
-      r.run1 = c0 - a0;
-    } else {
-      r.n0 = r.len0;
-      r.n = r.len0 + r.len1;
-      r.base1 = c0;
-      r.run1 = r.len0;
-    }
-  }
-  return r;
-}
-
-__host__ __device__ __forceinline__ int sq_abs(const AxisGroup& r, int e) {
-  return e < r.n0 ? r.base + e : r.base1 + e - r.n0;
-}
-
-__host__ __device__ __forceinline__ int n_groups(int L) { return 1 + (((L + 3) >> 2) - 1) / 2; }
 
 template <int I>
 struct IC {
@@ -642,17 +592,6 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
     cj = nj;
     cp = np;
   }
-}
-
-// every group of every axis fits the staged grid (at most four squares), and
-// each block's run along x is 2, 3 or 4 squares wide (the unrolled walks)
-bool groups_fit(int L, int k, bool x_axis) {
-  for (int i = 0; i < n_groups(L); ++i) {
-    const AxisGroup r = axis_group(i, L, k);
-    if (r.n > 4) return false;
-    if (x_axis && (r.len0 < 2 || (r.nblk == 2 && r.len1 < 2))) return false;
-  }
-  return true;
 }
 
 template <int KZ, int KY, int KX, int NL>
