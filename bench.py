@@ -557,6 +557,8 @@ def profile_workload(name: str, steps: int, warmup: int, calib_copy: bool = Fals
     the tiny, 8-tile and training-tile workloads), c4 (the training-tile
     backward), paper16_fwd / paper16_bwd (9x9x9 at 24 levels on 16x16-token
     tiles), paper32_fwd / paper32_bwd, z24_fwd (3x7x7 at 24 levels),
+    column_fwd / column_bwd (window 24x1x1 over all 24 levels), decoder_fwd /
+    decoder_bwd (head_dim 128, 9x9x9),
     rope (the standalone rotation of the training tile's Q), blend (the whole
     stitch of the face tiling), wind (the wind rotation cut from one face into
     the face tiling), duo (the planned Duo padding)."""
@@ -573,8 +575,10 @@ def profile_workload(name: str, steps: int, warmup: int, calib_copy: bool = Fals
         torch.cuda.synchronize()
         del src
     fwd_wl = {"c1": I.TINY_F32, "c2": I.SMALL_BF16, "c3": I.TRAIN_TILE, "paper16_fwd": I.PAPER_TILE16,
-              "paper32_fwd": I.PAPER_TILE32, "z24_fwd": I.Z24_TILE}
-    bwd_wl = {"c4": I.TRAIN_TILE_BWD, "paper16_bwd": I.PAPER_TILE16, "paper32_bwd": I.PAPER_TILE32}
+              "paper32_fwd": I.PAPER_TILE32, "z24_fwd": I.Z24_TILE, "column_fwd": I.PAPER_COLUMN,
+              "decoder_fwd": I.PAPER_DECODER}
+    bwd_wl = {"c4": I.TRAIN_TILE_BWD, "paper16_bwd": I.PAPER_TILE16, "paper32_bwd": I.PAPER_TILE32,
+              "column_bwd": I.PAPER_COLUMN, "decoder_bwd": I.PAPER_DECODER}
     if name in fwd_wl or name in bwd_wl or name == "rope":
         wl = fwd_wl.get(name) or bwd_wl.get(name) or I.TRAIN_TILE
         q, k, v, g = _seeded_device(wl, dev)
