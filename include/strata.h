@@ -131,8 +131,9 @@ strata_status strata_stereorope_apply(const void* x, void* y, const float* cs, i
  * head_dim 64 runs on MFMA for the windows (3,7,7), (5,9,9), (9,9,9) and every
  * column window (kz,1,1) with Z <= 32 (level sweeps for (3,7,7) and (5,9,9), a
  * query-stationary kernel for (9,9,9)); bf16 at head_dim 128 on MFMA for (9,9,9);
- * every other case (f32, head_dim 32, other windows) on a plain per-query
- * kernel in float32.  Softmax and accumulation in float32.
+ * every other case (f32, head_dim 32, other windows) on plain kernels in
+ * float32 (one thread per query, or one wave per query below 2^18 queries).
+ * Softmax and accumulation in float32.
  * Contraction precision: on the MFMA paths the logits q.k are float16 products
  * (wider mantissa than bf16) of float16 copies of the rotated, normalised and
  * scaled q and k, accumulated in float32; P.V is a float16 product (weights and
