@@ -424,6 +424,11 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
         qtr[t][1] = trl(bq[t] + o[1]);
       }
       f32x4 x[2], y[2];
+      // the two waves of a SIMD alternate between MFMA blocks and softmax work:
+      // raised priority while a wave issues its MFMAs keeps the matrix unit
+      // fed (measured: training-tile backward 13.41 -> 13.29 ms; the same in the
+      // dQ pass, three waves per SIMD, gained nothing)
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int c = 2 * st + h;
@@ -443,6 +448,7 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
         y[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(g0[h], vf[0], ys, 0, 0, 0);
         y[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(g1[h], vf[1], y[h], 0, 0, 0);
       }
+      __builtin_amdgcn_s_setprio(0);
       // exponent bound of |Y| for this lane's key (all four row groups)
       float my = 0.f;
 #pragma unroll
@@ -470,6 +476,7 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
       }
       const bf16x8 pf = __builtin_bit_cast(bf16x8, make_uint4(pb[0][0], pb[0][1], pb[1][0], pb[1][1]));
       const f16x8 df = __builtin_bit_cast(f16x8, make_uint4(db[0][0], db[0][1], db[1][0], db[1][1]));
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const bf16x8 gt = __builtin_bit_cast(bf16x8, make_uint4(gtr[t][0].x, gtr[t][0].y, gtr[t][1].x, gtr[t][1].y));
@@ -477,6 +484,7 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
         const f16x8 qt = __builtin_bit_cast(f16x8, make_uint4(qtr[t][0].x, qtr[t][0].y, qtr[t][1].x, qtr[t][1].y));
         accK[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(qt, df, accK[t], 0, 0, 0);
       }
+      __builtin_amdgcn_s_setprio(0);
       __builtin_amdgcn_sched_barrier(0);  // keep the next step's loads out of this one's registers
     });
   };
