@@ -169,7 +169,7 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
   const int64_t bh_base = (int64_t)bh * Z * HW;  // token index of (b, h, 0, 0, 0)
   const float4* csb = a.cs ? a.cs + (int64_t)b * HW * 16 : nullptr;
 
-  // ---- direct-to-LDS copy map: slot s = it*512 + tid of the 4 x 4 grid ---------
+  // ---- direct-to-LDS copy map: slot s = it*kThreads + tid of the 4 x 4 grid ---
   // square sq = s / 128 (entry (sq / 4, sq % 4) of the axis lists), row
   // u = s / 8 (position (u % 16) / 4, u % 4 inside the square), slot column
   // s % 8 holds data column (s % 8) ^ rswz(u); goff = -1 where no query is.
