@@ -189,19 +189,24 @@ static strata_status na3d_bwd_launch(const strata_na3d_desc* desc, const strata_
   bo.qk_norm = o.qk_norm;
   bo.eps = o.eps;
   const void* ga = dout;
+  // D = rowsum(dO * O): from the gate's pass, from the MFMA dq pass (which reads
+  // O beside the dO rows it loads anyway), or from a pass of its own
+  const bool fuse_d = !o.gate && na3d_bwd_dq_mfma_takes(*desc);
   if (o.gate) {
     void* lo = desc->dtype == STRATA_BF16 ? ws + L.da_lo : nullptr;
     launch_na3d_bwd_gate_prep(*desc, o, out, dout, dvec, ws + L.da_hi, lo, dgate, s);
     ga = ws + L.da_hi;
     bo.dout_lo = lo;
-  } else {
+  } else if (!fuse_d) {
     launch_na3d_bwd_ref(0, *desc, bo, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
   }
   if (launch_na3d_bwd_col(*desc, bo, q, k, v, ga, lse, dvec, dq, dk, dv, s))
     return check_launch(opts ? "strata_na3d_bwd_ex" : "strata_na3d_bwd");
-  if (!launch_na3d_bwd_dq_mfma(*desc, bo, q, k, v, cs, ga, lse, dvec, dq, s) &&
-      !launch_na3d_bwd_dq_d128(*desc, bo, q, k, v, cs, ga, lse, dvec, dq, s))
-    launch_na3d_bwd_ref(1, *desc, bo, q, k, v, cs, out, ga, lse, dq, dk, dv, dvec, s);
+  if (!launch_na3d_bwd_dq_mfma(*desc, bo, q, k, v, cs, ga, lse, dvec, fuse_d ? out : nullptr, dq, s)) {
+    if (fuse_d) launch_na3d_bwd_ref(0, *desc, bo, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
+    if (!launch_na3d_bwd_dq_d128(*desc, bo, q, k, v, cs, ga, lse, dvec, dq, s))
+      launch_na3d_bwd_ref(1, *desc, bo, q, k, v, cs, out, ga, lse, dq, dk, dv, dvec, s);
+  }
   if (!launch_na3d_bwd_dkdv_kvp(*desc, bo, q, k, v, cs, ga, lse, dvec, dk, dv, s) &&
       !launch_na3d_bwd_dkdv_mfma(*desc, bo, q, k, v, cs, ga, lse, dvec, dk, dv, s) &&
       !launch_na3d_bwd_dkdv_d128(*desc, bo, q, k, v, cs, ga, lse, dvec, dk, dv, s))

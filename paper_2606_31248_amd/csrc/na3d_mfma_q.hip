@@ -95,6 +95,17 @@ constexpr float kLazy = 8.0f;    // move the softmax reference only when a logit
 constexpr float kLow = -64.0f;   // ... or down, on a level's first key level
 constexpr int kMinExp = -100;    // lower bound of the dS exponent (keeps 2^(15-E) finite)
 
+// <x, y> over the 8 bf16 values of two 16-byte pieces, added to acc (the
+// products are exact in float32)
+__device__ __forceinline__ float dot8(uint4 x, uint4 y, float acc) {
+  const uint32_t u[4] = {x.x, x.y, x.z, x.w}, w[4] = {y.x, y.y, y.z, y.w};
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, u[t]), __builtin_bit_cast(bf16x2, w[t]), acc,
+                                          false);
+  return acc;
+}
+
 // NG groups of four waves, one wave per 4x4 sub-block in each group; group g
 // takes the levels g, g + NG, ... of the block's ZQ levels
 template <int KZ, int KY, int KX, int ZQ, bool BWD, int NG>
@@ -138,6 +149,8 @@ struct Args {
   const uint16_t* dout;  // backward: dO
   const float* lse_in;   // backward: LSE of the forward (natural log)
   const float* dvec;     // backward: D = rowsum(dO * O)
+  const uint16_t* fo;    // backward: the forward's O; when set, D is formed here
+  float* dvec_out;       //   from dO and O and stored for the dK/dV pass
   int heads, Z, H, W;
   int n_zb, n_yb, n_xb;
   int n_zc, zb_per;   // runs of query-level groups per column, groups per run
@@ -379,15 +392,24 @@ __global__ void __launch_bounds__(256 * NG, 1) na3d_mfma_q_kernel(Args a) {
       qf[j][1] = __builtin_bit_cast(f16x8, r1);
       if constexpr (BWD) {
         const uint4* gsrc = reinterpret_cast<const uint4*>(a.dout + tok * kD);
-        gf[j][0] = __builtin_bit_cast(bf16x8, gsrc[g]);
-        gf[j][1] = __builtin_bit_cast(bf16x8, gsrc[4 + g]);
+        const uint4 g0 = gsrc[g], g1 = gsrc[4 + g];
+        gf[j][0] = __builtin_bit_cast(bf16x8, g0);
+        gf[j][1] = __builtin_bit_cast(bf16x8, g1);
         if constexpr (LO) {
           const uint4* lsrc = reinterpret_cast<const uint4*>(a.dout_lo + tok * kD);
           gl[j][0] = __builtin_bit_cast(bf16x8, lsrc[g]);
           gl[j][1] = __builtin_bit_cast(bf16x8, lsrc[4 + g]);
         }
         m[j] = a.lse_in[tok] * kLog2e;  // lse2
-        l[j] = -a.dvec[tok];            // -D
+        float dj;
+        if (a.fo) {  // D = <dO, O> of the row over the 4 lanes that hold it, stored once
+          const uint4* osrc = reinterpret_cast<const uint4*>(a.fo + tok * kD);
+          dj = sum_over_rows(dot8(osrc[4 + g], g1, dot8(osrc[g], g0, 0.f)));
+          if (g == 0 && z0 + grp + NG * j < Z && qy_raw < H && qx_raw < W) a.dvec_out[tok] = dj;
+        } else {
+          dj = a.dvec[tok];
+        }
+        l[j] = -dj;  // -D
         ex[j] = kMinExp;
       } else {
         m[j] = 0.f;
@@ -754,13 +776,22 @@ bool launch_na3d_fwd_mfma(const strata_na3d_desc& d, const NaOpts& o, const void
   return launch<5, 9, 9, 2, false>(d, a, opt, s);
 }
 
-bool launch_na3d_bwd_dq_mfma(const strata_na3d_desc& d, const BwdOpts& o, const void* q,
-                             const void* k, const void* v, const float* cs, const void* dout,
-                             const float* lse, const float* dvec, void* dq, hipStream_t s) {
+bool na3d_bwd_dq_mfma_takes(const strata_na3d_desc& d) {
   if (!supported(d)) return false;
   const bool w377 = d.kz == 3 && d.ky == 7 && d.kx == 7, w599 = d.kz == 5 && d.ky == 9 && d.kx == 9;
   const bool w999 = d.kz == 9 && d.ky == 9 && d.kx == 9;
   if (!w377 && !w599 && !w999) return false;
+  const Args a = make_args(d, w377 ? 4 : 3, nullptr, nullptr, nullptr, nullptr);
+  return (int64_t)d.B * d.heads * a.n_zc * a.n_yb * a.n_xb < (int64_t)1 << 31;
+}
+
+bool launch_na3d_bwd_dq_mfma(const strata_na3d_desc& d, const BwdOpts& o, const void* q,
+                             const void* k, const void* v, const float* cs, const void* dout,
+                             const float* lse, float* dvec, const void* out, void* dq, hipStream_t s) {
+  if (!na3d_bwd_dq_mfma_takes(d)) return false;
+  if (out && o.dout_lo) return false;  // D of a two-term dO comes from the gate's pass
+  const bool w377 = d.kz == 3 && d.ky == 7 && d.kx == 7;
+  const bool w999 = d.kz == 9 && d.ky == 9 && d.kx == 9;
   // 9-wide windows: three groups of four waves, one query level each (12 waves,
   // three per SIMD); 3x7x7: two groups, two levels per wave
   Args a = make_args(d, w377 ? 4 : 3, q, k, v, cs);
@@ -768,6 +799,10 @@ bool launch_na3d_bwd_dq_mfma(const strata_na3d_desc& d, const BwdOpts& o, const 
   a.dout = static_cast<const uint16_t*>(dout);
   a.lse_in = lse;
   a.dvec = dvec;
+  if (out) {  // D formed from dO and O by this pass and stored to dvec
+    a.fo = static_cast<const uint16_t*>(out);
+    a.dvec_out = dvec;
+  }
   a.qk_norm = o.qk_norm;
   a.eps = o.eps;
   a.dout_lo = static_cast<const uint16_t*>(o.dout_lo);
