@@ -385,8 +385,13 @@ def run_bwd(shape, window, dtype, seed, coords32=None, g_exp=None):
     ((1, 1, 13, 13, 9, 64), (5, 9, 9), "bf16"),
     # the balanced dK/dV kernel (two key levels x four 4x4 blocks) and the
     # 12-wave dQ (three query levels): ragged planes whose block counts are odd
-    # (a group with one block, square runs of 2, 3 and 4), an odd Z (a run with
-    # one key level, a last group of one query level)
+    # (a group with one block, square runs of 2, 3 and 4, a 3 x 3 run whose
+    # walk ends in a half step), an odd Z (a run with one key level, a last
+    # group of one query level)
+    ((1, 1, 7, 25, 23, 64), (5, 9, 9), "bf16"),
+    ((1, 1, 11, 25, 13, 64), (9, 9, 9), "bf16"),
+    # axes of 17-20 positions, where a single block's query box spans five
+    # squares: dK/dV on the one-block kernel, dQ on the 12-wave kernel
     ((1, 1, 7, 18, 23, 64), (5, 9, 9), "bf16"),
     ((1, 1, 11, 13, 17, 64), (9, 9, 9), "bf16"),
 ])
