@@ -154,10 +154,16 @@ strata_status strata_na3d_fwd(const strata_na3d_desc* desc, const void* q, const
  *   P_ij = exp(s_ij - lse_i),   D_i = <dout_i, out_i>,
  *   dv_j = sum_{i: j in N(i)} P_ij dout_i,    dS_ij = P_ij (<dout_i, v_j> - D_i),
  *   dq_i = R_i^T scale sum_j dS_ij R_j k_j,    dk_j = R_j^T scale sum_i dS_ij R_i q_i.
- * Deterministic (no atomics).  workspace: device memory of at least
- * strata_na3d_bwd_workspace_size(desc) bytes (holds D), owned by the caller.
+ * Deterministic (the one atomic operation is an integer maximum, whose result
+ * does not depend on order).  workspace: device memory of at least
+ * strata_na3d_bwd_workspace_size(desc) bytes (holds D, one word per (batch,
+ * head) and, with a gate, dA), owned by the caller.
  * Kernels and input range as strata_na3d_fwd; on the MFMA paths the dS products
- * (dq, dk) are float16 with exact power-of-two scaling, P.dO and dO.V^T bf16. */
+ * (dq, dk) are float16 with exact power-of-two scaling; P.dO and dO.V^T are
+ * float16 products with dO scaled by a power of two per (batch, head) in the
+ * dK/dV kernel of the 9-wide windows (V then saturates at 65504 like the
+ * level-sweep forward's), bf16 ones elsewhere, with P carried in two bf16 terms
+ * for P.dO in the other dK/dV MFMA kernel. */
 size_t strata_na3d_bwd_workspace_size(const strata_na3d_desc* desc);
 strata_status strata_na3d_bwd(const strata_na3d_desc* desc, const void* q, const void* k,
                               const void* v, const float* cs, const void* out, const void* dout,
@@ -167,9 +173,10 @@ strata_status strata_na3d_bwd(const strata_na3d_desc* desc, const void* q, const
 /* ---- backward for callers that cannot allocate --------------------------------
  * For code under HIP graph capture, tight training loops and harnesses that
  * forbid hipMalloc: strata_na3d_bwd without a workspace.  Same arguments,
- * results and kernels as strata_na3d_bwd (plain attention, no options); D lives
- * in a static 32 MiB device array of the library, one per device, held until
- * the process ends.  Limit: B*heads*Z*H*W <= 2^23 token-heads, otherwise
+ * results and kernels as strata_na3d_bwd (plain attention, no options); D and
+ * one word per (batch, head) live in a static device array of the library
+ * (32 MiB + 256 KiB), one per device, held until the process ends.  Limits:
+ * B*heads*Z*H*W <= 2^23 token-heads and B*heads <= 2^16, otherwise
  * STRATA_ERR_INVALID_ARG and nothing is launched.  Nothing is allocated; the
  * array's device address is looked up once per device on the first call.
  * Every call on a device shares that device's array: calls that overlap on one

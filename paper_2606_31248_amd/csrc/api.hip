@@ -86,11 +86,11 @@ static strata_status check_opts(const strata_na3d_desc* d, const strata_na3d_opt
   return STRATA_OK;
 }
 
-// Backward workspace: D, then (with a gate) dA = sigmoid(g) dO as its rounded
-// value hi and, for bf16, the remainder lo; every region starts on a 256-byte
-// boundary.
+// Backward workspace: D, the per-(batch, head) exponent of the largest |dO|,
+// then (with a gate) dA = sigmoid(g) dO as its rounded value hi and, for bf16,
+// the remainder lo; every region starts on a 256-byte boundary.
 struct BwdLayout {
-  size_t dvec, da_hi, da_lo, total;
+  size_t dvec, emax, da_hi, da_lo, total;
 };
 
 static BwdLayout bwd_layout(const strata_na3d_desc& d, const NaOpts& o) {
@@ -99,6 +99,8 @@ static BwdLayout bwd_layout(const strata_na3d_desc& d, const NaOpts& o) {
   const size_t rowb = n * d.head_dim * (d.dtype == STRATA_BF16 ? 2 : 4);
   BwdLayout L = {};
   size_t off = al(n * sizeof(float));
+  L.emax = off;
+  off += al((size_t)d.B * d.heads * sizeof(int));
   L.da_hi = off;
   if (o.gate) off += al(rowb);
   L.da_lo = off;
@@ -202,12 +204,16 @@ static strata_status na3d_bwd_launch(const strata_na3d_desc* desc, const strata_
   }
   if (launch_na3d_bwd_col(*desc, bo, q, k, v, ga, lse, dvec, dq, dk, dv, s))
     return check_launch(opts ? "strata_na3d_bwd_ex" : "strata_na3d_bwd");
-  if (!launch_na3d_bwd_dq_mfma(*desc, bo, q, k, v, cs, ga, lse, dvec, fuse_d ? out : nullptr, dq, s)) {
+  // the MFMA dq pass also records the largest |dO| exponent per (batch, head),
+  // which the balanced dk/dv pass scales its float16 copy of dO by
+  int* emax = reinterpret_cast<int*>(ws + L.emax);
+  if (!launch_na3d_bwd_dq_mfma(*desc, bo, q, k, v, cs, ga, lse, dvec, fuse_d ? out : nullptr, emax, dq, s)) {
+    emax = nullptr;
     if (fuse_d) launch_na3d_bwd_ref(0, *desc, bo, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);
     if (!launch_na3d_bwd_dq_d128(*desc, bo, q, k, v, cs, ga, lse, dvec, dq, s))
       launch_na3d_bwd_ref(1, *desc, bo, q, k, v, cs, out, ga, lse, dq, dk, dv, dvec, s);
   }
-  if (!launch_na3d_bwd_dkdv_kvp(*desc, bo, q, k, v, cs, ga, lse, dvec, dk, dv, s) &&
+  if (!launch_na3d_bwd_dkdv_kvp(*desc, bo, q, k, v, cs, ga, lse, dvec, emax, dk, dv, s) &&
       !launch_na3d_bwd_dkdv_mfma(*desc, bo, q, k, v, cs, ga, lse, dvec, dk, dv, s) &&
       !launch_na3d_bwd_dkdv_d128(*desc, bo, q, k, v, cs, ga, lse, dvec, dk, dv, s))
     launch_na3d_bwd_ref(2, *desc, bo, q, k, v, cs, out, ga, lse, dq, dk, dv, dvec, s);
@@ -215,12 +221,14 @@ static strata_status na3d_bwd_launch(const strata_na3d_desc* desc, const strata_
 }
 
 // ---- backward without a caller workspace ---------------------------------------
-// D = rowsum(dO * O) of a plain backward lives in this file-scope device array
-// instead of a workspace: every device the library runs on holds its own copy
-// for the life of the process.  In host code `scratch` only names the symbol;
+// D = rowsum(dO * O) of a plain backward and the per-(batch, head) exponent of
+// the largest |dO| live in this file-scope device array instead of a
+// workspace: every device the library runs on holds its own copy for the life
+// of the process.  In host code `scratch` only names the symbol;
 // its device address is looked up once per device (hipGetSymbolAddress, with
 // the device current) and that address is what the kernels receive.
-constexpr int64_t kScratchFloats = (int64_t)1 << 23;  // 32 MiB: D of up to 2^23 token-heads
+constexpr int64_t kMaxTokenHeads = (int64_t)1 << 23, kMaxBatchHeads = (int64_t)1 << 16;
+constexpr int64_t kScratchFloats = kMaxTokenHeads + kMaxBatchHeads;  // 32 MiB + 256 KiB
 static __device__ __align__(256) float scratch[kScratchFloats];
 
 constexpr int kMaxDevices = 64;
@@ -254,10 +262,13 @@ static strata_status na3d_bwd_noalloc_impl(const strata_na3d_desc* desc, const v
   REQUIRE_PTR(dk);
   REQUIRE_PTR(dv);
   if (cs) REQUIRE(aligned16(cs), "cs: not 16-byte aligned");
-  const int64_t n = (int64_t)desc->B * desc->heads * desc->Z * desc->H * desc->W;
-  REQUIRE(n <= kScratchFloats,
-          "bwd_noalloc: %lld token-heads exceed the static scratch of %lld (use strata_na3d_bwd with a workspace)",
-          (long long)n, (long long)kScratchFloats);
+  const int64_t bh = (int64_t)desc->B * desc->heads, n = bh * desc->Z * desc->H * desc->W;
+  REQUIRE(n <= kMaxTokenHeads && bh <= kMaxBatchHeads,
+          "bwd_noalloc: %lld token-heads (%lld batch-heads) exceed the static scratch of %lld (%lld) (use "
+          "strata_na3d_bwd with a workspace)",
+          (long long)n, (long long)bh, (long long)kMaxTokenHeads, (long long)kMaxBatchHeads);
+  const NaOpts o;
+  REQUIRE(bwd_layout(*desc, o).total <= (size_t)kScratchFloats * sizeof(float), "bwd_noalloc: static scratch layout");
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return set_error(STRATA_ERR_HIP, "bwd_noalloc: hipGetDevice: %s", hipGetErrorString(e));
@@ -266,7 +277,6 @@ static strata_status na3d_bwd_noalloc_impl(const strata_na3d_desc* desc, const v
                      kMaxDevices);
   float* ws = device_scratch(dev, &e);
   if (!ws) return set_error(STRATA_ERR_HIP, "bwd_noalloc: hipGetSymbolAddress: %s", hipGetErrorString(e));
-  const NaOpts o;
   return na3d_bwd_launch(desc, nullptr, o, q, k, v, cs, out, dout, lse, dq, dk, dv, nullptr,
                          reinterpret_cast<char*>(ws), (hipStream_t)stream);
 }

@@ -99,11 +99,16 @@ void launch_na3d_bwd_gate_prep(const strata_na3d_desc& d, const NaOpts& o, const
 // dq: query-stationary (the forward's decomposition); dk/dv: key-stationary.
 // With `out` (the forward's O) set, the dq pass also forms D = rowsum(dO * O)
 // itself and stores it to dvec for the dk/dv pass (not with a two-term dO);
-// na3d_bwd_dq_mfma_takes is its test of whether it takes the problem.
+// with `emax` set ([B * heads] int32) it stores there, per (batch, head), the
+// largest frexp exponent of |dO| (kEmaxEmpty where every dO is zero), which the
+// balanced dk/dv pass scales dO by.  na3d_bwd_dq_mfma_takes is its test of
+// whether it takes the problem.
+constexpr int kEmaxEmpty = -1000;
 bool na3d_bwd_dq_mfma_takes(const strata_na3d_desc& d);
 bool launch_na3d_bwd_dq_mfma(const strata_na3d_desc& d, const BwdOpts& o, const void* q,
                              const void* k, const void* v, const float* cs, const void* dout,
-                             const float* lse, float* dvec, const void* out, void* dq, hipStream_t s);
+                             const float* lse, float* dvec, const void* out, int* emax, void* dq,
+                             hipStream_t s);
 // bf16 column-wise backward (dq, dk, dv together), windows (kz, 1, 1) with Z <= 32,
 // head_dim 64; false for any other problem.
 bool launch_na3d_bwd_col(const strata_na3d_desc& d, const BwdOpts& o, const void* q, const void* k,
@@ -113,7 +118,7 @@ bool launch_na3d_bwd_col(const strata_na3d_desc& d, const BwdOpts& o, const void
 // windows 5x9x9 and 9x9x9, no two-term dO); false if not applicable
 bool launch_na3d_bwd_dkdv_kvp(const strata_na3d_desc& d, const BwdOpts& o, const void* q, const void* k,
                               const void* v, const float* cs, const void* dout, const float* lse,
-                              const float* dvec, void* dk, void* dv, hipStream_t s);
+                              const float* dvec, const int* emax, void* dk, void* dv, hipStream_t s);
 bool launch_na3d_bwd_dkdv_mfma(const strata_na3d_desc& d, const BwdOpts& o, const void* q,
                                const void* k, const void* v, const float* cs, const void* dout,
                                const float* lse, const float* dvec, void* dk, void* dv,

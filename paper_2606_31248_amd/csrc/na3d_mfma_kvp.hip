@@ -82,6 +82,7 @@ struct KvpArgs {
   const uint16_t* dout;
   const float* lse;      // natural log
   const float* dvec;     // D = rowsum(dO * O)
+  const int* emax;       // [B * heads] largest frexp exponent of |dO| (the dQ pass)
   uint16_t* dk;
   uint16_t* dv;
   int heads, Z, H, W;
@@ -108,6 +109,15 @@ __device__ __forceinline__ void static_for(F&& f) {
 // every constant (square, column) into the read's immediate offset, while the
 // pointer still derives from the tile (so reads of one buffer are not made to
 // wait for the copies into the other).
+// bf16 x 8 -> float16 x 8 times a power of two `mul` that keeps them below 2^15
+__device__ __forceinline__ uint4 f16_scaled8(uint4 x, float mul) {
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  uint32_t r[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) r[t] = pack2h_rne(lo_bf16(w[t]) * mul, hi_bf16(w[t]) * mul);
+  return make_uint4(r[0], r[1], r[2], r[3]);
+}
+
 __device__ __forceinline__ const char* lds_base(const char* p, uint32_t off) {
   asm volatile("" : "+v"(off));
   return p + off;
@@ -168,6 +178,12 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
   const int64_t HW = (int64_t)H * W;
   const int64_t bh_base = (int64_t)bh * Z * HW;  // token index of (b, h, 0, 0, 0)
   const float4* csb = a.cs ? a.cs + (int64_t)b * HW * 16 : nullptr;
+  // dO is staged in float16 times 2^-sh, sh from the largest |dO| of this
+  // (batch, head) (below 2^eb), so the staged values stay below 2^14; D is
+  // scaled alike and dK, dV are scaled back when stored
+  const int eb = a.emax[bh];
+  const int sh = eb == kEmaxEmpty ? 0 : min(max(eb - 14, -120), 120);
+  const float dsc = __builtin_amdgcn_ldexpf(1.f, -sh), dun = __builtin_amdgcn_ldexpf(1.f, sh);
 
   // ---- direct-to-LDS copy map: slot s = it*kThreads + tid of the 4 x 4 grid ---
   // square sq = s / 128 (entry (sq / 4, sq % 4) of the axis lists), row
@@ -239,9 +255,9 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
   };
   // wait for this thread's copies and loads, rotate its own Q slots in place
   // (bf16 -> float16; with QK RMSNorm the 8 slots of a row, 8 consecutive lanes
-  // all valid or all not, add their sums of squares for the row's factor), store
-  // its LSE / D entry
-  auto finish = [&](char* tq, float* sl, float* sd) __attribute__((always_inline)) {
+  // all valid or all not, add their sums of squares for the row's factor),
+  // convert its own dO slots to scaled float16 in place, store its LSE / D entry
+  auto finish = [&](char* tq, char* tg, float* sl, float* sd) __attribute__((always_inline)) {
     __builtin_amdgcn_s_waitcnt(0);
 #pragma unroll
     for (int it = 0; it < kIT; ++it) {
@@ -250,10 +266,12 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
       const uint4 x = ld16(ad);
       const float mul = NORM ? __builtin_amdgcn_rsqf(sum_over_8_lanes(sumsq8(x, 0.f)) * (1.f / kD) + a.eps) : 1.f;
       st16(ad, csb ? rotate8h_pk(x, ph[it], mul) : scale8h(x, mul));
+      char* ag = tg + (it * kThreads + tid) * 16;
+      st16(ag, f16_scaled8(ld16(ag), dsc));
     }
     if (soff >= 0) {
       sl[tid] = -(pl * kLog2e);  // the seed of X: -LSE in log2 units
-      sd[tid] = -pd;
+      sd[tid] = -pd * dsc;
     }
   };
 
@@ -298,7 +316,7 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
   const float4* csk = csb ? csb + ((int64_t)ky * W + kx) * 16 : nullptr;
   const int64_t kpos = bh_base + (int64_t)ky * W + kx;  // token of the key on level 0
   f16x8 kf[2];
-  bf16x8 vf[2];
+  f16x8 vf[2];  // V in float16 (round toward zero: saturates at 65504)
   float rk = 1.f;  // QK RMSNorm factor of this lane's key
   f32x4 accK[4], accV[4];
   int ex = kMinExp;
@@ -348,8 +366,8 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
     }
     kf[0] = __builtin_bit_cast(f16x8, r0);
     kf[1] = __builtin_bit_cast(f16x8, r1);
-    vf[0] = __builtin_bit_cast(bf16x8, io.xv[0]);
-    vf[1] = __builtin_bit_cast(bf16x8, io.xv[1]);
+    vf[0] = __builtin_bit_cast(f16x8, bf16x8_to_f16x8(io.xv[0]));
+    vf[1] = __builtin_bit_cast(f16x8, bf16x8_to_f16x8(io.xv[1]));
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       accK[t] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -402,14 +420,14 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
       constexpr uint32_t o[2] = {Wk::rel(c0) * kSq, Wk::rel(c1) * kSq};
       constexpr uint32_t ol[2] = {Wk::rel(c0) * 64u, Wk::rel(c1) * 64u};
       f16x8 q0[2], q1[2];
-      bf16x8 g0[2], g1[2];
+      f16x8 g0[2], g1[2];
       float4 l4[2], d4[2];
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         q0[h] = __builtin_bit_cast(f16x8, ldl16(aq0 + o[h]));
         q1[h] = __builtin_bit_cast(f16x8, ldl16(aq1 + o[h]));
-        g0[h] = __builtin_bit_cast(bf16x8, ldl16(ag0 + o[h]));
-        g1[h] = __builtin_bit_cast(bf16x8, ldl16(ag1 + o[h]));
+        g0[h] = __builtin_bit_cast(f16x8, ldl16(ag0 + o[h]));
+        g1[h] = __builtin_bit_cast(f16x8, ldl16(ag1 + o[h]));
         l4[h] = ldlf4(sl4 + ol[h]);
         d4[h] = ldlf4(sd4 + ol[h]);
       }
@@ -445,8 +463,8 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
         const f32x4 ys = {d4[h].x, d4[h].y, d4[h].z, d4[h].w};
         x[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(q0[h], kf[0], xs, 0, 0, 0);
         x[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(q1[h], kf[1], x[h], 0, 0, 0);
-        y[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(g0[h], vf[0], ys, 0, 0, 0);
-        y[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(g1[h], vf[1], y[h], 0, 0, 0);
+        y[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(g0[h], vf[0], ys, 0, 0, 0);
+        y[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(g1[h], vf[1], y[h], 0, 0, 0);
       }
       __builtin_amdgcn_s_setprio(0);
       // exponent bound of |Y| for this lane's key (all four row groups)
@@ -464,35 +482,28 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
         ex = en;
       }
       const float sc = __builtin_amdgcn_ldexpf(1.f, 15 - ex);
-      // P for dV in two bf16 terms, P = hi + lo: bf16's rounding of P alone
-      // would put the largest dV of a peaked softmax several percent of RMS(dV)
-      // off; the second term leaves ~2^-17 P
-      uint32_t pb[2][2], pr[2][2], db[2][2];
+      // P for dV in float16 (bf16's rounding of P alone would put the largest
+      // dV of a peaked softmax several percent of RMS(dV) off)
+      uint32_t pb[2][2], db[2][2];
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const float p0 = __builtin_amdgcn_exp2f(x[h][0]), p1 = __builtin_amdgcn_exp2f(x[h][1]);
         const float p2 = __builtin_amdgcn_exp2f(x[h][2]), p3 = __builtin_amdgcn_exp2f(x[h][3]);
-        pb[h][0] = pack2(p0, p1);
-        pb[h][1] = pack2(p2, p3);
-        pr[h][0] = pack2(p0 - lo_bf16(pb[h][0]), p1 - hi_bf16(pb[h][0]));
-        pr[h][1] = pack2(p2 - lo_bf16(pb[h][1]), p3 - hi_bf16(pb[h][1]));
+        pb[h][0] = pack2h_rne(p0, p1);
+        pb[h][1] = pack2h_rne(p2, p3);
         db[h][0] = pack2h_rne(p0 * sc * y[h][0], p1 * sc * y[h][1]);
         db[h][1] = pack2h_rne(p2 * sc * y[h][2], p3 * sc * y[h][3]);
       }
-      const bf16x8 pf = __builtin_bit_cast(bf16x8, make_uint4(pb[0][0], pb[0][1], pb[1][0], pb[1][1]));
-      const bf16x8 prf = __builtin_bit_cast(bf16x8, make_uint4(pr[0][0], pr[0][1], pr[1][0], pr[1][1]));
+      const f16x8 pf = __builtin_bit_cast(f16x8, make_uint4(pb[0][0], pb[0][1], pb[1][0], pb[1][1]));
       const f16x8 df = __builtin_bit_cast(f16x8, make_uint4(db[0][0], db[0][1], db[1][0], db[1][1]));
-      bf16x8 gt[4];
       __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        gt[t] = __builtin_bit_cast(bf16x8, make_uint4(gtr[t][0].x, gtr[t][0].y, gtr[t][1].x, gtr[t][1].y));
-        accV[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gt[t], pf, accV[t], 0, 0, 0);
+        const f16x8 gt = __builtin_bit_cast(f16x8, make_uint4(gtr[t][0].x, gtr[t][0].y, gtr[t][1].x, gtr[t][1].y));
+        accV[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(gt, pf, accV[t], 0, 0, 0);
         const f16x8 qt = __builtin_bit_cast(f16x8, make_uint4(qtr[t][0].x, qtr[t][0].y, qtr[t][1].x, qtr[t][1].y));
         accK[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(qt, df, accK[t], 0, 0, 0);
       }
-#pragma unroll
-      for (int t = 0; t < 4; ++t) accV[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gt[t], prf, accV[t], 0, 0, 0);
       __builtin_amdgcn_s_setprio(0);
       __builtin_amdgcn_sched_barrier(0);  // keep the next step's loads out of this one's registers
     });
@@ -515,7 +526,7 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
   auto store_pair = [&](int j, const PairIo& io) __attribute__((always_inline)) {
     const int kz = NL * j + lev_w;
     const int64_t ktok = key_tok(j);
-    const float f = a.scale * __builtin_amdgcn_ldexpf(1.f, ex - 15);
+    const float f = a.scale * __builtin_amdgcn_ldexpf(1.f, ex - 15 + sh);
     f32x4 xk[4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
@@ -548,7 +559,8 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
     uint2* dvd = reinterpret_cast<uint2*>(a.dv + ktok * kD);
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      dvd[4 * t + g] = make_uint2(pack2(accV[t][0], accV[t][1]), pack2(accV[t][2], accV[t][3]));
+      const f32x4 xv = accV[t] * dun;
+      dvd[4 * t + g] = make_uint2(pack2(xv[0], xv[1]), pack2(xv[2], xv[3]));
       dkd[4 * t + g] = make_uint2(pack2(xk[t][0], xk[t][1]), pack2(xk[t][2], xk[t][3]));
     }
   };
@@ -584,7 +596,7 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
     begin_pair(io);
   }
   issue(cp, tQ0, tG0);
-  finish(tQ0, sL0, sD0);
+  finish(tQ0, tG0, sL0, sD0);
   __syncthreads();
   for (;;) {
     int nj, np;
@@ -594,7 +606,7 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
     if (active(cj, cp)) compute_level(tQ0, tG0, sL0, sD0);
     if (nj != cj) change_pair(cj, nj, more);
     if (!more) break;
-    finish(tQ1, sL1, sD1);
+    finish(tQ1, tG1, sL1, sD1);
     __syncthreads();
     cj = nj;
     cp = np;
@@ -604,7 +616,7 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
     if (active(cj, cp)) compute_level(tQ1, tG1, sL1, sD1);
     if (nj != cj) change_pair(cj, nj, more);
     if (!more) break;
-    finish(tQ0, sL0, sD0);
+    finish(tQ0, tG0, sL0, sD0);
     __syncthreads();
     cj = nj;
     cp = np;
@@ -630,8 +642,8 @@ bool launch_kvp(const strata_na3d_desc& d, const KvpArgs& a0, bool norm, hipStre
 
 bool launch_na3d_bwd_dkdv_kvp(const strata_na3d_desc& d, const BwdOpts& o, const void* q, const void* k,
                               const void* v, const float* cs, const void* dout, const float* lse,
-                              const float* dvec, void* dk, void* dv, hipStream_t s) {
-  if (d.dtype != STRATA_BF16 || d.head_dim != kD || o.dout_lo != nullptr) return false;
+                              const float* dvec, const int* emax, void* dk, void* dv, hipStream_t s) {
+  if (d.dtype != STRATA_BF16 || d.head_dim != kD || o.dout_lo != nullptr || !emax) return false;
   if ((int64_t)d.H * d.W * kD >= (int64_t)1 << 31) return false;
   KvpArgs a = {};
   a.q = static_cast<const uint16_t*>(q);
@@ -641,6 +653,7 @@ bool launch_na3d_bwd_dkdv_kvp(const strata_na3d_desc& d, const BwdOpts& o, const
   a.dout = static_cast<const uint16_t*>(dout);
   a.lse = lse;
   a.dvec = dvec;
+  a.emax = emax;
   a.dk = static_cast<uint16_t*>(dk);
   a.dv = static_cast<uint16_t*>(dv);
   a.heads = d.heads;

@@ -95,6 +95,14 @@ constexpr float kLazy = 8.0f;    // move the softmax reference only when a logit
 constexpr float kLow = -64.0f;   // ... or down, on a level's first key level
 constexpr int kMinExp = -100;    // lower bound of the dS exponent (keeps 2^(15-E) finite)
 
+// largest |x| over the 8 bf16 values of a 16-byte piece, or m if larger
+__device__ __forceinline__ float absmax8(uint4 x, float m) {
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+  for (int t = 0; t < 4; ++t) m = fmaxf(m, fmaxf(fabsf(lo_bf16(w[t])), fabsf(hi_bf16(w[t]))));
+  return m;
+}
+
 // <x, y> over the 8 bf16 values of two 16-byte pieces, added to acc (the
 // products are exact in float32)
 __device__ __forceinline__ float dot8(uint4 x, uint4 y, float acc) {
@@ -151,6 +159,8 @@ struct Args {
   const float* dvec;     // backward: D = rowsum(dO * O)
   const uint16_t* fo;    // backward: the forward's O; when set, D is formed here
   float* dvec_out;       //   from dO and O and stored for the dK/dV pass
+  int* emax;             // backward: per (batch, head) the largest exponent of
+                         //   |dO| (atomic max; frexp convention), or nullptr
   int heads, Z, H, W;
   int n_zb, n_yb, n_xb;
   int n_zc, zb_per;   // runs of query-level groups per column, groups per run
@@ -365,6 +375,7 @@ __global__ void __launch_bounds__(256 * NG, 1) na3d_mfma_q_kernel(Args a) {
   bool mset[C::QL];  // forward, wave-uniform: the reference m has moved from 0 somewhere in the wave
   int ex[C::QL];
   f32x4 o[C::QL][4];
+  float gmx = 0.f;  // backward: largest |dO| this lane has loaded
   const float4* csq = csb ? csb + ((int64_t)qy * W + qx) * 16 : nullptr;
   // queries of the group starting at level z0 (and, backward, their dO, LSE, D)
   auto begin_group = [&]() __attribute__((always_inline)) {
@@ -395,6 +406,9 @@ __global__ void __launch_bounds__(256 * NG, 1) na3d_mfma_q_kernel(Args a) {
         const uint4 g0 = gsrc[g], g1 = gsrc[4 + g];
         gf[j][0] = __builtin_bit_cast(bf16x8, g0);
         gf[j][1] = __builtin_bit_cast(bf16x8, g1);
+        if constexpr (!LO) {  // (the balanced dK/dV pass, which reads it, takes no two-term dO)
+          if (a.emax) gmx = absmax8(g1, absmax8(g0, gmx));
+        }
         if constexpr (LO) {
           const uint4* lsrc = reinterpret_cast<const uint4*>(a.dout_lo + tok * kD);
           gl[j][0] = __builtin_bit_cast(bf16x8, lsrc[g]);
@@ -706,6 +720,20 @@ __global__ void __launch_bounds__(256 * NG, 1) na3d_mfma_q_kernel(Args a) {
     cz = nz;
     cp = np;
   }
+  if constexpr (BWD && !LO) {
+    if (a.emax) {  // the exponent of the wave's largest |dO|, one atomic per wave
+      float wm = max_over_rows(gmx);
+#pragma unroll
+      for (int o2 = 8; o2 > 0; o2 >>= 1) wm = fmaxf(wm, __shfl_xor(wm, o2));
+      if (lane == 0 && wm > 0.f) atomicMax(a.emax + bh, __builtin_amdgcn_frexp_expf(wm));
+    }
+  }
+}
+
+// the empty value of the per-(batch, head) dO exponents before the dQ pass
+__global__ void __launch_bounds__(256) emax_init_kernel(int* e, int n) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < n) e[i] = kEmaxEmpty;
 }
 
 Args make_args(const strata_na3d_desc& d, int zq, const void* q, const void* k, const void* v,
@@ -787,7 +815,8 @@ bool na3d_bwd_dq_mfma_takes(const strata_na3d_desc& d) {
 
 bool launch_na3d_bwd_dq_mfma(const strata_na3d_desc& d, const BwdOpts& o, const void* q,
                              const void* k, const void* v, const float* cs, const void* dout,
-                             const float* lse, float* dvec, const void* out, void* dq, hipStream_t s) {
+                             const float* lse, float* dvec, const void* out, int* emax, void* dq,
+                             hipStream_t s) {
   if (!na3d_bwd_dq_mfma_takes(d)) return false;
   if (out && o.dout_lo) return false;  // D of a two-term dO comes from the gate's pass
   const bool w377 = d.kz == 3 && d.ky == 7 && d.kx == 7;
@@ -802,6 +831,11 @@ bool launch_na3d_bwd_dq_mfma(const strata_na3d_desc& d, const BwdOpts& o, const 
   if (out) {  // D formed from dO and O by this pass and stored to dvec
     a.fo = static_cast<const uint16_t*>(out);
     a.dvec_out = dvec;
+  }
+  if (emax && !o.dout_lo) {
+    const int n = d.B * d.heads;
+    hipLaunchKernelGGL(emax_init_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, emax, n);
+    a.emax = emax;
   }
   a.qk_norm = o.qk_norm;
   a.eps = o.eps;
