@@ -440,6 +440,27 @@ def test_bwd_dout_magnitude(window, g_shift):
         check_close(host_f64(got), ref, "bf16", name)
 
 
+@pytest.mark.parametrize("window", [(5, 9, 9), (9, 9, 9)])
+def test_bwd_dout_scale_per_head(window):
+    """The balanced dK/dV kernel scales its float16 copy of dO by a power of two
+    per (batch, head): a head whose dO is all zero, one at 2^-30 and one at 2^20
+    each keep the bf16 bound against their own RMS (and the zero head gives
+    exact zeros)."""
+    shape = (1, 3, 9, 21, 23, 64)  # planes the balanced kernel takes
+    pl = I.random_placement(shape[0], shape[3], shape[4], 95)
+    c32 = oracle_coords(pl, shape[3], shape[4])
+    g_exp = np.zeros(shape[:-1], dtype=np.int32)
+    g_exp[:, 0], g_exp[:, 1], g_exp[:, 2] = -200, -30, 20  # 2^-200 flushes to zero
+    (q, k, v, g), grads, scale = run_bwd(shape, window, "bf16", 45, c32, g_exp=g_exp)
+    assert not np.any(I.bf16_bits_to_f32(g)[:, 0])
+    refs = oracle.na3d_bwd(*(oracle.widen(a, "bf16") for a in (q, k, v, g)), window, scale, coords=c32)
+    for name, got, ref in zip(("dq", "dk", "dv"), grads, refs):
+        got = host_f64(got)
+        assert not np.any(got[:, 0]), f"{name}: head with zero dO"
+        for h in (1, 2):
+            check_close(got[:, h], ref[:, h], "bf16", f"{name} head {h}")
+
+
 @pytest.mark.parametrize("window", [(3, 7, 7), (5, 9, 9)])
 def test_bwd_dout_mixed_magnitudes_dq_per_class(window):
     """dO rows scaled by 2^e, e in {-24, -12, 0, 12}: dq of every magnitude class
