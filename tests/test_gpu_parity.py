@@ -461,6 +461,39 @@ def test_bwd_dout_scale_per_head(window):
             check_close(got[:, h], ref[:, h], "bf16", f"{name} head {h}")
 
 
+def test_bwd_workspace_holds_d_and_dout_exponents():
+    """What the MFMA dQ pass leaves in the workspace for the dK/dV pass: D =
+    rowsum(dO * O) of every token-head (from the forward's bf16 O), then one
+    word per (batch, head) holding the frexp exponent of its largest |dO|
+    (-1000 where all of its dO is zero)."""
+    shape = (2, 3, 5, 12, 12, 64)
+    window = (5, 9, 9)
+    (q, k, v), out, lse, scale = run_fwd(shape, window, "bf16", 46)
+    g_exp = np.zeros(shape[:-1], dtype=np.int32)
+    g_exp[0, 1], g_exp[1, 0], g_exp[1, 2] = -200, -37, 29  # one all-zero head
+    g = I.gaussian(shape, 46, I.STREAM_DO, "bf16")
+    g = I.f32_to_bf16_bits((I.bf16_bits_to_f32(g) * np.exp2(g_exp.astype(np.float32))[..., None]).astype(np.float32))
+    qd, kd, vd, gd = (dev_tensor(a, "bf16") for a in (q, k, v, g))
+    desc = B.desc_for(qd, window, scale)
+    ws = torch.zeros(B.strata_na3d_bwd_workspace_size(desc), dtype=torch.uint8, device="cuda")
+    dq, dk, dv = (torch.empty_like(qd) for _ in range(3))
+    B.strata_na3d_bwd(desc, qd, kd, vd, None, out, gd, lse, dq, dk, dv, ws)
+    torch.cuda.synchronize()
+    n = int(np.prod(shape[:-1]))
+    off = (4 * n + 255) // 256 * 256
+    w = ws.cpu().numpy()
+    d_got = w[:4 * n].view(np.float32).reshape(shape[:-1])
+    gf = I.bf16_bits_to_f32(g).astype(np.float64)
+    o64 = host_f64(out)
+    d_ref = np.sum(gf * o64, axis=-1)
+    d_abs = np.sum(np.abs(gf * o64), axis=-1)  # float32 sums of exact products: error <= ~64 ulp of this
+    assert np.all(np.abs(d_got - d_ref) <= 2.0 ** -17 * d_abs)
+    e_got = w[off:off + 4 * shape[0] * shape[1]].view(np.int32).reshape(shape[:2])
+    amax = np.abs(gf).reshape(shape[0], shape[1], -1).max(axis=-1)
+    e_ref = np.where(amax > 0, np.frexp(amax)[1], -1000)
+    assert np.array_equal(e_got, e_ref), (e_got, e_ref)
+
+
 @pytest.mark.parametrize("window", [(3, 7, 7), (5, 9, 9)])
 def test_bwd_dout_mixed_magnitudes_dq_per_class(window):
     """dO rows scaled by 2^e, e in {-24, -12, 0, 12}: dq of every magnitude class
