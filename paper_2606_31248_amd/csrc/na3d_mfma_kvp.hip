@@ -25,19 +25,24 @@
 //               four squares per axis unless a single block already spans five
 //               (axes of 17 to 20 positions; the host checks every group).
 //   staging   : per query level the workgroup copies the 4 x 4 squares of its
-//               group (16 rows each, 256 rows: Q rotated to float16 in place and
-//               dO, -LSE and -D per row) with the direct-to-LDS load, double
-//               buffered.  Two more zero squares sit past the grid for the
-//               padding chunk of an odd square count.
+//               group (16 rows each, 256 rows: Q rotated to float16 in place,
+//               dO converted in place to float16 times 2^-sh, -LSE and -D 2^-sh
+//               per row) with the direct-to-LDS load, double buffered.  sh comes
+//               from the largest |dO| of the (batch, head), which the dQ pass
+//               records, so the staged dO stays below 2^14.  Two more zero
+//               squares sit past the grid for the padding chunk of an odd
+//               square count.
 //   wave      : the 16 keys of its block and level stay in registers (K~ times
-//               scale log2(e) in float16 and V in bf16 as B operands, the dK~^T and
+//               scale log2(e) and V, both float16, as B operands, the dK~^T and
 //               dV^T accumulators); it walks the squares of its own block's
-//               query box, two squares (32 queries) per step, with the math of
-//               the one-block kernel:
+//               query box, two squares (32 queries) per step:
 //                 X = Q~ . K~^T (float16 MFMA seeded with -LSE or -inf outside the
-//                 query's window), P = exp2(X); Y = dO . V^T - D (bf16);
-//                 dV^T += dO^T . P (bf16); dK~^T += Q~^T . dS (float16, dS = P Y
-//                 with a per-key power-of-two scale 2^(15-E)).
+//                 query's window), P = exp2(X); Y = dO . V^T - D (float16);
+//                 dV^T += dO^T . P (float16: bf16's rounding of P alone would
+//                 cost dV several percent of its RMS at peaked weights);
+//                 dK~^T += Q~^T . dS (float16, dS = P Y with a per-key
+//                 power-of-two scale 2^(15-E)); dK and dV are scaled back by
+//                 2^sh when stored.
 //   addresses : a wave's squares are fixed offsets from its first one once the
 //               width of its box (in squares) is known, so the steps are
 //               unrolled for width 3 (squares taken row by row, the last chunk
