@@ -74,6 +74,11 @@
 //   scaled values stay below 2^15; when a step raises E the accumulator is
 //   rescaled exactly and the step's logits move by the change.  At the end
 //   dQ = R^T (scale 2^(E-15) dQ~).
+// The lanes that load a query's dO row also load its O row and form D = <dO, O>
+// (stored once for the dK/dV pass), and every lane keeps the largest |dO| it
+// loads: at the end each wave takes an integer atomic maximum of that value's
+// exponent into a word per (batch, head), by which the balanced dK/dV pass
+// scales its float16 copy of dO.
 #include "common.h"
 #include "kernels.h"
 #include "mfma_util.h"
