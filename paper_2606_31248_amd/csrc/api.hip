@@ -204,9 +204,10 @@ static strata_status na3d_bwd_launch(const strata_na3d_desc* desc, const strata_
   }
   if (launch_na3d_bwd_col(*desc, bo, q, k, v, ga, lse, dvec, dq, dk, dv, s))
     return check_launch(opts ? "strata_na3d_bwd_ex" : "strata_na3d_bwd");
-  // the MFMA dq pass also records the largest |dO| exponent per (batch, head),
-  // which the balanced dk/dv pass scales its float16 copy of dO by
-  int* emax = reinterpret_cast<int*>(ws + L.emax);
+  // the MFMA dq pass also records the largest |dO| exponent per (batch, head)
+  // when the balanced dk/dv pass, which scales its float16 copy of dO by it,
+  // takes the problem
+  int* emax = na3d_bwd_dkdv_kvp_takes(*desc, bo) ? reinterpret_cast<int*>(ws + L.emax) : nullptr;
   if (!launch_na3d_bwd_dq_mfma(*desc, bo, q, k, v, cs, ga, lse, dvec, fuse_d ? out : nullptr, emax, dq, s)) {
     emax = nullptr;
     if (fuse_d) launch_na3d_bwd_ref(0, *desc, bo, q, k, v, cs, out, dout, lse, dq, dk, dv, dvec, s);

@@ -116,6 +116,9 @@ bool launch_na3d_bwd_col(const strata_na3d_desc& d, const BwdOpts& o, const void
                          void* dk, void* dv, hipStream_t s);
 // dK/dV with two key levels x four 4x4 blocks per workgroup (bf16, head_dim 64,
 // windows 5x9x9 and 9x9x9, no two-term dO); false if not applicable
+// (emax: the dO exponents the MFMA dq pass recorded; na3d_bwd_dkdv_kvp_takes
+// is the launcher's test of whether it takes the problem)
+bool na3d_bwd_dkdv_kvp_takes(const strata_na3d_desc& d, const BwdOpts& o);
 bool launch_na3d_bwd_dkdv_kvp(const strata_na3d_desc& d, const BwdOpts& o, const void* q, const void* k,
                               const void* v, const float* cs, const void* dout, const float* lse,
                               const float* dvec, const int* emax, void* dk, void* dv, hipStream_t s);

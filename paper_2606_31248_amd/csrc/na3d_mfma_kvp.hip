@@ -630,12 +630,10 @@ __global__ void __launch_bounds__(256 * NL, 1) na3d_mfma_kvp_kernel(KvpArgs a) {
 
 template <int KZ, int KY, int KX, int NL>
 bool launch_kvp(const strata_na3d_desc& d, const KvpArgs& a0, bool norm, hipStream_t s) {
-  if (!groups_fit(d.H, KY, false) || !groups_fit(d.W, KX, true)) return false;
   KvpArgs a = a0;
   a.ngy = n_groups(d.H);
   a.ngx = n_groups(d.W);
   const int64_t blocks = (int64_t)d.B * d.heads * a.ngy * a.ngx;
-  if (blocks >= (int64_t)1 << 31) return false;
   if (norm)
     hipLaunchKernelGGL((na3d_mfma_kvp_kernel<KZ, KY, KX, true, NL>), dim3((unsigned)blocks), dim3(256 * NL), 0, s, a);
   else
@@ -645,11 +643,18 @@ bool launch_kvp(const strata_na3d_desc& d, const KvpArgs& a0, bool norm, hipStre
 
 }  // namespace
 
+bool na3d_bwd_dkdv_kvp_takes(const strata_na3d_desc& d, const BwdOpts& o) {
+  if (d.dtype != STRATA_BF16 || d.head_dim != kD || o.dout_lo != nullptr) return false;
+  if ((int64_t)d.H * d.W * kD >= (int64_t)1 << 31) return false;
+  if (!(d.ky == 9 && d.kx == 9 && (d.kz == 5 || d.kz == 9))) return false;
+  if (!groups_fit(d.H, d.ky, false) || !groups_fit(d.W, d.kx, true)) return false;
+  return (int64_t)d.B * d.heads * n_groups(d.H) * n_groups(d.W) < (int64_t)1 << 31;
+}
+
 bool launch_na3d_bwd_dkdv_kvp(const strata_na3d_desc& d, const BwdOpts& o, const void* q, const void* k,
                               const void* v, const float* cs, const void* dout, const float* lse,
                               const float* dvec, const int* emax, void* dk, void* dv, hipStream_t s) {
-  if (d.dtype != STRATA_BF16 || d.head_dim != kD || o.dout_lo != nullptr || !emax) return false;
-  if ((int64_t)d.H * d.W * kD >= (int64_t)1 << 31) return false;
+  if (!emax || !na3d_bwd_dkdv_kvp_takes(d, o)) return false;
   KvpArgs a = {};
   a.q = static_cast<const uint16_t*>(q);
   a.k = static_cast<const uint16_t*>(k);
@@ -668,7 +673,7 @@ bool launch_na3d_bwd_dkdv_kvp(const strata_na3d_desc& d, const BwdOpts& o, const
   a.scale = d.scale;
   a.kscale = d.scale * kLog2e;
   a.eps = o.eps;
-  // two key levels per workgroup (two waves per SIMD, 214 registers); three
+  // two key levels per workgroup (two waves per SIMD, ~240 registers); three
   // levels (three waves per SIMD) leave 168 registers and spill 52 of them:
   // 8.94 against 7.67 ms for the training-tile dK/dV
   if (d.kz == 5 && d.ky == 9 && d.kx == 9) return launch_kvp<5, 9, 9, 2>(d, a, o.qk_norm, s);
