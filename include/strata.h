@@ -161,8 +161,9 @@ strata_status strata_na3d_fwd(const strata_na3d_desc* desc, const void* q, const
  * Kernels and input range as strata_na3d_fwd; on the MFMA paths the dS products
  * (dq, dk) are float16 with exact power-of-two scaling; P.dO and dO.V^T are
  * float16 products with dO scaled by a power of two per (batch, head) in the
- * dK/dV kernel of the 9-wide windows (V then saturates at 65504 like the
- * level-sweep forward's); elsewhere they are bf16 products, P.dO with P in two
+ * dK/dV kernel of the 9-wide windows (V then saturates at 65504 and keeps
+ * float16's subnormal spacing below 2^-14, as in the level-sweep forward);
+ * elsewhere they are bf16 products, P.dO with P in two
  * bf16 terms in the one-block dK/dV kernel (3x7x7, the gate, planes of 17-20
  * positions) and with P rounded to bf16 once in the column and head_dim-128
  * kernels. */
