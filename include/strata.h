@@ -163,10 +163,10 @@ strata_status strata_na3d_fwd(const strata_na3d_desc* desc, const void* q, const
  * float16 products with dO scaled by a power of two per (batch, head) in the
  * dK/dV kernel of the 9-wide windows (V then saturates at 65504 and keeps
  * float16's subnormal spacing below 2^-14, as in the level-sweep forward);
- * elsewhere they are bf16 products, P.dO with P in two
- * bf16 terms in the one-block dK/dV kernel (3x7x7, the gate, planes of 17-20
- * positions) and with P rounded to bf16 once in the column and head_dim-128
- * kernels. */
+ * elsewhere they are bf16 products, P.dO with P in two bf16 terms in the
+ * one-block dK/dV kernel (3x7x7, planes of 17-20 positions; one term with the
+ * gate's two-term dA) and with P rounded to bf16 once in the column and
+ * head_dim-128 kernels. */
 size_t strata_na3d_bwd_workspace_size(const strata_na3d_desc* desc);
 strata_status strata_na3d_bwd(const strata_na3d_desc* desc, const void* q, const void* k,
                               const void* v, const float* cs, const void* out, const void* dout,

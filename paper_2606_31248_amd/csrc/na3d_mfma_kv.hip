@@ -444,8 +444,9 @@ __global__ void __launch_bounds__(64 * ZK, (KvCfg<KZ, KY, KX, ZK, NBUF, LO>::WG_
       const float sc = __builtin_amdgcn_ldexpf(1.f, 15 - ex);
       // P for dV in two bf16 terms, P = hi + lo: bf16's rounding of P alone
       // would put the largest dV of a peaked softmax several percent of RMS(dV)
-      // off; the second term leaves ~2^-17 P (the low term of a two-term dO
-      // meets only the high term of P)
+      // off; the second term leaves ~2^-17 P.  With the gate's two-term dA the
+      // rows of dA differ in magnitude anyway and dV is held to the elementwise
+      // bound of P's bf16 rounding (2^-8 sum P |dA|): one term there.
       uint32_t pb[2][2], pr[2][2], db[2][2];
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
@@ -453,13 +454,14 @@ __global__ void __launch_bounds__(64 * ZK, (KvCfg<KZ, KY, KX, ZK, NBUF, LO>::WG_
         const float p2 = __builtin_amdgcn_exp2f(x[h][2]), p3 = __builtin_amdgcn_exp2f(x[h][3]);
         pb[h][0] = pack2(p0, p1);
         pb[h][1] = pack2(p2, p3);
-        pr[h][0] = pack2(p0 - lo_bf16(pb[h][0]), p1 - hi_bf16(pb[h][0]));
-        pr[h][1] = pack2(p2 - lo_bf16(pb[h][1]), p3 - hi_bf16(pb[h][1]));
+        if constexpr (!LO) {
+          pr[h][0] = pack2(p0 - lo_bf16(pb[h][0]), p1 - hi_bf16(pb[h][0]));
+          pr[h][1] = pack2(p2 - lo_bf16(pb[h][1]), p3 - hi_bf16(pb[h][1]));
+        }
         db[h][0] = pack2h_rne(p0 * sc * y[h][0], p1 * sc * y[h][1]);
         db[h][1] = pack2h_rne(p2 * sc * y[h][2], p3 * sc * y[h][3]);
       }
       const bf16x8 pf = __builtin_bit_cast(bf16x8, make_uint4(pb[0][0], pb[0][1], pb[1][0], pb[1][1]));
-      const bf16x8 prf = __builtin_bit_cast(bf16x8, make_uint4(pr[0][0], pr[0][1], pr[1][0], pr[1][1]));
       const f16x8 df = __builtin_bit_cast(f16x8, make_uint4(db[0][0], db[0][1], db[1][0], db[1][1]));
       bf16x8 gt[4];
 #pragma unroll
@@ -475,8 +477,11 @@ __global__ void __launch_bounds__(64 * ZK, (KvCfg<KZ, KY, KX, ZK, NBUF, LO>::WG_
         const f16x8 qt = __builtin_bit_cast(f16x8, make_uint4(qtr[t][0].x, qtr[t][0].y, qtr[t][1].x, qtr[t][1].y));
         accK[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(qt, df, accK[t], 0, 0, 0);
       }
+      if constexpr (!LO) {
+        const bf16x8 prf = __builtin_bit_cast(bf16x8, make_uint4(pr[0][0], pr[0][1], pr[1][0], pr[1][1]));
 #pragma unroll
-      for (int t = 0; t < 4; ++t) accV[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gt[t], prf, accV[t], 0, 0, 0);
+        for (int t = 0; t < 4; ++t) accV[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gt[t], prf, accV[t], 0, 0, 0);
+      }
       __builtin_amdgcn_sched_barrier(0);  // keep the next step's loads out of this one's registers
     });
   };
