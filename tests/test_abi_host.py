@@ -263,3 +263,28 @@ def test_fwd_stitch_rules():
                                        None) == B.STRATA_ERR_INVALID_ARG
     assert L.strata_tile_blend_overlap(p, 9, 9, 4, 64, 64, 64, 56, 56, None, p, 512, 512, B.STRATA_BF16,
                                        None) == B.STRATA_ERR_INVALID_ARG
+
+
+def test_bwd_workspace_layout():
+    """D (float32 per token-head) and one int32 word per batch-head, each region
+    on a 256-byte boundary; the gate adds its dA terms after them."""
+    L = B.load()
+    al = lambda x: (x + 255) // 256 * 256
+    for kw in (dict(), dict(B=3, heads=5, Z=7, H=9, W=11), dict(B=70, heads=1000, Z=1, H=1, W=1, window=(1, 1, 1))):
+        d = desc(**kw)
+        bh = d.B * d.heads
+        n = bh * d.Z * d.H * d.W
+        assert L.strata_na3d_bwd_workspace_size(ctypes.byref(d)) == al(4 * n) + al(4 * bh)
+
+
+def test_noalloc_rejects_too_many_batch_heads():
+    """The allocation-free backward's static array holds one word per batch-head
+    up to 2^16 of them: more are rejected on the host, before any launch."""
+    L = B.load()
+    p = fake()
+    ok = desc(B=1 << 8, heads=1 << 8, Z=1, H=1, W=1, window=(1, 1, 1))  # 2^16 batch-heads: the limit
+    big = desc(B=(1 << 8) + 1, heads=1 << 8, Z=1, H=1, W=1, window=(1, 1, 1))
+    assert L.strata_na3d_bwd_noalloc(ctypes.byref(big), p, p, p, None, p, p, p, p, p, p, None) == \
+        B.STRATA_ERR_INVALID_ARG
+    assert b"static scratch" in L.strata_last_error()
+    assert L.strata_na3d_bwd_workspace_size(ctypes.byref(ok)) <= (1 << 25) + (1 << 18)
